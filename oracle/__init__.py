@@ -1,0 +1,16 @@
+"""CPU oracle for the Caffe convolution layer and its pooling/LRN glue.
+
+TEST INFRASTRUCTURE ONLY: only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package.  It shares no
+code with the HIP library (``paper_1408_5093_amd``) and never touches a GPU.
+"""
+from .ref import (  # noqa: F401
+    conv_out_shape,
+    conv_forward,
+    conv_backward,
+    maxpool_forward,
+    maxpool_backward,
+    lrn_forward,
+    lrn_backward,
+    num_threads,
+)

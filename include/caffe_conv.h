@@ -1,0 +1,152 @@
+/*
+ * caffe_conv.h -- C ABI of the MI355X (gfx950) convolution-layer library
+ * (libcaffe_conv.so).
+ *
+ * The operation is the convolution layer of Caffe (Jia et al., "Caffe:
+ * Convolutional Architecture for Fast Feature Embedding", 2014).  Sec. 3.1
+ * fixes the data: 4-D blobs (here N x C x H x W, row-major, "NCHW").
+ * Sec. 3.2 fixes the roles: the forward pass maps the input blob to the
+ * output blob; the backward pass maps the gradient w.r.t. the output to the
+ * gradients w.r.t. the parameters (weights, bias) and w.r.t. the input.
+ * Sec. 3.2 also lists rectified-linear units, which this library can fuse
+ * into the convolution.  The paper gives no formula; the library computes the
+ * textbook strided, zero-padded, grouped 2-D cross-correlation:
+ *
+ *   Ho = floor((H + 2 pad_h - kernel_h) / stride_h) + 1   (Wo likewise)
+ *   Cg = C / group, Kg = K / group, output channel k belongs to group t = k / Kg
+ *   Z[n,k,i,j] = bias[k] + sum_{c<Cg, u<kh, v<kw}
+ *                weight[k,c,u,v] * bottom[n, t*Cg + c, i*sh - ph + u, j*sw - pw + v]
+ *                (bottom reads as 0 outside the image, no kernel flip)
+ *   top = relu ? max(Z, 0) : Z
+ *
+ * and, with D = relu ? top_diff * [top > 0] : top_diff,
+ *
+ *   bias_diff[k]       = sum_{n,i,j} D[n,k,i,j]
+ *   weight_diff[k,c,u,v] = sum_{n,i,j} D[n,k,i,j] * bottom[n, t*Cg + c, i*sh - ph + u, j*sw - pw + v]
+ *   bottom_diff        = the adjoint of the forward map applied to D.
+ *
+ * Layouts.  bottom / bottom_diff: N x C x H x W.  weight / weight_diff:
+ * K x Cg x kernel_h x kernel_w.  bias / bias_diff: K.  top / top_diff:
+ * N x K x Ho x Wo.  All dense, row-major, no strides.
+ *
+ * Types.  `desc->dtype` selects the operand type of `bottom` and `weight`:
+ * CAFFE_F32 (float) or CAFFE_BF16 (bfloat16 stored as uint16_t; the caller
+ * rounds to nearest-even).  Everything else (bias, top, top_diff, every
+ * gradient) is float in both modes, and every product is accumulated in
+ * float.  In CAFFE_BF16 mode `top_diff` is rounded to bfloat16
+ * (nearest-even) before it enters a product.
+ *
+ * Memory and ownership.  Every tensor pointer is a device pointer (HIP
+ * device memory of the current device), allocated and owned by the caller,
+ * 16-byte aligned.  The library never allocates, frees or retains caller
+ * memory.  Scratch space comes from the caller as `workspace` / `ws_bytes`
+ * (device memory, 256-byte aligned); query the size with
+ * caffe_conv_workspace_size().  No tensor may exceed 2^31 - 1 bytes.
+ *
+ * Execution.  Every compute call only validates its arguments on the host
+ * and enqueues kernels on `stream` (a hipStream_t; NULL = the default
+ * stream), then returns: the results are ready when the stream reaches that
+ * point.  Device faults therefore surface at the caller's next
+ * synchronisation.  Calls on different streams that share no output or
+ * workspace memory may run concurrently; the library holds no mutable global
+ * state.  Results are bitwise reproducible run to run for the same
+ * arguments (no atomics; every sum has a fixed order).
+ *
+ * Errors.  Every call returns CAFFE_OK (0) or a negative caffe_status and
+ * then has enqueued nothing.  caffe_status_string() names a code;
+ * caffe_last_error() returns a thread-local message describing the last
+ * failure on the calling thread.
+ */
+#ifndef CAFFE_CONV_H
+#define CAFFE_CONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum caffe_status {
+    CAFFE_OK = 0,
+    CAFFE_ERR_INVALID_ARG = -1, /* bad shape, NULL required pointer, bad flag      */
+    CAFFE_ERR_ALIGN = -2,       /* pointer not 16-byte (workspace: 256-byte) aligned */
+    CAFFE_ERR_WORKSPACE = -3,   /* ws_bytes smaller than caffe_conv_workspace_size   */
+    CAFFE_ERR_UNSUPPORTED = -4, /* unknown dtype, or a tensor of 2^31 bytes or more  */
+    CAFFE_ERR_HIP = -5          /* the HIP runtime refused a launch                  */
+} caffe_status;
+
+typedef enum caffe_dtype { CAFFE_F32 = 0, CAFFE_BF16 = 1 } caffe_dtype;
+
+/* Layer geometry: the parameters Caffe's convolution layer is defined by. */
+typedef struct caffe_conv_desc {
+    int32_t N, C, H, W;           /* bottom blob; N may be 0 (empty batch)        */
+    int32_t K;                    /* number of output channels (filters)          */
+    int32_t kernel_h, kernel_w;   /* >= 1                                         */
+    int32_t stride_h, stride_w;   /* >= 1                                         */
+    int32_t pad_h, pad_w;         /* >= 0, zero padding on both sides             */
+    int32_t group;                /* >= 1, divides C and K; contiguous channel slices */
+    int32_t relu;                 /* 0 or 1: fuse max(., 0) after the bias        */
+    int32_t dtype;                /* caffe_dtype of bottom and weight             */
+} caffe_conv_desc;
+
+enum caffe_conv_pass {
+    CAFFE_PASS_FORWARD = 0,
+    CAFFE_PASS_BACKWARD_DATA = 1,
+    CAFFE_PASS_BACKWARD_WEIGHTS = 2,
+    CAFFE_PASS_BACKWARD = 3 /* caffe_conv_backward: data and weights together */
+};
+
+/* Output spatial size (formula above).  Host-only; never touches a GPU.
+ * Returns CAFFE_ERR_INVALID_ARG for an invalid descriptor. */
+int caffe_conv_out_shape(const caffe_conv_desc* desc, int32_t* Ho, int32_t* Wo);
+
+/* Bytes of device workspace that `pass` (a caffe_conv_pass) needs for this
+ * descriptor; 0 is a valid answer.  Host-only. */
+int caffe_conv_workspace_size(const caffe_conv_desc* desc, int32_t pass, size_t* bytes);
+
+/* Forward pass (Sec. 3.2): top = [relu](weight (*) bottom + bias).
+ * bias may be NULL (no bias).  top is overwritten. */
+int caffe_conv_forward(const caffe_conv_desc* desc, const void* bottom, const void* weight,
+                       const float* bias, float* top, void* workspace, size_t ws_bytes,
+                       void* stream);
+
+/* Backward pass w.r.t. the input (Sec. 3.2): bottom_diff = adjoint(D).
+ * top is the forward output and is required iff desc->relu; it is read only
+ * for the mask [top > 0].  bottom_diff is overwritten. */
+int caffe_conv_backward_data(const caffe_conv_desc* desc, const float* top_diff, const float* top,
+                             const void* weight, float* bottom_diff, void* workspace,
+                             size_t ws_bytes, void* stream);
+
+/* Backward pass w.r.t. the parameters (Sec. 3.2): weight_diff and (if not
+ * NULL) bias_diff.  accumulate = 0 overwrites them, 1 adds to them.  top is
+ * required iff desc->relu. */
+int caffe_conv_backward_weights(const caffe_conv_desc* desc, const float* top_diff,
+                                const float* top, const void* bottom, float* weight_diff,
+                                float* bias_diff, int32_t accumulate, void* workspace,
+                                size_t ws_bytes, void* stream);
+
+/* The whole backward pass of the layer in one call: the ReLU mask is applied
+ * once and shared by both gradients.  Any of bottom_diff, weight_diff,
+ * bias_diff may be NULL to skip it; bottom is required iff weight_diff is
+ * given, weight iff bottom_diff is given.  accumulate applies to
+ * weight_diff and bias_diff only. */
+int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, const float* top,
+                        const void* bottom, const void* weight, float* bottom_diff,
+                        float* weight_diff, float* bias_diff, int32_t accumulate,
+                        void* workspace, size_t ws_bytes, void* stream);
+
+/* Static name of a status code ("CAFFE_OK", ...). */
+const char* caffe_status_string(int32_t status);
+
+/* Thread-local text of the last error raised on this thread ("" if none). */
+const char* caffe_last_error(void);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int32_t caffe_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CAFFE_CONV_H */

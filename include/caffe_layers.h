@@ -1,0 +1,77 @@
+/*
+ * caffe_layers.h -- C ABI of the glue layers that sit between CaffeNet's
+ * convolutions, in the same library as caffe_conv.h (libcaffe_conv.so).
+ *
+ * Both layers are in the paper's list of Caffe layer types (Sec. 3.2:
+ * pooling, local response normalisation), with the same forward/backward
+ * roles as the convolution layer.  The paper gives no formulas; the library
+ * computes:
+ *
+ * Max pooling: Ho = floor((H + 2 pad_h - kernel_h) / stride_h) + 1 (Wo
+ * likewise); top[n,c,i,j] = max over rows i*sh - ph .. i*sh - ph + kh - 1 and
+ * the matching columns, clipped to the image.  Ties go to the first maximum
+ * in row-major window order.  `mask` (int32, N x C x Ho x Wo) records the
+ * winner as h * W + w within its plane; the backward pass sends each
+ * top_diff element to that position and sums what arrives (overwriting
+ * bottom_diff).  pad must be smaller than the kernel.
+ *
+ * Local response normalisation across channels:
+ *   s_c = k + (alpha / local_size) * sum_{c' in win(c)} bottom_{c'}^2
+ *   top_c = bottom_c * s_c^(-beta)
+ *   win(c) = c - (local_size-1)/2 ... c - (local_size-1)/2 + local_size - 1,
+ *            clipped to [0, C) (the divisor stays local_size)
+ * and the backward pass is its exact derivative:
+ *   bottom_diff_c = top_diff_c s_c^(-beta)
+ *       - (2 alpha beta / local_size) bottom_c sum_{c': c in win(c')} top_diff_c' top_c' / s_c'
+ *
+ * Conventions (memory, streams, errors, status codes) are those of
+ * caffe_conv.h: caller-owned 16-byte-aligned device pointers, asynchronous
+ * execution on `stream`, negative caffe_status on failure with nothing
+ * enqueued, no atomics.  All blobs are float, N x C x H x W.
+ */
+#ifndef CAFFE_LAYERS_H
+#define CAFFE_LAYERS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct caffe_pool_desc {
+    int32_t N, C, H, W;
+    int32_t kernel_h, kernel_w, stride_h, stride_w, pad_h, pad_w;
+} caffe_pool_desc;
+
+typedef struct caffe_lrn_desc {
+    int32_t N, C, H, W;
+    int32_t local_size; /* >= 1 */
+    float alpha, beta, k;
+} caffe_lrn_desc;
+
+/* Host-only. */
+int caffe_pool_out_shape(const caffe_pool_desc* desc, int32_t* Ho, int32_t* Wo);
+
+/* mask may be NULL when no backward pass will follow. */
+int caffe_maxpool_forward(const caffe_pool_desc* desc, const float* bottom, float* top,
+                          int32_t* mask, void* stream);
+
+int caffe_maxpool_backward(const caffe_pool_desc* desc, const float* top_diff,
+                           const int32_t* mask, float* bottom_diff, void* stream);
+
+int caffe_lrn_forward(const caffe_lrn_desc* desc, const float* bottom, float* top, void* stream);
+
+/* top is the forward output for the same bottom. */
+int caffe_lrn_backward(const caffe_lrn_desc* desc, const float* bottom, const float* top,
+                       const float* top_diff, float* bottom_diff, void* stream);
+
+/* out[i] = bfloat16(in[i]) rounded to nearest even, i < count.  The input for
+ * CAFFE_BF16 convolutions. */
+int caffe_cast_f32_to_bf16(const float* in, uint16_t* out, int64_t count, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CAFFE_LAYERS_H */

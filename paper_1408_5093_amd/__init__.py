@@ -1,0 +1,265 @@
+"""MI355X (gfx950) convolution layer of Caffe (Jia et al., 2014): Python binding.
+
+The layer (paper Sec. 3.2: forward pass, and a backward pass giving the
+parameter and input gradients) runs entirely in the HIP kernels of
+``libcaffe_conv.so`` behind the C ABI in ``include/caffe_conv.h`` and
+``include/caffe_layers.h``.  This module only marshals arguments: it takes
+PyTorch device tensors, checks dtype/device/contiguity, and passes their data
+pointers and the current HIP stream.  The functions named ``caffe_*`` take
+the same arguments as their C counterparts; the short names allocate outputs
+and workspace with PyTorch and call them.
+"""
+import ctypes
+
+import torch
+
+from . import _lib
+from ._lib import (  # noqa: F401
+    CAFFE_BF16, CAFFE_F32, PASS_BACKWARD, PASS_BACKWARD_DATA, PASS_BACKWARD_WEIGHTS, PASS_FORWARD,
+    CaffeError, ConvDesc, LrnDesc, PoolDesc, check, load, LIB_PATH,
+)
+
+__all__ = [
+    "conv_desc", "conv_out_shape", "conv_workspace_size", "conv_forward", "conv_backward",
+    "conv_backward_data", "conv_backward_weights", "maxpool_forward", "maxpool_backward",
+    "lrn_forward", "lrn_backward", "cast_f32_to_bf16", "Workspace", "CaffeError",
+]
+
+
+def _pair(v):
+    return (int(v), int(v)) if isinstance(v, int) else (int(v[0]), int(v[1]))
+
+
+def conv_desc(x_shape, w_shape, stride=1, pad=0, group=1, relu=False, dtype=CAFFE_F32):
+    """Descriptor for bottom x_shape = (N, C, H, W) and weight w_shape = (K, C/group, kh, kw)."""
+    N, C, H, W = (int(d) for d in x_shape)
+    K, Cg, kh, kw = (int(d) for d in w_shape)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    if Cg * group != C:
+        raise ValueError(f"weight has {Cg} channels per group but C={C}, group={group}")
+    return ConvDesc(N, C, H, W, K, kh, kw, sh, sw, ph, pw, int(group), int(bool(relu)), int(dtype))
+
+
+def conv_out_shape(desc):
+    Ho, Wo = ctypes.c_int32(), ctypes.c_int32()
+    check(load().caffe_conv_out_shape(ctypes.byref(desc), ctypes.byref(Ho), ctypes.byref(Wo)))
+    return Ho.value, Wo.value
+
+
+def conv_workspace_size(desc, pass_):
+    n = ctypes.c_size_t()
+    check(load().caffe_conv_workspace_size(ctypes.byref(desc), int(pass_), ctypes.byref(n)))
+    return n.value
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dev(t, name, dtype=None):
+    if t is None:
+        return
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+class Workspace:
+    """A growable device byte buffer for the library's scratch space."""
+
+    def __init__(self, device=None):
+        self.device = device
+        self.buf = None
+
+    def get(self, nbytes):
+        if nbytes == 0:
+            return None
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.empty(nbytes, dtype=torch.uint8, device=self.device or "cuda")
+        return self.buf
+
+
+def _op_dtype(desc):
+    return torch.bfloat16 if desc.dtype == CAFFE_BF16 else torch.float32
+
+
+# ----------------------------------------------------- C-ABI-shaped calls
+def caffe_conv_forward(desc, bottom, weight, bias, top, workspace=None, stream=None):
+    t = _op_dtype(desc)
+    _dev(bottom, "bottom", t), _dev(weight, "weight", t), _dev(bias, "bias", torch.float32)
+    _dev(top, "top", torch.float32)
+    ws_bytes = 0 if workspace is None else workspace.numel()
+    check(load().caffe_conv_forward(ctypes.byref(desc), _ptr(bottom), _ptr(weight), _ptr(bias),
+                                    _ptr(top), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def caffe_conv_backward(desc, top_diff, top, bottom, weight, bottom_diff, weight_diff, bias_diff,
+                        accumulate=0, workspace=None, stream=None):
+    t = _op_dtype(desc)
+    for x, n in ((top_diff, "top_diff"), (top, "top"), (bottom_diff, "bottom_diff"),
+                 (weight_diff, "weight_diff"), (bias_diff, "bias_diff")):
+        _dev(x, n, torch.float32)
+    _dev(bottom, "bottom", t), _dev(weight, "weight", t)
+    ws_bytes = 0 if workspace is None else workspace.numel()
+    check(load().caffe_conv_backward(ctypes.byref(desc), _ptr(top_diff), _ptr(top), _ptr(bottom),
+                                     _ptr(weight), _ptr(bottom_diff), _ptr(weight_diff),
+                                     _ptr(bias_diff), int(accumulate), _ptr(workspace), ws_bytes,
+                                     _stream(stream)))
+
+
+def caffe_conv_backward_data(desc, top_diff, top, weight, bottom_diff, workspace=None, stream=None):
+    _dev(top_diff, "top_diff", torch.float32), _dev(top, "top", torch.float32)
+    _dev(weight, "weight", _op_dtype(desc)), _dev(bottom_diff, "bottom_diff", torch.float32)
+    ws_bytes = 0 if workspace is None else workspace.numel()
+    check(load().caffe_conv_backward_data(ctypes.byref(desc), _ptr(top_diff), _ptr(top),
+                                          _ptr(weight), _ptr(bottom_diff), _ptr(workspace),
+                                          ws_bytes, _stream(stream)))
+
+
+def caffe_conv_backward_weights(desc, top_diff, top, bottom, weight_diff, bias_diff, accumulate=0,
+                                workspace=None, stream=None):
+    _dev(top_diff, "top_diff", torch.float32), _dev(top, "top", torch.float32)
+    _dev(bottom, "bottom", _op_dtype(desc)), _dev(weight_diff, "weight_diff", torch.float32)
+    _dev(bias_diff, "bias_diff", torch.float32)
+    ws_bytes = 0 if workspace is None else workspace.numel()
+    check(load().caffe_conv_backward_weights(ctypes.byref(desc), _ptr(top_diff), _ptr(top),
+                                             _ptr(bottom), _ptr(weight_diff), _ptr(bias_diff),
+                                             int(accumulate), _ptr(workspace), ws_bytes,
+                                             _stream(stream)))
+
+
+# ------------------------------------------------------ allocating helpers
+def conv_forward(x, w, b=None, stride=1, pad=0, group=1, relu=False, out=None, ws=None):
+    dtype = CAFFE_BF16 if x.dtype == torch.bfloat16 else CAFFE_F32
+    d = conv_desc(x.shape, w.shape, stride, pad, group, relu, dtype)
+    Ho, Wo = conv_out_shape(d)
+    if out is None:
+        out = torch.empty((d.N, d.K, Ho, Wo), dtype=torch.float32, device=x.device)
+    need = conv_workspace_size(d, PASS_FORWARD)
+    buf = (ws or Workspace(x.device)).get(need)
+    caffe_conv_forward(d, x, w, b, out, buf)
+    return out
+
+
+def conv_backward(x, w, top_diff, top=None, stride=1, pad=0, group=1, relu=False,
+                  need=("dx", "dw", "db"), accumulate=0, outs=None, ws=None):
+    """Returns (dx, dw, db), None where not requested."""
+    dtype = CAFFE_BF16 if x.dtype == torch.bfloat16 else CAFFE_F32
+    d = conv_desc(x.shape, w.shape, stride, pad, group, relu, dtype)
+    dev = top_diff.device
+    if outs is None:
+        dx = torch.empty(x.shape, dtype=torch.float32, device=dev) if "dx" in need else None
+        dw = torch.empty(w.shape, dtype=torch.float32, device=dev) if "dw" in need else None
+        db = torch.empty((w.shape[0],), dtype=torch.float32, device=dev) if "db" in need else None
+    else:
+        dx, dw, db = outs
+    buf = (ws or Workspace(dev)).get(conv_workspace_size(d, PASS_BACKWARD))
+    caffe_conv_backward(d, top_diff, top, x if dw is not None else None,
+                        w if dx is not None else None, dx, dw, db, accumulate, buf)
+    return dx, dw, db
+
+
+def conv_backward_data(x_shape, w, top_diff, top=None, stride=1, pad=0, group=1, relu=False,
+                       ws=None):
+    dtype = CAFFE_BF16 if w.dtype == torch.bfloat16 else CAFFE_F32
+    d = conv_desc(x_shape, w.shape, stride, pad, group, relu, dtype)
+    dx = torch.empty(tuple(x_shape), dtype=torch.float32, device=top_diff.device)
+    buf = (ws or Workspace(top_diff.device)).get(conv_workspace_size(d, PASS_BACKWARD_DATA))
+    caffe_conv_backward_data(d, top_diff, top, w, dx, buf)
+    return dx
+
+
+def conv_backward_weights(x, w_shape, top_diff, top=None, stride=1, pad=0, group=1, relu=False,
+                          with_bias=True, accumulate=0, ws=None):
+    dtype = CAFFE_BF16 if x.dtype == torch.bfloat16 else CAFFE_F32
+    d = conv_desc(x.shape, w_shape, stride, pad, group, relu, dtype)
+    dw = torch.empty(tuple(w_shape), dtype=torch.float32, device=x.device)
+    db = torch.empty((w_shape[0],), dtype=torch.float32, device=x.device) if with_bias else None
+    buf = (ws or Workspace(x.device)).get(conv_workspace_size(d, PASS_BACKWARD_WEIGHTS))
+    caffe_conv_backward_weights(d, top_diff, top, x, dw, db, accumulate, buf)
+    return dw, db
+
+
+def pool_desc(x_shape, kernel, stride, pad=0):
+    N, C, H, W = (int(v) for v in x_shape)
+    kh, kw = _pair(kernel)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    return PoolDesc(N, C, H, W, kh, kw, sh, sw, ph, pw)
+
+
+def pool_out_shape(desc):
+    Ho, Wo = ctypes.c_int32(), ctypes.c_int32()
+    check(load().caffe_pool_out_shape(ctypes.byref(desc), ctypes.byref(Ho), ctypes.byref(Wo)))
+    return Ho.value, Wo.value
+
+
+def maxpool_forward(x, kernel, stride, pad=0, out=None, mask=None, with_mask=True, stream=None):
+    _dev(x, "bottom", torch.float32)
+    d = pool_desc(x.shape, kernel, stride, pad)
+    Ho, Wo = pool_out_shape(d)
+    if out is None:
+        out = torch.empty((d.N, d.C, Ho, Wo), dtype=torch.float32, device=x.device)
+    if mask is None and with_mask:
+        mask = torch.empty((d.N, d.C, Ho, Wo), dtype=torch.int32, device=x.device)
+    _dev(out, "top", torch.float32), _dev(mask, "mask", torch.int32)
+    check(load().caffe_maxpool_forward(ctypes.byref(d), _ptr(x), _ptr(out), _ptr(mask),
+                                       _stream(stream)))
+    return out, mask
+
+
+def maxpool_backward(x_shape, top_diff, mask, kernel, stride, pad=0, out=None, stream=None):
+    _dev(top_diff, "top_diff", torch.float32), _dev(mask, "mask", torch.int32)
+    d = pool_desc(x_shape, kernel, stride, pad)
+    if out is None:
+        out = torch.empty(tuple(x_shape), dtype=torch.float32, device=top_diff.device)
+    _dev(out, "bottom_diff", torch.float32)
+    check(load().caffe_maxpool_backward(ctypes.byref(d), _ptr(top_diff), _ptr(mask), _ptr(out),
+                                        _stream(stream)))
+    return out
+
+
+def lrn_desc(x_shape, size=5, alpha=1e-4, beta=0.75, k=1.0):
+    N, C, H, W = (int(v) for v in x_shape)
+    return LrnDesc(N, C, H, W, int(size), float(alpha), float(beta), float(k))
+
+
+def lrn_forward(x, size=5, alpha=1e-4, beta=0.75, k=1.0, out=None, stream=None):
+    _dev(x, "bottom", torch.float32)
+    d = lrn_desc(x.shape, size, alpha, beta, k)
+    if out is None:
+        out = torch.empty_like(x)
+    _dev(out, "top", torch.float32)
+    check(load().caffe_lrn_forward(ctypes.byref(d), _ptr(x), _ptr(out), _stream(stream)))
+    return out
+
+
+def lrn_backward(x, y, top_diff, size=5, alpha=1e-4, beta=0.75, k=1.0, out=None, stream=None):
+    for t, n in ((x, "bottom"), (y, "top"), (top_diff, "top_diff")):
+        _dev(t, n, torch.float32)
+    d = lrn_desc(x.shape, size, alpha, beta, k)
+    if out is None:
+        out = torch.empty_like(x)
+    _dev(out, "bottom_diff", torch.float32)
+    check(load().caffe_lrn_backward(ctypes.byref(d), _ptr(x), _ptr(y), _ptr(top_diff), _ptr(out),
+                                    _stream(stream)))
+    return out
+
+
+def cast_f32_to_bf16(x, out=None, stream=None):
+    _dev(x, "in", torch.float32)
+    if out is None:
+        out = torch.empty(x.shape, dtype=torch.bfloat16, device=x.device)
+    _dev(out, "out", torch.bfloat16)
+    check(load().caffe_cast_f32_to_bf16(_ptr(x), _ptr(out), x.numel(), _stream(stream)))
+    return out

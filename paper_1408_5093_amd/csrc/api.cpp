@@ -1,0 +1,560 @@
+// api.cpp -- the C ABI (include/caffe_conv.h, include/caffe_layers.h):
+// argument validation, the workspace plan, and the choice of kernels.  No
+// function here touches the GPU before every argument has been checked.
+#include <hip/hip_runtime.h>
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "../../include/caffe_conv.h"
+#include "../../include/caffe_layers.h"
+#include "kernels.h"
+
+using namespace caffe_hip;
+
+namespace {
+
+thread_local char g_err[512];
+
+int fail(int status, const char* fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int hip_fail(hipError_t e, const char* what)
+{
+    return fail(CAFFE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr int64_t kMaxTensorBytes = (int64_t(1) << 31) - 1;
+constexpr int32_t kMaxSpatial = 16383;  // spatial sizes, kernels and pads
+constexpr size_t kWsAlign = 256;
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Everything the kernels need to know about one convolution.
+struct ConvPlan {
+    int N, C, H, W, K, kh, kw, sh, sw, ph, pw, G, relu, dtype;
+    int Ho, Wo, Cg, Kg, R;
+    int64_t esize;  // bytes per bottom/weight element
+    int64_t bottom_elems, top_elems, weight_elems;
+    // data gradient (phase-stacked)
+    int Th, Tw, a0h, a0w, Ah, Aw, Mt, Rt;
+    // weight gradient split-K
+    int splits, cols_per_split;
+    // workspace layout (byte offsets), per pass
+    size_t off_d, off_sums, off_wt, off_part;
+    size_t ws_data, ws_weights, ws_both;
+};
+
+int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
+{
+    if (!d)
+        return fail(CAFFE_ERR_INVALID_ARG, "desc is NULL");
+    if (d->N < 0 || d->C < 1 || d->H < 1 || d->W < 1 || d->K < 1)
+        return fail(CAFFE_ERR_INVALID_ARG, "blob dims must be >= 1 (N >= 0): N=%d C=%d H=%d W=%d K=%d",
+                    d->N, d->C, d->H, d->W, d->K);
+    if (d->kernel_h < 1 || d->kernel_w < 1 || d->stride_h < 1 || d->stride_w < 1 ||
+        d->pad_h < 0 || d->pad_w < 0)
+        return fail(CAFFE_ERR_INVALID_ARG, "kernel/stride must be >= 1 and pad >= 0");
+    if (d->group < 1 || d->C % d->group || d->K % d->group)
+        return fail(CAFFE_ERR_INVALID_ARG, "group %d must divide C=%d and K=%d", d->group, d->C,
+                    d->K);
+    if (d->group > 65535)
+        return fail(CAFFE_ERR_UNSUPPORTED, "group must be <= 65535");
+    if (d->relu != 0 && d->relu != 1)
+        return fail(CAFFE_ERR_INVALID_ARG, "relu must be 0 or 1");
+    if (d->dtype != CAFFE_F32 && d->dtype != CAFFE_BF16)
+        return fail(CAFFE_ERR_UNSUPPORTED, "unknown dtype %d", d->dtype);
+    if (d->H + 2 * (int64_t)d->pad_h < d->kernel_h || d->W + 2 * (int64_t)d->pad_w < d->kernel_w)
+        return fail(CAFFE_ERR_INVALID_ARG, "kernel larger than the padded input");
+    if (d->H > kMaxSpatial || d->W > kMaxSpatial || d->kernel_h > kMaxSpatial ||
+        d->kernel_w > kMaxSpatial || d->pad_h > kMaxSpatial || d->pad_w > kMaxSpatial ||
+        d->stride_h > kMaxSpatial || d->stride_w > kMaxSpatial)
+        return fail(CAFFE_ERR_UNSUPPORTED, "spatial sizes, kernels, strides and pads must be <= %d",
+                    kMaxSpatial);
+
+    ConvPlan& q = *p;
+    q.N = d->N; q.C = d->C; q.H = d->H; q.W = d->W; q.K = d->K;
+    q.kh = d->kernel_h; q.kw = d->kernel_w; q.sh = d->stride_h; q.sw = d->stride_w;
+    q.ph = d->pad_h; q.pw = d->pad_w; q.G = d->group; q.relu = d->relu; q.dtype = d->dtype;
+    q.Ho = (q.H + 2 * q.ph - q.kh) / q.sh + 1;
+    q.Wo = (q.W + 2 * q.pw - q.kw) / q.sw + 1;
+    q.Cg = q.C / q.G;
+    q.Kg = q.K / q.G;
+    q.esize = q.dtype == CAFFE_BF16 ? 2 : 4;
+
+    const int64_t R = (int64_t)q.Cg * q.kh * q.kw;
+    q.bottom_elems = (int64_t)q.N * q.C * q.H * q.W;
+    q.top_elems = (int64_t)q.N * q.K * q.Ho * q.Wo;
+    q.weight_elems = (int64_t)q.K * R;
+    if (q.bottom_elems * 4 > kMaxTensorBytes || q.top_elems * 4 > kMaxTensorBytes ||
+        q.weight_elems * 4 > kMaxTensorBytes)
+        return fail(CAFFE_ERR_UNSUPPORTED, "a tensor reaches 2^31 bytes");
+    q.R = (int)R;
+
+    // Phase-stacked data gradient: output row h with h + ph = sh*a + fh takes
+    // the taps u = fh + sh*t of output row i = a - t, t < Th = ceil(kh / sh).
+    q.Th = (q.kh + q.sh - 1) / q.sh;
+    q.Tw = (q.kw + q.sw - 1) / q.sw;
+    q.a0h = q.ph / q.sh;
+    q.a0w = q.pw / q.sw;
+    q.Ah = (q.H - 1 + q.ph) / q.sh - q.a0h + 1;
+    q.Aw = (q.W - 1 + q.pw) / q.sw - q.a0w + 1;
+    q.Mt = q.Cg * q.sh * q.sw;
+    q.Rt = q.Kg * q.Th * q.Tw;
+    const int64_t wt_elems = (int64_t)q.G * q.Mt * q.Rt;
+    const int64_t dcols = (int64_t)q.N * q.Ah * q.Aw;
+    if (wt_elems * 4 > kMaxTensorBytes || dcols > (int64_t(1) << 30))
+        return fail(CAFFE_ERR_UNSUPPORTED, "data-gradient operands reach 2^31 bytes");
+
+    // Weight-gradient split-K: aim for ~4 workgroups per CU, each split at
+    // least 8 stages deep.
+    const int64_t ncol = (int64_t)q.N * q.Ho * q.Wo;
+    const int tk = wgrad_tile_k();
+    const int64_t tiles = (int64_t)((q.Kg + wgrad_tile_m() - 1) / wgrad_tile_m()) *
+                          ((q.R + wgrad_tile_n() - 1) / wgrad_tile_n()) * q.G;
+    int64_t splits = (1024 + tiles - 1) / tiles;
+    const int64_t max_splits = std::max<int64_t>(1, ncol / (8 * tk));
+    const int64_t max_by_bytes = std::max<int64_t>(1, kMaxTensorBytes / (q.weight_elems * 4));
+    splits = std::max<int64_t>(1, std::min(std::min(splits, max_splits), max_by_bytes));
+    int64_t cps = (ncol + splits - 1) / splits;
+    cps = std::max<int64_t>(tk, (cps + tk - 1) / tk * tk);
+    splits = std::max<int64_t>(1, (ncol + cps - 1) / cps);
+    q.splits = (int)splits;
+    q.cols_per_split = (int)cps;
+    const int64_t part_bytes = splits * q.weight_elems * 4;
+    if (part_bytes > kMaxTensorBytes)
+        return fail(CAFFE_ERR_UNSUPPORTED, "weight-gradient partials reach 2^31 bytes");
+
+    // Workspace: [masked diff][plane sums][transformed weights][partials]
+    const size_t d_bytes = q.relu ? align_up(q.top_elems * 4, kWsAlign) : 0;
+    const size_t sums_bytes = align_up((size_t)q.N * q.K * 4, kWsAlign);
+    const size_t wt_bytes = align_up(wt_elems * 4, kWsAlign);
+    q.off_d = 0;
+    q.off_sums = d_bytes;
+    q.off_wt = q.off_sums + sums_bytes;
+    q.off_part = q.off_wt + wt_bytes;
+    q.ws_data = d_bytes + sums_bytes + wt_bytes;       // layout shared with ws_both
+    q.ws_weights = q.off_part + align_up(part_bytes, kWsAlign);
+    q.ws_both = q.ws_weights;
+    return CAFFE_OK;
+}
+
+int check_ptr(const void* ptr, bool required, const char* name)
+{
+    if (!ptr) {
+        if (required)
+            return fail(CAFFE_ERR_INVALID_ARG, "%s is NULL", name);
+        return CAFFE_OK;
+    }
+    if (!aligned(ptr, 16))
+        return fail(CAFFE_ERR_ALIGN, "%s is not 16-byte aligned", name);
+    return CAFFE_OK;
+}
+
+int check_ws(const void* ws, size_t ws_bytes, size_t need)
+{
+    if (need == 0)
+        return CAFFE_OK;
+    if (ws_bytes < need)
+        return fail(CAFFE_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu needed",
+                    ws_bytes, need);
+    if (!ws)
+        return fail(CAFFE_ERR_INVALID_ARG, "workspace is NULL");
+    if (!aligned(ws, kWsAlign))
+        return fail(CAFFE_ERR_ALIGN, "workspace is not 256-byte aligned");
+    return CAFFE_OK;
+}
+
+#define CHECK(expr)                                                                               \
+    do {                                                                                          \
+        int _st = (expr);                                                                         \
+        if (_st != CAFFE_OK)                                                                      \
+            return _st;                                                                           \
+    } while (0)
+
+#define LAUNCH(expr, what)                                                                        \
+    do {                                                                                          \
+        hipError_t _e = (expr);                                                                   \
+        if (_e != hipSuccess)                                                                     \
+            return hip_fail(_e, what);                                                            \
+    } while (0)
+
+int pick_tile(int M)
+{
+    // least padding of M, then the larger tile
+    int best = TILE_128x128;
+    double best_waste = 1e30;
+    for (int t = 0; t < TILE_COUNT; ++t) {
+        const int tm = gemm_tile_m(t);
+        const double waste = (double)((M + tm - 1) / tm * tm) / M;
+        if (waste < best_waste - 1e-9 ||
+            (waste < best_waste + 1e-9 && tm > gemm_tile_m(best))) {
+            best = t;
+            best_waste = waste;
+        }
+    }
+    return best;
+}
+
+uint32_t nbytes(int64_t elems, int64_t esize) { return (uint32_t)(elems * esize); }
+
+int run_forward(const ConvPlan& q, const void* bottom, const void* weight, const float* bias,
+                float* top, hipStream_t s)
+{
+    if (q.top_elems == 0)
+        return CAFFE_OK;
+    ConvGemmParams p = {};
+    p.A = weight;
+    p.X = bottom;
+    p.Y = top;
+    p.bias = bias;
+    p.A_bytes = nbytes(q.weight_elems, q.esize);
+    p.X_bytes = nbytes(q.bottom_elems, q.esize);
+    p.Y_bytes = nbytes(q.top_elems, 4);
+    p.N = q.N; p.Cin = q.C; p.IH = q.H; p.IW = q.W; p.Cin_g = q.Cg;
+    p.kh = q.kh; p.kw = q.kw; p.sh = q.sh; p.sw = q.sw; p.ph = q.ph; p.pw = q.pw;
+    p.OH = q.Ho; p.OW = q.Wo;
+    p.M = q.Kg; p.R = q.R; p.G = q.G;
+    p.Ncol = q.N * q.Ho * q.Wo;
+    p.relu = q.relu;
+    p.Cout = q.K; p.OutH = q.Ho; p.OutW = q.Wo;
+    LAUNCH(launch_conv_gemm_f32(p, 0, pick_tile(p.M), s), "forward launch");
+    return CAFFE_OK;
+}
+
+// D = masked top_diff (in the workspace when relu), plane sums for the bias.
+int run_mask(const ConvPlan& q, const float* top_diff, const float* top, char* ws, bool want_sums,
+             const float** dsrc, hipStream_t s)
+{
+    float* D = q.relu ? (float*)(ws + q.off_d) : nullptr;
+    float* sums = want_sums ? (float*)(ws + q.off_sums) : nullptr;
+    *dsrc = q.relu ? D : top_diff;
+    if (!D && !sums)
+        return CAFFE_OK;
+    LAUNCH(launch_relu_mask_bias(top_diff, top, D, sums, q.N * q.K, q.Ho * q.Wo, q.relu, s),
+           "relu/bias launch");
+    return CAFFE_OK;
+}
+
+int run_data(const ConvPlan& q, const float* dsrc, const void* weight, float* bottom_diff, char* ws,
+             hipStream_t s)
+{
+    if (q.bottom_elems == 0)
+        return CAFFE_OK;
+    float* wt = (float*)(ws + q.off_wt);
+    LAUNCH(launch_dgrad_weight_transform((const float*)weight, wt, q.G, q.Kg, q.Cg, q.kh, q.kw,
+                                         q.sh, q.sw, q.Th, q.Tw, s),
+           "weight transform launch");
+    ConvGemmParams p = {};
+    p.A = wt;
+    p.X = dsrc;
+    p.Y = bottom_diff;
+    p.bias = nullptr;
+    p.A_bytes = nbytes((int64_t)q.G * q.Mt * q.Rt, 4);
+    p.X_bytes = nbytes(q.top_elems, 4);
+    p.Y_bytes = nbytes(q.bottom_elems, 4);
+    p.N = q.N; p.Cin = q.K; p.IH = q.Ho; p.IW = q.Wo; p.Cin_g = q.Kg;
+    p.kh = q.Th; p.kw = q.Tw; p.sh = 1; p.sw = 1;
+    p.ph = q.Th - 1 - q.a0h; p.pw = q.Tw - 1 - q.a0w;  // may be negative: bounds-checked gather
+    p.OH = q.Ah; p.OW = q.Aw;
+    p.M = q.Mt; p.R = q.Rt; p.G = q.G;
+    p.Ncol = q.N * q.Ah * q.Aw;
+    p.relu = 0;
+    p.Cout = q.C; p.OutH = q.H; p.OutW = q.W;
+    p.psh = q.sh; p.psw = q.sw; p.a0h = q.a0h; p.a0w = q.a0w; p.oph = q.ph; p.opw = q.pw;
+    p.Cg_out = q.Cg;
+    LAUNCH(launch_conv_gemm_f32(p, 1, pick_tile(p.M), s), "data-gradient launch");
+    return CAFFE_OK;
+}
+
+int run_weights(const ConvPlan& q, const float* dsrc, const void* bottom, float* weight_diff,
+                float* bias_diff, int accumulate, char* ws, hipStream_t s)
+{
+    float* part = (float*)(ws + q.off_part);
+    if (weight_diff) {
+        WgradParams p = {};
+        p.D = dsrc;
+        p.X = bottom;
+        p.P = part;
+        p.D_bytes = nbytes(q.top_elems, 4);
+        p.X_bytes = nbytes(q.bottom_elems, q.esize);
+        p.P_bytes = nbytes((int64_t)q.splits * q.weight_elems, 4);
+        p.N = q.N; p.C = q.C; p.IH = q.H; p.IW = q.W; p.Cg = q.Cg; p.K = q.K; p.Kg = q.Kg;
+        p.kh = q.kh; p.kw = q.kw; p.sh = q.sh; p.sw = q.sw; p.ph = q.ph; p.pw = q.pw;
+        p.OH = q.Ho; p.OW = q.Wo;
+        p.R = q.R; p.G = q.G;
+        p.Ncol = q.N * q.Ho * q.Wo;
+        p.cols_per_split = q.cols_per_split;
+        p.splits = q.splits;
+        p.div_ohw = make_fastdiv((uint32_t)(q.Ho * q.Wo));
+        p.div_ow = make_fastdiv((uint32_t)q.Wo);
+        LAUNCH(launch_conv_wgrad_f32(p, s), "weight-gradient launch");
+    }
+    const float* sums = (const float*)(ws + q.off_sums);
+    LAUNCH(launch_wgrad_reduce(part, weight_diff, weight_diff ? (int)q.weight_elems : 0, q.splits,
+                               sums, bias_diff, q.N, q.K, accumulate, s),
+           "reduce launch");
+    return CAFFE_OK;
+}
+
+int check_conv_ptrs(const ConvPlan& q, const void* p, bool needed, bool is_blob, const char* name)
+{
+    // blob pointers may be NULL for an empty batch
+    const bool required = needed && (!is_blob || q.N > 0);
+    return check_ptr(p, required, name);
+}
+
+}  // namespace
+
+extern "C" {
+
+int caffe_conv_out_shape(const caffe_conv_desc* desc, int32_t* Ho, int32_t* Wo)
+{
+    ConvPlan q;
+    CHECK(plan_conv(desc, &q));
+    if (!Ho || !Wo)
+        return fail(CAFFE_ERR_INVALID_ARG, "Ho/Wo is NULL");
+    *Ho = q.Ho;
+    *Wo = q.Wo;
+    return CAFFE_OK;
+}
+
+int caffe_conv_workspace_size(const caffe_conv_desc* desc, int32_t pass, size_t* bytes)
+{
+    ConvPlan q;
+    CHECK(plan_conv(desc, &q));
+    if (!bytes)
+        return fail(CAFFE_ERR_INVALID_ARG, "bytes is NULL");
+    switch (pass) {
+    case CAFFE_PASS_FORWARD:
+        *bytes = 0;
+        return CAFFE_OK;
+    case CAFFE_PASS_BACKWARD_DATA:
+        *bytes = q.ws_data;
+        return CAFFE_OK;
+    case CAFFE_PASS_BACKWARD_WEIGHTS:
+        *bytes = q.ws_weights;
+        return CAFFE_OK;
+    case CAFFE_PASS_BACKWARD:
+        *bytes = q.ws_both;
+        return CAFFE_OK;
+    default:
+        return fail(CAFFE_ERR_INVALID_ARG, "unknown pass %d", pass);
+    }
+}
+
+int caffe_conv_forward(const caffe_conv_desc* desc, const void* bottom, const void* weight,
+                       const float* bias, float* top, void* workspace, size_t ws_bytes,
+                       void* stream)
+{
+    ConvPlan q;
+    CHECK(plan_conv(desc, &q));
+    CHECK(check_conv_ptrs(q, bottom, true, true, "bottom"));
+    CHECK(check_conv_ptrs(q, weight, true, false, "weight"));
+    CHECK(check_conv_ptrs(q, bias, false, false, "bias"));
+    CHECK(check_conv_ptrs(q, top, true, true, "top"));
+    CHECK(check_ws(workspace, ws_bytes, 0));
+    if (q.dtype != CAFFE_F32)
+        return fail(CAFFE_ERR_UNSUPPORTED, "bf16 forward is not built yet");
+    return run_forward(q, bottom, weight, bias, top, (hipStream_t)stream);
+}
+
+int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, const float* top,
+                        const void* bottom, const void* weight, float* bottom_diff,
+                        float* weight_diff, float* bias_diff, int32_t accumulate,
+                        void* workspace, size_t ws_bytes, void* stream)
+{
+    ConvPlan q;
+    CHECK(plan_conv(desc, &q));
+    if (accumulate != 0 && accumulate != 1)
+        return fail(CAFFE_ERR_INVALID_ARG, "accumulate must be 0 or 1");
+    CHECK(check_conv_ptrs(q, top_diff, true, true, "top_diff"));
+    CHECK(check_conv_ptrs(q, top, q.relu != 0, true, "top"));
+    CHECK(check_conv_ptrs(q, bottom, weight_diff != nullptr, true, "bottom"));
+    CHECK(check_conv_ptrs(q, weight, bottom_diff != nullptr, false, "weight"));
+    CHECK(check_conv_ptrs(q, bottom_diff, false, true, "bottom_diff"));
+    CHECK(check_conv_ptrs(q, weight_diff, false, false, "weight_diff"));
+    CHECK(check_conv_ptrs(q, bias_diff, false, false, "bias_diff"));
+    const size_t need = (weight_diff || bias_diff) ? q.ws_both : q.ws_data;
+    CHECK(check_ws(workspace, ws_bytes, need));
+    if (q.dtype != CAFFE_F32)
+        return fail(CAFFE_ERR_UNSUPPORTED, "bf16 backward is not built yet");
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    const float* dsrc = top_diff;
+    if (bottom_diff || weight_diff || bias_diff)
+        CHECK(run_mask(q, top_diff, top, ws, bias_diff != nullptr && q.N > 0, &dsrc, s));
+    if (bottom_diff)
+        CHECK(run_data(q, dsrc, weight, bottom_diff, ws, s));
+    if (weight_diff || bias_diff)
+        CHECK(run_weights(q, dsrc, bottom, weight_diff, bias_diff, accumulate, ws, s));
+    return CAFFE_OK;
+}
+
+int caffe_conv_backward_data(const caffe_conv_desc* desc, const float* top_diff, const float* top,
+                             const void* weight, float* bottom_diff, void* workspace,
+                             size_t ws_bytes, void* stream)
+{
+    ConvPlan q;
+    CHECK(plan_conv(desc, &q));
+    CHECK(check_conv_ptrs(q, bottom_diff, true, true, "bottom_diff"));
+    return caffe_conv_backward(desc, top_diff, top, nullptr, weight, bottom_diff, nullptr, nullptr,
+                               0, workspace, ws_bytes, stream);
+}
+
+int caffe_conv_backward_weights(const caffe_conv_desc* desc, const float* top_diff,
+                                const float* top, const void* bottom, float* weight_diff,
+                                float* bias_diff, int32_t accumulate, void* workspace,
+                                size_t ws_bytes, void* stream)
+{
+    ConvPlan q;
+    CHECK(plan_conv(desc, &q));
+    CHECK(check_conv_ptrs(q, weight_diff, true, false, "weight_diff"));
+    return caffe_conv_backward(desc, top_diff, top, bottom, nullptr, nullptr, weight_diff,
+                               bias_diff, accumulate, workspace, ws_bytes, stream);
+}
+
+const char* caffe_status_string(int32_t status)
+{
+    switch (status) {
+    case CAFFE_OK: return "CAFFE_OK";
+    case CAFFE_ERR_INVALID_ARG: return "CAFFE_ERR_INVALID_ARG";
+    case CAFFE_ERR_ALIGN: return "CAFFE_ERR_ALIGN";
+    case CAFFE_ERR_WORKSPACE: return "CAFFE_ERR_WORKSPACE";
+    case CAFFE_ERR_UNSUPPORTED: return "CAFFE_ERR_UNSUPPORTED";
+    case CAFFE_ERR_HIP: return "CAFFE_ERR_HIP";
+    default: return "CAFFE_ERR_UNKNOWN";
+    }
+}
+
+const char* caffe_last_error(void) { return g_err; }
+
+int32_t caffe_version(void) { return 100; }
+
+// ------------------------------------------------------------- glue layers
+static int plan_pool(const caffe_pool_desc* d, int* Ho, int* Wo)
+{
+    if (!d)
+        return fail(CAFFE_ERR_INVALID_ARG, "desc is NULL");
+    if (d->N < 0 || d->C < 1 || d->H < 1 || d->W < 1 || d->kernel_h < 1 || d->kernel_w < 1 ||
+        d->stride_h < 1 || d->stride_w < 1 || d->pad_h < 0 || d->pad_w < 0)
+        return fail(CAFFE_ERR_INVALID_ARG, "bad pooling geometry");
+    if (d->pad_h >= d->kernel_h || d->pad_w >= d->kernel_w)
+        return fail(CAFFE_ERR_INVALID_ARG, "pad must be smaller than the kernel");
+    if (d->H + 2 * (int64_t)d->pad_h < d->kernel_h || d->W + 2 * (int64_t)d->pad_w < d->kernel_w)
+        return fail(CAFFE_ERR_INVALID_ARG, "kernel larger than the padded input");
+    if (d->H > kMaxSpatial || d->W > kMaxSpatial || d->kernel_h > kMaxSpatial ||
+        d->kernel_w > kMaxSpatial || d->stride_h > kMaxSpatial || d->stride_w > kMaxSpatial)
+        return fail(CAFFE_ERR_UNSUPPORTED, "spatial sizes must be <= %d", kMaxSpatial);
+    if ((int64_t)d->N * d->C * d->H * d->W * 4 > kMaxTensorBytes)
+        return fail(CAFFE_ERR_UNSUPPORTED, "a tensor reaches 2^31 bytes");
+    *Ho = (d->H + 2 * d->pad_h - d->kernel_h) / d->stride_h + 1;
+    *Wo = (d->W + 2 * d->pad_w - d->kernel_w) / d->stride_w + 1;
+    return CAFFE_OK;
+}
+
+int caffe_pool_out_shape(const caffe_pool_desc* desc, int32_t* Ho, int32_t* Wo)
+{
+    int ho, wo;
+    CHECK(plan_pool(desc, &ho, &wo));
+    if (!Ho || !Wo)
+        return fail(CAFFE_ERR_INVALID_ARG, "Ho/Wo is NULL");
+    *Ho = ho;
+    *Wo = wo;
+    return CAFFE_OK;
+}
+
+int caffe_maxpool_forward(const caffe_pool_desc* d, const float* bottom, float* top,
+                          int32_t* mask, void* stream)
+{
+    int Ho, Wo;
+    CHECK(plan_pool(d, &Ho, &Wo));
+    const bool nz = d->N > 0;
+    CHECK(check_ptr(bottom, nz, "bottom"));
+    CHECK(check_ptr(top, nz, "top"));
+    CHECK(check_ptr(mask, false, "mask"));
+    LAUNCH(launch_maxpool_forward(bottom, top, mask, d->N * d->C, d->H, d->W, Ho, Wo, d->kernel_h,
+                                  d->kernel_w, d->stride_h, d->stride_w, d->pad_h, d->pad_w,
+                                  (hipStream_t)stream),
+           "max-pool forward launch");
+    return CAFFE_OK;
+}
+
+int caffe_maxpool_backward(const caffe_pool_desc* d, const float* top_diff, const int32_t* mask,
+                           float* bottom_diff, void* stream)
+{
+    int Ho, Wo;
+    CHECK(plan_pool(d, &Ho, &Wo));
+    const bool nz = d->N > 0;
+    CHECK(check_ptr(top_diff, nz, "top_diff"));
+    CHECK(check_ptr(mask, nz, "mask"));
+    CHECK(check_ptr(bottom_diff, nz, "bottom_diff"));
+    LAUNCH(launch_maxpool_backward(top_diff, mask, bottom_diff, d->N * d->C, d->H, d->W, Ho, Wo,
+                                   d->kernel_h, d->kernel_w, d->stride_h, d->stride_w, d->pad_h,
+                                   d->pad_w, (hipStream_t)stream),
+           "max-pool backward launch");
+    return CAFFE_OK;
+}
+
+static int check_lrn(const caffe_lrn_desc* d)
+{
+    if (!d)
+        return fail(CAFFE_ERR_INVALID_ARG, "desc is NULL");
+    if (d->N < 0 || d->C < 1 || d->H < 1 || d->W < 1 || d->local_size < 1)
+        return fail(CAFFE_ERR_INVALID_ARG, "bad LRN geometry");
+    if (!(d->k > 0.f) || !(d->alpha >= 0.f) || !(d->beta >= 0.f))
+        return fail(CAFFE_ERR_INVALID_ARG, "LRN needs k > 0, alpha >= 0, beta >= 0");
+    if ((int64_t)d->N * d->C * d->H * d->W * 4 > kMaxTensorBytes)
+        return fail(CAFFE_ERR_UNSUPPORTED, "a tensor reaches 2^31 bytes");
+    return CAFFE_OK;
+}
+
+int caffe_lrn_forward(const caffe_lrn_desc* d, const float* bottom, float* top, void* stream)
+{
+    CHECK(check_lrn(d));
+    const bool nz = d->N > 0;
+    CHECK(check_ptr(bottom, nz, "bottom"));
+    CHECK(check_ptr(top, nz, "top"));
+    LAUNCH(launch_lrn_forward(bottom, top, d->N, d->C, d->H * d->W, d->local_size, d->alpha,
+                              d->beta, d->k, (hipStream_t)stream),
+           "LRN forward launch");
+    return CAFFE_OK;
+}
+
+int caffe_lrn_backward(const caffe_lrn_desc* d, const float* bottom, const float* top,
+                       const float* top_diff, float* bottom_diff, void* stream)
+{
+    CHECK(check_lrn(d));
+    const bool nz = d->N > 0;
+    CHECK(check_ptr(bottom, nz, "bottom"));
+    CHECK(check_ptr(top, nz, "top"));
+    CHECK(check_ptr(top_diff, nz, "top_diff"));
+    CHECK(check_ptr(bottom_diff, nz, "bottom_diff"));
+    LAUNCH(launch_lrn_backward(bottom, top, top_diff, bottom_diff, d->N, d->C, d->H * d->W,
+                               d->local_size, d->alpha, d->beta, d->k, (hipStream_t)stream),
+           "LRN backward launch");
+    return CAFFE_OK;
+}
+
+int caffe_cast_f32_to_bf16(const float* in, uint16_t* out, int64_t count, void* stream)
+{
+    if (count < 0)
+        return fail(CAFFE_ERR_INVALID_ARG, "count < 0");
+    CHECK(check_ptr(in, count > 0, "in"));
+    CHECK(check_ptr(out, count > 0, "out"));
+    LAUNCH(launch_cast_f32_bf16(in, out, count, (hipStream_t)stream), "cast launch");
+    return CAFFE_OK;
+}
+
+}  // extern "C"

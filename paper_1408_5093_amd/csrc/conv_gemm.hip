@@ -1,0 +1,351 @@
+// conv_gemm.hip -- implicit-GEMM convolution on gfx950 fp32 MFMA.
+//
+// Forward pass and data gradient of the convolution layer (the paper's layer
+// definition, Sec. 3.2).  The lowering of the input to a dense contraction
+// ("im2col") is never materialised: each workgroup gathers its slice of the
+// lowered matrix straight from the NCHW blob into LDS, then runs the
+// contraction on the matrix cores.
+//
+// GEMM per group g:  C[m][col] = sum_r A[g][m][r] * B_g[r][col]
+//   r   = (c, u, v)  over Cin_g x kh x kw      (reduction, staged TK at a time)
+//   col = (n, i, j)  over N x OH x OW          (columns, TN per workgroup)
+//   B_g[r][col] = X[n][g*Cin_g + c][i*sh - ph + u][j*sw - pw + v]   (0 outside)
+//
+// Pipeline per workgroup: the global loads of stage s+1 are issued into
+// registers before the MFMAs of stage s run out of LDS buffer s%2, then the
+// registers go to LDS buffer (s+1)%2; one barrier per stage.
+//
+// MFMA operand layouts (single-block f32 variants):
+//   32x32x2 : A lane l -> (row l%32, k l/32), B lane l -> (k l/32, col l%32),
+//             D reg q -> (row 8*(q/4) + 4*(l/32) + q%4, col l%32)
+//   16x16x4 : A lane l -> (row l%16, k l/16), B lane l -> (k l/16, col l%16),
+//             D reg q -> (row 4*(l/16) + q, col l%16)
+#include "device_common.h"
+#include "kernels.h"
+
+namespace caffe_hip {
+
+template <int MT>
+struct Mfma;
+
+template <>
+struct Mfma<32> {
+    static constexpr int kStep = 2;
+    static constexpr int kRegs = 16;
+    typedef floatx16 acc_t;
+    static __device__ __forceinline__ acc_t run(float a, float b, acc_t c)
+    {
+        return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ int row(int q, int lane)
+    {
+        return 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
+    }
+};
+
+template <>
+struct Mfma<16> {
+    static constexpr int kStep = 4;
+    static constexpr int kRegs = 4;
+    typedef floatx4 acc_t;
+    static __device__ __forceinline__ acc_t run(float a, float b, acc_t c)
+    {
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ int row(int q, int lane) { return 4 * (lane >> 4) + q; }
+};
+
+template <int MT, int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH, int SW, int EPI>
+__global__ void __launch_bounds__(64 * WM * WN)
+conv_gemm_f32_kernel(const ConvGemmParams p)
+{
+    typedef Mfma<MT> Op;
+    constexpr int NT = 64 * WM * WN;
+    constexpr int TM = WM * MI * MT;
+    constexpr int TN = WN * NI * MT;
+    constexpr int EA = TM * TK / NT;  // A elements per thread per stage
+    constexpr int EB = TN * TK / NT;  // B elements per thread per stage
+    static_assert(TM * TK % NT == 0 && TN * TK % NT == 0, "tile/thread mismatch");
+    static_assert(NT % TK == 0, "A mapping needs TK | NT");
+    static_assert(TN % 64 == 0 && (NT % TN == 0 || TN % NT == 0), "B mapping");
+    static_assert(TK % Op::kStep == 0, "stage depth");
+    constexpr int BC = TN > NT ? TN / NT : 1;  // distinct B columns per thread
+    constexpr int PADA = 2;
+
+    __shared__ float As[2][TK][TM + PADA];
+    __shared__ float Bs[2][TK][TN];
+
+    const int kh = KH ? KH : p.kh;
+    const int kw = KW ? KW : p.kw;
+    const int sh = SH ? SH : p.sh;
+    const int sw = SW ? SW : p.sw;
+    const int khw = kh * kw;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave % WM;
+    const int wn = wave / WM;
+    const int g = blockIdx.z;
+    const int m0 = blockIdx.y * TM;
+    const int n0 = blockIdx.x * TN;
+    const int M = p.M, R = p.R;
+    const int IH = p.IH, IW = p.IW, IHW = IH * IW;
+    const int OHW = p.OH * p.OW;
+
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.A, p.A_bytes);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, p.X_bytes);
+
+    // ---- A mapping: k = tid % TK, m = tid / TK + (NT / TK) * q
+    const int a_k = tid % TK;
+    const int a_m = tid / TK;
+    int a_row[EA];
+#pragma unroll
+    for (int q = 0; q < EA; ++q) {
+        const int m = m0 + a_m + (NT / TK) * q;
+        a_row[q] = m < M ? (g * M + m) * R : -1;
+    }
+
+    // ---- B mapping: column(s) fixed per thread, reduction rows vary
+    int b_base[BC], b_ih0[BC], b_iw0[BC];
+#pragma unroll
+    for (int cc = 0; cc < BC; ++cc) {
+        const int col = n0 + (TN > NT ? tid + NT * cc : tid % TN);
+        if (col < p.Ncol) {
+            const int n = col / OHW;
+            const int pix = col - n * OHW;
+            const int i = pix / p.OW;
+            const int j = pix - i * p.OW;
+            b_ih0[cc] = i * sh - p.ph;
+            b_iw0[cc] = j * sw - p.pw;
+            b_base[cc] = (n * p.Cin + g * p.Cin_g) * IHW + b_ih0[cc] * IW + b_iw0[cc];
+        } else {
+            b_ih0[cc] = -(1 << 28);  // fails every bounds check
+            b_iw0[cc] = 0;
+            b_base[cc] = 0;
+        }
+    }
+
+    float rA[EA], rB[EB];
+
+    auto load_stage = [&](int kbase) {
+#pragma unroll
+        for (int q = 0; q < EA; ++q) {
+            const int r = kbase + a_k;
+            const uint32_t off =
+                (a_row[q] >= 0 && r < R) ? (uint32_t)(a_row[q] + r) * 4u : kOob;
+            rA[q] = buf_ld_f32(ra, off);
+        }
+#pragma unroll
+        for (int q = 0; q < EB; ++q) {
+            const int cc = TN > NT ? q % BC : 0;
+            const int kr = TN > NT ? q / BC : tid / TN + (NT / TN) * q;
+            const int r = __builtin_amdgcn_readfirstlane(kbase + kr);
+            const int c = r / khw;
+            const int rr = r - c * khw;
+            const int u = rr / kw;
+            const int v = rr - u * kw;
+            const int ih = b_ih0[cc] + u;
+            const int iw = b_iw0[cc] + v;
+            const bool ok = r < R && (unsigned)ih < (unsigned)IH && (unsigned)iw < (unsigned)IW;
+            const uint32_t off = ok ? (uint32_t)(b_base[cc] + c * IHW + u * IW + v) * 4u : kOob;
+            rB[q] = buf_ld_f32(rx, off);
+        }
+    };
+
+    auto store_stage = [&](int buf) {
+#pragma unroll
+        for (int q = 0; q < EA; ++q)
+            As[buf][a_k][a_m + (NT / TK) * q] = rA[q];
+#pragma unroll
+        for (int q = 0; q < EB; ++q) {
+            const int cc = TN > NT ? q % BC : 0;
+            const int kr = TN > NT ? q / BC : tid / TN + (NT / TN) * q;
+            const int col = TN > NT ? tid + NT * cc : tid % TN;
+            Bs[buf][kr][col] = rB[q];
+        }
+    };
+
+    typename Op::acc_t acc[MI][NI];
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+            acc[mi][ni] = typename Op::acc_t{};
+
+    const int nst = (R + TK - 1) / TK;
+    load_stage(0);
+    store_stage(0);
+    __syncthreads();
+
+    const int arow = wm * MI * MT + lane % MT;
+    const int bcol = wn * NI * MT + lane % MT;
+    const int kl = lane / MT;
+
+    for (int s = 0; s < nst; ++s) {
+        const int cur = s & 1;
+        if (s + 1 < nst)
+            load_stage((s + 1) * TK);
+#pragma unroll
+        for (int kk = 0; kk < TK; kk += Op::kStep) {
+            float a[MI], b[NI];
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi)
+                a[mi] = As[cur][kk + kl][arow + mi * MT];
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni)
+                b[ni] = Bs[cur][kk + kl][bcol + ni * MT];
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni)
+                    acc[mi][ni] = Op::run(a[mi], b[ni], acc[mi][ni]);
+        }
+        if (s + 1 < nst)
+            store_stage(cur ^ 1);
+        __syncthreads();
+    }
+
+    // ---- epilogue
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y, p.Y_bytes);
+    if constexpr (EPI == 0) {
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) {
+            const int col = n0 + bcol + ni * MT;
+            const bool cok = col < p.Ncol;
+            const int n = cok ? col / OHW : 0;
+            const int pix = col - n * OHW;
+            const int cbase = n * p.Cout * OHW + pix;
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi) {
+#pragma unroll
+                for (int q = 0; q < Op::kRegs; ++q) {
+                    const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
+                    if (m < M) {
+                        const int oc = g * M + m;
+                        float v = acc[mi][ni][q];
+                        if (p.bias)
+                            v += p.bias[oc];
+                        if (p.relu)
+                            v = v > 0.f ? v : 0.f;
+                        const uint32_t off = cok ? (uint32_t)(cbase + oc * OHW) * 4u : kOob;
+                        buf_st_f32(v, ry, off);
+                    }
+                }
+            }
+        }
+    } else {
+        const int pss = p.psh * p.psw;
+        const int OutHW = p.OutH * p.OutW;
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) {
+            const int col = n0 + bcol + ni * MT;
+            const bool cok = col < p.Ncol;
+            const int n = cok ? col / OHW : 0;
+            const int pix = col - n * OHW;
+            const int a = pix / p.OW;
+            const int b = pix - a * p.OW;
+            const int hb = p.psh * (a + p.a0h) - p.oph;
+            const int wb = p.psw * (b + p.a0w) - p.opw;
+            const int cbase = (n * p.Cout + g * p.Cg_out) * OutHW;
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi) {
+#pragma unroll
+                for (int q = 0; q < Op::kRegs; ++q) {
+                    const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
+                    if (m < M) {
+                        const int c = m / pss;
+                        const int fr = m - c * pss;
+                        const int fh = fr / p.psw;
+                        const int fw = fr - fh * p.psw;
+                        const int h = hb + fh;
+                        const int w = wb + fw;
+                        const bool ok = cok && (unsigned)h < (unsigned)p.OutH &&
+                                        (unsigned)w < (unsigned)p.OutW;
+                        const uint32_t off =
+                            ok ? (uint32_t)(cbase + c * OutHW + h * p.OutW + w) * 4u : kOob;
+                        buf_st_f32(acc[mi][ni][q], ry, off);
+                    }
+                }
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------------ launch
+namespace {
+
+struct TileShape {
+    int mt, wm, wn, mi, ni;
+};
+constexpr TileShape kTiles[TILE_COUNT] = {
+    {32, 2, 2, 2, 2},  // 128 x 128
+    {32, 1, 4, 3, 2},  // 96 x 256
+    {16, 1, 4, 3, 4},  // 48 x 256
+    {32, 1, 4, 2, 2},  // 64 x 256
+};
+
+template <int MT, int WM, int WN, int MI, int NI, int KH, int KW, int SH, int SW, int EPI>
+hipError_t launch_one(const ConvGemmParams& p, hipStream_t s)
+{
+    constexpr int TK = 16;
+    constexpr int TM = WM * MI * MT, TN = WN * NI * MT;
+    dim3 grid((p.Ncol + TN - 1) / TN, (p.M + TM - 1) / TM, p.G);
+    hipLaunchKernelGGL((conv_gemm_f32_kernel<MT, WM, WN, MI, NI, TK, KH, KW, SH, SW, EPI>), grid,
+                       dim3(64 * WM * WN), 0, s, p);
+    return hipGetLastError();
+}
+
+template <int MT, int WM, int WN, int MI, int NI, int EPI>
+hipError_t launch_geom(const ConvGemmParams& p, hipStream_t s)
+{
+    if (p.sh == 1 && p.sw == 1) {
+        if (p.kh == 3 && p.kw == 3)
+            return launch_one<MT, WM, WN, MI, NI, 3, 3, 1, 1, EPI>(p, s);
+        if (p.kh == 5 && p.kw == 5)
+            return launch_one<MT, WM, WN, MI, NI, 5, 5, 1, 1, EPI>(p, s);
+    }
+    if (EPI == 0 && p.kh == 11 && p.kw == 11 && p.sh == 4 && p.sw == 4)
+        return launch_one<MT, WM, WN, MI, NI, 11, 11, 4, 4, EPI>(p, s);
+    return launch_one<MT, WM, WN, MI, NI, 0, 0, 0, 0, EPI>(p, s);
+}
+
+template <int EPI>
+hipError_t launch_tile(const ConvGemmParams& p, int tile, hipStream_t s)
+{
+    switch (tile) {
+    case TILE_128x128:
+        return launch_geom<32, 2, 2, 2, 2, EPI>(p, s);
+    case TILE_96x256:
+        return launch_geom<32, 1, 4, 3, 2, EPI>(p, s);
+    case TILE_48x256:
+        return launch_geom<16, 1, 4, 3, 4, EPI>(p, s);
+    case TILE_64x256:
+        return launch_geom<32, 1, 4, 2, 2, EPI>(p, s);
+    default:
+        return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+int gemm_tile_m(int tile)
+{
+    const TileShape& t = kTiles[tile];
+    return t.wm * t.mi * t.mt;
+}
+
+int gemm_tile_n(int tile)
+{
+    const TileShape& t = kTiles[tile];
+    return t.wn * t.ni * t.mt;
+}
+
+hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, hipStream_t s)
+{
+    if (p.Ncol == 0)
+        return hipSuccess;
+    return epi == 0 ? launch_tile<0>(p, tile, s) : launch_tile<1>(p, tile, s);
+}
+
+}  // namespace caffe_hip

@@ -1,0 +1,235 @@
+// conv_wgrad.hip -- weight gradient of the convolution layer (the "gradients
+// with respect to the parameters" of the paper's Sec. 3.2 backward pass) as a
+// split-K implicit GEMM on gfx950 fp32 MFMA.
+//
+// Per group g:  dW_g[m][r] = sum_col D[n][g*Kg + m][i][j] * X[n][g*Cg + c][i*sh - ph + u][j*sw - pw + v]
+//   m   over Kg (output channels of the group)        -> GEMM rows, TM per workgroup
+//   r   = (c, u, v) over Cg x kh x kw                   -> GEMM columns, TN per workgroup
+//   col = (n, i, j) over N x OH x OW                    -> reduction, split into `splits`
+//                                                        contiguous ranges, TK per stage
+// Each (tile, split) writes its own partial sum; a separate kernel adds the
+// partials in a fixed order, so the result is reproducible bit for bit.
+//
+// Both operands are gathered with lanes running along the reduction index
+// (consecutive output pixels), which keeps the HBM/L2 reads coalesced.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace caffe_hip {
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t x, const FastDiv& f)
+{
+    return (uint32_t)(((uint64_t)x * f.mul) >> f.shift);
+}
+
+template <int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH, int SW>
+__global__ void __launch_bounds__(64 * WM * WN)
+conv_wgrad_f32_kernel(const WgradParams p)
+{
+    constexpr int MT = 32;
+    constexpr int NT = 64 * WM * WN;
+    constexpr int TM = WM * MI * MT;
+    constexpr int TN = WN * NI * MT;
+    constexpr int RS = NT / TK;       // rows covered by one pass of the block
+    constexpr int EA = TM / RS;       // A elements per thread per stage
+    constexpr int EB = TN / RS;       // B elements per thread per stage
+    static_assert(NT % TK == 0 && TM % RS == 0 && TN % RS == 0, "wgrad mapping");
+    static_assert(TK % 2 == 0, "stage depth");
+
+    // Row stride = 2 (mod 32) keeps the lane-along-k LDS writes conflict-free.
+    __shared__ float As[2][TK][TM + 2];
+    __shared__ float Bs[2][TK][TN + 2];
+
+    const int kh = KH ? KH : p.kh;
+    const int kw = KW ? KW : p.kw;
+    const int sh = SH ? SH : p.sh;
+    const int sw = SW ? SW : p.sw;
+    const int khw = kh * kw;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave % WM;
+    const int wn = wave / WM;
+    const int g = blockIdx.z % p.G;
+    const int split = blockIdx.z / p.G;
+    const int m0 = blockIdx.y * TM;
+    const int r0 = blockIdx.x * TN;
+    const int IH = p.IH, IW = p.IW, IHW = IH * IW;
+    const int OHW = p.OH * p.OW;
+
+    const int col_begin = split * p.cols_per_split;
+    const int col_end = min(p.Ncol, col_begin + p.cols_per_split);
+
+    const __amdgpu_buffer_rsrc_t rd = make_rsrc(p.D, p.D_bytes);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, p.X_bytes);
+
+    const int kc = tid % TK;  // reduction index within a stage
+    const int rw = tid / TK;  // row within one pass
+
+    // Per-thread A rows (output channels) and B rows (taps), fixed for the kernel.
+    int a_off[EA];
+#pragma unroll
+    for (int q = 0; q < EA; ++q) {
+        const int m = m0 + rw + RS * q;
+        a_off[q] = m < p.Kg ? (g * p.Kg + m) * OHW : -1;
+    }
+    int b_off[EB], b_uv[EB];
+#pragma unroll
+    for (int q = 0; q < EB; ++q) {
+        const int r = r0 + rw + RS * q;
+        if (r < p.R) {
+            const int c = r / khw;
+            const int rr = r - c * khw;
+            const int u = rr / kw;
+            const int v = rr - u * kw;
+            b_off[q] = c * IHW + u * IW + v;
+            b_uv[q] = u | (v << 16);
+        } else {
+            b_off[q] = 0;
+            b_uv[q] = 0x7fff;  // u beyond any image height: always out of range
+        }
+    }
+
+    float rA[EA], rB[EB];
+
+    auto load_stage = [&](int cbase) {
+        const int col = cbase + kc;
+        const bool cok = col < col_end;
+        const int n = (int)fdiv((uint32_t)col, p.div_ohw);
+        const int pix = col - n * OHW;
+        const int i = (int)fdiv((uint32_t)pix, p.div_ow);
+        const int j = pix - i * p.OW;
+        const int dbase = n * p.K * OHW + pix;
+        const int ih0 = i * sh - p.ph;
+        const int iw0 = j * sw - p.pw;
+        const int xbase = (n * p.C + g * p.Cg) * IHW + ih0 * IW + iw0;
+#pragma unroll
+        for (int q = 0; q < EA; ++q) {
+            const uint32_t off = (cok && a_off[q] >= 0) ? (uint32_t)(dbase + a_off[q]) * 4u : kOob;
+            rA[q] = buf_ld_f32(rd, off);
+        }
+#pragma unroll
+        for (int q = 0; q < EB; ++q) {
+            const int ih = ih0 + (b_uv[q] & 0xffff);
+            const int iw = iw0 + (b_uv[q] >> 16);
+            const bool ok = cok && (unsigned)ih < (unsigned)IH && (unsigned)iw < (unsigned)IW;
+            const uint32_t off = ok ? (uint32_t)(xbase + b_off[q]) * 4u : kOob;
+            rB[q] = buf_ld_f32(rx, off);
+        }
+    };
+
+    auto store_stage = [&](int buf) {
+#pragma unroll
+        for (int q = 0; q < EA; ++q)
+            As[buf][kc][rw + RS * q] = rA[q];
+#pragma unroll
+        for (int q = 0; q < EB; ++q)
+            Bs[buf][kc][rw + RS * q] = rB[q];
+    };
+
+    floatx16 acc[MI][NI];
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+            acc[mi][ni] = floatx16{};
+
+    const int nst = col_end > col_begin ? (col_end - col_begin + TK - 1) / TK : 0;
+    if (nst > 0) {
+        load_stage(col_begin);
+        store_stage(0);
+    }
+    __syncthreads();
+
+    const int arow = wm * MI * MT + (lane & 31);
+    const int bcol = wn * NI * MT + (lane & 31);
+    const int kl = lane >> 5;
+
+    for (int s = 0; s < nst; ++s) {
+        const int cur = s & 1;
+        if (s + 1 < nst)
+            load_stage(col_begin + (s + 1) * TK);
+#pragma unroll
+        for (int kk = 0; kk < TK; kk += 2) {
+            float a[MI], b[NI];
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi)
+                a[mi] = As[cur][kk + kl][arow + mi * MT];
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni)
+                b[ni] = Bs[cur][kk + kl][bcol + ni * MT];
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni)
+                    acc[mi][ni] =
+                        __builtin_amdgcn_mfma_f32_32x32x2f32(a[mi], b[ni], acc[mi][ni], 0, 0, 0);
+        }
+        if (s + 1 < nst)
+            store_stage(cur ^ 1);
+        __syncthreads();
+    }
+
+    // Partial result P[split][g*Kg + m][r]: lanes run along r (contiguous).
+    const __amdgpu_buffer_rsrc_t rp = make_rsrc(p.P, p.P_bytes);
+    const int pbase = split * p.K * p.R;
+#pragma unroll
+    for (int ni = 0; ni < NI; ++ni) {
+        const int r = r0 + bcol + ni * MT;
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) {
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                const int m = m0 + wm * MI * MT + mi * MT + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
+                const bool ok = m < p.Kg && r < p.R;
+                const uint32_t off = ok ? (uint32_t)(pbase + (g * p.Kg + m) * p.R + r) * 4u : kOob;
+                buf_st_f32(acc[mi][ni][q], rp, off);
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------------ launch
+namespace {
+constexpr int kWM = 2, kWN = 2, kMI = 2, kNI = 2, kTK = 16;
+
+template <int KH, int KW, int SH, int SW>
+hipError_t launch_w(const WgradParams& p, hipStream_t s)
+{
+    constexpr int TM = kWM * kMI * 32, TN = kWN * kNI * 32;
+    dim3 grid((p.R + TN - 1) / TN, (p.Kg + TM - 1) / TM, p.G * p.splits);
+    hipLaunchKernelGGL((conv_wgrad_f32_kernel<kWM, kWN, kMI, kNI, kTK, KH, KW, SH, SW>), grid,
+                       dim3(64 * kWM * kWN), 0, s, p);
+    return hipGetLastError();
+}
+}  // namespace
+
+int wgrad_tile_m() { return kWM * kMI * 32; }
+int wgrad_tile_n() { return kWN * kNI * 32; }
+int wgrad_tile_k() { return kTK; }
+
+hipError_t launch_conv_wgrad_f32(const WgradParams& p, hipStream_t s)
+{
+    if (p.sh == 1 && p.sw == 1) {
+        if (p.kh == 3 && p.kw == 3)
+            return launch_w<3, 3, 1, 1>(p, s);
+        if (p.kh == 5 && p.kw == 5)
+            return launch_w<5, 5, 1, 1>(p, s);
+    }
+    if (p.kh == 11 && p.kw == 11 && p.sh == 4 && p.sw == 4)
+        return launch_w<11, 11, 4, 4>(p, s);
+    return launch_w<0, 0, 0, 0>(p, s);
+}
+
+FastDiv make_fastdiv(uint32_t d)
+{
+    uint32_t l = 0;
+    while ((1ull << l) < d)
+        ++l;
+    const uint32_t shift = 31 + l;
+    const uint64_t mul = ((1ull << shift) + d - 1) / d;
+    return FastDiv{d, (uint32_t)mul, shift};
+}
+
+}  // namespace caffe_hip

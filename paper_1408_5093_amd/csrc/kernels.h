@@ -1,0 +1,107 @@
+// kernels.h -- host-side view of the gfx950 kernels: parameter blocks and
+// launchers.  Shapes are validated by the C ABI layer (api.cpp) before any
+// launcher runs; launchers trust their arguments.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace caffe_hip {
+
+// Unsigned division by a runtime constant d >= 1 for numerators < 2^31:
+// q = (x * mul) >> shift with shift = 31 + ceil(log2 d), mul = ceil(2^shift / d).
+struct FastDiv {
+    uint32_t d, mul, shift;
+};
+FastDiv make_fastdiv(uint32_t d);
+
+// Implicit GEMM whose reduction index r = (c, u, v) walks a kh x kw window of
+// a gather source X[N][Cin][IH][IW] and whose column index walks the output
+// grid (n, i, j) in N x OH x OW:
+//   C_g[m][col] = sum_r A[g][m][r] * X[n][g*Cin_g + c][i*sh - ph + u][j*sw - pw + v]
+// epi == 0 (forward): Y[n][g*M + m][i][j] = [relu](C + bias[g*M + m])
+// epi == 1 (data gradient, phase-stacked): row m = (c, fh, fw) and
+//   Y[n][g*Cg_out + c][psh*(i + a0h) + fh - oph][psw*(j + a0w) + fw - opw] = C
+//   for in-range positions (each output element is written exactly once).
+struct ConvGemmParams {
+    const void* A;
+    const void* X;
+    float* Y;
+    const float* bias;
+    uint32_t A_bytes, X_bytes, Y_bytes;
+    int N, Cin, IH, IW, Cin_g;
+    int kh, kw, sh, sw, ph, pw;
+    int OH, OW;
+    int M, R, G;
+    int Ncol;
+    int relu;
+    int Cout, OutH, OutW;
+    int psh, psw, a0h, a0w, oph, opw, Cg_out;
+};
+
+// Split-K weight gradient:
+//   P[s][g*Kg + m][r] = sum_{col in split s} D[n][g*Kg + m][i][j] * X[n][g*Cg + c][i*sh - ph + u][j*sw - pw + v]
+struct WgradParams {
+    const void* D;
+    const void* X;
+    float* P;
+    uint32_t D_bytes, X_bytes, P_bytes;
+    int N, C, IH, IW, Cg, K, Kg;
+    int kh, kw, sh, sw, ph, pw;
+    int OH, OW;
+    int R, G;
+    int Ncol, cols_per_split, splits;
+    FastDiv div_ohw, div_ow;
+};
+
+// Tile shapes a launcher may pick; see conv_gemm.hip.
+enum GemmTile : int {
+    TILE_128x128 = 0,  // 32x32x2 MFMA, 4 waves as 2x2, each 64x64
+    TILE_96x256 = 1,   // 32x32x2 MFMA, 4 waves as 1x4, each 96x64
+    TILE_48x256 = 2,   // 16x16x4 MFMA, 4 waves as 1x4, each 48x64
+    TILE_64x256 = 3,   // 32x32x2 MFMA, 4 waves as 1x4, each 64x64
+    TILE_COUNT
+};
+int gemm_tile_m(int tile);
+int gemm_tile_n(int tile);
+
+hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, hipStream_t s);
+
+int wgrad_tile_m();
+int wgrad_tile_n();
+int wgrad_tile_k();
+hipError_t launch_conv_wgrad_f32(const WgradParams& p, hipStream_t s);
+
+// D = relu ? G * [Y > 0] : G (written to D unless D is null) and, unless
+// plane_sums is null, plane_sums[p] = sum of D over plane p (fixed order).
+hipError_t launch_relu_mask_bias(const float* G, const float* Y, float* D, float* plane_sums,
+                                 int planes, int plane_size, int relu, hipStream_t s);
+
+// Wt[g][(c, fh, fw)][(k, th, tw)] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)]
+// (0 where the tap index passes the kernel edge).
+hipError_t launch_dgrad_weight_transform(const float* W, float* Wt, int G, int Kg, int Cg, int kh,
+                                         int kw, int sh, int sw, int Th, int Tw, hipStream_t s);
+
+// out[i] = (accumulate ? out[i] : 0) + sum_{s < splits} P[s*count + i]   (fixed order)
+// and, if db != null, db[k] = (accumulate ? db[k] : 0) + sum_{n < N} plane_sums[n*K + k].
+hipError_t launch_wgrad_reduce(const float* P, float* out, int count, int splits,
+                               const float* plane_sums, float* db, int N, int K, int accumulate,
+                               hipStream_t s);
+
+hipError_t launch_fill_zero(float* out, int64_t count, hipStream_t s);
+
+// Glue layers (layers.hip).
+hipError_t launch_maxpool_forward(const float* x, float* y, int32_t* mask, int NC, int H, int W,
+                                  int OH, int OW, int kh, int kw, int sh, int sw, int ph, int pw,
+                                  hipStream_t s);
+hipError_t launch_maxpool_backward(const float* dy, const int32_t* mask, float* dx, int NC, int H,
+                                   int W, int OH, int OW, int kh, int kw, int sh, int sw, int ph,
+                                   int pw, hipStream_t s);
+hipError_t launch_lrn_forward(const float* x, float* y, int N, int C, int HW, int size,
+                              float alpha, float beta, float k, hipStream_t s);
+hipError_t launch_lrn_backward(const float* x, const float* y, const float* dy, float* dx, int N,
+                               int C, int HW, int size, float alpha, float beta, float k,
+                               hipStream_t s);
+hipError_t launch_cast_f32_bf16(const float* x, uint16_t* y, int64_t count, hipStream_t s);
+
+}  // namespace caffe_hip

@@ -1,0 +1,137 @@
+"""A fixed chain of convolution layers with the glue between them, run
+forward and backward through the C ABI on one stream.
+
+The paper's Sec. 3.3 describes a network as bookkeeping over layers: a
+forward sweep from the data to the top, then a backward sweep that hands
+each layer the gradient of its output.  ``ConvStack`` is that bookkeeping for
+a fixed chain (CaffeNet conv1-5 with max-pool + LRN after conv1 and conv2, or
+the LeNet conv pair with max-pool between), with every blob preallocated
+once so that a step allocates nothing.  Every arithmetic step is a library
+call; this module only owns buffers and the call order.
+"""
+import torch
+
+from . import (CAFFE_BF16, CAFFE_F32, PASS_BACKWARD, Workspace, caffe_conv_backward,
+               caffe_conv_forward, cast_f32_to_bf16, conv_desc, conv_out_shape,
+               conv_workspace_size, lrn_backward, lrn_forward, maxpool_backward, maxpool_forward,
+               pool_desc, pool_out_shape)
+
+
+class ConvStack:
+    """layers: sequence of workloads.ConvLayer.  glue: {l: [("pool", {...}) | ("lrn", {...})]}
+    applied in order to the output of layer l.  bf16=True runs the convolutions on
+    bfloat16 operands (fp32 accumulation and outputs); glue stays fp32."""
+
+    def __init__(self, layers, N, weights, biases, glue=None, bf16=False, device="cuda"):
+        self.layers = list(layers)
+        self.N = N
+        self.bf16 = bf16
+        self.glue = glue or {}
+        dev = torch.device(device)
+        dt = CAFFE_BF16 if bf16 else CAFFE_F32
+        op = torch.bfloat16 if bf16 else torch.float32
+        self.descs, self.W, self.b, self.dW, self.db = [], [], [], [], []
+        self.top, self.dtop_glue, self.dbottom, self.bottom_op = [], [], [], []
+        self.stages = []  # per layer: list of glue stage dicts
+        ws_need = 0
+        for l, L in enumerate(self.layers):
+            d = conv_desc((N, L.C, L.H, L.W), (L.K, L.C // L.g, L.k, L.k), L.s, L.p, L.g, L.relu,
+                          dt)
+            Ho, Wo = conv_out_shape(d)
+            self.descs.append(d)
+            w = torch.as_tensor(weights[l], dtype=torch.float32).to(dev)
+            self.W.append(w.to(op).contiguous())
+            self.b.append(torch.as_tensor(biases[l], dtype=torch.float32).to(dev).contiguous())
+            self.dW.append(torch.empty(w.shape, dtype=torch.float32, device=dev))
+            self.db.append(torch.empty(L.K, dtype=torch.float32, device=dev))
+            self.top.append(torch.empty((N, L.K, Ho, Wo), dtype=torch.float32, device=dev))
+            self.dbottom.append(torch.empty((N, L.C, L.H, L.W), dtype=torch.float32, device=dev))
+            self.bottom_op.append(torch.empty((N, L.C, L.H, L.W), dtype=op, device=dev)
+                                  if bf16 else None)
+            ws_need = max(ws_need, conv_workspace_size(d, PASS_BACKWARD))
+            cur = (N, L.K, Ho, Wo)
+            stages = []
+            for kind, prm in self.glue.get(l, []):
+                st = dict(kind=kind, prm=dict(prm), in_shape=cur)
+                if kind == "pool":
+                    pd = pool_desc(cur, prm["kernel"], prm["stride"], prm.get("pad", 0))
+                    ph, pw = pool_out_shape(pd)
+                    cur = (N, cur[1], ph, pw)
+                    st["mask"] = torch.empty(cur, dtype=torch.int32, device=dev)
+                elif kind != "lrn":
+                    raise ValueError(f"unknown glue layer {kind}")
+                st["y"] = torch.empty(cur, dtype=torch.float32, device=dev)
+                st["dx"] = torch.empty(st["in_shape"], dtype=torch.float32, device=dev)
+                stages.append(st)
+            self.stages.append(stages)
+            if l + 1 < len(self.layers):
+                nx = self.layers[l + 1]
+                if cur != (N, nx.C, nx.H, nx.W):
+                    raise ValueError(f"layer {l} output {cur} does not feed layer {l + 1}")
+        self.ws = Workspace(dev).get(ws_need)
+        self.bottom = [None] * len(self.layers)
+        # when a list, (tag, event) pairs are recorded around every conv call
+        self.events = None
+
+    def _mark(self, tag, s):
+        if self.events is not None:
+            ev = torch.cuda.Event(enable_timing=True)
+            ev.record(s)
+            self.events.append((tag, ev))
+
+    def forward(self, x, stream=None):
+        """x: (N, C, H, W) float32 device tensor.  Returns the last layer's top."""
+        s = stream or torch.cuda.current_stream()
+        cur = x
+        for l in range(len(self.layers)):
+            self.bottom[l] = cur
+            src = cur
+            if self.bf16:
+                src = cast_f32_to_bf16(cur, out=self.bottom_op[l], stream=s)
+            self._mark(("fwd", l, "begin"), s)
+            caffe_conv_forward(self.descs[l], src, self.W[l], self.b[l], self.top[l], None, s)
+            self._mark(("fwd", l, "end"), s)
+            cur = self.top[l]
+            for st in self.stages[l]:
+                p = st["prm"]
+                st["x"] = cur
+                if st["kind"] == "pool":
+                    maxpool_forward(cur, p["kernel"], p["stride"], p.get("pad", 0), out=st["y"],
+                                    mask=st["mask"], stream=s)
+                else:
+                    lrn_forward(cur, p["size"], p["alpha"], p["beta"], p["k"], out=st["y"],
+                                stream=s)
+                cur = st["y"]
+        return self.top[-1]
+
+    def backward(self, top_diff, stream=None, data_grad_bottom=True):
+        """top_diff: gradient w.r.t. the last top.  Fills dW, db and dbottom
+        (dbottom[0] only when data_grad_bottom)."""
+        s = stream or torch.cuda.current_stream()
+        g = top_diff
+        for l in range(len(self.layers) - 1, -1, -1):
+            L = self.layers[l]
+            for st in reversed(self.stages[l]):
+                p = st["prm"]
+                if st["kind"] == "pool":
+                    g = maxpool_backward(st["in_shape"], g, st["mask"], p["kernel"], p["stride"],
+                                         p.get("pad", 0), out=st["dx"], stream=s)
+                else:
+                    g = lrn_backward(st["x"], st["y"], g, p["size"], p["alpha"], p["beta"],
+                                     p["k"], out=st["dx"], stream=s)
+            want_dx = l > 0 or data_grad_bottom
+            bottom = self.bottom_op[l] if self.bf16 else self.bottom[l]
+            self._mark(("bwd", l, "begin"), s)
+            caffe_conv_backward(self.descs[l], g, self.top[l] if L.relu else None, bottom,
+                                self.W[l], self.dbottom[l] if want_dx else None, self.dW[l],
+                                self.db[l], 0, self.ws, s)
+            self._mark(("bwd", l, "end"), s)
+            g = self.dbottom[l]
+        return self.dbottom[0]
+
+    def layer_top_diff(self, l, top_diff_last):
+        """Gradient that layer l received in the last backward (after its glue)."""
+        if l == len(self.layers) - 1:
+            return top_diff_last
+        st = self.stages[l]
+        return st[0]["dx"] if st else self.dbottom[l + 1]

@@ -1,0 +1,183 @@
+"""The C ABI on the CPU: the library loads, exports every symbol the public
+headers declare, and turns every invalid argument into its status code
+before any GPU work (so none of these calls needs a GPU)."""
+import ctypes
+import glob
+import os
+import re
+
+import pytest
+
+import paper_1408_5093_amd as cc
+from paper_1408_5093_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        src = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(caffe_[a-z0-9_]+)\s*\(", src))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = cc.load()
+    declared = _declared()
+    assert declared, "no declarations found"
+    assert declared == set(_lib.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert lib.caffe_version() >= 100
+
+
+def test_status_strings():
+    lib = cc.load()
+    for code, name in [(0, b"CAFFE_OK"), (-1, b"CAFFE_ERR_INVALID_ARG"), (-2, b"CAFFE_ERR_ALIGN"),
+                       (-3, b"CAFFE_ERR_WORKSPACE"), (-4, b"CAFFE_ERR_UNSUPPORTED"),
+                       (-5, b"CAFFE_ERR_HIP")]:
+        assert lib.caffe_status_string(code) == name
+
+
+@pytest.mark.parametrize("x,w,s,p,g,out", [
+    ((256, 3, 227, 227), (96, 3, 11, 11), 4, 0, 1, (55, 55)),
+    ((256, 96, 27, 27), (256, 48, 5, 5), 1, 2, 2, (27, 27)),
+    ((256, 256, 13, 13), (384, 256, 3, 3), 1, 1, 1, (13, 13)),
+    ((256, 384, 13, 13), (384, 192, 3, 3), 1, 1, 2, (13, 13)),
+    ((256, 384, 13, 13), (256, 192, 3, 3), 1, 1, 2, (13, 13)),
+    ((64, 1, 28, 28), (20, 1, 5, 5), 1, 0, 1, (24, 24)),
+    ((64, 20, 12, 12), (50, 20, 5, 5), 1, 0, 1, (8, 8)),
+    ((2, 3, 7, 9), (4, 3, 3, 2), (2, 3), (1, 0), 1, (4, 3)),
+])
+def test_out_shape(x, w, s, p, g, out):
+    assert cc.conv_out_shape(cc.conv_desc(x, w, s, p, g)) == out
+
+
+def _status(fn, *args):
+    return fn(*args)
+
+
+def _desc(**kw):
+    d = cc.conv_desc((2, 4, 9, 9), (6, 2, 3, 3), 1, 1, 2, True)
+    for k, v in kw.items():
+        setattr(d, k, v)
+    return d
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("C", 0, -1), ("H", -1, -1), ("K", 0, -1), ("N", -1, -1), ("kernel_h", 0, -1),
+    ("stride_w", 0, -1), ("pad_h", -1, -1), ("group", 0, -1), ("group", 3, -1),
+    ("K", 7, -1), ("relu", 2, -1), ("dtype", 7, -4), ("kernel_h", 12, -1),
+    ("H", 20000, -4), ("pad_w", 17000, -4),
+])
+def test_invalid_descriptor(field, value, code):
+    lib = cc.load()
+    d = _desc(**{field: value})
+    Ho, Wo = ctypes.c_int32(), ctypes.c_int32()
+    assert lib.caffe_conv_out_shape(ctypes.byref(d), ctypes.byref(Ho), ctypes.byref(Wo)) == code
+    n = ctypes.c_size_t()
+    assert lib.caffe_conv_workspace_size(ctypes.byref(d), 3, ctypes.byref(n)) == code
+    P = ctypes.c_void_p
+    assert lib.caffe_conv_forward(ctypes.byref(d), P(0x1000), P(0x2000), None, P(0x3000), None, 0,
+                                  None) == code
+    assert lib.caffe_last_error() != b""
+
+
+def test_null_desc_and_outputs():
+    lib = cc.load()
+    Ho = ctypes.c_int32()
+    assert lib.caffe_conv_out_shape(None, ctypes.byref(Ho), ctypes.byref(Ho)) == -1
+    d = _desc()
+    assert lib.caffe_conv_out_shape(ctypes.byref(d), None, None) == -1
+    assert lib.caffe_conv_workspace_size(ctypes.byref(d), 9, ctypes.byref(ctypes.c_size_t())) == -1
+
+
+def test_tensor_size_limit():
+    lib = cc.load()
+    d = cc.conv_desc((4096, 256, 256, 256), (8, 256, 3, 3))  # 2^36 bytes of input
+    n = ctypes.c_size_t()
+    assert lib.caffe_conv_workspace_size(ctypes.byref(d), 0, ctypes.byref(n)) == -4
+
+
+def test_workspace_sizes():
+    d = cc.conv_desc((256, 3, 227, 227), (96, 3, 11, 11), 4, 0, 1, True)
+    assert cc.conv_workspace_size(d, cc.PASS_FORWARD) == 0
+    data = cc.conv_workspace_size(d, cc.PASS_BACKWARD_DATA)
+    wts = cc.conv_workspace_size(d, cc.PASS_BACKWARD_WEIGHTS)
+    both = cc.conv_workspace_size(d, cc.PASS_BACKWARD)
+    top_bytes = 256 * 96 * 55 * 55 * 4
+    assert data >= top_bytes and wts >= top_bytes  # masked diff lives in the workspace
+    assert both >= max(data, wts)
+    for v in (data, wts, both):
+        assert v % 256 == 0
+    d.relu = 0
+    assert cc.conv_workspace_size(d, cc.PASS_BACKWARD) < both
+
+
+def test_pointer_checks_before_any_launch():
+    lib = cc.load()
+    P = ctypes.c_void_p
+    d = _desc()
+    ws = cc.conv_workspace_size(d, cc.PASS_BACKWARD)
+    fwd = lambda *a: lib.caffe_conv_forward(ctypes.byref(d), *a)
+    assert fwd(None, P(0x2000), None, P(0x3000), None, 0, None) == -1          # bottom NULL
+    assert fwd(P(0x1000), None, None, P(0x3000), None, 0, None) == -1          # weight NULL
+    assert fwd(P(0x1004), P(0x2000), None, P(0x3000), None, 0, None) == -2     # misaligned
+    assert fwd(P(0x1000), P(0x2000), P(0x4008), P(0x3000), None, 0, None) == -2  # bias
+    bwd = lambda *a: lib.caffe_conv_backward(ctypes.byref(d), *a)
+    # relu needs top
+    assert bwd(P(0x1000), None, P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0,
+               P(0x100000), ws, None) == -1
+    # workspace too small / NULL / misaligned
+    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0,
+               P(0x100000), ws - 1, None) == -3
+    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0,
+               None, ws, None) == -1
+    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0,
+               P(0x100080), ws, None) == -2
+    # accumulate flag
+    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 2,
+               P(0x100000), ws, None) == -1
+    # weight gradient needs bottom; data gradient needs weight
+    assert bwd(P(0x1000), P(0x1800), None, P(0x3000), None, P(0x5000), None, 0,
+               P(0x100000), ws, None) == -1
+    assert bwd(P(0x1000), P(0x1800), P(0x2000), None, P(0x4000), None, None, 0,
+               P(0x100000), ws, None) == -1
+    bd = lib.caffe_conv_backward_data
+    assert bd(ctypes.byref(d), P(0x1000), P(0x1800), P(0x2000), None, P(0x100000), ws, None) == -1
+    bw = lib.caffe_conv_backward_weights
+    assert bw(ctypes.byref(d), P(0x1000), P(0x1800), P(0x2000), None, None, 0, P(0x100000), ws,
+              None) == -1
+
+
+def test_glue_validation():
+    lib = cc.load()
+    P = ctypes.c_void_p
+    pd = cc.pool_desc((2, 3, 55, 55), 3, 2)
+    assert cc.pool_out_shape(pd) == (27, 27)
+    assert cc.pool_out_shape(cc.pool_desc((2, 3, 24, 24), 2, 2)) == (12, 12)
+    bad = cc.pool_desc((2, 3, 55, 55), 3, 2, 3)  # pad >= kernel
+    assert lib.caffe_maxpool_forward(ctypes.byref(bad), P(0x1000), P(0x2000), None, None) == -1
+    assert lib.caffe_maxpool_forward(ctypes.byref(pd), P(0x1004), P(0x2000), None, None) == -2
+    assert lib.caffe_maxpool_backward(ctypes.byref(pd), P(0x1000), None, P(0x2000), None) == -1
+    ld = cc.lrn_desc((2, 3, 5, 5), 0)
+    assert lib.caffe_lrn_forward(ctypes.byref(ld), P(0x1000), P(0x2000), None) == -1
+    ld = cc.lrn_desc((2, 3, 5, 5), 5, k=0.0)
+    assert lib.caffe_lrn_forward(ctypes.byref(ld), P(0x1000), P(0x2000), None) == -1
+    assert lib.caffe_cast_f32_to_bf16(P(0x1000), P(0x2000), -1, None) == -1
+    assert lib.caffe_cast_f32_to_bf16(P(0x1002), P(0x2000), 5, None) == -2
+
+
+def test_fastdiv_formula():
+    # the host-side magic numbers for unsigned division used by the weight-
+    # gradient kernel: q = (x * mul) >> (31 + ceil(log2 d)) for x < 2^31
+    import random
+    random.seed(3)
+    for d in list(range(1, 2000)) + [3025, 3249, 169, 729, 12544, 1 << 20, (1 << 30) + 3]:
+        l = (d - 1).bit_length()
+        sh = 31 + l
+        mul = ((1 << sh) + d - 1) // d
+        assert mul < (1 << 32)
+        for x in [0, d - 1, d, 2 ** 31 - 1] + [random.randrange(2 ** 31) for _ in range(50)]:
+            assert (x * mul) >> sh == x // d

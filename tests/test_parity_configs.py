@@ -1,0 +1,156 @@
+"""Parity at the full workload sizes, in the launch configuration the
+benchmark times (the same descriptors, the same ConvStack chain).
+
+* LeNet conv pair (N=64): every output is compared with the oracle.
+* CaffeNet at N=256: the oracle recomputes sampled outputs -- whole images
+  for the forward pass and the data gradient (each image is independent),
+  whole filters for the weight gradient (each filter's gradient is a sum
+  over the full batch), every bias gradient -- from the very tensors the GPU
+  consumed (layer by layer on shared inputs).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1408_5093_amd as cc
+from paper_1408_5093_amd import workloads as wl
+from paper_1408_5093_amd.net import ConvStack
+from helpers import TOL_F32, assert_close
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _np(t):
+    torch.cuda.synchronize()
+    return t.detach().float().cpu().numpy()
+
+
+def _geom(L):
+    return dict(stride=L.s, pad=L.p, group=L.g)
+
+
+def check_layer_sampled(L, x, w, b, top, top_diff, dx, dw, db, images, filters, tol=TOL_F32,
+                        what=""):
+    """x, w, b, top_diff: the operands the GPU layer consumed (numpy);
+    top, dx, dw, db: its outputs.  dx may be None (not computed)."""
+    print(f"check {what}: images {images} filters {filters}", flush=True)
+    xs = x[images]
+    y_ref = oracle.conv_forward(xs, w, b, L.s, L.p, L.g, L.relu)
+    assert_close(top[images], y_ref, tol, f"{what} forward")
+    if top_diff is None:
+        return
+    topm = top if L.relu else None
+    if dx is not None:
+        dx_ref, _, _ = oracle.conv_backward(xs, w, top_diff[images],
+                                            top=None if topm is None else topm[images],
+                                            relu=L.relu, need=("dx",), **_geom(L))
+        assert_close(dx[images], dx_ref, tol, f"{what} data gradient")
+    # bias gradient of every filter (the oracle's db loop alone is cheap at full size)
+    _, _, db_ref = oracle.conv_backward(x, w, top_diff, top=topm, relu=L.relu, need=("db",),
+                                        **_geom(L))
+    assert_close(db, db_ref, tol, f"{what} bias gradient")
+    Kg, Cg = L.K // L.g, L.C // L.g
+    for k in filters:
+        t = k // Kg
+        _, dw_ref, _ = oracle.conv_backward(
+            x[:, t * Cg:(t + 1) * Cg], w[k:k + 1], top_diff[:, k:k + 1],
+            top=None if topm is None else topm[:, k:k + 1], relu=L.relu, stride=L.s, pad=L.p,
+            need=("dw",))
+        assert_close(dw[k:k + 1], dw_ref, tol, f"{what} weight gradient filter {k}")
+
+
+def test_lenet_pair_full():
+    inp = wl.lenet_pair(64)
+    net = ConvStack(wl.LENET, 64, inp["W"], inp["b"], glue={0: [("pool", wl.LENET_POOL)]})
+    x = torch.from_numpy(inp["x"]).to(DEV)
+    g = torch.from_numpy(inp["top_diff"]).to(DEV)
+    net.forward(x)
+    net.backward(g)
+    L1, L2 = wl.LENET
+    x1 = inp["x"]
+    top1 = _np(net.top[0])
+    y1_ref = oracle.conv_forward(x1, inp["W"][0], inp["b"][0], 1, 0, 1, False)
+    assert_close(top1, y1_ref, TOL_F32, "conv1 forward")
+    pool = net.stages[0][0]
+    x2 = _np(pool["y"])
+    np.testing.assert_array_equal(x2, oracle.maxpool_forward(top1, 2, 2).astype(np.float32))
+    y2_ref = oracle.conv_forward(x2, inp["W"][1], inp["b"][1], 1, 0, 1, False)
+    assert_close(_np(net.top[1]), y2_ref, TOL_F32, "conv2 forward")
+    dx2_ref, dw2_ref, db2_ref = oracle.conv_backward(x2, inp["W"][1], inp["top_diff"])
+    assert_close(_np(net.dbottom[1]), dx2_ref, TOL_F32, "conv2 data gradient")
+    assert_close(_np(net.dW[1]), dw2_ref, TOL_F32, "conv2 weight gradient")
+    assert_close(_np(net.db[1]), db2_ref, TOL_F32, "conv2 bias gradient")
+    g1 = _np(pool["dx"])
+    assert_close(g1, oracle.maxpool_backward(top1, _np(net.dbottom[1]), 2, 2), TOL_F32,
+                 "pool backward")
+    dx1_ref, dw1_ref, db1_ref = oracle.conv_backward(x1, inp["W"][0], g1)
+    assert_close(_np(net.dbottom[0]), dx1_ref, TOL_F32, "conv1 data gradient")
+    assert_close(_np(net.dW[0]), dw1_ref, TOL_F32, "conv1 weight gradient")
+    assert_close(_np(net.db[0]), db1_ref, TOL_F32, "conv1 bias gradient")
+
+
+def test_caffenet_conv1_forward_full_size():
+    inp = wl.caffenet_conv1_fwd(256)
+    L = wl.CAFFENET[0]
+    y = cc.conv_forward(torch.from_numpy(inp["x"]).to(DEV), torch.from_numpy(inp["W"]).to(DEV),
+                        torch.from_numpy(inp["b"]).to(DEV), L.s, L.p, L.g, L.relu)
+    check_layer_sampled(L, inp["x"], inp["W"], inp["b"], _np(y), None, None, None, None,
+                        images=[0, 131, 255], filters=[], what="conv1")
+
+
+@pytest.mark.parametrize("l", [1, 2, 3, 4])
+def test_caffenet_conv25_forward_full_size(l):
+    inp = wl.caffenet_conv25_layer(l, 256)
+    L = wl.CAFFENET[l]
+    y = cc.conv_forward(torch.from_numpy(inp["x"]).to(DEV), torch.from_numpy(inp["W"]).to(DEV),
+                        torch.from_numpy(inp["b"]).to(DEV), L.s, L.p, L.g, L.relu)
+    check_layer_sampled(L, inp["x"], inp["W"], inp["b"], _np(y), None, None, None, None,
+                        images=[0, 77, 255], filters=[], what=L.name)
+
+
+def caffenet_glue():
+    return {0: [("pool", wl.CAFFENET_POOL), ("lrn", wl.CAFFENET_LRN)],
+            1: [("pool", wl.CAFFENET_POOL), ("lrn", wl.CAFFENET_LRN)]}
+
+
+def test_caffenet_training_step_full_size():
+    N = 256
+    inp = wl.caffenet_step(N)
+    net = ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue())
+    x = torch.from_numpy(inp["x"]).to(DEV)
+    g = torch.from_numpy(inp["top_diff"]).to(DEV)
+    net.forward(x)
+    net.backward(g)
+    torch.cuda.synchronize()
+    images = [0, 255]
+    for l, L in enumerate(wl.CAFFENET):
+        xl = _np(net.bottom[l])
+        gl = _np(net.layer_top_diff(l, g))
+        check_layer_sampled(L, xl, inp["W"][l], inp["b"][l], _np(net.top[l]), gl,
+                            _np(net.dbottom[l]), _np(net.dW[l]), _np(net.db[l]), images=images,
+                            filters=[0, L.K - 1], what=f"step {L.name}")
+        for st in net.stages[l]:
+            xin = _np(st["x"])[images]
+            p = st["prm"]
+            if st["kind"] == "pool":
+                ref = oracle.maxpool_forward(xin, p["kernel"], p["stride"])
+                np.testing.assert_array_equal(_np(st["y"])[images], ref.astype(np.float32))
+                gref = oracle.maxpool_backward(xin, _np(_glue_dy(net, l, st))[images],
+                                               p["kernel"], p["stride"])
+            else:
+                ref = oracle.lrn_forward(xin, p["size"], p["alpha"], p["beta"], p["k"])
+                assert_close(_np(st["y"])[images], ref, TOL_F32, f"{L.name} LRN forward")
+                gref = oracle.lrn_backward(xin, _np(_glue_dy(net, l, st))[images], p["size"],
+                                           p["alpha"], p["beta"], p["k"])
+            assert_close(_np(st["dx"])[images], gref, TOL_F32, f"{L.name} {st['kind']} backward")
+
+
+def _glue_dy(net, l, st):
+    """Gradient the glue stage st (after layer l) received in the backward sweep."""
+    stages = net.stages[l]
+    i = next(j for j, s in enumerate(stages) if s is st)
+    if i + 1 < len(stages):
+        return stages[i + 1]["dx"]
+    return net.dbottom[l + 1]

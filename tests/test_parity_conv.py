@@ -1,0 +1,171 @@
+"""GPU parity of the convolution layer (C ABI -> gfx950 kernels) against the
+CPU oracle on identical seeded inputs.
+
+Bar: max|gpu - oracle| / max|oracle| <= 1e-4 per output tensor (fp32).  The
+backward pass gets the same `top` (the oracle's forward output rounded to
+fp32) on both sides, so the ReLU mask [top > 0] is identical.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1408_5093_amd as cc
+from helpers import TOL_F32, assert_close
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _t(a, dtype=torch.float32):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV, dtype)
+
+
+def _np(t):
+    torch.cuda.synchronize()
+    return t.detach().float().cpu().numpy()
+
+
+def run_case(N, C, H, W, K, kh, kw, sh, sw, ph, pw, g, relu, bias=True, seed=0, tol=TOL_F32):
+    print(f"case N={N} C={C} H={H} W={W} K={K} k={kh}x{kw} s={sh},{sw} p={ph},{pw} g={g} "
+          f"relu={relu} bias={bias}", flush=True)
+    rng = np.random.default_rng([77, seed, N, C, H, W, K, kh, kw, sh, sw, ph, pw, g, int(relu)])
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    w = (rng.standard_normal((K, C // g, kh, kw)) * 0.3).astype(np.float32)
+    b = (rng.standard_normal(K) * 0.5).astype(np.float32) if bias else None
+    y_ref = oracle.conv_forward(x, w, b, (sh, sw), (ph, pw), g, relu)
+    y = cc.conv_forward(_t(x), _t(w), _t(b) if bias else None, (sh, sw), (ph, pw), g, relu)
+    assert_close(_np(y), y_ref, tol, "forward")
+
+    top = y_ref.astype(np.float32)
+    gd = rng.standard_normal(top.shape).astype(np.float32)
+    dx_ref, dw_ref, db_ref = oracle.conv_backward(x, w, gd, top=top, stride=(sh, sw),
+                                                  pad=(ph, pw), group=g, relu=relu)
+    dx, dw, db = cc.conv_backward(_t(x), _t(w), _t(gd), _t(top), (sh, sw), (ph, pw), g, relu)
+    assert_close(_np(dx), dx_ref, tol, "data gradient")
+    assert_close(_np(dw), dw_ref, tol, "weight gradient")
+    assert_close(_np(db), db_ref, tol, "bias gradient")
+    return y, dx, dw, db
+
+
+# geometry sweep: strides 1-4, pads 0-3, kernels 1-11, groups 1-4, ragged sizes
+SWEEP = [
+    # N, C, H, W, K, kh, kw, sh, sw, ph, pw, g
+    (2, 3, 17, 19, 5, 3, 3, 1, 1, 1, 1, 1),
+    (1, 1, 9, 9, 1, 1, 1, 1, 1, 0, 0, 1),
+    (3, 7, 19, 19, 150, 3, 3, 1, 1, 1, 1, 1),     # 2 row tiles, ragged columns
+    (2, 8, 15, 13, 12, 5, 5, 1, 1, 2, 2, 2),
+    (2, 3, 35, 35, 16, 11, 11, 4, 4, 0, 0, 1),    # conv1-like
+    (2, 3, 37, 33, 10, 11, 11, 4, 4, 2, 1, 1),    # conv1-like, padded, ragged
+    (1, 12, 11, 11, 20, 3, 3, 2, 2, 1, 1, 4),
+    (2, 6, 10, 14, 9, 2, 3, 3, 2, 1, 2, 3),       # stride > kernel rows
+    (1, 4, 8, 8, 6, 3, 3, 1, 1, 3, 3, 2),         # pad = kernel
+    (2, 5, 7, 6, 7, 7, 6, 1, 1, 0, 0, 1),         # kernel = image (1x1 output)
+    (3, 96, 13, 13, 70, 5, 5, 1, 1, 2, 2, 2),
+    (1, 2, 40, 3, 4, 1, 3, 1, 1, 0, 1, 1),
+    (2, 16, 9, 9, 200, 1, 1, 1, 1, 0, 0, 1),      # 1x1 conv, 2 row tiles
+    (1, 4, 23, 23, 48, 4, 4, 3, 3, 1, 1, 1),
+    (2, 9, 12, 12, 33, 5, 5, 2, 2, 2, 2, 3),
+]
+
+
+@pytest.mark.parametrize("case", SWEEP)
+@pytest.mark.parametrize("relu", [False, True])
+def test_sweep(case, relu):
+    run_case(*case, relu=relu, bias=(case[0] % 2 == 0) or relu)
+
+
+def test_tile_shapes_each_chooser_branch():
+    # output channels per group hitting each tile height: 20 (48-row tile), 50 (64),
+    # 96 (96), 128 (128), 192 (96 x 2), 256 (128 x 2), plus a 3-row-tile case
+    for K, g in [(20, 1), (50, 1), (96, 1), (128, 1), (384, 2), (256, 1), (300, 1)]:
+        run_case(2, 2 * g, 9, 10, K, 3, 3, 1, 1, 1, 1, g, True)
+
+
+def test_data_gradient_phase_stacked_row_heights():
+    # C/group * stride^2 rows: 3*16 = 48 (conv1), 1*4, 5*9, 8*16 = 128
+    for C, s, k in [(3, 4, 11), (1, 2, 5), (5, 3, 7), (8, 4, 5)]:
+        run_case(2, C, 29, 31, 6, k, k, s, s, 1, 2, 1, True)
+
+
+def test_empty_batch():
+    x = torch.empty((0, 4, 9, 9), device=DEV)
+    w = torch.randn((6, 2, 3, 3), device=DEV)
+    y = cc.conv_forward(x, w, torch.zeros(6, device=DEV), 1, 1, 2, True)
+    assert y.shape == (0, 6, 9, 9)
+    g = torch.empty(y.shape, device=DEV)
+    dx, dw, db = cc.conv_backward(x, w, g, y, 1, 1, 2, True)
+    torch.cuda.synchronize()
+    assert dx.shape == x.shape
+    assert torch.all(dw == 0) and torch.all(db == 0)
+
+
+def test_accumulate_adds():
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((2, 4, 11, 11)).astype(np.float32)
+    w = rng.standard_normal((8, 4, 3, 3)).astype(np.float32)
+    g = rng.standard_normal((2, 8, 11, 11)).astype(np.float32)
+    _, dw_ref, db_ref = oracle.conv_backward(x, w, g, stride=1, pad=1)
+    dw0 = rng.standard_normal(w.shape).astype(np.float32)
+    db0 = rng.standard_normal(8).astype(np.float32)
+    dwt, dbt = _t(dw0), _t(db0)
+    cc.conv_backward(_t(x), _t(w), _t(g), None, 1, 1, 1, False, need=("dw", "db"), accumulate=1,
+                     outs=(None, dwt, dbt))
+    assert_close(_np(dwt), dw_ref + dw0, TOL_F32, "accumulated dW")
+    assert_close(_np(dbt), db_ref + db0, TOL_F32, "accumulated db")
+
+
+def test_separate_entry_points_match_combined():
+    rng = np.random.default_rng(9)
+    x = _t(rng.standard_normal((2, 6, 13, 13)))
+    w = _t(rng.standard_normal((10, 3, 3, 3)) * 0.2)
+    y = cc.conv_forward(x, w, None, 1, 1, 2, True)
+    g = _t(rng.standard_normal(y.shape))
+    dx, dw, db = cc.conv_backward(x, w, g, y, 1, 1, 2, True)
+    dx2 = cc.conv_backward_data(x.shape, w, g, y, 1, 1, 2, True)
+    dw2, db2 = cc.conv_backward_weights(x, w.shape, g, y, 1, 1, 2, True)
+    torch.cuda.synchronize()
+    assert torch.equal(dx, dx2) and torch.equal(dw, dw2) and torch.equal(db, db2)
+
+
+def test_bitwise_determinism():
+    rng = np.random.default_rng(11)
+    x = _t(rng.standard_normal((4, 16, 27, 27)))
+    w = _t(rng.standard_normal((32, 8, 5, 5)) * 0.1)
+    b = _t(rng.standard_normal(32))
+    outs = []
+    for _ in range(2):
+        y = cc.conv_forward(x, w, b, 1, 2, 2, True)
+        g = torch.ones_like(y) * 0.5
+        outs.append((y,) + cc.conv_backward(x, w, g, y, 1, 2, 2, True))
+    torch.cuda.synchronize()
+    for a, b_ in zip(*outs):
+        assert torch.equal(a, b_)
+
+
+def test_no_writes_outside_outputs():
+    # canary bands around every output buffer must survive forward + backward
+    rng = np.random.default_rng(13)
+    N, C, H, W, K = 3, 6, 14, 15, 20
+    x = _t(rng.standard_normal((N, C, H, W)))
+    w = _t(rng.standard_normal((K, C // 2, 3, 3)))
+    band = 4096
+    canary = -12345.0
+
+    def guarded(n):
+        buf = torch.full((band + n + band,), canary, device=DEV)
+        return buf, buf[band:band + n]
+
+    ybuf, yv = guarded(N * K * H * W)
+    y = yv.view(N, K, H, W)
+    cc.caffe_conv_forward(cc.conv_desc(x.shape, w.shape, 1, 1, 2, True), x, w, None, y)
+    dxbuf, dxv = guarded(x.numel())
+    dwbuf, dwv = guarded(w.numel())
+    dbbuf, dbv = guarded(K)
+    g = _t(rng.standard_normal((N, K, H, W)))
+    cc.conv_backward(x, w, g, y, 1, 1, 2, True,
+                     outs=(dxv.view(x.shape), dwv.view(w.shape), dbv))
+    torch.cuda.synchronize()
+    for buf in (ybuf, dxbuf, dwbuf, dbbuf):
+        assert torch.all(buf[:band] == canary) and torch.all(buf[-band:] == canary)

@@ -51,9 +51,12 @@ struct ConvPlan {
     int Th, Tw, a0h, a0w, Ah, Aw, Mt, Rt;
     // weight gradient split-K
     int splits, cols_per_split;
+    // reduction order of the implicit GEMMs: tap-major r = (u, v, c) when the
+    // gathered channels per group fill whole pipeline stages
+    bool fwd_tap, dgrad_tap;
     // workspace layout (byte offsets), per pass
     size_t off_d, off_sums, off_wt, off_part;
-    size_t ws_data, ws_weights, ws_both;
+    size_t ws_fwd, ws_data, ws_weights, ws_both;
 };
 
 int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
@@ -136,6 +139,10 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     if (part_bytes > kMaxTensorBytes)
         return fail(CAFFE_ERR_UNSUPPORTED, "weight-gradient partials reach 2^31 bytes");
 
+    q.fwd_tap = q.Cg % kGemmTK == 0;
+    q.dgrad_tap = q.Kg % kGemmTK == 0;
+    q.ws_fwd = q.fwd_tap ? align_up(q.weight_elems * 4, kWsAlign) : 0;
+
     // Workspace: [masked diff][plane sums][transformed weights][partials]
     const size_t d_bytes = q.relu ? align_up(q.top_elems * 4, kWsAlign) : 0;
     const size_t sums_bytes = align_up((size_t)q.N * q.K * 4, kWsAlign);
@@ -210,12 +217,19 @@ int pick_tile(int M)
 uint32_t nbytes(int64_t elems, int64_t esize) { return (uint32_t)(elems * esize); }
 
 int run_forward(const ConvPlan& q, const void* bottom, const void* weight, const float* bias,
-                float* top, hipStream_t s)
+                float* top, char* ws, hipStream_t s)
 {
     if (q.top_elems == 0)
         return CAFFE_OK;
+    const void* A = weight;
+    if (q.fwd_tap) {
+        float* wp = (float*)ws;
+        LAUNCH(launch_pack_weights_tap((const float*)weight, wp, q.K, q.Cg, q.kh * q.kw, s),
+               "weight pack launch");
+        A = wp;
+    }
     ConvGemmParams p = {};
-    p.A = weight;
+    p.A = A;
     p.X = bottom;
     p.Y = top;
     p.bias = bias;
@@ -229,7 +243,7 @@ int run_forward(const ConvPlan& q, const void* bottom, const void* weight, const
     p.Ncol = q.N * q.Ho * q.Wo;
     p.relu = q.relu;
     p.Cout = q.K; p.OutH = q.Ho; p.OutW = q.Wo;
-    LAUNCH(launch_conv_gemm_f32(p, 0, pick_tile(p.M), s), "forward launch");
+    LAUNCH(launch_conv_gemm_f32(p, 0, pick_tile(p.M), q.fwd_tap, s), "forward launch");
     return CAFFE_OK;
 }
 
@@ -254,7 +268,7 @@ int run_data(const ConvPlan& q, const float* dsrc, const void* weight, float* bo
         return CAFFE_OK;
     float* wt = (float*)(ws + q.off_wt);
     LAUNCH(launch_dgrad_weight_transform((const float*)weight, wt, q.G, q.Kg, q.Cg, q.kh, q.kw,
-                                         q.sh, q.sw, q.Th, q.Tw, s),
+                                         q.sh, q.sw, q.Th, q.Tw, q.dgrad_tap, s),
            "weight transform launch");
     ConvGemmParams p = {};
     p.A = wt;
@@ -274,7 +288,7 @@ int run_data(const ConvPlan& q, const float* dsrc, const void* weight, float* bo
     p.Cout = q.C; p.OutH = q.H; p.OutW = q.W;
     p.psh = q.sh; p.psw = q.sw; p.a0h = q.a0h; p.a0w = q.a0w; p.oph = q.ph; p.opw = q.pw;
     p.Cg_out = q.Cg;
-    LAUNCH(launch_conv_gemm_f32(p, 1, pick_tile(p.M), s), "data-gradient launch");
+    LAUNCH(launch_conv_gemm_f32(p, 1, pick_tile(p.M), q.dgrad_tap, s), "data-gradient launch");
     return CAFFE_OK;
 }
 
@@ -338,7 +352,7 @@ int caffe_conv_workspace_size(const caffe_conv_desc* desc, int32_t pass, size_t*
         return fail(CAFFE_ERR_INVALID_ARG, "bytes is NULL");
     switch (pass) {
     case CAFFE_PASS_FORWARD:
-        *bytes = 0;
+        *bytes = q.ws_fwd;
         return CAFFE_OK;
     case CAFFE_PASS_BACKWARD_DATA:
         *bytes = q.ws_data;
@@ -364,10 +378,10 @@ int caffe_conv_forward(const caffe_conv_desc* desc, const void* bottom, const vo
     CHECK(check_conv_ptrs(q, weight, true, false, "weight"));
     CHECK(check_conv_ptrs(q, bias, false, false, "bias"));
     CHECK(check_conv_ptrs(q, top, true, true, "top"));
-    CHECK(check_ws(workspace, ws_bytes, 0));
+    CHECK(check_ws(workspace, ws_bytes, q.ws_fwd));
     if (q.dtype != CAFFE_F32)
         return fail(CAFFE_ERR_UNSUPPORTED, "bf16 forward is not built yet");
-    return run_forward(q, bottom, weight, bias, top, (hipStream_t)stream);
+    return run_forward(q, bottom, weight, bias, top, (char*)workspace, (hipStream_t)stream);
 }
 
 int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, const float* top,

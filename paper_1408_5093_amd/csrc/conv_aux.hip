@@ -49,11 +49,11 @@ hipError_t launch_relu_mask_bias(const float* G, const float* Y, float* D, float
     return hipGetLastError();
 }
 
-// Wt[g][m = (c, fh, fw)][r = (k, th, tw)]
-//   = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)], 0 past the kernel edge.
+// Wt[g][m = (c, fh, fw)][r] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)],
+// 0 past the kernel edge; r = (k, th, tw), or r = (th, tw, k) when tap.
 __global__ void __launch_bounds__(256)
 dgrad_weight_transform_kernel(const float* __restrict__ W, float* __restrict__ Wt, int G, int Kg,
-                              int Cg, int kh, int kw, int sh, int sw, int Th, int Tw)
+                              int Cg, int kh, int kw, int sh, int sw, int Th, int Tw, int tap)
 {
     const int Mt = Cg * sh * sw;
     const int Rt = Kg * Th * Tw;
@@ -64,8 +64,14 @@ dgrad_weight_transform_kernel(const float* __restrict__ W, float* __restrict__ W
         const long gm = e / Rt;
         const int m = (int)(gm % Mt);
         const int g = (int)(gm / Mt);
-        const int k = r / (Th * Tw);
-        const int t = r - k * Th * Tw;
+        int k, t;
+        if (tap) {  // r = (th, tw, k)
+            t = r / Kg;
+            k = r - t * Kg;
+        } else {    // r = (k, th, tw)
+            k = r / (Th * Tw);
+            t = r - k * Th * Tw;
+        }
         const int th = t / Tw, tw = t - th * Tw;
         const int c = m / (sh * sw);
         const int f = m - c * sh * sw;
@@ -80,7 +86,8 @@ dgrad_weight_transform_kernel(const float* __restrict__ W, float* __restrict__ W
 }
 
 hipError_t launch_dgrad_weight_transform(const float* W, float* Wt, int G, int Kg, int Cg, int kh,
-                                         int kw, int sh, int sw, int Th, int Tw, hipStream_t s)
+                                         int kw, int sh, int sw, int Th, int Tw, bool tap_major,
+                                         hipStream_t s)
 {
     const long total = (long)G * Cg * sh * sw * Kg * Th * Tw;
     if (total == 0)
@@ -89,31 +96,60 @@ hipError_t launch_dgrad_weight_transform(const float* W, float* Wt, int G, int K
     if (blocks > 4096)
         blocks = 4096;
     hipLaunchKernelGGL(dgrad_weight_transform_kernel, dim3((unsigned)blocks), dim3(256), 0, s, W,
-                       Wt, G, Kg, Cg, kh, kw, sh, sw, Th, Tw);
+                       Wt, G, Kg, Cg, kh, kw, sh, sw, Th, Tw, tap_major ? 1 : 0);
     return hipGetLastError();
 }
 
-// Fixed-order sums: out[i] = (acc ? out[i] : 0) + P[0][i] + P[1][i] + ...,
-// db[k] = (acc ? db[k] : 0) + sums[0*K + k] + sums[1*K + k] + ...
-__global__ void __launch_bounds__(256)
+// Fixed-order sums: out[i] = (acc ? out[i] : 0) + sum_s P[s][i],
+// db[k] = (acc ? db[k] : 0) + sum_n sums[n*K + k].
+// A block owns 32 consecutive outputs; its 8 waves-of-32-lanes each add the
+// terms q = part, part + 8, ... in order (lanes along i: coalesced), then one
+// lane per output adds the 8 part sums in order.  The association is fixed
+// by (count of terms, 8), so results are bitwise reproducible.
+constexpr int kRedParts = 8;
+constexpr int kRedCols = 32;
+
+__global__ void __launch_bounds__(kRedParts * kRedCols)
 wgrad_reduce_kernel(const float* __restrict__ P, float* __restrict__ out, int count, int splits,
                     const float* __restrict__ plane_sums, float* __restrict__ db, int N, int K,
                     int accumulate)
 {
+    __shared__ float part[kRedParts][kRedCols + 1];
+    const int col = threadIdx.x % kRedCols;
+    const int pt = threadIdx.x / kRedCols;
+    const int e = blockIdx.x * kRedCols + col;
     const int total = count + (db ? K : 0);
-    for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += gridDim.x * blockDim.x) {
-        if (e < count) {
-            float s = 0.f;
-            for (int q = 0; q < splits; ++q)
-                s += P[(size_t)q * count + e];
-            out[e] = accumulate ? out[e] + s : s;
-        } else {
-            const int k = e - count;
-            float s = 0.f;
-            for (int n = 0; n < N; ++n)
-                s += plane_sums[(size_t)n * K + k];
-            db[k] = accumulate ? db[k] + s : s;
+    const bool is_w = e < count;
+    const float* src = is_w ? P + e : plane_sums + (e - count);
+    const size_t stride = is_w ? (size_t)count : (size_t)K;
+    const int terms = is_w ? splits : N;
+    float s = 0.f;
+    if (e < total) {
+        int q = pt;
+        for (; q + 3 * kRedParts < terms; q += 4 * kRedParts) {
+            const float a0 = src[(size_t)q * stride];
+            const float a1 = src[(size_t)(q + kRedParts) * stride];
+            const float a2 = src[(size_t)(q + 2 * kRedParts) * stride];
+            const float a3 = src[(size_t)(q + 3 * kRedParts) * stride];
+            s += a0;
+            s += a1;
+            s += a2;
+            s += a3;
         }
+        for (; q < terms; q += kRedParts)
+            s += src[(size_t)q * stride];
+    }
+    part[pt][col] = s;
+    __syncthreads();
+    if (pt == 0 && e < total) {
+        float t = 0.f;
+#pragma unroll
+        for (int i = 0; i < kRedParts; ++i)
+            t += part[i][col];
+        if (is_w)
+            out[e] = accumulate ? out[e] + t : t;
+        else
+            db[e - count] = accumulate ? db[e - count] + t : t;
     }
 }
 
@@ -124,11 +160,9 @@ hipError_t launch_wgrad_reduce(const float* P, float* out, int count, int splits
     const int total = count + (db ? K : 0);
     if (total == 0)
         return hipSuccess;
-    int blocks = (total + 255) / 256;
-    if (blocks > 4096)
-        blocks = 4096;
-    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks), dim3(256), 0, s, P, out, count, splits,
-                       plane_sums, db, N, K, accumulate);
+    const int blocks = (total + kRedCols - 1) / kRedCols;
+    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks), dim3(kRedParts * kRedCols), 0, s, P, out,
+                       count, splits, plane_sums, db, N, K, accumulate);
     return hipGetLastError();
 }
 

@@ -55,7 +55,8 @@ struct Mfma<16> {
     static __device__ __forceinline__ int row(int q, int lane) { return 4 * (lane >> 4) + q; }
 };
 
-template <int MT, int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH, int SW, int EPI>
+template <int MT, int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH, int SW, int EPI,
+          bool TAP>
 __global__ void __launch_bounds__(64 * WM * WN)
 conv_gemm_f32_kernel(const ConvGemmParams p)
 {
@@ -65,6 +66,7 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     constexpr int TN = WN * NI * MT;
     constexpr int EA = TM * TK / NT;  // A elements per thread per stage
     constexpr int EB = TN * TK / NT;  // B elements per thread per stage
+    constexpr int KS = TK / Op::kStep;
     static_assert(TM * TK % NT == 0 && TN * TK % NT == 0, "tile/thread mismatch");
     static_assert(NT % TK == 0, "A mapping needs TK | NT");
     static_assert(TN % 64 == 0 && (NT % TN == 0 || TN % NT == 0), "B mapping");
@@ -92,6 +94,7 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     const int M = p.M, R = p.R;
     const int IH = p.IH, IW = p.IW, IHW = IH * IW;
     const int OHW = p.OH * p.OW;
+    const int Cin_g = p.Cin_g;
 
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.A, p.A_bytes);
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, p.X_bytes);
@@ -118,17 +121,19 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
             const int j = pix - i * p.OW;
             b_ih0[cc] = i * sh - p.ph;
             b_iw0[cc] = j * sw - p.pw;
-            b_base[cc] = (n * p.Cin + g * p.Cin_g) * IHW + b_ih0[cc] * IW + b_iw0[cc];
+            b_base[cc] = (n * p.Cin + g * Cin_g) * IHW + b_ih0[cc] * IW + b_iw0[cc];
         } else {
             b_ih0[cc] = -(1 << 28);  // fails every bounds check
             b_iw0[cc] = 0;
             b_base[cc] = 0;
         }
     }
+    auto b_row = [&](int q) { return TN > NT ? q / BC : tid / TN + (NT / TN) * q; };
+    auto b_cc = [&](int q) { return TN > NT ? q % BC : 0; };
 
     float rA[EA], rB[EB];
 
-    auto load_stage = [&](int kbase) {
+    auto load_a = [&](int kbase) {
 #pragma unroll
         for (int q = 0; q < EA; ++q) {
             const int r = kbase + a_k;
@@ -136,11 +141,33 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
                 (a_row[q] >= 0 && r < R) ? (uint32_t)(a_row[q] + r) * 4u : kOob;
             rA[q] = buf_ld_f32(ra, off);
         }
+    };
+
+    // Tap-major reduction order r = (u, v, c): Cin_g is a multiple of TK, so a
+    // stage covers TK channels of a single tap (u, v).  The tap's bounds check
+    // and address are computed once per column per stage.
+    auto load_b_tap = [&](int u, int v, int c0) {
+        uint32_t voff[BC];
+#pragma unroll
+        for (int cc = 0; cc < BC; ++cc) {
+            const int ih = b_ih0[cc] + u;
+            const int iw = b_iw0[cc] + v;
+            const bool ok = (unsigned)ih < (unsigned)IH && (unsigned)iw < (unsigned)IW;
+            voff[cc] = ok ? (uint32_t)(b_base[cc] + u * IW + v) * 4u : kOob;
+        }
 #pragma unroll
         for (int q = 0; q < EB; ++q) {
-            const int cc = TN > NT ? q % BC : 0;
-            const int kr = TN > NT ? q / BC : tid / TN + (NT / TN) * q;
-            const int r = __builtin_amdgcn_readfirstlane(kbase + kr);
+            const uint32_t coff = (uint32_t)((c0 + b_row(q)) * IHW) * 4u;
+            rB[q] = buf_ld_f32(rx, voff[b_cc(q)] + coff);
+        }
+    };
+
+    // Channel-major order r = (c, u, v) for any Cin_g.
+    auto load_b_any = [&](int kbase) {
+#pragma unroll
+        for (int q = 0; q < EB; ++q) {
+            const int cc = b_cc(q);
+            const int r = __builtin_amdgcn_readfirstlane(kbase + b_row(q));
             const int c = r / khw;
             const int rr = r - c * khw;
             const int u = rr / kw;
@@ -159,10 +186,8 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
             As[buf][a_k][a_m + (NT / TK) * q] = rA[q];
 #pragma unroll
         for (int q = 0; q < EB; ++q) {
-            const int cc = TN > NT ? q % BC : 0;
-            const int kr = TN > NT ? q / BC : tid / TN + (NT / TN) * q;
-            const int col = TN > NT ? tid + NT * cc : tid % TN;
-            Bs[buf][kr][col] = rB[q];
+            const int col = TN > NT ? tid + NT * b_cc(q) : tid % TN;
+            Bs[buf][b_row(q)][col] = rB[q];
         }
     };
 
@@ -174,7 +199,24 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
             acc[mi][ni] = typename Op::acc_t{};
 
     const int nst = (R + TK - 1) / TK;
-    load_stage(0);
+    // tap-major walk state: stage s covers tap (tu, tv), channels tc .. tc + TK - 1
+    int tu = 0, tv = 0, tc = 0;
+    auto advance = [&]() {
+        tc += TK;
+        if (tc == Cin_g) {
+            tc = 0;
+            if (++tv == kw) {
+                tv = 0;
+                ++tu;
+            }
+        }
+    };
+
+    load_a(0);
+    if constexpr (TAP)
+        load_b_tap(0, 0, 0);
+    else
+        load_b_any(0);
     store_stage(0);
     __syncthreads();
 
@@ -184,59 +226,79 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
 
     for (int s = 0; s < nst; ++s) {
         const int cur = s & 1;
-        if (s + 1 < nst)
-            load_stage((s + 1) * TK);
+        if (s + 1 < nst) {
+            load_a((s + 1) * TK);
+            if constexpr (TAP) {
+                advance();
+                load_b_tap(tu, tv, tc);
+            } else {
+                load_b_any((s + 1) * TK);
+            }
+        }
+        float a[KS][MI], b[KS][NI];
 #pragma unroll
-        for (int kk = 0; kk < TK; kk += Op::kStep) {
-            float a[MI], b[NI];
+        for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
             for (int mi = 0; mi < MI; ++mi)
-                a[mi] = As[cur][kk + kl][arow + mi * MT];
+                a[ks][mi] = As[cur][ks * Op::kStep + kl][arow + mi * MT];
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni)
-                b[ni] = Bs[cur][kk + kl][bcol + ni * MT];
+                b[ks][ni] = Bs[cur][ks * Op::kStep + kl][bcol + ni * MT];
+        }
+        // keep every LDS read of the stage ahead of its MFMAs (the scheduler
+        // would otherwise recycle four fragment registers and wait on LDS before
+        // every k-step)
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
             for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
                 for (int ni = 0; ni < NI; ++ni)
-                    acc[mi][ni] = Op::run(a[mi], b[ni], acc[mi][ni]);
-        }
+                    acc[mi][ni] = Op::run(a[ks][mi], b[ks][ni], acc[mi][ni]);
         if (s + 1 < nst)
             store_stage(cur ^ 1);
         __syncthreads();
     }
 
-    // ---- epilogue
+    // ---- epilogue (branch-free: masked lanes store to an out-of-range offset)
     const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y, p.Y_bytes);
     if constexpr (EPI == 0) {
+        // bias through a buffer resource: a null bias has 0 records and reads 0
+        const __amdgpu_buffer_rsrc_t rbias =
+            make_rsrc(p.bias, p.bias ? (uint32_t)(p.G * M) * 4u : 0u);
+        int cbase[NI];
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni) {
             const int col = n0 + bcol + ni * MT;
-            const bool cok = col < p.Ncol;
-            const int n = cok ? col / OHW : 0;
+            const int n = col / OHW;
             const int pix = col - n * OHW;
-            const int cbase = n * p.Cout * OHW + pix;
+            cbase[ni] = col < p.Ncol ? n * p.Cout * OHW + pix : -1;
+        }
 #pragma unroll
-            for (int mi = 0; mi < MI; ++mi) {
+        for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
-                for (int q = 0; q < Op::kRegs; ++q) {
-                    const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
-                    if (m < M) {
-                        const int oc = g * M + m;
-                        float v = acc[mi][ni][q];
-                        if (p.bias)
-                            v += p.bias[oc];
-                        if (p.relu)
-                            v = v > 0.f ? v : 0.f;
-                        const uint32_t off = cok ? (uint32_t)(cbase + oc * OHW) * 4u : kOob;
-                        buf_st_f32(v, ry, off);
-                    }
+            for (int q = 0; q < Op::kRegs; ++q) {
+                const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
+                const bool mok = m < M;
+                const int oc = g * M + m;
+                const float bv = buf_ld_f32(rbias, mok ? (uint32_t)oc * 4u : kOob);
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni) {
+                    float v = acc[mi][ni][q] + bv;
+                    if (p.relu)
+                        v = fmaxf(v, 0.f);
+                    const uint32_t off = (mok && cbase[ni] >= 0)
+                                             ? (uint32_t)(cbase[ni] + oc * OHW) * 4u
+                                             : kOob;
+                    buf_st_f32(v, ry, off);
                 }
             }
         }
     } else {
         const int pss = p.psh * p.psw;
         const int OutHW = p.OutH * p.OutW;
+        int cb[NI], hb[NI], wb[NI];
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni) {
             const int col = n0 + bcol + ni * MT;
@@ -245,31 +307,62 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
             const int pix = col - n * OHW;
             const int a = pix / p.OW;
             const int b = pix - a * p.OW;
-            const int hb = p.psh * (a + p.a0h) - p.oph;
-            const int wb = p.psw * (b + p.a0w) - p.opw;
-            const int cbase = (n * p.Cout + g * p.Cg_out) * OutHW;
+            hb[ni] = cok ? p.psh * (a + p.a0h) - p.oph : -(1 << 28);
+            wb[ni] = p.psw * (b + p.a0w) - p.opw;
+            cb[ni] = (n * p.Cout + g * p.Cg_out) * OutHW;
+        }
 #pragma unroll
-            for (int mi = 0; mi < MI; ++mi) {
+        for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
-                for (int q = 0; q < Op::kRegs; ++q) {
-                    const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
-                    if (m < M) {
-                        const int c = m / pss;
-                        const int fr = m - c * pss;
-                        const int fh = fr / p.psw;
-                        const int fw = fr - fh * p.psw;
-                        const int h = hb + fh;
-                        const int w = wb + fw;
-                        const bool ok = cok && (unsigned)h < (unsigned)p.OutH &&
-                                        (unsigned)w < (unsigned)p.OutW;
-                        const uint32_t off =
-                            ok ? (uint32_t)(cbase + c * OutHW + h * p.OutW + w) * 4u : kOob;
-                        buf_st_f32(acc[mi][ni][q], ry, off);
-                    }
+            for (int q = 0; q < Op::kRegs; ++q) {
+                const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
+                const bool mok = m < M;
+                int c = m, fh = 0, fw = 0;
+                if (pss != 1) {
+                    c = m / pss;
+                    const int fr = m - c * pss;
+                    fh = fr / p.psw;
+                    fw = fr - fh * p.psw;
+                }
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni) {
+                    const int h = hb[ni] + fh;
+                    const int w = wb[ni] + fw;
+                    const bool ok = mok && (unsigned)h < (unsigned)p.OutH &&
+                                    (unsigned)w < (unsigned)p.OutW;
+                    const uint32_t off =
+                        ok ? (uint32_t)(cb[ni] + c * OutHW + h * p.OutW + w) * 4u : kOob;
+                    buf_st_f32(acc[mi][ni][q], ry, off);
                 }
             }
         }
     }
+}
+
+// Forward weights in tap-major order: Wp[o][(u*kw + v)*Cg + c] = W[o][c][u][v].
+__global__ void __launch_bounds__(256)
+pack_weights_tap_kernel(const float* __restrict__ W, float* __restrict__ Wp, int K, int Cg,
+                        int khw)
+{
+    const int total = K * Cg * khw;
+    const int e = blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= total)
+        return;
+    const int c = e % Cg;
+    const int t = (e / Cg) % khw;
+    const int o = e / (Cg * khw);
+    Wp[e] = W[(o * Cg + c) * khw + t];
+}
+
+hipError_t launch_pack_weights_tap(const float* W, float* Wp, int K, int Cg, int khw,
+                                   hipStream_t s)
+{
+    const int total = K * Cg * khw;
+    if (total == 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(pack_weights_tap_kernel, dim3((total + 255) / 256), dim3(256), 0, s, W, Wp,
+                       K, Cg, khw);
+    return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ launch
@@ -285,43 +378,46 @@ constexpr TileShape kTiles[TILE_COUNT] = {
     {32, 1, 4, 2, 2},  // 64 x 256
 };
 
-template <int MT, int WM, int WN, int MI, int NI, int KH, int KW, int SH, int SW, int EPI>
+template <int MT, int WM, int WN, int MI, int NI, int KH, int KW, int SH, int SW, int EPI, bool TAP>
 hipError_t launch_one(const ConvGemmParams& p, hipStream_t s)
 {
-    constexpr int TK = 16;
     constexpr int TM = WM * MI * MT, TN = WN * NI * MT;
     dim3 grid((p.Ncol + TN - 1) / TN, (p.M + TM - 1) / TM, p.G);
-    hipLaunchKernelGGL((conv_gemm_f32_kernel<MT, WM, WN, MI, NI, TK, KH, KW, SH, SW, EPI>), grid,
-                       dim3(64 * WM * WN), 0, s, p);
+    hipLaunchKernelGGL(
+        (conv_gemm_f32_kernel<MT, WM, WN, MI, NI, kGemmTK, KH, KW, SH, SW, EPI, TAP>), grid,
+        dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();
 }
 
 template <int MT, int WM, int WN, int MI, int NI, int EPI>
-hipError_t launch_geom(const ConvGemmParams& p, hipStream_t s)
+hipError_t launch_geom(const ConvGemmParams& p, bool tap, hipStream_t s)
 {
-    if (p.sh == 1 && p.sw == 1) {
-        if (p.kh == 3 && p.kw == 3)
-            return launch_one<MT, WM, WN, MI, NI, 3, 3, 1, 1, EPI>(p, s);
-        if (p.kh == 5 && p.kw == 5)
-            return launch_one<MT, WM, WN, MI, NI, 5, 5, 1, 1, EPI>(p, s);
+    if (tap) {
+        if (p.sh == 1 && p.sw == 1) {
+            if (p.kh == 3 && p.kw == 3)
+                return launch_one<MT, WM, WN, MI, NI, 3, 3, 1, 1, EPI, true>(p, s);
+            if (p.kh == 5 && p.kw == 5)
+                return launch_one<MT, WM, WN, MI, NI, 5, 5, 1, 1, EPI, true>(p, s);
+        }
+        return launch_one<MT, WM, WN, MI, NI, 0, 0, 0, 0, EPI, true>(p, s);
     }
     if (EPI == 0 && p.kh == 11 && p.kw == 11 && p.sh == 4 && p.sw == 4)
-        return launch_one<MT, WM, WN, MI, NI, 11, 11, 4, 4, EPI>(p, s);
-    return launch_one<MT, WM, WN, MI, NI, 0, 0, 0, 0, EPI>(p, s);
+        return launch_one<MT, WM, WN, MI, NI, 11, 11, 4, 4, EPI, false>(p, s);
+    return launch_one<MT, WM, WN, MI, NI, 0, 0, 0, 0, EPI, false>(p, s);
 }
 
 template <int EPI>
-hipError_t launch_tile(const ConvGemmParams& p, int tile, hipStream_t s)
+hipError_t launch_tile(const ConvGemmParams& p, int tile, bool tap, hipStream_t s)
 {
     switch (tile) {
     case TILE_128x128:
-        return launch_geom<32, 2, 2, 2, 2, EPI>(p, s);
+        return launch_geom<32, 2, 2, 2, 2, EPI>(p, tap, s);
     case TILE_96x256:
-        return launch_geom<32, 1, 4, 3, 2, EPI>(p, s);
+        return launch_geom<32, 1, 4, 3, 2, EPI>(p, tap, s);
     case TILE_48x256:
-        return launch_geom<16, 1, 4, 3, 4, EPI>(p, s);
+        return launch_geom<16, 1, 4, 3, 4, EPI>(p, tap, s);
     case TILE_64x256:
-        return launch_geom<32, 1, 4, 2, 2, EPI>(p, s);
+        return launch_geom<32, 1, 4, 2, 2, EPI>(p, tap, s);
     default:
         return hipErrorInvalidValue;
     }
@@ -341,11 +437,14 @@ int gemm_tile_n(int tile)
     return t.wn * t.ni * t.mt;
 }
 
-hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, hipStream_t s)
+hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool tap_major,
+                                hipStream_t s)
 {
     if (p.Ncol == 0)
         return hipSuccess;
-    return epi == 0 ? launch_tile<0>(p, tile, s) : launch_tile<1>(p, tile, s);
+    if (tap_major && p.Cin_g % kGemmTK != 0)
+        return hipErrorInvalidValue;
+    return epi == 0 ? launch_tile<0>(p, tile, tap_major, s) : launch_tile<1>(p, tile, tap_major, s);
 }
 
 }  // namespace caffe_hip

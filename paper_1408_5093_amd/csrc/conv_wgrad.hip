@@ -69,10 +69,12 @@ conv_wgrad_f32_kernel(const WgradParams p)
 
     // Per-thread A rows (output channels) and B rows (taps), fixed for the kernel.
     int a_off[EA];
+    uint32_t a_bad[EA];
 #pragma unroll
     for (int q = 0; q < EA; ++q) {
         const int m = m0 + rw + RS * q;
-        a_off[q] = m < p.Kg ? (g * p.Kg + m) * OHW : -1;
+        a_off[q] = m < p.Kg ? (g * p.Kg + m) * OHW : 0;
+        a_bad[q] = m < p.Kg ? 0u : kOob;
     }
     int b_off[EB], b_uv[EB];
 #pragma unroll
@@ -93,9 +95,12 @@ conv_wgrad_f32_kernel(const WgradParams p)
 
     float rA[EA], rB[EB];
 
+    // Masked lanes get an offset with bit 31 set: always past num_records, so
+    // the hardware returns 0.  The mask is folded in with integer ops (no
+    // selects on load addresses, which the compiler would turn into branches).
     auto load_stage = [&](int cbase) {
         const int col = cbase + kc;
-        const bool cok = col < col_end;
+        const uint32_t cbad = (uint32_t)(col >= col_end) << 31;
         const int n = (int)fdiv((uint32_t)col, p.div_ohw);
         const int pix = col - n * OHW;
         const int i = (int)fdiv((uint32_t)pix, p.div_ow);
@@ -106,15 +111,16 @@ conv_wgrad_f32_kernel(const WgradParams p)
         const int xbase = (n * p.C + g * p.Cg) * IHW + ih0 * IW + iw0;
 #pragma unroll
         for (int q = 0; q < EA; ++q) {
-            const uint32_t off = (cok && a_off[q] >= 0) ? (uint32_t)(dbase + a_off[q]) * 4u : kOob;
+            const uint32_t off = ((uint32_t)(dbase + a_off[q]) * 4u) | cbad | a_bad[q];
             rA[q] = buf_ld_f32(rd, off);
         }
 #pragma unroll
         for (int q = 0; q < EB; ++q) {
             const int ih = ih0 + (b_uv[q] & 0xffff);
             const int iw = iw0 + (b_uv[q] >> 16);
-            const bool ok = cok && (unsigned)ih < (unsigned)IH && (unsigned)iw < (unsigned)IW;
-            const uint32_t off = ok ? (uint32_t)(xbase + b_off[q]) * 4u : kOob;
+            const uint32_t bad = ((uint32_t)((unsigned)ih >= (unsigned)IH) |
+                                  (uint32_t)((unsigned)iw >= (unsigned)IW)) << 31;
+            const uint32_t off = ((uint32_t)(xbase + b_off[q]) * 4u) | cbad | bad;
             rB[q] = buf_ld_f32(rx, off);
         }
     };
@@ -150,22 +156,26 @@ conv_wgrad_f32_kernel(const WgradParams p)
         const int cur = s & 1;
         if (s + 1 < nst)
             load_stage(col_begin + (s + 1) * TK);
+        constexpr int KS = TK / 2;
+        float a[KS][MI], b[KS][NI];
 #pragma unroll
-        for (int kk = 0; kk < TK; kk += 2) {
-            float a[MI], b[NI];
+        for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
             for (int mi = 0; mi < MI; ++mi)
-                a[mi] = As[cur][kk + kl][arow + mi * MT];
+                a[ks][mi] = As[cur][2 * ks + kl][arow + mi * MT];
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni)
-                b[ni] = Bs[cur][kk + kl][bcol + ni * MT];
+                b[ks][ni] = Bs[cur][2 * ks + kl][bcol + ni * MT];
+        }
+        __builtin_amdgcn_sched_barrier(0);  // all LDS reads of the stage ahead of its MFMAs
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
             for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
                 for (int ni = 0; ni < NI; ++ni)
-                    acc[mi][ni] =
-                        __builtin_amdgcn_mfma_f32_32x32x2f32(a[mi], b[ni], acc[mi][ni], 0, 0, 0);
-        }
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[ks][mi], b[ks][ni],
+                                                                       acc[mi][ni], 0, 0, 0);
         if (s + 1 < nst)
             store_stage(cur ^ 1);
         __syncthreads();

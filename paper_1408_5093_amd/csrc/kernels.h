@@ -65,7 +65,17 @@ enum GemmTile : int {
 int gemm_tile_m(int tile);
 int gemm_tile_n(int tile);
 
-hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, hipStream_t s);
+// Reduction depth of one pipeline stage of conv_gemm.
+constexpr int kGemmTK = 16;
+
+// tap_major: the reduction index runs r = (u, v, c) (A packed to match, see
+// launch_pack_weights_tap); needs Cin_g % kGemmTK == 0.  Otherwise r = (c, u, v).
+hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool tap_major,
+                                hipStream_t s);
+
+// Wp[o][(u*kw + v)*Cg + c] = W[o][c][u][v]  (K rows)
+hipError_t launch_pack_weights_tap(const float* W, float* Wp, int K, int Cg, int khw,
+                                   hipStream_t s);
 
 int wgrad_tile_m();
 int wgrad_tile_n();
@@ -77,10 +87,12 @@ hipError_t launch_conv_wgrad_f32(const WgradParams& p, hipStream_t s);
 hipError_t launch_relu_mask_bias(const float* G, const float* Y, float* D, float* plane_sums,
                                  int planes, int plane_size, int relu, hipStream_t s);
 
-// Wt[g][(c, fh, fw)][(k, th, tw)] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)]
-// (0 where the tap index passes the kernel edge).
+// Wt[g][(c, fh, fw)][r] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)]
+// (0 where the tap index passes the kernel edge), r = (k, th, tw), or
+// r = (th, tw, k) when tap_major.
 hipError_t launch_dgrad_weight_transform(const float* W, float* Wt, int G, int Kg, int Cg, int kh,
-                                         int kw, int sh, int sw, int Th, int Tw, hipStream_t s);
+                                         int kw, int sh, int sw, int Th, int Tw, bool tap_major,
+                                         hipStream_t s);
 
 // out[i] = (accumulate ? out[i] : 0) + sum_{s < splits} P[s*count + i]   (fixed order)
 // and, if db != null, db[k] = (accumulate ? db[k] : 0) + sum_{n < N} plane_sums[n*K + k].

@@ -11,7 +11,7 @@ call; this module only owns buffers and the call order.
 """
 import torch
 
-from . import (CAFFE_BF16, CAFFE_F32, PASS_BACKWARD, Workspace, caffe_conv_backward,
+from . import (CAFFE_BF16, CAFFE_F32, PASS_BACKWARD, PASS_FORWARD, Workspace, caffe_conv_backward,
                caffe_conv_forward, cast_f32_to_bf16, conv_desc, conv_out_shape,
                conv_workspace_size, lrn_backward, lrn_forward, maxpool_backward, maxpool_forward,
                pool_desc, pool_out_shape)
@@ -48,7 +48,8 @@ class ConvStack:
             self.dbottom.append(torch.empty((N, L.C, L.H, L.W), dtype=torch.float32, device=dev))
             self.bottom_op.append(torch.empty((N, L.C, L.H, L.W), dtype=op, device=dev)
                                   if bf16 else None)
-            ws_need = max(ws_need, conv_workspace_size(d, PASS_BACKWARD))
+            ws_need = max(ws_need, conv_workspace_size(d, PASS_BACKWARD),
+                          conv_workspace_size(d, PASS_FORWARD))
             cur = (N, L.K, Ho, Wo)
             stages = []
             for kind, prm in self.glue.get(l, []):
@@ -89,7 +90,7 @@ class ConvStack:
             if self.bf16:
                 src = cast_f32_to_bf16(cur, out=self.bottom_op[l], stream=s)
             self._mark(("fwd", l, "begin"), s)
-            caffe_conv_forward(self.descs[l], src, self.W[l], self.b[l], self.top[l], None, s)
+            caffe_conv_forward(self.descs[l], src, self.W[l], self.b[l], self.top[l], self.ws, s)
             self._mark(("fwd", l, "end"), s)
             cur = self.top[l]
             for st in self.stages[l]:

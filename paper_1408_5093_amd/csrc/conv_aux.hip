@@ -21,7 +21,26 @@ relu_mask_bias_kernel(const float* __restrict__ G, const float* __restrict__ Y,
     for (int pl = wave; pl < planes; pl += nwaves) {
         const size_t base = (size_t)pl * plane_size;
         float s = 0.f;
-        for (int e = lane; e < plane_size; e += 64) {
+        int e = lane;
+        // four independent loads in flight per lane, summed in index order
+        for (; e + 192 < plane_size; e += 256) {
+            float d[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                d[u] = G[base + e + 64 * u];
+            if (relu) {
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    d[u] = Y[base + e + 64 * u] > 0.f ? d[u] : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (D)
+                    D[base + e + 64 * u] = d[u];
+                s += d[u];
+            }
+        }
+        for (; e < plane_size; e += 64) {
             float d = G[base + e];
             if (relu && !(Y[base + e] > 0.f))
                 d = 0.f;

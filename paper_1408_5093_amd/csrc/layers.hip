@@ -10,67 +10,80 @@ namespace caffe_hip {
 // ----------------------------------------------------------------- max pool
 // Window rows i*sh - ph .. + kh - 1 clipped to the image; the first maximum in
 // row-major window order wins; mask holds its index h*W + w within the plane.
-__global__ void __launch_bounds__(256)
-maxpool_forward_kernel(const float* __restrict__ x, float* __restrict__ y,
-                       int32_t* __restrict__ mask, int NC, int H, int W, int OH, int OW, int kh,
-                       int kw, int sh, int sw, int ph, int pw)
+// Grid: x over 256-pixel tiles of a plane, y over planes (n, c); pixel
+// coordinates come from a multiply-shift division.  KS/SS fix the window and
+// stride at compile time (0 = runtime).
+__device__ __forceinline__ int udiv(int x, const FastDiv& f)
 {
-    const int total = NC * OH * OW;  // every tensor holds < 2^31 bytes
-    const int e = blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= total)
-        return;
-    const int j = e % OW;
-    const int t = e / OW;
-    const int i = t % OH;
-    const int nc = t / OH;
-    const float* plane = x + nc * (H * W);
-    int h0 = i * sh - ph, w0 = j * sw - pw;
-    const int h1 = min(h0 + kh, H), w1 = min(w0 + kw, W);
-    h0 = max(h0, 0);
-    w0 = max(w0, 0);
-    int best = h0 * W + w0;
-    float bv = plane[best];
-    for (int h = h0; h < h1; ++h)
-        for (int w = w0; w < w1; ++w) {
-            const float v = plane[h * W + w];
-            if (v > bv) {
-                bv = v;
-                best = h * W + w;
-            }
-        }
-    y[e] = bv;
-    if (mask)
-        mask[e] = best;
+    return (int)(((uint64_t)(uint32_t)x * f.mul) >> f.shift);
 }
 
-// Gather form (one thread per input element, outputs visited in row-major
-// order): deterministic, no atomics.
+template <int KS, int SS>
+__global__ void __launch_bounds__(256)
+maxpool_forward_kernel(const float* __restrict__ x, float* __restrict__ y,
+                       int32_t* __restrict__ mask, int NC, int H, int W, int OH, int OW, int kh_,
+                       int kw_, int sh_, int sw_, int ph, int pw, FastDiv div_ow)
+{
+    const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
+    const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
+    const int OHW = OH * OW;
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    if (p >= OHW)
+        return;
+    const int i = udiv(p, div_ow);
+    const int j = p - i * OW;
+    for (int nc = blockIdx.y; nc < NC; nc += gridDim.y) {
+        const float* plane = x + nc * (H * W);
+        int h0 = i * sh - ph, w0 = j * sw - pw;
+        const int h1 = min(h0 + kh, H), w1 = min(w0 + kw, W);
+        h0 = max(h0, 0);
+        w0 = max(w0, 0);
+        int best = h0 * W + w0;
+        float bv = plane[best];
+        for (int h = h0; h < h1; ++h)
+            for (int w = w0; w < w1; ++w) {
+                const float v = plane[h * W + w];
+                if (v > bv) {
+                    bv = v;
+                    best = h * W + w;
+                }
+            }
+        y[nc * OHW + p] = bv;
+        if (mask)
+            mask[nc * OHW + p] = best;
+    }
+}
+
+// Gather form (one thread per input element, covering outputs visited in
+// row-major order): deterministic, no atomics.
+template <int KS, int SS>
 __global__ void __launch_bounds__(256)
 maxpool_backward_kernel(const float* __restrict__ dy, const int32_t* __restrict__ mask,
-                        float* __restrict__ dx, int NC, int H, int W, int OH, int OW, int kh,
-                        int kw, int sh, int sw, int ph, int pw)
+                        float* __restrict__ dx, int NC, int H, int W, int OH, int OW, int kh_,
+                        int kw_, int sh_, int sw_, int ph, int pw, FastDiv div_w)
 {
-    const int total = NC * H * W;
-    const int e = blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= total)
+    const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
+    const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
+    const int HW = H * W;
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    if (p >= HW)
         return;
-    const int w = e % W;
-    const int t = e / W;
-    const int h = t % H;
-    const int nc = t / H;
+    const int h = udiv(p, div_w);
+    const int w = p - h * W;
     // outputs whose window covers (h, w): i*sh - ph <= h <= i*sh - ph + kh - 1
     const int i0 = max(0, (h + ph - kh + sh) / sh);
     const int i1 = min(OH - 1, (h + ph) / sh);
     const int j0 = max(0, (w + pw - kw + sw) / sw);
     const int j1 = min(OW - 1, (w + pw) / sw);
-    const int self = h * W + w;
-    const int obase = nc * (OH * OW);
-    float s = 0.f;
-    for (int i = i0; i <= i1; ++i)
-        for (int j = j0; j <= j1; ++j)
-            if (mask[obase + i * OW + j] == self)
-                s += dy[obase + i * OW + j];
-    dx[e] = s;
+    for (int nc = blockIdx.y; nc < NC; nc += gridDim.y) {
+        const int obase = nc * (OH * OW);
+        float s = 0.f;
+        for (int i = i0; i <= i1; ++i)
+            for (int j = j0; j <= j1; ++j)
+                if (mask[obase + i * OW + j] == p)
+                    s += dy[obase + i * OW + j];
+        dx[nc * HW + p] = s;
+    }
 }
 
 static unsigned grid_for(long total)
@@ -81,15 +94,28 @@ static unsigned grid_for(long total)
 
 static unsigned grid_exact(long total) { return (unsigned)((total + 255) / 256); }
 
+static dim3 plane_grid(int pixels, int planes)
+{
+    return dim3((unsigned)((pixels + 255) / 256), (unsigned)(planes < 65535 ? planes : 65535));
+}
+
 hipError_t launch_maxpool_forward(const float* x, float* y, int32_t* mask, int NC, int H, int W,
                                   int OH, int OW, int kh, int kw, int sh, int sw, int ph, int pw,
                                   hipStream_t s)
 {
-    const long total = (long)NC * OH * OW;
-    if (total == 0)
+    if ((long)NC * OH * OW == 0)
         return hipSuccess;
-    hipLaunchKernelGGL(maxpool_forward_kernel, dim3(grid_exact(total)), dim3(256), 0, s, x, y, mask,
-                       NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw);
+    const FastDiv d = make_fastdiv((uint32_t)OW);
+    const dim3 grid = plane_grid(OH * OW, NC);
+    if (kh == 3 && kw == 3 && sh == 2 && sw == 2)
+        hipLaunchKernelGGL((maxpool_forward_kernel<3, 2>), grid, dim3(256), 0, s, x, y, mask, NC,
+                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d);
+    else if (kh == 2 && kw == 2 && sh == 2 && sw == 2)
+        hipLaunchKernelGGL((maxpool_forward_kernel<2, 2>), grid, dim3(256), 0, s, x, y, mask, NC,
+                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d);
+    else
+        hipLaunchKernelGGL((maxpool_forward_kernel<0, 0>), grid, dim3(256), 0, s, x, y, mask, NC,
+                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d);
     return hipGetLastError();
 }
 
@@ -97,11 +123,19 @@ hipError_t launch_maxpool_backward(const float* dy, const int32_t* mask, float* 
                                    int W, int OH, int OW, int kh, int kw, int sh, int sw, int ph,
                                    int pw, hipStream_t s)
 {
-    const long total = (long)NC * H * W;
-    if (total == 0)
+    if ((long)NC * H * W == 0)
         return hipSuccess;
-    hipLaunchKernelGGL(maxpool_backward_kernel, dim3(grid_exact(total)), dim3(256), 0, s, dy, mask,
-                       dx, NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw);
+    const FastDiv d = make_fastdiv((uint32_t)W);
+    const dim3 grid = plane_grid(H * W, NC);
+    if (kh == 3 && kw == 3 && sh == 2 && sw == 2)
+        hipLaunchKernelGGL((maxpool_backward_kernel<3, 2>), grid, dim3(256), 0, s, dy, mask, dx,
+                           NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, d);
+    else if (kh == 2 && kw == 2 && sh == 2 && sw == 2)
+        hipLaunchKernelGGL((maxpool_backward_kernel<2, 2>), grid, dim3(256), 0, s, dy, mask, dx,
+                           NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, d);
+    else
+        hipLaunchKernelGGL((maxpool_backward_kernel<0, 0>), grid, dim3(256), 0, s, dy, mask, dx,
+                           NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, d);
     return hipGetLastError();
 }
 
@@ -113,110 +147,106 @@ hipError_t launch_maxpool_backward(const float* dy, const int32_t* mask, float* 
 // pixels, so every load is coalesced and every input is read once.  The
 // window's squares live in a register ring of SIZE entries and each sum is
 // re-added from the ring (no running add/subtract, so no drift).
-template <int SIZE>
-__global__ void __launch_bounds__(256)
-lrn_forward_kernel(const float* __restrict__ x, float* __restrict__ y, int N, int C, int HW,
-                   float alpha_over_n, float beta, float k)
+__device__ __forceinline__ float pow_neg(float s, float beta)
 {
-    constexpr int PRE = (SIZE - 1) / 2;
-    constexpr int POST = SIZE - 1 - PRE;
-    const int e = blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= N * HW)
-        return;
-    const int n = e / HW;
-    const int pix = e - n * HW;
-    const float* col = x + n * C * HW + pix;
-    float* out = y + n * C * HW + pix;
-    float a[SIZE];  // a[q] = value of channel c - PRE + q (0 outside)
-#pragma unroll
-    for (int q = 0; q < SIZE; ++q) {
-        const int ch = q - PRE;
-        a[q] = (ch >= 0 && ch < C) ? col[ch * HW] : 0.f;
-    }
-    for (int c = 0; c < C; ++c) {
-        float sq = 0.f;
-#pragma unroll
-        for (int q = 0; q < SIZE; ++q)
-            sq += a[q] * a[q];
-        const float s = k + alpha_over_n * sq;
-        out[c * HW] = a[PRE] * powf(s, -beta);
-#pragma unroll
-        for (int q = 0; q + 1 < SIZE; ++q)
-            a[q] = a[q + 1];
-        const int nxt = c + 1 + POST;
-        a[SIZE - 1] = nxt < C ? col[nxt * HW] : 0.f;
-    }
+    // s^-beta for s >= k > 0 via the hardware exp2/log2 (about 1 ulp each)
+    return __builtin_amdgcn_exp2f(-beta * __builtin_amdgcn_logf(s));
 }
 
-// dx_c = g_c s_c^-beta - (2 alpha beta / size) a_c sum_{c': c in win(c')} g_c' b_c' / s_c'
-// c in win(c') <=> c' in [c - POST, c + PRE].  Step j computes s_j and the
-// ratio r_j = g_j b_j / s_j, then emits dx for c = j - PRE.
-template <int SIZE>
+// One thread per (n, chunk of CH channels, pixel); lanes run along pixels.
+// Every input of the chunk and its halo is loaded up front (independent
+// loads), then the outputs are formed from registers.
+template <int SIZE, int CH>
 __global__ void __launch_bounds__(256)
-lrn_backward_kernel(const float* __restrict__ x, const float* __restrict__ y,
-                    const float* __restrict__ dy, float* __restrict__ dx, int N, int C, int HW,
-                    float alpha_over_n, float beta, float k)
+lrn_forward_kernel(const float* __restrict__ x, float* __restrict__ y, int N, int C, int HW,
+                   int nchunks, FastDiv div_hw, float alpha_over_n, float beta, float k)
 {
     constexpr int PRE = (SIZE - 1) / 2;
     constexpr int POST = SIZE - 1 - PRE;
+    constexpr int NA = CH + SIZE - 1;
     const int e = blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= N * HW)
+    if (e >= N * nchunks * HW)
         return;
-    const int n = e / HW;
-    const int pix = e - n * HW;
-    const int base = n * C * HW + pix;
-    float a[SIZE];          // inputs of channels j - PRE .. j + POST
-    float r[SIZE];          // ratios of channels j - SIZE + 1 .. j
-    float sc[PRE + 1];      // s of channels j - PRE .. j
-    float ac[PRE + 1];      // inputs of channels j - PRE .. j
-    float gc[PRE + 1];      // gradients of channels j - PRE .. j
+    const int rest = udiv(e, div_hw);
+    const int pix = e - rest * HW;
+    const int n = rest / nchunks;
+    const int c0 = (rest - n * nchunks) * CH;
+    const float* col = x + n * C * HW + pix;
+    float a[NA];  // channels c0 - PRE .. c0 + CH - 1 + POST
 #pragma unroll
-    for (int q = 0; q < SIZE; ++q) {
-        const int ch = q - PRE;
-        a[q] = (ch >= 0 && ch < C) ? x[base + ch * HW] : 0.f;
-        r[q] = 0.f;
+    for (int q = 0; q < NA; ++q) {
+        const int ch = c0 - PRE + q;
+        a[q] = (ch >= 0 && ch < C) ? col[ch * HW] : 0.f;
     }
 #pragma unroll
-    for (int q = 0; q <= PRE; ++q)
-        sc[q] = ac[q] = gc[q] = 0.f;
-    const float coef = 2.f * alpha_over_n * beta;
-    for (int j = 0; j < C + PRE; ++j) {
-        float s = 1.f, g = 0.f, rj = 0.f;
-        if (j < C) {
+    for (int t = 0; t < CH; ++t) {
+        const int c = c0 + t;
+        if (c < C) {
             float sq = 0.f;
 #pragma unroll
             for (int q = 0; q < SIZE; ++q)
-                sq += a[q] * a[q];
-            s = k + alpha_over_n * sq;
-            g = dy[base + j * HW];
-            rj = g * y[base + j * HW] / s;
+                sq += a[t + q] * a[t + q];
+            y[n * C * HW + c * HW + pix] = a[t + PRE] * pow_neg(k + alpha_over_n * sq, beta);
         }
+    }
+}
+
+// dx_c = g_c s_c^-beta - (2 alpha beta / size) a_c sum_{c' in [c - POST, c + PRE]} g_c' b_c' / s_c'
+template <int SIZE, int CH>
+__global__ void __launch_bounds__(256)
+lrn_backward_kernel(const float* __restrict__ x, const float* __restrict__ y,
+                    const float* __restrict__ dy, float* __restrict__ dx, int N, int C, int HW,
+                    int nchunks, FastDiv div_hw, float alpha_over_n, float beta, float k)
+{
+    constexpr int PRE = (SIZE - 1) / 2;
+    constexpr int POST = SIZE - 1 - PRE;
+    constexpr int NR = CH + SIZE - 1;      // ratios: channels c0 - POST .. c0 + CH - 1 + PRE
+    constexpr int NA = NR + SIZE - 1;      // inputs: channels c0 - POST - PRE .. + NA - 1
+    const int e = blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= N * nchunks * HW)
+        return;
+    const int rest = udiv(e, div_hw);
+    const int pix = e - rest * HW;
+    const int n = rest / nchunks;
+    const int c0 = (rest - n * nchunks) * CH;
+    const int base = n * C * HW + pix;
+    float a[NA], g[NR], b[NR];
 #pragma unroll
-        for (int q = 0; q + 1 < SIZE; ++q)
-            r[q] = r[q + 1];
-        r[SIZE - 1] = rj;
+    for (int q = 0; q < NA; ++q) {
+        const int ch = c0 - POST - PRE + q;
+        a[q] = (ch >= 0 && ch < C) ? x[base + ch * HW] : 0.f;
+    }
 #pragma unroll
-        for (int q = 0; q < PRE; ++q) {
-            sc[q] = sc[q + 1];
-            ac[q] = ac[q + 1];
-            gc[q] = gc[q + 1];
-        }
-        sc[PRE] = s;
-        ac[PRE] = a[PRE];
-        gc[PRE] = g;
-        const int c = j - PRE;
-        if (c >= 0) {
-            float cross = 0.f;  // r of channels c - POST .. c + PRE = j - SIZE + 1 .. j
+    for (int q = 0; q < NR; ++q) {
+        const int ch = c0 - POST + q;
+        const bool in = ch >= 0 && ch < C;
+        g[q] = in ? dy[base + ch * HW] : 0.f;
+        b[q] = in ? y[base + ch * HW] : 0.f;
+    }
+    float r[NR], sc[CH];
+#pragma unroll
+    for (int q = 0; q < NR; ++q) {
+        float sq = 0.f;
+#pragma unroll
+        for (int t = 0; t < SIZE; ++t)
+            sq += a[q + t] * a[q + t];
+        const float s = k + alpha_over_n * sq;
+        r[q] = g[q] * b[q] / s;
+        if (q >= POST && q < POST + CH)
+            sc[q - POST] = s;
+    }
+    const float coef = 2.f * alpha_over_n * beta;
+#pragma unroll
+    for (int t = 0; t < CH; ++t) {
+        const int c = c0 + t;
+        if (c < C) {
+            float cross = 0.f;
 #pragma unroll
             for (int q = 0; q < SIZE; ++q)
-                cross += r[q];
-            dx[base + c * HW] = gc[0] * powf(sc[0], -beta) - coef * ac[0] * cross;
+                cross += r[t + q];
+            dx[base + c * HW] =
+                g[t + POST] * pow_neg(sc[t], beta) - coef * a[t + POST + PRE] * cross;
         }
-#pragma unroll
-        for (int q = 0; q + 1 < SIZE; ++q)
-            a[q] = a[q + 1];
-        const int nxt = j + 1 + POST;
-        a[SIZE - 1] = nxt < C ? x[base + nxt * HW] : 0.f;
     }
 }
 
@@ -274,22 +304,26 @@ lrn_backward_any_kernel(const float* __restrict__ x, const float* __restrict__ y
     dx[e] = dy[e] * powf(s_c, -beta) - 2.f * alpha_over_n * beta * col[c * HW] * cross;
 }
 
+constexpr int kLrnChunk = 16;
+
 hipError_t launch_lrn_forward(const float* x, float* y, int N, int C, int HW, int size,
                               float alpha, float beta, float k, hipStream_t s)
 {
-    const long cols = (long)N * HW;
-    if (cols == 0)
+    if ((long)N * C * HW == 0)
         return hipSuccess;
     const float an = alpha / size;
+    const int nch = (C + kLrnChunk - 1) / kLrnChunk;
+    const long threads = (long)N * nch * HW;
+    const FastDiv d = make_fastdiv((uint32_t)HW);
     if (size == 5)
-        hipLaunchKernelGGL(lrn_forward_kernel<5>, dim3(grid_exact(cols)), dim3(256), 0, s, x, y,
-                           N, C, HW, an, beta, k);
+        hipLaunchKernelGGL((lrn_forward_kernel<5, kLrnChunk>), dim3(grid_exact(threads)),
+                           dim3(256), 0, s, x, y, N, C, HW, nch, d, an, beta, k);
     else if (size == 3)
-        hipLaunchKernelGGL(lrn_forward_kernel<3>, dim3(grid_exact(cols)), dim3(256), 0, s, x, y,
-                           N, C, HW, an, beta, k);
+        hipLaunchKernelGGL((lrn_forward_kernel<3, kLrnChunk>), dim3(grid_exact(threads)),
+                           dim3(256), 0, s, x, y, N, C, HW, nch, d, an, beta, k);
     else
-        hipLaunchKernelGGL(lrn_forward_any_kernel, dim3(grid_exact(cols * C)), dim3(256), 0, s, x,
-                           y, N, C, HW, size, an, beta, k);
+        hipLaunchKernelGGL(lrn_forward_any_kernel, dim3(grid_exact((long)N * C * HW)), dim3(256),
+                           0, s, x, y, N, C, HW, size, an, beta, k);
     return hipGetLastError();
 }
 
@@ -297,19 +331,21 @@ hipError_t launch_lrn_backward(const float* x, const float* y, const float* dy, 
                                int C, int HW, int size, float alpha, float beta, float k,
                                hipStream_t s)
 {
-    const long cols = (long)N * HW;
-    if (cols == 0)
+    if ((long)N * C * HW == 0)
         return hipSuccess;
     const float an = alpha / size;
+    const int nch = (C + kLrnChunk - 1) / kLrnChunk;
+    const long threads = (long)N * nch * HW;
+    const FastDiv d = make_fastdiv((uint32_t)HW);
     if (size == 5)
-        hipLaunchKernelGGL(lrn_backward_kernel<5>, dim3(grid_exact(cols)), dim3(256), 0, s, x, y,
-                           dy, dx, N, C, HW, an, beta, k);
+        hipLaunchKernelGGL((lrn_backward_kernel<5, kLrnChunk>), dim3(grid_exact(threads)),
+                           dim3(256), 0, s, x, y, dy, dx, N, C, HW, nch, d, an, beta, k);
     else if (size == 3)
-        hipLaunchKernelGGL(lrn_backward_kernel<3>, dim3(grid_exact(cols)), dim3(256), 0, s, x, y,
-                           dy, dx, N, C, HW, an, beta, k);
+        hipLaunchKernelGGL((lrn_backward_kernel<3, kLrnChunk>), dim3(grid_exact(threads)),
+                           dim3(256), 0, s, x, y, dy, dx, N, C, HW, nch, d, an, beta, k);
     else
-        hipLaunchKernelGGL(lrn_backward_any_kernel, dim3(grid_exact(cols * C)), dim3(256), 0, s,
-                           x, y, dy, dx, N, C, HW, size, an, beta, k);
+        hipLaunchKernelGGL(lrn_backward_any_kernel, dim3(grid_exact((long)N * C * HW)),
+                           dim3(256), 0, s, x, y, dy, dx, N, C, HW, size, an, beta, k);
     return hipGetLastError();
 }
 

@@ -5,6 +5,7 @@
 
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -53,11 +54,42 @@ struct ConvPlan {
     int splits, cols_per_split;
     // reduction order of the implicit GEMMs: tap-major r = (u, v, c) when the
     // gathered channels per group fill whole pipeline stages
+    int fwd_tile, dgrad_tile;
     bool fwd_tap, dgrad_tap;
     // workspace layout (byte offsets), per pass
     size_t off_d, off_sums, off_wt, off_part;
     size_t ws_fwd, ws_data, ws_weights, ws_both;
 };
+
+// Tile for a GEMM with M rows whose gather walks `cin_g` channels per group:
+// the least padding of M, then the larger tile; tap-major needs cin_g to be a
+// multiple of the stage depth.  `forced` >= 0 picks a tile (profiling only).
+int pick_tile(int M, int cin_g, int forced)
+{
+    if (forced >= 0 && forced < TILE_COUNT)
+        return forced;
+    static const int candidates[] = {TILE_128x128, TILE_96x256, TILE_48x256, TILE_64x256};
+    int best = TILE_128x128;
+    double best_waste = 1e30;
+    for (int t : candidates) {
+        const int tm = gemm_tile_m(t);
+        const double waste = (double)((M + tm - 1) / tm * tm) / M;
+        if (waste < best_waste - 1e-9 ||
+            (waste < best_waste + 1e-9 && tm > gemm_tile_m(best))) {
+            best = t;
+            best_waste = waste;
+        }
+    }
+    (void)cin_g;
+    return best;
+}
+
+// Profiling override of the tile choice: an integer GemmTile, read once.
+int env_tile(const char* name)
+{
+    const char* v = getenv(name);
+    return v && *v ? atoi(v) : -1;
+}
 
 int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
 {
@@ -139,8 +171,10 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     if (part_bytes > kMaxTensorBytes)
         return fail(CAFFE_ERR_UNSUPPORTED, "weight-gradient partials reach 2^31 bytes");
 
-    q.fwd_tap = q.Cg % kGemmTK == 0;
-    q.dgrad_tap = q.Kg % kGemmTK == 0;
+    q.fwd_tile = pick_tile(q.Kg, q.Cg, env_tile("CAFFE_CONV_FWD_TILE"));
+    q.dgrad_tile = pick_tile(q.Mt, q.Kg, env_tile("CAFFE_CONV_DGRAD_TILE"));
+    q.fwd_tap = q.Cg % gemm_tile_k(q.fwd_tile) == 0;
+    q.dgrad_tap = q.Kg % gemm_tile_k(q.dgrad_tile) == 0;
     q.ws_fwd = q.fwd_tap ? align_up(q.weight_elems * 4, kWsAlign) : 0;
 
     // Workspace: [masked diff][plane sums][transformed weights][partials]
@@ -197,23 +231,6 @@ int check_ws(const void* ws, size_t ws_bytes, size_t need)
             return hip_fail(_e, what);                                                            \
     } while (0)
 
-int pick_tile(int M)
-{
-    // least padding of M, then the larger tile
-    int best = TILE_128x128;
-    double best_waste = 1e30;
-    for (int t = 0; t < TILE_COUNT; ++t) {
-        const int tm = gemm_tile_m(t);
-        const double waste = (double)((M + tm - 1) / tm * tm) / M;
-        if (waste < best_waste - 1e-9 ||
-            (waste < best_waste + 1e-9 && tm > gemm_tile_m(best))) {
-            best = t;
-            best_waste = waste;
-        }
-    }
-    return best;
-}
-
 uint32_t nbytes(int64_t elems, int64_t esize) { return (uint32_t)(elems * esize); }
 
 int run_forward(const ConvPlan& q, const void* bottom, const void* weight, const float* bias,
@@ -243,7 +260,7 @@ int run_forward(const ConvPlan& q, const void* bottom, const void* weight, const
     p.Ncol = q.N * q.Ho * q.Wo;
     p.relu = q.relu;
     p.Cout = q.K; p.OutH = q.Ho; p.OutW = q.Wo;
-    LAUNCH(launch_conv_gemm_f32(p, 0, pick_tile(p.M), q.fwd_tap, s), "forward launch");
+    LAUNCH(launch_conv_gemm_f32(p, 0, q.fwd_tile, q.fwd_tap, s), "forward launch");
     return CAFFE_OK;
 }
 
@@ -288,7 +305,7 @@ int run_data(const ConvPlan& q, const float* dsrc, const void* weight, float* bo
     p.Cout = q.C; p.OutH = q.H; p.OutW = q.W;
     p.psh = q.sh; p.psw = q.sw; p.a0h = q.a0h; p.a0w = q.a0w; p.oph = q.ph; p.opw = q.pw;
     p.Cg_out = q.Cg;
-    LAUNCH(launch_conv_gemm_f32(p, 1, pick_tile(p.M), q.dgrad_tap, s), "data-gradient launch");
+    LAUNCH(launch_conv_gemm_f32(p, 1, q.dgrad_tile, q.dgrad_tap, s), "data-gradient launch");
     return CAFFE_OK;
 }
 

@@ -72,10 +72,14 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     static_assert(TN % 64 == 0 && (NT % TN == 0 || TN % NT == 0), "B mapping");
     static_assert(TK % Op::kStep == 0, "stage depth");
     constexpr int BC = TN > NT ? TN / NT : 1;  // distinct B columns per thread
+    // Row strides: A rows are written with lanes along k, so a stride of
+    // 2 (mod 32) keeps those writes conflict-free.  The 16x16x4 fragments read
+    // four k rows at once, so B rows then get a stride of 16 (mod 32).
     constexpr int PADA = 2;
+    constexpr int PADB = MT == 16 ? 16 : 0;
 
     __shared__ float As[2][TK][TM + PADA];
-    __shared__ float Bs[2][TK][TN];
+    __shared__ float Bs[2][TK][TN + PADB];
 
     const int kh = KH ? KH : p.kh;
     const int kw = KW ? KW : p.kw;
@@ -369,41 +373,44 @@ hipError_t launch_pack_weights_tap(const float* W, float* Wp, int K, int Cg, int
 namespace {
 
 struct TileShape {
-    int mt, wm, wn, mi, ni;
+    int mt, wm, wn, mi, ni, tk;
 };
 constexpr TileShape kTiles[TILE_COUNT] = {
-    {32, 2, 2, 2, 2},  // 128 x 128
-    {32, 1, 4, 3, 2},  // 96 x 256
-    {16, 1, 4, 3, 4},  // 48 x 256
-    {32, 1, 4, 2, 2},  // 64 x 256
+    {32, 2, 2, 2, 2, 16},  // 128 x 128
+    {32, 1, 4, 3, 2, 16},  // 96 x 256
+    {16, 1, 4, 3, 4, 16},  // 48 x 256
+    {32, 1, 4, 2, 2, 16},  // 64 x 256
+    {32, 2, 2, 2, 4, 16},  // 128 x 256
+    {32, 2, 2, 4, 2, 16},  // 256 x 128
+    {32, 2, 2, 2, 2, 32},  // 128 x 128, 32-deep stages
 };
 
-template <int MT, int WM, int WN, int MI, int NI, int KH, int KW, int SH, int SW, int EPI, bool TAP>
+template <int MT, int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH, int SW, int EPI,
+          bool TAP>
 hipError_t launch_one(const ConvGemmParams& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * MT, TN = WN * NI * MT;
     dim3 grid((p.Ncol + TN - 1) / TN, (p.M + TM - 1) / TM, p.G);
-    hipLaunchKernelGGL(
-        (conv_gemm_f32_kernel<MT, WM, WN, MI, NI, kGemmTK, KH, KW, SH, SW, EPI, TAP>), grid,
-        dim3(64 * WM * WN), 0, s, p);
+    hipLaunchKernelGGL((conv_gemm_f32_kernel<MT, WM, WN, MI, NI, TK, KH, KW, SH, SW, EPI, TAP>),
+                       grid, dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();
 }
 
-template <int MT, int WM, int WN, int MI, int NI, int EPI>
+template <int MT, int WM, int WN, int MI, int NI, int TK, int EPI>
 hipError_t launch_geom(const ConvGemmParams& p, bool tap, hipStream_t s)
 {
     if (tap) {
         if (p.sh == 1 && p.sw == 1) {
             if (p.kh == 3 && p.kw == 3)
-                return launch_one<MT, WM, WN, MI, NI, 3, 3, 1, 1, EPI, true>(p, s);
+                return launch_one<MT, WM, WN, MI, NI, TK, 3, 3, 1, 1, EPI, true>(p, s);
             if (p.kh == 5 && p.kw == 5)
-                return launch_one<MT, WM, WN, MI, NI, 5, 5, 1, 1, EPI, true>(p, s);
+                return launch_one<MT, WM, WN, MI, NI, TK, 5, 5, 1, 1, EPI, true>(p, s);
         }
-        return launch_one<MT, WM, WN, MI, NI, 0, 0, 0, 0, EPI, true>(p, s);
+        return launch_one<MT, WM, WN, MI, NI, TK, 0, 0, 0, 0, EPI, true>(p, s);
     }
     if (EPI == 0 && p.kh == 11 && p.kw == 11 && p.sh == 4 && p.sw == 4)
-        return launch_one<MT, WM, WN, MI, NI, 11, 11, 4, 4, EPI, false>(p, s);
-    return launch_one<MT, WM, WN, MI, NI, 0, 0, 0, 0, EPI, false>(p, s);
+        return launch_one<MT, WM, WN, MI, NI, TK, 11, 11, 4, 4, EPI, false>(p, s);
+    return launch_one<MT, WM, WN, MI, NI, TK, 0, 0, 0, 0, EPI, false>(p, s);
 }
 
 template <int EPI>
@@ -411,13 +418,19 @@ hipError_t launch_tile(const ConvGemmParams& p, int tile, bool tap, hipStream_t 
 {
     switch (tile) {
     case TILE_128x128:
-        return launch_geom<32, 2, 2, 2, 2, EPI>(p, tap, s);
+        return launch_geom<32, 2, 2, 2, 2, 16, EPI>(p, tap, s);
     case TILE_96x256:
-        return launch_geom<32, 1, 4, 3, 2, EPI>(p, tap, s);
+        return launch_geom<32, 1, 4, 3, 2, 16, EPI>(p, tap, s);
     case TILE_48x256:
-        return launch_geom<16, 1, 4, 3, 4, EPI>(p, tap, s);
+        return launch_geom<16, 1, 4, 3, 4, 16, EPI>(p, tap, s);
     case TILE_64x256:
-        return launch_geom<32, 1, 4, 2, 2, EPI>(p, tap, s);
+        return launch_geom<32, 1, 4, 2, 2, 16, EPI>(p, tap, s);
+    case TILE_128x256:
+        return launch_geom<32, 2, 2, 2, 4, 16, EPI>(p, tap, s);
+    case TILE_256x128:
+        return launch_geom<32, 2, 2, 4, 2, 16, EPI>(p, tap, s);
+    case TILE_128x128_K32:
+        return launch_geom<32, 2, 2, 2, 2, 32, EPI>(p, tap, s);
     default:
         return hipErrorInvalidValue;
     }
@@ -437,12 +450,14 @@ int gemm_tile_n(int tile)
     return t.wn * t.ni * t.mt;
 }
 
+int gemm_tile_k(int tile) { return kTiles[tile].tk; }
+
 hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool tap_major,
                                 hipStream_t s)
 {
     if (p.Ncol == 0)
         return hipSuccess;
-    if (tap_major && p.Cin_g % kGemmTK != 0)
+    if (tile < 0 || tile >= TILE_COUNT || (tap_major && p.Cin_g % kTiles[tile].tk != 0))
         return hipErrorInvalidValue;
     return epi == 0 ? launch_tile<0>(p, tile, tap_major, s) : launch_tile<1>(p, tile, tap_major, s);
 }

@@ -56,20 +56,26 @@ struct WgradParams {
 
 // Tile shapes a launcher may pick; see conv_gemm.hip.
 enum GemmTile : int {
-    TILE_128x128 = 0,  // 32x32x2 MFMA, 4 waves as 2x2, each 64x64
-    TILE_96x256 = 1,   // 32x32x2 MFMA, 4 waves as 1x4, each 96x64
-    TILE_48x256 = 2,   // 16x16x4 MFMA, 4 waves as 1x4, each 48x64
-    TILE_64x256 = 3,   // 32x32x2 MFMA, 4 waves as 1x4, each 64x64
+    TILE_128x128 = 0,      // 32x32x2 MFMA, 4 waves as 2x2, each 64x64, 16-deep stages
+    TILE_96x256 = 1,       // 32x32x2 MFMA, 4 waves as 1x4, each 96x64
+    TILE_48x256 = 2,       // 16x16x4 MFMA, 4 waves as 1x4, each 48x64
+    TILE_64x256 = 3,       // 32x32x2 MFMA, 4 waves as 1x4, each 64x64
+    TILE_128x256 = 4,      // 32x32x2 MFMA, 4 waves as 2x2, each 64x128
+    TILE_256x128 = 5,      // 32x32x2 MFMA, 4 waves as 2x2, each 128x64
+    TILE_128x128_K32 = 6,  // as TILE_128x128 with 32-deep stages
     TILE_COUNT
 };
 int gemm_tile_m(int tile);
 int gemm_tile_n(int tile);
+int gemm_tile_k(int tile);  // reduction depth of one pipeline stage
 
-// Reduction depth of one pipeline stage of conv_gemm.
-constexpr int kGemmTK = 16;
+// Smallest stage depth of any tile: channel counts divisible by it can use
+// the tap-major order with some tile.
+constexpr int kGemmMinTK = 16;
 
 // tap_major: the reduction index runs r = (u, v, c) (A packed to match, see
-// launch_pack_weights_tap); needs Cin_g % kGemmTK == 0.  Otherwise r = (c, u, v).
+// launch_pack_weights_tap); needs Cin_g % gemm_tile_k(tile) == 0.  Otherwise
+// r = (c, u, v).
 hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool tap_major,
                                 hipStream_t s);
 

@@ -32,22 +32,43 @@ maxpool_forward_kernel(const float* __restrict__ x, float* __restrict__ y,
         return;
     const int i = udiv(p, div_ow);
     const int j = p - i * OW;
+    const int hs = i * sh - ph, ws = j * sw - pw;
+    const int h0 = max(hs, 0), w0 = max(ws, 0);
     for (int nc = blockIdx.y; nc < NC; nc += gridDim.y) {
         const float* plane = x + nc * (H * W);
-        int h0 = i * sh - ph, w0 = j * sw - pw;
-        const int h1 = min(h0 + kh, H), w1 = min(w0 + kw, W);
-        h0 = max(h0, 0);
-        w0 = max(w0, 0);
         int best = h0 * W + w0;
         float bv = plane[best];
-        for (int h = h0; h < h1; ++h)
-            for (int w = w0; w < w1; ++w) {
-                const float v = plane[h * W + w];
-                if (v > bv) {
-                    bv = v;
-                    best = h * W + w;
+        if constexpr (KS > 0) {
+            // fixed window: every load is independent; out-of-image taps are
+            // skipped by the predicate (strict '>' keeps the first maximum)
+            float v[KS][KS];
+#pragma unroll
+            for (int du = 0; du < KS; ++du)
+#pragma unroll
+                for (int dv = 0; dv < KS; ++dv) {
+                    const int h = hs + du, w = ws + dv;
+                    const bool in = (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+                    v[du][dv] = in ? plane[h * W + w] : bv;
                 }
-            }
+#pragma unroll
+            for (int du = 0; du < KS; ++du)
+#pragma unroll
+                for (int dv = 0; dv < KS; ++dv)
+                    if (v[du][dv] > bv) {
+                        bv = v[du][dv];
+                        best = (hs + du) * W + ws + dv;
+                    }
+        } else {
+            const int h1 = min(hs + kh, H), w1 = min(ws + kw, W);
+            for (int h = h0; h < h1; ++h)
+                for (int w = w0; w < w1; ++w) {
+                    const float v = plane[h * W + w];
+                    if (v > bv) {
+                        bv = v;
+                        best = h * W + w;
+                    }
+                }
+        }
         y[nc * OHW + p] = bv;
         if (mask)
             mask[nc * OHW + p] = best;
@@ -55,7 +76,10 @@ maxpool_forward_kernel(const float* __restrict__ x, float* __restrict__ y,
 }
 
 // Gather form (one thread per input element, covering outputs visited in
-// row-major order): deterministic, no atomics.
+// row-major order): deterministic, no atomics.  With a fixed window, at most
+// ceil(KS/SS)^2 outputs cover an input; their masks and gradients are loaded
+// unconditionally (clamped indices), then added in order where the mask
+// names this input.
 template <int KS, int SS>
 __global__ void __launch_bounds__(256)
 maxpool_backward_kernel(const float* __restrict__ dy, const int32_t* __restrict__ mask,
@@ -78,10 +102,30 @@ maxpool_backward_kernel(const float* __restrict__ dy, const int32_t* __restrict_
     for (int nc = blockIdx.y; nc < NC; nc += gridDim.y) {
         const int obase = nc * (OH * OW);
         float s = 0.f;
-        for (int i = i0; i <= i1; ++i)
-            for (int j = j0; j <= j1; ++j)
-                if (mask[obase + i * OW + j] == p)
-                    s += dy[obase + i * OW + j];
+        if constexpr (KS > 0) {
+            constexpr int T = (KS + SS - 1) / SS;
+            int mk[T][T];
+            float g[T][T];
+#pragma unroll
+            for (int di = 0; di < T; ++di)
+#pragma unroll
+                for (int dj = 0; dj < T; ++dj) {
+                    const int o = obase + min(i0 + di, OH - 1) * OW + min(j0 + dj, OW - 1);
+                    mk[di][dj] = mask[o];
+                    g[di][dj] = dy[o];
+                }
+#pragma unroll
+            for (int di = 0; di < T; ++di)
+#pragma unroll
+                for (int dj = 0; dj < T; ++dj)
+                    if (i0 + di <= i1 && j0 + dj <= j1 && mk[di][dj] == p)
+                        s += g[di][dj];
+        } else {
+            for (int i = i0; i <= i1; ++i)
+                for (int j = j0; j <= j1; ++j)
+                    if (mask[obase + i * OW + j] == p)
+                        s += dy[obase + i * OW + j];
+        }
         dx[nc * HW + p] = s;
     }
 }

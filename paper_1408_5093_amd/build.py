@@ -30,6 +30,15 @@ CFLAGS = [
 ]
 
 
+# Per-source extra flags.  The implicit-GEMM kernels keep their MFMA
+# accumulators in VGPRs: occupancy counts VGPRs + AGPRs together, and the
+# VGPR form avoids a bulk AGPR -> VGPR copy before the fused ReLU epilogue.
+EXTRA = {
+    "conv_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "conv_wgrad.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+}
+
+
 def _sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
 
@@ -49,7 +58,7 @@ def _torch_lib_dir():
 
 def _compile(src, verbose):
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC] + CFLAGS + ["-c", src, "-o", obj]
+    cmd = [HIPCC] + CFLAGS + EXTRA.get(os.path.basename(src), []) + ["-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -106,12 +106,9 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     // ---- A mapping: k = tid % TK, m = tid / TK + (NT / TK) * q
     const int a_k = tid % TK;
     const int a_m = tid / TK;
-    int a_row[EA];
-#pragma unroll
-    for (int q = 0; q < EA; ++q) {
-        const int m = m0 + a_m + (NT / TK) * q;
-        a_row[q] = m < M ? (g * M + m) * R : -1;
-    }
+    // A rows m0 + a_m + (NT/TK)*q: offsets linear in q, valid while m < M
+    const int a_row0 = (g * M + m0 + a_m) * R;
+    const int a_rows_ok = M - (m0 + a_m);
 
     // ---- B mapping: column(s) fixed per thread, reduction rows vary
     int b_base[BC], b_ih0[BC], b_iw0[BC];
@@ -141,8 +138,9 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
 #pragma unroll
         for (int q = 0; q < EA; ++q) {
             const int r = kbase + a_k;
-            const uint32_t off =
-                (a_row[q] >= 0 && r < R) ? (uint32_t)(a_row[q] + r) * 4u : kOob;
+            const uint32_t bad =
+                ((uint32_t)((NT / TK) * q >= a_rows_ok) | (uint32_t)(r >= R)) << 31;
+            const uint32_t off = ((uint32_t)(a_row0 + (NT / TK) * q * R + r) * 4u) | bad;
             rA[q] = buf_ld_f32(ra, off);
         }
     };
@@ -195,12 +193,26 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
         }
     };
 
+    // The forward pass starts every accumulator at its row's bias (the sum
+    // then runs bias + products, as in the layer's definition); a null bias
+    // is a zero-record buffer that reads 0.
     typename Op::acc_t acc[MI][NI];
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
+    for (int mi = 0; mi < MI; ++mi) {
+        typename Op::acc_t init{};
+        if constexpr (EPI == 0) {
+            const __amdgpu_buffer_rsrc_t rbias =
+                make_rsrc(p.bias, p.bias ? (uint32_t)(p.G * M) * 4u : 0u);
+#pragma unroll
+            for (int q = 0; q < Op::kRegs; ++q) {
+                const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
+                init[q] = buf_ld_f32(rbias, m < M ? (uint32_t)(g * M + m) * 4u : kOob);
+            }
+        }
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni)
-            acc[mi][ni] = typename Op::acc_t{};
+            acc[mi][ni] = init;
+    }
 
     const int nst = (R + TK - 1) / TK;
     // tap-major walk state: stage s covers tap (tu, tv), channels tc .. tc + TK - 1
@@ -239,27 +251,36 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
                 load_b_any((s + 1) * TK);
             }
         }
-        float a[KS][MI], b[KS][NI];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
+        // Rolling fragment prefetch: the LDS reads of k-step ks + PF are issued
+        // before the MFMAs of k-step ks (a ring of PF + 1 fragment sets).  The
+        // scheduling barriers pin that order; left alone, the scheduler trades
+        // it for fewer registers and waits on LDS before every k-step.
+        constexpr int PF = KS > 2 ? 2 : KS - 1;
+        float fa[PF + 1][MI], fb[PF + 1][NI];
+        auto read_frag = [&](int ks, int slot) {
 #pragma unroll
             for (int mi = 0; mi < MI; ++mi)
-                a[ks][mi] = As[cur][ks * Op::kStep + kl][arow + mi * MT];
+                fa[slot][mi] = As[cur][ks * Op::kStep + kl][arow + mi * MT];
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni)
-                b[ks][ni] = Bs[cur][ks * Op::kStep + kl][bcol + ni * MT];
-        }
-        // keep every LDS read of the stage ahead of its MFMAs (the scheduler
-        // would otherwise recycle four fragment registers and wait on LDS before
-        // every k-step)
-        __builtin_amdgcn_sched_barrier(0);
+                fb[slot][ni] = Bs[cur][ks * Op::kStep + kl][bcol + ni * MT];
+        };
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
+        for (int ks = 0; ks < PF; ++ks)
+            read_frag(ks, ks);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            if (ks + PF < KS)
+                read_frag(ks + PF, (ks + PF) % (PF + 1));
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
                 for (int ni = 0; ni < NI; ++ni)
-                    acc[mi][ni] = Op::run(a[ks][mi], b[ks][ni], acc[mi][ni]);
+                    acc[mi][ni] = Op::run(fa[ks % (PF + 1)][mi], fb[ks % (PF + 1)][ni],
+                                          acc[mi][ni]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
         if (s + 1 < nst)
             store_stage(cur ^ 1);
         __syncthreads();
@@ -267,34 +288,36 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
 
     // ---- epilogue (branch-free: masked lanes store to an out-of-range offset)
     const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y, p.Y_bytes);
+    // Masks are folded into the offsets with integer ops (bit 31 = past the
+    // buffer, dropped by the hardware): short-circuit tests here become
+    // divergent branches and make the compiler copy every accumulator out of
+    // the AGPRs at once.
     if constexpr (EPI == 0) {
-        // bias through a buffer resource: a null bias has 0 records and reads 0
-        const __amdgpu_buffer_rsrc_t rbias =
-            make_rsrc(p.bias, p.bias ? (uint32_t)(p.G * M) * 4u : 0u);
         int cbase[NI];
+        uint32_t cbad[NI];
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni) {
             const int col = n0 + bcol + ni * MT;
             const int n = col / OHW;
             const int pix = col - n * OHW;
-            cbase[ni] = col < p.Ncol ? n * p.Cout * OHW + pix : -1;
+            cbase[ni] = n * p.Cout * OHW + pix;
+            cbad[ni] = (uint32_t)(col >= p.Ncol) << 31;
         }
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
-            for (int q = 0; q < Op::kRegs; ++q) {
-                const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
-                const bool mok = m < M;
-                const int oc = g * M + m;
-                const float bv = buf_ld_f32(rbias, mok ? (uint32_t)oc * 4u : kOob);
+            for (int ni = 0; ni < NI; ++ni) {
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int ni = 0; ni < NI; ++ni) {
-                    float v = acc[mi][ni][q] + bv;
-                    if (p.relu)
-                        v = fmaxf(v, 0.f);
-                    const uint32_t off = (mok && cbase[ni] >= 0)
-                                             ? (uint32_t)(cbase[ni] + oc * OHW) * 4u
-                                             : kOob;
+                for (int q = 0; q < Op::kRegs; ++q) {
+                    const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
+                    const int oc = g * M + m;
+                    const float z = acc[mi][ni][q];
+                    // ReLU: non-positive values (NaN included) become 0; without
+                    // ReLU every value passes unchanged
+                    const float v = z > 0.f ? z : (p.relu ? 0.f : z);
+                    const uint32_t off = ((uint32_t)(cbase[ni] + oc * OHW) * 4u) | cbad[ni] |
+                                         ((uint32_t)(m >= M) << 31);
                     buf_st_f32(v, ry, off);
                 }
             }
@@ -320,7 +343,6 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
 #pragma unroll
             for (int q = 0; q < Op::kRegs; ++q) {
                 const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
-                const bool mok = m < M;
                 int c = m, fh = 0, fw = 0;
                 if (pss != 1) {
                     c = m / pss;
@@ -332,10 +354,12 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
                 for (int ni = 0; ni < NI; ++ni) {
                     const int h = hb[ni] + fh;
                     const int w = wb[ni] + fw;
-                    const bool ok = mok && (unsigned)h < (unsigned)p.OutH &&
-                                    (unsigned)w < (unsigned)p.OutW;
+                    const uint32_t bad = ((uint32_t)(m >= M) |
+                                          (uint32_t)((unsigned)h >= (unsigned)p.OutH) |
+                                          (uint32_t)((unsigned)w >= (unsigned)p.OutW))
+                                         << 31;
                     const uint32_t off =
-                        ok ? (uint32_t)(cb[ni] + c * OutHW + h * p.OutW + w) * 4u : kOob;
+                        ((uint32_t)(cb[ni] + c * OutHW + h * p.OutW + w) * 4u) | bad;
                     buf_st_f32(acc[mi][ni][q], ry, off);
                 }
             }

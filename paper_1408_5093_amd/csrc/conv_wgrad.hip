@@ -68,14 +68,9 @@ conv_wgrad_f32_kernel(const WgradParams p)
     const int rw = tid / TK;  // row within one pass
 
     // Per-thread A rows (output channels) and B rows (taps), fixed for the kernel.
-    int a_off[EA];
-    uint32_t a_bad[EA];
-#pragma unroll
-    for (int q = 0; q < EA; ++q) {
-        const int m = m0 + rw + RS * q;
-        a_off[q] = m < p.Kg ? (g * p.Kg + m) * OHW : 0;
-        a_bad[q] = m < p.Kg ? 0u : kOob;
-    }
+    // A rows m0 + rw + RS*q: offsets are linear in q, validity is m < Kg
+    const int a_off0 = (g * p.Kg + m0 + rw) * OHW;
+    const int a_rows_ok = p.Kg - (m0 + rw);  // row q is valid iff RS*q < a_rows_ok
     int b_off[EB], b_uv[EB];
 #pragma unroll
     for (int q = 0; q < EB; ++q) {
@@ -111,7 +106,9 @@ conv_wgrad_f32_kernel(const WgradParams p)
         const int xbase = (n * p.C + g * p.Cg) * IHW + ih0 * IW + iw0;
 #pragma unroll
         for (int q = 0; q < EA; ++q) {
-            const uint32_t off = ((uint32_t)(dbase + a_off[q]) * 4u) | cbad | a_bad[q];
+            const uint32_t bad = (uint32_t)(RS * q >= a_rows_ok) << 31;
+            const uint32_t off =
+                ((uint32_t)(dbase + a_off0 + RS * q * OHW) * 4u) | cbad | bad;
             rA[q] = buf_ld_f32(rd, off);
         }
 #pragma unroll
@@ -156,26 +153,34 @@ conv_wgrad_f32_kernel(const WgradParams p)
         const int cur = s & 1;
         if (s + 1 < nst)
             load_stage(col_begin + (s + 1) * TK);
+        // rolling fragment prefetch, as in the forward kernel
         constexpr int KS = TK / 2;
-        float a[KS][MI], b[KS][NI];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
+        constexpr int PF = 2;
+        float fa[PF + 1][MI], fb[PF + 1][NI];
+        auto read_frag = [&](int ks, int slot) {
 #pragma unroll
             for (int mi = 0; mi < MI; ++mi)
-                a[ks][mi] = As[cur][2 * ks + kl][arow + mi * MT];
+                fa[slot][mi] = As[cur][2 * ks + kl][arow + mi * MT];
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni)
-                b[ks][ni] = Bs[cur][2 * ks + kl][bcol + ni * MT];
-        }
-        __builtin_amdgcn_sched_barrier(0);  // all LDS reads of the stage ahead of its MFMAs
+                fb[slot][ni] = Bs[cur][2 * ks + kl][bcol + ni * MT];
+        };
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
+        for (int ks = 0; ks < PF; ++ks)
+            read_frag(ks, ks);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            if (ks + PF < KS)
+                read_frag(ks + PF, (ks + PF) % (PF + 1));
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
                 for (int ni = 0; ni < NI; ++ni)
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[ks][mi], b[ks][ni],
-                                                                       acc[mi][ni], 0, 0, 0);
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                        fa[ks % (PF + 1)][mi], fb[ks % (PF + 1)][ni], acc[mi][ni], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
         if (s + 1 < nst)
             store_stage(cur ^ 1);
         __syncthreads();

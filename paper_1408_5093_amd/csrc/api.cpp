@@ -51,7 +51,7 @@ struct ConvPlan {
     // data gradient (phase-stacked)
     int Th, Tw, a0h, a0w, Ah, Aw, Mt, Rt;
     // weight gradient split-K
-    int splits, cols_per_split;
+    int splits, cols_per_split, wgrad_tile;
     // reduction order of the implicit GEMMs: tap-major r = (u, v, c) when the
     // gathered channels per group fill whole pipeline stages
     int fwd_tile, dgrad_tile;
@@ -84,7 +84,27 @@ int pick_tile(int M, int cin_g, int forced)
     return best;
 }
 
-// Profiling override of the tile choice: an integer GemmTile, read once.
+// Weight-gradient tile: the least padding of Kg, then the taller tile.
+int pick_wgrad_tile(int Kg, int forced)
+{
+    if (forced >= 0 && forced < WTILE_COUNT)
+        return forced;
+    int best = WTILE_128x128;
+    double best_waste = 1e30;
+    for (int t = 0; t < WTILE_COUNT; ++t) {
+        const int tm = wgrad_tile_m(t);
+        const double waste = (double)((Kg + tm - 1) / tm * tm) / Kg;
+        if (waste < best_waste - 1e-9 ||
+            (waste < best_waste + 1e-9 && tm > wgrad_tile_m(best))) {
+            best = t;
+            best_waste = waste;
+        }
+    }
+    return best;
+}
+
+// Profiling override of a tuning choice (tile index, block target): an
+// integer from the environment, -1 when unset.
 int env_tile(const char* name)
 {
     const char* v = getenv(name);
@@ -152,13 +172,18 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     if (wt_elems * 4 > kMaxTensorBytes || dcols > (int64_t(1) << 30))
         return fail(CAFFE_ERR_UNSUPPORTED, "data-gradient operands reach 2^31 bytes");
 
-    // Weight-gradient split-K: aim for ~4 workgroups per CU, each split at
-    // least 8 stages deep.
+    // Weight-gradient split-K: the tile with the least padding of Kg, then
+    // enough splits of the reduction for ~`target` workgroups (8 per CU by
+    // default), each split at least 8 stages deep.
     const int64_t ncol = (int64_t)q.N * q.Ho * q.Wo;
     const int tk = wgrad_tile_k();
-    const int64_t tiles = (int64_t)((q.Kg + wgrad_tile_m() - 1) / wgrad_tile_m()) *
-                          ((q.R + wgrad_tile_n() - 1) / wgrad_tile_n()) * q.G;
-    int64_t splits = (1024 + tiles - 1) / tiles;
+    q.wgrad_tile = pick_wgrad_tile(q.Kg, env_tile("CAFFE_CONV_WGRAD_TILE"));
+    const int wtm = wgrad_tile_m(q.wgrad_tile), wtn = wgrad_tile_n(q.wgrad_tile);
+    const int64_t tiles = (int64_t)((q.Kg + wtm - 1) / wtm) * ((q.R + wtn - 1) / wtn) * q.G;
+    const int64_t target = env_tile("CAFFE_CONV_WGRAD_BLOCKS") > 0
+                               ? env_tile("CAFFE_CONV_WGRAD_BLOCKS")
+                               : 2048;
+    int64_t splits = (target + tiles - 1) / tiles;
     const int64_t max_splits = std::max<int64_t>(1, ncol / (8 * tk));
     const int64_t max_by_bytes = std::max<int64_t>(1, kMaxTensorBytes / (q.weight_elems * 4));
     splits = std::max<int64_t>(1, std::min(std::min(splits, max_splits), max_by_bytes));
@@ -330,7 +355,7 @@ int run_weights(const ConvPlan& q, const float* dsrc, const void* bottom, float*
         p.splits = q.splits;
         p.div_ohw = make_fastdiv((uint32_t)(q.Ho * q.Wo));
         p.div_ow = make_fastdiv((uint32_t)q.Wo);
-        LAUNCH(launch_conv_wgrad_f32(p, s), "weight-gradient launch");
+        LAUNCH(launch_conv_wgrad_f32(p, q.wgrad_tile, s), "weight-gradient launch");
     }
     const float* sums = (const float*)(ws + q.off_sums);
     LAUNCH(launch_wgrad_reduce(part, weight_diff, weight_diff ? (int)q.weight_elems : 0, q.splits,

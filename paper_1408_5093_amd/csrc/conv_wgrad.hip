@@ -207,34 +207,58 @@ conv_wgrad_f32_kernel(const WgradParams p)
 
 // ------------------------------------------------------------------ launch
 namespace {
-constexpr int kWM = 2, kWN = 2, kMI = 2, kNI = 2, kTK = 16;
+constexpr int kTK = 16;
 
-template <int KH, int KW, int SH, int SW>
+struct WTile {
+    int wm, wn, mi, ni;
+};
+constexpr WTile kWTiles[WTILE_COUNT] = {
+    {2, 2, 2, 2},  // 128 x 128
+    {1, 4, 3, 1},  // 96 x 128
+    {2, 2, 1, 2},  // 64 x 128
+};
+
+template <int WM, int WN, int MI, int NI, int KH, int KW, int SH, int SW>
 hipError_t launch_w(const WgradParams& p, hipStream_t s)
 {
-    constexpr int TM = kWM * kMI * 32, TN = kWN * kNI * 32;
+    constexpr int TM = WM * MI * 32, TN = WN * NI * 32;
     dim3 grid((p.R + TN - 1) / TN, (p.Kg + TM - 1) / TM, p.G * p.splits);
-    hipLaunchKernelGGL((conv_wgrad_f32_kernel<kWM, kWN, kMI, kNI, kTK, KH, KW, SH, SW>), grid,
-                       dim3(64 * kWM * kWN), 0, s, p);
+    hipLaunchKernelGGL((conv_wgrad_f32_kernel<WM, WN, MI, NI, kTK, KH, KW, SH, SW>), grid,
+                       dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();
 }
-}  // namespace
 
-int wgrad_tile_m() { return kWM * kMI * 32; }
-int wgrad_tile_n() { return kWN * kNI * 32; }
-int wgrad_tile_k() { return kTK; }
-
-hipError_t launch_conv_wgrad_f32(const WgradParams& p, hipStream_t s)
+template <int WM, int WN, int MI, int NI>
+hipError_t launch_wg(const WgradParams& p, hipStream_t s)
 {
     if (p.sh == 1 && p.sw == 1) {
         if (p.kh == 3 && p.kw == 3)
-            return launch_w<3, 3, 1, 1>(p, s);
+            return launch_w<WM, WN, MI, NI, 3, 3, 1, 1>(p, s);
         if (p.kh == 5 && p.kw == 5)
-            return launch_w<5, 5, 1, 1>(p, s);
+            return launch_w<WM, WN, MI, NI, 5, 5, 1, 1>(p, s);
     }
     if (p.kh == 11 && p.kw == 11 && p.sh == 4 && p.sw == 4)
-        return launch_w<11, 11, 4, 4>(p, s);
-    return launch_w<0, 0, 0, 0>(p, s);
+        return launch_w<WM, WN, MI, NI, 11, 11, 4, 4>(p, s);
+    return launch_w<WM, WN, MI, NI, 0, 0, 0, 0>(p, s);
+}
+}  // namespace
+
+int wgrad_tile_m(int tile) { return kWTiles[tile].wm * kWTiles[tile].mi * 32; }
+int wgrad_tile_n(int tile) { return kWTiles[tile].wn * kWTiles[tile].ni * 32; }
+int wgrad_tile_k() { return kTK; }
+
+hipError_t launch_conv_wgrad_f32(const WgradParams& p, int tile, hipStream_t s)
+{
+    switch (tile) {
+    case WTILE_128x128:
+        return launch_wg<2, 2, 2, 2>(p, s);
+    case WTILE_96x128:
+        return launch_wg<1, 4, 3, 1>(p, s);
+    case WTILE_64x128:
+        return launch_wg<2, 2, 1, 2>(p, s);
+    default:
+        return hipErrorInvalidValue;
+    }
 }
 
 FastDiv make_fastdiv(uint32_t d)

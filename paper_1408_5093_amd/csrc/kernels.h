@@ -83,10 +83,16 @@ hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool
 hipError_t launch_pack_weights_tap(const float* W, float* Wp, int K, int Cg, int khw,
                                    hipStream_t s);
 
-int wgrad_tile_m();
-int wgrad_tile_n();
+enum WgradTile : int {
+    WTILE_128x128 = 0,  // 4 waves as 2x2, each 64x64
+    WTILE_96x128 = 1,   // 4 waves as 1x4, each 96x32
+    WTILE_64x128 = 2,   // 4 waves as 2x2, each 32x64
+    WTILE_COUNT
+};
+int wgrad_tile_m(int tile);
+int wgrad_tile_n(int tile);
 int wgrad_tile_k();
-hipError_t launch_conv_wgrad_f32(const WgradParams& p, hipStream_t s);
+hipError_t launch_conv_wgrad_f32(const WgradParams& p, int tile, hipStream_t s);
 
 // D = relu ? G * [Y > 0] : G (written to D unless D is null) and, unless
 // plane_sums is null, plane_sums[p] = sum of D over plane p (fixed order).

@@ -202,15 +202,17 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     q.dgrad_tap = q.Kg % gemm_tile_k(q.dgrad_tile) == 0;
     q.ws_fwd = q.fwd_tap ? align_up(q.weight_elems * 4, kWsAlign) : 0;
 
-    // Workspace: [masked diff][plane sums][transformed weights][partials]
-    const size_t d_bytes = q.relu ? align_up(q.top_elems * 4, kWsAlign) : 0;
-    const size_t sums_bytes = align_up((size_t)q.N * q.K * 4, kWsAlign);
+    // Workspace: [bias partial sums][transformed weights][weight partials].
+    // The ReLU mask is applied inside the gradient kernels, so the masked
+    // top gradient is never stored.
+    const size_t sums_bytes =
+        align_up((size_t)std::max<int64_t>(q.N, q.splits) * q.K * 4, kWsAlign);
     const size_t wt_bytes = align_up(wt_elems * 4, kWsAlign);
     q.off_d = 0;
-    q.off_sums = d_bytes;
+    q.off_sums = 0;
     q.off_wt = q.off_sums + sums_bytes;
     q.off_part = q.off_wt + wt_bytes;
-    q.ws_data = d_bytes + sums_bytes + wt_bytes;       // layout shared with ws_both
+    q.ws_data = sums_bytes + wt_bytes;
     q.ws_weights = q.off_part + align_up(part_bytes, kWsAlign);
     q.ws_both = q.ws_weights;
     return CAFFE_OK;
@@ -289,22 +291,23 @@ int run_forward(const ConvPlan& q, const void* bottom, const void* weight, const
     return CAFFE_OK;
 }
 
-// D = masked top_diff (in the workspace when relu), plane sums for the bias.
-int run_mask(const ConvPlan& q, const float* top_diff, const float* top, char* ws, bool want_sums,
-             const float** dsrc, hipStream_t s)
+// Bias gradient without a weight gradient: per-(n, k) plane sums of the
+// masked top gradient, reduced over n in order.
+int run_bias_only(const ConvPlan& q, const float* top_diff, const float* top, float* bias_diff,
+                  int accumulate, char* ws, hipStream_t s)
 {
-    float* D = q.relu ? (float*)(ws + q.off_d) : nullptr;
-    float* sums = want_sums ? (float*)(ws + q.off_sums) : nullptr;
-    *dsrc = q.relu ? D : top_diff;
-    if (!D && !sums)
-        return CAFFE_OK;
-    LAUNCH(launch_relu_mask_bias(top_diff, top, D, sums, q.N * q.K, q.Ho * q.Wo, q.relu, s),
-           "relu/bias launch");
+    float* sums = (float*)(ws + q.off_sums);
+    if (q.N > 0)
+        LAUNCH(launch_relu_mask_bias(top_diff, top, nullptr, sums, q.N * q.K, q.Ho * q.Wo,
+                                     q.relu, s),
+               "bias launch");
+    LAUNCH(launch_wgrad_reduce(nullptr, nullptr, 0, 0, sums, bias_diff, q.N, q.K, accumulate, s),
+           "bias reduce launch");
     return CAFFE_OK;
 }
 
-int run_data(const ConvPlan& q, const float* dsrc, const void* weight, float* bottom_diff, char* ws,
-             hipStream_t s)
+int run_data(const ConvPlan& q, const float* top_diff, const float* top, const void* weight,
+             float* bottom_diff, char* ws, hipStream_t s)
 {
     if (q.bottom_elems == 0)
         return CAFFE_OK;
@@ -314,7 +317,8 @@ int run_data(const ConvPlan& q, const float* dsrc, const void* weight, float* bo
            "weight transform launch");
     ConvGemmParams p = {};
     p.A = wt;
-    p.X = dsrc;
+    p.X = top_diff;
+    p.Xmask = q.relu ? top : nullptr;
     p.Y = bottom_diff;
     p.bias = nullptr;
     p.A_bytes = nbytes((int64_t)q.G * q.Mt * q.Rt, 4);
@@ -334,32 +338,33 @@ int run_data(const ConvPlan& q, const float* dsrc, const void* weight, float* bo
     return CAFFE_OK;
 }
 
-int run_weights(const ConvPlan& q, const float* dsrc, const void* bottom, float* weight_diff,
-                float* bias_diff, int accumulate, char* ws, hipStream_t s)
+int run_weights(const ConvPlan& q, const float* top_diff, const float* top, const void* bottom,
+                float* weight_diff, float* bias_diff, int accumulate, char* ws, hipStream_t s)
 {
     float* part = (float*)(ws + q.off_part);
-    if (weight_diff) {
-        WgradParams p = {};
-        p.D = dsrc;
-        p.X = bottom;
-        p.P = part;
-        p.D_bytes = nbytes(q.top_elems, 4);
-        p.X_bytes = nbytes(q.bottom_elems, q.esize);
-        p.P_bytes = nbytes((int64_t)q.splits * q.weight_elems, 4);
-        p.N = q.N; p.C = q.C; p.IH = q.H; p.IW = q.W; p.Cg = q.Cg; p.K = q.K; p.Kg = q.Kg;
-        p.kh = q.kh; p.kw = q.kw; p.sh = q.sh; p.sw = q.sw; p.ph = q.ph; p.pw = q.pw;
-        p.OH = q.Ho; p.OW = q.Wo;
-        p.R = q.R; p.G = q.G;
-        p.Ncol = q.N * q.Ho * q.Wo;
-        p.cols_per_split = q.cols_per_split;
-        p.splits = q.splits;
-        p.div_ohw = make_fastdiv((uint32_t)(q.Ho * q.Wo));
-        p.div_ow = make_fastdiv((uint32_t)q.Wo);
-        LAUNCH(launch_conv_wgrad_f32(p, q.wgrad_tile, s), "weight-gradient launch");
-    }
-    const float* sums = (const float*)(ws + q.off_sums);
-    LAUNCH(launch_wgrad_reduce(part, weight_diff, weight_diff ? (int)q.weight_elems : 0, q.splits,
-                               sums, bias_diff, q.N, q.K, accumulate, s),
+    float* sums = (float*)(ws + q.off_sums);
+    WgradParams p = {};
+    p.D = top_diff;
+    p.Dmask = q.relu ? top : nullptr;
+    p.X = bottom;
+    p.P = part;
+    p.dbp = bias_diff ? sums : nullptr;
+    p.D_bytes = nbytes(q.top_elems, 4);
+    p.X_bytes = nbytes(q.bottom_elems, q.esize);
+    p.P_bytes = nbytes((int64_t)q.splits * q.weight_elems, 4);
+    p.N = q.N; p.C = q.C; p.IH = q.H; p.IW = q.W; p.Cg = q.Cg; p.K = q.K; p.Kg = q.Kg;
+    p.kh = q.kh; p.kw = q.kw; p.sh = q.sh; p.sw = q.sw; p.ph = q.ph; p.pw = q.pw;
+    p.OH = q.Ho; p.OW = q.Wo;
+    p.R = q.R; p.G = q.G;
+    p.Ncol = q.N * q.Ho * q.Wo;
+    p.cols_per_split = q.cols_per_split;
+    p.splits = q.splits;
+    p.div_ohw = make_fastdiv((uint32_t)(q.Ho * q.Wo));
+    p.div_ow = make_fastdiv((uint32_t)q.Wo);
+    LAUNCH(launch_conv_wgrad_f32(p, q.wgrad_tile, s), "weight-gradient launch");
+    // dW = sum of the split partials; db = sum of the split bias partials
+    LAUNCH(launch_wgrad_reduce(part, weight_diff, (int)q.weight_elems, q.splits, sums, bias_diff,
+                               q.splits, q.K, accumulate, s),
            "reduce launch");
     return CAFFE_OK;
 }
@@ -442,19 +447,18 @@ int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, cons
     CHECK(check_conv_ptrs(q, bottom_diff, false, true, "bottom_diff"));
     CHECK(check_conv_ptrs(q, weight_diff, false, false, "weight_diff"));
     CHECK(check_conv_ptrs(q, bias_diff, false, false, "bias_diff"));
-    const size_t need = (weight_diff || bias_diff) ? q.ws_both : q.ws_data;
+    const size_t need = weight_diff ? q.ws_both : q.ws_data;
     CHECK(check_ws(workspace, ws_bytes, need));
     if (q.dtype != CAFFE_F32)
         return fail(CAFFE_ERR_UNSUPPORTED, "bf16 backward is not built yet");
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    const float* dsrc = top_diff;
-    if (bottom_diff || weight_diff || bias_diff)
-        CHECK(run_mask(q, top_diff, top, ws, bias_diff != nullptr && q.N > 0, &dsrc, s));
     if (bottom_diff)
-        CHECK(run_data(q, dsrc, weight, bottom_diff, ws, s));
-    if (weight_diff || bias_diff)
-        CHECK(run_weights(q, dsrc, bottom, weight_diff, bias_diff, accumulate, ws, s));
+        CHECK(run_data(q, top_diff, top, weight, bottom_diff, ws, s));
+    if (weight_diff)
+        CHECK(run_weights(q, top_diff, top, bottom, weight_diff, bias_diff, accumulate, ws, s));
+    else if (bias_diff)
+        CHECK(run_bias_only(q, top_diff, top, bias_diff, accumulate, ws, s));
     return CAFFE_OK;
 }
 

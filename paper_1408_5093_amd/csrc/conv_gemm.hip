@@ -56,7 +56,7 @@ struct Mfma<16> {
 };
 
 template <int MT, int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH, int SW, int EPI,
-          bool TAP>
+          bool TAP, bool MASK>
 __global__ void __launch_bounds__(64 * WM * WN)
 conv_gemm_f32_kernel(const ConvGemmParams p)
 {
@@ -102,6 +102,7 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
 
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.A, p.A_bytes);
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, p.X_bytes);
+    const __amdgpu_buffer_rsrc_t rxm = make_rsrc(MASK ? p.Xmask : p.X, p.X_bytes);
 
     // ---- A mapping: k = tid % TK, m = tid / TK + (NT / TK) * q
     const int a_k = tid % TK;
@@ -133,6 +134,7 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     auto b_cc = [&](int q) { return TN > NT ? q % BC : 0; };
 
     float rA[EA], rB[EB];
+    float rM[MASK ? EB : 1];  // ReLU-mask values matching rB (MASK only)
 
     auto load_a = [&](int kbase) {
 #pragma unroll
@@ -161,6 +163,8 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
         for (int q = 0; q < EB; ++q) {
             const uint32_t coff = (uint32_t)((c0 + b_row(q)) * IHW) * 4u;
             rB[q] = buf_ld_f32(rx, voff[b_cc(q)] + coff);
+            if constexpr (MASK)
+                rM[q] = buf_ld_f32(rxm, voff[b_cc(q)] + coff);
         }
     };
 
@@ -179,6 +183,8 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
             const bool ok = r < R && (unsigned)ih < (unsigned)IH && (unsigned)iw < (unsigned)IW;
             const uint32_t off = ok ? (uint32_t)(b_base[cc] + c * IHW + u * IW + v) * 4u : kOob;
             rB[q] = buf_ld_f32(rx, off);
+            if constexpr (MASK)
+                rM[q] = buf_ld_f32(rxm, off);
         }
     };
 
@@ -189,7 +195,10 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
 #pragma unroll
         for (int q = 0; q < EB; ++q) {
             const int col = TN > NT ? tid + NT * b_cc(q) : tid % TN;
-            Bs[buf][b_row(q)][col] = rB[q];
+            float v = rB[q];
+            if constexpr (MASK)
+                v = rM[q] > 0.f ? v : 0.f;
+            Bs[buf][b_row(q)][col] = v;
         }
     };
 
@@ -404,57 +413,52 @@ constexpr TileShape kTiles[TILE_COUNT] = {
     {32, 1, 4, 3, 2, 16},  // 96 x 256
     {16, 1, 4, 3, 4, 16},  // 48 x 256
     {32, 1, 4, 2, 2, 16},  // 64 x 256
-    {32, 2, 2, 2, 4, 16},  // 128 x 256
-    {32, 2, 2, 4, 2, 16},  // 256 x 128
     {32, 2, 2, 2, 2, 32},  // 128 x 128, 32-deep stages
 };
 
 template <int MT, int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH, int SW, int EPI,
-          bool TAP>
+          bool TAP, bool MASK>
 hipError_t launch_one(const ConvGemmParams& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * MT, TN = WN * NI * MT;
     dim3 grid((p.Ncol + TN - 1) / TN, (p.M + TM - 1) / TM, p.G);
-    hipLaunchKernelGGL((conv_gemm_f32_kernel<MT, WM, WN, MI, NI, TK, KH, KW, SH, SW, EPI, TAP>),
-                       grid, dim3(64 * WM * WN), 0, s, p);
+    hipLaunchKernelGGL(
+        (conv_gemm_f32_kernel<MT, WM, WN, MI, NI, TK, KH, KW, SH, SW, EPI, TAP, MASK>), grid,
+        dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();
 }
 
-template <int MT, int WM, int WN, int MI, int NI, int TK, int EPI>
+template <int MT, int WM, int WN, int MI, int NI, int TK, int EPI, bool MASK>
 hipError_t launch_geom(const ConvGemmParams& p, bool tap, hipStream_t s)
 {
     if (tap) {
         if (p.sh == 1 && p.sw == 1) {
             if (p.kh == 3 && p.kw == 3)
-                return launch_one<MT, WM, WN, MI, NI, TK, 3, 3, 1, 1, EPI, true>(p, s);
+                return launch_one<MT, WM, WN, MI, NI, TK, 3, 3, 1, 1, EPI, true, MASK>(p, s);
             if (p.kh == 5 && p.kw == 5)
-                return launch_one<MT, WM, WN, MI, NI, TK, 5, 5, 1, 1, EPI, true>(p, s);
+                return launch_one<MT, WM, WN, MI, NI, TK, 5, 5, 1, 1, EPI, true, MASK>(p, s);
         }
-        return launch_one<MT, WM, WN, MI, NI, TK, 0, 0, 0, 0, EPI, true>(p, s);
+        return launch_one<MT, WM, WN, MI, NI, TK, 0, 0, 0, 0, EPI, true, MASK>(p, s);
     }
     if (EPI == 0 && p.kh == 11 && p.kw == 11 && p.sh == 4 && p.sw == 4)
-        return launch_one<MT, WM, WN, MI, NI, TK, 11, 11, 4, 4, EPI, false>(p, s);
-    return launch_one<MT, WM, WN, MI, NI, TK, 0, 0, 0, 0, EPI, false>(p, s);
+        return launch_one<MT, WM, WN, MI, NI, TK, 11, 11, 4, 4, EPI, false, MASK>(p, s);
+    return launch_one<MT, WM, WN, MI, NI, TK, 0, 0, 0, 0, EPI, false, MASK>(p, s);
 }
 
-template <int EPI>
+template <int EPI, bool MASK>
 hipError_t launch_tile(const ConvGemmParams& p, int tile, bool tap, hipStream_t s)
 {
     switch (tile) {
     case TILE_128x128:
-        return launch_geom<32, 2, 2, 2, 2, 16, EPI>(p, tap, s);
+        return launch_geom<32, 2, 2, 2, 2, 16, EPI, MASK>(p, tap, s);
     case TILE_96x256:
-        return launch_geom<32, 1, 4, 3, 2, 16, EPI>(p, tap, s);
+        return launch_geom<32, 1, 4, 3, 2, 16, EPI, MASK>(p, tap, s);
     case TILE_48x256:
-        return launch_geom<16, 1, 4, 3, 4, 16, EPI>(p, tap, s);
+        return launch_geom<16, 1, 4, 3, 4, 16, EPI, MASK>(p, tap, s);
     case TILE_64x256:
-        return launch_geom<32, 1, 4, 2, 2, 16, EPI>(p, tap, s);
-    case TILE_128x256:
-        return launch_geom<32, 2, 2, 2, 4, 16, EPI>(p, tap, s);
-    case TILE_256x128:
-        return launch_geom<32, 2, 2, 4, 2, 16, EPI>(p, tap, s);
+        return launch_geom<32, 1, 4, 2, 2, 16, EPI, MASK>(p, tap, s);
     case TILE_128x128_K32:
-        return launch_geom<32, 2, 2, 2, 2, 32, EPI>(p, tap, s);
+        return launch_geom<32, 2, 2, 2, 2, 32, EPI, MASK>(p, tap, s);
     default:
         return hipErrorInvalidValue;
     }
@@ -483,7 +487,10 @@ hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool
         return hipSuccess;
     if (tile < 0 || tile >= TILE_COUNT || (tap_major && p.Cin_g % kTiles[tile].tk != 0))
         return hipErrorInvalidValue;
-    return epi == 0 ? launch_tile<0>(p, tile, tap_major, s) : launch_tile<1>(p, tile, tap_major, s);
+    if (epi == 0)
+        return launch_tile<0, false>(p, tile, tap_major, s);
+    return p.Xmask ? launch_tile<1, true>(p, tile, tap_major, s)
+                   : launch_tile<1, false>(p, tile, tap_major, s);
 }
 
 }  // namespace caffe_hip

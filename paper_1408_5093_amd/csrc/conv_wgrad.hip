@@ -22,7 +22,7 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t x, const FastDiv& f)
     return (uint32_t)(((uint64_t)x * f.mul) >> f.shift);
 }
 
-template <int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH, int SW>
+template <int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH, int SW, bool MASK>
 __global__ void __launch_bounds__(64 * WM * WN)
 conv_wgrad_f32_kernel(const WgradParams p)
 {
@@ -62,6 +62,7 @@ conv_wgrad_f32_kernel(const WgradParams p)
     const int col_end = min(p.Ncol, col_begin + p.cols_per_split);
 
     const __amdgpu_buffer_rsrc_t rd = make_rsrc(p.D, p.D_bytes);
+    const __amdgpu_buffer_rsrc_t rdm = make_rsrc(MASK ? p.Dmask : p.D, p.D_bytes);
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, p.X_bytes);
 
     const int kc = tid % TK;  // reduction index within a stage
@@ -71,29 +72,46 @@ conv_wgrad_f32_kernel(const WgradParams p)
     // A rows m0 + rw + RS*q: offsets are linear in q, validity is m < Kg
     const int a_off0 = (g * p.Kg + m0 + rw) * OHW;
     const int a_rows_ok = p.Kg - (m0 + rw);  // row q is valid iff RS*q < a_rows_ok
-    int b_off[EB], b_uv[EB];
+    // Per-thread tap table.  With a compile-time kernel (PACK) each entry is
+    // one word: offset c*IH*IW + u*IW + v in bits 0..21, u in 22..26, v in
+    // 27..31 (the launcher checks Cg*IH*IW < 2^22 and kh, kw <= 32); taps past
+    // R are flagged in r_bad.
+    constexpr bool PACK = KH != 0;
+    int b_off[EB];
+    int b_uv[PACK ? 1 : EB];
+    uint32_t r_bad = 0;
 #pragma unroll
     for (int q = 0; q < EB; ++q) {
         const int r = r0 + rw + RS * q;
-        if (r < p.R) {
-            const int c = r / khw;
-            const int rr = r - c * khw;
-            const int u = rr / kw;
-            const int v = rr - u * kw;
+        const int rr_ = r < p.R ? r : 0;
+        const int c = rr_ / khw;
+        const int rr = rr_ - c * khw;
+        const int u = rr / kw;
+        const int v = rr - u * kw;
+        if (r >= p.R)
+            r_bad |= 1u << q;
+        if constexpr (PACK) {
+            b_off[q] = (c * IHW + u * IW + v) | (u << 22) | (v << 27);
+        } else {
             b_off[q] = c * IHW + u * IW + v;
             b_uv[q] = u | (v << 16);
-        } else {
-            b_off[q] = 0;
-            b_uv[q] = 0x7fff;  // u beyond any image height: always out of range
         }
     }
 
     float rA[EA], rB[EB];
+    float rM[MASK ? EA : 1];  // ReLU-mask values matching rA (MASK only)
+    // bias-gradient partials: in the first tap tile's workgroups, thread t < TM
+    // owns row t and adds the staged (masked) diff of its row, stage by stage
+    const bool want_db = p.dbp != nullptr && blockIdx.x == 0;
+    float dsum = 0.f;
 
-    // Masked lanes get an offset with bit 31 set: always past num_records, so
-    // the hardware returns 0.  The mask is folded in with integer ops (no
-    // selects on load addresses, which the compiler would turn into branches).
     auto load_stage = [&](int cbase) {
+        // The tap table is decoded afresh each stage: the empty asm hides its
+        // loop invariance, which would otherwise keep decoded copies live in
+        // extra registers for the whole loop.
+#pragma unroll
+        for (int q = 0; q < EB; ++q)
+            asm volatile("" : "+v"(b_off[q]));
         const int col = cbase + kc;
         const uint32_t cbad = (uint32_t)(col >= col_end) << 31;
         const int n = (int)fdiv((uint32_t)col, p.div_ohw);
@@ -110,22 +128,37 @@ conv_wgrad_f32_kernel(const WgradParams p)
             const uint32_t off =
                 ((uint32_t)(dbase + a_off0 + RS * q * OHW) * 4u) | cbad | bad;
             rA[q] = buf_ld_f32(rd, off);
+            if constexpr (MASK)
+                rM[q] = buf_ld_f32(rdm, off);
         }
 #pragma unroll
         for (int q = 0; q < EB; ++q) {
-            const int ih = ih0 + (b_uv[q] & 0xffff);
-            const int iw = iw0 + (b_uv[q] >> 16);
+            int ih, iw, boff;
+            if constexpr (PACK) {
+                ih = ih0 + ((b_off[q] >> 22) & 31);
+                iw = iw0 + ((uint32_t)b_off[q] >> 27);
+                boff = b_off[q] & 0x3fffff;
+            } else {
+                ih = ih0 + (b_uv[q] & 0xffff);
+                iw = iw0 + (b_uv[q] >> 16);
+                boff = b_off[q];
+            }
             const uint32_t bad = ((uint32_t)((unsigned)ih >= (unsigned)IH) |
                                   (uint32_t)((unsigned)iw >= (unsigned)IW)) << 31;
-            const uint32_t off = ((uint32_t)(xbase + b_off[q]) * 4u) | cbad | bad;
+            const uint32_t off = ((uint32_t)(xbase + boff) * 4u) | cbad | bad |
+                                 (((r_bad >> q) & 1u) << 31);
             rB[q] = buf_ld_f32(rx, off);
         }
     };
 
     auto store_stage = [&](int buf) {
 #pragma unroll
-        for (int q = 0; q < EA; ++q)
-            As[buf][kc][rw + RS * q] = rA[q];
+        for (int q = 0; q < EA; ++q) {
+            float v = rA[q];
+            if constexpr (MASK)
+                v = rM[q] > 0.f ? v : 0.f;
+            As[buf][kc][rw + RS * q] = v;
+        }
 #pragma unroll
         for (int q = 0; q < EB; ++q)
             Bs[buf][kc][rw + RS * q] = rB[q];
@@ -153,6 +186,11 @@ conv_wgrad_f32_kernel(const WgradParams p)
         const int cur = s & 1;
         if (s + 1 < nst)
             load_stage(col_begin + (s + 1) * TK);
+        if (want_db && tid < TM) {
+#pragma unroll
+            for (int k = 0; k < TK; ++k)
+                dsum += As[cur][k][tid];
+        }
         // rolling fragment prefetch, as in the forward kernel
         constexpr int KS = TK / 2;
         constexpr int PF = 2;
@@ -184,6 +222,12 @@ conv_wgrad_f32_kernel(const WgradParams p)
         if (s + 1 < nst)
             store_stage(cur ^ 1);
         __syncthreads();
+    }
+
+    if (want_db) {
+        const int m = m0 + tid;
+        if (tid < TM && m < p.Kg)
+            p.dbp[split * p.K + g * p.Kg + m] = dsum;
     }
 
     // Partial result P[split][g*Kg + m][r]: lanes run along r (contiguous).
@@ -223,14 +267,21 @@ hipError_t launch_w(const WgradParams& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * 32, TN = WN * NI * 32;
     dim3 grid((p.R + TN - 1) / TN, (p.Kg + TM - 1) / TM, p.G * p.splits);
-    hipLaunchKernelGGL((conv_wgrad_f32_kernel<WM, WN, MI, NI, kTK, KH, KW, SH, SW>), grid,
-                       dim3(64 * WM * WN), 0, s, p);
+    if (p.Dmask)
+        hipLaunchKernelGGL((conv_wgrad_f32_kernel<WM, WN, MI, NI, kTK, KH, KW, SH, SW, true>),
+                           grid, dim3(64 * WM * WN), 0, s, p);
+    else
+        hipLaunchKernelGGL((conv_wgrad_f32_kernel<WM, WN, MI, NI, kTK, KH, KW, SH, SW, false>),
+                           grid, dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();
 }
 
 template <int WM, int WN, int MI, int NI>
 hipError_t launch_wg(const WgradParams& p, hipStream_t s)
 {
+    // compile-time kernels pack their tap table (offsets below 2^22)
+    if ((int64_t)p.Cg * p.IH * p.IW >= (int64_t(1) << 22))
+        return launch_w<WM, WN, MI, NI, 0, 0, 0, 0>(p, s);
     if (p.sh == 1 && p.sw == 1) {
         if (p.kh == 3 && p.kw == 3)
             return launch_w<WM, WN, MI, NI, 3, 3, 1, 1>(p, s);

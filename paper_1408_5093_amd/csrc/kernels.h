@@ -23,9 +23,12 @@ FastDiv make_fastdiv(uint32_t d);
 // epi == 1 (data gradient, phase-stacked): row m = (c, fh, fw) and
 //   Y[n][g*Cg_out + c][psh*(i + a0h) + fh - oph][psw*(j + a0w) + fw - opw] = C
 //   for in-range positions (each output element is written exactly once).
+// Xmask (epi 1 only, may be null): a tensor laid out like X; gathered values
+// are taken as 0 wherever Xmask is not > 0 (the fused ReLU backward).
 struct ConvGemmParams {
     const void* A;
     const void* X;
+    const void* Xmask;
     float* Y;
     const float* bias;
     uint32_t A_bytes, X_bytes, Y_bytes;
@@ -41,10 +44,15 @@ struct ConvGemmParams {
 
 // Split-K weight gradient:
 //   P[s][g*Kg + m][r] = sum_{col in split s} D[n][g*Kg + m][i][j] * X[n][g*Cg + c][i*sh - ph + u][j*sw - pw + v]
+// D is read as Dmask > 0 ? D : 0 when Dmask is given (the fused ReLU
+// backward).  When dbp is given, the workgroups of the first tap tile also
+// write dbp[s][g*Kg + m] = sum_{col in split s} D (the bias-gradient partials).
 struct WgradParams {
     const void* D;
+    const void* Dmask;
     const void* X;
     float* P;
+    float* dbp;
     uint32_t D_bytes, X_bytes, P_bytes;
     int N, C, IH, IW, Cg, K, Kg;
     int kh, kw, sh, sw, ph, pw;
@@ -60,9 +68,7 @@ enum GemmTile : int {
     TILE_96x256 = 1,       // 32x32x2 MFMA, 4 waves as 1x4, each 96x64
     TILE_48x256 = 2,       // 16x16x4 MFMA, 4 waves as 1x4, each 48x64
     TILE_64x256 = 3,       // 32x32x2 MFMA, 4 waves as 1x4, each 64x64
-    TILE_128x256 = 4,      // 32x32x2 MFMA, 4 waves as 2x2, each 64x128
-    TILE_256x128 = 5,      // 32x32x2 MFMA, 4 waves as 2x2, each 128x64
-    TILE_128x128_K32 = 6,  // as TILE_128x128 with 32-deep stages
+    TILE_128x128_K32 = 4,  // as TILE_128x128 with 32-deep stages
     TILE_COUNT
 };
 int gemm_tile_m(int tile);

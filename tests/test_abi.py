@@ -102,18 +102,18 @@ def test_tensor_size_limit():
 
 def test_workspace_sizes():
     d = cc.conv_desc((256, 3, 227, 227), (96, 3, 11, 11), 4, 0, 1, True)
-    assert cc.conv_workspace_size(d, cc.PASS_FORWARD) == 0
-    data = cc.conv_workspace_size(d, cc.PASS_BACKWARD_DATA)
-    wts = cc.conv_workspace_size(d, cc.PASS_BACKWARD_WEIGHTS)
-    both = cc.conv_workspace_size(d, cc.PASS_BACKWARD)
-    top_bytes = 256 * 96 * 55 * 55 * 4
-    assert data >= top_bytes and wts >= top_bytes  # masked diff lives in the workspace
-    assert both >= max(data, wts)
-    for v in (data, wts, both):
-        assert v % 256 == 0
-    d.relu = 0
-    assert cc.conv_workspace_size(d, cc.PASS_BACKWARD) < both
-
+    assert cc.conv_workspace_size(d, cc.PASS_FORWARD) == 0  # 3 channels: no packed weights
+    d2 = cc.conv_desc((256, 96, 27, 27), (256, 48, 5, 5), 1, 2, 2, True)
+    assert cc.conv_workspace_size(d2, cc.PASS_FORWARD) >= 256 * 48 * 25 * 4  # packed weights
+    for desc in (d, d2):
+        data = cc.conv_workspace_size(desc, cc.PASS_BACKWARD_DATA)
+        wts = cc.conv_workspace_size(desc, cc.PASS_BACKWARD_WEIGHTS)
+        both = cc.conv_workspace_size(desc, cc.PASS_BACKWARD)
+        assert both >= max(data, wts)
+        for v in (data, wts, both):
+            assert v % 256 == 0
+        # the ReLU mask is fused: no copy of the top gradient in the workspace
+        assert both < desc.N * desc.K * 27 * 27 * 4
 
 def test_pointer_checks_before_any_launch():
     lib = cc.load()

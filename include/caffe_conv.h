@@ -126,14 +126,28 @@ int caffe_conv_backward_weights(const caffe_conv_desc* desc, const float* top_di
                                 float* bias_diff, int32_t accumulate, void* workspace,
                                 size_t ws_bytes, void* stream);
 
+/* Flags of caffe_conv_backward: they let a network fold the backward pass of
+ * the ReLUs around a layer into the neighbouring layers' kernels instead of
+ * running it as a pass of its own. */
+enum caffe_backward_flags {
+    /* top_diff is already zero wherever top <= 0: the fused ReLU's backward
+     * was applied by whoever produced top_diff.  top is then not read. */
+    CAFFE_BACKWARD_TOP_DIFF_MASKED = 1,
+    /* bottom_diff is stored multiplied by [bottom > 0]: the backward pass of
+     * a ReLU whose output is this layer's bottom, fused into the data
+     * gradient.  Needs bottom (CAFFE_F32 only). */
+    CAFFE_BACKWARD_MASK_BOTTOM_DIFF = 2
+};
+
 /* The whole backward pass of the layer in one call: the ReLU mask is applied
  * once and shared by both gradients.  Any of bottom_diff, weight_diff,
  * bias_diff may be NULL to skip it; bottom is required iff weight_diff is
- * given, weight iff bottom_diff is given.  accumulate applies to
- * weight_diff and bias_diff only. */
+ * given or flags has CAFFE_BACKWARD_MASK_BOTTOM_DIFF, weight iff bottom_diff
+ * is given.  accumulate applies to weight_diff and bias_diff only; flags is a
+ * set of caffe_backward_flags. */
 int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, const float* top,
                         const void* bottom, const void* weight, float* bottom_diff,
-                        float* weight_diff, float* bias_diff, int32_t accumulate,
+                        float* weight_diff, float* bias_diff, int32_t accumulate, int32_t flags,
                         void* workspace, size_t ws_bytes, void* stream);
 
 /* Static name of a status code ("CAFFE_OK", ...). */

@@ -11,9 +11,10 @@
  * likewise); top[n,c,i,j] = max over rows i*sh - ph .. i*sh - ph + kh - 1 and
  * the matching columns, clipped to the image.  Ties go to the first maximum
  * in row-major window order.  `mask` (int32, N x C x Ho x Wo) records the
- * winner as h * W + w within its plane; the backward pass sends each
- * top_diff element to that position and sums what arrives (overwriting
- * bottom_diff).  pad must be smaller than the kernel.
+ * winner as h * W + w within its plane (or -1, see CAFFE_POOL_RELU_INPUT);
+ * the backward pass sends each top_diff element to that position and sums
+ * what arrives (overwriting bottom_diff).  pad must be smaller than the
+ * kernel.
  *
  * Local response normalisation across channels:
  *   s_c = k + (alpha / local_size) * sum_{c' in win(c)} bottom_{c'}^2
@@ -53,9 +54,19 @@ typedef struct caffe_lrn_desc {
 /* Host-only. */
 int caffe_pool_out_shape(const caffe_pool_desc* desc, int32_t* Ho, int32_t* Wo);
 
-/* mask may be NULL when no backward pass will follow. */
+/* Flags of caffe_maxpool_forward. */
+enum caffe_pool_flags {
+    /* bottom is the output of a ReLU: a window whose maximum is not > 0
+     * records mask -1 (no winner), so the backward pass also applies that
+     * ReLU's backward (it routes nothing where the ReLU's output was 0).
+     * top is unchanged. */
+    CAFFE_POOL_RELU_INPUT = 1
+};
+
+/* mask may be NULL when no backward pass will follow; flags is a set of
+ * caffe_pool_flags. */
 int caffe_maxpool_forward(const caffe_pool_desc* desc, const float* bottom, float* top,
-                          int32_t* mask, void* stream);
+                          int32_t* mask, int32_t flags, void* stream);
 
 int caffe_maxpool_backward(const caffe_pool_desc* desc, const float* top_diff,
                            const int32_t* mask, float* bottom_diff, void* stream);

@@ -15,8 +15,9 @@ import torch
 
 from . import _lib
 from ._lib import (  # noqa: F401
-    CAFFE_BF16, CAFFE_F32, PASS_BACKWARD, PASS_BACKWARD_DATA, PASS_BACKWARD_WEIGHTS, PASS_FORWARD,
-    CaffeError, ConvDesc, LrnDesc, PoolDesc, check, load, LIB_PATH,
+    BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED, CAFFE_BF16, CAFFE_F32, PASS_BACKWARD,
+    PASS_BACKWARD_DATA, PASS_BACKWARD_WEIGHTS, PASS_FORWARD, POOL_RELU_INPUT, CaffeError, ConvDesc,
+    LrnDesc, PoolDesc, check, load, LIB_PATH,
 )
 
 __all__ = [
@@ -104,7 +105,7 @@ def caffe_conv_forward(desc, bottom, weight, bias, top, workspace=None, stream=N
 
 
 def caffe_conv_backward(desc, top_diff, top, bottom, weight, bottom_diff, weight_diff, bias_diff,
-                        accumulate=0, workspace=None, stream=None):
+                        accumulate=0, flags=0, workspace=None, stream=None):
     t = _op_dtype(desc)
     for x, n in ((top_diff, "top_diff"), (top, "top"), (bottom_diff, "bottom_diff"),
                  (weight_diff, "weight_diff"), (bias_diff, "bias_diff")):
@@ -113,8 +114,8 @@ def caffe_conv_backward(desc, top_diff, top, bottom, weight, bottom_diff, weight
     ws_bytes = 0 if workspace is None else workspace.numel()
     check(load().caffe_conv_backward(ctypes.byref(desc), _ptr(top_diff), _ptr(top), _ptr(bottom),
                                      _ptr(weight), _ptr(bottom_diff), _ptr(weight_diff),
-                                     _ptr(bias_diff), int(accumulate), _ptr(workspace), ws_bytes,
-                                     _stream(stream)))
+                                     _ptr(bias_diff), int(accumulate), int(flags), _ptr(workspace),
+                                     ws_bytes, _stream(stream)))
 
 
 def caffe_conv_backward_data(desc, top_diff, top, weight, bottom_diff, workspace=None, stream=None):
@@ -152,7 +153,7 @@ def conv_forward(x, w, b=None, stride=1, pad=0, group=1, relu=False, out=None, w
 
 
 def conv_backward(x, w, top_diff, top=None, stride=1, pad=0, group=1, relu=False,
-                  need=("dx", "dw", "db"), accumulate=0, outs=None, ws=None):
+                  need=("dx", "dw", "db"), accumulate=0, outs=None, ws=None, flags=0):
     """Returns (dx, dw, db), None where not requested."""
     dtype = CAFFE_BF16 if x.dtype == torch.bfloat16 else CAFFE_F32
     d = conv_desc(x.shape, w.shape, stride, pad, group, relu, dtype)
@@ -164,8 +165,9 @@ def conv_backward(x, w, top_diff, top=None, stride=1, pad=0, group=1, relu=False
     else:
         dx, dw, db = outs
     buf = (ws or Workspace(dev)).get(conv_workspace_size(d, PASS_BACKWARD))
-    caffe_conv_backward(d, top_diff, top, x if dw is not None else None,
-                        w if dx is not None else None, dx, dw, db, accumulate, buf)
+    need_x = dw is not None or (flags & BACKWARD_MASK_BOTTOM_DIFF)
+    caffe_conv_backward(d, top_diff, top, x if need_x else None, w if dx is not None else None,
+                        dx, dw, db, accumulate, flags, buf)
     return dx, dw, db
 
 
@@ -204,7 +206,8 @@ def pool_out_shape(desc):
     return Ho.value, Wo.value
 
 
-def maxpool_forward(x, kernel, stride, pad=0, out=None, mask=None, with_mask=True, stream=None):
+def maxpool_forward(x, kernel, stride, pad=0, out=None, mask=None, with_mask=True, flags=0,
+                    stream=None):
     _dev(x, "bottom", torch.float32)
     d = pool_desc(x.shape, kernel, stride, pad)
     Ho, Wo = pool_out_shape(d)
@@ -213,7 +216,7 @@ def maxpool_forward(x, kernel, stride, pad=0, out=None, mask=None, with_mask=Tru
     if mask is None and with_mask:
         mask = torch.empty((d.N, d.C, Ho, Wo), dtype=torch.int32, device=x.device)
     _dev(out, "top", torch.float32), _dev(mask, "mask", torch.int32)
-    check(load().caffe_maxpool_forward(ctypes.byref(d), _ptr(x), _ptr(out), _ptr(mask),
+    check(load().caffe_maxpool_forward(ctypes.byref(d), _ptr(x), _ptr(out), _ptr(mask), int(flags),
                                        _stream(stream)))
     return out, mask
 

@@ -20,6 +20,10 @@ CAFFE_ERR_HIP = -5
 CAFFE_F32 = 0
 CAFFE_BF16 = 1
 
+BACKWARD_TOP_DIFF_MASKED = 1
+BACKWARD_MASK_BOTTOM_DIFF = 2
+POOL_RELU_INPUT = 1
+
 PASS_FORWARD = 0
 PASS_BACKWARD_DATA = 1
 PASS_BACKWARD_WEIGHTS = 2
@@ -83,9 +87,9 @@ def load():
         "caffe_conv_forward": [cdp, vp, vp, vp, vp, vp, sz, vp],
         "caffe_conv_backward_data": [cdp, vp, vp, vp, vp, vp, sz, vp],
         "caffe_conv_backward_weights": [cdp, vp, vp, vp, vp, vp, i32, vp, sz, vp],
-        "caffe_conv_backward": [cdp, vp, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp],
+        "caffe_conv_backward": [cdp, vp, vp, vp, vp, vp, vp, vp, i32, i32, vp, sz, vp],
         "caffe_pool_out_shape": [pdp, pi32, pi32],
-        "caffe_maxpool_forward": [pdp, vp, vp, vp, vp],
+        "caffe_maxpool_forward": [pdp, vp, vp, vp, i32, vp],
         "caffe_maxpool_backward": [pdp, vp, vp, vp, vp],
         "caffe_lrn_forward": [ldp, vp, vp, vp],
         "caffe_lrn_backward": [ldp, vp, vp, vp, vp, vp],

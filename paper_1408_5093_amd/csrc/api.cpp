@@ -202,17 +202,18 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     q.dgrad_tap = q.Kg % gemm_tile_k(q.dgrad_tile) == 0;
     q.ws_fwd = q.fwd_tap ? align_up(q.weight_elems * 4, kWsAlign) : 0;
 
-    // Workspace: [bias partial sums][transformed weights][weight partials].
-    // The ReLU mask is applied inside the gradient kernels, so the masked
-    // top gradient is never stored.
+    // Workspace: [masked top diff][bias partial sums][transformed weights]
+    // [weight partials].  The masked top diff is written only when relu is
+    // set and the caller has not masked top_diff already.
+    const size_t d_bytes = q.relu ? align_up(q.top_elems * 4, kWsAlign) : 0;
     const size_t sums_bytes =
         align_up((size_t)std::max<int64_t>(q.N, q.splits) * q.K * 4, kWsAlign);
     const size_t wt_bytes = align_up(wt_elems * 4, kWsAlign);
     q.off_d = 0;
-    q.off_sums = 0;
+    q.off_sums = d_bytes;
     q.off_wt = q.off_sums + sums_bytes;
     q.off_part = q.off_wt + wt_bytes;
-    q.ws_data = sums_bytes + wt_bytes;
+    q.ws_data = q.off_part;
     q.ws_weights = q.off_part + align_up(part_bytes, kWsAlign);
     q.ws_both = q.ws_weights;
     return CAFFE_OK;
@@ -293,20 +294,20 @@ int run_forward(const ConvPlan& q, const void* bottom, const void* weight, const
 
 // Bias gradient without a weight gradient: per-(n, k) plane sums of the
 // masked top gradient, reduced over n in order.
-int run_bias_only(const ConvPlan& q, const float* top_diff, const float* top, float* bias_diff,
-                  int accumulate, char* ws, hipStream_t s)
+int run_bias_only(const ConvPlan& q, const float* top_diff, const float* top, bool masked,
+                  float* bias_diff, int accumulate, char* ws, hipStream_t s)
 {
     float* sums = (float*)(ws + q.off_sums);
     if (q.N > 0)
         LAUNCH(launch_relu_mask_bias(top_diff, top, nullptr, sums, q.N * q.K, q.Ho * q.Wo,
-                                     q.relu, s),
+                                     q.relu && !masked, s),
                "bias launch");
     LAUNCH(launch_wgrad_reduce(nullptr, nullptr, 0, 0, sums, bias_diff, q.N, q.K, accumulate, s),
            "bias reduce launch");
     return CAFFE_OK;
 }
 
-int run_data(const ConvPlan& q, const float* top_diff, const float* top, const void* weight,
+int run_data(const ConvPlan& q, const float* dsrc, const float* bottom_mask, const void* weight,
              float* bottom_diff, char* ws, hipStream_t s)
 {
     if (q.bottom_elems == 0)
@@ -317,8 +318,8 @@ int run_data(const ConvPlan& q, const float* top_diff, const float* top, const v
            "weight transform launch");
     ConvGemmParams p = {};
     p.A = wt;
-    p.X = top_diff;
-    p.Xmask = q.relu ? top : nullptr;
+    p.X = dsrc;
+    p.Omask = bottom_mask;
     p.Y = bottom_diff;
     p.bias = nullptr;
     p.A_bytes = nbytes((int64_t)q.G * q.Mt * q.Rt, 4);
@@ -338,14 +339,13 @@ int run_data(const ConvPlan& q, const float* top_diff, const float* top, const v
     return CAFFE_OK;
 }
 
-int run_weights(const ConvPlan& q, const float* top_diff, const float* top, const void* bottom,
-                float* weight_diff, float* bias_diff, int accumulate, char* ws, hipStream_t s)
+int run_weights(const ConvPlan& q, const float* dsrc, const void* bottom, float* weight_diff,
+                float* bias_diff, int accumulate, char* ws, hipStream_t s)
 {
     float* part = (float*)(ws + q.off_part);
     float* sums = (float*)(ws + q.off_sums);
     WgradParams p = {};
-    p.D = top_diff;
-    p.Dmask = q.relu ? top : nullptr;
+    p.D = dsrc;
     p.X = bottom;
     p.P = part;
     p.dbp = bias_diff ? sums : nullptr;
@@ -433,16 +433,20 @@ int caffe_conv_forward(const caffe_conv_desc* desc, const void* bottom, const vo
 
 int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, const float* top,
                         const void* bottom, const void* weight, float* bottom_diff,
-                        float* weight_diff, float* bias_diff, int32_t accumulate,
+                        float* weight_diff, float* bias_diff, int32_t accumulate, int32_t flags,
                         void* workspace, size_t ws_bytes, void* stream)
 {
     ConvPlan q;
     CHECK(plan_conv(desc, &q));
     if (accumulate != 0 && accumulate != 1)
         return fail(CAFFE_ERR_INVALID_ARG, "accumulate must be 0 or 1");
+    if (flags & ~(CAFFE_BACKWARD_TOP_DIFF_MASKED | CAFFE_BACKWARD_MASK_BOTTOM_DIFF))
+        return fail(CAFFE_ERR_INVALID_ARG, "unknown backward flags 0x%x", flags);
+    const bool masked = (flags & CAFFE_BACKWARD_TOP_DIFF_MASKED) != 0;
+    const bool mask_bottom = (flags & CAFFE_BACKWARD_MASK_BOTTOM_DIFF) != 0 && bottom_diff;
     CHECK(check_conv_ptrs(q, top_diff, true, true, "top_diff"));
-    CHECK(check_conv_ptrs(q, top, q.relu != 0, true, "top"));
-    CHECK(check_conv_ptrs(q, bottom, weight_diff != nullptr, true, "bottom"));
+    CHECK(check_conv_ptrs(q, top, q.relu != 0 && !masked, true, "top"));
+    CHECK(check_conv_ptrs(q, bottom, weight_diff != nullptr || mask_bottom, true, "bottom"));
     CHECK(check_conv_ptrs(q, weight, bottom_diff != nullptr, false, "weight"));
     CHECK(check_conv_ptrs(q, bottom_diff, false, true, "bottom_diff"));
     CHECK(check_conv_ptrs(q, weight_diff, false, false, "weight_diff"));
@@ -453,12 +457,21 @@ int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, cons
         return fail(CAFFE_ERR_UNSUPPORTED, "bf16 backward is not built yet");
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
+    const float* dsrc = top_diff;
+    if (q.relu && !masked && (bottom_diff || weight_diff) && q.top_elems > 0) {
+        // D = top_diff [top > 0], shared by both gradients
+        float* D = (float*)(ws + q.off_d);
+        LAUNCH(launch_relu_mask_bias(top_diff, top, D, nullptr, q.N * q.K, q.Ho * q.Wo, 1, s),
+               "ReLU backward launch");
+        dsrc = D;
+    }
     if (bottom_diff)
-        CHECK(run_data(q, top_diff, top, weight, bottom_diff, ws, s));
+        CHECK(run_data(q, dsrc, mask_bottom ? (const float*)bottom : nullptr, weight, bottom_diff,
+                       ws, s));
     if (weight_diff)
-        CHECK(run_weights(q, top_diff, top, bottom, weight_diff, bias_diff, accumulate, ws, s));
+        CHECK(run_weights(q, dsrc, bottom, weight_diff, bias_diff, accumulate, ws, s));
     else if (bias_diff)
-        CHECK(run_bias_only(q, top_diff, top, bias_diff, accumulate, ws, s));
+        CHECK(run_bias_only(q, top_diff, top, masked, bias_diff, accumulate, ws, s));
     return CAFFE_OK;
 }
 
@@ -470,7 +483,7 @@ int caffe_conv_backward_data(const caffe_conv_desc* desc, const float* top_diff,
     CHECK(plan_conv(desc, &q));
     CHECK(check_conv_ptrs(q, bottom_diff, true, true, "bottom_diff"));
     return caffe_conv_backward(desc, top_diff, top, nullptr, weight, bottom_diff, nullptr, nullptr,
-                               0, workspace, ws_bytes, stream);
+                               0, 0, workspace, ws_bytes, stream);
 }
 
 int caffe_conv_backward_weights(const caffe_conv_desc* desc, const float* top_diff,
@@ -482,7 +495,7 @@ int caffe_conv_backward_weights(const caffe_conv_desc* desc, const float* top_di
     CHECK(plan_conv(desc, &q));
     CHECK(check_conv_ptrs(q, weight_diff, true, false, "weight_diff"));
     return caffe_conv_backward(desc, top_diff, top, bottom, nullptr, nullptr, weight_diff,
-                               bias_diff, accumulate, workspace, ws_bytes, stream);
+                               bias_diff, accumulate, 0, workspace, ws_bytes, stream);
 }
 
 const char* caffe_status_string(int32_t status)
@@ -536,8 +549,10 @@ int caffe_pool_out_shape(const caffe_pool_desc* desc, int32_t* Ho, int32_t* Wo)
 }
 
 int caffe_maxpool_forward(const caffe_pool_desc* d, const float* bottom, float* top,
-                          int32_t* mask, void* stream)
+                          int32_t* mask, int32_t flags, void* stream)
 {
+    if (flags & ~CAFFE_POOL_RELU_INPUT)
+        return fail(CAFFE_ERR_INVALID_ARG, "unknown pooling flags 0x%x", flags);
     int Ho, Wo;
     CHECK(plan_pool(d, &Ho, &Wo));
     const bool nz = d->N > 0;
@@ -546,7 +561,7 @@ int caffe_maxpool_forward(const caffe_pool_desc* d, const float* bottom, float* 
     CHECK(check_ptr(mask, false, "mask"));
     LAUNCH(launch_maxpool_forward(bottom, top, mask, d->N * d->C, d->H, d->W, Ho, Wo, d->kernel_h,
                                   d->kernel_w, d->stride_h, d->stride_w, d->pad_h, d->pad_w,
-                                  (hipStream_t)stream),
+                                  (flags & CAFFE_POOL_RELU_INPUT) ? 1 : 0, (hipStream_t)stream),
            "max-pool forward launch");
     return CAFFE_OK;
 }

@@ -102,7 +102,6 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
 
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.A, p.A_bytes);
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, p.X_bytes);
-    const __amdgpu_buffer_rsrc_t rxm = make_rsrc(MASK ? p.Xmask : p.X, p.X_bytes);
 
     // ---- A mapping: k = tid % TK, m = tid / TK + (NT / TK) * q
     const int a_k = tid % TK;
@@ -134,7 +133,6 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     auto b_cc = [&](int q) { return TN > NT ? q % BC : 0; };
 
     float rA[EA], rB[EB];
-    float rM[MASK ? EB : 1];  // ReLU-mask values matching rB (MASK only)
 
     auto load_a = [&](int kbase) {
 #pragma unroll
@@ -163,8 +161,6 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
         for (int q = 0; q < EB; ++q) {
             const uint32_t coff = (uint32_t)((c0 + b_row(q)) * IHW) * 4u;
             rB[q] = buf_ld_f32(rx, voff[b_cc(q)] + coff);
-            if constexpr (MASK)
-                rM[q] = buf_ld_f32(rxm, voff[b_cc(q)] + coff);
         }
     };
 
@@ -183,8 +179,6 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
             const bool ok = r < R && (unsigned)ih < (unsigned)IH && (unsigned)iw < (unsigned)IW;
             const uint32_t off = ok ? (uint32_t)(b_base[cc] + c * IHW + u * IW + v) * 4u : kOob;
             rB[q] = buf_ld_f32(rx, off);
-            if constexpr (MASK)
-                rM[q] = buf_ld_f32(rxm, off);
         }
     };
 
@@ -195,10 +189,7 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
 #pragma unroll
         for (int q = 0; q < EB; ++q) {
             const int col = TN > NT ? tid + NT * b_cc(q) : tid % TN;
-            float v = rB[q];
-            if constexpr (MASK)
-                v = rM[q] > 0.f ? v : 0.f;
-            Bs[buf][b_row(q)][col] = v;
+            Bs[buf][b_row(q)][col] = rB[q];
         }
     };
 
@@ -334,6 +325,7 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     } else {
         const int pss = p.psh * p.psw;
         const int OutHW = p.OutH * p.OutW;
+        const __amdgpu_buffer_rsrc_t rom = make_rsrc(MASK ? p.Omask : p.Y, p.Y_bytes);
         int cb[NI], hb[NI], wb[NI];
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni) {
@@ -369,7 +361,14 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
                                          << 31;
                     const uint32_t off =
                         ((uint32_t)(cb[ni] + c * OutHW + h * p.OutW + w) * 4u) | bad;
-                    buf_st_f32(acc[mi][ni][q], ry, off);
+                    float v = acc[mi][ni][q];
+                    if constexpr (MASK) {
+                        // backward of the ReLU that produced the gather target:
+                        // keep the gradient only where that output was > 0
+                        const float y = buf_ld_f32(rom, off);
+                        v = y > 0.f ? v : 0.f;
+                    }
+                    buf_st_f32(v, ry, off);
                 }
             }
         }
@@ -489,7 +488,7 @@ hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool
         return hipErrorInvalidValue;
     if (epi == 0)
         return launch_tile<0, false>(p, tile, tap_major, s);
-    return p.Xmask ? launch_tile<1, true>(p, tile, tap_major, s)
+    return p.Omask ? launch_tile<1, true>(p, tile, tap_major, s)
                    : launch_tile<1, false>(p, tile, tap_major, s);
 }
 

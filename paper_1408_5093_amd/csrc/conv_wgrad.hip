@@ -22,7 +22,7 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t x, const FastDiv& f)
     return (uint32_t)(((uint64_t)x * f.mul) >> f.shift);
 }
 
-template <int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH, int SW, bool MASK>
+template <int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH, int SW>
 __global__ void __launch_bounds__(64 * WM * WN)
 conv_wgrad_f32_kernel(const WgradParams p)
 {
@@ -62,7 +62,7 @@ conv_wgrad_f32_kernel(const WgradParams p)
     const int col_end = min(p.Ncol, col_begin + p.cols_per_split);
 
     const __amdgpu_buffer_rsrc_t rd = make_rsrc(p.D, p.D_bytes);
-    const __amdgpu_buffer_rsrc_t rdm = make_rsrc(MASK ? p.Dmask : p.D, p.D_bytes);
+
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, p.X_bytes);
 
     const int kc = tid % TK;  // reduction index within a stage
@@ -99,7 +99,6 @@ conv_wgrad_f32_kernel(const WgradParams p)
     }
 
     float rA[EA], rB[EB];
-    float rM[MASK ? EA : 1];  // ReLU-mask values matching rA (MASK only)
     // bias-gradient partials: in the first tap tile's workgroups, thread t < TM
     // owns row t and adds the staged (masked) diff of its row, stage by stage
     const bool want_db = p.dbp != nullptr && blockIdx.x == 0;
@@ -128,8 +127,6 @@ conv_wgrad_f32_kernel(const WgradParams p)
             const uint32_t off =
                 ((uint32_t)(dbase + a_off0 + RS * q * OHW) * 4u) | cbad | bad;
             rA[q] = buf_ld_f32(rd, off);
-            if constexpr (MASK)
-                rM[q] = buf_ld_f32(rdm, off);
         }
 #pragma unroll
         for (int q = 0; q < EB; ++q) {
@@ -153,12 +150,8 @@ conv_wgrad_f32_kernel(const WgradParams p)
 
     auto store_stage = [&](int buf) {
 #pragma unroll
-        for (int q = 0; q < EA; ++q) {
-            float v = rA[q];
-            if constexpr (MASK)
-                v = rM[q] > 0.f ? v : 0.f;
-            As[buf][kc][rw + RS * q] = v;
-        }
+        for (int q = 0; q < EA; ++q)
+            As[buf][kc][rw + RS * q] = rA[q];
 #pragma unroll
         for (int q = 0; q < EB; ++q)
             Bs[buf][kc][rw + RS * q] = rB[q];
@@ -267,12 +260,8 @@ hipError_t launch_w(const WgradParams& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * 32, TN = WN * NI * 32;
     dim3 grid((p.R + TN - 1) / TN, (p.Kg + TM - 1) / TM, p.G * p.splits);
-    if (p.Dmask)
-        hipLaunchKernelGGL((conv_wgrad_f32_kernel<WM, WN, MI, NI, kTK, KH, KW, SH, SW, true>),
-                           grid, dim3(64 * WM * WN), 0, s, p);
-    else
-        hipLaunchKernelGGL((conv_wgrad_f32_kernel<WM, WN, MI, NI, kTK, KH, KW, SH, SW, false>),
-                           grid, dim3(64 * WM * WN), 0, s, p);
+    hipLaunchKernelGGL((conv_wgrad_f32_kernel<WM, WN, MI, NI, kTK, KH, KW, SH, SW>), grid,
+                       dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();
 }
 

@@ -23,12 +23,13 @@ FastDiv make_fastdiv(uint32_t d);
 // epi == 1 (data gradient, phase-stacked): row m = (c, fh, fw) and
 //   Y[n][g*Cg_out + c][psh*(i + a0h) + fh - oph][psw*(j + a0w) + fw - opw] = C
 //   for in-range positions (each output element is written exactly once).
-// Xmask (epi 1 only, may be null): a tensor laid out like X; gathered values
-// are taken as 0 wherever Xmask is not > 0 (the fused ReLU backward).
+// Omask (epi 1 only, may be null): a float tensor laid out like Y; each
+// result is stored as 0 wherever Omask is not > 0 (the backward of a ReLU
+// whose output the gradient flows into).
 struct ConvGemmParams {
     const void* A;
     const void* X;
-    const void* Xmask;
+    const float* Omask;
     float* Y;
     const float* bias;
     uint32_t A_bytes, X_bytes, Y_bytes;
@@ -44,12 +45,10 @@ struct ConvGemmParams {
 
 // Split-K weight gradient:
 //   P[s][g*Kg + m][r] = sum_{col in split s} D[n][g*Kg + m][i][j] * X[n][g*Cg + c][i*sh - ph + u][j*sw - pw + v]
-// D is read as Dmask > 0 ? D : 0 when Dmask is given (the fused ReLU
-// backward).  When dbp is given, the workgroups of the first tap tile also
-// write dbp[s][g*Kg + m] = sum_{col in split s} D (the bias-gradient partials).
+// When dbp is given, the workgroups of the first tap tile also write
+// dbp[s][g*Kg + m] = sum_{col in split s} D (the bias-gradient partials).
 struct WgradParams {
     const void* D;
-    const void* Dmask;
     const void* X;
     float* P;
     float* dbp;
@@ -121,9 +120,11 @@ hipError_t launch_wgrad_reduce(const float* P, float* out, int count, int splits
 hipError_t launch_fill_zero(float* out, int64_t count, hipStream_t s);
 
 // Glue layers (layers.hip).
+// relu_input: windows whose maximum is not > 0 record mask -1 (no winner),
+// so the backward pass routes them nothing.
 hipError_t launch_maxpool_forward(const float* x, float* y, int32_t* mask, int NC, int H, int W,
                                   int OH, int OW, int kh, int kw, int sh, int sw, int ph, int pw,
-                                  hipStream_t s);
+                                  int relu_input, hipStream_t s);
 hipError_t launch_maxpool_backward(const float* dy, const int32_t* mask, float* dx, int NC, int H,
                                    int W, int OH, int OW, int kh, int kw, int sh, int sw, int ph,
                                    int pw, hipStream_t s);

@@ -22,7 +22,7 @@ template <int KS, int SS>
 __global__ void __launch_bounds__(256)
 maxpool_forward_kernel(const float* __restrict__ x, float* __restrict__ y,
                        int32_t* __restrict__ mask, int NC, int H, int W, int OH, int OW, int kh_,
-                       int kw_, int sh_, int sw_, int ph, int pw, FastDiv div_ow)
+                       int kw_, int sh_, int sw_, int ph, int pw, FastDiv div_ow, int relu_input)
 {
     const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
     const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
@@ -70,8 +70,8 @@ maxpool_forward_kernel(const float* __restrict__ x, float* __restrict__ y,
                 }
         }
         y[nc * OHW + p] = bv;
-        if (mask)
-            mask[nc * OHW + p] = best;
+        if (mask)  // a ReLU output window with no positive value routes nothing
+            mask[nc * OHW + p] = (relu_input && !(bv > 0.f)) ? -1 : best;
     }
 }
 
@@ -145,7 +145,7 @@ static dim3 plane_grid(int pixels, int planes)
 
 hipError_t launch_maxpool_forward(const float* x, float* y, int32_t* mask, int NC, int H, int W,
                                   int OH, int OW, int kh, int kw, int sh, int sw, int ph, int pw,
-                                  hipStream_t s)
+                                  int relu_input, hipStream_t s)
 {
     if ((long)NC * OH * OW == 0)
         return hipSuccess;
@@ -153,13 +153,13 @@ hipError_t launch_maxpool_forward(const float* x, float* y, int32_t* mask, int N
     const dim3 grid = plane_grid(OH * OW, NC);
     if (kh == 3 && kw == 3 && sh == 2 && sw == 2)
         hipLaunchKernelGGL((maxpool_forward_kernel<3, 2>), grid, dim3(256), 0, s, x, y, mask, NC,
-                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d);
+                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d, relu_input);
     else if (kh == 2 && kw == 2 && sh == 2 && sw == 2)
         hipLaunchKernelGGL((maxpool_forward_kernel<2, 2>), grid, dim3(256), 0, s, x, y, mask, NC,
-                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d);
+                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d, relu_input);
     else
         hipLaunchKernelGGL((maxpool_forward_kernel<0, 0>), grid, dim3(256), 0, s, x, y, mask, NC,
-                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d);
+                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d, relu_input);
     return hipGetLastError();
 }
 

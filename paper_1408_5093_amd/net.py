@@ -11,7 +11,8 @@ call; this module only owns buffers and the call order.
 """
 import torch
 
-from . import (CAFFE_BF16, CAFFE_F32, PASS_BACKWARD, PASS_FORWARD, Workspace, caffe_conv_backward,
+from . import (BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED, CAFFE_BF16, CAFFE_F32,
+               PASS_BACKWARD, PASS_FORWARD, POOL_RELU_INPUT, Workspace, caffe_conv_backward,
                caffe_conv_forward, cast_f32_to_bf16, conv_desc, conv_out_shape,
                conv_workspace_size, lrn_backward, lrn_forward, maxpool_backward, maxpool_forward,
                pool_desc, pool_out_shape)
@@ -71,6 +72,25 @@ class ConvStack:
                     raise ValueError(f"layer {l} output {cur} does not feed layer {l + 1}")
         self.ws = Workspace(dev).get(ws_need)
         self.bottom = [None] * len(self.layers)
+        # Fused ReLU backward passes.  A ReLU output that feeds a max-pool gets
+        # its backward folded into the pool's routing (CAFFE_POOL_RELU_INPUT);
+        # one that feeds the next convolution directly gets it folded into
+        # that layer's data gradient (CAFFE_BACKWARD_MASK_BOTTOM_DIFF).  Either
+        # way the layer then receives an already masked top gradient.
+        n = len(self.layers)
+        self.pool_flags = [0] * n
+        self.mask_bottom = [False] * n
+        self.top_masked = [False] * n
+        for l, L in enumerate(self.layers):
+            if not L.relu:
+                continue
+            st = self.stages[l]
+            if st and st[0]["kind"] == "pool":
+                self.pool_flags[l] = POOL_RELU_INPUT
+                self.top_masked[l] = True
+            elif not st and l + 1 < n:
+                self.mask_bottom[l + 1] = True
+                self.top_masked[l] = True
         # when a list, (tag, event) pairs are recorded around every conv call
         self.events = None
 
@@ -97,8 +117,9 @@ class ConvStack:
                 p = st["prm"]
                 st["x"] = cur
                 if st["kind"] == "pool":
+                    flags = self.pool_flags[l] if st is self.stages[l][0] else 0
                     maxpool_forward(cur, p["kernel"], p["stride"], p.get("pad", 0), out=st["y"],
-                                    mask=st["mask"], stream=s)
+                                    mask=st["mask"], flags=flags, stream=s)
                 else:
                     lrn_forward(cur, p["size"], p["alpha"], p["beta"], p["k"], out=st["y"],
                                 stream=s)
@@ -122,10 +143,15 @@ class ConvStack:
                                      p["k"], out=st["dx"], stream=s)
             want_dx = l > 0 or data_grad_bottom
             bottom = self.bottom_op[l] if self.bf16 else self.bottom[l]
+            flags = 0
+            if self.top_masked[l]:
+                flags |= BACKWARD_TOP_DIFF_MASKED
+            if self.mask_bottom[l] and want_dx:
+                flags |= BACKWARD_MASK_BOTTOM_DIFF
             self._mark(("bwd", l, "begin"), s)
             caffe_conv_backward(self.descs[l], g, self.top[l] if L.relu else None, bottom,
                                 self.W[l], self.dbottom[l] if want_dx else None, self.dW[l],
-                                self.db[l], 0, self.ws, s)
+                                self.db[l], 0, flags, self.ws, s)
             self._mark(("bwd", l, "end"), s)
             g = self.dbottom[l]
         return self.dbottom[0]

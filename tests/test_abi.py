@@ -105,15 +105,18 @@ def test_workspace_sizes():
     assert cc.conv_workspace_size(d, cc.PASS_FORWARD) == 0  # 3 channels: no packed weights
     d2 = cc.conv_desc((256, 96, 27, 27), (256, 48, 5, 5), 1, 2, 2, True)
     assert cc.conv_workspace_size(d2, cc.PASS_FORWARD) >= 256 * 48 * 25 * 4  # packed weights
-    for desc in (d, d2):
+    for desc, top_hw in ((d, 55 * 55), (d2, 27 * 27)):
         data = cc.conv_workspace_size(desc, cc.PASS_BACKWARD_DATA)
         wts = cc.conv_workspace_size(desc, cc.PASS_BACKWARD_WEIGHTS)
         both = cc.conv_workspace_size(desc, cc.PASS_BACKWARD)
         assert both >= max(data, wts)
         for v in (data, wts, both):
             assert v % 256 == 0
-        # the ReLU mask is fused: no copy of the top gradient in the workspace
-        assert both < desc.N * desc.K * 27 * 27 * 4
+        top_bytes = desc.N * desc.K * top_hw * 4
+        assert data >= top_bytes  # room for the masked top gradient (relu)
+        desc.relu = 0
+        assert cc.conv_workspace_size(desc, cc.PASS_BACKWARD_DATA) < top_bytes
+        desc.relu = 1
 
 def test_pointer_checks_before_any_launch():
     lib = cc.load()
@@ -126,23 +129,28 @@ def test_pointer_checks_before_any_launch():
     assert fwd(P(0x1004), P(0x2000), None, P(0x3000), None, 0, None) == -2     # misaligned
     assert fwd(P(0x1000), P(0x2000), P(0x4008), P(0x3000), None, 0, None) == -2  # bias
     bwd = lambda *a: lib.caffe_conv_backward(ctypes.byref(d), *a)
-    # relu needs top
-    assert bwd(P(0x1000), None, P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0,
+    # relu needs top (unless the top gradient comes masked)
+    assert bwd(P(0x1000), None, P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0, 0,
                P(0x100000), ws, None) == -1
     # workspace too small / NULL / misaligned
-    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0,
+    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0, 0,
                P(0x100000), ws - 1, None) == -3
-    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0,
+    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0, 0,
                None, ws, None) == -1
-    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0,
+    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0, 0,
                P(0x100080), ws, None) == -2
-    # accumulate flag
-    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 2,
+    # accumulate flag, unknown backward flags
+    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 2, 0,
                P(0x100000), ws, None) == -1
-    # weight gradient needs bottom; data gradient needs weight
-    assert bwd(P(0x1000), P(0x1800), None, P(0x3000), None, P(0x5000), None, 0,
+    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0, 4,
                P(0x100000), ws, None) == -1
-    assert bwd(P(0x1000), P(0x1800), P(0x2000), None, P(0x4000), None, None, 0,
+    # weight gradient needs bottom; data gradient needs weight; a masked
+    # bottom gradient needs bottom
+    assert bwd(P(0x1000), P(0x1800), None, P(0x3000), None, P(0x5000), None, 0, 0,
+               P(0x100000), ws, None) == -1
+    assert bwd(P(0x1000), P(0x1800), P(0x2000), None, P(0x4000), None, None, 0, 0,
+               P(0x100000), ws, None) == -1
+    assert bwd(P(0x1000), P(0x1800), None, P(0x3000), P(0x4000), None, None, 0, 2,
                P(0x100000), ws, None) == -1
     bd = lib.caffe_conv_backward_data
     assert bd(ctypes.byref(d), P(0x1000), P(0x1800), P(0x2000), None, P(0x100000), ws, None) == -1
@@ -158,8 +166,9 @@ def test_glue_validation():
     assert cc.pool_out_shape(pd) == (27, 27)
     assert cc.pool_out_shape(cc.pool_desc((2, 3, 24, 24), 2, 2)) == (12, 12)
     bad = cc.pool_desc((2, 3, 55, 55), 3, 2, 3)  # pad >= kernel
-    assert lib.caffe_maxpool_forward(ctypes.byref(bad), P(0x1000), P(0x2000), None, None) == -1
-    assert lib.caffe_maxpool_forward(ctypes.byref(pd), P(0x1004), P(0x2000), None, None) == -2
+    assert lib.caffe_maxpool_forward(ctypes.byref(bad), P(0x1000), P(0x2000), None, 0, None) == -1
+    assert lib.caffe_maxpool_forward(ctypes.byref(pd), P(0x1004), P(0x2000), None, 0, None) == -2
+    assert lib.caffe_maxpool_forward(ctypes.byref(pd), P(0x1000), P(0x2000), None, 2, None) == -1
     assert lib.caffe_maxpool_backward(ctypes.byref(pd), P(0x1000), None, P(0x2000), None) == -1
     ld = cc.lrn_desc((2, 3, 5, 5), 0)
     assert lib.caffe_lrn_forward(ctypes.byref(ld), P(0x1000), P(0x2000), None) == -1

@@ -32,9 +32,10 @@ def _geom(L):
 
 
 def check_layer_sampled(L, x, w, b, top, top_diff, dx, dw, db, images, filters, tol=TOL_F32,
-                        what=""):
+                        what="", dx_mask=None):
     """x, w, b, top_diff: the operands the GPU layer consumed (numpy);
-    top, dx, dw, db: its outputs.  dx may be None (not computed)."""
+    top, dx, dw, db: its outputs.  dx may be None (not computed).  dx_mask:
+    the data gradient was stored times this mask (a fused ReLU backward)."""
     print(f"check {what}: images {images} filters {filters}", flush=True)
     xs = x[images]
     y_ref = oracle.conv_forward(xs, w, b, L.s, L.p, L.g, L.relu)
@@ -46,6 +47,8 @@ def check_layer_sampled(L, x, w, b, top, top_diff, dx, dw, db, images, filters, 
         dx_ref, _, _ = oracle.conv_backward(xs, w, top_diff[images],
                                             top=None if topm is None else topm[images],
                                             relu=L.relu, need=("dx",), **_geom(L))
+        if dx_mask is not None:
+            dx_ref = dx_ref * dx_mask[images]
         assert_close(dx[images], dx_ref, tol, f"{what} data gradient")
     # bias gradient of every filter (the oracle's db loop alone is cheap at full size)
     _, _, db_ref = oracle.conv_backward(x, w, top_diff, top=topm, relu=L.relu, need=("db",),
@@ -130,7 +133,8 @@ def test_caffenet_training_step_full_size():
         gl = _np(net.layer_top_diff(l, g))
         check_layer_sampled(L, xl, inp["W"][l], inp["b"][l], _np(net.top[l]), gl,
                             _np(net.dbottom[l]), _np(net.dW[l]), _np(net.db[l]), images=images,
-                            filters=[0, L.K - 1], what=f"step {L.name}")
+                            filters=[0, L.K - 1], what=f"step {L.name}",
+                            dx_mask=(xl > 0) if net.mask_bottom[l] else None)
         for st in net.stages[l]:
             xin = _np(st["x"])[images]
             p = st["prm"]
@@ -139,6 +143,8 @@ def test_caffenet_training_step_full_size():
                 np.testing.assert_array_equal(_np(st["y"])[images], ref.astype(np.float32))
                 gref = oracle.maxpool_backward(xin, _np(_glue_dy(net, l, st))[images],
                                                p["kernel"], p["stride"])
+                if net.pool_flags[l] and st is net.stages[l][0]:
+                    gref = gref * (xin > 0)  # the fused backward of conv's ReLU
             else:
                 ref = oracle.lrn_forward(xin, p["size"], p["alpha"], p["beta"], p["k"])
                 assert_close(_np(st["y"])[images], ref, TOL_F32, f"{L.name} LRN forward")

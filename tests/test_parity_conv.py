@@ -169,3 +169,33 @@ def test_no_writes_outside_outputs():
     torch.cuda.synchronize()
     for buf in (ybuf, dxbuf, dwbuf, dbbuf):
         assert torch.all(buf[:band] == canary) and torch.all(buf[-band:] == canary)
+
+
+def test_backward_flags_fused_relu():
+    """CAFFE_BACKWARD_TOP_DIFF_MASKED: top_diff comes masked and top is not
+    read; CAFFE_BACKWARD_MASK_BOTTOM_DIFF: bottom_diff = adjoint(D) [bottom > 0]."""
+    rng = np.random.default_rng(21)
+    N, C, H, W, K = 2, 8, 13, 13, 24
+    x = np.maximum(rng.standard_normal((N, C, H, W)), 0).astype(np.float32)  # a ReLU output
+    w = (rng.standard_normal((K, C // 2, 3, 3)) * 0.3).astype(np.float32)
+    b = rng.standard_normal(K).astype(np.float32)
+    y_ref = oracle.conv_forward(x, w, b, 1, 1, 2, True)
+    top = y_ref.astype(np.float32)
+    gd = rng.standard_normal(top.shape).astype(np.float32)
+    dx_ref, dw_ref, db_ref = oracle.conv_backward(x, w, gd, top=top, stride=1, pad=1, group=2,
+                                                  relu=True)
+    gmasked = (gd * (top > 0)).astype(np.float32)
+    for flags in (cc.BACKWARD_TOP_DIFF_MASKED, cc.BACKWARD_MASK_BOTTOM_DIFF,
+                  cc.BACKWARD_TOP_DIFF_MASKED | cc.BACKWARD_MASK_BOTTOM_DIFF):
+        masked_in = flags & cc.BACKWARD_TOP_DIFF_MASKED
+        g_in = gmasked if masked_in else gd
+        top_in = None if masked_in else _t(top)
+        dx, dw, db = cc.conv_backward(_t(x), _t(w), _t(g_in), top_in, 1, 1, 2, True, flags=flags)
+        want_dx = dx_ref * (x > 0) if flags & cc.BACKWARD_MASK_BOTTOM_DIFF else dx_ref
+        assert_close(_np(dx), want_dx, TOL_F32, f"dx flags={flags}")
+        assert_close(_np(dw), dw_ref, TOL_F32, f"dw flags={flags}")
+        assert_close(_np(db), db_ref, TOL_F32, f"db flags={flags}")
+    # bias gradient alone from a masked top gradient
+    dx, dw, db = cc.conv_backward(_t(x), _t(w), _t(gmasked), None, 1, 1, 2, True, need=("db",),
+                                  flags=cc.BACKWARD_TOP_DIFF_MASKED)
+    assert_close(_np(db), db_ref, TOL_F32, "db only, masked")

@@ -75,3 +75,19 @@ def test_cast_bf16_round_to_nearest_even():
     # torch's own float -> bfloat16 conversion also rounds to nearest even
     ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
     np.testing.assert_array_equal(got, ref)
+
+
+def test_maxpool_relu_input_flag():
+    """CAFFE_POOL_RELU_INPUT: same forward output; the backward pass also
+    applies the backward of the ReLU that produced the input."""
+    rng = np.random.default_rng(31)
+    x = np.maximum(rng.standard_normal((2, 6, 27, 27)), 0).astype(np.float32)
+    x[0, 0, :5, :5] = 0.0  # whole windows of zeros
+    y, mask = cc.maxpool_forward(_t(x), 3, 2, 0, flags=cc.POOL_RELU_INPUT)
+    np.testing.assert_array_equal(_np(y), oracle.maxpool_forward(x, 3, 2).astype(np.float32))
+    m = _np(mask)
+    assert np.all(m[_np(y) <= 0] == -1) and np.all(m[_np(y) > 0] >= 0)
+    g = rng.standard_normal(m.shape).astype(np.float32)
+    dx = cc.maxpool_backward(x.shape, _t(g), mask, 3, 2, 0)
+    assert_close(_np(dx), oracle.maxpool_backward(x, g, 3, 2) * (x > 0), TOL_F32,
+                 "pool backward with ReLU input")

@@ -61,26 +61,28 @@ struct ConvPlan {
     size_t ws_fwd, ws_data, ws_weights, ws_both;
 };
 
-// Tile for a GEMM with M rows whose gather walks `cin_g` channels per group:
-// the least padding of M, then the larger tile; tap-major needs cin_g to be a
-// multiple of the stage depth.  `forced` >= 0 picks a tile (profiling only).
-int pick_tile(int M, int cin_g, int forced)
+// Tile for a GEMM with M rows: the least padding of M; ties go to the first
+// tile of the pass's preference order (measured: the forward pass favours
+// 64-row tiles over 96-row ones, the data gradient the reverse).  `forced`
+// >= 0 picks a tile (profiling only).
+int pick_tile(int M, bool forward, int forced)
 {
     if (forced >= 0 && forced < TILE_COUNT)
         return forced;
-    static const int candidates[] = {TILE_128x128, TILE_96x256, TILE_48x256, TILE_64x256};
-    int best = TILE_128x128;
+    static const int fwd_order[] = {TILE_128x128, TILE_64x256, TILE_96x256, TILE_48x256};
+    static const int bwd_order[] = {TILE_128x128, TILE_96x256, TILE_64x256, TILE_48x256};
+    const int* order = forward ? fwd_order : bwd_order;
+    int best = order[0];
     double best_waste = 1e30;
-    for (int t : candidates) {
+    for (int i = 0; i < 4; ++i) {
+        const int t = order[i];
         const int tm = gemm_tile_m(t);
         const double waste = (double)((M + tm - 1) / tm * tm) / M;
-        if (waste < best_waste - 1e-9 ||
-            (waste < best_waste + 1e-9 && tm > gemm_tile_m(best))) {
+        if (waste < best_waste - 1e-9) {
             best = t;
             best_waste = waste;
         }
     }
-    (void)cin_g;
     return best;
 }
 
@@ -196,8 +198,8 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     if (part_bytes > kMaxTensorBytes)
         return fail(CAFFE_ERR_UNSUPPORTED, "weight-gradient partials reach 2^31 bytes");
 
-    q.fwd_tile = pick_tile(q.Kg, q.Cg, env_tile("CAFFE_CONV_FWD_TILE"));
-    q.dgrad_tile = pick_tile(q.Mt, q.Kg, env_tile("CAFFE_CONV_DGRAD_TILE"));
+    q.fwd_tile = pick_tile(q.Kg, true, env_tile("CAFFE_CONV_FWD_TILE"));
+    q.dgrad_tile = pick_tile(q.Mt, false, env_tile("CAFFE_CONV_DGRAD_TILE"));
     q.fwd_tap = q.Cg % gemm_tile_k(q.fwd_tile) == 0;
     q.dgrad_tap = q.Kg % gemm_tile_k(q.dgrad_tile) == 0;
     q.ws_fwd = q.fwd_tap ? align_up(q.weight_elems * 4, kWsAlign) : 0;

@@ -18,12 +18,18 @@ __device__ __forceinline__ int udiv(int x, const FastDiv& f)
     return (int)(((uint64_t)(uint32_t)x * f.mul) >> f.shift);
 }
 
+// Each thread owns PPT planes at the same pixel (planes nc, nc + NCg, ...):
+// all their loads are independent, which keeps enough memory traffic in
+// flight for these short, latency-bound kernels.
+constexpr int kPoolPlanesPerThread = 4;
+
 template <int KS, int SS>
 __global__ void __launch_bounds__(256)
 maxpool_forward_kernel(const float* __restrict__ x, float* __restrict__ y,
                        int32_t* __restrict__ mask, int NC, int H, int W, int OH, int OW, int kh_,
                        int kw_, int sh_, int sw_, int ph, int pw, FastDiv div_ow, int relu_input)
 {
+    constexpr int PPT = kPoolPlanesPerThread;
     const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
     const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
     const int OHW = OH * OW;
@@ -34,48 +40,73 @@ maxpool_forward_kernel(const float* __restrict__ x, float* __restrict__ y,
     const int j = p - i * OW;
     const int hs = i * sh - ph, ws = j * sw - pw;
     const int h0 = max(hs, 0), w0 = max(ws, 0);
-    for (int nc = blockIdx.y; nc < NC; nc += gridDim.y) {
-        const float* plane = x + nc * (H * W);
-        int best = h0 * W + w0;
-        float bv = plane[best];
+    const int first = h0 * W + w0;
+    const int stride = gridDim.y;  // planes handled by one grid row
+    for (int nc0 = blockIdx.y; nc0 < NC; nc0 += stride * PPT) {
+        float bv[PPT];
+        int best[PPT];
         if constexpr (KS > 0) {
             // fixed window: every load is independent; out-of-image taps are
-            // skipped by the predicate (strict '>' keeps the first maximum)
-            float v[KS][KS];
+            // replaced by the window's first tap (strict '>' keeps the first
+            // maximum in row-major order)
+            float v[PPT][KS][KS];
 #pragma unroll
-            for (int du = 0; du < KS; ++du)
+            for (int t = 0; t < PPT; ++t) {
+                const int nc = min(nc0 + t * stride, NC - 1);
+                const float* plane = x + nc * (H * W);
+                bv[t] = plane[first];
 #pragma unroll
-                for (int dv = 0; dv < KS; ++dv) {
-                    const int h = hs + du, w = ws + dv;
-                    const bool in = (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
-                    v[du][dv] = in ? plane[h * W + w] : bv;
-                }
+                for (int du = 0; du < KS; ++du)
 #pragma unroll
-            for (int du = 0; du < KS; ++du)
-#pragma unroll
-                for (int dv = 0; dv < KS; ++dv)
-                    if (v[du][dv] > bv) {
-                        bv = v[du][dv];
-                        best = (hs + du) * W + ws + dv;
+                    for (int dv = 0; dv < KS; ++dv) {
+                        const int h = hs + du, w = ws + dv;
+                        const bool in = (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+                        v[t][du][dv] = plane[in ? h * W + w : first];
                     }
+            }
+#pragma unroll
+            for (int t = 0; t < PPT; ++t) {
+                best[t] = first;
+#pragma unroll
+                for (int du = 0; du < KS; ++du)
+#pragma unroll
+                    for (int dv = 0; dv < KS; ++dv)
+                        if (v[t][du][dv] > bv[t]) {
+                            bv[t] = v[t][du][dv];
+                            best[t] = (hs + du) * W + ws + dv;
+                        }
+            }
         } else {
             const int h1 = min(hs + kh, H), w1 = min(ws + kw, W);
-            for (int h = h0; h < h1; ++h)
-                for (int w = w0; w < w1; ++w) {
-                    const float v = plane[h * W + w];
-                    if (v > bv) {
-                        bv = v;
-                        best = h * W + w;
+#pragma unroll
+            for (int t = 0; t < PPT; ++t) {
+                const int nc = min(nc0 + t * stride, NC - 1);
+                const float* plane = x + nc * (H * W);
+                bv[t] = plane[first];
+                best[t] = first;
+                for (int h = h0; h < h1; ++h)
+                    for (int w = w0; w < w1; ++w) {
+                        const float v = plane[h * W + w];
+                        if (v > bv[t]) {
+                            bv[t] = v;
+                            best[t] = h * W + w;
+                        }
                     }
-                }
+            }
         }
-        y[nc * OHW + p] = bv;
-        if (mask)  // a ReLU output window with no positive value routes nothing
-            mask[nc * OHW + p] = (relu_input && !(bv > 0.f)) ? -1 : best;
+#pragma unroll
+        for (int t = 0; t < PPT; ++t) {
+            const int nc = nc0 + t * stride;
+            if (nc < NC) {
+                y[nc * OHW + p] = bv[t];
+                if (mask)  // a ReLU output window with no positive value routes nothing
+                    mask[nc * OHW + p] = (relu_input && !(bv[t] > 0.f)) ? -1 : best[t];
+            }
+        }
     }
 }
 
-// Gather form (one thread per input element, covering outputs visited in
+// Gather form (one thread per input position, covering outputs visited in
 // row-major order): deterministic, no atomics.  With a fixed window, at most
 // ceil(KS/SS)^2 outputs cover an input; their masks and gradients are loaded
 // unconditionally (clamped indices), then added in order where the mask
@@ -86,6 +117,7 @@ maxpool_backward_kernel(const float* __restrict__ dy, const int32_t* __restrict_
                         float* __restrict__ dx, int NC, int H, int W, int OH, int OW, int kh_,
                         int kw_, int sh_, int sw_, int ph, int pw, FastDiv div_w)
 {
+    constexpr int PPT = kPoolPlanesPerThread;
     const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
     const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
     const int HW = H * W;
@@ -99,34 +131,52 @@ maxpool_backward_kernel(const float* __restrict__ dy, const int32_t* __restrict_
     const int i1 = min(OH - 1, (h + ph) / sh);
     const int j0 = max(0, (w + pw - kw + sw) / sw);
     const int j1 = min(OW - 1, (w + pw) / sw);
-    for (int nc = blockIdx.y; nc < NC; nc += gridDim.y) {
-        const int obase = nc * (OH * OW);
-        float s = 0.f;
+    const int stride = gridDim.y;
+    for (int nc0 = blockIdx.y; nc0 < NC; nc0 += stride * PPT) {
+        float s[PPT];
         if constexpr (KS > 0) {
             constexpr int T = (KS + SS - 1) / SS;
-            int mk[T][T];
-            float g[T][T];
+            int mk[PPT][T][T];
+            float g[PPT][T][T];
 #pragma unroll
-            for (int di = 0; di < T; ++di)
+            for (int t = 0; t < PPT; ++t) {
+                const int obase = min(nc0 + t * stride, NC - 1) * (OH * OW);
 #pragma unroll
-                for (int dj = 0; dj < T; ++dj) {
-                    const int o = obase + min(i0 + di, OH - 1) * OW + min(j0 + dj, OW - 1);
-                    mk[di][dj] = mask[o];
-                    g[di][dj] = dy[o];
-                }
+                for (int di = 0; di < T; ++di)
 #pragma unroll
-            for (int di = 0; di < T; ++di)
+                    for (int dj = 0; dj < T; ++dj) {
+                        const int o = obase + min(i0 + di, OH - 1) * OW + min(j0 + dj, OW - 1);
+                        mk[t][di][dj] = mask[o];
+                        g[t][di][dj] = dy[o];
+                    }
+            }
 #pragma unroll
-                for (int dj = 0; dj < T; ++dj)
-                    if (i0 + di <= i1 && j0 + dj <= j1 && mk[di][dj] == p)
-                        s += g[di][dj];
+            for (int t = 0; t < PPT; ++t) {
+                s[t] = 0.f;
+#pragma unroll
+                for (int di = 0; di < T; ++di)
+#pragma unroll
+                    for (int dj = 0; dj < T; ++dj)
+                        if (i0 + di <= i1 && j0 + dj <= j1 && mk[t][di][dj] == p)
+                            s[t] += g[t][di][dj];
+            }
         } else {
-            for (int i = i0; i <= i1; ++i)
-                for (int j = j0; j <= j1; ++j)
-                    if (mask[obase + i * OW + j] == p)
-                        s += dy[obase + i * OW + j];
+#pragma unroll
+            for (int t = 0; t < PPT; ++t) {
+                const int obase = min(nc0 + t * stride, NC - 1) * (OH * OW);
+                s[t] = 0.f;
+                for (int i = i0; i <= i1; ++i)
+                    for (int j = j0; j <= j1; ++j)
+                        if (mask[obase + i * OW + j] == p)
+                            s[t] += dy[obase + i * OW + j];
+            }
         }
-        dx[nc * HW + p] = s;
+#pragma unroll
+        for (int t = 0; t < PPT; ++t) {
+            const int nc = nc0 + t * stride;
+            if (nc < NC)
+                dx[nc * HW + p] = s[t];
+        }
     }
 }
 
@@ -140,7 +190,9 @@ static unsigned grid_exact(long total) { return (unsigned)((total + 255) / 256);
 
 static dim3 plane_grid(int pixels, int planes)
 {
-    return dim3((unsigned)((pixels + 255) / 256), (unsigned)(planes < 65535 ? planes : 65535));
+    // y covers the planes kPoolPlanesPerThread at a time
+    const int rows = (planes + kPoolPlanesPerThread - 1) / kPoolPlanesPerThread;
+    return dim3((unsigned)((pixels + 255) / 256), (unsigned)(rows < 65535 ? rows : 65535));
 }
 
 hipError_t launch_maxpool_forward(const float* x, float* y, int32_t* mask, int NC, int H, int W,

@@ -32,9 +32,28 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--batch", type=int, default=256)
     ap.add_argument("--bf16", action="store_true", help="bfloat16 operands (N=512 workload)")
-    ap.add_argument("--cpu-images", type=int, default=48,
+    ap.add_argument("--cpu-images", type=int, default=128,
                     help="images in the CPU-oracle baseline sample (0 = skip)")
+    ap.add_argument("--calibrate-copy-mb", type=int, default=0,
+                    help="first run one plain device copy of this many MiB (a known-size "
+                         "reference for the HBM byte counters)")
     return ap.parse_args()
+
+
+def traffic_record(kernel_source):
+    """HBM bytes per launch of the dominant kernel, as measured with the
+    FETCH_SIZE / WRITE_SIZE counters and committed under profiles/ -- or None
+    when the kernel's source has changed since that measurement."""
+    import hashlib
+    here = os.path.dirname(os.path.abspath(__file__))
+    try:
+        rec = json.load(open(os.path.join(here, "profiles", "traffic.json")))
+        src = open(os.path.join(here, kernel_source), "rb").read()
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha256") != hashlib.sha256(src).hexdigest():
+        return None
+    return rec
 
 
 def caffenet_glue(wl):
@@ -116,6 +135,13 @@ def main():
     x = torch.from_numpy(inp["x"]).cuda()
     g = torch.from_numpy(inp["top_diff"]).cuda()
     stream = torch.cuda.current_stream()
+    if args.calibrate_copy_mb > 0:
+        n = args.calibrate_copy_mb * (1 << 20) // 4
+        src = torch.ones(n, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step():
         net.forward(x, stream)
@@ -162,8 +188,12 @@ def main():
     kdom = max(fwd, key=fwd.get)
     Ldom = wl.CAFFENET[kdom[1]]
     ach = Ldom.flops(N) / (fwd[kdom] * 1e-3) / 1e12
+    rec = traffic_record("paper_1408_5093_amd/csrc/conv_gemm.hip")
+    traffic = None
+    if rec and rec.get("layer") == Ldom.name and rec.get("batch") == N and not args.bf16:
+        traffic = rec["bytes_per_launch"]
     roofline = {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
-                "frac": ach / peak, "traffic": None,
+                "frac": ach / peak, "traffic": traffic,
                 "kernel": f"conv_gemm (forward, {Ldom.name})",
                 "kernel_ms": fwd[kdom], "flops_per_launch": Ldom.flops(N)}
 

@@ -271,7 +271,8 @@ int run_forward(const ConvPlan& q, const void* bottom, const void* weight, const
     const void* A = weight;
     if (q.fwd_tap) {
         float* wp = (float*)ws;
-        LAUNCH(launch_pack_weights_tap((const float*)weight, wp, q.K, q.Cg, q.kh * q.kw, s),
+        LAUNCH(launch_pack_weights_blocked((const float*)weight, wp, q.K, q.Cg, q.kh * q.kw,
+                                           gemm_tile_k(q.fwd_tile), s),
                "weight pack launch");
         A = wp;
     }
@@ -316,7 +317,8 @@ int run_data(const ConvPlan& q, const float* dsrc, const float* bottom_mask, con
         return CAFFE_OK;
     float* wt = (float*)(ws + q.off_wt);
     LAUNCH(launch_dgrad_weight_transform((const float*)weight, wt, q.G, q.Kg, q.Cg, q.kh, q.kw,
-                                         q.sh, q.sw, q.Th, q.Tw, q.dgrad_tap, s),
+                                         q.sh, q.sw, q.Th, q.Tw,
+                                         q.dgrad_tap ? gemm_tile_k(q.dgrad_tile) : 0, s),
            "weight transform launch");
     ConvGemmParams p = {};
     p.A = wt;

@@ -69,10 +69,11 @@ hipError_t launch_relu_mask_bias(const float* G, const float* Y, float* D, float
 }
 
 // Wt[g][m = (c, fh, fw)][r] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)],
-// 0 past the kernel edge; r = (k, th, tw), or r = (th, tw, k) when tap.
+// 0 past the kernel edge; r = (k, th, tw), or r = (k / tk, th, tw, k % tk)
+// when tk > 0.
 __global__ void __launch_bounds__(256)
 dgrad_weight_transform_kernel(const float* __restrict__ W, float* __restrict__ Wt, int G, int Kg,
-                              int Cg, int kh, int kw, int sh, int sw, int Th, int Tw, int tap)
+                              int Cg, int kh, int kw, int sh, int sw, int Th, int Tw, int tk)
 {
     const int Mt = Cg * sh * sw;
     const int Rt = Kg * Th * Tw;
@@ -84,10 +85,11 @@ dgrad_weight_transform_kernel(const float* __restrict__ W, float* __restrict__ W
         const int m = (int)(gm % Mt);
         const int g = (int)(gm / Mt);
         int k, t;
-        if (tap) {  // r = (th, tw, k)
-            t = r / Kg;
-            k = r - t * Kg;
-        } else {    // r = (k, th, tw)
+        if (tk > 0) {  // r = (k / tk, th, tw, k % tk)
+            const int ki = r % tk;
+            t = (r / tk) % (Th * Tw);
+            k = (r / (tk * Th * Tw)) * tk + ki;
+        } else {       // r = (k, th, tw)
             k = r / (Th * Tw);
             t = r - k * Th * Tw;
         }
@@ -105,7 +107,7 @@ dgrad_weight_transform_kernel(const float* __restrict__ W, float* __restrict__ W
 }
 
 hipError_t launch_dgrad_weight_transform(const float* W, float* Wt, int G, int Kg, int Cg, int kh,
-                                         int kw, int sh, int sw, int Th, int Tw, bool tap_major,
+                                         int kw, int sh, int sw, int Th, int Tw, int tk,
                                          hipStream_t s)
 {
     const long total = (long)G * Cg * sh * sw * Kg * Th * Tw;
@@ -115,7 +117,7 @@ hipError_t launch_dgrad_weight_transform(const float* W, float* Wt, int G, int K
     if (blocks > 4096)
         blocks = 4096;
     hipLaunchKernelGGL(dgrad_weight_transform_kernel, dim3((unsigned)blocks), dim3(256), 0, s, W,
-                       Wt, G, Kg, Cg, kh, kw, sh, sw, Th, Tw, tap_major ? 1 : 0);
+                       Wt, G, Kg, Cg, kh, kw, sh, sw, Th, Tw, tk);
     return hipGetLastError();
 }
 

@@ -92,9 +92,22 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave % WM;
     const int wn = wave / WM;
-    const int g = blockIdx.z;
-    const int m0 = blockIdx.y * TM;
-    const int n0 = blockIdx.x * TN;
+    // XCD-contiguous tile order: the hardware deals workgroups to the 8 XCDs
+    // round-robin, so workgroup L runs on XCD L % 8; tile T = (L % 8) * per_xcd
+    // + L / 8 gives each XCD a contiguous run of tiles.  Row tiles vary
+    // fastest, so the tiles that share a column block of the gathered operand
+    // run together on one XCD and share its L2.
+    const int n_mt = (p.M + TM - 1) / TM;
+    const int n_ct = (p.Ncol + TN - 1) / TN;
+    const int per_xcd = gridDim.x >> 3;
+    const int T = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if (T >= n_mt * n_ct * p.G)
+        return;
+    const int mt = T % n_mt;
+    const int ct = (T / n_mt) % n_ct;
+    const int g = T / (n_mt * n_ct);
+    const int m0 = mt * TM;
+    const int n0 = ct * TN;
     const int M = p.M, R = p.R;
     const int IH = p.IH, IW = p.IW, IHW = IH * IW;
     const int OHW = p.OH * p.OW;
@@ -145,9 +158,11 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
         }
     };
 
-    // Tap-major reduction order r = (u, v, c): Cin_g is a multiple of TK, so a
-    // stage covers TK channels of a single tap (u, v).  The tap's bounds check
-    // and address are computed once per column per stage.
+    // Channel-blocked reduction order r = (c / TK, u, v, c % TK): Cin_g is a
+    // multiple of TK, so a stage covers TK channels of a single tap (u, v);
+    // the tap's bounds check and address are computed once per column per
+    // stage.  All taps of a channel block run back to back, so a workgroup
+    // re-reads the same TK channel planes (from L1/L2) tap after tap.
     auto load_b_tap = [&](int u, int v, int c0) {
         uint32_t voff[BC];
 #pragma unroll
@@ -215,15 +230,14 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     }
 
     const int nst = (R + TK - 1) / TK;
-    // tap-major walk state: stage s covers tap (tu, tv), channels tc .. tc + TK - 1
+    // blocked walk state: stage s covers tap (tu, tv) of channels tc .. tc + TK - 1
     int tu = 0, tv = 0, tc = 0;
     auto advance = [&]() {
-        tc += TK;
-        if (tc == Cin_g) {
-            tc = 0;
-            if (++tv == kw) {
-                tv = 0;
-                ++tu;
+        if (++tv == kw) {
+            tv = 0;
+            if (++tu == kh) {
+                tu = 0;
+                tc += TK;
             }
         }
     };
@@ -375,29 +389,33 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     }
 }
 
-// Forward weights in tap-major order: Wp[o][(u*kw + v)*Cg + c] = W[o][c][u][v].
+// Forward weights in the channel-blocked order:
+// Wp[o][((c / tk) * khw + t) * tk + c % tk] = W[o][c][t], t = u*kw + v.
 __global__ void __launch_bounds__(256)
-pack_weights_tap_kernel(const float* __restrict__ W, float* __restrict__ Wp, int K, int Cg,
-                        int khw)
+pack_weights_blocked_kernel(const float* __restrict__ W, float* __restrict__ Wp, int K, int Cg,
+                            int khw, int tk)
 {
     const int total = K * Cg * khw;
     const int e = blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= total)
         return;
-    const int c = e % Cg;
-    const int t = (e / Cg) % khw;
-    const int o = e / (Cg * khw);
+    const int R = Cg * khw;
+    const int o = e / R;
+    const int r = e - o * R;
+    const int ci = r % tk;
+    const int t = (r / tk) % khw;
+    const int c = (r / (tk * khw)) * tk + ci;
     Wp[e] = W[(o * Cg + c) * khw + t];
 }
 
-hipError_t launch_pack_weights_tap(const float* W, float* Wp, int K, int Cg, int khw,
-                                   hipStream_t s)
+hipError_t launch_pack_weights_blocked(const float* W, float* Wp, int K, int Cg, int khw, int tk,
+                                       hipStream_t s)
 {
     const int total = K * Cg * khw;
     if (total == 0)
         return hipSuccess;
-    hipLaunchKernelGGL(pack_weights_tap_kernel, dim3((total + 255) / 256), dim3(256), 0, s, W, Wp,
-                       K, Cg, khw);
+    hipLaunchKernelGGL(pack_weights_blocked_kernel, dim3((total + 255) / 256), dim3(256), 0, s, W,
+                       Wp, K, Cg, khw, tk);
     return hipGetLastError();
 }
 
@@ -420,10 +438,12 @@ template <int MT, int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH
 hipError_t launch_one(const ConvGemmParams& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * MT, TN = WN * NI * MT;
-    dim3 grid((p.Ncol + TN - 1) / TN, (p.M + TM - 1) / TM, p.G);
+    const int64_t tiles =
+        (int64_t)((p.Ncol + TN - 1) / TN) * ((p.M + TM - 1) / TM) * p.G;
+    const int64_t per_xcd = (tiles + 7) / 8;  // 8 XCDs; see the kernel's tile order
     hipLaunchKernelGGL(
-        (conv_gemm_f32_kernel<MT, WM, WN, MI, NI, TK, KH, KW, SH, SW, EPI, TAP, MASK>), grid,
-        dim3(64 * WM * WN), 0, s, p);
+        (conv_gemm_f32_kernel<MT, WM, WN, MI, NI, TK, KH, KW, SH, SW, EPI, TAP, MASK>),
+        dim3((unsigned)(per_xcd * 8)), dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();
 }
 

@@ -51,10 +51,21 @@ conv_wgrad_f32_kernel(const WgradParams p)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave % WM;
     const int wn = wave / WM;
-    const int g = blockIdx.z % p.G;
-    const int split = blockIdx.z / p.G;
-    const int m0 = blockIdx.y * TM;
-    const int r0 = blockIdx.x * TN;
+    // XCD-contiguous tile order (workgroup L runs on XCD L % 8; tile
+    // T = (L % 8) * per_xcd + L / 8).  Tap tiles vary fastest, then row tiles:
+    // the workgroups sharing a split's diff rows run together on one XCD.
+    const int n_rt = (p.R + TN - 1) / TN;
+    const int n_mt = (p.Kg + TM - 1) / TM;
+    const int per_xcd = gridDim.x >> 3;
+    const int T = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if (T >= n_rt * n_mt * p.G * p.splits)
+        return;
+    const int rt = T % n_rt;
+    const int mt = (T / n_rt) % n_mt;
+    const int g = (T / (n_rt * n_mt)) % p.G;
+    const int split = T / (n_rt * n_mt * p.G);
+    const int m0 = mt * TM;
+    const int r0 = rt * TN;
     const int IH = p.IH, IW = p.IW, IHW = IH * IW;
     const int OHW = p.OH * p.OW;
 
@@ -101,7 +112,7 @@ conv_wgrad_f32_kernel(const WgradParams p)
     float rA[EA], rB[EB];
     // bias-gradient partials: in the first tap tile's workgroups, thread t < TM
     // owns row t and adds the staged (masked) diff of its row, stage by stage
-    const bool want_db = p.dbp != nullptr && blockIdx.x == 0;
+    const bool want_db = p.dbp != nullptr && rt == 0;
     float dsum = 0.f;
 
     auto load_stage = [&](int cbase) {
@@ -259,9 +270,11 @@ template <int WM, int WN, int MI, int NI, int KH, int KW, int SH, int SW>
 hipError_t launch_w(const WgradParams& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * 32, TN = WN * NI * 32;
-    dim3 grid((p.R + TN - 1) / TN, (p.Kg + TM - 1) / TM, p.G * p.splits);
-    hipLaunchKernelGGL((conv_wgrad_f32_kernel<WM, WN, MI, NI, kTK, KH, KW, SH, SW>), grid,
-                       dim3(64 * WM * WN), 0, s, p);
+    const int64_t tiles =
+        (int64_t)((p.R + TN - 1) / TN) * ((p.Kg + TM - 1) / TM) * p.G * p.splits;
+    const int64_t per_xcd = (tiles + 7) / 8;  // 8 XCDs; see the kernel's tile order
+    hipLaunchKernelGGL((conv_wgrad_f32_kernel<WM, WN, MI, NI, kTK, KH, KW, SH, SW>),
+                       dim3((unsigned)(per_xcd * 8)), dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();
 }
 

@@ -78,15 +78,15 @@ int gemm_tile_k(int tile);  // reduction depth of one pipeline stage
 // the tap-major order with some tile.
 constexpr int kGemmMinTK = 16;
 
-// tap_major: the reduction index runs r = (u, v, c) (A packed to match, see
-// launch_pack_weights_tap); needs Cin_g % gemm_tile_k(tile) == 0.  Otherwise
-// r = (c, u, v).
+// tap_major: the reduction index runs in the channel-blocked order
+// r = (c / TK, u, v, c % TK), TK = gemm_tile_k(tile) (A packed to match, see
+// launch_pack_weights_blocked); needs Cin_g % TK == 0.  Otherwise r = (c, u, v).
 hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool tap_major,
                                 hipStream_t s);
 
-// Wp[o][(u*kw + v)*Cg + c] = W[o][c][u][v]  (K rows)
-hipError_t launch_pack_weights_tap(const float* W, float* Wp, int K, int Cg, int khw,
-                                   hipStream_t s);
+// Wp[o][((c / tk) * khw + u*kw + v) * tk + c % tk] = W[o][c][u][v]  (K rows)
+hipError_t launch_pack_weights_blocked(const float* W, float* Wp, int K, int Cg, int khw, int tk,
+                                       hipStream_t s);
 
 enum WgradTile : int {
     WTILE_128x128 = 0,  // 4 waves as 2x2, each 64x64
@@ -105,10 +105,10 @@ hipError_t launch_relu_mask_bias(const float* G, const float* Y, float* D, float
                                  int planes, int plane_size, int relu, hipStream_t s);
 
 // Wt[g][(c, fh, fw)][r] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)]
-// (0 where the tap index passes the kernel edge), r = (k, th, tw), or
-// r = (th, tw, k) when tap_major.
+// (0 where the tap index passes the kernel edge), r = (k, th, tw), or the
+// channel-blocked r = (k / tk, th, tw, k % tk) when tk > 0.
 hipError_t launch_dgrad_weight_transform(const float* W, float* Wt, int G, int Kg, int Cg, int kh,
-                                         int kw, int sh, int sw, int Th, int Tw, bool tap_major,
+                                         int kw, int sh, int sw, int Th, int Tw, int tk,
                                          hipStream_t s);
 
 // out[i] = (accumulate ? out[i] : 0) + sum_{s < splits} P[s*count + i]   (fixed order)

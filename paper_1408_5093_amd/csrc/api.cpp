@@ -56,6 +56,7 @@ struct ConvPlan {
     // gathered channels per group fill whole pipeline stages
     int fwd_tile, dgrad_tile;
     bool fwd_tap, dgrad_tap;
+    int blocked, xcd_order;  // reduction order and tile order (see kernels.h)
     // workspace layout (byte offsets), per pass
     size_t off_d, off_sums, off_wt, off_part;
     size_t ws_fwd, ws_data, ws_weights, ws_both;
@@ -200,6 +201,8 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
 
     q.fwd_tile = pick_tile(q.Kg, true, env_tile("CAFFE_CONV_FWD_TILE"));
     q.dgrad_tile = pick_tile(q.Mt, false, env_tile("CAFFE_CONV_DGRAD_TILE"));
+    q.blocked = env_tile("CAFFE_CONV_BLOCKED") != 0;
+    q.xcd_order = env_tile("CAFFE_CONV_XCD_ORDER") != 0;
     q.fwd_tap = q.Cg % gemm_tile_k(q.fwd_tile) == 0;
     q.dgrad_tap = q.Kg % gemm_tile_k(q.dgrad_tile) == 0;
     q.ws_fwd = q.fwd_tap ? align_up(q.weight_elems * 4, kWsAlign) : 0;
@@ -272,7 +275,7 @@ int run_forward(const ConvPlan& q, const void* bottom, const void* weight, const
     if (q.fwd_tap) {
         float* wp = (float*)ws;
         LAUNCH(launch_pack_weights_blocked((const float*)weight, wp, q.K, q.Cg, q.kh * q.kw,
-                                           gemm_tile_k(q.fwd_tile), s),
+                                           gemm_tile_k(q.fwd_tile), q.blocked, s),
                "weight pack launch");
         A = wp;
     }
@@ -291,6 +294,8 @@ int run_forward(const ConvPlan& q, const void* bottom, const void* weight, const
     p.Ncol = q.N * q.Ho * q.Wo;
     p.relu = q.relu;
     p.Cout = q.K; p.OutH = q.Ho; p.OutW = q.Wo;
+    p.blocked = q.blocked;
+    p.xcd_order = q.xcd_order;
     LAUNCH(launch_conv_gemm_f32(p, 0, q.fwd_tile, q.fwd_tap, s), "forward launch");
     return CAFFE_OK;
 }
@@ -318,7 +323,9 @@ int run_data(const ConvPlan& q, const float* dsrc, const float* bottom_mask, con
     float* wt = (float*)(ws + q.off_wt);
     LAUNCH(launch_dgrad_weight_transform((const float*)weight, wt, q.G, q.Kg, q.Cg, q.kh, q.kw,
                                          q.sh, q.sw, q.Th, q.Tw,
-                                         q.dgrad_tap ? gemm_tile_k(q.dgrad_tile) : 0, s),
+                                         q.dgrad_tap ? (q.blocked ? gemm_tile_k(q.dgrad_tile) : -1)
+                                                     : 0,
+                                         s),
            "weight transform launch");
     ConvGemmParams p = {};
     p.A = wt;
@@ -339,6 +346,8 @@ int run_data(const ConvPlan& q, const float* dsrc, const float* bottom_mask, con
     p.Cout = q.C; p.OutH = q.H; p.OutW = q.W;
     p.psh = q.sh; p.psw = q.sw; p.a0h = q.a0h; p.a0w = q.a0w; p.oph = q.ph; p.opw = q.pw;
     p.Cg_out = q.Cg;
+    p.blocked = q.blocked;
+    p.xcd_order = q.xcd_order;
     LAUNCH(launch_conv_gemm_f32(p, 1, q.dgrad_tile, q.dgrad_tap, s), "data-gradient launch");
     return CAFFE_OK;
 }
@@ -365,6 +374,7 @@ int run_weights(const ConvPlan& q, const float* dsrc, const void* bottom, float*
     p.splits = q.splits;
     p.div_ohw = make_fastdiv((uint32_t)(q.Ho * q.Wo));
     p.div_ow = make_fastdiv((uint32_t)q.Wo);
+    p.xcd_order = q.xcd_order;
     LAUNCH(launch_conv_wgrad_f32(p, q.wgrad_tile, s), "weight-gradient launch");
     // dW = sum of the split partials; db = sum of the split bias partials
     LAUNCH(launch_wgrad_reduce(part, weight_diff, (int)q.weight_elems, q.splits, sums, bias_diff,

@@ -89,6 +89,9 @@ dgrad_weight_transform_kernel(const float* __restrict__ W, float* __restrict__ W
             const int ki = r % tk;
             t = (r / tk) % (Th * Tw);
             k = (r / (tk * Th * Tw)) * tk + ki;
+        } else if (tk < 0) {  // r = (th, tw, k)
+            t = r / Kg;
+            k = r - t * Kg;
         } else {       // r = (k, th, tw)
             k = r / (Th * Tw);
             t = r - k * Th * Tw;

@@ -100,7 +100,7 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     const int n_mt = (p.M + TM - 1) / TM;
     const int n_ct = (p.Ncol + TN - 1) / TN;
     const int per_xcd = gridDim.x >> 3;
-    const int T = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    const int T = p.xcd_order ? (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3) : blockIdx.x;
     if (T >= n_mt * n_ct * p.G)
         return;
     const int mt = T % n_mt;
@@ -233,11 +233,22 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     // blocked walk state: stage s covers tap (tu, tv) of channels tc .. tc + TK - 1
     int tu = 0, tv = 0, tc = 0;
     auto advance = [&]() {
-        if (++tv == kw) {
-            tv = 0;
-            if (++tu == kh) {
-                tu = 0;
-                tc += TK;
+        if (p.blocked) {  // (c / TK, u, v, c % TK)
+            if (++tv == kw) {
+                tv = 0;
+                if (++tu == kh) {
+                    tu = 0;
+                    tc += TK;
+                }
+            }
+        } else {          // (u, v, c)
+            tc += TK;
+            if (tc == Cin_g) {
+                tc = 0;
+                if (++tv == kw) {
+                    tv = 0;
+                    ++tu;
+                }
             }
         }
     };
@@ -393,7 +404,7 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
 // Wp[o][((c / tk) * khw + t) * tk + c % tk] = W[o][c][t], t = u*kw + v.
 __global__ void __launch_bounds__(256)
 pack_weights_blocked_kernel(const float* __restrict__ W, float* __restrict__ Wp, int K, int Cg,
-                            int khw, int tk)
+                            int khw, int tk, int blocked)
 {
     const int total = K * Cg * khw;
     const int e = blockIdx.x * blockDim.x + threadIdx.x;
@@ -402,20 +413,26 @@ pack_weights_blocked_kernel(const float* __restrict__ W, float* __restrict__ Wp,
     const int R = Cg * khw;
     const int o = e / R;
     const int r = e - o * R;
-    const int ci = r % tk;
-    const int t = (r / tk) % khw;
-    const int c = (r / (tk * khw)) * tk + ci;
+    int c, t;
+    if (blocked) {
+        const int ci = r % tk;
+        t = (r / tk) % khw;
+        c = (r / (tk * khw)) * tk + ci;
+    } else {
+        t = r / Cg;
+        c = r - t * Cg;
+    }
     Wp[e] = W[(o * Cg + c) * khw + t];
 }
 
 hipError_t launch_pack_weights_blocked(const float* W, float* Wp, int K, int Cg, int khw, int tk,
-                                       hipStream_t s)
+                                       int blocked, hipStream_t s)
 {
     const int total = K * Cg * khw;
     if (total == 0)
         return hipSuccess;
     hipLaunchKernelGGL(pack_weights_blocked_kernel, dim3((total + 255) / 256), dim3(256), 0, s, W,
-                       Wp, K, Cg, khw, tk);
+                       Wp, K, Cg, khw, tk, blocked);
     return hipGetLastError();
 }
 

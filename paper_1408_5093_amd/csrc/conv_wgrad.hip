@@ -57,7 +57,7 @@ conv_wgrad_f32_kernel(const WgradParams p)
     const int n_rt = (p.R + TN - 1) / TN;
     const int n_mt = (p.Kg + TM - 1) / TM;
     const int per_xcd = gridDim.x >> 3;
-    const int T = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    const int T = p.xcd_order ? (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3) : blockIdx.x;
     if (T >= n_rt * n_mt * p.G * p.splits)
         return;
     const int rt = T % n_rt;

@@ -41,6 +41,8 @@ struct ConvGemmParams {
     int relu;
     int Cout, OutH, OutW;
     int psh, psw, a0h, a0w, oph, opw, Cg_out;
+    int blocked;    // channel-blocked reduction order (else tap-major), with tap_major
+    int xcd_order;  // XCD-contiguous tile order (else linear)
 };
 
 // Split-K weight gradient:
@@ -59,6 +61,7 @@ struct WgradParams {
     int R, G;
     int Ncol, cols_per_split, splits;
     FastDiv div_ohw, div_ow;
+    int xcd_order;  // XCD-contiguous tile order (else linear)
 };
 
 // Tile shapes a launcher may pick; see conv_gemm.hip.
@@ -84,9 +87,10 @@ constexpr int kGemmMinTK = 16;
 hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool tap_major,
                                 hipStream_t s);
 
-// Wp[o][((c / tk) * khw + u*kw + v) * tk + c % tk] = W[o][c][u][v]  (K rows)
+// blocked: Wp[o][((c / tk) * khw + u*kw + v) * tk + c % tk] = W[o][c][u][v];
+// else tap-major: Wp[o][(u*kw + v) * Cg + c] = W[o][c][u][v]   (K rows)
 hipError_t launch_pack_weights_blocked(const float* W, float* Wp, int K, int Cg, int khw, int tk,
-                                       hipStream_t s);
+                                       int blocked, hipStream_t s);
 
 enum WgradTile : int {
     WTILE_128x128 = 0,  // 4 waves as 2x2, each 64x64
@@ -105,8 +109,9 @@ hipError_t launch_relu_mask_bias(const float* G, const float* Y, float* D, float
                                  int planes, int plane_size, int relu, hipStream_t s);
 
 // Wt[g][(c, fh, fw)][r] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)]
-// (0 where the tap index passes the kernel edge), r = (k, th, tw), or the
-// channel-blocked r = (k / tk, th, tw, k % tk) when tk > 0.
+// (0 where the tap index passes the kernel edge), r = (k, th, tw), the
+// channel-blocked r = (k / tk, th, tw, k % tk) when tk > 0, or the tap-major
+// r = (th, tw, k) when tk < 0.
 hipError_t launch_dgrad_weight_transform(const float* W, float* Wt, int G, int Kg, int Cg, int kh,
                                          int kw, int sh, int sw, int Th, int Tw, int tk,
                                          hipStream_t s);

@@ -56,7 +56,7 @@ struct ConvPlan {
     // gathered channels per group fill whole pipeline stages
     int fwd_tile, dgrad_tile;
     bool fwd_tap, dgrad_tap;
-    int blocked, xcd_order;  // reduction order and tile order (see kernels.h)
+    int blocked, xcd_order, wgrad_xcd_order;  // reduction and tile orders (see kernels.h)
     // workspace layout (byte offsets), per pass
     size_t off_d, off_sums, off_wt, off_part;
     size_t ws_fwd, ws_data, ws_weights, ws_both;
@@ -201,8 +201,12 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
 
     q.fwd_tile = pick_tile(q.Kg, true, env_tile("CAFFE_CONV_FWD_TILE"));
     q.dgrad_tile = pick_tile(q.Mt, false, env_tile("CAFFE_CONV_DGRAD_TILE"));
+    // defaults from measurement: the channel-blocked order and the XCD tile
+    // order help the forward / data-gradient GEMMs; the weight gradient keeps
+    // the linear tile order (its split partials gain nothing from it)
     q.blocked = env_tile("CAFFE_CONV_BLOCKED") != 0;
     q.xcd_order = env_tile("CAFFE_CONV_XCD_ORDER") != 0;
+    q.wgrad_xcd_order = env_tile("CAFFE_CONV_WGRAD_XCD_ORDER") > 0;
     q.fwd_tap = q.Cg % gemm_tile_k(q.fwd_tile) == 0;
     q.dgrad_tap = q.Kg % gemm_tile_k(q.dgrad_tile) == 0;
     q.ws_fwd = q.fwd_tap ? align_up(q.weight_elems * 4, kWsAlign) : 0;
@@ -374,7 +378,7 @@ int run_weights(const ConvPlan& q, const float* dsrc, const void* bottom, float*
     p.splits = q.splits;
     p.div_ohw = make_fastdiv((uint32_t)(q.Ho * q.Wo));
     p.div_ow = make_fastdiv((uint32_t)q.Wo);
-    p.xcd_order = q.xcd_order;
+    p.xcd_order = q.wgrad_xcd_order;
     LAUNCH(launch_conv_wgrad_f32(p, q.wgrad_tile, s), "weight-gradient launch");
     // dW = sum of the split partials; db = sum of the split bias partials
     LAUNCH(launch_wgrad_reduce(part, weight_diff, (int)q.weight_elems, q.splits, sums, bias_diff,

@@ -32,7 +32,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--batch", type=int, default=256)
     ap.add_argument("--bf16", action="store_true", help="bfloat16 operands (N=512 workload)")
-    ap.add_argument("--cpu-images", type=int, default=128,
+    ap.add_argument("--cpu-images", type=int, default=192,
                     help="images in the CPU-oracle baseline sample (0 = skip)")
     ap.add_argument("--calibrate-copy-mb", type=int, default=0,
                     help="first run one plain device copy of this many MiB (a known-size "

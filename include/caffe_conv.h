@@ -33,8 +33,9 @@
  * CAFFE_F32 (float) or CAFFE_BF16 (bfloat16 stored as uint16_t; the caller
  * rounds to nearest-even).  Everything else (bias, top, top_diff, every
  * gradient) is float in both modes, and every product is accumulated in
- * float.  In CAFFE_BF16 mode `top_diff` is rounded to bfloat16
- * (nearest-even) before it enters a product.
+ * float.  In CAFFE_BF16 mode `top_diff` (after the ReLU mask) is rounded to
+ * bfloat16 (nearest-even) before it enters a product; bias_diff sums the
+ * unrounded float values.
  *
  * Memory and ownership.  Every tensor pointer is a device pointer (HIP
  * device memory of the current device), allocated and owned by the caller,
@@ -135,7 +136,8 @@ enum caffe_backward_flags {
     CAFFE_BACKWARD_TOP_DIFF_MASKED = 1,
     /* bottom_diff is stored multiplied by [bottom > 0]: the backward pass of
      * a ReLU whose output is this layer's bottom, fused into the data
-     * gradient.  Needs bottom (CAFFE_F32 only). */
+     * gradient.  Needs bottom (in CAFFE_BF16 mode the mask is taken from
+     * the bf16 bottom). */
     CAFFE_BACKWARD_MASK_BOTTOM_DIFF = 2
 };
 

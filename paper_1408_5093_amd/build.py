@@ -36,6 +36,7 @@ CFLAGS = [
 EXTRA = {
     "conv_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "conv_wgrad.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "conv_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
 
 

@@ -60,6 +60,12 @@ struct ConvPlan {
     // workspace layout (byte offsets), per pass
     size_t off_d, off_sums, off_wt, off_part;
     size_t ws_fwd, ws_data, ws_weights, ws_both;
+    // bf16 operands: channel-contiguous staging with each group's channels
+    // padded to a multiple of 8 (Cgp, Kgp); padded reduction lengths of the
+    // forward (Rp) and data-gradient (Rtp) GEMMs; weight-gradient columns Rw
+    int Cgp, Kgp, Rp, Rtp, Rw;
+    size_t off_xh_fwd, off_wp_fwd;  // forward: [Xh][Wp]
+    size_t off_dh, off_xh;          // backward: [Dh][Xh][sums][Wt][partials]
 };
 
 // Tile for a GEMM with M rows: the least padding of M; ties go to the first
@@ -112,6 +118,73 @@ int env_tile(const char* name)
 {
     const char* v = getenv(name);
     return v && *v ? atoi(v) : -1;
+}
+
+int round_up(int x, int a) { return (x + a - 1) / a * a; }
+
+// The bf16-operand plan: staging sizes, padded reductions, the weight-gradient
+// split and the workspace layout.  Called by plan_conv once the common fields
+// are set.
+int plan_bf16(ConvPlan* p)
+{
+    ConvPlan& q = *p;
+    q.Cgp = round_up(q.Cg, 8);
+    q.Kgp = round_up(q.Kg, 8);
+    const int khw = q.kh * q.kw;
+    const int64_t xh = (int64_t)q.N * q.H * q.W * q.G * q.Cgp * 2;
+    const int64_t dh = (int64_t)q.N * q.Ho * q.Wo * q.G * q.Kgp * 2;
+    const int64_t rp = ((int64_t)khw * q.Cgp + kBf16TK - 1) / kBf16TK * kBf16TK;
+    const int64_t rtp = ((int64_t)q.Th * q.Tw * q.Kgp + kBf16TK - 1) / kBf16TK * kBf16TK;
+    const int64_t rw = (int64_t)khw * q.Cgp;
+    const int64_t wp = (int64_t)q.K * rp * 2;
+    const int64_t wt = (int64_t)q.G * q.Mt * rtp * 2;
+    if (xh > kMaxTensorBytes || dh > kMaxTensorBytes || wp > kMaxTensorBytes ||
+        wt > kMaxTensorBytes || rw * q.K * 4 > kMaxTensorBytes)
+        return fail(CAFFE_ERR_UNSUPPORTED, "bf16 staging buffers reach 2^31 bytes");
+    q.Rp = (int)rp;
+    q.Rtp = (int)rtp;
+    q.Rw = (int)rw;
+
+    // weight-gradient split-K over the output pixels, as for fp32
+    const int64_t ncol = (int64_t)q.N * q.Ho * q.Wo;
+    const int tk = kBf16WgradTK;
+    q.wgrad_tile = pick_wgrad_tile(q.Kg, env_tile("CAFFE_CONV_WGRAD_TILE"));
+    const int wtm = wgrad_tile_m(q.wgrad_tile), wtn = wgrad_tile_n(q.wgrad_tile);
+    const int64_t tiles = (int64_t)((q.Kg + wtm - 1) / wtm) * ((q.Rw + wtn - 1) / wtn) * q.G;
+    const int64_t target = env_tile("CAFFE_CONV_WGRAD_BLOCKS") > 0
+                               ? env_tile("CAFFE_CONV_WGRAD_BLOCKS")
+                               : 2048;
+    int64_t splits = (target + tiles - 1) / tiles;
+    const int64_t max_splits = std::max<int64_t>(1, ncol / (8 * tk));
+    const int64_t max_by_bytes = std::max<int64_t>(1, kMaxTensorBytes / (rw * q.K * 4));
+    splits = std::max<int64_t>(1, std::min(std::min(splits, max_splits), max_by_bytes));
+    int64_t cps = (ncol + splits - 1) / splits;
+    cps = std::max<int64_t>(tk, (cps + tk - 1) / tk * tk);
+    splits = std::max<int64_t>(1, (ncol + cps - 1) / cps);
+    q.splits = (int)splits;
+    q.cols_per_split = (int)cps;
+    const int64_t part_bytes = splits * rw * q.K * 4;
+    if (part_bytes > kMaxTensorBytes)
+        return fail(CAFFE_ERR_UNSUPPORTED, "weight-gradient partials reach 2^31 bytes");
+
+    q.fwd_tile = pick_tile(q.Kg, true, env_tile("CAFFE_CONV_FWD_TILE"));
+    q.dgrad_tile = pick_tile(q.Mt, false, env_tile("CAFFE_CONV_DGRAD_TILE"));
+    q.xcd_order = env_tile("CAFFE_CONV_XCD_ORDER") != 0;
+
+    q.off_xh_fwd = 0;
+    q.off_wp_fwd = align_up(xh, kWsAlign);
+    q.ws_fwd = q.off_wp_fwd + align_up(wp, kWsAlign);
+    const size_t sums_bytes =
+        align_up((size_t)std::max<int64_t>(q.N, q.splits) * q.K * 4, kWsAlign);
+    q.off_dh = 0;
+    q.off_xh = align_up(dh, kWsAlign);
+    q.off_sums = q.off_xh + align_up(xh, kWsAlign);
+    q.off_wt = q.off_sums + sums_bytes;
+    q.off_part = q.off_wt + align_up(wt, kWsAlign);
+    q.ws_data = q.off_part;
+    q.ws_weights = q.off_part + align_up(part_bytes, kWsAlign);
+    q.ws_both = q.ws_weights;
+    return CAFFE_OK;
 }
 
 int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
@@ -210,6 +283,9 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     q.fwd_tap = q.Cg % gemm_tile_k(q.fwd_tile) == 0;
     q.dgrad_tap = q.Kg % gemm_tile_k(q.dgrad_tile) == 0;
     q.ws_fwd = q.fwd_tap ? align_up(q.weight_elems * 4, kWsAlign) : 0;
+
+    if (q.dtype == CAFFE_BF16)
+        return plan_bf16(&q);
 
     // Workspace: [masked top diff][bias partial sums][transformed weights]
     // [weight partials].  The masked top diff is written only when relu is
@@ -387,6 +463,133 @@ int run_weights(const ConvPlan& q, const float* dsrc, const void* bottom, float*
     return CAFFE_OK;
 }
 
+// ---- bf16 operands
+int run_forward_bf16(const ConvPlan& q, const void* bottom, const void* weight, const float* bias,
+                     float* top, char* ws, hipStream_t s)
+{
+    if (q.top_elems == 0)
+        return CAFFE_OK;
+    uint16_t* xh = (uint16_t*)(ws + q.off_xh_fwd);
+    uint16_t* wp = (uint16_t*)(ws + q.off_wp_fwd);
+    const int Ctot = q.G * q.Cgp;
+    LAUNCH(launch_nhwc_from_nchw_bf16((const uint16_t*)bottom, xh, q.N, q.C, q.H * q.W, q.Cg,
+                                      q.Cgp, Ctot, s),
+           "bf16 staging launch");
+    LAUNCH(launch_pack_weights_bf16((const uint16_t*)weight, wp, q.K, q.Cg, q.Cgp, q.kh * q.kw,
+                                    q.Rp, s),
+           "bf16 weight pack launch");
+    GemmBf16Params p = {};
+    p.A = wp;
+    p.X = xh;
+    p.Y = top;
+    p.bias = bias;
+    p.A_bytes = nbytes((int64_t)q.K * q.Rp, 2);
+    p.X_bytes = nbytes((int64_t)q.N * q.H * q.W * Ctot, 2);
+    p.Y_bytes = nbytes(q.top_elems, 4);
+    p.N = q.N; p.IH = q.H; p.IW = q.W; p.Ctot = Ctot; p.Cgp = q.Cgp;
+    p.kh = q.kh; p.kw = q.kw; p.sh = q.sh; p.sw = q.sw; p.ph = q.ph; p.pw = q.pw;
+    p.OH = q.Ho; p.OW = q.Wo;
+    p.M = q.Kg; p.Rp = q.Rp; p.G = q.G;
+    p.Ncol = q.N * q.Ho * q.Wo;
+    p.relu = q.relu;
+    p.Cout = q.K; p.OutH = q.Ho; p.OutW = q.Wo;
+    p.xcd_order = q.xcd_order;
+    LAUNCH(launch_conv_gemm_bf16(p, 0, q.fwd_tile, s), "bf16 forward launch");
+    return CAFFE_OK;
+}
+
+int run_data_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom_mask,
+                  const void* weight, float* bottom_diff, char* ws, hipStream_t s)
+{
+    if (q.bottom_elems == 0)
+        return CAFFE_OK;
+    uint16_t* wt = (uint16_t*)(ws + q.off_wt);
+    LAUNCH(launch_dgrad_weights_bf16((const uint16_t*)weight, wt, q.G, q.Kg, q.Kgp, q.Cg, q.kh,
+                                     q.kw, q.sh, q.sw, q.Th, q.Tw, q.Rtp, s),
+           "bf16 weight transform launch");
+    const int Ktot = q.G * q.Kgp;
+    GemmBf16Params p = {};
+    p.A = wt;
+    p.X = dh;
+    p.Omask = (const uint16_t*)bottom_mask;
+    p.Y = bottom_diff;
+    p.A_bytes = nbytes((int64_t)q.G * q.Mt * q.Rtp, 2);
+    p.X_bytes = nbytes((int64_t)q.N * q.Ho * q.Wo * Ktot, 2);
+    p.Y_bytes = nbytes(q.bottom_elems, 4);
+    p.N = q.N; p.IH = q.Ho; p.IW = q.Wo; p.Ctot = Ktot; p.Cgp = q.Kgp;
+    p.kh = q.Th; p.kw = q.Tw; p.sh = 1; p.sw = 1;
+    p.ph = q.Th - 1 - q.a0h; p.pw = q.Tw - 1 - q.a0w;
+    p.OH = q.Ah; p.OW = q.Aw;
+    p.M = q.Mt; p.Rp = q.Rtp; p.G = q.G;
+    p.Ncol = q.N * q.Ah * q.Aw;
+    p.Cout = q.C; p.OutH = q.H; p.OutW = q.W;
+    p.psh = q.sh; p.psw = q.sw; p.a0h = q.a0h; p.a0w = q.a0w; p.oph = q.ph; p.opw = q.pw;
+    p.Cg_out = q.Cg;
+    p.xcd_order = q.xcd_order;
+    LAUNCH(launch_conv_gemm_bf16(p, 1, q.dgrad_tile, s), "bf16 data-gradient launch");
+    return CAFFE_OK;
+}
+
+int run_weights_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom,
+                     float* weight_diff, int accumulate, char* ws, hipStream_t s)
+{
+    uint16_t* xh = (uint16_t*)(ws + q.off_xh);
+    float* part = (float*)(ws + q.off_part);
+    const int Ctot = q.G * q.Cgp;
+    LAUNCH(launch_nhwc_from_nchw_bf16((const uint16_t*)bottom, xh, q.N, q.C, q.H * q.W, q.Cg,
+                                      q.Cgp, Ctot, s),
+           "bf16 staging launch");
+    WgradBf16Params p = {};
+    p.D = dh;
+    p.X = xh;
+    p.P = part;
+    p.D_bytes = nbytes((int64_t)q.N * q.Ho * q.Wo * q.G * q.Kgp, 2);
+    p.X_bytes = nbytes((int64_t)q.N * q.H * q.W * Ctot, 2);
+    p.P_bytes = nbytes((int64_t)q.splits * q.K * q.Rw, 4);
+    p.N = q.N; p.IH = q.H; p.IW = q.W; p.Ctot = Ctot; p.Cgp = q.Cgp;
+    p.K = q.K; p.Kg = q.Kg; p.Kgp = q.Kgp; p.Ktot = q.G * q.Kgp;
+    p.kh = q.kh; p.kw = q.kw; p.sh = q.sh; p.sw = q.sw; p.ph = q.ph; p.pw = q.pw;
+    p.OH = q.Ho; p.OW = q.Wo;
+    p.Rw = q.Rw; p.G = q.G;
+    p.Ncol = q.N * q.Ho * q.Wo;
+    p.cols_per_split = q.cols_per_split;
+    p.splits = q.splits;
+    p.div_ohw = make_fastdiv((uint32_t)(q.Ho * q.Wo));
+    p.div_ow = make_fastdiv((uint32_t)q.Wo);
+    LAUNCH(launch_conv_wgrad_bf16(p, q.wgrad_tile, s), "bf16 weight-gradient launch");
+    LAUNCH(launch_wgrad_reduce_perm(part, weight_diff, q.K, q.Rw, q.Cgp, q.Cg, q.kh * q.kw,
+                                    q.splits, accumulate, s),
+           "bf16 reduce launch");
+    return CAFFE_OK;
+}
+
+int backward_bf16(const ConvPlan& q, const float* top_diff, const float* top, bool masked,
+                  bool mask_bottom, const void* bottom, const void* weight, float* bottom_diff,
+                  float* weight_diff, float* bias_diff, int accumulate, char* ws, hipStream_t s)
+{
+    if (!bottom_diff && !weight_diff) {
+        if (bias_diff)
+            return run_bias_only(q, top_diff, top, masked, bias_diff, accumulate, ws, s);
+        return CAFFE_OK;
+    }
+    uint16_t* dh = (uint16_t*)(ws + q.off_dh);
+    float* sums = (float*)(ws + q.off_sums);
+    // D = bf16(top_diff [top > 0]) staged channel-contiguous; the fp32 plane
+    // sums give the bias gradient
+    LAUNCH(launch_diff_prep_bf16(top_diff, top, dh, bias_diff ? sums : nullptr, q.N, q.K,
+                                 q.Ho * q.Wo, q.Kg, q.Kgp, q.G * q.Kgp, q.relu && !masked, s),
+           "bf16 top-gradient staging launch");
+    if (bottom_diff)
+        CHECK(run_data_bf16(q, dh, mask_bottom ? bottom : nullptr, weight, bottom_diff, ws, s));
+    if (weight_diff)
+        CHECK(run_weights_bf16(q, dh, bottom, weight_diff, accumulate, ws, s));
+    if (bias_diff)
+        LAUNCH(launch_wgrad_reduce(nullptr, nullptr, 0, 0, sums, bias_diff, q.N, q.K, accumulate,
+                                   s),
+               "bias reduce launch");
+    return CAFFE_OK;
+}
+
 int check_conv_ptrs(const ConvPlan& q, const void* p, bool needed, bool is_blob, const char* name)
 {
     // blob pointers may be NULL for an empty batch
@@ -444,8 +647,9 @@ int caffe_conv_forward(const caffe_conv_desc* desc, const void* bottom, const vo
     CHECK(check_conv_ptrs(q, bias, false, false, "bias"));
     CHECK(check_conv_ptrs(q, top, true, true, "top"));
     CHECK(check_ws(workspace, ws_bytes, q.ws_fwd));
-    if (q.dtype != CAFFE_F32)
-        return fail(CAFFE_ERR_UNSUPPORTED, "bf16 forward is not built yet");
+    if (q.dtype == CAFFE_BF16)
+        return run_forward_bf16(q, bottom, weight, bias, top, (char*)workspace,
+                                (hipStream_t)stream);
     return run_forward(q, bottom, weight, bias, top, (char*)workspace, (hipStream_t)stream);
 }
 
@@ -471,10 +675,11 @@ int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, cons
     CHECK(check_conv_ptrs(q, bias_diff, false, false, "bias_diff"));
     const size_t need = weight_diff ? q.ws_both : q.ws_data;
     CHECK(check_ws(workspace, ws_bytes, need));
-    if (q.dtype != CAFFE_F32)
-        return fail(CAFFE_ERR_UNSUPPORTED, "bf16 backward is not built yet");
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
+    if (q.dtype == CAFFE_BF16)
+        return backward_bf16(q, top_diff, top, masked, mask_bottom, bottom, weight, bottom_diff,
+                             weight_diff, bias_diff, accumulate, ws, s);
     const float* dsrc = top_diff;
     if (q.relu && !masked && (bottom_diff || weight_diff) && q.top_elems > 0) {
         // D = top_diff [top > 0], shared by both gradients

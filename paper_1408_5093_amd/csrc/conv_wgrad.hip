@@ -17,11 +17,6 @@
 
 namespace caffe_hip {
 
-__device__ __forceinline__ uint32_t fdiv(uint32_t x, const FastDiv& f)
-{
-    return (uint32_t)(((uint64_t)x * f.mul) >> f.shift);
-}
-
 template <int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH, int SW>
 __global__ void __launch_bounds__(64 * WM * WN)
 conv_wgrad_f32_kernel(const WgradParams p)

@@ -7,6 +7,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "kernels.h"
+
 namespace caffe_hip {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
@@ -55,6 +57,12 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f)
 __device__ __forceinline__ float bf16_to_f32(uint16_t h)
 {
     return __builtin_bit_cast(float, (uint32_t)h << 16);
+}
+
+// x / f.d for x < 2^31 (see FastDiv).
+__device__ __forceinline__ uint32_t fdiv(uint32_t x, const FastDiv& f)
+{
+    return (uint32_t)(((uint64_t)x * f.mul) >> f.shift);
 }
 
 __device__ __forceinline__ float wave_sum(float v)

@@ -103,6 +103,81 @@ int wgrad_tile_n(int tile);
 int wgrad_tile_k();
 hipError_t launch_conv_wgrad_f32(const WgradParams& p, int tile, hipStream_t s);
 
+// ---- bf16 operands (conv_bf16.hip) ----
+// Reduction depth of one pipeline stage of the bf16 implicit GEMM; padded
+// reduction lengths are multiples of it.
+constexpr int kBf16TK = 32;
+
+// Implicit GEMM over a channel-contiguous bf16 gather source
+// X[N][IH][IW][Ctot] whose group g owns channels g*Cgp .. g*Cgp + Cgp - 1
+// (Cgp a multiple of 8).  Reduction r = (u, v, c) over kh x kw x Cgp, padded
+// with zeros to Rp (a multiple of kBf16TK); A is [G*M][Rp] bf16.
+//   C_g[m][col] = sum_r A[g*M + m][r] * X[n][i*sh - ph + u][j*sw - pw + v][g*Cgp + c]
+// Epilogues as ConvGemmParams (epi 0 forward, epi 1 phase-stacked data
+// gradient); Omask (epi 1, may be null) is a bf16 tensor laid out like Y.
+struct GemmBf16Params {
+    const uint16_t* A;
+    const uint16_t* X;
+    const uint16_t* Omask;
+    float* Y;
+    const float* bias;
+    uint32_t A_bytes, X_bytes, Y_bytes;
+    int N, IH, IW, Ctot, Cgp;
+    int kh, kw, sh, sw, ph, pw;
+    int OH, OW;
+    int M, Rp, G, Ncol;
+    int relu;
+    int Cout, OutH, OutW;
+    int psh, psw, a0h, a0w, oph, opw, Cg_out;
+    int xcd_order;
+};
+hipError_t launch_conv_gemm_bf16(const GemmBf16Params& p, int epi, int tile, hipStream_t s);
+
+// Split-K weight gradient over channel-contiguous bf16 operands:
+//   P[s][g*Kg + m][(u*kw + v)*Cgp + c] =
+//       sum_{col in split s} D[col][g*Kgp + m] * X[n][i*sh - ph + u][j*sw - pw + v][g*Cgp + c]
+// with col = (n, i, j) and Rw = kh*kw*Cgp columns per output channel.
+struct WgradBf16Params {
+    const uint16_t* D;
+    const uint16_t* X;
+    float* P;
+    uint32_t D_bytes, X_bytes, P_bytes;
+    int N, IH, IW, Ctot, Cgp, K, Kg, Kgp, Ktot;
+    int kh, kw, sh, sw, ph, pw;
+    int OH, OW;
+    int Rw, G;
+    int Ncol, cols_per_split, splits;
+    FastDiv div_ohw, div_ow;
+};
+constexpr int kBf16WgradTK = 32;  // output pixels per weight-gradient stage
+hipError_t launch_conv_wgrad_bf16(const WgradBf16Params& p, int tile, hipStream_t s);
+
+// dW[k][c][t] = (accumulate ? dW : 0) + sum_s P[s][k][t*Cgp + c] for c < Cg,
+// t < khw (fixed order).
+hipError_t launch_wgrad_reduce_perm(const float* P, float* dW, int K, int Rw, int Cgp, int Cg,
+                                    int khw, int splits, int accumulate, hipStream_t s);
+
+// Xh[n][p][g*Cgp + c] = X[n][g*Cg + c][p] (c < Cg, else 0), p over H*W;
+// Ctot = G*Cgp.
+hipError_t launch_nhwc_from_nchw_bf16(const uint16_t* X, uint16_t* Xh, int N, int C, int HW,
+                                      int Cg, int Cgp, int Ctot, hipStream_t s);
+
+// Dh[n][p][g*Kgp + k] = bf16(relu ? G [Y > 0] : G)[n][g*Kg + k][p] (k < Kg,
+// else 0); plane_sums (may be null)[n*K + k] = fp32 sum of the masked plane.
+hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, float* plane_sums,
+                                 int N, int K, int HW, int Kg, int Kgp, int Ktot, int relu,
+                                 hipStream_t s);
+
+// Wp[o][(u*kw + v)*Cgp + c] = W[o][c][u][v] (0 for c >= Cg and past khw*Cgp).
+hipError_t launch_pack_weights_bf16(const uint16_t* W, uint16_t* Wp, int K, int Cg, int Cgp,
+                                    int khw, int Rp, hipStream_t s);
+
+// Wt[g][(c, fh, fw)][(th*Tw + tw)*Kgp + k] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)]
+// (0 past the kernel edge, for k >= Kg and past Th*Tw*Kgp).
+hipError_t launch_dgrad_weights_bf16(const uint16_t* W, uint16_t* Wt, int G, int Kg, int Kgp,
+                                     int Cg, int kh, int kw, int sh, int sw, int Th, int Tw,
+                                     int Rtp, hipStream_t s);
+
 // D = relu ? G * [Y > 0] : G (written to D unless D is null) and, unless
 // plane_sums is null, plane_sums[p] = sum of D over plane p (fixed order).
 hipError_t launch_relu_mask_bias(const float* G, const float* Y, float* D, float* plane_sums,

@@ -118,6 +118,22 @@ def test_workspace_sizes():
         assert cc.conv_workspace_size(desc, cc.PASS_BACKWARD_DATA) < top_bytes
         desc.relu = 1
 
+def test_workspace_sizes_bf16():
+    # bf16 operands are staged channel-contiguous, each group's channels padded
+    # to a multiple of 8, next to the packed weights (rows padded to 32)
+    d = cc.conv_desc((256, 3, 227, 227), (96, 3, 11, 11), 4, 0, 1, True, cc.CAFFE_BF16)
+    xh = 256 * 227 * 227 * 8 * 2
+    assert cc.conv_workspace_size(d, cc.PASS_FORWARD) >= xh + 96 * 992 * 2
+    dh = 256 * 55 * 55 * 96 * 2
+    both = cc.conv_workspace_size(d, cc.PASS_BACKWARD)
+    assert both >= dh + xh
+    assert both >= cc.conv_workspace_size(d, cc.PASS_BACKWARD_DATA)
+    for p in range(4):
+        assert cc.conv_workspace_size(d, p) % 256 == 0
+    d2 = cc.conv_desc((2, 20, 9, 9), (8, 5, 3, 3), 1, 1, 4, False, cc.CAFFE_BF16)
+    assert cc.conv_workspace_size(d2, cc.PASS_FORWARD) >= 2 * 81 * 4 * 8 * 2
+
+
 def test_pointer_checks_before_any_launch():
     lib = cc.load()
     P = ctypes.c_void_p

@@ -1,0 +1,206 @@
+"""GPU parity of the bf16-operand convolution (bf16 bottom and weights, fp32
+accumulation and results) against the CPU oracle, through the C ABI.
+
+Two bars per output tensor, max|gpu - ref| / max|ref|:
+* 1e-4 against the oracle fed the very values the GPU multiplied -- the
+  bf16-rounded bottom and weights and, for the gradients, the bf16-rounded
+  (masked) top gradient.  Products of bf16 values are exact in fp32, so only
+  the order of the fp32 sums differs from the oracle's fp64 sums.
+* 2e-2 against the oracle on the unrounded fp32 operands: the tolerance the
+  bf16 variant is held to.
+The bias gradient sums the unrounded fp32 top gradient, so it is held to
+1e-4 against the oracle on that gradient.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1408_5093_amd as cc
+from paper_1408_5093_amd import workloads as wl
+from paper_1408_5093_amd.net import ConvStack
+from helpers import TOL_BF16, TOL_F32, assert_close
+from layer_check import check_layer_sampled
+from test_parity_conv import SWEEP
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _t(a, dtype=torch.float32):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV).to(dtype)
+
+
+def _np(t):
+    torch.cuda.synchronize()
+    return t.detach().float().cpu().numpy()
+
+
+def run_case(N, C, H, W, K, kh, kw, sh, sw, ph, pw, g, relu, bias=True, seed=0, flags=0):
+    print(f"bf16 case N={N} C={C} H={H} W={W} K={K} k={kh}x{kw} s={sh},{sw} p={ph},{pw} g={g} "
+          f"relu={relu} flags={flags}", flush=True)
+    rng = np.random.default_rng([78, seed, N, C, H, W, K, kh, kw, sh, sw, ph, pw, g, int(relu)])
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    if flags & cc.BACKWARD_MASK_BOTTOM_DIFF:
+        x = np.maximum(x, 0)  # a ReLU output
+    w = (rng.standard_normal((K, C // g, kh, kw)) * 0.3).astype(np.float32)
+    b = (rng.standard_normal(K) * 0.5).astype(np.float32) if bias else None
+    xr, wr = wl.round_bf16(x), wl.round_bf16(w)
+    geom = dict(stride=(sh, sw), pad=(ph, pw), group=g)
+    xb, wb = _t(xr, torch.bfloat16), _t(wr, torch.bfloat16)
+
+    y = _np(cc.conv_forward(xb, wb, _t(b) if bias else None, (sh, sw), (ph, pw), g, relu))
+    y_ref_r = oracle.conv_forward(xr, wr, b, (sh, sw), (ph, pw), g, relu)
+    assert_close(y, y_ref_r, TOL_F32, "forward (rounded operands)")
+    assert_close(y, oracle.conv_forward(x, w, b, (sh, sw), (ph, pw), g, relu), TOL_BF16,
+                 "forward (fp32 operands)")
+
+    top = y_ref_r.astype(np.float32)
+    gd = rng.standard_normal(top.shape).astype(np.float32)
+    masked_in = bool(flags & cc.BACKWARD_TOP_DIFF_MASKED)
+    if masked_in and relu:
+        gd = (gd * (top > 0)).astype(np.float32)
+    gr = wl.round_bf16(gd)
+    dx, dw, db = cc.conv_backward(xb, wb, _t(gd), None if masked_in else _t(top), (sh, sw),
+                                  (ph, pw), g, relu, flags=flags)
+    dx, dw, db = _np(dx), _np(dw), _np(db)
+    keep = (xr > 0) if flags & cc.BACKWARD_MASK_BOTTOM_DIFF else 1.0
+    dx_r, dw_r, _ = oracle.conv_backward(xr, wr, gr, top=top, relu=relu, need=("dx", "dw"), **geom)
+    _, _, db_ref = oracle.conv_backward(xr, wr, gd, top=top, relu=relu, need=("db",), **geom)
+    assert_close(dx, dx_r * keep, TOL_F32, "data gradient (rounded operands)")
+    assert_close(dw, dw_r, TOL_F32, "weight gradient (rounded operands)")
+    assert_close(db, db_ref, TOL_F32, "bias gradient")
+    dx_f, dw_f, _ = oracle.conv_backward(x, w, gd, top=top, relu=relu, need=("dx", "dw"), **geom)
+    assert_close(dx, dx_f * keep, TOL_BF16, "data gradient (fp32 operands)")
+    assert_close(dw, dw_f, TOL_BF16, "weight gradient (fp32 operands)")
+
+
+@pytest.mark.parametrize("case", SWEEP)
+@pytest.mark.parametrize("relu", [False, True])
+def test_sweep_bf16(case, relu):
+    run_case(*case, relu=relu, bias=(case[0] % 2 == 0) or relu)
+
+
+def test_tile_shapes_each_chooser_branch_bf16():
+    # forward rows Kg: 48-, 64-, 96-, 128-row tiles and several row tiles;
+    # data-gradient rows Cg * s^2 alike
+    for K, g in [(20, 1), (50, 1), (96, 1), (128, 1), (384, 2), (300, 1)]:
+        run_case(2, 2 * g, 9, 10, K, 3, 3, 1, 1, 1, 1, g, True)
+    for C, s, k in [(3, 4, 11), (1, 2, 5), (5, 3, 7), (8, 4, 5), (40, 1, 3)]:
+        run_case(2, C, 29, 31, 6, k, k, s, s, 1, 2, 1, True)
+
+
+def test_channel_padding_and_long_reductions_bf16():
+    # channels per group that are not multiples of 8 (zero padding), and
+    # channel counts spanning several 32-deep stages per tap
+    for C, K, g in [(9, 10, 1), (18, 30, 3), (64, 72, 1), (200, 40, 2)]:
+        run_case(2, C, 11, 12, K, 3, 3, 1, 1, 1, 1, g, True)
+
+
+@pytest.mark.parametrize("flags", [1, 2, 3])
+def test_backward_flags_bf16(flags):
+    run_case(2, 8, 13, 13, 24, 3, 3, 1, 1, 1, 1, 2, True, flags=flags)
+
+
+def test_empty_batch_bf16():
+    x = torch.empty((0, 4, 9, 9), device=DEV, dtype=torch.bfloat16)
+    w = torch.randn((6, 2, 3, 3), device=DEV).to(torch.bfloat16)
+    y = cc.conv_forward(x, w, torch.zeros(6, device=DEV), 1, 1, 2, True)
+    assert y.shape == (0, 6, 9, 9)
+    g = torch.empty(y.shape, device=DEV)
+    dx, dw, db = cc.conv_backward(x, w, g, y, 1, 1, 2, True)
+    torch.cuda.synchronize()
+    assert dx.shape == x.shape
+    assert torch.all(dw == 0) and torch.all(db == 0)
+
+
+def test_accumulate_bf16():
+    rng = np.random.default_rng(6)
+    x = wl.round_bf16(rng.standard_normal((2, 4, 11, 11)).astype(np.float32))
+    w = wl.round_bf16(rng.standard_normal((8, 4, 3, 3)).astype(np.float32))
+    g = rng.standard_normal((2, 8, 11, 11)).astype(np.float32)
+    _, dw_ref, _ = oracle.conv_backward(x, w, wl.round_bf16(g), stride=1, pad=1, need=("dw",))
+    _, _, db_ref = oracle.conv_backward(x, w, g, stride=1, pad=1, need=("db",))
+    dw0 = rng.standard_normal(w.shape).astype(np.float32)
+    db0 = rng.standard_normal(8).astype(np.float32)
+    dwt, dbt = _t(dw0), _t(db0)
+    cc.conv_backward(_t(x, torch.bfloat16), _t(w, torch.bfloat16), _t(g), None, 1, 1, 1, False,
+                     need=("dw", "db"), accumulate=1, outs=(None, dwt, dbt))
+    assert_close(_np(dwt), dw_ref + dw0, TOL_F32, "accumulated dW")
+    assert_close(_np(dbt), db_ref + db0, TOL_F32, "accumulated db")
+
+
+def test_bitwise_determinism_bf16():
+    rng = np.random.default_rng(12)
+    x = _t(rng.standard_normal((4, 16, 27, 27)), torch.bfloat16)
+    w = _t(rng.standard_normal((32, 8, 5, 5)) * 0.1, torch.bfloat16)
+    b = _t(rng.standard_normal(32))
+    outs = []
+    for _ in range(2):
+        y = cc.conv_forward(x, w, b, 1, 2, 2, True)
+        g = torch.ones_like(y) * 0.5
+        outs.append((y,) + cc.conv_backward(x, w, g, y, 1, 2, 2, True))
+    torch.cuda.synchronize()
+    for a, b_ in zip(*outs):
+        assert torch.equal(a, b_)
+
+
+def test_no_writes_outside_outputs_bf16():
+    rng = np.random.default_rng(14)
+    N, C, H, W, K = 3, 6, 14, 15, 20
+    x = _t(rng.standard_normal((N, C, H, W)), torch.bfloat16)
+    w = _t(rng.standard_normal((K, C // 2, 3, 3)), torch.bfloat16)
+    band, canary = 4096, -12345.0
+
+    def guarded(n):
+        buf = torch.full((band + n + band,), canary, device=DEV)
+        return buf, buf[band:band + n]
+
+    ybuf, yv = guarded(N * K * H * W)
+    y = yv.view(N, K, H, W)
+    d = cc.conv_desc(x.shape, w.shape, 1, 1, 2, True, cc.CAFFE_BF16)
+    cc.caffe_conv_forward(d, x, w, None, y, cc.Workspace().get(
+        cc.conv_workspace_size(d, cc.PASS_FORWARD)))
+    dxbuf, dxv = guarded(x.numel())
+    dwbuf, dwv = guarded(w.numel())
+    dbbuf, dbv = guarded(K)
+    g = _t(rng.standard_normal((N, K, H, W)))
+    cc.conv_backward(x, w, g, y, 1, 1, 2, True, outs=(dxv.view(x.shape), dwv.view(w.shape), dbv))
+    torch.cuda.synchronize()
+    for buf in (ybuf, dxbuf, dwbuf, dbbuf):
+        assert torch.all(buf[:band] == canary) and torch.all(buf[-band:] == canary)
+
+
+def caffenet_glue():
+    return {0: [("pool", wl.CAFFENET_POOL), ("lrn", wl.CAFFENET_LRN)],
+            1: [("pool", wl.CAFFENET_POOL), ("lrn", wl.CAFFENET_LRN)]}
+
+
+def test_caffenet_bf16_training_step_full_size():
+    """The CaffeNet conv1-5 step at N=512 with bf16 operands, layer by layer
+    on the tensors the GPU consumed (sampled images and filters)."""
+    N = 512
+    inp = wl.caffenet_step(N, wl.CAFFENET_STEP_BF16)
+    net = ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(), bf16=True)
+    x = torch.from_numpy(inp["x"]).to(DEV)
+    g = torch.from_numpy(inp["top_diff"]).to(DEV)
+    net.forward(x)
+    net.backward(g)
+    torch.cuda.synchronize()
+    images = [0, N - 1]
+    for l, L in enumerate(wl.CAFFENET):
+        xl = _np(net.bottom[l])          # the fp32 input
+        xr = _np(net.bottom_op[l])       # the bf16 operand the layer multiplied
+        np.testing.assert_array_equal(xr[images], wl.round_bf16(xl[images]))
+        wr = _np(net.W[l])
+        gl = _np(net.layer_top_diff(l, g))
+        top = _np(net.top[l])
+        dx, dw, db = _np(net.dbottom[l]), _np(net.dW[l]), _np(net.db[l])
+        mask = (xr > 0) if net.mask_bottom[l] else None
+        check_layer_sampled(L, xr, wr, inp["b"][l], top, wl.round_bf16(gl), dx, dw, db,
+                            images=images, filters=[0, L.K - 1], what=f"bf16 step {L.name}",
+                            dx_mask=mask, db_top_diff=gl)
+        check_layer_sampled(L, xl, inp["W"][l], inp["b"][l], top, gl, dx, dw, db,
+                            images=images, filters=[L.K // 2], tol=TOL_BF16,
+                            what=f"bf16 step {L.name} vs fp32 operands",
+                            dx_mask=(xl > 0) if net.mask_bottom[l] else None)

@@ -17,6 +17,7 @@ import paper_1408_5093_amd as cc
 from paper_1408_5093_amd import workloads as wl
 from paper_1408_5093_amd.net import ConvStack
 from helpers import TOL_F32, assert_close
+from layer_check import check_layer_sampled
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -25,43 +26,6 @@ DEV = "cuda"
 def _np(t):
     torch.cuda.synchronize()
     return t.detach().float().cpu().numpy()
-
-
-def _geom(L):
-    return dict(stride=L.s, pad=L.p, group=L.g)
-
-
-def check_layer_sampled(L, x, w, b, top, top_diff, dx, dw, db, images, filters, tol=TOL_F32,
-                        what="", dx_mask=None):
-    """x, w, b, top_diff: the operands the GPU layer consumed (numpy);
-    top, dx, dw, db: its outputs.  dx may be None (not computed).  dx_mask:
-    the data gradient was stored times this mask (a fused ReLU backward)."""
-    print(f"check {what}: images {images} filters {filters}", flush=True)
-    xs = x[images]
-    y_ref = oracle.conv_forward(xs, w, b, L.s, L.p, L.g, L.relu)
-    assert_close(top[images], y_ref, tol, f"{what} forward")
-    if top_diff is None:
-        return
-    topm = top if L.relu else None
-    if dx is not None:
-        dx_ref, _, _ = oracle.conv_backward(xs, w, top_diff[images],
-                                            top=None if topm is None else topm[images],
-                                            relu=L.relu, need=("dx",), **_geom(L))
-        if dx_mask is not None:
-            dx_ref = dx_ref * dx_mask[images]
-        assert_close(dx[images], dx_ref, tol, f"{what} data gradient")
-    # bias gradient of every filter (the oracle's db loop alone is cheap at full size)
-    _, _, db_ref = oracle.conv_backward(x, w, top_diff, top=topm, relu=L.relu, need=("db",),
-                                        **_geom(L))
-    assert_close(db, db_ref, tol, f"{what} bias gradient")
-    Kg, Cg = L.K // L.g, L.C // L.g
-    for k in filters:
-        t = k // Kg
-        _, dw_ref, _ = oracle.conv_backward(
-            x[:, t * Cg:(t + 1) * Cg], w[k:k + 1], top_diff[:, k:k + 1],
-            top=None if topm is None else topm[:, k:k + 1], relu=L.relu, stride=L.s, pad=L.p,
-            need=("dw",))
-        assert_close(dw[k:k + 1], dw_ref, tol, f"{what} weight gradient filter {k}")
 
 
 def test_lenet_pair_full():

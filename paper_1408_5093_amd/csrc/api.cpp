@@ -174,8 +174,12 @@ int plan_bf16(ConvPlan* p)
     q.off_xh_fwd = 0;
     q.off_wp_fwd = align_up(xh, kWsAlign);
     q.ws_fwd = q.off_wp_fwd + align_up(wp, kWsAlign);
-    const size_t sums_bytes =
-        align_up((size_t)std::max<int64_t>(q.N, q.splits) * q.K * 4, kWsAlign);
+    // bias-gradient partials of the top-gradient staging (and room for the
+    // per-image sums of the bias-only pass)
+    const int64_t terms = std::max<int64_t>(diff_prep_terms(q.N, q.Ho * q.Wo), q.N);
+    const size_t sums_bytes = align_up((size_t)terms * q.K * 4, kWsAlign);
+    if ((int64_t)sums_bytes > kMaxTensorBytes)
+        return fail(CAFFE_ERR_UNSUPPORTED, "bias partials reach 2^31 bytes");
     q.off_dh = 0;
     q.off_xh = align_up(dh, kWsAlign);
     q.off_sums = q.off_xh + align_up(xh, kWsAlign);
@@ -584,8 +588,8 @@ int backward_bf16(const ConvPlan& q, const float* top_diff, const float* top, bo
     if (weight_diff)
         CHECK(run_weights_bf16(q, dh, bottom, weight_diff, accumulate, ws, s));
     if (bias_diff)
-        LAUNCH(launch_wgrad_reduce(nullptr, nullptr, 0, 0, sums, bias_diff, q.N, q.K, accumulate,
-                                   s),
+        LAUNCH(launch_bias_reduce(sums, bias_diff, diff_prep_terms(q.N, q.Ho * q.Wo), q.K,
+                                  accumulate, s),
                "bias reduce launch");
     return CAFFE_OK;
 }

@@ -587,124 +587,139 @@ wgrad_reduce_perm_kernel(const float* __restrict__ P, float* __restrict__ dW, in
 
 // ------------------------------------------------------------------ staging
 // NCHW bf16 -> channel-contiguous bf16 with per-group channel padding, through
-// a 64-channel x 64-pixel LDS tile: coalesced 2-byte reads along pixels,
-// 16-byte writes along channels.
+// a CT-channel x (4096/CT)-pixel LDS tile (CT = 8 .. 64, sized to the padded
+// channel count): coalesced 2-byte reads along pixels, 16-byte writes along
+// channels.
+template <int CT>
 __global__ void __launch_bounds__(256)
 nhwc_from_nchw_bf16_kernel(const bf16_t* __restrict__ X, bf16_t* __restrict__ Xh, int C, int HW,
-                           int Cg, int Cgp, int Ctot)
+                           int Cg, int Cgp, int Ctot, int ptiles, int ctiles)
 {
-    __shared__ bf16_t tile[64][66];
+    constexpr int PT = 4096 / CT;
+    constexpr int C8 = CT / 8;
+    __shared__ bf16_t tile[CT][PT + 2];
     // block -> (n, channel tile, pixel tile), pixel tiles fastest
-    const int ptiles = (HW + 63) / 64;
-    const int ctiles = (Ctot + 63) / 64;
     const int n = blockIdx.x / (ptiles * ctiles);
     const int rem = blockIdx.x - n * ptiles * ctiles;
-    const int c0 = (rem / ptiles) * 64;
-    const int p0 = (rem - (rem / ptiles) * ptiles) * 64;
+    const int ct = rem / ptiles;
+    const int c0 = ct * CT;
+    const int p0 = (rem - ct * ptiles) * PT;
     const int tid = threadIdx.x;
-    {
-        const int px = tid & 63;
-        const int pix = p0 + px;
 #pragma unroll 4
-        for (int q = 0; q < 16; ++q) {
-            const int cl = (tid >> 6) + 4 * q;
-            const int cp = c0 + cl;
-            const int g = cp / Cgp;
-            const int c = cp - g * Cgp;
-            bf16_t v = 0;
-            if (cp < Ctot && c < Cg && pix < HW)
-                v = X[((size_t)n * C + g * Cg + c) * HW + pix];
-            tile[cl][px] = v;
-        }
+    for (int q = 0; q < 16; ++q) {
+        const int e = tid + 256 * q;
+        const int c = e / PT;
+        const int px = e % PT;
+        const int cp = c0 + c;
+        const int g = cp / Cgp;
+        const int cl = cp - g * Cgp;
+        const int pix = p0 + px;
+        bf16_t v = 0;
+        if (cp < Ctot && cl < Cg && pix < HW)
+            v = X[((size_t)n * C + g * Cg + cl) * HW + pix];
+        tile[c][px] = v;
     }
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
         const int id = tid + 256 * q;
-        const int px = id >> 3;
-        const int ch = id & 7;
+        const int px = id / C8;
+        const int c8 = id % C8;
         const int pix = p0 + px;
-        const int cp = c0 + ch * 8;
+        const int cp = c0 + 8 * c8;
         if (pix < HW && cp < Ctot) {
             u32x4 w;
 #pragma unroll
             for (int k = 0; k < 4; ++k)
-                w[k] = (uint32_t)tile[ch * 8 + 2 * k][px] |
-                       ((uint32_t)tile[ch * 8 + 2 * k + 1][px] << 16);
+                w[k] = (uint32_t)tile[8 * c8 + 2 * k][px] |
+                       ((uint32_t)tile[8 * c8 + 2 * k + 1][px] << 16);
             *(u32x4*)&Xh[((size_t)n * HW + pix) * Ctot + cp] = w;
         }
     }
 }
 
 // Top-gradient staging: Dh = bf16(relu ? G [Y > 0] : G) channel-contiguous,
-// and plane_sums[n*K + k] = sum over the plane of the fp32 masked gradient
-// (the per-image bias-gradient terms), in a fixed order.  A block owns one
-// image and 64 padded channels and walks the plane 64 pixels at a time; wave
-// w sums channels w, w + 4, ... with its lanes along the pixels.
+// one block per (image, 64 padded channels, 64 pixels).  Each wave also sums
+// the fp32 masked gradient of its channels over the block's pixels (a fixed
+// butterfly) into sums[(g*Kg + k) * T + n * ptiles + pt]: the bias-gradient
+// partials, T = N * ptiles per channel.
 __global__ void __launch_bounds__(256)
 diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
-                      bf16_t* __restrict__ Dh, float* __restrict__ plane_sums, int K, int HW,
-                      int Kg, int Kgp, int Ktot, int relu)
+                      bf16_t* __restrict__ Dh, float* __restrict__ sums, int K, int HW, int Kg,
+                      int Kgp, int Ktot, int relu, int ptiles, int ctiles, int T)
 {
     __shared__ bf16_t tile[64][66];
-    const int ctiles = (Ktot + 63) / 64;
-    const int n = blockIdx.x / ctiles;
-    const int c0 = (blockIdx.x - n * ctiles) * 64;
+    const int n = blockIdx.x / (ptiles * ctiles);
+    const int rem = blockIdx.x - n * ptiles * ctiles;
+    const int ct = rem / ptiles;
+    const int pt = rem - ct * ptiles;
+    const int c0 = ct * 64;
+    const int p0 = pt * 64;
     const int tid = threadIdx.x;
     const int px = tid & 63;
     const int cw = tid >> 6;
-    float sum[16];
-#pragma unroll
-    for (int q = 0; q < 16; ++q)
-        sum[q] = 0.f;
-    for (int p0 = 0; p0 < HW; p0 += 64) {
-        const int pix = p0 + px;
+    const int pix = p0 + px;
 #pragma unroll 4
-        for (int q = 0; q < 16; ++q) {
-            const int cl = cw + 4 * q;
-            const int cp = c0 + cl;
-            const int g = cp / Kgp;
-            const int k = cp - g * Kgp;
-            float d = 0.f;
-            if (cp < Ktot && k < Kg && pix < HW) {
-                const size_t idx = ((size_t)n * K + g * Kg + k) * HW + pix;
-                d = G[idx];
-                if (relu && !(Y[idx] > 0.f))
-                    d = 0.f;
-            }
-            sum[q] += d;
-            tile[cl][px] = f32_to_bf16_rne(d);
+    for (int q = 0; q < 16; ++q) {
+        const int cl = cw + 4 * q;
+        const int cp = c0 + cl;
+        const int g = cp / Kgp;
+        const int k = cp - g * Kgp;
+        const bool ok = cp < Ktot && k < Kg;
+        float d = 0.f;
+        if (ok && pix < HW) {
+            const size_t idx = ((size_t)n * K + g * Kg + k) * HW + pix;
+            d = G[idx];
+            if (relu && !(Y[idx] > 0.f))
+                d = 0.f;
         }
-        __syncthreads();
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-            const int id = tid + 256 * q;
-            const int pl = id >> 3;
-            const int ch = id & 7;
-            const int pw = p0 + pl;
-            const int cp = c0 + ch * 8;
-            if (pw < HW && cp < Ktot) {
-                u32x4 w;
-#pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    w[k] = (uint32_t)tile[ch * 8 + 2 * k][pl] |
-                           ((uint32_t)tile[ch * 8 + 2 * k + 1][pl] << 16);
-                *(u32x4*)&Dh[((size_t)n * HW + pw) * Ktot + cp] = w;
-            }
-        }
-        __syncthreads();
-    }
-    if (plane_sums) {
-#pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            const float s = wave_sum(sum[q]);
-            const int cp = c0 + cw + 4 * q;
-            const int g = cp / Kgp;
-            const int k = cp - g * Kgp;
-            if (px == 0 && cp < Ktot && k < Kg)
-                plane_sums[(size_t)n * K + g * Kg + k] = s;
+        tile[cl][px] = f32_to_bf16_rne(d);
+        if (sums) {
+            const float s = wave_sum(d);
+            if (px == 0 && ok)
+                sums[(size_t)(g * Kg + k) * T + n * ptiles + pt] = s;
         }
     }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int id = tid + 256 * q;
+        const int pl = id >> 3;
+        const int c8 = id & 7;
+        const int pw = p0 + pl;
+        const int cp = c0 + 8 * c8;
+        if (pw < HW && cp < Ktot) {
+            u32x4 w;
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                w[k] = (uint32_t)tile[8 * c8 + 2 * k][pl] |
+                       ((uint32_t)tile[8 * c8 + 2 * k + 1][pl] << 16);
+            *(u32x4*)&Dh[((size_t)n * HW + pw) * Ktot + cp] = w;
+        }
+    }
+}
+
+// db[k] = (accumulate ? db[k] : 0) + sum_{t < T} sums[k*T + t]: one block per
+// channel, thread i adds the terms i, i + 256, ... in order, then a fixed
+// pairwise tree over the threads.
+__global__ void __launch_bounds__(256)
+bias_reduce_kernel(const float* __restrict__ sums, float* __restrict__ db, int T, int accumulate)
+{
+    __shared__ float red[256];
+    const int k = blockIdx.x;
+    const float* src = sums + (size_t)k * T;
+    float s = 0.f;
+    for (int t = threadIdx.x; t < T; t += 256)
+        s += src[t];
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+        if (threadIdx.x < off)
+            red[threadIdx.x] += red[threadIdx.x + off];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0)
+        db[k] = accumulate ? db[k] + red[0] : red[0];
 }
 
 // Forward weights: Wp[o][(u*kw + v)*Cgp + c] = W[o][c][u][v], zero for c >= Cg
@@ -853,21 +868,53 @@ hipError_t launch_nhwc_from_nchw_bf16(const uint16_t* X, uint16_t* Xh, int N, in
 {
     if (N == 0)
         return hipSuccess;
-    const int64_t blocks = (int64_t)((HW + 63) / 64) * ((Ctot + 63) / 64) * N;
-    hipLaunchKernelGGL(nhwc_from_nchw_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, s, X, Xh,
-                       C, HW, Cg, Cgp, Ctot);
+    const int ct = Ctot <= 8 ? 8 : Ctot <= 16 ? 16 : Ctot <= 32 ? 32 : 64;
+    const int pt = 4096 / ct;
+    const int ptiles = (HW + pt - 1) / pt;
+    const int ctiles = (Ctot + ct - 1) / ct;
+    const dim3 grid((unsigned)((int64_t)ptiles * ctiles * N));
+    switch (ct) {
+    case 8:
+        hipLaunchKernelGGL(nhwc_from_nchw_bf16_kernel<8>, grid, dim3(256), 0, s, X, Xh, C, HW, Cg,
+                           Cgp, Ctot, ptiles, ctiles);
+        break;
+    case 16:
+        hipLaunchKernelGGL(nhwc_from_nchw_bf16_kernel<16>, grid, dim3(256), 0, s, X, Xh, C, HW, Cg,
+                           Cgp, Ctot, ptiles, ctiles);
+        break;
+    case 32:
+        hipLaunchKernelGGL(nhwc_from_nchw_bf16_kernel<32>, grid, dim3(256), 0, s, X, Xh, C, HW, Cg,
+                           Cgp, Ctot, ptiles, ctiles);
+        break;
+    default:
+        hipLaunchKernelGGL(nhwc_from_nchw_bf16_kernel<64>, grid, dim3(256), 0, s, X, Xh, C, HW, Cg,
+                           Cgp, Ctot, ptiles, ctiles);
+        break;
+    }
     return hipGetLastError();
 }
 
-hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, float* plane_sums,
-                                 int N, int K, int HW, int Kg, int Kgp, int Ktot, int relu,
-                                 hipStream_t s)
+int diff_prep_terms(int N, int HW) { return N * ((HW + 63) / 64); }
+
+hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, float* sums, int N,
+                                 int K, int HW, int Kg, int Kgp, int Ktot, int relu, hipStream_t s)
 {
     if (N == 0)
         return hipSuccess;
-    const int64_t blocks = (int64_t)((Ktot + 63) / 64) * N;
-    hipLaunchKernelGGL(diff_prep_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, s, G, Y, Dh,
-                       plane_sums, K, HW, Kg, Kgp, Ktot, relu);
+    const int ptiles = (HW + 63) / 64;
+    const int ctiles = (Ktot + 63) / 64;
+    hipLaunchKernelGGL(diff_prep_bf16_kernel, dim3((unsigned)((int64_t)ptiles * ctiles * N)),
+                       dim3(256), 0, s, G, Y, Dh, sums, K, HW, Kg, Kgp, Ktot, relu, ptiles, ctiles,
+                       N * ptiles);
+    return hipGetLastError();
+}
+
+hipError_t launch_bias_reduce(const float* sums, float* db, int T, int K, int accumulate,
+                              hipStream_t s)
+{
+    if (K == 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(bias_reduce_kernel, dim3(K), dim3(256), 0, s, sums, db, T, accumulate);
     return hipGetLastError();
 }
 

@@ -163,10 +163,15 @@ hipError_t launch_nhwc_from_nchw_bf16(const uint16_t* X, uint16_t* Xh, int N, in
                                       int Cg, int Cgp, int Ctot, hipStream_t s);
 
 // Dh[n][p][g*Kgp + k] = bf16(relu ? G [Y > 0] : G)[n][g*Kg + k][p] (k < Kg,
-// else 0); plane_sums (may be null)[n*K + k] = fp32 sum of the masked plane.
-hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, float* plane_sums,
-                                 int N, int K, int HW, int Kg, int Kgp, int Ktot, int relu,
-                                 hipStream_t s);
+// else 0).  sums (may be null): the fp32 bias-gradient partials,
+// sums[k*T + t] for T = diff_prep_terms(N, HW) terms per output channel.
+int diff_prep_terms(int N, int HW);
+hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, float* sums, int N,
+                                 int K, int HW, int Kg, int Kgp, int Ktot, int relu, hipStream_t s);
+
+// db[k] = (accumulate ? db[k] : 0) + sum_{t < T} sums[k*T + t] (fixed order).
+hipError_t launch_bias_reduce(const float* sums, float* db, int T, int K, int accumulate,
+                              hipStream_t s);
 
 // Wp[o][(u*kw + v)*Cgp + c] = W[o][c][u][v] (0 for c >= Cg and past khw*Cgp).
 hipError_t launch_pack_weights_bf16(const uint16_t* W, uint16_t* Wp, int K, int Cg, int Cgp,

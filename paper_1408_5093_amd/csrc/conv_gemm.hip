@@ -230,28 +230,11 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     }
 
     const int nst = (R + TK - 1) / TK;
-    // blocked walk state: stage s covers tap (tu, tv) of channels tc .. tc + TK - 1
+    // blocked walk state: stage s covers tap (tu, tv) of channels tc .. tc + TK - 1.
+    // It is updated in the loop body itself: captured by reference in a
+    // lambda, it was kept in scratch memory, and the scratch accesses' waits
+    // also stalled on the next stage's global loads.
     int tu = 0, tv = 0, tc = 0;
-    auto advance = [&]() {
-        if (p.blocked) {  // (c / TK, u, v, c % TK)
-            if (++tv == kw) {
-                tv = 0;
-                if (++tu == kh) {
-                    tu = 0;
-                    tc += TK;
-                }
-            }
-        } else {          // (u, v, c)
-            tc += TK;
-            if (tc == Cin_g) {
-                tc = 0;
-                if (++tv == kw) {
-                    tv = 0;
-                    ++tu;
-                }
-            }
-        }
-    };
 
     load_a(0);
     if constexpr (TAP)
@@ -270,7 +253,24 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
         if (s + 1 < nst) {
             load_a((s + 1) * TK);
             if constexpr (TAP) {
-                advance();
+                if (p.blocked) {  // (c / TK, u, v, c % TK)
+                    if (++tv == kw) {
+                        tv = 0;
+                        if (++tu == kh) {
+                            tu = 0;
+                            tc += TK;
+                        }
+                    }
+                } else {          // (u, v, c)
+                    tc += TK;
+                    if (tc == Cin_g) {
+                        tc = 0;
+                        if (++tv == kw) {
+                            tv = 0;
+                            ++tu;
+                        }
+                    }
+                }
                 load_b_tap(tu, tv, tc);
             } else {
                 load_b_any((s + 1) * TK);

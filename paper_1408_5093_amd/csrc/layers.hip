@@ -180,6 +180,167 @@ maxpool_backward_kernel(const float* __restrict__ dy, const int32_t* __restrict_
     }
 }
 
+// Plane-staged variants for planes that fit in LDS: a block copies PB whole
+// consecutive planes (one contiguous run of memory) into LDS with coalesced
+// loads, so every input is read from HBM once and the overlapping windows
+// are served from LDS; outputs are written coalesced in plane order.
+constexpr int kPoolLdsFloats = 8192;  // 32 KB of staged planes per block
+
+template <int KS, int SS>
+__global__ void __launch_bounds__(256)
+maxpool_forward_lds_kernel(const float* __restrict__ x, float* __restrict__ y,
+                           int32_t* __restrict__ mask, int NC, int H, int W, int OH, int OW,
+                           int kh_, int kw_, int sh_, int sw_, int ph, int pw, int PB,
+                           FastDiv div_ohw, FastDiv div_ow, int relu_input)
+{
+    __shared__ float xs[kPoolLdsFloats];
+    const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
+    const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
+    const int HW = H * W, OHW = OH * OW;
+    const int nc0 = blockIdx.x * PB;
+    const int np = min(PB, NC - nc0);
+    const float* src = x + (size_t)nc0 * HW;
+    const int ne = np * HW;
+    // eight independent loads in flight per thread, then their LDS stores
+    for (int e0 = threadIdx.x; e0 < ne; e0 += 256 * 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            v[u] = e0 + 256 * u < ne ? src[e0 + 256 * u] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (e0 + 256 * u < ne)
+                xs[e0 + 256 * u] = v[u];
+    }
+    __syncthreads();
+    for (int o = threadIdx.x; o < np * OHW; o += 256) {
+        const int pl = udiv(o, div_ohw);
+        const int p = o - pl * OHW;
+        const int i = udiv(p, div_ow);
+        const int j = p - i * OW;
+        const int hs = i * sh - ph, ws = j * sw - pw;
+        const int h0 = max(hs, 0), w0 = max(ws, 0);
+        const int h1 = min(hs + kh, H), w1 = min(ws + kw, W);
+        const float* plane = xs + pl * HW;
+        const int first = h0 * W + w0;
+        float bv = plane[first];
+        int best = first;
+        if constexpr (KS > 0) {
+            // all taps read first; taps outside the image read the window's
+            // first tap, which never wins the strict '>' below
+            float v[KS][KS];
+#pragma unroll
+            for (int du = 0; du < KS; ++du)
+#pragma unroll
+                for (int dv = 0; dv < KS; ++dv) {
+                    const int h = hs + du, w = ws + dv;
+                    const bool in = (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+                    v[du][dv] = plane[in ? h * W + w : first];
+                }
+#pragma unroll
+            for (int du = 0; du < KS; ++du)
+#pragma unroll
+                for (int dv = 0; dv < KS; ++dv)
+                    if (v[du][dv] > bv) {
+                        bv = v[du][dv];
+                        best = (hs + du) * W + ws + dv;
+                    }
+        } else {
+            for (int h = h0; h < h1; ++h)
+                for (int w = w0; w < w1; ++w) {
+                    const float v = plane[h * W + w];
+                    if (v > bv) {
+                        bv = v;
+                        best = h * W + w;
+                    }
+                }
+        }
+        const size_t out = (size_t)nc0 * OHW + o;
+        y[out] = bv;
+        if (mask)  // a ReLU output window with no positive value routes nothing
+            mask[out] = (relu_input && !(bv > 0.f)) ? -1 : best;
+    }
+}
+
+// Gather form from staged masks and gradients: each input position adds, in
+// row-major output order, the gradients of the covering windows whose mask
+// names it.
+template <int KS, int SS>
+__global__ void __launch_bounds__(256)
+maxpool_backward_lds_kernel(const float* __restrict__ dy, const int32_t* __restrict__ mask,
+                            float* __restrict__ dx, int NC, int H, int W, int OH, int OW, int kh_,
+                            int kw_, int sh_, int sw_, int ph, int pw, int PB, FastDiv div_hw,
+                            FastDiv div_w)
+{
+    __shared__ float gs[kPoolLdsFloats / 2];
+    __shared__ int32_t ms[kPoolLdsFloats / 2];
+    const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
+    const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
+    const int HW = H * W, OHW = OH * OW;
+    const int nc0 = blockIdx.x * PB;
+    const int np = min(PB, NC - nc0);
+    const size_t obase = (size_t)nc0 * OHW;
+    const int ne = np * OHW;
+    for (int e0 = threadIdx.x; e0 < ne; e0 += 256 * 4) {
+        float g[4];
+        int32_t m[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const bool in = e0 + 256 * u < ne;
+            g[u] = in ? dy[obase + e0 + 256 * u] : 0.f;
+            m[u] = in ? mask[obase + e0 + 256 * u] : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (e0 + 256 * u < ne) {
+                gs[e0 + 256 * u] = g[u];
+                ms[e0 + 256 * u] = m[u];
+            }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < np * HW; e += 256) {
+        const int pl = udiv(e, div_hw);
+        const int p = e - pl * HW;
+        const int h = udiv(p, div_w);
+        const int w = p - h * W;
+        const int i0 = max(0, (h + ph - kh + sh) / sh);
+        const int i1 = min(OH - 1, (h + ph) / sh);
+        const int j0 = max(0, (w + pw - kw + sw) / sw);
+        const int j1 = min(OW - 1, (w + pw) / sw);
+        const int ob = pl * OHW;
+        float sum = 0.f;
+        if constexpr (KS > 0) {
+            // covering windows read first (indices clamped into the plane),
+            // then added in row-major order where valid and routed here
+            constexpr int T = (KS + SS - 1) / SS;
+            int m[T][T];
+            float g[T][T];
+#pragma unroll
+            for (int di = 0; di < T; ++di)
+#pragma unroll
+                for (int dj = 0; dj < T; ++dj) {
+                    const int o = ob + min(i0 + di, OH - 1) * OW + min(j0 + dj, OW - 1);
+                    m[di][dj] = ms[o];
+                    g[di][dj] = gs[o];
+                }
+#pragma unroll
+            for (int di = 0; di < T; ++di)
+#pragma unroll
+                for (int dj = 0; dj < T; ++dj)
+                    if (i0 + di <= i1 && j0 + dj <= j1 && m[di][dj] == p)
+                        sum += g[di][dj];
+        } else {
+            for (int i = i0; i <= i1; ++i)
+                for (int j = j0; j <= j1; ++j) {
+                    const int o = ob + i * OW + j;
+                    if (ms[o] == p)
+                        sum += gs[o];
+                }
+        }
+        dx[(size_t)nc0 * HW + e] = sum;
+    }
+}
+
 static unsigned grid_for(long total)
 {
     long b = (total + 255) / 256;
@@ -202,6 +363,22 @@ hipError_t launch_maxpool_forward(const float* x, float* y, int32_t* mask, int N
     if ((long)NC * OH * OW == 0)
         return hipSuccess;
     const FastDiv d = make_fastdiv((uint32_t)OW);
+    if (H * W <= kPoolLdsFloats) {
+        // planes staged in LDS, as many whole planes per block as fit
+        const int PB = kPoolLdsFloats / (H * W);
+        const dim3 g((unsigned)((NC + PB - 1) / PB));
+        const FastDiv dohw = make_fastdiv((uint32_t)(OH * OW));
+        if (kh == 3 && kw == 3 && sh == 2 && sw == 2)
+            hipLaunchKernelGGL((maxpool_forward_lds_kernel<3, 2>), g, dim3(256), 0, s, x, y, mask,
+                               NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, PB, dohw, d, relu_input);
+        else if (kh == 2 && kw == 2 && sh == 2 && sw == 2)
+            hipLaunchKernelGGL((maxpool_forward_lds_kernel<2, 2>), g, dim3(256), 0, s, x, y, mask,
+                               NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, PB, dohw, d, relu_input);
+        else
+            hipLaunchKernelGGL((maxpool_forward_lds_kernel<0, 0>), g, dim3(256), 0, s, x, y, mask,
+                               NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, PB, dohw, d, relu_input);
+        return hipGetLastError();
+    }
     const dim3 grid = plane_grid(OH * OW, NC);
     if (kh == 3 && kw == 3 && sh == 2 && sw == 2)
         hipLaunchKernelGGL((maxpool_forward_kernel<3, 2>), grid, dim3(256), 0, s, x, y, mask, NC,
@@ -222,6 +399,21 @@ hipError_t launch_maxpool_backward(const float* dy, const int32_t* mask, float* 
     if ((long)NC * H * W == 0)
         return hipSuccess;
     const FastDiv d = make_fastdiv((uint32_t)W);
+    if (OH * OW <= kPoolLdsFloats / 2) {
+        const int PB = (kPoolLdsFloats / 2) / (OH * OW);
+        const dim3 g((unsigned)((NC + PB - 1) / PB));
+        const FastDiv dhw = make_fastdiv((uint32_t)(H * W));
+        if (kh == 3 && kw == 3 && sh == 2 && sw == 2)
+            hipLaunchKernelGGL((maxpool_backward_lds_kernel<3, 2>), g, dim3(256), 0, s, dy, mask,
+                               dx, NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, PB, dhw, d);
+        else if (kh == 2 && kw == 2 && sh == 2 && sw == 2)
+            hipLaunchKernelGGL((maxpool_backward_lds_kernel<2, 2>), g, dim3(256), 0, s, dy, mask,
+                               dx, NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, PB, dhw, d);
+        else
+            hipLaunchKernelGGL((maxpool_backward_lds_kernel<0, 0>), g, dim3(256), 0, s, dy, mask,
+                               dx, NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, PB, dhw, d);
+        return hipGetLastError();
+    }
     const dim3 grid = plane_grid(H * W, NC);
     if (kh == 3 && kw == 3 && sh == 2 && sw == 2)
         hipLaunchKernelGGL((maxpool_backward_kernel<3, 2>), grid, dim3(256), 0, s, dy, mask, dx,

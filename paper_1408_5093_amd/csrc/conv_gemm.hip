@@ -119,9 +119,10 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     // ---- A mapping: k = tid % TK, m = tid / TK + (NT / TK) * q
     const int a_k = tid % TK;
     const int a_m = tid / TK;
-    // A rows m0 + a_m + (NT/TK)*q: offsets linear in q, valid while m < M
-    const int a_row0 = (g * M + m0 + a_m) * R;
-    const int a_rows_ok = M - (m0 + a_m);
+    // A rows m0 + a_m + (NT/TK)*q, byte offsets linear in q.  Rows past M need
+    // no mask: they only feed accumulator rows the epilogue never stores, and
+    // their loads stay inside the weights or read 0.
+    const uint32_t a_base4 = (uint32_t)((g * M + m0 + a_m) * R) * 4u;
 
     // ---- B mapping: column(s) fixed per thread, reduction rows vary
     int b_base[BC], b_ih0[BC], b_iw0[BC];
@@ -148,14 +149,13 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     float rA[EA], rB[EB];
 
     auto load_a = [&](int kbase) {
+        const int r = kbase + a_k;
+        // the channel-blocked order covers R in whole stages (R % TK == 0)
+        const uint32_t rbad = TAP ? 0u : (uint32_t)(r >= R) << 31;
+        const uint32_t r4 = a_base4 + (uint32_t)r * 4u;
 #pragma unroll
-        for (int q = 0; q < EA; ++q) {
-            const int r = kbase + a_k;
-            const uint32_t bad =
-                ((uint32_t)((NT / TK) * q >= a_rows_ok) | (uint32_t)(r >= R)) << 31;
-            const uint32_t off = ((uint32_t)(a_row0 + (NT / TK) * q * R + r) * 4u) | bad;
-            rA[q] = buf_ld_f32(ra, off);
-        }
+        for (int q = 0; q < EA; ++q)
+            rA[q] = buf_ld_f32(ra, (r4 + (uint32_t)((NT / TK) * q * R) * 4u) | rbad);
     };
 
     // Channel-blocked reduction order r = (c / TK, u, v, c % TK): Cin_g is a

@@ -74,15 +74,28 @@ conv_wgrad_f32_kernel(const WgradParams p)
     const int kc = tid % TK;  // reduction index within a stage
     const int rw = tid / TK;  // row within one pass
 
-    // Per-thread A rows (output channels) and B rows (taps), fixed for the kernel.
-    // A rows m0 + rw + RS*q: offsets are linear in q, validity is m < Kg
+    // Per-thread A rows (output channels) and B rows (taps), fixed for the
+    // kernel.  Neither needs a row mask: A rows past Kg and B rows past R only
+    // feed accumulator rows / columns that the epilogue never stores, and
+    // their loads stay inside the tensors or read 0.  A columns need none
+    // either: splits are whole stages, so the only columns past a split's end
+    // lie past Ncol, in images n >= N, which are outside D (read as 0).
     const int a_off0 = (g * p.Kg + m0 + rw) * OHW;
-    const int a_rows_ok = p.Kg - (m0 + rw);  // row q is valid iff RS*q < a_rows_ok
-    // Per-thread tap table.  With a compile-time kernel (PACK) each entry is
-    // one word: offset c*IH*IW + u*IW + v in bits 0..21, u in 22..26, v in
-    // 27..31 (the launcher checks Cg*IH*IW < 2^22 and kh, kw <= 32); taps past
-    // R are flagged in r_bad.
+    // Per-thread tap table.  MASKED (a compile-time kernel with kh*kw < 32):
+    // entry q packs the byte offset (c*IH*IW + u*IW + v) * 4 in bits 5..31 and
+    // the tap index u*kw + v in bits 0..4, and the bounds test reads the tap's
+    // bit of the column's in-image mask.  Otherwise, with a compile-time
+    // kernel (PACK): offset c*IH*IW + u*IW + v in bits 0..21, u in 22..26, v
+    // in 27..31 (the launcher checks Cg*IH*IW < 2^22 and kh, kw <= 32), taps
+    // past R flagged in r_bad.
     constexpr bool PACK = KH != 0;
+    constexpr bool MASKED = KH != 0 && KH * KW < 32;
+    constexpr uint32_t kRep = [] {
+        uint32_t r = 0;
+        for (int u = 0; u < (MASKED ? KH : 0); ++u)
+            r |= 1u << (u * KW);
+        return r;
+    }();
     int b_off[EB];
     int b_uv[PACK ? 1 : EB];
     uint32_t r_bad = 0;
@@ -96,7 +109,9 @@ conv_wgrad_f32_kernel(const WgradParams p)
         const int v = rr - u * kw;
         if (r >= p.R)
             r_bad |= 1u << q;
-        if constexpr (PACK) {
+        if constexpr (MASKED) {
+            b_off[q] = (int)((uint32_t)((c * IHW + u * IW + v) * 4) << 5 | (uint32_t)(u * KW + v));
+        } else if constexpr (PACK) {
             b_off[q] = (c * IHW + u * IW + v) | (u << 22) | (v << 27);
         } else {
             b_off[q] = c * IHW + u * IW + v;
@@ -118,39 +133,54 @@ conv_wgrad_f32_kernel(const WgradParams p)
         for (int q = 0; q < EB; ++q)
             asm volatile("" : "+v"(b_off[q]));
         const int col = cbase + kc;
-        const uint32_t cbad = (uint32_t)(col >= col_end) << 31;
         const int n = (int)fdiv((uint32_t)col, p.div_ohw);
         const int pix = col - n * OHW;
         const int i = (int)fdiv((uint32_t)pix, p.div_ow);
         const int j = pix - i * p.OW;
-        const int dbase = n * p.K * OHW + pix;
+        uint32_t dbase4 = (uint32_t)(n * p.K * OHW + pix + a_off0) * 4u;
+        // materialised once, so each row below is one add (left alone, the
+        // compiler re-derives every row's offset with a 64-bit multiply-add)
+        asm volatile("" : "+v"(dbase4));
         const int ih0 = i * sh - p.ph;
         const int iw0 = j * sw - p.pw;
         const int xbase = (n * p.C + g * p.Cg) * IHW + ih0 * IW + iw0;
 #pragma unroll
-        for (int q = 0; q < EA; ++q) {
-            const uint32_t bad = (uint32_t)(RS * q >= a_rows_ok) << 31;
-            const uint32_t off =
-                ((uint32_t)(dbase + a_off0 + RS * q * OHW) * 4u) | cbad | bad;
-            rA[q] = buf_ld_f32(rd, off);
-        }
+        for (int q = 0; q < EA; ++q)
+            rA[q] = buf_ld_f32(rd, dbase4 + (uint32_t)(RS * q * OHW) * 4u);
+        if constexpr (MASKED) {
+            // taps of this column's window that lie in the image, bit u*KW + v
+            // (none for a column past Ncol)
+            const int ulo = min(max(-ih0, 0), KH), uhi = max(min(IH - ih0, KH), ulo);
+            const int vlo = min(max(-iw0, 0), KW), vhi = max(min(IW - iw0, KW), vlo);
+            const uint32_t wbits = (1u << vhi) - (1u << vlo);
+            const uint32_t rows = (1u << (uhi * KW)) - (1u << (ulo * KW));
+            const uint32_t nok = col < p.Ncol ? ~(wbits * kRep & rows) : ~0u;
+            const uint32_t xb4 = (uint32_t)xbase * 4u;
 #pragma unroll
-        for (int q = 0; q < EB; ++q) {
-            int ih, iw, boff;
-            if constexpr (PACK) {
-                ih = ih0 + ((b_off[q] >> 22) & 31);
-                iw = iw0 + ((uint32_t)b_off[q] >> 27);
-                boff = b_off[q] & 0x3fffff;
-            } else {
-                ih = ih0 + (b_uv[q] & 0xffff);
-                iw = iw0 + (b_uv[q] >> 16);
-                boff = b_off[q];
+            for (int q = 0; q < EB; ++q) {
+                const uint32_t e = (uint32_t)b_off[q];
+                rB[q] = buf_ld_f32(rx, (xb4 + (e >> 5)) | (((nok >> (e & 31u)) & 1u) << 31));
             }
-            const uint32_t bad = ((uint32_t)((unsigned)ih >= (unsigned)IH) |
-                                  (uint32_t)((unsigned)iw >= (unsigned)IW)) << 31;
-            const uint32_t off = ((uint32_t)(xbase + boff) * 4u) | cbad | bad |
-                                 (((r_bad >> q) & 1u) << 31);
-            rB[q] = buf_ld_f32(rx, off);
+        } else {
+            const uint32_t cbad = (uint32_t)(col >= col_end) << 31;
+#pragma unroll
+            for (int q = 0; q < EB; ++q) {
+                int ih, iw, boff;
+                if constexpr (PACK) {
+                    ih = ih0 + ((b_off[q] >> 22) & 31);
+                    iw = iw0 + ((uint32_t)b_off[q] >> 27);
+                    boff = b_off[q] & 0x3fffff;
+                } else {
+                    ih = ih0 + (b_uv[q] & 0xffff);
+                    iw = iw0 + (b_uv[q] >> 16);
+                    boff = b_off[q];
+                }
+                const uint32_t bad = ((uint32_t)((unsigned)ih >= (unsigned)IH) |
+                                      (uint32_t)((unsigned)iw >= (unsigned)IW)) << 31;
+                const uint32_t off = ((uint32_t)(xbase + boff) * 4u) | cbad | bad |
+                                     (((r_bad >> q) & 1u) << 31);
+                rB[q] = buf_ld_f32(rx, off);
+            }
         }
     };
 

@@ -450,7 +450,6 @@ lrn_forward_kernel(const float* __restrict__ x, float* __restrict__ y, int N, in
                    int nchunks, FastDiv div_hw, float alpha_over_n, float beta, float k)
 {
     constexpr int PRE = (SIZE - 1) / 2;
-    constexpr int POST = SIZE - 1 - PRE;
     constexpr int NA = CH + SIZE - 1;
     const int e = blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= N * nchunks * HW)
@@ -459,23 +458,28 @@ lrn_forward_kernel(const float* __restrict__ x, float* __restrict__ y, int N, in
     const int pix = e - rest * HW;
     const int n = rest / nchunks;
     const int c0 = (rest - n * nchunks) * CH;
-    const float* col = x + n * C * HW + pix;
+    // Range-checked buffer accesses: a channel outside [0, C) gets an offset
+    // with bit 31 set, which reads 0 / drops the store, so every load is
+    // unconditional and all of them are in flight together.
+    const uint32_t bytes = (uint32_t)(N * C * HW) * 4u;
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, bytes);
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(y, bytes);
+    const uint32_t base4 = (uint32_t)(n * C * HW + pix) * 4u;
+    const uint32_t hw4 = (uint32_t)HW * 4u;
+    auto off = [&](int ch) {
+        return (base4 + (uint32_t)ch * hw4) | ((uint32_t)((unsigned)ch >= (unsigned)C) << 31);
+    };
     float a[NA];  // channels c0 - PRE .. c0 + CH - 1 + POST
 #pragma unroll
-    for (int q = 0; q < NA; ++q) {
-        const int ch = c0 - PRE + q;
-        a[q] = (ch >= 0 && ch < C) ? col[ch * HW] : 0.f;
-    }
+    for (int q = 0; q < NA; ++q)
+        a[q] = buf_ld_f32(rx, off(c0 - PRE + q));
 #pragma unroll
     for (int t = 0; t < CH; ++t) {
-        const int c = c0 + t;
-        if (c < C) {
-            float sq = 0.f;
+        float sq = 0.f;
 #pragma unroll
-            for (int q = 0; q < SIZE; ++q)
-                sq += a[t + q] * a[t + q];
-            y[n * C * HW + c * HW + pix] = a[t + PRE] * pow_neg(k + alpha_over_n * sq, beta);
-        }
+        for (int q = 0; q < SIZE; ++q)
+            sq += a[t + q] * a[t + q];
+        buf_st_f32(a[t + PRE] * pow_neg(k + alpha_over_n * sq, beta), ry, off(c0 + t));
     }
 }
 
@@ -497,19 +501,25 @@ lrn_backward_kernel(const float* __restrict__ x, const float* __restrict__ y,
     const int pix = e - rest * HW;
     const int n = rest / nchunks;
     const int c0 = (rest - n * nchunks) * CH;
-    const int base = n * C * HW + pix;
+    // range-checked buffer accesses, as in the forward kernel
+    const uint32_t bytes = (uint32_t)(N * C * HW) * 4u;
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, bytes);
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(y, bytes);
+    const __amdgpu_buffer_rsrc_t rg = make_rsrc(dy, bytes);
+    const __amdgpu_buffer_rsrc_t rd = make_rsrc(dx, bytes);
+    const uint32_t base4 = (uint32_t)(n * C * HW + pix) * 4u;
+    const uint32_t hw4 = (uint32_t)HW * 4u;
+    auto off = [&](int ch) {
+        return (base4 + (uint32_t)ch * hw4) | ((uint32_t)((unsigned)ch >= (unsigned)C) << 31);
+    };
     float a[NA], g[NR], b[NR];
 #pragma unroll
-    for (int q = 0; q < NA; ++q) {
-        const int ch = c0 - POST - PRE + q;
-        a[q] = (ch >= 0 && ch < C) ? x[base + ch * HW] : 0.f;
-    }
+    for (int q = 0; q < NA; ++q)
+        a[q] = buf_ld_f32(rx, off(c0 - POST - PRE + q));
 #pragma unroll
     for (int q = 0; q < NR; ++q) {
-        const int ch = c0 - POST + q;
-        const bool in = ch >= 0 && ch < C;
-        g[q] = in ? dy[base + ch * HW] : 0.f;
-        b[q] = in ? y[base + ch * HW] : 0.f;
+        g[q] = buf_ld_f32(rg, off(c0 - POST + q));
+        b[q] = buf_ld_f32(ry, off(c0 - POST + q));
     }
     float r[NR], sc[CH];
 #pragma unroll
@@ -519,22 +529,20 @@ lrn_backward_kernel(const float* __restrict__ x, const float* __restrict__ y,
         for (int t = 0; t < SIZE; ++t)
             sq += a[q + t] * a[q + t];
         const float s = k + alpha_over_n * sq;
-        r[q] = g[q] * b[q] / s;
+        // hardware reciprocal (about 1 ulp): s >= k > 0
+        r[q] = g[q] * b[q] * __builtin_amdgcn_rcpf(s);
         if (q >= POST && q < POST + CH)
             sc[q - POST] = s;
     }
     const float coef = 2.f * alpha_over_n * beta;
 #pragma unroll
     for (int t = 0; t < CH; ++t) {
-        const int c = c0 + t;
-        if (c < C) {
-            float cross = 0.f;
+        float cross = 0.f;
 #pragma unroll
-            for (int q = 0; q < SIZE; ++q)
-                cross += r[t + q];
-            dx[base + c * HW] =
-                g[t + POST] * pow_neg(sc[t], beta) - coef * a[t + POST + PRE] * cross;
-        }
+        for (int q = 0; q < SIZE; ++q)
+            cross += r[t + q];
+        buf_st_f32(g[t + POST] * pow_neg(sc[t], beta) - coef * a[t + POST + PRE] * cross, rd,
+                   off(c0 + t));
     }
 }
 

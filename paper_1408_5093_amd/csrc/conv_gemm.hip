@@ -179,21 +179,44 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
         }
     };
 
-    // Channel-major order r = (c, u, v) for any Cin_g.
-    auto load_b_any = [&](int kbase) {
+    // Channel-major order r = (c, u, v) for any Cin_g.  The tap decomposition
+    // is wave-uniform (scalar).  Out-of-range taps get an offset with bit 31
+    // set; a wave whose columns all have their whole window inside the image
+    // (every wave of an unpadded layer) skips the per-tap bounds test.
+    bool b_inside = true;
 #pragma unroll
-        for (int q = 0; q < EB; ++q) {
-            const int cc = b_cc(q);
-            const int r = __builtin_amdgcn_readfirstlane(kbase + b_row(q));
-            const int c = r / khw;
-            const int rr = r - c * khw;
-            const int u = rr / kw;
-            const int v = rr - u * kw;
-            const int ih = b_ih0[cc] + u;
-            const int iw = b_iw0[cc] + v;
-            const bool ok = r < R && (unsigned)ih < (unsigned)IH && (unsigned)iw < (unsigned)IW;
-            const uint32_t off = ok ? (uint32_t)(b_base[cc] + c * IHW + u * IW + v) * 4u : kOob;
-            rB[q] = buf_ld_f32(rx, off);
+    for (int cc = 0; cc < BC; ++cc)
+        b_inside = b_inside && b_ih0[cc] >= 0 && b_ih0[cc] + kh <= IH && b_iw0[cc] >= 0 &&
+                   b_iw0[cc] + kw <= IW;
+    const bool b_all_inside = __all(b_inside);
+    auto load_b_any = [&](int kbase) {
+        if (b_all_inside) {
+#pragma unroll
+            for (int q = 0; q < EB; ++q) {
+                const int r = __builtin_amdgcn_readfirstlane(kbase + b_row(q));
+                const int c = r / khw;
+                const int rr = r - c * khw;
+                const int u = rr / kw;
+                const int v = rr - u * kw;
+                const uint32_t rbad = r < R ? 0u : kOob;
+                rB[q] = buf_ld_f32(rx, ((uint32_t)(b_base[b_cc(q)] + c * IHW + u * IW + v) * 4u) |
+                                           rbad);
+            }
+        } else {
+#pragma unroll
+            for (int q = 0; q < EB; ++q) {
+                const int cc = b_cc(q);
+                const int r = __builtin_amdgcn_readfirstlane(kbase + b_row(q));
+                const int c = r / khw;
+                const int rr = r - c * khw;
+                const int u = rr / kw;
+                const int v = rr - u * kw;
+                const int ih = b_ih0[cc] + u;
+                const int iw = b_iw0[cc] + v;
+                const uint32_t bad = ((uint32_t)(r >= R) | (uint32_t)((unsigned)ih >= (unsigned)IH) |
+                                      (uint32_t)((unsigned)iw >= (unsigned)IW)) << 31;
+                rB[q] = buf_ld_f32(rx, ((uint32_t)(b_base[cc] + c * IHW + u * IW + v) * 4u) | bad);
+            }
         }
     };
 

@@ -286,7 +286,7 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     q.wgrad_xcd_order = env_tile("CAFFE_CONV_WGRAD_XCD_ORDER") > 0;
     q.fwd_tap = q.Cg % gemm_tile_k(q.fwd_tile) == 0;
     q.dgrad_tap = q.Kg % gemm_tile_k(q.dgrad_tile) == 0;
-    q.ws_fwd = q.fwd_tap ? align_up(q.weight_elems * 4, kWsAlign) : 0;
+    q.ws_fwd = align_up(q.weight_elems * 4, kWsAlign);  // the packed weights
 
     if (q.dtype == CAFFE_BF16)
         return plan_bf16(&q);
@@ -355,16 +355,14 @@ int run_forward(const ConvPlan& q, const void* bottom, const void* weight, const
 {
     if (q.top_elems == 0)
         return CAFFE_OK;
-    const void* A = weight;
-    if (q.fwd_tap) {
-        float* wp = (float*)ws;
-        LAUNCH(launch_pack_weights_blocked((const float*)weight, wp, q.K, q.Cg, q.kh * q.kw,
-                                           gemm_tile_k(q.fwd_tile), q.blocked, s),
-               "weight pack launch");
-        A = wp;
-    }
+    // weights transposed to [group][r][m] in the kernel's reduction order
+    float* wp = (float*)ws;
+    LAUNCH(launch_pack_weights((const float*)weight, wp, q.G, q.Kg, q.Cg, q.kh * q.kw,
+                               gemm_tile_k(q.fwd_tile), q.fwd_tap ? (q.blocked ? 1 : -1) : 0,
+                               s),
+           "weight pack launch");
     ConvGemmParams p = {};
-    p.A = A;
+    p.A = wp;
     p.X = bottom;
     p.Y = top;
     p.bias = bias;

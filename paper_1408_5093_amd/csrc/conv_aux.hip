@@ -68,9 +68,10 @@ hipError_t launch_relu_mask_bias(const float* G, const float* Y, float* D, float
     return hipGetLastError();
 }
 
-// Wt[g][m = (c, fh, fw)][r] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)],
+// Wt[g][r][m = (c, fh, fw)] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)],
 // 0 past the kernel edge; r = (k, th, tw), or r = (k / tk, th, tw, k % tk)
-// when tk > 0.
+// when tk > 0, or r = (th, tw, k) when tk < 0.  m is contiguous (the layout
+// the GEMM copies into LDS).
 __global__ void __launch_bounds__(256)
 dgrad_weight_transform_kernel(const float* __restrict__ W, float* __restrict__ Wt, int G, int Kg,
                               int Cg, int kh, int kw, int sh, int sw, int Th, int Tw, int tk)
@@ -80,10 +81,10 @@ dgrad_weight_transform_kernel(const float* __restrict__ W, float* __restrict__ W
     const long total = (long)G * Mt * Rt;
     for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < total;
          e += (long)gridDim.x * blockDim.x) {
-        const int r = (int)(e % Rt);
-        const long gm = e / Rt;
-        const int m = (int)(gm % Mt);
-        const int g = (int)(gm / Mt);
+        const int m = (int)(e % Mt);
+        const long gr = e / Mt;
+        const int r = (int)(gr % Rt);
+        const int g = (int)(gr / Rt);
         int k, t;
         if (tk > 0) {  // r = (k / tk, th, tw, k % tk)
             const int ki = r % tk;

@@ -55,6 +55,17 @@ struct Mfma<16> {
     static __device__ __forceinline__ int row(int q, int lane) { return 4 * (lane >> 4) + q; }
 };
 
+typedef __attribute__((address_space(3))) void lds_void;
+
+// One wave copies 64 consecutive floats into LDS at `dst` (wave-uniform):
+// lane i's element from byte offset voff + soff lands at dst + 4*i.  An offset
+// with bit 31 set is out of range and writes 0.
+__device__ __forceinline__ void copy_to_lds(__amdgpu_buffer_rsrc_t r, float* dst, uint32_t voff,
+                                            uint32_t soff)
+{
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 4, voff, soff, 0, 0);
+}
+
 template <int MT, int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH, int SW, int EPI,
           bool TAP, bool MASK>
 __global__ void __launch_bounds__(64 * WM * WN)
@@ -62,24 +73,31 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
 {
     typedef Mfma<MT> Op;
     constexpr int NT = 64 * WM * WN;
+    constexpr int NW = NT / 64;          // waves
     constexpr int TM = WM * MI * MT;
     constexpr int TN = WN * NI * MT;
-    constexpr int EA = TM * TK / NT;  // A elements per thread per stage
-    constexpr int EB = TN * TK / NT;  // B elements per thread per stage
     constexpr int KS = TK / Op::kStep;
-    static_assert(TM * TK % NT == 0 && TN * TK % NT == 0, "tile/thread mismatch");
-    static_assert(NT % TK == 0, "A mapping needs TK | NT");
-    static_assert(TN % 64 == 0 && (NT % TN == 0 || TN % NT == 0), "B mapping");
+    constexpr int NC = TN / 64;          // 64-column copies per B row of the tile
+    constexpr int NA = TK * TM / 64 / NW;  // A copies per wave per stage
+    constexpr int NB = TK * NC / NW;       // B copies per wave per stage
+    static_assert(TN % 64 == 0 && NW % NC == 0, "B copy mapping");
+    static_assert(TK * TM % (64 * NW) == 0 && TK * NC % NW == 0, "copy split");
     static_assert(TK % Op::kStep == 0, "stage depth");
-    constexpr int BC = TN > NT ? TN / NT : 1;  // distinct B columns per thread
-    // Row strides: A rows are written with lanes along k, so a stride of
-    // 2 (mod 32) keeps those writes conflict-free.  The 16x16x4 fragments read
-    // four k rows at once, so B rows then get a stride of 16 (mod 32).
-    constexpr int PADA = 2;
-    constexpr int PADB = MT == 16 ? 16 : 0;
+    // A is staged as the flat [TK][TM] array (row stride TM: 96 and 48 put the
+    // k rows a fragment read touches on distinct banks); B rows hold whole
+    // 64-column copies, with a stride of 16 (mod 32) for the 16x16x4
+    // fragments, which read four k rows at once.
+    constexpr int LDA = TM;
+    constexpr int LDB = TN + (MT == 16 ? 16 : 0);
 
-    __shared__ float As[2][TK][TM + PADA];
-    __shared__ float Bs[2][TK][TN + PADB];
+    // One array per pipeline buffer: with the buffer a compile-time choice
+    // (the stage loop below is unrolled by two), the compiler can tell the
+    // copies into one buffer from the fragment reads of the other and inserts
+    // no waits between them.
+    __shared__ float As0[TK][LDA], As1[TK][LDA];
+    __shared__ float Bs0[TK][LDB], Bs1[TK][LDB];
+    typedef float ATile[TK][LDA];
+    typedef float BTile[TK][LDB];
 
     const int kh = KH ? KH : p.kh;
     const int kw = KW ? KW : p.kw;
@@ -116,118 +134,103 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.A, p.A_bytes);
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, p.X_bytes);
 
-    // ---- A mapping: k = tid % TK, m = tid / TK + (NT / TK) * q
-    const int a_k = tid % TK;
-    const int a_m = tid / TK;
-    // A rows m0 + a_m + (NT/TK)*q, byte offsets linear in q.  Rows past M need
-    // no mask: they only feed accumulator rows the epilogue never stores, and
-    // their loads stay inside the weights or read 0.
-    const uint32_t a_base4 = (uint32_t)((g * M + m0 + a_m) * R) * 4u;
-
-    // ---- B mapping: column(s) fixed per thread, reduction rows vary
-    int b_base[BC], b_ih0[BC], b_iw0[BC];
+    // Operands go from global memory straight to LDS, one wave copy = 64
+    // consecutive floats.  A copy j of a stage (j = wave + NW*q) covers the
+    // flat elements 64*j .. 64*j + 63 of the [TK][TM] A tile: lane l takes
+    // k row (64*j + l) / TM, tile row (64*j + l) % TM of A (laid out
+    // [group][r][m], m contiguous); its offset without the stage's k base is
+    // fixed for the kernel.  B copy j covers k row j / NC, columns
+    // n0 + 64*(j % NC) + lane; a wave's column is fixed and its k rows advance
+    // by NW / NC per copy.
+    // A rows past M need no mask: they only feed accumulator rows the
+    // epilogue never stores, and their loads stay inside A or read 0.
+    // (When TM is a multiple of 64 a copy's k row and column offset are
+    // wave-uniform and go to the scalar offset; one lane offset serves all.)
+    constexpr bool A_UNIFORM = TM % 64 == 0;
+    uint32_t a_voff[A_UNIFORM ? 1 : NA];
 #pragma unroll
-    for (int cc = 0; cc < BC; ++cc) {
-        const int col = n0 + (TN > NT ? tid + NT * cc : tid % TN);
-        if (col < p.Ncol) {
-            const int n = col / OHW;
-            const int pix = col - n * OHW;
-            const int i = pix / p.OW;
-            const int j = pix - i * p.OW;
-            b_ih0[cc] = i * sh - p.ph;
-            b_iw0[cc] = j * sw - p.pw;
-            b_base[cc] = (n * p.Cin + g * Cin_g) * IHW + b_ih0[cc] * IW + b_iw0[cc];
-        } else {
-            b_ih0[cc] = -(1 << 28);  // fails every bounds check
-            b_iw0[cc] = 0;
-            b_base[cc] = 0;
-        }
+    for (int q = 0; q < (A_UNIFORM ? 1 : NA); ++q) {
+        const int flat = A_UNIFORM ? lane : 64 * (wave + NW * q) + lane;
+        const int k = flat / TM;
+        a_voff[q] = (uint32_t)((g * R + k) * M + m0 + flat - k * TM) * 4u;
     }
-    auto b_row = [&](int q) { return TN > NT ? q / BC : tid / TN + (NT / TN) * q; };
-    auto b_cc = [&](int q) { return TN > NT ? q % BC : 0; };
+    const uint32_t a_row4 = (uint32_t)M * 4u;
+    const int b_nc = wave % NC;
+    int b_ih0, b_iw0, b_base;
+    uint32_t b_cbad;
+    {
+        const int col = n0 + b_nc * 64 + lane;
+        const int n = col / OHW;
+        const int pix = col - n * OHW;
+        const int i = pix / p.OW;
+        const int j = pix - i * p.OW;
+        b_ih0 = i * sh - p.ph;
+        b_iw0 = j * sw - p.pw;
+        b_base = (n * p.Cin + g * Cin_g) * IHW + b_ih0 * IW + b_iw0;
+        b_cbad = col < p.Ncol ? 0u : kOob;
+    }
+    auto b_row = [&](int q) { return (wave + NW * q) / NC; };
 
-    float rA[EA], rB[EB];
-
-    auto load_a = [&](int kbase) {
-        const int r = kbase + a_k;
-        // the channel-blocked order covers R in whole stages (R % TK == 0)
-        const uint32_t rbad = TAP ? 0u : (uint32_t)(r >= R) << 31;
-        const uint32_t r4 = a_base4 + (uint32_t)r * 4u;
+    auto copy_a = [&](ATile& dst, int kbase) {
 #pragma unroll
-        for (int q = 0; q < EA; ++q)
-            rA[q] = buf_ld_f32(ra, (r4 + (uint32_t)((NT / TK) * q * R) * 4u) | rbad);
+        for (int q = 0; q < NA; ++q) {
+            float* d = &dst[0][0] + 64 * (wave + NW * q);
+            if constexpr (A_UNIFORM) {
+                const int k = 64 * (wave + NW * q) / TM;
+                const uint32_t mo = (uint32_t)(64 * (wave + NW * q) - k * TM) * 4u;
+                // (the channel-blocked order covers R in whole stages, R % TK == 0)
+                const bool rok = TAP || kbase + k < R;
+                copy_to_lds(ra, d, rok ? a_voff[0] : kOob,
+                            rok ? (uint32_t)(kbase + k) * a_row4 + mo : 0u);
+            } else if constexpr (TAP) {
+                copy_to_lds(ra, d, a_voff[q], (uint32_t)kbase * a_row4);
+            } else {
+                const int k = (64 * (wave + NW * q) + lane) / TM;
+                copy_to_lds(ra, d, kbase + k < R ? a_voff[q] : kOob,
+                            kbase + k < R ? (uint32_t)kbase * a_row4 : 0u);
+            }
+        }
     };
 
-    // Channel-blocked reduction order r = (c / TK, u, v, c % TK): Cin_g is a
-    // multiple of TK, so a stage covers TK channels of a single tap (u, v);
-    // the tap's bounds check and address are computed once per column per
-    // stage.  All taps of a channel block run back to back, so a workgroup
-    // re-reads the same TK channel planes (from L1/L2) tap after tap.
-    auto load_b_tap = [&](int u, int v, int c0) {
-        uint32_t voff[BC];
+    // Channel-blocked order r = (c / TK, u, v, c % TK) (or tap-major
+    // (u, v, c)): a stage covers TK channels of a single tap (u, v), so the
+    // column's bounds test and address are formed once per stage and each
+    // copy only adds its channel's plane offset as the uniform soffset.
+    auto copy_b_tap = [&](BTile& dst, int u, int v, int c0) {
+        const int ih = b_ih0 + u;
+        const int iw = b_iw0 + v;
+        const bool ok = (unsigned)ih < (unsigned)IH && (unsigned)iw < (unsigned)IW;
+        const uint32_t voff = (ok ? (uint32_t)(b_base + u * IW + v) * 4u : kOob) | b_cbad;
 #pragma unroll
-        for (int cc = 0; cc < BC; ++cc) {
-            const int ih = b_ih0[cc] + u;
-            const int iw = b_iw0[cc] + v;
-            const bool ok = (unsigned)ih < (unsigned)IH && (unsigned)iw < (unsigned)IW;
-            voff[cc] = ok ? (uint32_t)(b_base[cc] + u * IW + v) * 4u : kOob;
-        }
-#pragma unroll
-        for (int q = 0; q < EB; ++q) {
-            const uint32_t coff = (uint32_t)((c0 + b_row(q)) * IHW) * 4u;
-            rB[q] = buf_ld_f32(rx, voff[b_cc(q)] + coff);
-        }
+        for (int q = 0; q < NB; ++q)
+            copy_to_lds(rx, &dst[b_row(q)][b_nc * 64], voff,
+                        (uint32_t)((c0 + b_row(q)) * IHW) * 4u);
     };
 
     // Channel-major order r = (c, u, v) for any Cin_g.  The tap decomposition
     // is wave-uniform (scalar).  Out-of-range taps get an offset with bit 31
     // set; a wave whose columns all have their whole window inside the image
     // (every wave of an unpadded layer) skips the per-tap bounds test.
-    bool b_inside = true;
-#pragma unroll
-    for (int cc = 0; cc < BC; ++cc)
-        b_inside = b_inside && b_ih0[cc] >= 0 && b_ih0[cc] + kh <= IH && b_iw0[cc] >= 0 &&
-                   b_iw0[cc] + kw <= IW;
+    const bool b_inside =
+        b_ih0 >= 0 && b_ih0 + kh <= IH && b_iw0 >= 0 && b_iw0 + kw <= IW;
     const bool b_all_inside = __all(b_inside);
-    auto load_b_any = [&](int kbase) {
-        if (b_all_inside) {
+    auto copy_b_any = [&](BTile& dst, int kbase) {
 #pragma unroll
-            for (int q = 0; q < EB; ++q) {
-                const int r = __builtin_amdgcn_readfirstlane(kbase + b_row(q));
-                const int c = r / khw;
-                const int rr = r - c * khw;
-                const int u = rr / kw;
-                const int v = rr - u * kw;
-                const uint32_t rbad = r < R ? 0u : kOob;
-                rB[q] = buf_ld_f32(rx, ((uint32_t)(b_base[b_cc(q)] + c * IHW + u * IW + v) * 4u) |
-                                           rbad);
+        for (int q = 0; q < NB; ++q) {
+            const int r = kbase + b_row(q);
+            const int c = r / khw;
+            const int rr = r - c * khw;
+            const int u = rr / kw;
+            const int v = rr - u * kw;
+            uint32_t bad = (r < R ? 0u : kOob) | b_cbad;
+            if (!b_all_inside) {
+                const int ih = b_ih0 + u;
+                const int iw = b_iw0 + v;
+                bad |= ((uint32_t)((unsigned)ih >= (unsigned)IH) |
+                        (uint32_t)((unsigned)iw >= (unsigned)IW)) << 31;
             }
-        } else {
-#pragma unroll
-            for (int q = 0; q < EB; ++q) {
-                const int cc = b_cc(q);
-                const int r = __builtin_amdgcn_readfirstlane(kbase + b_row(q));
-                const int c = r / khw;
-                const int rr = r - c * khw;
-                const int u = rr / kw;
-                const int v = rr - u * kw;
-                const int ih = b_ih0[cc] + u;
-                const int iw = b_iw0[cc] + v;
-                const uint32_t bad = ((uint32_t)(r >= R) | (uint32_t)((unsigned)ih >= (unsigned)IH) |
-                                      (uint32_t)((unsigned)iw >= (unsigned)IW)) << 31;
-                rB[q] = buf_ld_f32(rx, ((uint32_t)(b_base[cc] + c * IHW + u * IW + v) * 4u) | bad);
-            }
-        }
-    };
-
-    auto store_stage = [&](int buf) {
-#pragma unroll
-        for (int q = 0; q < EA; ++q)
-            As[buf][a_k][a_m + (NT / TK) * q] = rA[q];
-#pragma unroll
-        for (int q = 0; q < EB; ++q) {
-            const int col = TN > NT ? tid + NT * b_cc(q) : tid % TN;
-            Bs[buf][b_row(q)][col] = rB[q];
+            copy_to_lds(rx, &dst[b_row(q)][b_nc * 64],
+                        ((uint32_t)(b_base + c * IHW + u * IW + v) * 4u) | bad, 0u);
         }
     };
 
@@ -259,79 +262,91 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     // also stalled on the next stage's global loads.
     int tu = 0, tv = 0, tc = 0;
 
-    load_a(0);
+    copy_a(As0, 0);
     if constexpr (TAP)
-        load_b_tap(0, 0, 0);
+        copy_b_tap(Bs0, 0, 0, 0);
     else
-        load_b_any(0);
-    store_stage(0);
+        copy_b_any(Bs0, 0);
+    __builtin_amdgcn_s_waitcnt(kVmcnt0);
     __syncthreads();
 
     const int arow = wm * MI * MT + lane % MT;
     const int bcol = wn * NI * MT + lane % MT;
     const int kl = lane / MT;
 
-    for (int s = 0; s < nst; ++s) {
-        const int cur = s & 1;
-        if (s + 1 < nst) {
-            load_a((s + 1) * TK);
-            if constexpr (TAP) {
-                if (p.blocked) {  // (c / TK, u, v, c % TK)
-                    if (++tv == kw) {
-                        tv = 0;
-                        if (++tu == kh) {
-                            tu = 0;
-                            tc += TK;
-                        }
-                    }
-                } else {          // (u, v, c)
-                    tc += TK;
-                    if (tc == Cin_g) {
-                        tc = 0;
+    // The stage loop is unrolled by two so that each half has its buffers
+    // fixed: half h copies stage s + h + 1 into buffer 1 - h and multiplies
+    // the fragments of stage s + h from buffer h.
+    for (int s0 = 0; s0 < nst; s0 += 2) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int s = s0 + h;
+            if (s >= nst)
+                break;
+            ATile& Ac = h ? As1 : As0;
+            BTile& Bc = h ? Bs1 : Bs0;
+            ATile& An = h ? As0 : As1;
+            BTile& Bn = h ? Bs0 : Bs1;
+            if (s + 1 < nst) {
+                copy_a(An, (s + 1) * TK);
+                if constexpr (TAP) {
+                    if (p.blocked) {  // (c / TK, u, v, c % TK)
                         if (++tv == kw) {
                             tv = 0;
-                            ++tu;
+                            if (++tu == kh) {
+                                tu = 0;
+                                tc += TK;
+                            }
+                        }
+                    } else {          // (u, v, c)
+                        tc += TK;
+                        if (tc == Cin_g) {
+                            tc = 0;
+                            if (++tv == kw) {
+                                tv = 0;
+                                ++tu;
+                            }
                         }
                     }
+                    copy_b_tap(Bn, tu, tv, tc);
+                } else {
+                    copy_b_any(Bn, (s + 1) * TK);
                 }
-                load_b_tap(tu, tv, tc);
-            } else {
-                load_b_any((s + 1) * TK);
             }
-        }
-        // Rolling fragment prefetch: the LDS reads of k-step ks + PF are issued
-        // before the MFMAs of k-step ks (a ring of PF + 1 fragment sets).  The
-        // scheduling barriers pin that order; left alone, the scheduler trades
-        // it for fewer registers and waits on LDS before every k-step.
-        constexpr int PF = KS > 2 ? 2 : KS - 1;
-        float fa[PF + 1][MI], fb[PF + 1][NI];
-        auto read_frag = [&](int ks, int slot) {
-#pragma unroll
-            for (int mi = 0; mi < MI; ++mi)
-                fa[slot][mi] = As[cur][ks * Op::kStep + kl][arow + mi * MT];
-#pragma unroll
-            for (int ni = 0; ni < NI; ++ni)
-                fb[slot][ni] = Bs[cur][ks * Op::kStep + kl][bcol + ni * MT];
-        };
-#pragma unroll
-        for (int ks = 0; ks < PF; ++ks)
-            read_frag(ks, ks);
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            if (ks + PF < KS)
-                read_frag(ks + PF, (ks + PF) % (PF + 1));
             __builtin_amdgcn_sched_barrier(0);
+            // Rolling fragment prefetch: the LDS reads of k-step ks + PF are
+            // issued before the MFMAs of k-step ks (a ring of PF + 1 fragment
+            // sets).  The scheduling barriers pin that order; left alone, the
+            // scheduler trades it for fewer registers and waits on LDS before
+            // every k-step.
+            constexpr int PF = KS > 2 ? 2 : KS - 1;
+            float fa[PF + 1][MI], fb[PF + 1][NI];
 #pragma unroll
-            for (int mi = 0; mi < MI; ++mi)
+            for (int ks = 0; ks < KS + PF; ++ks) {
+                if (ks < KS) {  // fragments of k-step ks into ring slot ks % (PF + 1)
 #pragma unroll
-                for (int ni = 0; ni < NI; ++ni)
-                    acc[mi][ni] = Op::run(fa[ks % (PF + 1)][mi], fb[ks % (PF + 1)][ni],
-                                          acc[mi][ni]);
-            __builtin_amdgcn_sched_barrier(0);
+                    for (int mi = 0; mi < MI; ++mi)
+                        fa[ks % (PF + 1)][mi] = Ac[ks * Op::kStep + kl][arow + mi * MT];
+#pragma unroll
+                    for (int ni = 0; ni < NI; ++ni)
+                        fb[ks % (PF + 1)][ni] = Bc[ks * Op::kStep + kl][bcol + ni * MT];
+                }
+                if (ks >= PF) {  // MFMAs of k-step ks - PF
+                    const int k = ks - PF;
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+                        for (int ni = 0; ni < NI; ++ni)
+                            acc[mi][ni] = Op::run(fa[k % (PF + 1)][mi], fb[k % (PF + 1)][ni],
+                                                  acc[mi][ni]);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+            // the next stage's copies have landed in LDS, for every wave
+            __builtin_amdgcn_s_waitcnt(kVmcnt0);
+            __syncthreads();
         }
-        if (s + 1 < nst)
-            store_stage(cur ^ 1);
-        __syncthreads();
     }
 
     // ---- epilogue (branch-free: masked lanes store to an out-of-range offset)
@@ -423,39 +438,50 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     }
 }
 
-// Forward weights in the channel-blocked order:
-// Wp[o][((c / tk) * khw + t) * tk + c % tk] = W[o][c][t], t = u*kw + v.
+// Forward weights, transposed for the LDS copies and reordered to the
+// reduction order: Wp[g][r][m] = W[g*M + m][c][t] (t = u*kw + v) with
+//   order > 0:  r = ((c / tk) * khw + t) * tk + c % tk    (channel-blocked)
+//   order < 0:  r = t * Cg + c                             (tap-major)
+//   order == 0: r = c * khw + t                            (channel-major)
 __global__ void __launch_bounds__(256)
-pack_weights_blocked_kernel(const float* __restrict__ W, float* __restrict__ Wp, int K, int Cg,
-                            int khw, int tk, int blocked)
+pack_weights_kernel(const float* __restrict__ W, float* __restrict__ Wp, int G, int M, int Cg,
+                    int khw, int tk, int order)
 {
-    const int total = K * Cg * khw;
-    const int e = blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= total)
-        return;
     const int R = Cg * khw;
-    const int o = e / R;
-    const int r = e - o * R;
-    int c, t;
-    if (blocked) {
-        const int ci = r % tk;
-        t = (r / tk) % khw;
-        c = (r / (tk * khw)) * tk + ci;
-    } else {
-        t = r / Cg;
-        c = r - t * Cg;
+    const long total = (long)G * M * R;
+    for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < total;
+         e += (long)gridDim.x * blockDim.x) {
+        const int m = (int)(e % M);
+        const long gr = e / M;
+        const int r = (int)(gr % R);
+        const int g = (int)(gr / R);
+        int c, t;
+        if (order > 0) {
+            const int ci = r % tk;
+            t = (r / tk) % khw;
+            c = (r / (tk * khw)) * tk + ci;
+        } else if (order < 0) {
+            t = r / Cg;
+            c = r - t * Cg;
+        } else {
+            c = r / khw;
+            t = r - c * khw;
+        }
+        Wp[e] = W[((long)(g * M + m) * Cg + c) * khw + t];
     }
-    Wp[e] = W[(o * Cg + c) * khw + t];
 }
 
-hipError_t launch_pack_weights_blocked(const float* W, float* Wp, int K, int Cg, int khw, int tk,
-                                       int blocked, hipStream_t s)
+hipError_t launch_pack_weights(const float* W, float* Wp, int G, int M, int Cg, int khw, int tk,
+                               int order, hipStream_t s)
 {
-    const int total = K * Cg * khw;
+    const long total = (long)G * M * Cg * khw;
     if (total == 0)
         return hipSuccess;
-    hipLaunchKernelGGL(pack_weights_blocked_kernel, dim3((total + 255) / 256), dim3(256), 0, s, W,
-                       Wp, K, Cg, khw, tk, blocked);
+    long blocks = (total + 255) / 256;
+    if (blocks > 4096)
+        blocks = 4096;
+    hipLaunchKernelGGL(pack_weights_kernel, dim3((unsigned)blocks), dim3(256), 0, s, W, Wp, G, M,
+                       Cg, khw, tk, order);
     return hipGetLastError();
 }
 

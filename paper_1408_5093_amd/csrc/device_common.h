@@ -22,6 +22,10 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr uint32_t kBufferWord3 = 0x00020000u;
 // Byte offset that is always out of range (every tensor is < 2^31 bytes).
 constexpr uint32_t kOob = 0x80000000u;
+// s_waitcnt immediate that waits for vmcnt(0) only (expcnt and lgkmcnt left
+// at their maxima): all of this wave's vector-memory loads, including
+// global-to-LDS copies, have completed.
+constexpr int kVmcnt0 = 0x0F70;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes)
 {

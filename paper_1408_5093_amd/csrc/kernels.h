@@ -18,7 +18,10 @@ FastDiv make_fastdiv(uint32_t d);
 // Implicit GEMM whose reduction index r = (c, u, v) walks a kh x kw window of
 // a gather source X[N][Cin][IH][IW] and whose column index walks the output
 // grid (n, i, j) in N x OH x OW:
-//   C_g[m][col] = sum_r A[g][m][r] * X[n][g*Cin_g + c][i*sh - ph + u][j*sw - pw + v]
+//   C_g[m][col] = sum_r A[g][r][m] * X[n][g*Cin_g + c][i*sh - ph + u][j*sw - pw + v]
+// A is laid out [G][R][M] (m contiguous): both operands are copied from
+// global memory straight into LDS, 64 consecutive elements of one k row per
+// wave copy.
 // epi == 0 (forward): Y[n][g*M + m][i][j] = [relu](C + bias[g*M + m])
 // epi == 1 (data gradient, phase-stacked): row m = (c, fh, fw) and
 //   Y[n][g*Cg_out + c][psh*(i + a0h) + fh - oph][psw*(j + a0w) + fw - opw] = C
@@ -82,15 +85,17 @@ int gemm_tile_k(int tile);  // reduction depth of one pipeline stage
 constexpr int kGemmMinTK = 16;
 
 // tap_major: the reduction index runs in the channel-blocked order
-// r = (c / TK, u, v, c % TK), TK = gemm_tile_k(tile) (A packed to match, see
-// launch_pack_weights_blocked); needs Cin_g % TK == 0.  Otherwise r = (c, u, v).
+// r = (c / TK, u, v, c % TK), TK = gemm_tile_k(tile), or tap-major
+// r = (u, v, c) (A packed to match, see launch_pack_weights); needs
+// Cin_g % TK == 0.  Otherwise r = (c, u, v).
 hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool tap_major,
                                 hipStream_t s);
 
-// blocked: Wp[o][((c / tk) * khw + u*kw + v) * tk + c % tk] = W[o][c][u][v];
-// else tap-major: Wp[o][(u*kw + v) * Cg + c] = W[o][c][u][v]   (K rows)
-hipError_t launch_pack_weights_blocked(const float* W, float* Wp, int K, int Cg, int khw, int tk,
-                                       int blocked, hipStream_t s);
+// Forward weights W[G*M][Cg][khw] -> Wp[g][r][m] in the reduction order
+// r = ((c / tk) * khw + t) * tk + c % tk (order > 0), r = t * Cg + c
+// (order < 0) or r = c * khw + t (order == 0), t = u*kw + v.
+hipError_t launch_pack_weights(const float* W, float* Wp, int G, int M, int Cg, int khw, int tk,
+                               int order, hipStream_t s);
 
 enum WgradTile : int {
     WTILE_128x128 = 0,  // 4 waves as 2x2, each 64x64
@@ -188,10 +193,10 @@ hipError_t launch_dgrad_weights_bf16(const uint16_t* W, uint16_t* Wt, int G, int
 hipError_t launch_relu_mask_bias(const float* G, const float* Y, float* D, float* plane_sums,
                                  int planes, int plane_size, int relu, hipStream_t s);
 
-// Wt[g][(c, fh, fw)][r] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)]
-// (0 where the tap index passes the kernel edge), r = (k, th, tw), the
-// channel-blocked r = (k / tk, th, tw, k % tk) when tk > 0, or the tap-major
-// r = (th, tw, k) when tk < 0.
+// Wt[g][r][(c, fh, fw)] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)]
+// (0 where the tap index passes the kernel edge; m = (c, fh, fw) contiguous),
+// r = (k, th, tw), the channel-blocked r = (k / tk, th, tw, k % tk) when
+// tk > 0, or the tap-major r = (th, tw, k) when tk < 0.
 hipError_t launch_dgrad_weight_transform(const float* W, float* Wt, int G, int Kg, int Cg, int kh,
                                          int kw, int sh, int sw, int Th, int Tw, int tk,
                                          hipStream_t s);

@@ -159,7 +159,9 @@ def test_no_writes_outside_outputs():
 
     ybuf, yv = guarded(N * K * H * W)
     y = yv.view(N, K, H, W)
-    cc.caffe_conv_forward(cc.conv_desc(x.shape, w.shape, 1, 1, 2, True), x, w, None, y)
+    d = cc.conv_desc(x.shape, w.shape, 1, 1, 2, True)
+    cc.caffe_conv_forward(d, x, w, None, y,
+                          cc.Workspace().get(cc.conv_workspace_size(d, cc.PASS_FORWARD)))
     dxbuf, dxv = guarded(x.numel())
     dwbuf, dwv = guarded(w.numel())
     dbbuf, dbv = guarded(K)

@@ -161,6 +161,14 @@ conv_wgrad_f32_kernel(const WgradParams p)
                 const uint32_t e = (uint32_t)b_off[q];
                 rB[q] = buf_ld_f32(rx, (xb4 + (e >> 5)) | (((nok >> (e & 31u)) & 1u) << 31));
             }
+        } else if (PACK && __all(ih0 >= 0 && ih0 + kh <= IH && iw0 >= 0 && iw0 + kw <= IW)) {
+            // every column of the wave has its whole window inside the image
+            // (every wave of an unpadded layer): no per-tap bounds test.  A
+            // column past Ncol lies in an image n >= N, outside X (reads 0);
+            // taps past R only feed columns that are never stored.
+#pragma unroll
+            for (int q = 0; q < EB; ++q)
+                rB[q] = buf_ld_f32(rx, (uint32_t)(xbase + (b_off[q] & 0x3fffff)) * 4u);
         } else {
             const uint32_t cbad = (uint32_t)(col >= col_end) << 31;
 #pragma unroll

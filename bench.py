@@ -34,6 +34,9 @@ def parse():
     ap.add_argument("--bf16", action="store_true", help="bfloat16 operands (N=512 workload)")
     ap.add_argument("--cpu-images", type=int, default=192,
                     help="images in the CPU-oracle baseline sample (0 = skip)")
+    ap.add_argument("--network-steps", type=int, default=-1,
+                    help="steps of the whole-network step (conv1-5, pool5, fc6-fc8) timed "
+                         "after the conv stack (-1 = --steps; 0 = skip; fp32 only)")
     ap.add_argument("--calibrate-copy-mb", type=int, default=0,
                     help="first run one plain device copy of this many MiB (a known-size "
                          "reference for the HBM byte counters)")
@@ -105,6 +108,45 @@ def cpu_baseline(inp, wl, n_img):
             "kind": "oracle", "images_per_s": n_img / dt, "seconds": dt, "cpu": cpu,
             "sample": f"CaffeNet conv1-5 fwd + bwd (with pool/LRN glue) on the first {n_img} "
                       f"of the step's 256 seeded images, plain fp64 loops, OpenMP"}
+
+
+def network_step(wl, ConvStack, N, steps, warmup, stream):
+    """The whole CaffeNet chain -- conv1-5 with their glue, max-pool after
+    conv5, the fc6-fc8 inner products -- forward and backward from a
+    synthetic fc8 top gradient: images/s and per-layer call times."""
+    import numpy as np
+    import torch
+    print(f"[bench] whole-network step N={N}", file=sys.stderr, flush=True)
+    inp = wl.caffenet_net_step(N)
+    net = ConvStack(wl.CAFFENET_NET, N, inp["W"], inp["b"], glue=wl.CAFFENET_NET_GLUE)
+    x = torch.from_numpy(inp["x"]).cuda()
+    g = torch.from_numpy(inp["top_diff"]).cuda()
+    for _ in range(warmup):
+        net.forward(x, stream)
+        net.backward(g, stream)
+    torch.cuda.synchronize()
+    net.events = []
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        net.forward(x, stream)
+        net.backward(g, stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    acc = {}
+    evs, net.events = net.events, None
+    for i in range(0, len(evs), 2):
+        (tb, eb), (_, ee) = evs[i], evs[i + 1]
+        acc.setdefault(tb[:2], []).append(eb.elapsed_time(ee))
+    flops = sum(3 * L.flops(N) for L in wl.CAFFENET_NET)
+    return {"workload": ("CaffeNet conv1-5 + max-pool + fc6-fc8 (ReLU on fc6, fc7) forward + "
+                         "data, weight and bias gradients"),
+            "global_batch": N, "ms_per_step": ms, "images_per_s": N / (ms * 1e-3),
+            "tflops": flops / (ms * 1e-3) / 1e12, "flops_per_step": flops,
+            "breakdown_ms": {f"{k[0]}_{wl.CAFFENET_NET[k[1]].name}": round(float(np.mean(v)), 4)
+                             for k, v in sorted(acc.items())}}
 
 
 def main():
@@ -226,6 +268,9 @@ def main():
         "roofline": roofline,
         "cpu_baseline": None,
     }
+    nsteps = args.steps if args.network_steps < 0 else args.network_steps
+    if nsteps > 0 and not args.bf16:
+        out["network"] = network_step(wl, ConvStack, N, nsteps, args.warmup, stream)
     if args.cpu_images > 0:
         print(f"[bench] CPU oracle baseline on {args.cpu_images} images", file=sys.stderr,
               flush=True)

@@ -66,7 +66,54 @@ struct ConvPlan {
     int Cgp, Kgp, Rp, Rtp, Rw;
     size_t off_xh_fwd, off_wp_fwd;  // forward: [Xh][Wp]
     size_t off_dh, off_xh;          // backward: [Dh][Xh][sums][Wt][partials]
+    // inner-product shape (1x1 kernel on 1x1 spatial, one group, fp32): dense
+    // split-K GEMMs with rows = samples (forward, data gradient) or outputs
+    // (weight gradient)
+    bool dense;
+    int fc_tile_f, fc_tile_d, fc_tile_w;
+    int fc_splits_f, fc_sps_f, fc_splits_d, fc_sps_d, fc_splits_w, fc_sps_w;
+    size_t fc_off_xt, fc_off_wp, fc_off_pf;  // forward: [X^T][W^T] (C % 4 != 0)[partials]
+    size_t fc_off_d, fc_off_dt, fc_off_pb;   // backward: [D][D^T][partials]
 };
+
+// Split-K plan of a dense GEMM with M rows, ncol columns and a reduction of R
+// on `cus` compute units.  Workgroups are dealt evenly to the units and a
+// unit works through its share at its MFMA rate, so the GEMM takes about
+// ceil(tiles * s / cus) * ceil(stages / s) workgroup-stages of time (measured
+// on the inner-product shapes: splits that leave some units one workgroup
+// more than the rest cost that whole extra workgroup; a unit with a single
+// workgroup runs it ~10% slower, its memory latency less hidden); s splits
+// add s * M * ncol partial sums written and read back once.  The plan takes
+// the s with the least modelled time (ties: fewer splits).
+void plan_splits(int M, int ncol, int R, int tile, int cus, int forced, int* splits, int* sps)
+{
+    const int tm = gemm_tile_m(tile), tn = gemm_tile_n(tile), tk = gemm_tile_k(tile);
+    const int64_t tiles = std::max<int64_t>(1, (int64_t)((M + tm - 1) / tm) * ((ncol + tn - 1) / tn));
+    const int64_t nst = std::max(1, (R + tk - 1) / tk);
+    cus = std::max(1, cus);
+    // one workgroup-stage at ~85% of a unit's fp32 MFMA rate (157.3 TFLOP/s
+    // over 256 units), partials at ~4 TB/s
+    const double t_stage = 2.0 * tm * tn * tk / (0.85 * 157.3e12 / 256);
+    const double t_byte = 1.0 / 4e12;
+    int64_t best = 1;
+    double best_t = -1;
+    for (int64_t sp = 1; sp <= nst; ++sp) {
+        const double part = sp > 1 ? 8.0 * sp * M * ncol : 0.0;
+        if (part / 2 > (double)kMaxTensorBytes)
+            break;
+        const int64_t load = (tiles * sp + cus - 1) / cus;  // workgroups per unit
+        const double t = (double)load * ((nst + sp - 1) / sp) * t_stage * (load == 1 ? 1.1 : 1.0) +
+                         part * t_byte;
+        if (best_t < 0 || t < best_t * (1 - 1e-9)) {
+            best = sp;
+            best_t = t;
+        }
+    }
+    if (forced > 0)  // profiling only
+        best = std::min<int64_t>(forced, nst);
+    *sps = (int)((nst + best - 1) / best);
+    *splits = (int)((nst + *sps - 1) / *sps);
+}
 
 // Tile for a GEMM with M rows: the least padding of M; ties go to the first
 // tile of the pass's preference order (measured: the forward pass favours
@@ -91,6 +138,18 @@ int pick_tile(int M, bool forward, int forced)
         }
     }
     return best;
+}
+
+// Dense (inner-product) GEMM tile for M rows: 128 x 128 unless it pads M by
+// more than 5% (measured: on 1000 rows it beats the 48-row tile's lesser
+// padding), else the forward pass's choice.
+int pick_dense_tile(int M, int forced)
+{
+    if (forced >= 0 && forced < TILE_COUNT && forced != TILE_128x128_K32)
+        return forced;
+    if ((double)((M + 127) / 128 * 128) <= 1.05 * M)
+        return TILE_128x128;
+    return pick_tile(M, true, -1);
 }
 
 // Weight-gradient tile: the least padding of Kg, then the taller tile.
@@ -288,8 +347,43 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     q.dgrad_tap = q.Kg % gemm_tile_k(q.dgrad_tile) == 0;
     q.ws_fwd = align_up(q.weight_elems * 4, kWsAlign);  // the packed weights
 
+    q.dense = false;
     if (q.dtype == CAFFE_BF16)
         return plan_bf16(&q);
+
+    q.dense = q.H == 1 && q.W == 1 && q.kh == 1 && q.kw == 1 && q.ph == 0 && q.pw == 0 &&
+              q.G == 1;
+    if (q.dense) {
+        // forward: Y[n][k] = sum_c X^T[c][n] W^T[c][k]; data gradient:
+        // dX[n][c] = sum_k D^T[k][n] W[k][c]; weight gradient:
+        // dW[k][c] = sum_n D[n][k] X[n][c]
+        const int N = q.N, C = q.C, K = q.K;
+        q.fc_tile_f = pick_dense_tile(std::max(N, 1), env_tile("CAFFE_FC_TILE_F"));
+        q.fc_tile_d = pick_dense_tile(std::max(N, 1), env_tile("CAFFE_FC_TILE_D"));
+        q.fc_tile_w = pick_dense_tile(K, env_tile("CAFFE_FC_TILE_W"));
+        plan_splits(N, K, C, q.fc_tile_f, device_cu_count(),
+                    env_tile("CAFFE_FC_SPLITS_F"), &q.fc_splits_f, &q.fc_sps_f);
+        plan_splits(N, C, K, q.fc_tile_d, device_cu_count(),
+                    env_tile("CAFFE_FC_SPLITS_D"), &q.fc_splits_d, &q.fc_sps_d);
+        plan_splits(K, C, N, q.fc_tile_w, device_cu_count(),
+                    env_tile("CAFFE_FC_SPLITS_W"), &q.fc_splits_w, &q.fc_sps_w);
+        const int64_t pf = (int64_t)q.fc_splits_f * N * K * 4;
+        const int64_t pb = std::max((int64_t)q.fc_splits_d * N * C, (int64_t)q.fc_splits_w * K * C) * 4;
+        if (pf > kMaxTensorBytes || pb > kMaxTensorBytes)
+            return fail(CAFFE_ERR_UNSUPPORTED, "inner-product partials reach 2^31 bytes");
+        // the forward stages X^T and W^T only when C % 4 != 0 (the
+        // reduction-contiguous GEMM reads 16-byte chunks of rows of C floats)
+        const bool staged = C % 4 != 0;
+        q.fc_off_xt = 0;
+        q.fc_off_wp = staged ? align_up((size_t)N * C * 4, kWsAlign) : 0;
+        q.fc_off_pf = staged ? q.fc_off_wp + align_up((size_t)K * C * 4, kWsAlign) : 0;
+        q.ws_fwd = q.fc_off_pf + align_up(pf, kWsAlign);
+        q.fc_off_d = 0;
+        q.fc_off_dt = align_up((size_t)N * K * 4, kWsAlign);
+        q.fc_off_pb = q.fc_off_dt + align_up((size_t)N * K * 4, kWsAlign);
+        q.ws_data = q.ws_weights = q.ws_both = q.fc_off_pb + align_up(pb, kWsAlign);
+        return CAFFE_OK;
+    }
 
     // Workspace: [masked top diff][bias partial sums][transformed weights]
     // [weight partials].  The masked top diff is written only when relu is
@@ -462,6 +556,111 @@ int run_weights(const ConvPlan& q, const float* dsrc, const void* bottom, float*
     LAUNCH(launch_wgrad_reduce(part, weight_diff, (int)q.weight_elems, q.splits, sums, bias_diff,
                                q.splits, q.K, accumulate, s),
            "reduce launch");
+    return CAFFE_OK;
+}
+
+// ---- inner product (dense split-K GEMMs)
+ConvGemmParams dense_params(const float* A, uint32_t A_bytes, const float* X, uint32_t X_bytes,
+                            float* P, uint32_t P_bytes, int M, int ncol, int R, int splits,
+                            int sps)
+{
+    ConvGemmParams p = {};
+    p.A = A;
+    p.X = X;
+    p.Y = P;
+    p.A_bytes = A_bytes;
+    p.X_bytes = X_bytes;
+    p.Y_bytes = P_bytes;
+    p.M = M;
+    p.R = R;
+    p.G = 1;
+    p.Ncol = ncol;
+    p.splits = splits;
+    p.stages_per_split = sps;
+    p.xcd_order = 1;
+    return p;
+}
+
+int run_dense_forward(const ConvPlan& q, const float* bottom, const float* weight,
+                      const float* bias, float* top, char* ws, hipStream_t s)
+{
+    const int N = q.N, C = q.C, K = q.K;
+    if (N == 0)
+        return CAFFE_OK;
+    float* part = (float*)(ws + q.fc_off_pf);
+    if (C % 4 == 0) {
+        // both operands as stored: X [N][C] and W [K][C], C contiguous (and
+        // 16-byte aligned, as every tensor argument)
+        const ConvGemmParams p =
+            dense_params(bottom, nbytes((int64_t)N * C, 4), weight, nbytes((int64_t)K * C, 4), part,
+                         nbytes((int64_t)q.fc_splits_f * N * K, 4), N, K, C, q.fc_splits_f,
+                         q.fc_sps_f);
+        LAUNCH(launch_dense_gemm_nt_f32(p, q.fc_tile_f, s), "inner-product forward launch");
+        LAUNCH(launch_split_reduce(part, q.fc_splits_f, N * K, K, bias, q.relu, nullptr, top, s),
+               "inner-product reduce launch");
+        return CAFFE_OK;
+    }
+    // otherwise through X^T [C][N] and W^T [C][K]
+    float* xt = (float*)(ws + q.fc_off_xt);
+    float* wp = (float*)(ws + q.fc_off_wp);
+    LAUNCH(launch_transpose_f32(bottom, xt, N, C, s), "transpose launch");
+    LAUNCH(launch_transpose_f32(weight, wp, K, C, s), "transpose launch");
+    const ConvGemmParams p =
+        dense_params(xt, nbytes((int64_t)N * C, 4), wp, nbytes((int64_t)K * C, 4), part,
+                     nbytes((int64_t)q.fc_splits_f * N * K, 4), N, K, C, q.fc_splits_f,
+                     q.fc_sps_f);
+    LAUNCH(launch_dense_gemm_f32(p, q.fc_tile_f, s), "inner-product forward launch");
+    LAUNCH(launch_split_reduce(part, q.fc_splits_f, N * K, K, bias, q.relu, nullptr, top, s),
+           "inner-product reduce launch");
+    return CAFFE_OK;
+}
+
+int backward_dense(const ConvPlan& q, const float* top_diff, const float* top, bool masked,
+                   bool mask_bottom, const float* bottom, const float* weight, float* bottom_diff,
+                   float* weight_diff, float* bias_diff, int accumulate, char* ws, hipStream_t s)
+{
+    const int N = q.N, C = q.C, K = q.K;
+    const float* D = top_diff;
+    if (q.relu && !masked && N > 0) {
+        float* d = (float*)(ws + q.fc_off_d);
+        LAUNCH(launch_relu_mask(top_diff, top, d, (int64_t)N * K, s), "ReLU backward launch");
+        D = d;
+    }
+    float* part = (float*)(ws + q.fc_off_pb);
+    if (bottom_diff && N > 0) {
+        float* dt = (float*)(ws + q.fc_off_dt);
+        LAUNCH(launch_transpose_f32(D, dt, N, K, s), "transpose launch");
+        const ConvGemmParams p =
+            dense_params(dt, nbytes((int64_t)N * K, 4), weight, nbytes((int64_t)K * C, 4), part,
+                         nbytes((int64_t)q.fc_splits_d * N * C, 4), N, C, K, q.fc_splits_d,
+                         q.fc_sps_d);
+        LAUNCH(launch_dense_gemm_f32(p, q.fc_tile_d, s), "inner-product data-gradient launch");
+        LAUNCH(launch_split_reduce(part, q.fc_splits_d, N * C, C, nullptr, 0,
+                                   mask_bottom ? bottom : nullptr, bottom_diff, s),
+               "inner-product reduce launch");
+    }
+    if (weight_diff) {
+        // one split and no accumulation: the GEMM writes dW itself
+        const bool direct = q.fc_splits_w == 1 && !accumulate;
+        float* dst = direct ? weight_diff : part;
+        if (N > 0) {
+            const ConvGemmParams p =
+                dense_params(D, nbytes((int64_t)N * K, 4), bottom, nbytes((int64_t)N * C, 4), dst,
+                             nbytes((int64_t)q.fc_splits_w * K * C, 4), K, C, N, q.fc_splits_w,
+                             q.fc_sps_w);
+            LAUNCH(launch_dense_gemm_f32(p, q.fc_tile_w, s), "inner-product weight-gradient launch");
+        } else if (!accumulate) {
+            LAUNCH(launch_fill_zero(weight_diff, (int64_t)K * C, s), "zero fill launch");
+        }
+        // dW = sum of the split partials; db[k] = sum_n D[n][k]
+        const bool sum_w = !direct && N > 0;
+        LAUNCH(launch_wgrad_reduce(part, weight_diff, sum_w ? K * C : 0, q.fc_splits_w, D,
+                                   bias_diff, N, K, accumulate, s),
+               "reduce launch");
+    } else if (bias_diff) {
+        LAUNCH(launch_wgrad_reduce(nullptr, nullptr, 0, 0, D, bias_diff, N, K, accumulate, s),
+               "bias reduce launch");
+    }
     return CAFFE_OK;
 }
 
@@ -652,6 +851,9 @@ int caffe_conv_forward(const caffe_conv_desc* desc, const void* bottom, const vo
     if (q.dtype == CAFFE_BF16)
         return run_forward_bf16(q, bottom, weight, bias, top, (char*)workspace,
                                 (hipStream_t)stream);
+    if (q.dense)
+        return run_dense_forward(q, (const float*)bottom, (const float*)weight, bias, top,
+                                 (char*)workspace, (hipStream_t)stream);
     return run_forward(q, bottom, weight, bias, top, (char*)workspace, (hipStream_t)stream);
 }
 
@@ -682,6 +884,10 @@ int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, cons
     if (q.dtype == CAFFE_BF16)
         return backward_bf16(q, top_diff, top, masked, mask_bottom, bottom, weight, bottom_diff,
                              weight_diff, bias_diff, accumulate, ws, s);
+    if (q.dense)
+        return backward_dense(q, top_diff, top, masked, mask_bottom, (const float*)bottom,
+                              (const float*)weight, bottom_diff, weight_diff, bias_diff,
+                              accumulate, ws, s);
     const float* dsrc = top_diff;
     if (q.relu && !masked && (bottom_diff || weight_diff) && q.top_elems > 0) {
         // D = top_diff [top > 0], shared by both gradients

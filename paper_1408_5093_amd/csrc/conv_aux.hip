@@ -68,6 +68,41 @@ hipError_t launch_relu_mask_bias(const float* G, const float* Y, float* D, float
     return hipGetLastError();
 }
 
+// D = G [Y > 0], element by element (four per lane per iteration when all
+// three pointers are 16-byte aligned).
+__global__ void __launch_bounds__(256)
+relu_mask_kernel(const float* __restrict__ G, const float* __restrict__ Y, float* __restrict__ D,
+                 int64_t count, int vec)
+{
+    const int64_t n4 = vec ? count >> 2 : 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n4; i += stride) {
+        const float4 g = reinterpret_cast<const float4*>(G)[i];
+        const float4 y = reinterpret_cast<const float4*>(Y)[i];
+        float4 d;
+        d.x = y.x > 0.f ? g.x : 0.f;
+        d.y = y.y > 0.f ? g.y : 0.f;
+        d.z = y.z > 0.f ? g.z : 0.f;
+        d.w = y.w > 0.f ? g.w : 0.f;
+        reinterpret_cast<float4*>(D)[i] = d;
+    }
+    for (int64_t i = (n4 << 2) + blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count;
+         i += stride)
+        D[i] = Y[i] > 0.f ? G[i] : 0.f;
+}
+
+hipError_t launch_relu_mask(const float* G, const float* Y, float* D, int64_t count, hipStream_t s)
+{
+    if (count == 0)
+        return hipSuccess;
+    int64_t blocks = ((count >> 2) + 255) / 256;
+    blocks = std::max<int64_t>(1, std::min<int64_t>(blocks, 4096));
+    const int vec = (((uintptr_t)G | (uintptr_t)Y | (uintptr_t)D) & 15) == 0;
+    hipLaunchKernelGGL(relu_mask_kernel, dim3((unsigned)blocks), dim3(256), 0, s, G, Y, D, count,
+                       vec);
+    return hipGetLastError();
+}
+
 // Wt[g][r][m = (c, fh, fw)] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)],
 // 0 past the kernel edge; r = (k, th, tw), or r = (k / tk, th, tw, k % tk)
 // when tk > 0, or r = (th, tw, k) when tk < 0.  m is contiguous (the layout
@@ -188,6 +223,71 @@ hipError_t launch_wgrad_reduce(const float* P, float* out, int count, int splits
     const int blocks = (total + kRedCols - 1) / kRedCols;
     hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks), dim3(kRedParts * kRedCols), 0, s, P, out,
                        count, splits, plane_sums, db, N, K, accumulate);
+    return hipGetLastError();
+}
+
+// 32 x 32 tiles through LDS: coalesced reads along c, coalesced writes along r.
+__global__ void __launch_bounds__(256)
+transpose_f32_kernel(const float* __restrict__ in, float* __restrict__ out, int R, int C)
+{
+    __shared__ float tile[32][33];
+    const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+#pragma unroll
+    for (int k = 0; k < 32; k += 8) {
+        const int r = r0 + ty + k, c = c0 + tx;
+        if (r < R && c < C)
+            tile[ty + k][tx] = in[(size_t)r * C + c];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 32; k += 8) {
+        const int c = c0 + ty + k, r = r0 + tx;
+        if (r < R && c < C)
+            out[(size_t)c * R + r] = tile[tx][ty + k];
+    }
+}
+
+hipError_t launch_transpose_f32(const float* in, float* out, int R, int C, hipStream_t s)
+{
+    if ((long)R * C == 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(transpose_f32_kernel, dim3((C + 31) / 32, (R + 31) / 32), dim3(256), 0, s,
+                       in, out, R, C);
+    return hipGetLastError();
+}
+
+// Split-K partials added in order (s = 0, 1, ...), then the bias and ReLU.
+__global__ void __launch_bounds__(256)
+split_reduce_kernel(const float* __restrict__ P, int splits, int count, int ncol,
+                    const float* __restrict__ bias, int relu, const float* __restrict__ mask,
+                    float* __restrict__ out)
+{
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < count;
+         i += gridDim.x * blockDim.x) {
+        float t = 0.f;
+        for (int q = 0; q < splits; ++q)
+            t += P[(size_t)q * count + i];
+        if (bias)
+            t += bias[i % ncol];
+        if (relu && !(t > 0.f))
+            t = 0.f;
+        if (mask && !(mask[i] > 0.f))
+            t = 0.f;
+        out[i] = t;
+    }
+}
+
+hipError_t launch_split_reduce(const float* P, int splits, int count, int ncol, const float* bias,
+                               int relu, const float* mask, float* out, hipStream_t s)
+{
+    if (count == 0)
+        return hipSuccess;
+    int blocks = (count + 255) / 256;
+    if (blocks > 8192)
+        blocks = 8192;
+    hipLaunchKernelGGL(split_reduce_kernel, dim3(blocks), dim3(256), 0, s, P, splits, count, ncol,
+                       bias, relu, mask, out);
     return hipGetLastError();
 }
 

@@ -119,11 +119,15 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     const int n_ct = (p.Ncol + TN - 1) / TN;
     const int per_xcd = gridDim.x >> 3;
     const int T = p.xcd_order ? (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3) : blockIdx.x;
-    if (T >= n_mt * n_ct * p.G)
+    // EPI 2 (dense split-K): the reduction is cut into p.splits ranges of
+    // p.stages_per_split stages, the split index varying slowest
+    const int n_split = EPI == 2 ? p.splits : 1;
+    if (T >= n_mt * n_ct * p.G * n_split)
         return;
     const int mt = T % n_mt;
     const int ct = (T / n_mt) % n_ct;
-    const int g = T / (n_mt * n_ct);
+    const int g = (T / (n_mt * n_ct)) % p.G;
+    const int split = T / (n_mt * n_ct * p.G);
     const int m0 = mt * TM;
     const int n0 = ct * TN;
     const int M = p.M, R = p.R;
@@ -156,9 +160,9 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     }
     const uint32_t a_row4 = (uint32_t)M * 4u;
     const int b_nc = wave % NC;
-    int b_ih0, b_iw0, b_base;
-    uint32_t b_cbad;
-    {
+    int b_ih0 = 0, b_iw0 = 0, b_base = 0;
+    uint32_t b_cbad = 0;
+    if constexpr (EPI != 2) {
         const int col = n0 + b_nc * 64 + lane;
         const int n = col / OHW;
         const int pix = col - n * OHW;
@@ -170,6 +174,21 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
         b_cbad = col < p.Ncol ? 0u : kOob;
     }
     auto b_row = [&](int q) { return (wave + NW * q) / NC; };
+
+    // Dense B (EPI 2): B[r][col] row-major with Ncol columns, the row offset
+    // in the scalar offset.  Rows past R (only when R % TK != 0) get the
+    // out-of-range bit in the lane offset and read 0.
+    const uint32_t b_dvoff =
+        (uint32_t)(n0 + b_nc * 64 + lane) * 4u | (n0 + b_nc * 64 + lane < p.Ncol ? 0u : kOob);
+    auto copy_b_dense = [&](BTile& dst, int kbase) {
+#pragma unroll
+        for (int q = 0; q < NB; ++q) {
+            const int r = kbase + b_row(q);
+            const bool rok = TAP || r < R;
+            copy_to_lds(rx, &dst[b_row(q)][b_nc * 64], rok ? b_dvoff : kOob,
+                        rok ? (uint32_t)r * (uint32_t)p.Ncol * 4u : 0u);
+        }
+    };
 
     auto copy_a = [&](ATile& dst, int kbase) {
 #pragma unroll
@@ -255,15 +274,19 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
             acc[mi][ni] = init;
     }
 
-    const int nst = (R + TK - 1) / TK;
+    const int nst_all = (R + TK - 1) / TK;
+    const int s_begin = EPI == 2 ? split * p.stages_per_split : 0;
+    const int nst = EPI == 2 ? min(nst_all, s_begin + p.stages_per_split) : nst_all;
     // blocked walk state: stage s covers tap (tu, tv) of channels tc .. tc + TK - 1.
     // It is updated in the loop body itself: captured by reference in a
     // lambda, it was kept in scratch memory, and the scratch accesses' waits
     // also stalled on the next stage's global loads.
     int tu = 0, tv = 0, tc = 0;
 
-    copy_a(As0, 0);
-    if constexpr (TAP)
+    copy_a(As0, s_begin * TK);
+    if constexpr (EPI == 2)
+        copy_b_dense(Bs0, s_begin * TK);
+    else if constexpr (TAP)
         copy_b_tap(Bs0, 0, 0, 0);
     else
         copy_b_any(Bs0, 0);
@@ -277,7 +300,7 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     // The stage loop is unrolled by two so that each half has its buffers
     // fixed: half h copies stage s + h + 1 into buffer 1 - h and multiplies
     // the fragments of stage s + h from buffer h.
-    for (int s0 = 0; s0 < nst; s0 += 2) {
+    for (int s0 = s_begin; s0 < nst; s0 += 2) {
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const int s = s0 + h;
@@ -289,7 +312,9 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
             BTile& Bn = h ? Bs0 : Bs1;
             if (s + 1 < nst) {
                 copy_a(An, (s + 1) * TK);
-                if constexpr (TAP) {
+                if constexpr (EPI == 2) {
+                    copy_b_dense(Bn, (s + 1) * TK);
+                } else if constexpr (TAP) {
                     if (p.blocked) {  // (c / TK, u, v, c % TK)
                         if (++tv == kw) {
                             tv = 0;
@@ -355,7 +380,26 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     // buffer, dropped by the hardware): short-circuit tests here become
     // divergent branches and make the compiler copy every accumulator out of
     // the AGPRs at once.
-    if constexpr (EPI == 0) {
+    if constexpr (EPI == 2) {
+        // split partial P[split][m][col] (rows of the single group), lanes along col
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) {
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni) {
+                const int col = n0 + bcol + ni * MT;
+                const uint32_t cbad = (uint32_t)(col >= p.Ncol) << 31;
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int q = 0; q < Op::kRegs; ++q) {
+                    const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
+                    const uint32_t off =
+                        ((uint32_t)((split * M + m) * p.Ncol + col) * 4u) | cbad |
+                        ((uint32_t)(m >= M) << 31);
+                    buf_st_f32(acc[mi][ni][q], ry, off);
+                }
+            }
+        }
+    } else if constexpr (EPI == 0) {
         int cbase[NI];
         uint32_t cbad[NI];
 #pragma unroll
@@ -504,8 +548,8 @@ template <int MT, int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH
 hipError_t launch_one(const ConvGemmParams& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * MT, TN = WN * NI * MT;
-    const int64_t tiles =
-        (int64_t)((p.Ncol + TN - 1) / TN) * ((p.M + TM - 1) / TM) * p.G;
+    const int64_t tiles = (int64_t)((p.Ncol + TN - 1) / TN) * ((p.M + TM - 1) / TM) * p.G *
+                          (EPI == 2 ? p.splits : 1);
     const int64_t per_xcd = (tiles + 7) / 8;  // 8 XCDs; see the kernel's tile order
     hipLaunchKernelGGL(
         (conv_gemm_f32_kernel<MT, WM, WN, MI, NI, TK, KH, KW, SH, SW, EPI, TAP, MASK>),
@@ -564,6 +608,275 @@ int gemm_tile_n(int tile)
 }
 
 int gemm_tile_k(int tile) { return kTiles[tile].tk; }
+
+namespace {
+template <int MT, int WM, int WN, int MI, int NI, int TK>
+hipError_t launch_dense(const ConvGemmParams& p, hipStream_t s)
+{
+    // whole stages (R % TK == 0) need no masking of the reduction tail
+    if (p.R % TK == 0)
+        return launch_one<MT, WM, WN, MI, NI, TK, 0, 0, 0, 0, 2, true, false>(p, s);
+    return launch_one<MT, WM, WN, MI, NI, TK, 0, 0, 0, 0, 2, false, false>(p, s);
+}
+}  // namespace
+
+hipError_t launch_dense_gemm_f32(const ConvGemmParams& p, int tile, hipStream_t s)
+{
+    if (p.Ncol == 0 || p.M == 0)
+        return hipSuccess;
+    if (p.G != 1 || p.splits < 1 || p.stages_per_split < 1)
+        return hipErrorInvalidValue;
+    switch (tile) {
+    case TILE_128x128:
+        return launch_dense<32, 2, 2, 2, 2, 16>(p, s);
+    case TILE_96x256:
+        return launch_dense<32, 1, 4, 3, 2, 16>(p, s);
+    case TILE_48x256:
+        return launch_dense<16, 1, 4, 3, 4, 16>(p, s);
+    case TILE_64x256:
+        return launch_dense<32, 1, 4, 2, 2, 16>(p, s);
+    default:
+        return hipErrorInvalidValue;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Dense split-K GEMM with both operands reduction-contiguous:
+// P[split][m][n] = sum over the split's range of r of A[m][r] B[n][r]
+// (A = p.A, M x R; B = p.X, Ncol x R; P = p.Y).  The inner-product forward
+// pass (Y[n][k] = sum_c X[n][c] W[k][c]) reads its operands as stored.
+//
+// A stage is 16 deep: each operand row contributes 16 consecutive floats,
+// four 16-byte chunks, copied global -> LDS by 16-byte DMA (a wave copy =
+// 16 rows).  In LDS, logical chunk c of row r sits in slot c ^ kc_swz(r);
+// the fragment reads (ds_read_b128 of one chunk of 16 consecutive rows) then
+// touch distinct banks.  The MFMA k index is permuted within a stage: lane
+// group q (lane / MT) takes the stage's k = q * (16 / (64 / MT)) + step, so a
+// lane's values for the whole stage are consecutive floats of one row.  A and
+// B use the same permutation, so the sum over the stage is unchanged.
+__device__ __forceinline__ int kc_swz(int r)
+{
+    return ((r >> 2) & 1) | ((((r >> 1) ^ (r >> 3)) & 1) << 1);
+}
+
+__device__ __forceinline__ void copy16_to_lds(__amdgpu_buffer_rsrc_t r, float* dst, uint32_t voff,
+                                              uint32_t soff)
+{
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, voff, soff, 0, 0);
+}
+
+template <int MT, int WM, int WN, int MI, int NI, bool FULL>
+__global__ void __launch_bounds__(64 * WM * WN)
+dense_gemm_nt_kernel(const ConvGemmParams p)
+{
+    typedef Mfma<MT> Op;
+    constexpr int TK = 16;
+    constexpr int NW = WM * WN;
+    constexpr int TM = WM * MI * MT;
+    constexpr int TN = WN * NI * MT;
+    constexpr int CA = TM / 16, CB = TN / 16;  // 16-row wave copies per stage
+    constexpr int NA = (CA + NW - 1) / NW, NB = (CB + NW - 1) / NW;
+    constexpr int KL = TK / (64 / MT);        // stage k values per lane: 8 or 4
+    constexpr int NCH = KL / 4;               // 16-byte chunks per lane and row
+    static_assert(TK / Op::kStep == KL, "one k value per lane per MFMA step");
+    __shared__ floatx4 As0[TM * 4], As1[TM * 4], Bs0[TN * 4], Bs1[TN * 4];
+    typedef floatx4 ATile[TM * 4];
+    typedef floatx4 BTile[TN * 4];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave % WM;
+    const int wn = wave / WM;
+    // XCD-contiguous tile order, row tiles fastest, the split slowest
+    const int n_mt = (p.M + TM - 1) / TM;
+    const int n_ct = (p.Ncol + TN - 1) / TN;
+    const int per_xcd = gridDim.x >> 3;
+    const int T = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if (T >= n_mt * n_ct * p.splits)
+        return;
+    const int mt = T % n_mt;
+    const int ct = (T / n_mt) % n_ct;
+    const int split = T / (n_mt * n_ct);
+    const int m0 = mt * TM, n0 = ct * TN;
+    const int M = p.M, R = p.R;
+
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.A, p.A_bytes);
+    const __amdgpu_buffer_rsrc_t rb = make_rsrc(p.X, p.X_bytes);
+
+    // copy lane mapping: row lane / 4 of the copy's 16, logical chunk
+    // (lane % 4) ^ kc_swz(row) -> LDS slot lane % 4 of that row
+    const int crow = lane >> 2;
+    const int cch = (lane & 3) ^ kc_swz(crow);
+    uint32_t a_off[NA], b_off[NB];
+#pragma unroll
+    for (int q = 0; q < NA; ++q) {
+        const int row = m0 + (wave + NW * q) * 16 + crow;
+        a_off[q] = row < M ? (uint32_t)(row * R + 4 * cch) * 4u : kOob;
+    }
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+        const int col = n0 + (wave + NW * q) * 16 + crow;
+        b_off[q] = col < p.Ncol ? (uint32_t)(col * R + 4 * cch) * 4u : kOob;
+    }
+    // stage k base in the scalar offset; past the reduction's end (R % 16 != 0)
+    // a chunk reads 0 (R % 4 == 0: a chunk never straddles the end)
+    auto tail = [&](uint32_t off, int kbase) -> uint32_t {
+        if constexpr (FULL)
+            return off;
+        else
+            return kbase + 4 * cch < R ? off : kOob;
+    };
+    auto copy_stage = [&](ATile& a, BTile& b, int kbase) {
+#pragma unroll
+        for (int q = 0; q < NA; ++q)
+            if (CA % NW == 0 || wave + NW * q < CA)
+                copy16_to_lds(ra, (float*)&a[(wave + NW * q) * 64], tail(a_off[q], kbase),
+                              (uint32_t)kbase * 4u);
+#pragma unroll
+        for (int q = 0; q < NB; ++q)
+            if (CB % NW == 0 || wave + NW * q < CB)
+                copy16_to_lds(rb, (float*)&b[(wave + NW * q) * 64], tail(b_off[q], kbase),
+                              (uint32_t)kbase * 4u);
+    };
+
+    typename Op::acc_t acc[MI][NI];
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+            acc[mi][ni] = typename Op::acc_t{};
+
+    const int nst_all = (R + TK - 1) / TK;
+    const int s_begin = split * p.stages_per_split;
+    const int nst = min(nst_all, s_begin + p.stages_per_split);
+    copy_stage(As0, Bs0, s_begin * TK);
+    __builtin_amdgcn_s_waitcnt(kVmcnt0);
+    __syncthreads();
+
+    // fragment slots: row i = lane % MT of each MT-row block, logical chunks
+    // (lane / MT) * NCH + t
+    const int fi = lane % MT;
+    const int fq = lane / MT;
+    int fslot[NCH];
+#pragma unroll
+    for (int t = 0; t < NCH; ++t)
+        fslot[t] = fi * 4 + ((fq * NCH + t) ^ kc_swz(fi & 15));
+    const int arow0 = wm * MI * MT, bcol0 = wn * NI * MT;
+
+    for (int s0 = s_begin; s0 < nst; s0 += 2) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int s = s0 + h;
+            if (s >= nst)
+                break;
+            ATile& Ac = h ? As1 : As0;
+            BTile& Bc = h ? Bs1 : Bs0;
+            ATile& An = h ? As0 : As1;
+            BTile& Bn = h ? Bs0 : Bs1;
+            if (s + 1 < nst)
+                copy_stage(An, Bn, (s + 1) * TK);
+            __builtin_amdgcn_sched_barrier(0);
+            floatx4 fa[NCH][MI], fb[NCH][NI];
+#pragma unroll
+            for (int t = 0; t < NCH; ++t) {
+#pragma unroll
+                for (int mi = 0; mi < MI; ++mi)
+                    fa[t][mi] = Ac[(arow0 + mi * MT) * 4 + fslot[t]];
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni)
+                    fb[t][ni] = Bc[(bcol0 + ni * MT) * 4 + fslot[t]];
+            }
+#pragma unroll
+            for (int t = 0; t < NCH; ++t)
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+#pragma unroll
+                    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+                        for (int ni = 0; ni < NI; ++ni)
+                            acc[mi][ni] = Op::run(fa[t][mi][u], fb[t][ni][u], acc[mi][ni]);
+            __builtin_amdgcn_s_waitcnt(kVmcnt0);
+            __syncthreads();
+        }
+    }
+
+    // split partial P[split][m][col], lanes along col
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y, p.Y_bytes);
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi) {
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) {
+            const int col = n0 + bcol0 + ni * MT + fi;
+            const uint32_t cbad = (uint32_t)(col >= p.Ncol) << 31;
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int q = 0; q < Op::kRegs; ++q) {
+                const int m = m0 + arow0 + mi * MT + Op::row(q, lane);
+                const uint32_t off = ((uint32_t)((split * M + m) * p.Ncol + col) * 4u) | cbad |
+                                     ((uint32_t)(m >= M) << 31);
+                buf_st_f32(acc[mi][ni][q], ry, off);
+            }
+        }
+    }
+}
+
+namespace {
+template <int MT, int WM, int WN, int MI, int NI>
+hipError_t launch_nt(const ConvGemmParams& p, hipStream_t s)
+{
+    constexpr int TM = WM * MI * MT, TN = WN * NI * MT;
+    const int64_t tiles =
+        (int64_t)((p.Ncol + TN - 1) / TN) * ((p.M + TM - 1) / TM) * p.splits;
+    const int64_t per_xcd = (tiles + 7) / 8;
+    if (p.R % 16 == 0)
+        hipLaunchKernelGGL((dense_gemm_nt_kernel<MT, WM, WN, MI, NI, true>),
+                           dim3((unsigned)(per_xcd * 8)), dim3(64 * WM * WN), 0, s, p);
+    else
+        hipLaunchKernelGGL((dense_gemm_nt_kernel<MT, WM, WN, MI, NI, false>),
+                           dim3((unsigned)(per_xcd * 8)), dim3(64 * WM * WN), 0, s, p);
+    return hipGetLastError();
+}
+}  // namespace
+
+// Compute units of the current device (queried once; 256 when no device
+// answers).
+int device_cu_count()
+{
+    static int cus = 0;
+    if (cus > 0)
+        return cus;
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0) {
+        (void)hipGetLastError();
+        return 256;
+    }
+    cus = n;
+    return cus;
+}
+
+hipError_t launch_dense_gemm_nt_f32(const ConvGemmParams& p, int tile, hipStream_t s)
+{
+    if (p.Ncol == 0 || p.M == 0)
+        return hipSuccess;
+    if (p.R % 4 != 0 || p.splits < 1 || p.stages_per_split < 1 ||
+        (((uintptr_t)p.A | (uintptr_t)p.X) & 15) != 0)
+        return hipErrorInvalidValue;
+    switch (tile) {
+    case TILE_128x128:
+        return launch_nt<32, 2, 2, 2, 2>(p, s);
+    case TILE_96x256:
+        return launch_nt<32, 1, 4, 3, 2>(p, s);
+    case TILE_48x256:
+        return launch_nt<16, 1, 4, 3, 4>(p, s);
+    case TILE_64x256:
+        return launch_nt<32, 1, 4, 2, 2>(p, s);
+    default:
+        return hipErrorInvalidValue;
+    }
+}
 
 hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool tap_major,
                                 hipStream_t s)

@@ -46,7 +46,31 @@ struct ConvGemmParams {
     int psh, psw, a0h, a0w, oph, opw, Cg_out;
     int blocked;    // channel-blocked reduction order (else tap-major), with tap_major
     int xcd_order;  // XCD-contiguous tile order (else linear)
+    int splits, stages_per_split;  // dense split-K GEMM only
 };
+
+// Dense split-K GEMM on the same core (the inner-product layer):
+//   P[s][m][col] = sum_{r in split s} A[r][m] * X[r][col]
+// A is [R][M] and X is [R][Ncol] (row-major, G = 1); split s covers the
+// reduction stages s*stages_per_split .. (s+1)*stages_per_split - 1; Y is P.
+hipError_t launch_dense_gemm_f32(const ConvGemmParams& p, int tile, hipStream_t s);
+// Dense split-K GEMM with reduction-contiguous operands: P[split][m][n] =
+// sum_r A[m][r] B[n][r] (A = p.A [M][R], B = p.X [Ncol][R], P = p.Y).
+// R % 4 == 0 and 16-byte aligned A and B, else hipErrorInvalidValue.
+hipError_t launch_dense_gemm_nt_f32(const ConvGemmParams& p, int tile, hipStream_t s);
+// Compute units of the current device; 256 when no device answers.
+int device_cu_count();
+
+// out[c][r] = in[r][c] for an R x C row-major float matrix.
+hipError_t launch_transpose_f32(const float* in, float* out, int R, int C, hipStream_t s);
+
+// out[i] = act(sum_{s < splits} P[s*count + i] + bias[i % ncol]) in a fixed
+// order (bias may be null; act = ReLU when relu), stored as 0 where a non-null
+// mask is not > 0.
+// D = G [Y > 0] element by element.
+hipError_t launch_relu_mask(const float* G, const float* Y, float* D, int64_t count, hipStream_t s);
+hipError_t launch_split_reduce(const float* P, int splits, int count, int ncol, const float* bias,
+                               int relu, const float* mask, float* out, hipStream_t s);
 
 // Split-K weight gradient:
 //   P[s][g*Kg + m][r] = sum_{col in split s} D[n][g*Kg + m][i][j] * X[n][g*Cg + c][i*sh - ph + u][j*sw - pw + v]

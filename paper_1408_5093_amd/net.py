@@ -4,8 +4,9 @@ forward and backward through the C ABI on one stream.
 The paper's Sec. 3.3 describes a network as bookkeeping over layers: a
 forward sweep from the data to the top, then a backward sweep that hands
 each layer the gradient of its output.  ``ConvStack`` is that bookkeeping for
-a fixed chain (CaffeNet conv1-5 with max-pool + LRN after conv1 and conv2, or
-the LeNet conv pair with max-pool between), with every blob preallocated
+a fixed chain (CaffeNet conv1-5 with max-pool + LRN after conv1 and conv2,
+optionally followed by max-pool and the fc6-fc8 inner products; or the LeNet
+conv pair with max-pool between), with every blob preallocated
 once so that a step allocates nothing.  Every arithmetic step is a library
 call; this module only owns buffers and the call order.
 """
@@ -34,6 +35,9 @@ class ConvStack:
         self.descs, self.W, self.b, self.dW, self.db = [], [], [], [], []
         self.top, self.dtop_glue, self.dbottom, self.bottom_op = [], [], [], []
         self.stages = []  # per layer: list of glue stage dicts
+        # shape of layer l's output after its glue; an inner-product layer (a
+        # 1x1 image) takes it flattened, channels (c, h, w) -- a view
+        self.out_shape = []
         ws_need = 0
         for l, L in enumerate(self.layers):
             d = conv_desc((N, L.C, L.H, L.W), (L.K, L.C // L.g, L.k, L.k), L.s, L.p, L.g, L.relu,
@@ -66,9 +70,11 @@ class ConvStack:
                 st["dx"] = torch.empty(st["in_shape"], dtype=torch.float32, device=dev)
                 stages.append(st)
             self.stages.append(stages)
+            self.out_shape.append(cur)
             if l + 1 < len(self.layers):
                 nx = self.layers[l + 1]
-                if cur != (N, nx.C, nx.H, nx.W):
+                flat = nx.H == 1 and nx.W == 1 and cur[1] * cur[2] * cur[3] == nx.C
+                if cur != (N, nx.C, nx.H, nx.W) and not flat:
                     raise ValueError(f"layer {l} output {cur} does not feed layer {l + 1}")
         self.ws = Workspace(dev).get(ws_need)
         self.bottom = [None] * len(self.layers)
@@ -105,6 +111,8 @@ class ConvStack:
         s = stream or torch.cuda.current_stream()
         cur = x
         for l in range(len(self.layers)):
+            L = self.layers[l]
+            cur = cur.view(self.N, L.C, L.H, L.W)
             self.bottom[l] = cur
             src = cur
             if self.bf16:
@@ -133,6 +141,7 @@ class ConvStack:
         g = top_diff
         for l in range(len(self.layers) - 1, -1, -1):
             L = self.layers[l]
+            g = g.view(self.out_shape[l])
             for st in reversed(self.stages[l]):
                 p = st["prm"]
                 if st["kind"] == "pool":
@@ -161,4 +170,4 @@ class ConvStack:
         if l == len(self.layers) - 1:
             return top_diff_last
         st = self.stages[l]
-        return st[0]["dx"] if st else self.dbottom[l + 1]
+        return st[0]["dx"] if st else self.dbottom[l + 1].view(self.top[l].shape)

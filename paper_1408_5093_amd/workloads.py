@@ -61,12 +61,35 @@ LENET = (
 )
 LENET_POOL = dict(kernel=2, stride=2, pad=0)
 
+# The inner-product (fully connected) layers that follow the conv stacks:
+# CaffeNet fc6-fc8 on pool5's 256 x 6 x 6 output and LeNet ip1-ip2 on pool2's
+# 50 x 4 x 4 output.  An inner product is the 1x1 convolution of a 1x1 image
+# whose channels are the flattened (c, h, w) input.
+CAFFENET_FC = (
+    ConvLayer("fc6", 256 * 6 * 6, 1, 1, 4096, 1, 1, 0, 1, True),
+    ConvLayer("fc7", 4096, 1, 1, 4096, 1, 1, 0, 1, True),
+    ConvLayer("fc8", 4096, 1, 1, 1000, 1, 1, 0, 1, False),
+)
+# The whole CaffeNet chain of the paper's reference model: conv1-5, max-pool
+# after conv5, fc6-fc8 (dropout, a training-time mask, is not part of it).
+CAFFENET_NET = CAFFENET + CAFFENET_FC
+CAFFENET_NET_GLUE = {0: [("pool", CAFFENET_POOL), ("lrn", CAFFENET_LRN)],
+                     1: [("pool", CAFFENET_POOL), ("lrn", CAFFENET_LRN)],
+                     4: [("pool", CAFFENET_POOL)]}
+
+LENET_FC = (
+    ConvLayer("ip1", 50 * 4 * 4, 1, 1, 500, 1, 1, 0, 1, True),
+    ConvLayer("ip2", 500, 1, 1, 10, 1, 1, 0, 1, False),
+)
+
 # Workload ids (the third seed word).
 LENET_PAIR = 1          # LeNet conv pair, N=64
 CAFFENET_CONV1_FWD = 2  # conv1 forward, N=256
 CAFFENET_CONV25_FWD = 3 # conv2..5 forward, N=256, inputs drawn per layer
 CAFFENET_STEP = 4       # conv1-5 forward + backward with pool/LRN glue, N=256
 CAFFENET_STEP_BF16 = 5  # the same at N=512 with bfloat16 operands
+CAFFENET_FC_LAYER = 6   # one inner-product layer fc6..fc8, N=256, inputs drawn per layer
+CAFFENET_NET_STEP = 7   # conv1-5 + pool5 + fc6-fc8 forward + backward, N=256
 
 
 def rng(workload, tensor_id):
@@ -149,4 +172,31 @@ def caffenet_step(N=256, workload=CAFFENET_STEP):
     bs = [np.full((L.K,), 0.0 if l == 0 else 0.1, np.float32) for l, L in enumerate(CAFFENET)]
     Ho, Wo = CAFFENET[4].out_hw()
     g = normal(workload, 30, (N, CAFFENET[4].K, Ho, Wo), 1e-3)
+    return dict(x=x, W=Ws, b=bs, top_diff=g)
+
+
+def caffenet_fc_layer(l, N=256):
+    """Input, weights, bias and top gradient of inner-product layer l (0..2 ->
+    fc6..fc8): post-ReLU activations in, Gaussian weights (std 0.005 for
+    fc6-fc7, 0.01 for fc8, as the reference model initialises them)."""
+    w = CAFFENET_FC_LAYER
+    L = CAFFENET_FC[l]
+    return dict(x=half_normal(w, 40 + l, (N, L.C, 1, 1)),
+                W=normal(w, 10 + l, (L.K, L.C, 1, 1), 0.01 if l == 2 else 0.005),
+                b=np.full((L.K,), 0.1 if l < 2 else 0.0, np.float32),
+                top_diff=normal(w, 30 + l, (N, L.K, 1, 1), 1e-3))
+
+
+def caffenet_net_step(N=256):
+    """Weights, biases, input batch and fc8 top gradient of the whole-network
+    CaffeNet step (conv weights N(0, 0.01); fc6-fc7 N(0, 0.005), fc8
+    N(0, 0.01); biases 0.1, 0 for conv1 and fc8)."""
+    w = CAFFENET_NET_STEP
+    x = normal(w, 0, (N, 3, 227, 227), 50.0)
+    Ws, bs = [], []
+    for l, L in enumerate(CAFFENET_NET):
+        std = 0.005 if L.name in ("fc6", "fc7") else 0.01
+        Ws.append(normal(w, 10 + l, (L.K, L.C // L.g, L.k, L.k), std))
+        bs.append(np.full((L.K,), 0.0 if L.name in ("conv1", "fc8") else 0.1, np.float32))
+    g = normal(w, 30, (N, CAFFENET_NET[-1].K, 1, 1), 1e-3)
     return dict(x=x, W=Ws, b=bs, top_diff=g)

@@ -135,6 +135,29 @@ def test_workspace_sizes_bf16():
     assert cc.conv_workspace_size(d2, cc.PASS_FORWARD) >= 2 * 81 * 4 * 8 * 2
 
 
+def test_workspace_sizes_inner_product():
+    # a 1x1 convolution of a 1x1 image (one group, fp32) runs as dense GEMMs:
+    # the forward holds split-K partials (and X^T, W^T when C % 4 != 0), the
+    # backward D and D^T next to the partials
+    N, C, K = 256, 9216, 4096
+    d = cc.conv_desc((N, C, 1, 1), (K, C, 1, 1), 1, 0, 1, True)
+    assert cc.conv_workspace_size(d, cc.PASS_FORWARD) >= N * K * 4
+    d3 = cc.conv_desc((N, C - 1, 1, 1), (K, C - 1, 1, 1), 1, 0, 1, True)
+    assert cc.conv_workspace_size(d3, cc.PASS_FORWARD) >= (N * (C - 1) + K * (C - 1) + N * K) * 4
+    both = cc.conv_workspace_size(d, cc.PASS_BACKWARD)
+    assert both >= (2 * N * K + max(N * C, K * C)) * 4
+    for p in range(4):
+        assert cc.conv_workspace_size(d, p) % 256 == 0
+    # an empty batch plans (no tiles) without failing
+    d0 = cc.conv_desc((0, C, 1, 1), (K, C, 1, 1), 1, 0, 1, True)
+    for p in range(4):
+        assert cc.conv_workspace_size(d0, p) >= 0
+    # partials of 2^31 bytes or more are refused
+    with pytest.raises(cc.CaffeError):
+        cc.conv_workspace_size(cc.conv_desc((1, 1 << 20, 1, 1), (1 << 12, 1 << 20, 1, 1)),
+                               cc.PASS_BACKWARD)
+
+
 def test_pointer_checks_before_any_launch():
     lib = cc.load()
     P = ctypes.c_void_p

@@ -116,6 +116,24 @@ def test_full_size_kernel_is_inner_product():
                                rtol=1e-12, atol=1e-12)
 
 
+def test_inner_product_with_relu_is_masked_matmuls():
+    # an inner-product layer (Sec. 3.2's fully connected layers) is the 1x1
+    # convolution of a 1x1 image: y = relu(W x + b); with D = G [y > 0],
+    # dx = D W, dW = D^T x, db = sum over the batch of D
+    x = _rand(5, 9, 1, 1)
+    w = _rand(4, 9, 1, 1)
+    b = _rand(4)
+    X, Wm = x[:, :, 0, 0], w[:, :, 0, 0]
+    y = oracle.conv_forward(x, w, b, relu=True)
+    np.testing.assert_allclose(y[:, :, 0, 0], np.maximum(X @ Wm.T + b, 0), rtol=1e-13, atol=1e-13)
+    g = _rand(5, 4, 1, 1)
+    dx, dw, db = oracle.conv_backward(x, w, g, top=y, relu=True)
+    D = g[:, :, 0, 0] * (y[:, :, 0, 0] > 0)
+    np.testing.assert_allclose(dx[:, :, 0, 0], D @ Wm, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(dw[:, :, 0, 0], D.T @ X, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(db, D.sum(axis=0), rtol=1e-12, atol=1e-12)
+
+
 CASES = [
     # N, C, H, W, K, kh, kw, s, p, g
     (2, 3, 11, 9, 4, 3, 3, 1, 1, 1),

@@ -86,13 +86,25 @@ def test_caffenet_training_step_full_size():
     N = 256
     inp = wl.caffenet_step(N)
     net = ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue())
+    _run_and_check_step(net, wl.CAFFENET, inp, images=[0, 255])
+
+
+def test_caffenet_network_step_full_size():
+    """conv1-5, pool5 and the fc6-fc8 inner products at N=256: every layer
+    and glue stage on the tensors the GPU consumed, sampled as above."""
+    N = 256
+    inp = wl.caffenet_net_step(N)
+    net = ConvStack(wl.CAFFENET_NET, N, inp["W"], inp["b"], glue=wl.CAFFENET_NET_GLUE)
+    _run_and_check_step(net, wl.CAFFENET_NET, inp, images=[0, 200])
+
+
+def _run_and_check_step(net, layers, inp, images):
     x = torch.from_numpy(inp["x"]).to(DEV)
     g = torch.from_numpy(inp["top_diff"]).to(DEV)
     net.forward(x)
     net.backward(g)
     torch.cuda.synchronize()
-    images = [0, 255]
-    for l, L in enumerate(wl.CAFFENET):
+    for l, L in enumerate(layers):
         xl = _np(net.bottom[l])
         gl = _np(net.layer_top_diff(l, g))
         check_layer_sampled(L, xl, inp["W"][l], inp["b"][l], _np(net.top[l]), gl,
@@ -123,4 +135,4 @@ def _glue_dy(net, l, st):
     i = next(j for j, s in enumerate(stages) if s is st)
     if i + 1 < len(stages):
         return stages[i + 1]["dx"]
-    return net.dbottom[l + 1]
+    return net.dbottom[l + 1].view(st["y"].shape)

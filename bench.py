@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--network-steps", type=int, default=-1,
                     help="steps of the whole-network step (conv1-5, pool5, fc6-fc8) timed "
                          "after the conv stack (-1 = --steps; 0 = skip; fp32 only)")
+    ap.add_argument("--network-only", action="store_true",
+                    help="time only the whole-network step (profiling); the JSON line then "
+                         "carries its images/s as the value")
     ap.add_argument("--calibrate-copy-mb", type=int, default=0,
                     help="first run one plain device copy of this many MiB (a known-size "
                          "reference for the HBM byte counters)")
@@ -167,6 +170,18 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(3)
+    if args.network_only:
+        from paper_1408_5093_amd import workloads as wl
+        stream = torch.cuda.current_stream()
+        r = network_step(wl, ConvStack, args.batch, args.steps, args.warmup, stream)
+        print(json.dumps({"metric": "CaffeNet whole-network training images/s", "value":
+                          r["images_per_s"], "unit": "images/s", "n_gpus": 1, "steps": args.steps,
+                          "warmup": args.warmup, "ms_per_step": r["ms_per_step"],
+                          "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+                          "dtype": "f32", "data": "synthetic", "config": {
+                              "workload": r["workload"], "global_batch": args.batch},
+                          "network": r}), flush=True)
+        return
     N = args.batch if not args.bf16 or args.batch != 256 else 512
     workload = wl.CAFFENET_STEP_BF16 if args.bf16 else wl.CAFFENET_STEP
     print(f"[bench] generating seeded inputs N={N}", file=sys.stderr, flush=True)

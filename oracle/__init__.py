@@ -1,4 +1,5 @@
-"""CPU oracle for the Caffe convolution layer and its pooling/LRN glue.
+"""CPU oracle for the Caffe convolution layer, its pooling/LRN glue, the
+softmax loss and the SGD update.
 
 TEST INFRASTRUCTURE ONLY: only ``tests/``, ``__graft_entry__.smoke()`` and the
 ``cpu_baseline`` leg of ``bench.py`` may import this package.  It shares no
@@ -14,3 +15,4 @@ from .ref import (  # noqa: F401
     lrn_backward,
     num_threads,
 )
+from .solver import learning_rate, sgd_step, softmax_loss  # noqa: F401

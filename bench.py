@@ -152,6 +152,66 @@ def network_step(wl, ConvStack, N, steps, warmup, stream):
                              for k, v in sorted(acc.items())}}
 
 
+def shard_step(wl, ConvStack, steps, warmup, stream, N=32):
+    """The conv1-5 step on one GPU's shard of a data-parallel batch (32 of
+    8 x 32 images): what each GPU would compute between two gradient
+    all-reduces."""
+    import torch
+    print(f"[bench] conv1-5 step on a shard N={N}", file=sys.stderr, flush=True)
+    inp = wl.caffenet_step(N)
+    net = ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(wl))
+    x = torch.from_numpy(inp["x"]).cuda()
+    g = torch.from_numpy(inp["top_diff"]).cuda()
+    for _ in range(warmup):
+        net.forward(x, stream)
+        net.backward(g, stream)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        net.forward(x, stream)
+        net.backward(g, stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    flops = sum(3 * L.flops(N) for L in wl.CAFFENET)
+    return {"workload": "CaffeNet conv1-5 training step on a 32-image shard", "global_batch": N,
+            "ms_per_step": ms, "images_per_s": N / (ms * 1e-3),
+            "tflops": flops / (ms * 1e-3) / 1e12}
+
+
+def lenet_training(wl, ConvStack, steps, warmup, stream, N=64):
+    """LeNet training iterations (forward, softmax loss, backward, SGD update
+    of every blob) at N=64 on one resident synthetic batch: images/s."""
+    import torch
+    from paper_1408_5093_amd.net import SGDTrainer
+    print(f"[bench] LeNet training N={N}", file=sys.stderr, flush=True)
+    inp = wl.lenet_train(N, 1)
+    net = ConvStack(wl.LENET_NET, N, inp["W"], inp["b"], glue=wl.LENET_NET_GLUE)
+    sol = dict(wl.LENET_SOLVER)
+    tr = SGDTrainer(net, momentum=sol.pop("momentum"), weight_decay=sol.pop("weight_decay"),
+                    **sol)
+    x = torch.from_numpy(inp["x"][0]).cuda()
+    y = torch.from_numpy(inp["labels"][0]).cuda()
+    for _ in range(warmup):
+        tr.step(x, y, stream)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        tr.step(x, y, stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    return {"workload": ("LeNet training iteration: conv1, max-pool, conv2, max-pool, ip1 + ReLU, "
+                         "ip2, softmax loss, backward, SGD (momentum 0.9, decay 5e-4, inv "
+                         "schedule)"),
+            "global_batch": N, "ms_per_step": ms, "images_per_s": N / (ms * 1e-3),
+            "final_loss": float(tr.loss.item())}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -286,6 +346,8 @@ def main():
     nsteps = args.steps if args.network_steps < 0 else args.network_steps
     if nsteps > 0 and not args.bf16:
         out["network"] = network_step(wl, ConvStack, N, nsteps, args.warmup, stream)
+        out["lenet_training"] = lenet_training(wl, ConvStack, 10 * nsteps, args.warmup, stream)
+        out["shard_n32"] = shard_step(wl, ConvStack, nsteps, args.warmup, stream)
     if args.cpu_images > 0:
         print(f"[bench] CPU oracle baseline on {args.cpu_images} images", file=sys.stderr,
               flush=True)

@@ -15,7 +15,8 @@ import torch
 
 from . import _lib
 from ._lib import (  # noqa: F401
-    BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED, CAFFE_BF16, CAFFE_F32, PASS_BACKWARD,
+    BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED, CAFFE_BF16, CAFFE_F32, CAFFE_LR_EXP,
+    CAFFE_LR_FIXED, CAFFE_LR_INV, CAFFE_LR_STEP, LrSchedule, PASS_BACKWARD,
     PASS_BACKWARD_DATA, PASS_BACKWARD_WEIGHTS, PASS_FORWARD, POOL_RELU_INPUT, CaffeError, ConvDesc,
     LrnDesc, PoolDesc, check, load, LIB_PATH,
 )
@@ -24,6 +25,7 @@ __all__ = [
     "conv_desc", "conv_out_shape", "conv_workspace_size", "conv_forward", "conv_backward",
     "conv_backward_data", "conv_backward_weights", "maxpool_forward", "maxpool_backward",
     "lrn_forward", "lrn_backward", "cast_f32_to_bf16", "Workspace", "CaffeError",
+    "sgd_learning_rate", "softmax_loss", "sgd_update",
 ]
 
 
@@ -266,3 +268,52 @@ def cast_f32_to_bf16(x, out=None, stream=None):
     _dev(out, "out", torch.bfloat16)
     check(load().caffe_cast_f32_to_bf16(_ptr(x), _ptr(out), x.numel(), _stream(stream)))
     return out
+
+
+# ------------------------------------------------------------------ solver
+_POLICIES = {"fixed": CAFFE_LR_FIXED, "step": CAFFE_LR_STEP, "exp": CAFFE_LR_EXP,
+             "inv": CAFFE_LR_INV}
+
+
+def sgd_learning_rate(policy, base_lr, it, gamma=0.0, power=0.0, stepsize=1):
+    """The schedule's learning rate at iteration `it` (host-only C call)."""
+    sc = LrSchedule(_POLICIES[policy] if isinstance(policy, str) else int(policy),
+                    float(base_lr), float(gamma), float(power), int(stepsize))
+    out = ctypes.c_float()
+    check(load().caffe_sgd_learning_rate(ctypes.byref(sc), int(it), ctypes.byref(out)))
+    return out.value
+
+
+def caffe_softmax_loss(scores, labels, N, K, loss_weight, loss, sample_loss, prob, scores_diff,
+                       stream=None):
+    check(load().caffe_softmax_loss(_ptr(scores), _ptr(labels), int(N), int(K),
+                                    float(loss_weight), _ptr(loss), _ptr(sample_loss), _ptr(prob),
+                                    _ptr(scores_diff), _stream(stream)))
+
+
+def softmax_loss(scores, labels, loss_weight=1.0, prob=False, diff=True, out=None, stream=None):
+    """scores: (N, K, ...) float32 with K classes per row, labels: (N,) int32.
+    Returns (loss (1,), sample_loss (N,), prob or None, scores_diff or None);
+    `out` may hold preallocated (loss, sample_loss, prob, diff) tensors."""
+    _dev(scores, "scores", torch.float32)
+    _dev(labels, "labels", torch.int32)
+    N = scores.shape[0]
+    K = scores.numel() // N if N else int(torch.tensor(scores.shape[1:]).prod())
+    dev = scores.device
+    if out is None:
+        out = (torch.empty(1, dtype=torch.float32, device=dev),
+               torch.empty(N, dtype=torch.float32, device=dev),
+               torch.empty(scores.shape, dtype=torch.float32, device=dev) if prob else None,
+               torch.empty(scores.shape, dtype=torch.float32, device=dev) if diff else None)
+    caffe_softmax_loss(scores, labels, N, K, loss_weight, *out, stream=stream)
+    return out
+
+
+def sgd_update(w, g, v, lr, momentum=0.0, weight_decay=0.0, stream=None):
+    """In place: v <- momentum v + lr (g + weight_decay w); w <- w - v."""
+    for t, n in ((w, "w"), (g, "g"), (v, "v")):
+        _dev(t, n, torch.float32)
+    if not (w.numel() == g.numel() == v.numel()):
+        raise ValueError("w, g and v must have the same number of elements")
+    check(load().caffe_sgd_update(_ptr(w), _ptr(g), _ptr(v), w.numel(), float(lr),
+                                  float(momentum), float(weight_decay), _stream(stream)))

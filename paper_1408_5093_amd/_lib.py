@@ -29,13 +29,19 @@ PASS_BACKWARD_DATA = 1
 PASS_BACKWARD_WEIGHTS = 2
 PASS_BACKWARD = 3
 
-# every symbol the two public headers declare
+CAFFE_LR_FIXED = 0
+CAFFE_LR_STEP = 1
+CAFFE_LR_EXP = 2
+CAFFE_LR_INV = 3
+
+# every symbol the public headers declare
 EXPORTS = (
     "caffe_conv_out_shape", "caffe_conv_workspace_size", "caffe_conv_forward",
     "caffe_conv_backward_data", "caffe_conv_backward_weights", "caffe_conv_backward",
     "caffe_status_string", "caffe_last_error", "caffe_version",
     "caffe_pool_out_shape", "caffe_maxpool_forward", "caffe_maxpool_backward",
     "caffe_lrn_forward", "caffe_lrn_backward", "caffe_cast_f32_to_bf16",
+    "caffe_sgd_learning_rate", "caffe_softmax_loss", "caffe_sgd_update",
 )
 
 
@@ -54,6 +60,12 @@ class LrnDesc(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int32), ("C", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("W", ctypes.c_int32), ("local_size", ctypes.c_int32),
                 ("alpha", ctypes.c_float), ("beta", ctypes.c_float), ("k", ctypes.c_float)]
+
+
+class LrSchedule(ctypes.Structure):
+    _fields_ = [("policy", ctypes.c_int32), ("base_lr", ctypes.c_float),
+                ("gamma", ctypes.c_float), ("power", ctypes.c_float),
+                ("stepsize", ctypes.c_int32)]
 
 
 class CaffeError(RuntimeError):
@@ -94,6 +106,11 @@ def load():
         "caffe_lrn_forward": [ldp, vp, vp, vp],
         "caffe_lrn_backward": [ldp, vp, vp, vp, vp, vp],
         "caffe_cast_f32_to_bf16": [vp, vp, i64, vp],
+        "caffe_sgd_learning_rate": [ctypes.POINTER(LrSchedule), i64,
+                                    ctypes.POINTER(ctypes.c_float)],
+        "caffe_softmax_loss": [vp, vp, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp],
+        "caffe_sgd_update": [vp, vp, vp, i64, ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                             vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)

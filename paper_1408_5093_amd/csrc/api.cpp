@@ -9,9 +9,11 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cmath>
 
 #include "../../include/caffe_conv.h"
 #include "../../include/caffe_layers.h"
+#include "../../include/caffe_solver.h"
 #include "kernels.h"
 
 using namespace caffe_hip;
@@ -1060,6 +1062,81 @@ int caffe_cast_f32_to_bf16(const float* in, uint16_t* out, int64_t count, void* 
     CHECK(check_ptr(in, count > 0, "in"));
     CHECK(check_ptr(out, count > 0, "out"));
     LAUNCH(launch_cast_f32_bf16(in, out, count, (hipStream_t)stream), "cast launch");
+    return CAFFE_OK;
+}
+
+// ------------------------------------------------------------- solver
+int caffe_sgd_learning_rate(const caffe_lr_schedule* sc, int64_t iter, float* lr)
+{
+    if (!sc || !lr)
+        return fail(CAFFE_ERR_INVALID_ARG, "schedule or lr is NULL");
+    if (iter < 0)
+        return fail(CAFFE_ERR_INVALID_ARG, "iteration %lld < 0", (long long)iter);
+    if (!(sc->base_lr >= 0.f))
+        return fail(CAFFE_ERR_INVALID_ARG, "base_lr must be >= 0");
+    const double base = sc->base_lr, gamma = sc->gamma, t = (double)iter;
+    double r;
+    switch (sc->policy) {
+    case CAFFE_LR_FIXED:
+        r = base;
+        break;
+    case CAFFE_LR_STEP:
+        if (sc->stepsize < 1)
+            return fail(CAFFE_ERR_INVALID_ARG, "step schedule needs stepsize >= 1");
+        r = base * std::pow(gamma, (double)(iter / sc->stepsize));
+        break;
+    case CAFFE_LR_EXP:
+        r = base * std::pow(gamma, t);
+        break;
+    case CAFFE_LR_INV:
+        r = base * std::pow(1.0 + gamma * t, -(double)sc->power);
+        break;
+    default:
+        return fail(CAFFE_ERR_INVALID_ARG, "unknown learning-rate policy %d", sc->policy);
+    }
+    if (!std::isfinite(r) || !std::isfinite((float)r))
+        return fail(CAFFE_ERR_INVALID_ARG, "learning rate is not finite at iteration %lld",
+                    (long long)iter);
+    *lr = (float)r;
+    return CAFFE_OK;
+}
+
+int caffe_softmax_loss(const float* scores, const int32_t* labels, int32_t N, int32_t K,
+                       float loss_weight, float* loss, float* sample_loss, float* prob,
+                       float* scores_diff, void* stream)
+{
+    if (N < 0 || K < 1 || K > (1 << 24))
+        return fail(CAFFE_ERR_INVALID_ARG, "softmax loss needs N >= 0 and 1 <= K <= 2^24");
+    if ((int64_t)N * K * 4 > kMaxTensorBytes)
+        return fail(CAFFE_ERR_UNSUPPORTED, "a tensor reaches 2^31 bytes");
+    if (!std::isfinite(loss_weight))
+        return fail(CAFFE_ERR_INVALID_ARG, "loss_weight is not finite");
+    const bool nz = N > 0;
+    CHECK(check_ptr(scores, nz, "scores"));
+    CHECK(check_ptr(labels, nz, "labels"));
+    CHECK(check_ptr(loss, true, "loss"));
+    CHECK(check_ptr(sample_loss, nz, "sample_loss"));
+    CHECK(check_ptr(prob, false, "prob"));
+    CHECK(check_ptr(scores_diff, false, "scores_diff"));
+    LAUNCH(launch_softmax_loss(scores, labels, N, K, loss_weight, loss, sample_loss, prob,
+                               scores_diff, (hipStream_t)stream),
+           "softmax loss launch");
+    return CAFFE_OK;
+}
+
+int caffe_sgd_update(float* w, const float* g, float* v, int64_t count, float lr, float momentum,
+                     float weight_decay, void* stream)
+{
+    if (count < 0)
+        return fail(CAFFE_ERR_INVALID_ARG, "count < 0");
+    if (!std::isfinite(lr) || !std::isfinite(momentum) || !std::isfinite(weight_decay))
+        return fail(CAFFE_ERR_INVALID_ARG, "lr, momentum and weight_decay must be finite");
+    const bool nz = count > 0;
+    CHECK(check_ptr(w, nz, "w"));
+    CHECK(check_ptr(g, nz, "g"));
+    CHECK(check_ptr(v, nz, "v"));
+    LAUNCH(launch_sgd_update(w, g, v, count, lr, momentum, weight_decay, (hipStream_t)stream),
+           "SGD update launch");
     return CAFFE_OK;
 }
 

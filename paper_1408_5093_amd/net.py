@@ -16,7 +16,7 @@ from . import (BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED, CAFFE_BF16, 
                PASS_BACKWARD, PASS_FORWARD, POOL_RELU_INPUT, Workspace, caffe_conv_backward,
                caffe_conv_forward, cast_f32_to_bf16, conv_desc, conv_out_shape,
                conv_workspace_size, lrn_backward, lrn_forward, maxpool_backward, maxpool_forward,
-               pool_desc, pool_out_shape)
+               pool_desc, pool_out_shape, sgd_learning_rate, sgd_update, softmax_loss)
 
 
 class ConvStack:
@@ -171,3 +171,55 @@ class ConvStack:
             return top_diff_last
         st = self.stages[l]
         return st[0]["dx"] if st else self.dbottom[l + 1].view(self.top[l].shape)
+
+
+class SGDTrainer:
+    """Training of a ConvStack that ends in class scores (Sec. 3.4): each
+    iteration runs the forward pass, the softmax loss and its gradient, the
+    backward pass (no data gradient for the input batch) and one SGD update
+    of every weight and bias blob at the schedule's learning rate.  The
+    momentum histories start at zero; all blobs share one rate and decay."""
+
+    def __init__(self, net, policy="inv", base_lr=0.01, gamma=1e-4, power=0.75, stepsize=1,
+                 momentum=0.9, weight_decay=5e-4):
+        if net.bf16:
+            raise ValueError("SGDTrainer runs fp32 networks")
+        self.net = net
+        self.schedule = dict(policy=policy, base_lr=base_lr, gamma=gamma, power=power,
+                             stepsize=stepsize)
+        self.momentum = momentum
+        self.weight_decay = weight_decay
+        self.vW = [torch.zeros_like(w) for w in net.W]
+        self.vb = [torch.zeros_like(b) for b in net.b]
+        dev = net.W[0].device
+        top = net.top[-1]
+        self.loss = torch.empty(1, dtype=torch.float32, device=dev)
+        self.sample_loss = torch.empty(net.N, dtype=torch.float32, device=dev)
+        self.scores_diff = torch.empty(top.shape, dtype=torch.float32, device=dev)
+        self.iter = 0
+
+    def forward_backward(self, x, labels, stream=None):
+        """Loss and every parameter gradient of the batch; returns the loss (1,)."""
+        s = stream or torch.cuda.current_stream()
+        scores = self.net.forward(x, s)
+        softmax_loss(scores, labels, out=(self.loss, self.sample_loss, None, self.scores_diff),
+                     stream=s)
+        self.net.backward(self.scores_diff, s, data_grad_bottom=False)
+        return self.loss
+
+    def update(self, stream=None):
+        """One SGD step of every blob at iteration self.iter's rate."""
+        s = stream or torch.cuda.current_stream()
+        lr = sgd_learning_rate(it=self.iter, **self.schedule)
+        for l in range(len(self.net.layers)):
+            sgd_update(self.net.W[l], self.net.dW[l], self.vW[l], lr, self.momentum,
+                       self.weight_decay, stream=s)
+            sgd_update(self.net.b[l], self.net.db[l], self.vb[l], lr, self.momentum,
+                       self.weight_decay, stream=s)
+        self.iter += 1
+        return lr
+
+    def step(self, x, labels, stream=None):
+        loss = self.forward_backward(x, labels, stream)
+        self.update(stream)
+        return loss

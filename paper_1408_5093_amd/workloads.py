@@ -81,6 +81,13 @@ LENET_FC = (
     ConvLayer("ip1", 50 * 4 * 4, 1, 1, 500, 1, 1, 0, 1, True),
     ConvLayer("ip2", 500, 1, 1, 10, 1, 1, 0, 1, False),
 )
+# The whole LeNet of Fig. 1: conv1, pool, conv2, pool, ip1 + ReLU, ip2, then
+# the softmax loss; trained by SGD with momentum 0.9, weight decay 5e-4 and
+# the "inv" schedule lr = 0.01 (1 + 1e-4 t)^-0.75.
+LENET_NET = LENET + LENET_FC
+LENET_NET_GLUE = {0: [("pool", LENET_POOL)], 1: [("pool", LENET_POOL)]}
+LENET_SOLVER = dict(policy="inv", base_lr=0.01, gamma=1e-4, power=0.75, momentum=0.9,
+                    weight_decay=5e-4)
 
 # Workload ids (the third seed word).
 LENET_PAIR = 1          # LeNet conv pair, N=64
@@ -90,6 +97,7 @@ CAFFENET_STEP = 4       # conv1-5 forward + backward with pool/LRN glue, N=256
 CAFFENET_STEP_BF16 = 5  # the same at N=512 with bfloat16 operands
 CAFFENET_FC_LAYER = 6   # one inner-product layer fc6..fc8, N=256, inputs drawn per layer
 CAFFENET_NET_STEP = 7   # conv1-5 + pool5 + fc6-fc8 forward + backward, N=256
+LENET_TRAIN = 8         # LeNet training iterations (softmax loss + SGD), N=64
 
 
 def rng(workload, tensor_id):
@@ -200,3 +208,14 @@ def caffenet_net_step(N=256):
         bs.append(np.full((L.K,), 0.0 if L.name in ("conv1", "fc8") else 0.1, np.float32))
     g = normal(w, 30, (N, CAFFENET_NET[-1].K, 1, 1), 1e-3)
     return dict(x=x, W=Ws, b=bs, top_diff=g)
+
+
+def lenet_train(N=64, batches=1):
+    """Weights (Xavier-uniform), zero biases, `batches` input batches
+    (MNIST-like pixels U[0, 1)) and int32 labels uniform over the 10 classes."""
+    w = LENET_TRAIN
+    Ws = [xavier_uniform(w, 10 + l, (L.K, L.C // L.g, L.k, L.k)) for l, L in enumerate(LENET_NET)]
+    bs = [np.zeros((L.K,), np.float32) for L in LENET_NET]
+    xs = [uniform(w, 100 + i, (N, 1, 28, 28), 0.0, 1.0) for i in range(batches)]
+    ys = [rng(w, 200 + i).integers(0, 10, N).astype(np.int32) for i in range(batches)]
+    return dict(W=Ws, b=bs, x=xs, labels=ys)

@@ -230,3 +230,56 @@ def test_fastdiv_formula():
         assert mul < (1 << 32)
         for x in [0, d - 1, d, 2 ** 31 - 1] + [random.randrange(2 ** 31) for _ in range(50)]:
             assert (x * mul) >> sh == x // d
+
+
+# ------------------------------------------------------------------ solver ABI
+def test_learning_rate_schedules_match_oracle():
+    import oracle
+    cases = [("fixed", dict()), ("step", dict(gamma=0.1, stepsize=100)),
+             ("exp", dict(gamma=0.999)), ("inv", dict(gamma=1e-4, power=0.75))]
+    import numpy as np
+    f32 = lambda v: float(np.float32(v))  # the schedule's parameters are stored as float32
+    for policy, kw in cases:
+        kw32 = {k: (f32(v) if k != "stepsize" else v) for k, v in kw.items()}
+        for it in (0, 1, 99, 100, 101, 250, 5000, 10000):
+            got = cc.sgd_learning_rate(policy, 0.01, it, **kw)
+            ref = oracle.learning_rate(policy, f32(0.01), it, **kw32)
+            assert abs(got - ref) <= 1e-7 * ref + 1e-30, (policy, it, got, ref)
+
+
+def test_solver_argument_checks():
+    lib = cc.load()
+    P = ctypes.c_void_p
+    sm = lambda *a: lib.caffe_softmax_loss(*a)
+    ok = (P(0x1000), P(0x2000), 4, 10, 1.0, P(0x3000), P(0x4000), None, None, None)
+    bad = list(ok)
+    bad[3] = 0
+    assert sm(*bad) == -1                                          # K = 0
+    bad = list(ok)
+    bad[2] = -1
+    assert sm(*bad) == -1                                          # N < 0
+    bad = list(ok)
+    bad[5] = None
+    assert sm(*bad) == -1                                          # loss NULL
+    bad = list(ok)
+    bad[0] = P(0x1004)
+    assert sm(*bad) == -2                                          # misaligned scores
+    bad = list(ok)
+    bad[4] = float("nan")
+    assert sm(*bad) == -1                                          # loss_weight NaN
+    assert sm(P(0x1000), P(0x2000), 1 << 16, 1 << 14, 1.0, P(0x3000), P(0x4000), None, None,
+              None) == -4                                          # 2^32 bytes of scores
+    up = lambda *a: lib.caffe_sgd_update(*a)
+    assert up(P(0x1000), P(0x2000), P(0x3000), -1, 0.1, 0.9, 0.0, None) == -1
+    assert up(None, P(0x2000), P(0x3000), 8, 0.1, 0.9, 0.0, None) == -1
+    assert up(P(0x1000), P(0x2000), P(0x3008), 8, 0.1, 0.9, 0.0, None) == -2
+    assert up(P(0x1000), P(0x2000), P(0x3000), 8, float("inf"), 0.9, 0.0, None) == -1
+    assert up(None, None, None, 0, 0.1, 0.9, 0.0, None) == 0       # nothing to do
+    with pytest.raises(cc.CaffeError):
+        cc.sgd_learning_rate(7, 0.01, 0)                           # unknown policy
+    with pytest.raises(cc.CaffeError):
+        cc.sgd_learning_rate("step", 0.01, 5, gamma=0.1, stepsize=0)
+    with pytest.raises(cc.CaffeError):
+        cc.sgd_learning_rate("fixed", 0.01, -1)
+    with pytest.raises(cc.CaffeError):
+        cc.sgd_learning_rate("inv", 0.01, 2, gamma=-1.0, power=0.75)  # (1 - 2)^-0.75

@@ -77,6 +77,30 @@ int caffe_lrn_forward(const caffe_lrn_desc* desc, const float* bottom, float* to
 int caffe_lrn_backward(const caffe_lrn_desc* desc, const float* bottom, const float* top,
                        const float* top_diff, float* bottom_diff, void* stream);
 
+/* Max pooling followed by LRN of the pooled blob (CaffeNet's glue after
+ * conv1 and conv2).  `pool` describes the pooling of bottom; `lrn` must
+ * describe its output (N, C, Ho, Wo).  pooled, mask and top are written as
+ * caffe_maxpool_forward (with `flags`) followed by caffe_lrn_forward on
+ * `pooled` write them (the same two kernels, back to back: the pooled blob is
+ * an output the backward needs).  mask may be NULL.  The support conditions
+ * are those of caffe_lrn_pool_backward, so that a forward this call accepts
+ * has a fused backward; with N = 0 nothing is launched and the status says
+ * whether a geometry is supported. */
+int caffe_pool_lrn_forward(const caffe_pool_desc* pool, const caffe_lrn_desc* lrn,
+                           const float* bottom, float* pooled, int32_t* mask, float* top,
+                           int32_t flags, void* stream);
+
+/* The backward of that pair in one pass: bottom_diff as caffe_lrn_backward
+ * (pooled, top, top_diff) followed by caffe_maxpool_backward (with `mask`)
+ * would write it, without storing the pooled gradient (each block stages the
+ * pooled gradient of its input rows' covering windows in LDS).
+ * CAFFE_ERR_UNSUPPORTED unless lrn->local_size is 3 or 5, W <= 256 and
+ * min(Ho, (kernel_h - 1) / stride_h + 2) * Wo <= 256 (a block stages at most
+ * 256 pooled positions, one per thread). */
+int caffe_lrn_pool_backward(const caffe_pool_desc* pool, const caffe_lrn_desc* lrn,
+                            const float* pooled, const float* top, const float* top_diff,
+                            const int32_t* mask, float* bottom_diff, void* stream);
+
 /* out[i] = bfloat16(in[i]) rounded to nearest even, i < count.  The input for
  * CAFFE_BF16 convolutions. */
 int caffe_cast_f32_to_bf16(const float* in, uint16_t* out, int64_t count, void* stream);

@@ -15,7 +15,7 @@ import torch
 
 from . import _lib
 from ._lib import (  # noqa: F401
-    BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED, CAFFE_BF16, CAFFE_F32, CAFFE_LR_EXP,
+    CAFFE_ERR_UNSUPPORTED, BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED, CAFFE_BF16, CAFFE_F32, CAFFE_LR_EXP,
     CAFFE_LR_FIXED, CAFFE_LR_INV, CAFFE_LR_STEP, LrSchedule, PASS_BACKWARD,
     PASS_BACKWARD_DATA, PASS_BACKWARD_WEIGHTS, PASS_FORWARD, POOL_RELU_INPUT, CaffeError, ConvDesc,
     LrnDesc, PoolDesc, check, load, LIB_PATH,
@@ -25,7 +25,8 @@ __all__ = [
     "conv_desc", "conv_out_shape", "conv_workspace_size", "conv_forward", "conv_backward",
     "conv_backward_data", "conv_backward_weights", "maxpool_forward", "maxpool_backward",
     "lrn_forward", "lrn_backward", "cast_f32_to_bf16", "Workspace", "CaffeError",
-    "sgd_learning_rate", "softmax_loss", "sgd_update",
+    "sgd_learning_rate", "softmax_loss", "sgd_update", "pool_lrn_forward", "lrn_pool_backward",
+    "pool_lrn_supported",
 ]
 
 
@@ -258,6 +259,57 @@ def lrn_backward(x, y, top_diff, size=5, alpha=1e-4, beta=0.75, k=1.0, out=None,
     _dev(out, "bottom_diff", torch.float32)
     check(load().caffe_lrn_backward(ctypes.byref(d), _ptr(x), _ptr(y), _ptr(top_diff), _ptr(out),
                                     _stream(stream)))
+    return out
+
+
+def _pool_lrn_descs(x_shape, kernel, stride, pad, size, alpha, beta, k):
+    pd = pool_desc(x_shape, kernel, stride, pad)
+    Ho, Wo = pool_out_shape(pd)
+    ld = lrn_desc((pd.N, pd.C, Ho, Wo), size, alpha, beta, k)
+    return pd, ld, (pd.N, pd.C, Ho, Wo)
+
+
+def pool_lrn_supported(x_shape, kernel, stride, pad=0, size=5, alpha=1e-4, beta=0.75, k=1.0):
+    """Whether the fused max-pool + LRN kernels take this geometry (no launch)."""
+    shape = (0,) + tuple(x_shape[1:])
+    pd, ld, _ = _pool_lrn_descs(shape, kernel, stride, pad, size, alpha, beta, k)
+    st = load().caffe_pool_lrn_forward(ctypes.byref(pd), ctypes.byref(ld), None, None, None, None,
+                                       0, None)
+    if st == CAFFE_ERR_UNSUPPORTED:
+        return False
+    check(st)
+    return True
+
+
+def pool_lrn_forward(x, kernel, stride, pad=0, size=5, alpha=1e-4, beta=0.75, k=1.0,
+                     pooled=None, mask=None, out=None, flags=0, stream=None):
+    """Max-pool then LRN in one pass; returns (pooled, mask, out)."""
+    _dev(x, "bottom", torch.float32)
+    pd, ld, shape = _pool_lrn_descs(x.shape, kernel, stride, pad, size, alpha, beta, k)
+    pooled = torch.empty(shape, dtype=torch.float32, device=x.device) if pooled is None else pooled
+    mask = torch.empty(shape, dtype=torch.int32, device=x.device) if mask is None else mask
+    out = torch.empty(shape, dtype=torch.float32, device=x.device) if out is None else out
+    for t, n in ((pooled, "pooled"), (out, "top")):
+        _dev(t, n, torch.float32)
+    _dev(mask, "mask", torch.int32)
+    check(load().caffe_pool_lrn_forward(ctypes.byref(pd), ctypes.byref(ld), _ptr(x), _ptr(pooled),
+                                        _ptr(mask), _ptr(out), int(flags), _stream(stream)))
+    return pooled, mask, out
+
+
+def lrn_pool_backward(x_shape, pooled, top, top_diff, mask, kernel, stride, pad=0, size=5,
+                      alpha=1e-4, beta=0.75, k=1.0, out=None, stream=None):
+    """The backward of pool_lrn_forward in one pass; returns bottom_diff."""
+    pd, ld, _ = _pool_lrn_descs(x_shape, kernel, stride, pad, size, alpha, beta, k)
+    for t, n in ((pooled, "pooled"), (top, "top"), (top_diff, "top_diff")):
+        _dev(t, n, torch.float32)
+    _dev(mask, "mask", torch.int32)
+    if out is None:
+        out = torch.empty(tuple(x_shape), dtype=torch.float32, device=top_diff.device)
+    _dev(out, "bottom_diff", torch.float32)
+    check(load().caffe_lrn_pool_backward(ctypes.byref(pd), ctypes.byref(ld), _ptr(pooled),
+                                         _ptr(top), _ptr(top_diff), _ptr(mask), _ptr(out),
+                                         _stream(stream)))
     return out
 
 

@@ -42,6 +42,7 @@ EXPORTS = (
     "caffe_pool_out_shape", "caffe_maxpool_forward", "caffe_maxpool_backward",
     "caffe_lrn_forward", "caffe_lrn_backward", "caffe_cast_f32_to_bf16",
     "caffe_sgd_learning_rate", "caffe_softmax_loss", "caffe_sgd_update",
+    "caffe_pool_lrn_forward", "caffe_lrn_pool_backward",
 )
 
 
@@ -106,6 +107,8 @@ def load():
         "caffe_lrn_forward": [ldp, vp, vp, vp],
         "caffe_lrn_backward": [ldp, vp, vp, vp, vp, vp],
         "caffe_cast_f32_to_bf16": [vp, vp, i64, vp],
+        "caffe_pool_lrn_forward": [pdp, ldp, vp, vp, vp, vp, i32, vp],
+        "caffe_lrn_pool_backward": [pdp, ldp, vp, vp, vp, vp, vp, vp],
         "caffe_sgd_learning_rate": [ctypes.POINTER(LrSchedule), i64,
                                     ctypes.POINTER(ctypes.c_float)],
         "caffe_softmax_loss": [vp, vp, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp],

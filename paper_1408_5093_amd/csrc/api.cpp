@@ -1055,6 +1055,64 @@ int caffe_lrn_backward(const caffe_lrn_desc* d, const float* bottom, const float
     return CAFFE_OK;
 }
 
+static int check_pool_lrn(const caffe_pool_desc* pd, const caffe_lrn_desc* ld, int* Ho, int* Wo)
+{
+    CHECK(plan_pool(pd, Ho, Wo));
+    CHECK(check_lrn(ld));
+    if (ld->N != pd->N || ld->C != pd->C || ld->H != *Ho || ld->W != *Wo)
+        return fail(CAFFE_ERR_INVALID_ARG, "the LRN blob (%d, %d, %d, %d) is not the pooled blob "
+                    "(%d, %d, %d, %d)", ld->N, ld->C, ld->H, ld->W, pd->N, pd->C, *Ho, *Wo);
+    if (!pool_lrn_fusable(pd->H, pd->W, *Ho, *Wo, pd->kernel_h, pd->stride_h, pd->pad_h,
+                          ld->local_size))
+        return fail(CAFFE_ERR_UNSUPPORTED, "fused pool + LRN needs local_size 3 or 5, W <= 256 "
+                    "and at most 256 staged pooled positions");
+    return CAFFE_OK;
+}
+
+int caffe_pool_lrn_forward(const caffe_pool_desc* pd, const caffe_lrn_desc* ld,
+                           const float* bottom, float* pooled, int32_t* mask, float* top,
+                           int32_t flags, void* stream)
+{
+    if (flags & ~CAFFE_POOL_RELU_INPUT)
+        return fail(CAFFE_ERR_INVALID_ARG, "unknown pooling flags 0x%x", flags);
+    int Ho, Wo;
+    CHECK(check_pool_lrn(pd, ld, &Ho, &Wo));
+    const bool nz = pd->N > 0;
+    CHECK(check_ptr(bottom, nz, "bottom"));
+    CHECK(check_ptr(pooled, nz, "pooled"));
+    CHECK(check_ptr(mask, false, "mask"));
+    CHECK(check_ptr(top, nz, "top"));
+    LAUNCH(launch_maxpool_forward(bottom, pooled, mask, pd->N * pd->C, pd->H, pd->W, Ho, Wo,
+                                  pd->kernel_h, pd->kernel_w, pd->stride_h, pd->stride_w,
+                                  pd->pad_h, pd->pad_w, (flags & CAFFE_POOL_RELU_INPUT) ? 1 : 0,
+                                  (hipStream_t)stream),
+           "max-pool forward launch");
+    LAUNCH(launch_lrn_forward(pooled, top, ld->N, ld->C, ld->H * ld->W, ld->local_size, ld->alpha,
+                              ld->beta, ld->k, (hipStream_t)stream),
+           "LRN forward launch");
+    return CAFFE_OK;
+}
+
+int caffe_lrn_pool_backward(const caffe_pool_desc* pd, const caffe_lrn_desc* ld,
+                            const float* pooled, const float* top, const float* top_diff,
+                            const int32_t* mask, float* bottom_diff, void* stream)
+{
+    int Ho, Wo;
+    CHECK(check_pool_lrn(pd, ld, &Ho, &Wo));
+    const bool nz = pd->N > 0;
+    CHECK(check_ptr(pooled, nz, "pooled"));
+    CHECK(check_ptr(top, nz, "top"));
+    CHECK(check_ptr(top_diff, nz, "top_diff"));
+    CHECK(check_ptr(mask, nz, "mask"));
+    CHECK(check_ptr(bottom_diff, nz, "bottom_diff"));
+    LAUNCH(launch_lrn_pool_backward(pooled, top, top_diff, mask, bottom_diff, pd->N, pd->C, pd->H,
+                                    pd->W, Ho, Wo, pd->kernel_h, pd->kernel_w, pd->stride_h,
+                                    pd->stride_w, pd->pad_h, pd->pad_w, ld->local_size, ld->alpha,
+                                    ld->beta, ld->k, (hipStream_t)stream),
+           "fused LRN + pool backward launch");
+    return CAFFE_OK;
+}
+
 int caffe_cast_f32_to_bf16(const float* in, uint16_t* out, int64_t count, void* stream)
 {
     if (count < 0)

@@ -247,6 +247,14 @@ hipError_t launch_lrn_forward(const float* x, float* y, int N, int C, int HW, in
 hipError_t launch_lrn_backward(const float* x, const float* y, const float* dy, float* dx, int N,
                                int C, int HW, int size, float alpha, float beta, float k,
                                hipStream_t s);
+// The backward of max-pool then LRN in one pass (no pooled gradient in HBM).
+// LRN sizes 3 and 5; the geometry must pass pool_lrn_fusable
+// (hipErrorInvalidValue otherwise).
+bool pool_lrn_fusable(int H, int W, int OH, int OW, int kh, int sh, int ph, int size);
+hipError_t launch_lrn_pool_backward(const float* pooled, const float* top, const float* top_diff,
+                                    const int32_t* mask, float* dx, int N, int C, int H, int W,
+                                    int OH, int OW, int kh, int kw, int sh, int sw, int ph, int pw,
+                                    int size, float alpha, float beta, float k, hipStream_t s);
 hipError_t launch_cast_f32_bf16(const float* x, uint16_t* y, int64_t count, hipStream_t s);
 
 // ---- solver (solver.hip)

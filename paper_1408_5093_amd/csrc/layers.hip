@@ -645,6 +645,210 @@ hipError_t launch_lrn_backward(const float* x, const float* y, const float* dy, 
     return hipGetLastError();
 }
 
+// ------------------------------------------------------ fused LRN + max-pool backward
+// The CaffeNet glue after conv1 and conv2 is max-pool then LRN over the pooled
+// blob.  Its backward runs in one pass: a block owns (image, 16 channels, a
+// strip of input rows); it forms the LRN backward (the pooled gradient) for
+// every pooled row whose windows reach its input rows into LDS, then gathers
+// each input position's gradient from LDS -- the pooled gradient never goes
+// to HBM.  The arithmetic, and the order of every sum, is that of the
+// separate LRN and pool kernels.  (The forward keeps the two separate
+// kernels: the pooled blob must be stored for the backward anyway, so a
+// one-pass forward saves only its re-read, and staging 20 channels of input
+// rows per block left it slower than the plane-staged pool kernel.)
+constexpr int kFuseCh = 16;      // channels owned by a block
+constexpr int kFusePos = 256;    // pooled positions staged per block (one per thread)
+
+template <int KS, int SS, int SIZE>
+__global__ void __launch_bounds__(256)
+lrn_pool_backward_kernel(const float* __restrict__ a_in, const float* __restrict__ b_in,
+                         const float* __restrict__ g_in, const int32_t* __restrict__ mask,
+                         float* __restrict__ dx, int N, int C, int H, int W, int OH, int OW,
+                         int kh_, int kw_, int sh_, int sw_, int ph, int pw, int yrows,
+                         int nstrips, int nchunks, float alpha_over_n, float beta, float k)
+{
+    constexpr int PRE = (SIZE - 1) / 2;
+    constexpr int POST = SIZE - 1 - PRE;
+    constexpr int NR = kFuseCh + SIZE - 1;   // ratios: channels c0 - POST .. c0 + 15 + PRE
+    constexpr int NA = NR + SIZE - 1;        // inputs: channels c0 - POST - PRE .. + NA - 1
+    __shared__ float gs[kFuseCh][kFusePos];
+    __shared__ int32_t ms[kFuseCh][kFusePos];
+    const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
+    const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
+    const int strip = blockIdx.x % nstrips;
+    const int rest = blockIdx.x / nstrips;
+    const int c0 = (rest % nchunks) * kFuseCh;
+    const int n = rest / nchunks;
+    const int y_lo = strip * yrows;
+    const int y_hi = min(H, y_lo + yrows) - 1;
+    // pooled rows whose windows reach input rows y_lo .. y_hi
+    const int i_lo = max(0, (y_lo + ph - kh + sh) / sh);
+    const int i_hi = min(OH - 1, (y_hi + ph) / sh);
+    const int npos = (i_hi - i_lo + 1) * OW;
+    const int OHW = OH * OW, HW = H * W;
+    // phase 1: the pooled gradient (LRN backward) of the block's 16 channels at
+    // every staged pooled position, and the winners, into LDS
+    const int pos = threadIdx.x;
+    if (pos < npos) {
+        const int pix = (i_lo + pos / OW) * OW + (pos - (pos / OW) * OW);
+        const uint32_t bytes = (uint32_t)(N * C * OHW) * 4u;
+        const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_in, bytes);
+        const __amdgpu_buffer_rsrc_t rb = make_rsrc(b_in, bytes);
+        const __amdgpu_buffer_rsrc_t rg = make_rsrc(g_in, bytes);
+        const __amdgpu_buffer_rsrc_t rm = make_rsrc(mask, bytes);
+        const uint32_t base4 = (uint32_t)(n * C * OHW + pix) * 4u;
+        const uint32_t hw4 = (uint32_t)OHW * 4u;
+        auto off = [&](int ch) {
+            return (base4 + (uint32_t)ch * hw4) | ((uint32_t)((unsigned)ch >= (unsigned)C) << 31);
+        };
+        float a[NA], g[NR], b[NR];
+#pragma unroll
+        for (int q = 0; q < NA; ++q)
+            a[q] = buf_ld_f32(ra, off(c0 - POST - PRE + q));
+#pragma unroll
+        for (int q = 0; q < NR; ++q) {
+            g[q] = buf_ld_f32(rg, off(c0 - POST + q));
+            b[q] = buf_ld_f32(rb, off(c0 - POST + q));
+        }
+        float r[NR], sc[kFuseCh];
+#pragma unroll
+        for (int q = 0; q < NR; ++q) {
+            float sq = 0.f;
+#pragma unroll
+            for (int t = 0; t < SIZE; ++t)
+                sq += a[q + t] * a[q + t];
+            const float s = k + alpha_over_n * sq;
+            r[q] = g[q] * b[q] * __builtin_amdgcn_rcpf(s);
+            if (q >= POST && q < POST + kFuseCh)
+                sc[q - POST] = s;
+        }
+        const float coef = 2.f * alpha_over_n * beta;
+#pragma unroll
+        for (int t = 0; t < kFuseCh; ++t) {
+            float cross = 0.f;
+#pragma unroll
+            for (int q = 0; q < SIZE; ++q)
+                cross += r[t + q];
+            gs[t][pos] = g[t + POST] * pow_neg(sc[t], beta) - coef * a[t + POST + PRE] * cross;
+            // (channels past C stage zeros; phase 2 never reads them)
+            ms[t][pos] = (int32_t)__builtin_bit_cast(uint32_t, buf_ld_f32(rm, off(c0 + t)));
+        }
+    }
+    __syncthreads();
+    // phase 2: each input position of rows y_lo .. y_hi adds, in row-major
+    // window order, the pooled gradients of the covering windows whose winner
+    // it is
+    // Thread -> one input column w (threads past the last full group of W
+    // columns idle) and every g-th row of each channel; the covering windows'
+    // column range is fixed per thread.
+    const int groups = 256 / W;             // W <= 256 (the staged rows hold >= 1 row)
+    const int grp = threadIdx.x / W;
+    const int w = threadIdx.x - grp * W;
+    if (grp >= groups)
+        return;
+    const int ny = y_hi - y_lo + 1;
+    const int j0 = max(0, (w + pw - kw + sw) / sw);
+    const int j1 = min(OW - 1, (w + pw) / sw);
+    for (int t = 0; t < kFuseCh; ++t) {
+        const int ch = c0 + t;
+        if (ch >= C)
+            break;
+        float* dplane = dx + ((size_t)n * C + ch) * HW;
+        for (int hh = grp; hh < ny; hh += groups) {
+            const int h = y_lo + hh;
+            const int hw = h * W + w;
+            const int i0 = max(0, (h + ph - kh + sh) / sh);
+            const int i1 = min(OH - 1, (h + ph) / sh);
+            float sum = 0.f;
+            if constexpr (KS > 0) {
+                // the covering windows (at most T x T), read first with their
+                // indices clamped into the staged rows, then added in
+                // row-major order where valid and routed here
+                constexpr int T = (KS + SS - 1) / SS;
+                int m[T][T];
+                float g[T][T];
+#pragma unroll
+                for (int di = 0; di < T; ++di)
+#pragma unroll
+                    for (int dj = 0; dj < T; ++dj) {
+                        const int o = (min(i0 + di, i_hi) - i_lo) * OW + min(j0 + dj, OW - 1);
+                        m[di][dj] = ms[t][o];
+                        g[di][dj] = gs[t][o];
+                    }
+#pragma unroll
+                for (int di = 0; di < T; ++di)
+#pragma unroll
+                    for (int dj = 0; dj < T; ++dj)
+                        if (i0 + di <= i1 && j0 + dj <= j1 && m[di][dj] == hw)
+                            sum += g[di][dj];
+            } else {
+                for (int ii = i0; ii <= i1; ++ii)
+                    for (int jj = j0; jj <= j1; ++jj) {
+                        const int o = (ii - i_lo) * OW + jj;
+                        if (ms[t][o] == hw)
+                            sum += gs[t][o];
+                    }
+            }
+            dplane[hw] = sum;
+        }
+    }
+}
+
+// The backward's strip: `yrows` input rows whose covering pooled rows (at
+// most 256 positions) are staged; 0 when even one row does not fit.
+static int fused_backward_yrows(int H, int OH, int OW, int kh, int sh, int ph)
+{
+    for (int yr = H; yr >= 1; --yr) {
+        // worst strip: pooled rows reached by yr consecutive input rows
+        const int span = (yr - 1 + kh - 1) / sh + 1 + 1;
+        if (min(span, OH) * OW <= kFusePos)
+            return yr;
+    }
+    (void)ph;
+    return 0;
+}
+
+bool pool_lrn_fusable(int H, int W, int OH, int OW, int kh, int sh, int ph, int size)
+{
+    // (the backward gives each thread one input column of a row group)
+    return (size == 3 || size == 5) && W <= kFusePos &&
+           fused_backward_yrows(H, OH, OW, kh, sh, ph) > 0;
+}
+
+hipError_t launch_lrn_pool_backward(const float* pooled, const float* top, const float* top_diff,
+                                    const int32_t* mask, float* dx, int N, int C, int H, int W,
+                                    int OH, int OW, int kh, int kw, int sh, int sw, int ph, int pw,
+                                    int size, float alpha, float beta, float k, hipStream_t s)
+{
+    if ((long)N * C * H * W == 0)
+        return hipSuccess;
+    const int yrows = fused_backward_yrows(H, OH, OW, kh, sh, ph);
+    if (yrows == 0 || (size != 3 && size != 5))
+        return hipErrorInvalidValue;
+    const int nstrips = (H + yrows - 1) / yrows;
+    const int nchunks = (C + kFuseCh - 1) / kFuseCh;
+    const dim3 g((unsigned)((long)N * nchunks * nstrips));
+    const float an = alpha / size;
+#define FUSED_BWD(KS_, SS_, SZ_)                                                                  \
+    hipLaunchKernelGGL((lrn_pool_backward_kernel<KS_, SS_, SZ_>), g, dim3(256), 0, s, pooled,    \
+                       top, top_diff, mask, dx, N, C, H, W, OH, OW, kh, kw, sh, sw, ph, pw,     \
+                       yrows, nstrips, nchunks, an, beta, k)
+    const bool k32 = kh == 3 && kw == 3 && sh == 2 && sw == 2;
+    if (size == 5) {
+        if (k32)
+            FUSED_BWD(3, 2, 5);
+        else
+            FUSED_BWD(0, 0, 5);
+    } else {
+        if (k32)
+            FUSED_BWD(3, 2, 3);
+        else
+            FUSED_BWD(0, 0, 3);
+    }
+#undef FUSED_BWD
+    return hipGetLastError();
+}
+
 // --------------------------------------------------------------------- cast
 __global__ void __launch_bounds__(256)
 cast_f32_bf16_kernel(const float* __restrict__ x, uint16_t* __restrict__ y, int64_t count)

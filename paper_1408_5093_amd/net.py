@@ -16,7 +16,8 @@ from . import (BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED, CAFFE_BF16, 
                PASS_BACKWARD, PASS_FORWARD, POOL_RELU_INPUT, Workspace, caffe_conv_backward,
                caffe_conv_forward, cast_f32_to_bf16, conv_desc, conv_out_shape,
                conv_workspace_size, lrn_backward, lrn_forward, maxpool_backward, maxpool_forward,
-               pool_desc, pool_out_shape, sgd_learning_rate, sgd_update, softmax_loss)
+               lrn_pool_backward, pool_desc, pool_lrn_forward, pool_lrn_supported,
+               pool_out_shape, sgd_learning_rate, sgd_update, softmax_loss)
 
 
 class ConvStack:
@@ -24,7 +25,8 @@ class ConvStack:
     applied in order to the output of layer l.  bf16=True runs the convolutions on
     bfloat16 operands (fp32 accumulation and outputs); glue stays fp32."""
 
-    def __init__(self, layers, N, weights, biases, glue=None, bf16=False, device="cuda"):
+    def __init__(self, layers, N, weights, biases, glue=None, bf16=False, device="cuda",
+                 fuse_glue=True):
         self.layers = list(layers)
         self.N = N
         self.bf16 = bf16
@@ -97,6 +99,17 @@ class ConvStack:
             elif not st and l + 1 < n:
                 self.mask_bottom[l + 1] = True
                 self.top_masked[l] = True
+        # A max-pool directly followed by an LRN runs as one fused pass each
+        # way (the pooled gradient never stored) when the kernels take the
+        # geometry; the LRN stage then has no "dx".
+        self.fused = [False] * n
+        for l in range(n):
+            st = self.stages[l]
+            if (fuse_glue and len(st) == 2 and st[0]["kind"] == "pool" and st[1]["kind"] == "lrn"):
+                p, r = st[0]["prm"], st[1]["prm"]
+                self.fused[l] = pool_lrn_supported(st[0]["in_shape"], p["kernel"], p["stride"],
+                                                   p.get("pad", 0), r["size"], r["alpha"],
+                                                   r["beta"], r["k"])
         # when a list, (tag, event) pairs are recorded around every conv call
         self.events = None
 
@@ -121,6 +134,15 @@ class ConvStack:
             caffe_conv_forward(self.descs[l], src, self.W[l], self.b[l], self.top[l], self.ws, s)
             self._mark(("fwd", l, "end"), s)
             cur = self.top[l]
+            if self.fused[l]:
+                pst, lst = self.stages[l]
+                p, r = pst["prm"], lst["prm"]
+                pst["x"], lst["x"] = cur, pst["y"]
+                pool_lrn_forward(cur, p["kernel"], p["stride"], p.get("pad", 0), r["size"],
+                                 r["alpha"], r["beta"], r["k"], pooled=pst["y"], mask=pst["mask"],
+                                 out=lst["y"], flags=self.pool_flags[l], stream=s)
+                cur = lst["y"]
+                continue
             for st in self.stages[l]:
                 p = st["prm"]
                 st["x"] = cur
@@ -142,7 +164,13 @@ class ConvStack:
         for l in range(len(self.layers) - 1, -1, -1):
             L = self.layers[l]
             g = g.view(self.out_shape[l])
-            for st in reversed(self.stages[l]):
+            if self.fused[l]:
+                pst, lst = self.stages[l]
+                p, r = pst["prm"], lst["prm"]
+                g = lrn_pool_backward(pst["in_shape"], pst["y"], lst["y"], g, pst["mask"],
+                                      p["kernel"], p["stride"], p.get("pad", 0), r["size"],
+                                      r["alpha"], r["beta"], r["k"], out=pst["dx"], stream=s)
+            for st in (reversed(self.stages[l]) if not self.fused[l] else ()):
                 p = st["prm"]
                 if st["kind"] == "pool":
                     g = maxpool_backward(st["in_shape"], g, st["mask"], p["kernel"], p["stride"],

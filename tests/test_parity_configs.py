@@ -117,10 +117,23 @@ def _run_and_check_step(net, layers, inp, images):
             if st["kind"] == "pool":
                 ref = oracle.maxpool_forward(xin, p["kernel"], p["stride"])
                 np.testing.assert_array_equal(_np(st["y"])[images], ref.astype(np.float32))
-                gref = oracle.maxpool_backward(xin, _np(_glue_dy(net, l, st))[images],
-                                               p["kernel"], p["stride"])
+                if net.fused[l]:
+                    # pool + LRN backward in one pass: the pooled gradient is
+                    # the LRN backward of what the LRN received
+                    lst = net.stages[l][1]
+                    r = lst["prm"]
+                    dy = oracle.lrn_backward(_np(lst["x"])[images],
+                                             _np(_glue_dy(net, l, lst))[images], r["size"],
+                                             r["alpha"], r["beta"], r["k"])
+                else:
+                    dy = _np(_glue_dy(net, l, st))[images]
+                gref = oracle.maxpool_backward(xin, dy, p["kernel"], p["stride"])
                 if net.pool_flags[l] and st is net.stages[l][0]:
                     gref = gref * (xin > 0)  # the fused backward of conv's ReLU
+            elif net.fused[l]:
+                ref = oracle.lrn_forward(xin, p["size"], p["alpha"], p["beta"], p["k"])
+                assert_close(_np(st["y"])[images], ref, TOL_F32, f"{L.name} LRN forward")
+                continue  # no separate LRN gradient
             else:
                 ref = oracle.lrn_forward(xin, p["size"], p["alpha"], p["beta"], p["k"])
                 assert_close(_np(st["y"])[images], ref, TOL_F32, f"{L.name} LRN forward")

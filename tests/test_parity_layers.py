@@ -91,3 +91,61 @@ def test_maxpool_relu_input_flag():
     dx = cc.maxpool_backward(x.shape, _t(g), mask, 3, 2, 0)
     assert_close(_np(dx), oracle.maxpool_backward(x, g, 3, 2) * (x > 0), TOL_F32,
                  "pool backward with ReLU input")
+
+
+# ------------------------------------------------ fused max-pool + LRN
+FUSED = [
+    # shape, pool k, s, p, LRN size, alpha, beta, k
+    ((3, 96, 55, 55), 3, 2, 0, 5, 1e-4, 0.75, 1.0),    # CaffeNet pool1 + norm1 (3 strips)
+    ((2, 256, 27, 27), 3, 2, 0, 5, 1e-4, 0.75, 1.0),   # pool2 + norm2
+    ((2, 20, 17, 19), 3, 2, 0, 5, 0.5, 0.75, 2.0),     # a partial 16-channel chunk
+    ((1, 5, 21, 23), 3, 2, 1, 3, 1.0, 0.5, 1.0),       # padded windows, LRN size 3
+    ((2, 18, 24, 24), 2, 2, 0, 5, 0.3, 0.6, 1.5),      # 2x2/2
+    ((1, 33, 80, 78), 3, 3, 2, 5, 0.4, 0.75, 1.0),     # any-window path, several strips
+]
+
+
+@pytest.mark.parametrize("shape,pk,ps,pp,size,alpha,beta,k", FUSED)
+@pytest.mark.parametrize("relu_input", [False, True])
+def test_pool_lrn_fused(shape, pk, ps, pp, size, alpha, beta, k, relu_input):
+    print(f"fused pool+lrn {shape} pool {pk}/{ps}/{pp} lrn {size} relu_input={relu_input}",
+          flush=True)
+    rng = np.random.default_rng([5, *shape, pk, ps, pp, size, int(relu_input)])
+    x = (rng.standard_normal(shape) * 20).astype(np.float32)
+    if relu_input:
+        x = np.maximum(x, 0)
+    flags = cc.POOL_RELU_INPUT if relu_input else 0
+    assert cc.pool_lrn_supported(shape, pk, ps, pp, size, alpha, beta, k)
+    pooled, mask, y = cc.pool_lrn_forward(_t(x), pk, ps, pp, size, alpha, beta, k, flags=flags)
+    p_ref = oracle.maxpool_forward(x, pk, ps, pp)
+    np.testing.assert_array_equal(_np(pooled), p_ref.astype(np.float32))
+    assert_close(_np(y), oracle.lrn_forward(_np(pooled), size, alpha, beta, k), TOL_F32,
+                 "fused forward (LRN)")
+    # the same values and winners as the two separate layers
+    y2, mask2 = cc.maxpool_forward(_t(x), pk, ps, pp, flags=flags)
+    np.testing.assert_array_equal(_np(mask), _np(mask2))
+    z2 = cc.lrn_forward(y2, size, alpha, beta, k)
+    assert_close(_np(y), _np(z2), 1e-6, "fused vs separate forward")
+    g = rng.standard_normal(p_ref.shape).astype(np.float32)
+    dx = cc.lrn_pool_backward(shape, pooled, y, _t(g), mask, pk, ps, pp, size, alpha, beta, k)
+    dp_ref = oracle.lrn_backward(_np(pooled), g, size, alpha, beta, k)
+    dx_ref = oracle.maxpool_backward(x, dp_ref, pk, ps, pp)
+    if relu_input:
+        dx_ref = dx_ref * (x > 0)
+    assert_close(_np(dx), dx_ref, TOL_F32, "fused backward")
+    dp2 = cc.lrn_backward(pooled, y, _t(g), size, alpha, beta, k)
+    dx2 = cc.maxpool_backward(shape, dp2, mask, pk, ps, pp)
+    assert_close(_np(dx), _np(dx2), 1e-6, "fused vs separate backward")
+
+
+def test_pool_lrn_fused_unsupported_and_empty():
+    # 3 staged pooled rows of 200 columns exceed 256 positions
+    assert not cc.pool_lrn_supported((1, 4, 401, 401), 3, 2, 0, 5)
+    with pytest.raises(cc.CaffeError):
+        cc.pool_lrn_forward(torch.zeros((1, 4, 401, 401), device=DEV), 3, 2, 0, 5)
+    assert not cc.pool_lrn_supported((1, 4, 55, 55), 3, 2, 0, 7)   # LRN size 7
+    x = torch.zeros((0, 8, 9, 9), device=DEV)
+    pooled, mask, y = cc.pool_lrn_forward(x, 3, 2, 0, 5)
+    dx = cc.lrn_pool_backward(x.shape, pooled, y, torch.zeros_like(y), mask, 3, 2, 0, 5)
+    torch.cuda.synchronize()
+    assert dx.shape == x.shape

@@ -85,6 +85,13 @@ int caffe_softmax_loss(const float* scores, const int32_t* labels, int32_t N, in
 int caffe_sgd_update(float* w, const float* g, float* v, int64_t count, float lr, float momentum,
                      float weight_decay, void* stream);
 
+/* The same update with the learning rate read from device memory (`lr`, one
+ * float, 4-byte aligned) when the kernel runs, not when it is enqueued: a
+ * captured HIP graph of a training iteration then follows a schedule when
+ * the caller writes the iteration's rate to `lr` before each replay. */
+int caffe_sgd_update_device_lr(float* w, const float* g, float* v, int64_t count, const float* lr,
+                               float momentum, float weight_decay, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

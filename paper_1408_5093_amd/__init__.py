@@ -362,10 +362,18 @@ def softmax_loss(scores, labels, loss_weight=1.0, prob=False, diff=True, out=Non
 
 
 def sgd_update(w, g, v, lr, momentum=0.0, weight_decay=0.0, stream=None):
-    """In place: v <- momentum v + lr (g + weight_decay w); w <- w - v."""
+    """In place: v <- momentum v + lr (g + weight_decay w); w <- w - v.  `lr`
+    is a number, or a one-element float32 device tensor read when the kernel
+    runs (for graph capture)."""
     for t, n in ((w, "w"), (g, "g"), (v, "v")):
         _dev(t, n, torch.float32)
     if not (w.numel() == g.numel() == v.numel()):
         raise ValueError("w, g and v must have the same number of elements")
+    if isinstance(lr, torch.Tensor):
+        _dev(lr, "lr", torch.float32)
+        check(load().caffe_sgd_update_device_lr(_ptr(w), _ptr(g), _ptr(v), w.numel(), _ptr(lr),
+                                                float(momentum), float(weight_decay),
+                                                _stream(stream)))
+        return
     check(load().caffe_sgd_update(_ptr(w), _ptr(g), _ptr(v), w.numel(), float(lr),
                                   float(momentum), float(weight_decay), _stream(stream)))

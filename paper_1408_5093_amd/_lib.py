@@ -42,7 +42,7 @@ EXPORTS = (
     "caffe_pool_out_shape", "caffe_maxpool_forward", "caffe_maxpool_backward",
     "caffe_lrn_forward", "caffe_lrn_backward", "caffe_cast_f32_to_bf16",
     "caffe_sgd_learning_rate", "caffe_softmax_loss", "caffe_sgd_update",
-    "caffe_pool_lrn_forward", "caffe_lrn_pool_backward",
+    "caffe_pool_lrn_forward", "caffe_lrn_pool_backward", "caffe_sgd_update_device_lr",
 )
 
 
@@ -114,6 +114,7 @@ def load():
         "caffe_softmax_loss": [vp, vp, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp],
         "caffe_sgd_update": [vp, vp, vp, i64, ctypes.c_float, ctypes.c_float, ctypes.c_float,
                              vp],
+        "caffe_sgd_update_device_lr": [vp, vp, vp, i64, vp, ctypes.c_float, ctypes.c_float, vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)

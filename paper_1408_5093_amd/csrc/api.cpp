@@ -1193,7 +1193,28 @@ int caffe_sgd_update(float* w, const float* g, float* v, int64_t count, float lr
     CHECK(check_ptr(w, nz, "w"));
     CHECK(check_ptr(g, nz, "g"));
     CHECK(check_ptr(v, nz, "v"));
-    LAUNCH(launch_sgd_update(w, g, v, count, lr, momentum, weight_decay, (hipStream_t)stream),
+    LAUNCH(launch_sgd_update(w, g, v, count, lr, nullptr, momentum, weight_decay,
+                             (hipStream_t)stream),
+           "SGD update launch");
+    return CAFFE_OK;
+}
+
+int caffe_sgd_update_device_lr(float* w, const float* g, float* v, int64_t count, const float* lr,
+                               float momentum, float weight_decay, void* stream)
+{
+    if (count < 0)
+        return fail(CAFFE_ERR_INVALID_ARG, "count < 0");
+    if (!std::isfinite(momentum) || !std::isfinite(weight_decay))
+        return fail(CAFFE_ERR_INVALID_ARG, "momentum and weight_decay must be finite");
+    const bool nz = count > 0;
+    CHECK(check_ptr(w, nz, "w"));
+    CHECK(check_ptr(g, nz, "g"));
+    CHECK(check_ptr(v, nz, "v"));
+    if (nz && !lr)
+        return fail(CAFFE_ERR_INVALID_ARG, "lr is NULL");
+    if (lr && !aligned(lr, 4))
+        return fail(CAFFE_ERR_ALIGN, "lr is not 4-byte aligned");
+    LAUNCH(launch_sgd_update(w, g, v, count, 0.f, lr, momentum, weight_decay, (hipStream_t)stream),
            "SGD update launch");
     return CAFFE_OK;
 }

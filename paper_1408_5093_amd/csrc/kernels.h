@@ -263,8 +263,9 @@ hipError_t launch_cast_f32_bf16(const float* x, uint16_t* y, int64_t count, hipS
 hipError_t launch_softmax_loss(const float* z, const int32_t* labels, int N, int K,
                                float loss_weight, float* loss, float* sample_loss, float* prob,
                                float* diff, hipStream_t s);
-// v <- momentum v + lr (g + decay w); w <- w - v (16-byte aligned pointers).
+// v <- momentum v + lr (g + decay w); w <- w - v (16-byte aligned pointers);
+// lr is read from lr_dev when that is non-null.
 hipError_t launch_sgd_update(float* w, const float* g, float* v, int64_t count, float lr,
-                             float momentum, float decay, hipStream_t s);
+                             const float* lr_dev, float momentum, float decay, hipStream_t s);
 
 }  // namespace caffe_hip

@@ -87,11 +87,14 @@ hipError_t launch_softmax_loss(const float* z, const int32_t* labels, int N, int
 }
 
 // v <- momentum v + lr (g + decay w); w <- w - v, four elements per lane per
-// iteration (the pointers are 16-byte aligned), then the tail.
+// iteration (the pointers are 16-byte aligned), then the tail.  With lr_dev
+// non-null the rate is read from device memory when the kernel runs.
 __global__ void __launch_bounds__(256)
 sgd_update_kernel(float* __restrict__ w, const float* __restrict__ g, float* __restrict__ v,
-                  int64_t count, float lr, float momentum, float decay)
+                  int64_t count, float lr_arg, const float* __restrict__ lr_dev, float momentum,
+                  float decay)
 {
+    const float lr = lr_dev ? *lr_dev : lr_arg;
     const int64_t n4 = count >> 2;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n4; i += stride) {
@@ -118,14 +121,14 @@ sgd_update_kernel(float* __restrict__ w, const float* __restrict__ g, float* __r
 }
 
 hipError_t launch_sgd_update(float* w, const float* g, float* v, int64_t count, float lr,
-                             float momentum, float decay, hipStream_t s)
+                             const float* lr_dev, float momentum, float decay, hipStream_t s)
 {
     if (count == 0)
         return hipSuccess;
     int64_t blocks = ((count >> 2) + 255) / 256;
     blocks = blocks < 1 ? 1 : (blocks > 4096 ? 4096 : blocks);
     hipLaunchKernelGGL(sgd_update_kernel, dim3((unsigned)blocks), dim3(256), 0, s, w, g, v, count,
-                       lr, momentum, decay);
+                       lr, lr_dev, momentum, decay);
     return hipGetLastError();
 }
 

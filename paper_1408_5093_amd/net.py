@@ -251,3 +251,38 @@ class SGDTrainer:
         loss = self.forward_backward(x, labels, stream)
         self.update(stream)
         return loss
+
+    # ------------------------------------------------------------ HIP graph
+    def capture(self, x, labels):
+        """Record one whole iteration -- forward, loss, backward and the
+        updates, with the learning rate read from device memory -- as a HIP
+        graph over the static batch buffers x and labels (which must stay
+        allocated; refill them in place to train on other batches).  Every
+        buffer the iteration touches is preallocated and no call in it
+        allocates or records a memset, so replays rerun the same launches."""
+        dev = self.net.W[0].device
+        self.lr_dev = torch.empty(1, dtype=torch.float32, device=dev)
+        # one eager pass first, so every host-side plan query happens before
+        # capture (it leaves only gradients behind, which the graph rewrites)
+        self.forward_backward(x, labels)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            s = torch.cuda.current_stream()
+            self.forward_backward(x, labels, s)
+            for l in range(len(self.net.layers)):
+                sgd_update(self.net.W[l], self.net.dW[l], self.vW[l], self.lr_dev, self.momentum,
+                           self.weight_decay, stream=s)
+                sgd_update(self.net.b[l], self.net.db[l], self.vb[l], self.lr_dev, self.momentum,
+                           self.weight_decay, stream=s)
+        self.graph = g
+        return g
+
+    def replay(self):
+        """One iteration through the captured graph at iteration self.iter's
+        rate (written to device memory before the replay, outside the graph)."""
+        lr = sgd_learning_rate(it=self.iter, **self.schedule)
+        self.lr_dev.fill_(lr)
+        self.graph.replay()
+        self.iter += 1
+        return self.loss

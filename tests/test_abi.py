@@ -275,6 +275,10 @@ def test_solver_argument_checks():
     assert up(P(0x1000), P(0x2000), P(0x3008), 8, 0.1, 0.9, 0.0, None) == -2
     assert up(P(0x1000), P(0x2000), P(0x3000), 8, float("inf"), 0.9, 0.0, None) == -1
     assert up(None, None, None, 0, 0.1, 0.9, 0.0, None) == 0       # nothing to do
+    upd = lambda *a: lib.caffe_sgd_update_device_lr(*a)
+    assert upd(P(0x1000), P(0x2000), P(0x3000), 8, None, 0.9, 0.0, None) == -1   # lr NULL
+    assert upd(P(0x1000), P(0x2000), P(0x3000), 8, P(0x4002), 0.9, 0.0, None) == -2
+    assert upd(P(0x1000), P(0x2000), P(0x3000), -1, P(0x4000), 0.9, 0.0, None) == -1
     with pytest.raises(cc.CaffeError):
         cc.sgd_learning_rate(7, 0.01, 0)                           # unknown policy
     with pytest.raises(cc.CaffeError):

@@ -168,3 +168,28 @@ def test_lenet_training_fits_a_batch():
     losses = [float(_np(tr.step(x, y))[0]) for _ in range(60)]
     assert abs(losses[0] - np.log(10)) < 0.5
     assert losses[-1] < 0.5 * losses[0], losses[::10]
+
+
+def test_lenet_training_graph_replays_match_eager():
+    """The captured iteration, replayed with eager work and synchronizations
+    between replays, gives bitwise the weights, histories and losses of the
+    eager iterations from the same start (trainer state after every replay)."""
+    N = 64
+    inp, net_e, tr_e = _lenet_trainer(N, 3)
+    _, net_g, tr_g = _lenet_trainer(N, 3)
+    xs = [_t(a) for a in inp["x"]]
+    ys = [_t(a, torch.int32) for a in inp["labels"]]
+    xg, yg = xs[0].clone(), ys[0].clone()      # the graph's static batch buffers
+    tr_g.capture(xg, yg)
+    for it in range(3):
+        print(f"graph replay {it}", flush=True)
+        le = tr_e.step(xs[it], ys[it])
+        xg.copy_(xs[it])
+        yg.copy_(ys[it])
+        lg = tr_g.replay()
+        torch.cuda.synchronize()
+        _ = torch.randn(1000, device=DEV).sum().item()   # eager work between replays
+        assert torch.equal(le, lg), (le, lg)
+        for a, b in zip(net_e.W + net_e.b + tr_e.vW + tr_e.vb,
+                        net_g.W + net_g.b + tr_g.vW + tr_g.vb):
+            assert torch.equal(a, b)

@@ -71,6 +71,11 @@ struct ConvPlan {
     // inner-product shape (1x1 kernel on 1x1 spatial, one group, fp32): dense
     // split-K GEMMs with rows = samples (forward, data gradient) or outputs
     // (weight gradient)
+    // split-K of the convolution GEMMs (1 = the fused epilogue): partials
+    // after the packed weights (forward) and in the weight-partial region
+    // (data gradient)
+    int fwd_splits, fwd_sps, dgrad_splits, dgrad_sps;
+    size_t off_fwd_part;
     bool dense;
     int fc_tile_f, fc_tile_d, fc_tile_w;
     int fc_splits_f, fc_sps_f, fc_splits_d, fc_sps_d, fc_splits_w, fc_sps_w;
@@ -85,12 +90,15 @@ struct ConvPlan {
 // on the inner-product shapes: splits that leave some units one workgroup
 // more than the rest cost that whole extra workgroup; a unit with a single
 // workgroup runs it ~10% slower, its memory latency less hidden); s splits
-// add s * M * ncol partial sums written and read back once.  The plan takes
-// the s with the least modelled time (ties: fewer splits).
-void plan_splits(int M, int ncol, int R, int tile, int cus, int forced, int* splits, int* sps)
+// add s * groups * M * ncol partial sums written and read back once.  The
+// plan takes the s with the least modelled time (ties: fewer splits), and
+// splits only when that time is at least 10% below the unsplit one.
+void plan_splits(int M, int ncol, int R, int tile, int cus, int forced, int* splits, int* sps,
+                 int groups = 1)
 {
     const int tm = gemm_tile_m(tile), tn = gemm_tile_n(tile), tk = gemm_tile_k(tile);
-    const int64_t tiles = std::max<int64_t>(1, (int64_t)((M + tm - 1) / tm) * ((ncol + tn - 1) / tn));
+    const int64_t tiles = std::max<int64_t>(
+        1, (int64_t)groups * ((M + tm - 1) / tm) * ((ncol + tn - 1) / tn));
     const int64_t nst = std::max(1, (R + tk - 1) / tk);
     cus = std::max(1, cus);
     // one workgroup-stage at ~85% of a unit's fp32 MFMA rate (157.3 TFLOP/s
@@ -98,19 +106,25 @@ void plan_splits(int M, int ncol, int R, int tile, int cus, int forced, int* spl
     const double t_stage = 2.0 * tm * tn * tk / (0.85 * 157.3e12 / 256);
     const double t_byte = 1.0 / 4e12;
     int64_t best = 1;
-    double best_t = -1;
+    double best_t = -1, t1 = 0;
     for (int64_t sp = 1; sp <= nst; ++sp) {
-        const double part = sp > 1 ? 8.0 * sp * M * ncol : 0.0;
+        const double part = sp > 1 ? 8.0 * sp * groups * M * ncol : 0.0;
         if (part / 2 > (double)kMaxTensorBytes)
             break;
         const int64_t load = (tiles * sp + cus - 1) / cus;  // workgroups per unit
         const double t = (double)load * ((nst + sp - 1) / sp) * t_stage * (load == 1 ? 1.1 : 1.0) +
                          part * t_byte;
+        if (sp == 1)
+            t1 = t;
         if (best_t < 0 || t < best_t * (1 - 1e-9)) {
             best = sp;
             best_t = t;
         }
     }
+    // split only for a clear modelled gain (the model ignores the reduce's
+    // launch and its read of the partials' first split)
+    if (best > 1 && best_t > 0.9 * t1)
+        best = 1;
     if (forced > 0)  // profiling only
         best = std::min<int64_t>(forced, nst);
     *sps = (int)((nst + best - 1) / best);
@@ -350,6 +364,9 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     q.ws_fwd = align_up(q.weight_elems * 4, kWsAlign);  // the packed weights
 
     q.dense = false;
+    q.fwd_splits = q.dgrad_splits = 1;
+    q.fwd_sps = q.dgrad_sps = 0;
+    q.off_fwd_part = 0;
     if (q.dtype == CAFFE_BF16)
         return plan_bf16(&q);
 
@@ -387,9 +404,24 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
         return CAFFE_OK;
     }
 
+    // Split-K of the forward and data-gradient GEMMs for grids too small to
+    // fill the device (small batches, long reductions).
+    const int cus = device_cu_count();
+    plan_splits(q.Kg, q.N * q.Ho * q.Wo, q.R, q.fwd_tile, cus, env_tile("CAFFE_CONV_FWD_SPLITS"),
+                &q.fwd_splits, &q.fwd_sps, q.G);
+    plan_splits(q.Mt, (int)dcols, q.Rt, q.dgrad_tile, cus, env_tile("CAFFE_CONV_DGRAD_SPLITS"),
+                &q.dgrad_splits, &q.dgrad_sps, q.G);
+    const int64_t fpart = q.fwd_splits > 1 ? (int64_t)q.fwd_splits * q.top_elems * 4 : 0;
+    const int64_t dpart =
+        q.dgrad_splits > 1 ? (int64_t)q.dgrad_splits * q.G * q.Mt * dcols * 4 : 0;
+    if (fpart > kMaxTensorBytes || dpart > kMaxTensorBytes)
+        return fail(CAFFE_ERR_UNSUPPORTED, "split partials reach 2^31 bytes");
+    q.off_fwd_part = q.ws_fwd;
+    q.ws_fwd += align_up(fpart, kWsAlign);
+
     // Workspace: [masked top diff][bias partial sums][transformed weights]
-    // [weight partials].  The masked top diff is written only when relu is
-    // set and the caller has not masked top_diff already.
+    // [weight or data-gradient partials].  The masked top diff is written
+    // only when relu is set and the caller has not masked top_diff already.
     const size_t d_bytes = q.relu ? align_up(q.top_elems * 4, kWsAlign) : 0;
     const size_t sums_bytes =
         align_up((size_t)std::max<int64_t>(q.N, q.splits) * q.K * 4, kWsAlign);
@@ -398,9 +430,9 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     q.off_sums = d_bytes;
     q.off_wt = q.off_sums + sums_bytes;
     q.off_part = q.off_wt + wt_bytes;
-    q.ws_data = q.off_part;
+    q.ws_data = q.off_part + align_up(dpart, kWsAlign);
     q.ws_weights = q.off_part + align_up(part_bytes, kWsAlign);
-    q.ws_both = q.ws_weights;
+    q.ws_both = std::max(q.ws_data, q.ws_weights);
     return CAFFE_OK;
 }
 
@@ -474,6 +506,18 @@ int run_forward(const ConvPlan& q, const void* bottom, const void* weight, const
     p.Cout = q.K; p.OutH = q.Ho; p.OutW = q.Wo;
     p.blocked = q.blocked;
     p.xcd_order = q.xcd_order;
+    if (q.fwd_splits > 1) {
+        float* part = (float*)(ws + q.off_fwd_part);
+        ConvGemmParams pp = p;
+        pp.Y = part;
+        pp.Y_bytes = nbytes((int64_t)q.fwd_splits * q.top_elems, 4);
+        pp.splits = q.fwd_splits;
+        pp.stages_per_split = q.fwd_sps;
+        LAUNCH(launch_conv_gemm_f32(pp, 3, q.fwd_tile, q.fwd_tap, s), "forward launch");
+        LAUNCH(launch_conv_split_reduce_fwd(part, q.fwd_splits, p, top, s),
+               "forward reduce launch");
+        return CAFFE_OK;
+    }
     LAUNCH(launch_conv_gemm_f32(p, 0, q.fwd_tile, q.fwd_tap, s), "forward launch");
     return CAFFE_OK;
 }
@@ -526,6 +570,21 @@ int run_data(const ConvPlan& q, const float* dsrc, const float* bottom_mask, con
     p.Cg_out = q.Cg;
     p.blocked = q.blocked;
     p.xcd_order = q.xcd_order;
+    if (q.dgrad_splits > 1) {
+        float* part = (float*)(ws + q.off_part);
+        ConvGemmParams pp = p;
+        pp.Y = part;
+        pp.Y_bytes = nbytes((int64_t)q.dgrad_splits * q.G * q.Mt * p.Ncol, 4);
+        pp.Omask = nullptr;
+        pp.splits = q.dgrad_splits;
+        pp.stages_per_split = q.dgrad_sps;
+        LAUNCH(launch_conv_gemm_f32(pp, 3, q.dgrad_tile, q.dgrad_tap, s),
+               "data-gradient launch");
+        LAUNCH(launch_conv_split_reduce_dgrad(part, q.dgrad_splits, p, bottom_mask, bottom_diff,
+                                              s),
+               "data-gradient reduce launch");
+        return CAFFE_OK;
+    }
     LAUNCH(launch_conv_gemm_f32(p, 1, q.dgrad_tile, q.dgrad_tap, s), "data-gradient launch");
     return CAFFE_OK;
 }
@@ -879,7 +938,12 @@ int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, cons
     CHECK(check_conv_ptrs(q, bottom_diff, false, true, "bottom_diff"));
     CHECK(check_conv_ptrs(q, weight_diff, false, false, "weight_diff"));
     CHECK(check_conv_ptrs(q, bias_diff, false, false, "bias_diff"));
-    const size_t need = weight_diff ? q.ws_both : q.ws_data;
+    // the pass sizes of caffe_conv_workspace_size: both gradients, data only,
+    // weights (with or without the bias) only; the bias alone fits either
+    const size_t need = bottom_diff && weight_diff ? q.ws_both
+                        : bottom_diff              ? q.ws_data
+                        : weight_diff              ? q.ws_weights
+                                                   : std::min(q.ws_data, q.ws_weights);
     CHECK(check_ws(workspace, ws_bytes, need));
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;

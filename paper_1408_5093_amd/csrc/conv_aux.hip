@@ -291,6 +291,93 @@ hipError_t launch_split_reduce(const float* P, int splits, int count, int ncol, 
     return hipGetLastError();
 }
 
+// Split convolution GEMM epilogues: one thread per GEMM output (g, m, col),
+// col fastest (coalesced partial reads); the partials of an output are added
+// in split order after the bias.
+__global__ void __launch_bounds__(256)
+conv_split_reduce_fwd_kernel(const float* __restrict__ P, int splits, int G, int M, int Ncol,
+                             int OHW, int Cout, const float* __restrict__ bias, int relu,
+                             float* __restrict__ Y)
+{
+    const int64_t count = (int64_t)G * M * Ncol;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int col = (int)(e % Ncol);
+        const int gm = (int)(e / Ncol);            // g * M + m = output channel
+        float t = bias ? bias[gm] : 0.f;
+        for (int q = 0; q < splits; ++q)
+            t += P[(int64_t)q * count + e];
+        const int n = col / OHW;
+        const int pix = col - n * OHW;
+        Y[((int64_t)n * Cout + gm) * OHW + pix] = t > 0.f ? t : (relu ? 0.f : t);
+    }
+}
+
+__global__ void __launch_bounds__(256)
+conv_split_reduce_dgrad_kernel(const float* __restrict__ P, int splits, int G, int M, int Ncol,
+                               int OHW, int OW, int psh, int psw, int a0h, int a0w, int oph,
+                               int opw, int Cout, int Cg_out, int OutH, int OutW,
+                               const float* __restrict__ mask, float* __restrict__ dX)
+{
+    const int64_t count = (int64_t)G * M * Ncol;
+    const int pss = psh * psw;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int col = (int)(e % Ncol);
+        const int gm = (int)(e / Ncol);
+        const int g = gm / M;
+        const int m = gm - g * M;
+        const int c = m / pss;
+        const int fr = m - c * pss;
+        const int fh = fr / psw;
+        const int fw = fr - fh * psw;
+        const int n = col / OHW;
+        const int pix = col - n * OHW;
+        const int a = pix / OW;
+        const int b = pix - a * OW;
+        const int h = psh * (a + a0h) - oph + fh;
+        const int w = psw * (b + a0w) - opw + fw;
+        if ((unsigned)h >= (unsigned)OutH || (unsigned)w >= (unsigned)OutW)
+            continue;
+        float t = 0.f;
+        for (int q = 0; q < splits; ++q)
+            t += P[(int64_t)q * count + e];
+        const int64_t o = (((int64_t)n * Cout + g * Cg_out + c) * OutH + h) * OutW + w;
+        if (mask && !(mask[o] > 0.f))
+            t = 0.f;
+        dX[o] = t;
+    }
+}
+
+hipError_t launch_conv_split_reduce_fwd(const float* P, int splits, const ConvGemmParams& q,
+                                        float* Y, hipStream_t s)
+{
+    const int64_t count = (int64_t)q.G * q.M * q.Ncol;
+    if (count == 0)
+        return hipSuccess;
+    int64_t blocks = (count + 255) / 256;
+    if (blocks > 8192)
+        blocks = 8192;
+    hipLaunchKernelGGL(conv_split_reduce_fwd_kernel, dim3((unsigned)blocks), dim3(256), 0, s, P,
+                       splits, q.G, q.M, q.Ncol, q.OH * q.OW, q.Cout, q.bias, q.relu, Y);
+    return hipGetLastError();
+}
+
+hipError_t launch_conv_split_reduce_dgrad(const float* P, int splits, const ConvGemmParams& q,
+                                          const float* mask, float* dX, hipStream_t s)
+{
+    const int64_t count = (int64_t)q.G * q.M * q.Ncol;
+    if (count == 0)
+        return hipSuccess;
+    int64_t blocks = (count + 255) / 256;
+    if (blocks > 8192)
+        blocks = 8192;
+    hipLaunchKernelGGL(conv_split_reduce_dgrad_kernel, dim3((unsigned)blocks), dim3(256), 0, s, P,
+                       splits, q.G, q.M, q.Ncol, q.OH * q.OW, q.OW, q.psh, q.psw, q.a0h, q.a0w,
+                       q.oph, q.opw, q.Cout, q.Cg_out, q.OutH, q.OutW, mask, dX);
+    return hipGetLastError();
+}
+
 __global__ void __launch_bounds__(256) fill_zero_kernel(float* __restrict__ out, int64_t count)
 {
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count;

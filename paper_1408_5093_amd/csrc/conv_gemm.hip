@@ -119,9 +119,10 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     const int n_ct = (p.Ncol + TN - 1) / TN;
     const int per_xcd = gridDim.x >> 3;
     const int T = p.xcd_order ? (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3) : blockIdx.x;
-    // EPI 2 (dense split-K): the reduction is cut into p.splits ranges of
+    // EPI 2 (dense) and EPI 3 (gathered convolution operands) store split-K
+    // partials: the reduction is cut into p.splits ranges of
     // p.stages_per_split stages, the split index varying slowest
-    const int n_split = EPI == 2 ? p.splits : 1;
+    const int n_split = EPI >= 2 ? p.splits : 1;
     if (T >= n_mt * n_ct * p.G * n_split)
         return;
     const int mt = T % n_mt;
@@ -275,21 +276,35 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     }
 
     const int nst_all = (R + TK - 1) / TK;
-    const int s_begin = EPI == 2 ? split * p.stages_per_split : 0;
-    const int nst = EPI == 2 ? min(nst_all, s_begin + p.stages_per_split) : nst_all;
+    const int s_begin = EPI >= 2 ? split * p.stages_per_split : 0;
+    const int nst = EPI >= 2 ? min(nst_all, s_begin + p.stages_per_split) : nst_all;
     // blocked walk state: stage s covers tap (tu, tv) of channels tc .. tc + TK - 1.
     // It is updated in the loop body itself: captured by reference in a
     // lambda, it was kept in scratch memory, and the scratch accesses' waits
     // also stalled on the next stage's global loads.
     int tu = 0, tv = 0, tc = 0;
+    if constexpr (EPI == 3 && TAP) {
+        // the walk state of the split's first stage
+        if (p.blocked) {  // stage s: channels (s / khw) * TK.., tap s % khw
+            const int t = s_begin % khw;
+            tc = (s_begin / khw) * TK;
+            tu = t / kw;
+            tv = t - tu * kw;
+        } else {          // stage s: channels (s * TK) % Cin_g.., tap (s * TK) / Cin_g
+            const int t = (s_begin * TK) / Cin_g;
+            tc = s_begin * TK - t * Cin_g;
+            tu = t / kw;
+            tv = t - tu * kw;
+        }
+    }
 
     copy_a(As0, s_begin * TK);
     if constexpr (EPI == 2)
         copy_b_dense(Bs0, s_begin * TK);
     else if constexpr (TAP)
-        copy_b_tap(Bs0, 0, 0, 0);
+        copy_b_tap(Bs0, tu, tv, tc);
     else
-        copy_b_any(Bs0, 0);
+        copy_b_any(Bs0, s_begin * TK);
     __builtin_amdgcn_s_waitcnt(kVmcnt0);
     __syncthreads();
 
@@ -380,8 +395,8 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     // buffer, dropped by the hardware): short-circuit tests here become
     // divergent branches and make the compiler copy every accumulator out of
     // the AGPRs at once.
-    if constexpr (EPI == 2) {
-        // split partial P[split][m][col] (rows of the single group), lanes along col
+    if constexpr (EPI >= 2) {
+        // split partial P[split][g][m][col], lanes along col
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
@@ -393,7 +408,7 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
                 for (int q = 0; q < Op::kRegs; ++q) {
                     const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
                     const uint32_t off =
-                        ((uint32_t)((split * M + m) * p.Ncol + col) * 4u) | cbad |
+                        ((uint32_t)(((split * p.G + g) * M + m) * p.Ncol + col) * 4u) | cbad |
                         ((uint32_t)(m >= M) << 31);
                     buf_st_f32(acc[mi][ni][q], ry, off);
                 }
@@ -549,7 +564,7 @@ hipError_t launch_one(const ConvGemmParams& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * MT, TN = WN * NI * MT;
     const int64_t tiles = (int64_t)((p.Ncol + TN - 1) / TN) * ((p.M + TM - 1) / TM) * p.G *
-                          (EPI == 2 ? p.splits : 1);
+                          (EPI >= 2 ? p.splits : 1);
     const int64_t per_xcd = (tiles + 7) / 8;  // 8 XCDs; see the kernel's tile order
     hipLaunchKernelGGL(
         (conv_gemm_f32_kernel<MT, WM, WN, MI, NI, TK, KH, KW, SH, SW, EPI, TAP, MASK>),
@@ -569,7 +584,7 @@ hipError_t launch_geom(const ConvGemmParams& p, bool tap, hipStream_t s)
         }
         return launch_one<MT, WM, WN, MI, NI, TK, 0, 0, 0, 0, EPI, true, MASK>(p, s);
     }
-    if (EPI == 0 && p.kh == 11 && p.kw == 11 && p.sh == 4 && p.sw == 4)
+    if ((EPI == 0 || EPI == 3) && p.kh == 11 && p.kw == 11 && p.sh == 4 && p.sw == 4)
         return launch_one<MT, WM, WN, MI, NI, TK, 11, 11, 4, 4, EPI, false, MASK>(p, s);
     return launch_one<MT, WM, WN, MI, NI, TK, 0, 0, 0, 0, EPI, false, MASK>(p, s);
 }
@@ -887,6 +902,11 @@ hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool
         return hipErrorInvalidValue;
     if (epi == 0)
         return launch_tile<0, false>(p, tile, tap_major, s);
+    if (epi == 3) {
+        if (p.splits < 1 || p.stages_per_split < 1)
+            return hipErrorInvalidValue;
+        return launch_tile<3, false>(p, tile, tap_major, s);
+    }
     return p.Omask ? launch_tile<1, true>(p, tile, tap_major, s)
                    : launch_tile<1, false>(p, tile, tap_major, s);
 }

@@ -64,13 +64,25 @@ int device_cu_count();
 // out[c][r] = in[r][c] for an R x C row-major float matrix.
 hipError_t launch_transpose_f32(const float* in, float* out, int R, int C, hipStream_t s);
 
+// D = G [Y > 0] element by element.
+hipError_t launch_relu_mask(const float* G, const float* Y, float* D, int64_t count, hipStream_t s);
 // out[i] = act(sum_{s < splits} P[s*count + i] + bias[i % ncol]) in a fixed
 // order (bias may be null; act = ReLU when relu), stored as 0 where a non-null
 // mask is not > 0.
-// D = G [Y > 0] element by element.
-hipError_t launch_relu_mask(const float* G, const float* Y, float* D, int64_t count, hipStream_t s);
 hipError_t launch_split_reduce(const float* P, int splits, int count, int ncol, const float* bias,
                                int relu, const float* mask, float* out, hipStream_t s);
+// The epilogues of split convolution GEMMs, from the partials
+// P[split][g][m][col] (col = n * OHW + pix of the GEMM's output grid), each
+// output's partials added in split order:
+//   forward: Y[n][g*M + m][pix] = act(bias[g*M + m] + sum_s P[s][g][m][col])
+//   data gradient (phase-stacked rows m = (c, fh, fw)): dX[n][g*Cg_out + c]
+//   [psh (a + a0h) - oph + fh][psw (b + a0w) - opw + fw] = sum_s P[s][g][m][col]
+//   (pix = a * OW + b; positions outside the image are dropped), times
+//   [mask > 0] where mask is non-null.
+hipError_t launch_conv_split_reduce_fwd(const float* P, int splits, const ConvGemmParams& q,
+                                        float* Y, hipStream_t s);
+hipError_t launch_conv_split_reduce_dgrad(const float* P, int splits, const ConvGemmParams& q,
+                                          const float* mask, float* dX, hipStream_t s);
 
 // Split-K weight gradient:
 //   P[s][g*Kg + m][r] = sum_{col in split s} D[n][g*Kg + m][i][j] * X[n][g*Cg + c][i*sh - ph + u][j*sw - pw + v]
@@ -112,6 +124,10 @@ constexpr int kGemmMinTK = 16;
 // r = (c / TK, u, v, c % TK), TK = gemm_tile_k(tile), or tap-major
 // r = (u, v, c) (A packed to match, see launch_pack_weights); needs
 // Cin_g % TK == 0.  Otherwise r = (c, u, v).
+// epi 0: forward epilogue (bias, ReLU, NCHW store); epi 1: data-gradient
+// scatter (with p.Omask, the bottom mask); epi 3: the same gathered GEMM cut
+// into p.splits reduction ranges of p.stages_per_split stages, each storing
+// its partial P[split][g][m][col] to p.Y (see launch_conv_split_reduce_*).
 hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool tap_major,
                                 hipStream_t s);
 

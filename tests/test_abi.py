@@ -135,6 +135,17 @@ def test_workspace_sizes_bf16():
     assert cc.conv_workspace_size(d2, cc.PASS_FORWARD) >= 2 * 81 * 4 * 8 * 2
 
 
+def test_workspace_sizes_split_data_gradient():
+    # one image with a long reduction: the data gradient's split partials
+    # make its pass larger than the weight pass; PASS_BACKWARD covers both
+    d = cc.conv_desc((1, 64, 6, 6), (64, 64, 5, 5), 1, 2, 1, True)
+    data = cc.conv_workspace_size(d, cc.PASS_BACKWARD_DATA)
+    wts = cc.conv_workspace_size(d, cc.PASS_BACKWARD_WEIGHTS)
+    both = cc.conv_workspace_size(d, cc.PASS_BACKWARD)
+    assert both == max(data, wts)
+    assert cc.conv_workspace_size(d, cc.PASS_FORWARD) >= 64 * 64 * 25 * 4
+
+
 def test_workspace_sizes_inner_product():
     # a 1x1 convolution of a 1x1 image (one group, fp32) runs as dense GEMMs:
     # the forward holds split-K partials (and X^T, W^T when C % 4 != 0), the

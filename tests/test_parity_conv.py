@@ -201,3 +201,43 @@ def test_backward_flags_fused_relu():
     dx, dw, db = cc.conv_backward(_t(x), _t(w), _t(gmasked), None, 1, 1, 2, True, need=("db",),
                                   flags=cc.BACKWARD_TOP_DIFF_MASKED)
     assert_close(_np(db), db_ref, TOL_F32, "db only, masked")
+
+
+# ------------------------------------------------ split-K forward / data gradient
+SPLIT_CASES = [
+    (2, 32, 9, 9, 64, 3, 3, 1, 1, 1, 1, 1),       # reduction-blocked / tap-major walks
+    (1, 48, 11, 10, 96, 5, 5, 1, 1, 2, 2, 2),     # groups, 48 channels per group
+    (2, 3, 35, 35, 16, 11, 11, 4, 4, 0, 0, 1),    # conv1-like: 11x11/4, phase-stacked gradient
+    (3, 7, 19, 19, 150, 3, 3, 1, 1, 1, 1, 1),     # generic gather, 2 row tiles, ragged columns
+    (2, 9, 12, 12, 33, 5, 5, 2, 2, 2, 2, 3),      # stride-2 phases, 3 groups
+]
+
+
+@pytest.mark.parametrize("case", SPLIT_CASES)
+@pytest.mark.parametrize("splits", [2, 5])
+@pytest.mark.parametrize("blocked", ["1", "0"])
+def test_split_k(case, splits, blocked, monkeypatch):
+    """Forced split counts (profiling overrides) on both reduction orders:
+    each split starts its walk mid-reduction, the reduce applies the
+    epilogue."""
+    monkeypatch.setenv("CAFFE_CONV_FWD_SPLITS", str(splits))
+    monkeypatch.setenv("CAFFE_CONV_DGRAD_SPLITS", str(splits))
+    monkeypatch.setenv("CAFFE_CONV_BLOCKED", blocked)
+    run_case(*case, relu=True, bias=True)
+    run_case(*case, relu=False, bias=False, seed=1)
+
+
+def test_split_k_masked_bottom_and_default_plan(monkeypatch):
+    # the bottom mask applied by the data-gradient reduce; then a shape whose
+    # own plan splits (one image, a long reduction)
+    monkeypatch.setenv("CAFFE_CONV_DGRAD_SPLITS", "3")
+    rng = np.random.default_rng(31)
+    x = np.maximum(rng.standard_normal((2, 16, 10, 10)), 0).astype(np.float32)
+    w = rng.standard_normal((32, 16, 3, 3)).astype(np.float32)
+    g = rng.standard_normal((2, 32, 10, 10)).astype(np.float32)
+    dx_ref, _, _ = oracle.conv_backward(x, w, g, stride=1, pad=1, need=("dx",))
+    dx, _, _ = cc.conv_backward(_t(x), _t(w), _t(g), None, 1, 1, 1, False, need=("dx",),
+                                flags=cc.BACKWARD_MASK_BOTTOM_DIFF)
+    assert_close(_np(dx), dx_ref * (x > 0), TOL_F32, "masked data gradient")
+    monkeypatch.delenv("CAFFE_CONV_DGRAD_SPLITS")
+    run_case(1, 64, 6, 6, 64, 5, 5, 1, 1, 2, 2, 1, True)

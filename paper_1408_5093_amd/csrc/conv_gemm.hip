@@ -153,10 +153,12 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     // wave-uniform and go to the scalar offset; one lane offset serves all.)
     constexpr bool A_UNIFORM = TM % 64 == 0;
     uint32_t a_voff[A_UNIFORM ? 1 : NA];
+    int a_k[A_UNIFORM ? 1 : NA];  // the lane's k row within a stage, per copy
 #pragma unroll
     for (int q = 0; q < (A_UNIFORM ? 1 : NA); ++q) {
         const int flat = A_UNIFORM ? lane : 64 * (wave + NW * q) + lane;
         const int k = flat / TM;
+        a_k[q] = k;
         a_voff[q] = (uint32_t)((g * R + k) * M + m0 + flat - k * TM) * 4u;
     }
     const uint32_t a_row4 = (uint32_t)M * 4u;
@@ -177,10 +179,11 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     auto b_row = [&](int q) { return (wave + NW * q) / NC; };
 
     // Dense B (EPI 2): B[r][col] row-major with Ncol columns, the row offset
-    // in the scalar offset.  Rows past R (only when R % TK != 0) get the
-    // out-of-range bit in the lane offset and read 0.
+    // in the scalar offset.  Columns past Ncol, and rows past R (only when
+    // R % TK != 0), get the out-of-range offset alone in the lane offset and
+    // read 0.
     const uint32_t b_dvoff =
-        (uint32_t)(n0 + b_nc * 64 + lane) * 4u | (n0 + b_nc * 64 + lane < p.Ncol ? 0u : kOob);
+        n0 + b_nc * 64 + lane < p.Ncol ? (uint32_t)(n0 + b_nc * 64 + lane) * 4u : kOob;
     auto copy_b_dense = [&](BTile& dst, int kbase) {
 #pragma unroll
         for (int q = 0; q < NB; ++q) {
@@ -204,10 +207,15 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
                             rok ? (uint32_t)(kbase + k) * a_row4 + mo : 0u);
             } else if constexpr (TAP) {
                 copy_to_lds(ra, d, a_voff[q], (uint32_t)kbase * a_row4);
+            } else if (kbase + TK <= R) {  // a whole stage: no row past R
+                copy_to_lds(ra, d, a_voff[q], (uint32_t)kbase * a_row4);
             } else {
-                const int k = (64 * (wave + NW * q) + lane) / TM;
-                copy_to_lds(ra, d, kbase + k < R ? a_voff[q] : kOob,
-                            kbase + k < R ? (uint32_t)kbase * a_row4 : 0u);
+                // k varies across the wave: the scalar offset stays the
+                // stage's (wave-uniform) and a row past R gets the
+                // out-of-range offset alone, which the scalar offset cannot
+                // carry back into range
+                copy_to_lds(ra, d, kbase + a_k[q] < R ? a_voff[q] : kOob,
+                            (uint32_t)kbase * a_row4);
             }
         }
     };
@@ -219,8 +227,11 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     auto copy_b_tap = [&](BTile& dst, int u, int v, int c0) {
         const int ih = b_ih0 + u;
         const int iw = b_iw0 + v;
-        const bool ok = (unsigned)ih < (unsigned)IH && (unsigned)iw < (unsigned)IW;
-        const uint32_t voff = (ok ? (uint32_t)(b_base + u * IW + v) * 4u : kOob) | b_cbad;
+        // (a column past Ncol or a tap outside the image takes the
+        // out-of-range offset alone: with the channel's scalar offset added
+        // it stays out of range)
+        const bool ok = b_cbad == 0u && (unsigned)ih < (unsigned)IH && (unsigned)iw < (unsigned)IW;
+        const uint32_t voff = ok ? (uint32_t)(b_base + u * IW + v) * 4u : kOob;
 #pragma unroll
         for (int q = 0; q < NB; ++q)
             copy_to_lds(rx, &dst[b_row(q)][b_nc * 64], voff,
@@ -234,23 +245,55 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     const bool b_inside =
         b_ih0 >= 0 && b_ih0 + kh <= IH && b_iw0 >= 0 && b_iw0 + kw <= IW;
     const bool b_all_inside = __all(b_inside);
+    // A wave's copies of a stage take rows r0, r0 + STEP, r0 + 2 STEP, ...
+    // (STEP = NW / NC): (c, u, v) and the plane offset of r0 come from one
+    // division per stage, the later rows from a scalar walk (one tap at a
+    // time, carrying v into u and u into c).
+    constexpr int STEP = NW / NC;
+    static_assert(STEP * NC == NW, "B copy rows advance by a whole step");
     auto copy_b_any = [&](BTile& dst, int kbase) {
+        int r = kbase + b_row(0);
+        int c = r / khw;
+        int u = (r - c * khw) / kw;
+        int v = r - c * khw - u * kw;
+        int off = c * IHW + u * IW + v;
+        // (carries as 0/1 arithmetic: straight-line scalar code, no branch
+        // per row)
+        auto advance = [&]() {
 #pragma unroll
-        for (int q = 0; q < NB; ++q) {
-            const int r = kbase + b_row(q);
-            const int c = r / khw;
-            const int rr = r - c * khw;
-            const int u = rr / kw;
-            const int v = rr - u * kw;
-            uint32_t bad = (r < R ? 0u : kOob) | b_cbad;
-            if (!b_all_inside) {
+            for (int t = 0; t < STEP; ++t) {
+                ++r;
+                ++v;
+                ++off;
+                const int cv = v == kw;
+                v -= cv * kw;
+                u += cv;
+                off += cv * (IW - kw);
+                const int cu = u == kh;
+                u -= cu * kh;
+                off += cu * (IHW - kh * IW);
+            }
+        };
+        if (b_all_inside) {  // no tap leaves the image: no per-tap test
+#pragma unroll
+            for (int q = 0; q < NB; ++q) {
+                const uint32_t bad = (r < R ? 0u : kOob) | b_cbad;
+                copy_to_lds(rx, &dst[b_row(q)][b_nc * 64], ((uint32_t)(b_base + off) * 4u) | bad,
+                            0u);
+                advance();
+            }
+        } else {
+#pragma unroll
+            for (int q = 0; q < NB; ++q) {
                 const int ih = b_ih0 + u;
                 const int iw = b_iw0 + v;
-                bad |= ((uint32_t)((unsigned)ih >= (unsigned)IH) |
-                        (uint32_t)((unsigned)iw >= (unsigned)IW)) << 31;
+                const uint32_t bad = (r < R ? 0u : kOob) | b_cbad |
+                                     (((uint32_t)((unsigned)ih >= (unsigned)IH) |
+                                       (uint32_t)((unsigned)iw >= (unsigned)IW)) << 31);
+                copy_to_lds(rx, &dst[b_row(q)][b_nc * 64], ((uint32_t)(b_base + off) * 4u) | bad,
+                            0u);
+                advance();
             }
-            copy_to_lds(rx, &dst[b_row(q)][b_nc * 64],
-                        ((uint32_t)(b_base + c * IHW + u * IW + v) * 4u) | bad, 0u);
         }
     };
 

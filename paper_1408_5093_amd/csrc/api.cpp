@@ -10,6 +10,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdint>
 
 #include "../../include/caffe_conv.h"
 #include "../../include/caffe_layers.h"
@@ -66,6 +67,11 @@ struct ConvPlan {
     // padded to a multiple of 8 (Cgp, Kgp); padded reduction lengths of the
     // forward (Rp) and data-gradient (Rtp) GEMMs; weight-gradient columns Rw
     int Cgp, Kgp, Rp, Rtp, Rw;
+    // zero-bordered bf16 staging: the input on an XHp x XWp grid (real pixels
+    // at (ph, pw)), the top gradient on a DHp x DWp grid (real pixels at
+    // (dtb, dlb)); the data-gradient gather reads the latter from (doh0, dow0)
+    int XHp, XWp, DHp, DWp, dtb, dlb, doh0, dow0;
+    int fwd_pipe, dgrad_pipe;       // bf16 GEMM pipelines (Bf16Pipe)
     size_t off_xh_fwd, off_wp_fwd;  // forward: [Xh][Wp]
     size_t off_dh, off_xh;          // backward: [Dh][Xh][sums][Wt][partials]
     // inner-product shape (1x1 kernel on 1x1 spatial, one group, fp32): dense
@@ -197,6 +203,37 @@ int env_tile(const char* name)
 
 int round_up(int x, int a) { return (x + a - 1) / a * a; }
 
+// bf16 GEMM pipeline for a tile: three LDS buffers (copies two stages ahead)
+// unless double buffering lets two workgroups share a compute unit's LDS
+// (measured on the CaffeNet layers: the 48-row data-gradient tiles gain more
+// from the second workgroup than from the deeper pipeline; the 96- and
+// 128-row tiles, one workgroup per unit either way, gain from the depth).
+int pick_bf16_pipe(int tile)
+{
+    const int bytes2 = (bf16_tile_m(tile) + 256) * kBf16TK * 2 * 2;
+    return 2 * bytes2 <= 160 * 1024 ? BPIPE_2 : BPIPE_3;
+}
+
+// bf16 GEMM tile for M rows: the least row padding, ties to the earlier of
+// 128, 96, 64, 48 rows.
+int pick_bf16_tile(int M, int forced)
+{
+    if (forced >= 0 && forced < BTILE_COUNT)
+        return forced;
+    static const int order[] = {BTILE_128x256, BTILE_96x256, BTILE_64x256, BTILE_48x256};
+    int best = order[0];
+    int64_t best_rows = INT64_MAX;
+    for (int t : order) {
+        const int tm = bf16_tile_m(t);
+        const int64_t rows = (int64_t)(M + tm - 1) / tm * tm;
+        if (rows < best_rows) {
+            best = t;
+            best_rows = rows;
+        }
+    }
+    return best;
+}
+
 // The bf16-operand plan: staging sizes, padded reductions, the weight-gradient
 // split and the workspace layout.  Called by plan_conv once the common fields
 // are set.
@@ -206,8 +243,21 @@ int plan_bf16(ConvPlan* p)
     q.Cgp = round_up(q.Cg, 8);
     q.Kgp = round_up(q.Kg, 8);
     const int khw = q.kh * q.kw;
-    const int64_t xh = (int64_t)q.N * q.H * q.W * q.G * q.Cgp * 2;
-    const int64_t dh = (int64_t)q.N * q.Ho * q.Wo * q.G * q.Kgp * 2;
+    // The staged copies carry the gathers' zero padding as a border: the
+    // input's covers every forward tap, the top gradient's every tap of the
+    // phase-stacked data-gradient gather (whose padding Th - 1 - a0h may be
+    // negative: then the gather starts doh0 rows into the grid instead).
+    q.XHp = std::max(q.ph + q.H, (q.Ho - 1) * q.sh + q.kh);
+    q.XWp = std::max(q.pw + q.W, (q.Wo - 1) * q.sw + q.kw);
+    const int php = q.Th - 1 - q.a0h, pwp = q.Tw - 1 - q.a0w;
+    q.dtb = std::max(php, 0);
+    q.dlb = std::max(pwp, 0);
+    q.doh0 = q.dtb - php;
+    q.dow0 = q.dlb - pwp;
+    q.DHp = std::max(q.dtb + q.Ho, q.Ah + q.Th - 1 + q.doh0);
+    q.DWp = std::max(q.dlb + q.Wo, q.Aw + q.Tw - 1 + q.dow0);
+    const int64_t xh = (int64_t)q.N * q.XHp * q.XWp * q.G * q.Cgp * 2;
+    const int64_t dh = (int64_t)q.N * q.DHp * q.DWp * q.G * q.Kgp * 2;
     const int64_t rp = ((int64_t)khw * q.Cgp + kBf16TK - 1) / kBf16TK * kBf16TK;
     const int64_t rtp = ((int64_t)q.Th * q.Tw * q.Kgp + kBf16TK - 1) / kBf16TK * kBf16TK;
     const int64_t rw = (int64_t)khw * q.Cgp;
@@ -242,8 +292,11 @@ int plan_bf16(ConvPlan* p)
     if (part_bytes > kMaxTensorBytes)
         return fail(CAFFE_ERR_UNSUPPORTED, "weight-gradient partials reach 2^31 bytes");
 
-    q.fwd_tile = pick_tile(q.Kg, true, env_tile("CAFFE_CONV_FWD_TILE"));
-    q.dgrad_tile = pick_tile(q.Mt, false, env_tile("CAFFE_CONV_DGRAD_TILE"));
+    q.fwd_tile = pick_bf16_tile(q.Kg, env_tile("CAFFE_BF16_FWD_TILE"));
+    q.dgrad_tile = pick_bf16_tile(q.Mt, env_tile("CAFFE_BF16_DGRAD_TILE"));
+    const int pipe = env_tile("CAFFE_BF16_PIPE");
+    q.fwd_pipe = pipe >= 0 && pipe < BPIPE_COUNT ? pipe : pick_bf16_pipe(q.fwd_tile);
+    q.dgrad_pipe = pipe >= 0 && pipe < BPIPE_COUNT ? pipe : pick_bf16_pipe(q.dgrad_tile);
     q.xcd_order = env_tile("CAFFE_CONV_XCD_ORDER") != 0;
 
     q.off_xh_fwd = 0;
@@ -251,7 +304,7 @@ int plan_bf16(ConvPlan* p)
     q.ws_fwd = q.off_wp_fwd + align_up(wp, kWsAlign);
     // bias-gradient partials of the top-gradient staging (and room for the
     // per-image sums of the bias-only pass)
-    const int64_t terms = std::max<int64_t>(diff_prep_terms(q.N, q.Ho * q.Wo), q.N);
+    const int64_t terms = std::max<int64_t>(diff_prep_terms(q.N, q.DHp * q.DWp), q.N);
     const size_t sums_bytes = align_up((size_t)terms * q.K * 4, kWsAlign);
     if ((int64_t)sums_bytes > kMaxTensorBytes)
         return fail(CAFFE_ERR_UNSUPPORTED, "bias partials reach 2^31 bytes");
@@ -734,8 +787,8 @@ int run_forward_bf16(const ConvPlan& q, const void* bottom, const void* weight, 
     uint16_t* xh = (uint16_t*)(ws + q.off_xh_fwd);
     uint16_t* wp = (uint16_t*)(ws + q.off_wp_fwd);
     const int Ctot = q.G * q.Cgp;
-    LAUNCH(launch_nhwc_from_nchw_bf16((const uint16_t*)bottom, xh, q.N, q.C, q.H * q.W, q.Cg,
-                                      q.Cgp, Ctot, s),
+    LAUNCH(launch_stage_nhwc_bf16((const uint16_t*)bottom, xh, q.N, q.C, q.H, q.W, q.Cg, q.Cgp,
+                                  Ctot, q.XHp, q.XWp, q.ph, q.pw, s),
            "bf16 staging launch");
     LAUNCH(launch_pack_weights_bf16((const uint16_t*)weight, wp, q.K, q.Cg, q.Cgp, q.kh * q.kw,
                                     q.Rp, s),
@@ -746,17 +799,19 @@ int run_forward_bf16(const ConvPlan& q, const void* bottom, const void* weight, 
     p.Y = top;
     p.bias = bias;
     p.A_bytes = nbytes((int64_t)q.K * q.Rp, 2);
-    p.X_bytes = nbytes((int64_t)q.N * q.H * q.W * Ctot, 2);
+    p.X_bytes = nbytes((int64_t)q.N * q.XHp * q.XWp * Ctot, 2);
     p.Y_bytes = nbytes(q.top_elems, 4);
-    p.N = q.N; p.IH = q.H; p.IW = q.W; p.Ctot = Ctot; p.Cgp = q.Cgp;
-    p.kh = q.kh; p.kw = q.kw; p.sh = q.sh; p.sw = q.sw; p.ph = q.ph; p.pw = q.pw;
+    p.N = q.N; p.IHp = q.XHp; p.IWp = q.XWp; p.Ctot = Ctot; p.Cgp = q.Cgp;
+    p.Cg8 = q.Cgp / 8; p.KC = q.kh * q.kw * p.Cg8;
+    p.div_cg8 = make_fastdiv((uint32_t)p.Cg8); p.div_kw = make_fastdiv((uint32_t)q.kw);
+    p.kh = q.kh; p.kw = q.kw; p.sh = q.sh; p.sw = q.sw; p.oh0 = 0; p.ow0 = 0;
     p.OH = q.Ho; p.OW = q.Wo;
     p.M = q.Kg; p.Rp = q.Rp; p.G = q.G;
     p.Ncol = q.N * q.Ho * q.Wo;
     p.relu = q.relu;
     p.Cout = q.K; p.OutH = q.Ho; p.OutW = q.Wo;
     p.xcd_order = q.xcd_order;
-    LAUNCH(launch_conv_gemm_bf16(p, 0, q.fwd_tile, s), "bf16 forward launch");
+    LAUNCH(launch_conv_gemm_bf16(p, 0, q.fwd_tile, q.fwd_pipe, s), "bf16 forward launch");
     return CAFFE_OK;
 }
 
@@ -776,11 +831,12 @@ int run_data_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom_mask
     p.Omask = (const uint16_t*)bottom_mask;
     p.Y = bottom_diff;
     p.A_bytes = nbytes((int64_t)q.G * q.Mt * q.Rtp, 2);
-    p.X_bytes = nbytes((int64_t)q.N * q.Ho * q.Wo * Ktot, 2);
+    p.X_bytes = nbytes((int64_t)q.N * q.DHp * q.DWp * Ktot, 2);
     p.Y_bytes = nbytes(q.bottom_elems, 4);
-    p.N = q.N; p.IH = q.Ho; p.IW = q.Wo; p.Ctot = Ktot; p.Cgp = q.Kgp;
-    p.kh = q.Th; p.kw = q.Tw; p.sh = 1; p.sw = 1;
-    p.ph = q.Th - 1 - q.a0h; p.pw = q.Tw - 1 - q.a0w;
+    p.N = q.N; p.IHp = q.DHp; p.IWp = q.DWp; p.Ctot = Ktot; p.Cgp = q.Kgp;
+    p.Cg8 = q.Kgp / 8; p.KC = q.Th * q.Tw * p.Cg8;
+    p.div_cg8 = make_fastdiv((uint32_t)p.Cg8); p.div_kw = make_fastdiv((uint32_t)q.Tw);
+    p.kh = q.Th; p.kw = q.Tw; p.sh = 1; p.sw = 1; p.oh0 = q.doh0; p.ow0 = q.dow0;
     p.OH = q.Ah; p.OW = q.Aw;
     p.M = q.Mt; p.Rp = q.Rtp; p.G = q.G;
     p.Ncol = q.N * q.Ah * q.Aw;
@@ -788,7 +844,8 @@ int run_data_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom_mask
     p.psh = q.sh; p.psw = q.sw; p.a0h = q.a0h; p.a0w = q.a0w; p.oph = q.ph; p.opw = q.pw;
     p.Cg_out = q.Cg;
     p.xcd_order = q.xcd_order;
-    LAUNCH(launch_conv_gemm_bf16(p, 1, q.dgrad_tile, s), "bf16 data-gradient launch");
+    LAUNCH(launch_conv_gemm_bf16(p, 1, q.dgrad_tile, q.dgrad_pipe, s),
+           "bf16 data-gradient launch");
     return CAFFE_OK;
 }
 
@@ -798,19 +855,20 @@ int run_weights_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom,
     uint16_t* xh = (uint16_t*)(ws + q.off_xh);
     float* part = (float*)(ws + q.off_part);
     const int Ctot = q.G * q.Cgp;
-    LAUNCH(launch_nhwc_from_nchw_bf16((const uint16_t*)bottom, xh, q.N, q.C, q.H * q.W, q.Cg,
-                                      q.Cgp, Ctot, s),
+    LAUNCH(launch_stage_nhwc_bf16((const uint16_t*)bottom, xh, q.N, q.C, q.H, q.W, q.Cg, q.Cgp,
+                                  Ctot, q.XHp, q.XWp, q.ph, q.pw, s),
            "bf16 staging launch");
     WgradBf16Params p = {};
     p.D = dh;
     p.X = xh;
     p.P = part;
-    p.D_bytes = nbytes((int64_t)q.N * q.Ho * q.Wo * q.G * q.Kgp, 2);
-    p.X_bytes = nbytes((int64_t)q.N * q.H * q.W * Ctot, 2);
+    p.D_bytes = nbytes((int64_t)q.N * q.DHp * q.DWp * q.G * q.Kgp, 2);
+    p.X_bytes = nbytes((int64_t)q.N * q.XHp * q.XWp * Ctot, 2);
     p.P_bytes = nbytes((int64_t)q.splits * q.K * q.Rw, 4);
-    p.N = q.N; p.IH = q.H; p.IW = q.W; p.Ctot = Ctot; p.Cgp = q.Cgp;
+    p.N = q.N; p.IHp = q.XHp; p.IWp = q.XWp; p.Ctot = Ctot; p.Cgp = q.Cgp;
     p.K = q.K; p.Kg = q.Kg; p.Kgp = q.Kgp; p.Ktot = q.G * q.Kgp;
-    p.kh = q.kh; p.kw = q.kw; p.sh = q.sh; p.sw = q.sw; p.ph = q.ph; p.pw = q.pw;
+    p.DHp = q.DHp; p.DWp = q.DWp; p.dtb = q.dtb; p.dlb = q.dlb;
+    p.kh = q.kh; p.kw = q.kw; p.sh = q.sh; p.sw = q.sw;
     p.OH = q.Ho; p.OW = q.Wo;
     p.Rw = q.Rw; p.G = q.G;
     p.Ncol = q.N * q.Ho * q.Wo;
@@ -838,15 +896,16 @@ int backward_bf16(const ConvPlan& q, const float* top_diff, const float* top, bo
     float* sums = (float*)(ws + q.off_sums);
     // D = bf16(top_diff [top > 0]) staged channel-contiguous; the fp32 plane
     // sums give the bias gradient
-    LAUNCH(launch_diff_prep_bf16(top_diff, top, dh, bias_diff ? sums : nullptr, q.N, q.K,
-                                 q.Ho * q.Wo, q.Kg, q.Kgp, q.G * q.Kgp, q.relu && !masked, s),
+    LAUNCH(launch_diff_prep_bf16(top_diff, top, dh, bias_diff ? sums : nullptr, q.N, q.K, q.Ho,
+                                 q.Wo, q.Kg, q.Kgp, q.G * q.Kgp, q.DHp, q.DWp, q.dtb, q.dlb,
+                                 q.relu && !masked, s),
            "bf16 top-gradient staging launch");
     if (bottom_diff)
         CHECK(run_data_bf16(q, dh, mask_bottom ? bottom : nullptr, weight, bottom_diff, ws, s));
     if (weight_diff)
         CHECK(run_weights_bf16(q, dh, bottom, weight_diff, accumulate, ws, s));
     if (bias_diff)
-        LAUNCH(launch_bias_reduce(sums, bias_diff, diff_prep_terms(q.N, q.Ho * q.Wo), q.K,
+        LAUNCH(launch_bias_reduce(sums, bias_diff, diff_prep_terms(q.N, q.DHp * q.DWp), q.K,
                                   accumulate, s),
                "bias reduce launch");
     return CAFFE_OK;

@@ -69,29 +69,89 @@ struct MfmaBf16<16> {
 };
 
 // ------------------------------------------------------------ forward / dgrad
-template <int MT, int WM, int WN, int MI, int NI, int TK, int EPI, bool MASK>
-__global__ void __launch_bounds__(64 * WM * WN)
+// Both operands are copied global -> LDS by 16-byte DMA in 64-deep stages:
+// each operand row contributes 8 chunks of 8 bf16 (128 bytes, one cache line
+// when aligned) per stage.  One wave copy moves 8 rows: lane l takes row
+// l / 8 and lands at slot l % 8 of that row's 128 bytes, the row's chunks
+// in order along the lanes (the address unit then handles whole lines; a
+// copy whose lanes step across rows runs at a quarter of the rate).  Inside
+// a row, chunk c sits at slot c ^ chunk_swz(row), so that the fragment reads
+// (one chunk of consecutive rows across the lanes) hit distinct banks
+// whether the LDS serves 8 or 16 lanes of 16 bytes per cycle.
+//
+// A rows are contiguous in global memory.  A B row is one output column:
+// its chunk kc sits at tap (u, v) = (kc / Cg8 / kw, kc / Cg8 % kw), channels
+// 8*(kc % Cg8) .. +7, at a byte offset from the column's pixel that does not
+// depend on the column, so each lane walks its one chunk index per stage and
+// adds the offset to the pixel base of each of its columns.  Past the last
+// chunk the offset is out of range (the copy lands zeros).  Columns past
+// Ncol re-read the last column; their results are never stored.
+__device__ __forceinline__ void copy16_lds(__amdgpu_buffer_rsrc_t r, u32x4* dst, uint32_t voff,
+                                           uint32_t soff)
+{
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, voff, soff, 0, 0);
+}
+
+// Slot permutation of the 8 chunks of tile row r (bits 0..3 of r only).
+__device__ __forceinline__ int chunk_swz(int r)
+{
+    return (r & 6) | ((r ^ (r >> 3)) & 1);
+}
+
+// Workgroup barrier between pipeline stages.  Each wave has already waited
+// (vmcnt) for its own copies of the stage it is about to read, and its reads
+// of the buffer the next copies overwrite were consumed by MFMAs before it
+// arrives; __syncthreads would in addition wait for every copy still in
+// flight (its release fence covers LDS DMA), serialising a deeper pipeline.
+// The empty asm statements keep the compiler from moving LDS accesses across.
+__device__ __forceinline__ void stage_barrier()
+{
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// s_waitcnt vmcnt(n), expcnt and lgkmcnt left at their maxima.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | (((N >> 4) & 3) << 14));
+}
+
+// Workgroups of the bf16 GEMM that fit one compute unit's LDS at once: the
+// register budget follows (one workgroup of 4 waves = one wave per SIMD may
+// use the whole register file).
+constexpr int bf16_gemm_blocks_per_cu(int tm, int tn, int ns)
+{
+    return (160 * 1024) / ((tm + tn) * kBf16TK * 2 * ns);
+}
+
+template <int MT, int WM, int WN, int MI, int NI, int NS, int EPI, bool MASK>
+__global__ void __launch_bounds__(64 * WM * WN,
+                                  bf16_gemm_blocks_per_cu(WM * MI * MT, WN * NI * MT, NS))
 conv_gemm_bf16_kernel(const GemmBf16Params p)
 {
     typedef MfmaBf16<MT> Op;
-    constexpr int NT = 64 * WM * WN;
+    constexpr int NW = WM * WN;
     constexpr int TM = WM * MI * MT;
     constexpr int TN = WN * NI * MT;
-    constexpr int TB = TK / 8;       // 16-byte chunks of a row per stage
-    constexpr int LD = TK + 8;       // LDS row length: 16 bytes of padding
-    constexpr int CA = TM * TB;      // A chunks per stage
-    constexpr int EA = (CA + NT - 1) / NT;
-    static_assert(TN <= NT && NT % TN == 0, "B mapping: a thread owns one column");
-    constexpr int BS = NT / TN;      // B chunk slots covered by one pass of the block
-    static_assert(TB % BS == 0, "B mapping");
-    constexpr int EB = TB / BS;      // B chunks per thread per stage
-    constexpr int KS = TK / Op::kK;
-    static_assert(TK % Op::kK == 0, "stage depth");
+    constexpr int TK = kBf16TK;       // reduction depth of a stage
+    constexpr int CH = TK / 8;        // chunks per row per stage
+    constexpr int RPI = 64 / CH;      // rows per wave copy
+    constexpr int IA = TM / RPI;      // A copies per stage
+    constexpr int NA = (IA + NW - 1) / NW;
+    constexpr int NB = TN / RPI / NW; // B copies per wave per stage
+    constexpr int KL = 64 / MT;       // lane groups along k of one instruction
+    constexpr int KS = TK / Op::kK;   // instructions along k per stage
+    static_assert(CH == 8 && NW % 2 == 0, "copy mapping: 8-chunk rows, swizzle by wave parity");
+    static_assert(TM % RPI == 0 && TN % (RPI * NW) == 0 && MT % 16 == 0, "copy mapping");
+    static_assert(Op::kK == 8 * KL && TK % Op::kK == 0, "stage depth");
+    static_assert(NS == 2 || NS == 3, "buffers");
 
-    __shared__ __attribute__((aligned(16))) bf16_t As[2][TM][LD];
-    __shared__ __attribute__((aligned(16))) bf16_t Bs[2][TN][LD];
+    __shared__ u32x4 A0[TM * CH], A1[TM * CH], A2[NS > 2 ? TM * CH : 1];
+    __shared__ u32x4 B0[TN * CH], B1[TN * CH], B2[NS > 2 ? TN * CH : 1];
 
-    const int kh = p.kh, kw = p.kw;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -109,90 +169,77 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
     const int g = T / (n_mt * n_ct);
     const int m0 = mt * TM;
     const int n0 = ct * TN;
-    const int M = p.M, Rp = p.Rp;
-    const int IH = p.IH, IW = p.IW, Ctot = p.Ctot;
+    const int M = p.M;
     const int OHW = p.OH * p.OW;
-    const int Cg8 = p.Cgp >> 3;
 
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.A, p.A_bytes);
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, p.X_bytes);
 
-    // ---- B: one output column per thread; its chunk slots are wave-uniform
-    const int bcl = tid % TN;
-    const int slot0 = __builtin_amdgcn_readfirstlane(tid / TN);
-    int b_ih0, b_iw0, b_base;
-    uint32_t b_cbad;
-    {
-        const int col = n0 + bcl;
+    // copy i (= wave + NW*q) moves tile rows 8i .. 8i + 7; bit 3 of the row,
+    // the only one of i in chunk_swz, is the wave's parity
+    const int cr = lane >> 3;
+    const int ck = (lane & 7) ^ chunk_swz(8 * wave + cr);  // this lane's chunk
+    uint32_t a_voff[NA];
+#pragma unroll
+    for (int q = 0; q < NA; ++q) {
+        const int row = m0 + RPI * (wave + NW * q) + cr;
+        a_voff[q] = row < M ? ((uint32_t)((g * M + row) * p.Rp) + 8u * ck) * 2u : kOob;
+    }
+    uint32_t b_pix[NB];
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+        const int col = min(n0 + RPI * (wave + NW * q) + cr, p.Ncol - 1);
         const int n = col / OHW;
         const int pix = col - n * OHW;
         const int i = pix / p.OW;
         const int j = pix - i * p.OW;
-        b_ih0 = i * p.sh - p.ph;
-        b_iw0 = j * p.sw - p.pw;
-        b_base = ((n * IH + b_ih0) * IW + b_iw0) * Ctot + g * p.Cgp;
-        b_cbad = (uint32_t)(col >= p.Ncol) << 31;
+        b_pix[q] = (uint32_t)(((n * p.IHp + i * p.sh + p.oh0) * p.IWp + j * p.sw + p.ow0) *
+                                  p.Ctot + g * p.Cgp) * 2u;
     }
-    // Reduction walk of each slot: chunk kc = s*TB + slot0 + BS*q sits at tap
-    // (wu, wv), channels 8*wc .. 8*wc + 7.  Scalar state, advanced by TB
-    // chunks per stage.
-    int wu[EB], wv[EB], wc[EB];
+    // byte offset of this lane's chunk of stage t from a column's pixel
+    auto b_delta = [&](int t) -> uint32_t {
+        const int kc = t * CH + ck;
+        const int tap = (int)fdiv((uint32_t)kc, p.div_cg8);
+        const int c8 = kc - tap * p.Cg8;
+        const int u = (int)fdiv((uint32_t)tap, p.div_kw);
+        const int v = tap - u * p.kw;
+        const uint32_t d = (uint32_t)((u * p.IWp + v) * p.Ctot + 8 * c8) * 2u;
+        return kc < p.KC ? d : kOob;
+    };
+    // The copies of one stage, NA + NB per wave, go out in KS parts, one
+    // after each step of MFMAs: issued all at once they back up in the
+    // address unit and stall the wave before its first MFMA.
+    constexpr int NC = NA + NB;
+    constexpr int CPP = (NC + KS - 1) / KS;  // copies per part
+    auto issue_part = [&](int t, u32x4* As, u32x4* Bs, int part, uint32_t d) {
+        const uint32_t soff = (uint32_t)(t * TK) * 2u;
 #pragma unroll
-    for (int q = 0; q < EB; ++q) {
-        const int kc = slot0 + BS * q;
-        const int t = kc / Cg8;
-        wc[q] = kc - t * Cg8;
-        wu[q] = t / kw;
-        wv[q] = t - wu[q] * kw;
-    }
-    auto advance = [&]() {
-#pragma unroll
-        for (int q = 0; q < EB; ++q) {
-            wc[q] += TB;
-            while (wc[q] >= Cg8) {
-                wc[q] -= Cg8;
-                if (++wv[q] == kw) {
-                    wv[q] = 0;
-                    ++wu[q];
-                }
+        for (int c = part * CPP; c < (part + 1) * CPP && c < NC; ++c) {
+            if (c < NA) {
+                if (IA % NW == 0 || wave + NW * c < IA)
+                    copy16_lds(ra, &As[(wave + NW * c) * 64], a_voff[c], soff);
+            } else {
+                copy16_lds(rx, &Bs[(wave + NW * (c - NA)) * 64], b_pix[c - NA] + d, 0u);
             }
         }
     };
-
-    u32x4 rA[EA], rB[EB];
-    auto load_a = [&](int kbase) {
+    auto issue = [&](int t, u32x4* As, u32x4* Bs) {
+        const uint32_t d = b_delta(t);
 #pragma unroll
-        for (int q = 0; q < EA; ++q) {
-            const int id = tid + NT * q;
-            const int row = id / TB;
-            const int kc = id % TB;
-            const uint32_t bad = ((uint32_t)(id >= CA) | (uint32_t)(m0 + row >= M)) << 31;
-            rA[q] = buf_ld_b128(ra, ((uint32_t)((g * M + m0 + row) * Rp + kbase + kc * 8) * 2u) |
-                                        bad);
-        }
+        for (int part = 0; part < KS; ++part)
+            issue_part(t, As, Bs, part, d);
     };
-    auto load_b = [&]() {
-#pragma unroll
-        for (int q = 0; q < EB; ++q) {
-            const int delta = (wu[q] * IW + wv[q]) * Ctot + wc[q] * 8;
-            const int ih = b_ih0 + wu[q];
-            const int iw = b_iw0 + wv[q];
-            const uint32_t bad = ((uint32_t)(wu[q] >= kh) |
-                                  (uint32_t)((unsigned)ih >= (unsigned)IH) |
-                                  (uint32_t)((unsigned)iw >= (unsigned)IW)) << 31;
-            rB[q] = buf_ld_b128(rx, ((uint32_t)(b_base + delta) * 2u) | bad | b_cbad);
+    // this wave's copies of one stage (the vmcnt still allowed while the
+    // next stage's copies are in flight)
+    auto wait_all_but_next = [&]() {
+        if constexpr (IA % NW == 0) {
+            wait_vmcnt<NA + NB>();
+        } else {
+            if (wave < IA % NW)
+                wait_vmcnt<NA + NB>();
+            else
+                wait_vmcnt<NA - 1 + NB>();
         }
-    };
-    auto store_stage = [&](int buf) {
-#pragma unroll
-        for (int q = 0; q < EA; ++q) {
-            const int id = tid + NT * q;
-            if (CA % NT == 0 || id < CA)
-                *(u32x4*)&As[buf][id / TB][(id % TB) * 8] = rA[q];
-        }
-#pragma unroll
-        for (int q = 0; q < EB; ++q)
-            *(u32x4*)&Bs[buf][bcl][(slot0 + BS * q) * 8] = rB[q];
     };
 
     // forward: accumulators start at the bias of their row
@@ -214,51 +261,87 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
             acc[mi][ni] = init;
     }
 
-    const int nst = Rp / TK;
-    load_a(0);
-    load_b();
-    store_stage(0);
-    __syncthreads();
-
-    const int arow = wm * MI * MT + lane % MT;
-    const int brow = wn * NI * MT + lane % MT;
-    const int kl = (lane / MT) * 8;
-
-    for (int s = 0; s < nst; ++s) {
-        const int cur = s & 1;
-        if (s + 1 < nst) {
-            load_a((s + 1) * TK);
-            advance();
-            load_b();
-        }
-        constexpr int PF = KS > 1 ? 1 : 0;
-        bf16x8 fa[PF + 1][MI], fb[PF + 1][NI];
-        auto read_frag = [&](int ks, int slot) {
-#pragma unroll
-            for (int mi = 0; mi < MI; ++mi)
-                fa[slot][mi] = lds_frag(&As[cur][arow + mi * MT][ks * Op::kK + kl]);
-#pragma unroll
-            for (int ni = 0; ni < NI; ++ni)
-                fb[slot][ni] = lds_frag(&Bs[cur][brow + ni * MT][ks * Op::kK + kl]);
-        };
-        read_frag(0, 0);
+    // fragment slots: tile row R = base + mi*MT + lane % MT, chunk
+    // c = ks*KL + lane / MT at slot (R / 8)*64 + (R % 8)*8 + (c ^ chunk_swz(R));
+    // chunk_swz(R) and (R % 8) do not change with mi (MT % 16 == 0) and
+    // ks*KL only sets bits above lane / MT
+    int fa[KS], fb[KS];
+    {
+        const int ra0 = wm * MI * MT + lane % MT;
+        const int rb0 = wn * NI * MT + lane % MT;
+        const int ea = (lane / MT) ^ chunk_swz(ra0);
+        const int eb = (lane / MT) ^ chunk_swz(rb0);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            if (ks + PF < KS && PF > 0)
-                read_frag(ks + PF, (ks + PF) % (PF + 1));
+            fa[ks] = (ra0 >> 3) * 64 + (ra0 & 7) * 8 + (ea ^ (ks * KL));
+            fb[ks] = (rb0 >> 3) * 64 + (rb0 & 7) * 8 + (eb ^ (ks * KL));
+        }
+    }
+    constexpr int FSTR = (MT / 8) * 64;  // next MT-row block
+
+    // fragments of step ks + 1 are read while the instructions of step ks
+    // run; after(ks) follows the instructions of step ks
+    auto compute = [&](const u32x4* As, const u32x4* Bs, auto&& after) {
+        bf16x8 xa[2][MI], xb[2][NI];
+        auto read = [&](int ks, int b) {
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi)
+                xa[b][mi] = __builtin_bit_cast(bf16x8, As[fa[ks] + mi * FSTR]);
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni)
+                xb[b][ni] = __builtin_bit_cast(bf16x8, Bs[fb[ks] + ni * FSTR]);
+        };
+        read(0, 0);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            if (ks + 1 < KS)
+                read(ks + 1, (ks + 1) & 1);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
                 for (int ni = 0; ni < NI; ++ni)
-                    acc[mi][ni] = Op::run(fa[ks % (PF + 1)][mi], fb[ks % (PF + 1)][ni],
-                                          acc[mi][ni]);
+                    acc[mi][ni] = Op::run(xa[ks & 1][mi], xb[ks & 1][ni], acc[mi][ni]);
+            __builtin_amdgcn_sched_barrier(0);
+            after(ks);
             __builtin_amdgcn_sched_barrier(0);
         }
-        if (s + 1 < nst)
-            store_stage(cur ^ 1);
-        __syncthreads();
+    };
+
+    const int nst = (p.KC + CH - 1) / CH;
+    if (nst > 0)
+        issue(0, A0, B0);
+    if (NS > 2 && nst > 1)
+        issue(1, A1, B1);
+    for (int s0 = 0; s0 < nst; s0 += NS) {
+#pragma unroll
+        for (int h = 0; h < NS; ++h) {
+            const int s = s0 + h;
+            if (s >= nst)
+                break;
+            u32x4* Ac = h == 0 ? A0 : (h == 1 ? A1 : A2);
+            u32x4* Bc = h == 0 ? B0 : (h == 1 ? B1 : B2);
+            const int hnx = (h + NS - 1) % NS;
+            u32x4* An = hnx == 0 ? A0 : (hnx == 1 ? A1 : A2);
+            u32x4* Bn = hnx == 0 ? B0 : (hnx == 1 ? B1 : B2);
+            if (NS > 2 && s + 1 < nst)
+                wait_all_but_next();
+            else
+                wait_vmcnt<0>();
+            stage_barrier();
+            // one code path: the copies of stage t are skipped (a uniform
+            // branch) past the last stage
+            const int t = s + NS - 1;
+            const bool more = t < nst;
+            const uint32_t d = b_delta(t);
+            compute(Ac, Bc, [&](int part) {
+                if (more)
+                    issue_part(t, An, Bn, part, d);
+            });
+        }
     }
+
+    const int brow = wn * NI * MT + lane % MT;
 
     // ---- epilogue (branch-free: masked lanes store to an out-of-range offset)
     const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y, p.Y_bytes);
@@ -383,7 +466,7 @@ conv_wgrad_bf16_kernel(const WgradBf16Params p)
     const int split = T / (n_rt * n_mt * p.G);
     const int m0 = mt * TM;
     const int r0 = rt * TN;
-    const int IH = p.IH, IW = p.IW, Ctot = p.Ctot;
+    const int Ctot = p.Ctot;
     const int OHW = p.OH * p.OW;
     const int col_begin = split * p.cols_per_split;
     const int col_end = min(p.Ncol, col_begin + p.cols_per_split);
@@ -403,8 +486,9 @@ conv_wgrad_bf16_kernel(const WgradBf16Params p)
         a_off[q] = g * p.Kgp + m0 + 8 * row;
         a_bad[q] = ((uint32_t)(row >= CAM) | (uint32_t)(m0 + 8 * row >= p.Kg)) << 31;
     }
-    // B chunk rows: r = r0 + 8*(cr + RS*q) = (u, v, c) over kh x kw x Cgp
-    int b_u[EB], b_v[EB], b_off[EB];
+    // B chunk rows: r = r0 + 8*(cr + RS*q) = (u, v, c) over kh x kw x Cgp;
+    // the zero border of X covers every tap, so no position check is needed
+    int b_off[EB];
     uint32_t b_bad[EB];
 #pragma unroll
     for (int q = 0; q < EB; ++q) {
@@ -412,9 +496,9 @@ conv_wgrad_bf16_kernel(const WgradBf16Params p)
         const int r = r0 + 8 * row;
         const int t = r / p.Cgp;
         const int c = r - t * p.Cgp;
-        b_u[q] = t / p.kw;
-        b_v[q] = t - b_u[q] * p.kw;
-        b_off[q] = (b_u[q] * IW + b_v[q]) * Ctot + g * p.Cgp + c;
+        const int u = t / p.kw;
+        const int v = t - u * p.kw;
+        b_off[q] = (u * p.IWp + v) * Ctot + g * p.Cgp + c;
         b_bad[q] = ((uint32_t)(row >= CBN) | (uint32_t)(r >= p.Rw)) << 31;
     }
 
@@ -428,22 +512,16 @@ conv_wgrad_bf16_kernel(const WgradBf16Params p)
             const int pix = col - n * OHW;
             const int i = (int)fdiv((uint32_t)pix, p.div_ow);
             const int j = pix - i * p.OW;
-            const int ih0 = i * p.sh - p.ph;
-            const int iw0 = j * p.sw - p.pw;
-            const int xbase = ((n * IH + ih0) * IW + iw0) * Ctot;
+            const int dbase = ((n * p.DHp + i + p.dtb) * p.DWp + j + p.dlb) * p.Ktot;
+            const int xbase = ((n * p.IHp + i * p.sh) * p.IWp + j * p.sw) * Ctot;
 #pragma unroll
             for (int q = 0; q < EA; ++q)
                 rA[q][e] = buf_ld_b128(
-                    rd, ((uint32_t)(col * p.Ktot + a_off[q]) * 2u) | cbad | a_bad[q]);
+                    rd, ((uint32_t)(dbase + a_off[q]) * 2u) | cbad | a_bad[q]);
 #pragma unroll
-            for (int q = 0; q < EB; ++q) {
-                const int ih = ih0 + b_u[q];
-                const int iw = iw0 + b_v[q];
-                const uint32_t bad = ((uint32_t)((unsigned)ih >= (unsigned)IH) |
-                                      (uint32_t)((unsigned)iw >= (unsigned)IW)) << 31;
+            for (int q = 0; q < EB; ++q)
                 rB[q][e] = buf_ld_b128(
-                    rx, ((uint32_t)(xbase + b_off[q]) * 2u) | cbad | bad | b_bad[q]);
-            }
+                    rx, ((uint32_t)(xbase + b_off[q]) * 2u) | cbad | b_bad[q]);
         }
     };
     // channel k of the two pixels -> one word (pixel 2pp in the low half)
@@ -586,17 +664,28 @@ wgrad_reduce_perm_kernel(const float* __restrict__ P, float* __restrict__ dW, in
 }
 
 // ------------------------------------------------------------------ staging
-// NCHW bf16 -> channel-contiguous bf16 with per-group channel padding, through
-// a CT-channel x (4096/CT)-pixel LDS tile (CT = 8 .. 64, sized to the padded
-// channel count): coalesced 2-byte reads along pixels, 16-byte writes along
-// channels.
+// NCHW bf16 -> zero-bordered channel-contiguous bf16 with per-group channel
+// padding, through a CT-channel x PT-pixel LDS tile (CT = 8 .. 64, sized to
+// the padded channel count; PT = min(4096 / CT, 256)) over the bordered
+// Hp x Wp grid: coalesced 2-byte reads along pixels (zeros outside the
+// image), 16-byte writes along channels.
+template <int CT>
+constexpr int stage_tile_pixels()
+{
+    return 4096 / CT < 256 ? 4096 / CT : 256;
+}
+
 template <int CT>
 __global__ void __launch_bounds__(256)
-nhwc_from_nchw_bf16_kernel(const bf16_t* __restrict__ X, bf16_t* __restrict__ Xh, int C, int HW,
-                           int Cg, int Cgp, int Ctot, int ptiles, int ctiles)
+stage_nhwc_bf16_kernel(const bf16_t* __restrict__ X, bf16_t* __restrict__ Xp, int C, int H, int W,
+                       int Cg, int Cgp, int Ctot, int Hp, int Wp, int tb, int lb, int ptiles,
+                       int ctiles)
 {
-    constexpr int PT = 4096 / CT;
+    constexpr int PT = stage_tile_pixels<CT>();
     constexpr int C8 = CT / 8;
+    constexpr int NQ = CT * PT / 256;  // tile elements per thread
+    constexpr int NW = PT * C8 / 256;  // 16-byte writes per thread
+    static_assert(256 % PT == 0 && NW >= 1, "tile shape");
     __shared__ bf16_t tile[CT][PT + 2];
     // block -> (n, channel tile, pixel tile), pixel tiles fastest
     const int n = blockIdx.x / (ptiles * ctiles);
@@ -604,49 +693,57 @@ nhwc_from_nchw_bf16_kernel(const bf16_t* __restrict__ X, bf16_t* __restrict__ Xh
     const int ct = rem / ptiles;
     const int c0 = ct * CT;
     const int p0 = (rem - ct * ptiles) * PT;
+    const int HWp = Hp * Wp;
     const int tid = threadIdx.x;
+    // the thread's pixel is the same for every element it loads (256 % PT == 0)
+    const int px = tid % PT;
+    const int pix = p0 + px;
+    const int hp = pix / Wp;
+    const int h = hp - tb;
+    const int w = pix - hp * Wp - lb;
+    const bool inside = pix < HWp && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+    const size_t src = (size_t)n * C * H * W + (size_t)h * W + w;
 #pragma unroll 4
-    for (int q = 0; q < 16; ++q) {
-        const int e = tid + 256 * q;
-        const int c = e / PT;
-        const int px = e % PT;
+    for (int q = 0; q < NQ; ++q) {
+        const int c = (tid + 256 * q) / PT;
         const int cp = c0 + c;
         const int g = cp / Cgp;
         const int cl = cp - g * Cgp;
-        const int pix = p0 + px;
         bf16_t v = 0;
-        if (cp < Ctot && cl < Cg && pix < HW)
-            v = X[((size_t)n * C + g * Cg + cl) * HW + pix];
+        if (inside && cp < Ctot && cl < Cg)
+            v = X[src + (size_t)(g * Cg + cl) * H * W];
         tile[c][px] = v;
     }
     __syncthreads();
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int q = 0; q < NW; ++q) {
         const int id = tid + 256 * q;
-        const int px = id / C8;
+        const int pl = id / C8;
         const int c8 = id % C8;
-        const int pix = p0 + px;
+        const int pw = p0 + pl;
         const int cp = c0 + 8 * c8;
-        if (pix < HW && cp < Ctot) {
-            u32x4 w;
+        if (pw < HWp && cp < Ctot) {
+            u32x4 v;
 #pragma unroll
             for (int k = 0; k < 4; ++k)
-                w[k] = (uint32_t)tile[8 * c8 + 2 * k][px] |
-                       ((uint32_t)tile[8 * c8 + 2 * k + 1][px] << 16);
-            *(u32x4*)&Xh[((size_t)n * HW + pix) * Ctot + cp] = w;
+                v[k] = (uint32_t)tile[8 * c8 + 2 * k][pl] |
+                       ((uint32_t)tile[8 * c8 + 2 * k + 1][pl] << 16);
+            *(u32x4*)&Xp[((size_t)n * HWp + pw) * Ctot + cp] = v;
         }
     }
 }
 
-// Top-gradient staging: Dh = bf16(relu ? G [Y > 0] : G) channel-contiguous,
-// one block per (image, 64 padded channels, 64 pixels).  Each wave also sums
-// the fp32 masked gradient of its channels over the block's pixels (a fixed
-// butterfly) into sums[(g*Kg + k) * T + n * ptiles + pt]: the bias-gradient
-// partials, T = N * ptiles per channel.
+// Top-gradient staging: Dh = bf16(relu ? G [Y > 0] : G) channel-contiguous on
+// the zero-bordered Hp x Wp grid, one block per (image, 64 padded channels,
+// 64 bordered pixels).  Each wave also sums the fp32 masked gradient of its
+// channels over the block's pixels (a fixed butterfly; the border adds 0)
+// into sums[(g*Kg + k) * T + n * ptiles + pt]: the bias-gradient partials,
+// T = N * ptiles per channel.
 __global__ void __launch_bounds__(256)
 diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
-                      bf16_t* __restrict__ Dh, float* __restrict__ sums, int K, int HW, int Kg,
-                      int Kgp, int Ktot, int relu, int ptiles, int ctiles, int T)
+                      bf16_t* __restrict__ Dh, float* __restrict__ sums, int K, int H, int W,
+                      int Kg, int Kgp, int Ktot, int Hp, int Wp, int tb, int lb, int relu,
+                      int ptiles, int ctiles, int T)
 {
     __shared__ bf16_t tile[64][66];
     const int n = blockIdx.x / (ptiles * ctiles);
@@ -655,10 +752,17 @@ diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
     const int pt = rem - ct * ptiles;
     const int c0 = ct * 64;
     const int p0 = pt * 64;
+    const int HWp = Hp * Wp;
     const int tid = threadIdx.x;
     const int px = tid & 63;
     const int cw = tid >> 6;
     const int pix = p0 + px;
+    const int hp = pix / Wp;
+    const int h = hp - tb;
+    const int w = pix - hp * Wp - lb;
+    const bool inside = pix < HWp && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+    const size_t plane = (size_t)H * W;
+    const size_t src = (size_t)n * K * plane + (size_t)h * W + w;
 #pragma unroll 4
     for (int q = 0; q < 16; ++q) {
         const int cl = cw + 4 * q;
@@ -667,17 +771,17 @@ diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
         const int k = cp - g * Kgp;
         const bool ok = cp < Ktot && k < Kg;
         float d = 0.f;
-        if (ok && pix < HW) {
-            const size_t idx = ((size_t)n * K + g * Kg + k) * HW + pix;
+        if (ok && inside) {
+            const size_t idx = src + (size_t)(g * Kg + k) * plane;
             d = G[idx];
             if (relu && !(Y[idx] > 0.f))
                 d = 0.f;
         }
         tile[cl][px] = f32_to_bf16_rne(d);
         if (sums) {
-            const float s = wave_sum(d);
+            const float sm = wave_sum(d);
             if (px == 0 && ok)
-                sums[(size_t)(g * Kg + k) * T + n * ptiles + pt] = s;
+                sums[(size_t)(g * Kg + k) * T + n * ptiles + pt] = sm;
         }
     }
     __syncthreads();
@@ -688,13 +792,13 @@ diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
         const int c8 = id & 7;
         const int pw = p0 + pl;
         const int cp = c0 + 8 * c8;
-        if (pw < HW && cp < Ktot) {
-            u32x4 w;
+        if (pw < HWp && cp < Ktot) {
+            u32x4 v;
 #pragma unroll
             for (int k = 0; k < 4; ++k)
-                w[k] = (uint32_t)tile[8 * c8 + 2 * k][pl] |
+                v[k] = (uint32_t)tile[8 * c8 + 2 * k][pl] |
                        ((uint32_t)tile[8 * c8 + 2 * k + 1][pl] << 16);
-            *(u32x4*)&Dh[((size_t)n * HW + pw) * Ktot + cp] = w;
+            *(u32x4*)&Dh[((size_t)n * HWp + pw) * Ktot + cp] = v;
         }
     }
 }
@@ -784,29 +888,42 @@ unsigned grid_1d(long total)
     return (unsigned)(blocks > 4096 ? 4096 : (blocks < 1 ? 1 : blocks));
 }
 
-template <int MT, int WM, int WN, int MI, int NI, int TK, int EPI, bool MASK>
+template <int MT, int WM, int WN, int MI, int NI, int NS, int EPI, bool MASK>
 hipError_t launch_gemm(const GemmBf16Params& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * MT, TN = WN * NI * MT;
     const int64_t tiles = (int64_t)((p.Ncol + TN - 1) / TN) * ((p.M + TM - 1) / TM) * p.G;
     const int64_t per_xcd = (tiles + 7) / 8;
-    hipLaunchKernelGGL((conv_gemm_bf16_kernel<MT, WM, WN, MI, NI, TK, EPI, MASK>),
+    hipLaunchKernelGGL((conv_gemm_bf16_kernel<MT, WM, WN, MI, NI, NS, EPI, MASK>),
                        dim3((unsigned)(per_xcd * 8)), dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();
 }
 
-template <int EPI, bool MASK>
+template <int NS, int EPI, bool MASK>
 hipError_t launch_gemm_tile(const GemmBf16Params& p, int tile, hipStream_t s)
 {
     switch (tile) {
-    case TILE_128x128:
-        return launch_gemm<32, 2, 2, 2, 2, kBf16TK, EPI, MASK>(p, s);
-    case TILE_96x256:
-        return launch_gemm<32, 1, 4, 3, 2, kBf16TK, EPI, MASK>(p, s);
-    case TILE_48x256:
-        return launch_gemm<16, 1, 4, 3, 4, kBf16TK, EPI, MASK>(p, s);
-    case TILE_64x256:
-        return launch_gemm<32, 1, 4, 2, 2, kBf16TK, EPI, MASK>(p, s);
+    case BTILE_128x256:
+        return launch_gemm<32, 1, 4, 4, 2, NS, EPI, MASK>(p, s);
+    case BTILE_96x256:
+        return launch_gemm<32, 1, 4, 3, 2, NS, EPI, MASK>(p, s);
+    case BTILE_64x256:
+        return launch_gemm<32, 1, 4, 2, 2, NS, EPI, MASK>(p, s);
+    case BTILE_48x256:
+        return launch_gemm<16, 1, 4, 3, 4, NS, EPI, MASK>(p, s);
+    default:
+        return hipErrorInvalidValue;
+    }
+}
+
+template <int EPI, bool MASK>
+hipError_t launch_gemm_pipe(const GemmBf16Params& p, int tile, int pipe, hipStream_t s)
+{
+    switch (pipe) {
+    case BPIPE_2:
+        return launch_gemm_tile<2, EPI, MASK>(p, tile, s);
+    case BPIPE_3:
+        return launch_gemm_tile<3, EPI, MASK>(p, tile, s);
     default:
         return hipErrorInvalidValue;
     }
@@ -824,15 +941,34 @@ hipError_t launch_wg(const WgradBf16Params& p, hipStream_t s)
 
 }  // namespace
 
-hipError_t launch_conv_gemm_bf16(const GemmBf16Params& p, int epi, int tile, hipStream_t s)
+int bf16_tile_m(int tile)
+{
+    switch (tile) {
+    case BTILE_128x256:
+        return 128;
+    case BTILE_96x256:
+        return 96;
+    case BTILE_64x256:
+        return 64;
+    case BTILE_48x256:
+        return 48;
+    default:
+        return 0;
+    }
+}
+
+hipError_t launch_conv_gemm_bf16(const GemmBf16Params& p, int epi, int tile, int pipe,
+                                 hipStream_t s)
 {
     if (p.Ncol == 0)
         return hipSuccess;
-    if (p.Rp % kBf16TK != 0 || p.Cgp % 8 != 0 || p.Ctot % 8 != 0)
+    if (p.Rp % kBf16TK != 0 || p.Cgp % 8 != 0 || p.Ctot % 8 != 0 || p.Cg8 * 8 != p.Cgp ||
+        p.KC * 8 > p.Rp || p.KC != p.kh * p.kw * p.Cg8)
         return hipErrorInvalidValue;
     if (epi == 0)
-        return launch_gemm_tile<0, false>(p, tile, s);
-    return p.Omask ? launch_gemm_tile<1, true>(p, tile, s) : launch_gemm_tile<1, false>(p, tile, s);
+        return launch_gemm_pipe<0, false>(p, tile, pipe, s);
+    return p.Omask ? launch_gemm_pipe<1, true>(p, tile, pipe, s)
+                   : launch_gemm_pipe<1, false>(p, tile, pipe, s);
 }
 
 hipError_t launch_conv_wgrad_bf16(const WgradBf16Params& p, int tile, hipStream_t s)
@@ -863,49 +999,52 @@ hipError_t launch_wgrad_reduce_perm(const float* P, float* dW, int K, int Rw, in
     return hipGetLastError();
 }
 
-hipError_t launch_nhwc_from_nchw_bf16(const uint16_t* X, uint16_t* Xh, int N, int C, int HW,
-                                      int Cg, int Cgp, int Ctot, hipStream_t s)
+hipError_t launch_stage_nhwc_bf16(const uint16_t* X, uint16_t* Xp, int N, int C, int H, int W,
+                                  int Cg, int Cgp, int Ctot, int Hp, int Wp, int tb, int lb,
+                                  hipStream_t s)
 {
     if (N == 0)
         return hipSuccess;
     const int ct = Ctot <= 8 ? 8 : Ctot <= 16 ? 16 : Ctot <= 32 ? 32 : 64;
-    const int pt = 4096 / ct;
-    const int ptiles = (HW + pt - 1) / pt;
+    const int pt = ct == 8 ? stage_tile_pixels<8>() : ct == 16 ? stage_tile_pixels<16>()
+                 : ct == 32 ? stage_tile_pixels<32>() : stage_tile_pixels<64>();
+    const int ptiles = (Hp * Wp + pt - 1) / pt;
     const int ctiles = (Ctot + ct - 1) / ct;
     const dim3 grid((unsigned)((int64_t)ptiles * ctiles * N));
+#define CAFFE_STAGE_LAUNCH(CT)                                                                    \
+    hipLaunchKernelGGL(stage_nhwc_bf16_kernel<CT>, grid, dim3(256), 0, s, X, Xp, C, H, W, Cg, Cgp, \
+                       Ctot, Hp, Wp, tb, lb, ptiles, ctiles)
     switch (ct) {
     case 8:
-        hipLaunchKernelGGL(nhwc_from_nchw_bf16_kernel<8>, grid, dim3(256), 0, s, X, Xh, C, HW, Cg,
-                           Cgp, Ctot, ptiles, ctiles);
+        CAFFE_STAGE_LAUNCH(8);
         break;
     case 16:
-        hipLaunchKernelGGL(nhwc_from_nchw_bf16_kernel<16>, grid, dim3(256), 0, s, X, Xh, C, HW, Cg,
-                           Cgp, Ctot, ptiles, ctiles);
+        CAFFE_STAGE_LAUNCH(16);
         break;
     case 32:
-        hipLaunchKernelGGL(nhwc_from_nchw_bf16_kernel<32>, grid, dim3(256), 0, s, X, Xh, C, HW, Cg,
-                           Cgp, Ctot, ptiles, ctiles);
+        CAFFE_STAGE_LAUNCH(32);
         break;
     default:
-        hipLaunchKernelGGL(nhwc_from_nchw_bf16_kernel<64>, grid, dim3(256), 0, s, X, Xh, C, HW, Cg,
-                           Cgp, Ctot, ptiles, ctiles);
+        CAFFE_STAGE_LAUNCH(64);
         break;
     }
+#undef CAFFE_STAGE_LAUNCH
     return hipGetLastError();
 }
 
-int diff_prep_terms(int N, int HW) { return N * ((HW + 63) / 64); }
+int diff_prep_terms(int N, int HWp) { return N * ((HWp + 63) / 64); }
 
 hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, float* sums, int N,
-                                 int K, int HW, int Kg, int Kgp, int Ktot, int relu, hipStream_t s)
+                                 int K, int H, int W, int Kg, int Kgp, int Ktot, int Hp, int Wp,
+                                 int tb, int lb, int relu, hipStream_t s)
 {
     if (N == 0)
         return hipSuccess;
-    const int ptiles = (HW + 63) / 64;
+    const int ptiles = (Hp * Wp + 63) / 64;
     const int ctiles = (Ktot + 63) / 64;
     hipLaunchKernelGGL(diff_prep_bf16_kernel, dim3((unsigned)((int64_t)ptiles * ctiles * N)),
-                       dim3(256), 0, s, G, Y, Dh, sums, K, HW, Kg, Kgp, Ktot, relu, ptiles, ctiles,
-                       N * ptiles);
+                       dim3(256), 0, s, G, Y, Dh, sums, K, H, W, Kg, Kgp, Ktot, Hp, Wp, tb, lb,
+                       relu, ptiles, ctiles, N * ptiles);
     return hipGetLastError();
 }
 

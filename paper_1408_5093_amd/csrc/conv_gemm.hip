@@ -55,8 +55,6 @@ struct Mfma<16> {
     static __device__ __forceinline__ int row(int q, int lane) { return 4 * (lane >> 4) + q; }
 };
 
-typedef __attribute__((address_space(3))) void lds_void;
-
 // One wave copies 64 consecutive floats into LDS at `dst` (wave-uniform):
 // lane i's element from byte offset voff + soff lands at dst + 4*i.  An offset
 // with bit 31 set is out of range and writes 0.

@@ -149,15 +149,35 @@ int wgrad_tile_k();
 hipError_t launch_conv_wgrad_f32(const WgradParams& p, int tile, hipStream_t s);
 
 // ---- bf16 operands (conv_bf16.hip) ----
-// Reduction depth of one pipeline stage of the bf16 implicit GEMM; padded
-// reduction lengths are multiples of it.
-constexpr int kBf16TK = 32;
+// Reduction depth of a bf16 implicit-GEMM stage (8 chunks of 8 bf16: 128
+// bytes of each operand row); the packed reductions Rp and Rtp are padded to
+// multiples of it.
+constexpr int kBf16TK = 64;
 
-// Implicit GEMM over a channel-contiguous bf16 gather source
-// X[N][IH][IW][Ctot] whose group g owns channels g*Cgp .. g*Cgp + Cgp - 1
-// (Cgp a multiple of 8).  Reduction r = (u, v, c) over kh x kw x Cgp, padded
-// with zeros to Rp (a multiple of kBf16TK); A is [G*M][Rp] bf16.
-//   C_g[m][col] = sum_r A[g*M + m][r] * X[n][i*sh - ph + u][j*sw - pw + v][g*Cgp + c]
+// bf16 implicit-GEMM tiles (rows x columns per workgroup of 4 waves, 1 x 4).
+enum Bf16Tile {
+    BTILE_128x256 = 0,  // 32x32x16 MFMA, each wave 128x64
+    BTILE_96x256 = 1,   // 32x32x16, each wave 96x64
+    BTILE_64x256 = 2,   // 32x32x16, each wave 64x64
+    BTILE_48x256 = 3,   // 16x16x32 MFMA, each wave 48x64
+    BTILE_COUNT
+};
+int bf16_tile_m(int tile);
+// Pipeline of the bf16 implicit GEMM (kBf16TK-deep stages): LDS buffers.
+enum Bf16Pipe {
+    BPIPE_2 = 0,  // double-buffered
+    BPIPE_3 = 1,  // three buffers (copies two stages ahead)
+    BPIPE_COUNT
+};
+
+// Implicit GEMM over a channel-contiguous, zero-bordered bf16 gather source
+// X[N][IHp][IWp][Ctot] whose group g owns channels g*Cgp .. g*Cgp + Cgp - 1
+// (Cgp a multiple of 8).  The reduction r = (u, v, c) over kh x kw x Cgp
+// runs in 16-byte chunks of 8 channels, KC = kh*kw*Cgp/8 of them; A is
+// [G*M][Rp] bf16 (Rp >= 8*KC a multiple of kBf16TK, zero past 8*KC).
+//   C_g[m][col] = sum_r A[g*M + m][r] * X[n][i*sh + oh0 + u][j*sw + ow0 + v][g*Cgp + c]
+// for col = (n, i, j) in N x OH x OW: the borders of X stand for the
+// convolution's zero padding, so every gathered position lies inside it.
 // Epilogues as ConvGemmParams (epi 0 forward, epi 1 phase-stacked data
 // gradient); Omask (epi 1, may be null) is a bf16 tensor laid out like Y.
 struct GemmBf16Params {
@@ -167,28 +187,33 @@ struct GemmBf16Params {
     float* Y;
     const float* bias;
     uint32_t A_bytes, X_bytes, Y_bytes;
-    int N, IH, IW, Ctot, Cgp;
-    int kh, kw, sh, sw, ph, pw;
+    int N, IHp, IWp, Ctot, Cgp, Cg8, KC;
+    int kh, kw, sh, sw, oh0, ow0;
     int OH, OW;
     int M, Rp, G, Ncol;
     int relu;
     int Cout, OutH, OutW;
     int psh, psw, a0h, a0w, oph, opw, Cg_out;
     int xcd_order;
+    FastDiv div_cg8, div_kw;
 };
-hipError_t launch_conv_gemm_bf16(const GemmBf16Params& p, int epi, int tile, hipStream_t s);
+hipError_t launch_conv_gemm_bf16(const GemmBf16Params& p, int epi, int tile, int pipe,
+                                 hipStream_t s);
 
-// Split-K weight gradient over channel-contiguous bf16 operands:
+// Split-K weight gradient over channel-contiguous, zero-bordered bf16
+// operands (D laid out [N][DHp][DWp][Ktot] with the real pixels at offset
+// (dtb, dlb); X as in GemmBf16Params with oh0 = ow0 = 0):
 //   P[s][g*Kg + m][(u*kw + v)*Cgp + c] =
-//       sum_{col in split s} D[col][g*Kgp + m] * X[n][i*sh - ph + u][j*sw - pw + v][g*Cgp + c]
+//       sum_{col in split s} D[n][i + dtb][j + dlb][g*Kgp + m] * X[n][i*sh + u][j*sw + v][g*Cgp + c]
 // with col = (n, i, j) and Rw = kh*kw*Cgp columns per output channel.
 struct WgradBf16Params {
     const uint16_t* D;
     const uint16_t* X;
     float* P;
     uint32_t D_bytes, X_bytes, P_bytes;
-    int N, IH, IW, Ctot, Cgp, K, Kg, Kgp, Ktot;
-    int kh, kw, sh, sw, ph, pw;
+    int N, IHp, IWp, Ctot, Cgp, K, Kg, Kgp, Ktot;
+    int DHp, DWp, dtb, dlb;
+    int kh, kw, sh, sw;
     int OH, OW;
     int Rw, G;
     int Ncol, cols_per_split, splits;
@@ -202,17 +227,21 @@ hipError_t launch_conv_wgrad_bf16(const WgradBf16Params& p, int tile, hipStream_
 hipError_t launch_wgrad_reduce_perm(const float* P, float* dW, int K, int Rw, int Cgp, int Cg,
                                     int khw, int splits, int accumulate, hipStream_t s);
 
-// Xh[n][p][g*Cgp + c] = X[n][g*Cg + c][p] (c < Cg, else 0), p over H*W;
-// Ctot = G*Cgp.
-hipError_t launch_nhwc_from_nchw_bf16(const uint16_t* X, uint16_t* Xh, int N, int C, int HW,
-                                      int Cg, int Cgp, int Ctot, hipStream_t s);
+// Xp[n][hp][wp][g*Cgp + c] = X[n][g*Cg + c][hp - tb][wp - lb] inside the H x W
+// image (c < Cg), else 0: the zero-bordered channel-contiguous copy, Hp x Wp
+// pixels per image; Ctot = G*Cgp.
+hipError_t launch_stage_nhwc_bf16(const uint16_t* X, uint16_t* Xp, int N, int C, int H, int W,
+                                  int Cg, int Cgp, int Ctot, int Hp, int Wp, int tb, int lb,
+                                  hipStream_t s);
 
-// Dh[n][p][g*Kgp + k] = bf16(relu ? G [Y > 0] : G)[n][g*Kg + k][p] (k < Kg,
-// else 0).  sums (may be null): the fp32 bias-gradient partials,
-// sums[k*T + t] for T = diff_prep_terms(N, HW) terms per output channel.
-int diff_prep_terms(int N, int HW);
+// Dh[n][hp][wp][g*Kgp + k] = bf16(relu ? G [Y > 0] : G)[n][g*Kg + k][hp - tb][wp - lb]
+// inside the H x W grid (k < Kg), else 0.  sums (may be null): the fp32
+// bias-gradient partials, sums[k*T + t] for T = diff_prep_terms(N, Hp*Wp)
+// terms per output channel.
+int diff_prep_terms(int N, int HWp);
 hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, float* sums, int N,
-                                 int K, int HW, int Kg, int Kgp, int Ktot, int relu, hipStream_t s);
+                                 int K, int H, int W, int Kg, int Kgp, int Ktot, int Hp, int Wp,
+                                 int tb, int lb, int relu, hipStream_t s);
 
 // db[k] = (accumulate ? db[k] : 0) + sum_{t < T} sums[k*T + t] (fixed order).
 hipError_t launch_bias_reduce(const float* sums, float* db, int T, int K, int accumulate,

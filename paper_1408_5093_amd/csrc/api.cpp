@@ -203,6 +203,16 @@ int env_tile(const char* name)
 
 int round_up(int x, int a) { return (x + a - 1) / a * a; }
 
+// bf16 weight-gradient tile for Kg output channels per group: the least row
+// padding, ties to 128 rows.
+int pick_bf16_wgrad_tile(int Kg, int forced)
+{
+    if (forced >= 0 && forced < BWTILE_COUNT)
+        return forced;
+    const int64_t r128 = (int64_t)(Kg + 127) / 128 * 128, r96 = (int64_t)(Kg + 95) / 96 * 96;
+    return r96 < r128 ? BWTILE_96x256 : BWTILE_128x256;
+}
+
 // bf16 GEMM pipeline for a tile: three LDS buffers (copies two stages ahead)
 // unless double buffering lets two workgroups share a compute unit's LDS
 // (measured on the CaffeNet layers: the 48-row data-gradient tiles gain more
@@ -273,12 +283,13 @@ int plan_bf16(ConvPlan* p)
     // weight-gradient split-K over the output pixels, as for fp32
     const int64_t ncol = (int64_t)q.N * q.Ho * q.Wo;
     const int tk = kBf16WgradTK;
-    q.wgrad_tile = pick_wgrad_tile(q.Kg, env_tile("CAFFE_CONV_WGRAD_TILE"));
-    const int wtm = wgrad_tile_m(q.wgrad_tile), wtn = wgrad_tile_n(q.wgrad_tile);
+    q.wgrad_tile = pick_bf16_wgrad_tile(q.Kg, env_tile("CAFFE_BF16_WGRAD_TILE"));
+    const int wtm = bf16_wgrad_tile_m(q.wgrad_tile), wtn = kBf16WgradTN;
     const int64_t tiles = (int64_t)((q.Kg + wtm - 1) / wtm) * ((q.Rw + wtn - 1) / wtn) * q.G;
+    // one workgroup per compute unit at a time (its LDS): about two rounds
     const int64_t target = env_tile("CAFFE_CONV_WGRAD_BLOCKS") > 0
                                ? env_tile("CAFFE_CONV_WGRAD_BLOCKS")
-                               : 2048;
+                               : 2 * (int64_t)device_cu_count();
     int64_t splits = (target + tiles - 1) / tiles;
     const int64_t max_splits = std::max<int64_t>(1, ncol / (8 * tk));
     const int64_t max_by_bytes = std::max<int64_t>(1, kMaxTensorBytes / (rw * q.K * 4));

@@ -425,30 +425,54 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
 }
 
 // ----------------------------------------------------------- weight gradient
-// Split-K over the output pixels (n, i, j), 32 per stage.  Both operands are
-// gathered as 16-byte chunks of 8 channels per pixel; each thread loads the
-// same chunk row for two adjacent pixels and writes the pair of values of
-// every channel as one 32-bit word, so LDS rows hold consecutive pixels (the
-// reduction index) as the bf16 instructions want them.
-template <int WM, int WN, int MI, int NI>
+// Split-K over the output pixels (n, i, j), TKP = 64 per stage.  Both operands
+// are gathered pixel by pixel into LDS tiles laid out [pixel][channel] (the
+// channel-contiguous staging read as is): a pixel row of the D tile holds the
+// tile's 128 output channels, one of the X tile the tile's TN reduction
+// indices r = (u, v, c) (8 channels of one tap per 16-byte chunk), each
+// 64-channel line of a row copied by 16-byte DMA as in the forward kernel
+// (8 rows x 128 bytes per wave copy, chunks swizzled by chunk_swz of the
+// pixel).  The instructions want 8 consecutive pixels per lane for one
+// channel; ds_read_b64_tr_b16 supplies them: in each group of 16 lanes, lane
+// (4i + q) points at channels 4q .. 4q + 3 of pixel row k0 + i, and lane j of
+// the group receives pixels k0 .. k0 + 3 of channel j.  Two such reads make a
+// fragment.
+typedef short short4v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ short4v lds_read_tr16(const void* p)
+{
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) short4v*)p);
+}
+
+// Byte offset of element (pixel k, channel c) in a [pixel][channel] tile of
+// NL 64-channel lines per pixel.
+__device__ __forceinline__ int wtile_off(int k, int c, int NL)
+{
+    return ((k >> 3) * NL + (c >> 6)) * 1024 + (k & 7) * 128 +
+           ((((c & 63) >> 3) ^ chunk_swz(k)) << 4) + (c & 7) * 2;
+}
+
+template <int WM, int WN, int MI, int NI, int NS>
 __global__ void __launch_bounds__(64 * WM * WN)
 conv_wgrad_bf16_kernel(const WgradBf16Params p)
 {
     constexpr int MT = 32;
-    constexpr int NT = 64 * WM * WN;
+    constexpr int NW = WM * WN;
     constexpr int TM = WM * MI * MT;
     constexpr int TN = WN * NI * MT;
-    constexpr int TKP = 32;            // pixels per stage
-    constexpr int PP = TKP / 2;        // pixel pairs per stage
-    constexpr int LD = TKP + 8;
-    constexpr int RS = NT / PP;        // chunk rows covered by one pass
-    constexpr int CAM = TM / 8, CBN = TN / 8;
-    constexpr int EA = (CAM + RS - 1) / RS;
-    constexpr int EB = (CBN + RS - 1) / RS;
-    constexpr int KS = TKP / 16;
+    constexpr int TKP = 64;            // pixels per stage
+    constexpr int KS = TKP / 16;       // instructions along k per stage
+    constexpr int NLA = 2;             // 64-channel lines per D row (TM <= 128)
+    constexpr int NLB = TN / 64;       // lines per X row
+    constexpr int EA = TKP / 8 / NW;   // row groups (8 pixels) per wave
+    constexpr int NC = EA * (NLA + NLB);
+    constexpr int CPP = (NC + KS - 1) / KS;
+    static_assert(NW == 4 && TM <= 128 && TN % 64 == 0 && EA == 2, "tile shape");
+    static_assert(NS == 2 || NS == 3, "buffers");
 
-    __shared__ __attribute__((aligned(16))) bf16_t As[2][TM][LD];
-    __shared__ __attribute__((aligned(16))) bf16_t Bs[2][TN][LD];
+    __shared__ u32x4 A0[TKP * NLA * 8], A1[TKP * NLA * 8], A2[NS > 2 ? TKP * NLA * 8 : 1];
+    __shared__ u32x4 B0[TKP * NLB * 8], B1[TKP * NLB * 8], B2[NS > 2 ? TKP * NLB * 8 : 1];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -466,7 +490,6 @@ conv_wgrad_bf16_kernel(const WgradBf16Params p)
     const int split = T / (n_rt * n_mt * p.G);
     const int m0 = mt * TM;
     const int r0 = rt * TN;
-    const int Ctot = p.Ctot;
     const int OHW = p.OH * p.OW;
     const int col_begin = split * p.cols_per_split;
     const int col_end = min(p.Ncol, col_begin + p.cols_per_split);
@@ -474,81 +497,66 @@ conv_wgrad_bf16_kernel(const WgradBf16Params p)
     const __amdgpu_buffer_rsrc_t rd = make_rsrc(p.D, p.D_bytes);
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, p.X_bytes);
 
-    const int pp = tid % PP;  // pixel pair within a stage
-    const int cr = tid / PP;  // chunk row within a pass
-
-    // A chunk rows: channels m0 + 8*(cr + RS*q) .. +7 of the group
-    int a_off[EA];
-    uint32_t a_bad[EA];
+    // copies: this wave's row groups 2*wave + e (pixels 16*wave + 8e + lane/8
+    // of a stage), lane's chunk of a line (lane % 8) ^ chunk_swz(pixel).  Byte
+    // offsets from a pixel: rows past Kg and columns past Rw are read (inside
+    // the buffer or as zeros past its end) but feed only results that are
+    // never stored, so they need no mask.
+    const int cr = lane >> 3;
+    uint32_t a_off[EA][NLA], b_off[EA][NLB];
 #pragma unroll
-    for (int q = 0; q < EA; ++q) {
-        const int row = cr + RS * q;
-        a_off[q] = g * p.Kgp + m0 + 8 * row;
-        a_bad[q] = ((uint32_t)(row >= CAM) | (uint32_t)(m0 + 8 * row >= p.Kg)) << 31;
+    for (int e = 0; e < EA; ++e) {
+        const int ch = (lane & 7) ^ chunk_swz(8 * (EA * wave + e) + cr);
+#pragma unroll
+        for (int L = 0; L < NLA; ++L)
+            a_off[e][L] = (uint32_t)(g * p.Kgp + m0 + 64 * L + 8 * ch) * 2u;
+#pragma unroll
+        for (int L = 0; L < NLB; ++L) {
+            const int r = r0 + 64 * L + 8 * ch;  // 8 channels of one tap
+            const int t = r / p.Cgp;
+            const int c = r - t * p.Cgp;
+            const int u = t / p.kw;
+            const int v = t - u * p.kw;
+            b_off[e][L] = (uint32_t)((u * p.IWp + v) * p.Ctot + g * p.Cgp + c) * 2u;
+        }
     }
-    // B chunk rows: r = r0 + 8*(cr + RS*q) = (u, v, c) over kh x kw x Cgp;
-    // the zero border of X covers every tap, so no position check is needed
-    int b_off[EB];
-    uint32_t b_bad[EB];
+    // byte offsets of this wave's pixel rows in stage t; kOob past the
+    // split's end (base + offset then stays out of range: offsets < 2^31)
+    uint32_t pd[EA], px[EA];
+    auto pixels = [&](int t) {
 #pragma unroll
-    for (int q = 0; q < EB; ++q) {
-        const int row = cr + RS * q;
-        const int r = r0 + 8 * row;
-        const int t = r / p.Cgp;
-        const int c = r - t * p.Cgp;
-        const int u = t / p.kw;
-        const int v = t - u * p.kw;
-        b_off[q] = (u * p.IWp + v) * Ctot + g * p.Cgp + c;
-        b_bad[q] = ((uint32_t)(row >= CBN) | (uint32_t)(r >= p.Rw)) << 31;
-    }
-
-    u32x4 rA[EA][2], rB[EB][2];
-    auto load_stage = [&](int cbase) {
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            const int col = cbase + 2 * pp + e;
-            const uint32_t cbad = (uint32_t)(col >= col_end) << 31;
+        for (int e = 0; e < EA; ++e) {
+            const int col = col_begin + t * TKP + 16 * wave + 8 * e + cr;
             const int n = (int)fdiv((uint32_t)col, p.div_ohw);
             const int pix = col - n * OHW;
             const int i = (int)fdiv((uint32_t)pix, p.div_ow);
             const int j = pix - i * p.OW;
-            const int dbase = ((n * p.DHp + i + p.dtb) * p.DWp + j + p.dlb) * p.Ktot;
-            const int xbase = ((n * p.IHp + i * p.sh) * p.IWp + j * p.sw) * Ctot;
-#pragma unroll
-            for (int q = 0; q < EA; ++q)
-                rA[q][e] = buf_ld_b128(
-                    rd, ((uint32_t)(dbase + a_off[q]) * 2u) | cbad | a_bad[q]);
-#pragma unroll
-            for (int q = 0; q < EB; ++q)
-                rB[q][e] = buf_ld_b128(
-                    rx, ((uint32_t)(xbase + b_off[q]) * 2u) | cbad | b_bad[q]);
+            const bool ok = col < col_end;
+            pd[e] = ok ? (uint32_t)(((n * p.DHp + i + p.dtb) * p.DWp + j + p.dlb) * p.Ktot) * 2u
+                       : kOob;
+            px[e] = ok ? (uint32_t)(((n * p.IHp + i * p.sh) * p.IWp + j * p.sw) * p.Ctot) * 2u
+                       : kOob;
         }
     };
-    // channel k of the two pixels -> one word (pixel 2pp in the low half)
-    auto pair = [](const u32x4& x0, const u32x4& x1, int k) -> uint32_t {
-        const uint32_t w0 = x0[k >> 1], w1 = x1[k >> 1];
-        return (k & 1) ? ((w0 >> 16) | (w1 & 0xffff0000u)) : ((w0 & 0xffffu) | (w1 << 16));
-    };
-    auto store_stage = [&](int buf) {
+    auto issue_part = [&](u32x4* As, u32x4* Bs, int part) {
 #pragma unroll
-        for (int q = 0; q < EA; ++q) {
-            const int row = cr + RS * q;
-            if (CAM % RS == 0 || row < CAM) {
-#pragma unroll
-                for (int k = 0; k < 8; ++k)
-                    *(uint32_t*)&As[buf][8 * row + k][2 * pp] = pair(rA[q][0], rA[q][1], k);
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < EB; ++q) {
-            const int row = cr + RS * q;
-            if (CBN % RS == 0 || row < CBN) {
-#pragma unroll
-                for (int k = 0; k < 8; ++k)
-                    *(uint32_t*)&Bs[buf][8 * row + k][2 * pp] = pair(rB[q][0], rB[q][1], k);
-            }
+        for (int c = part * CPP; c < (part + 1) * CPP && c < NC; ++c) {
+            const int e = c / (NLA + NLB);
+            const int L = c % (NLA + NLB);
+            const int rg = EA * wave + e;
+            if (L < NLA)
+                copy16_lds(rd, &As[(rg * NLA + L) * 64], pd[e] + a_off[e][L], 0u);
+            else
+                copy16_lds(rx, &Bs[(rg * NLB + L - NLA) * 64], px[e] + b_off[e][L - NLA], 0u);
         }
     };
+    auto issue = [&](int t, u32x4* As, u32x4* Bs) {
+        pixels(t);
+#pragma unroll
+        for (int part = 0; part < KS; ++part)
+            issue_part(As, Bs, part);
+    };
+    auto wait_all_but_next = [&]() { wait_vmcnt<NC>(); };
 
     floatx16 acc[MI][NI];
 #pragma unroll
@@ -557,50 +565,98 @@ conv_wgrad_bf16_kernel(const WgradBf16Params p)
         for (int ni = 0; ni < NI; ++ni)
             acc[mi][ni] = floatx16{};
 
-    const int nst = col_end > col_begin ? (col_end - col_begin + TKP - 1) / TKP : 0;
-    if (nst > 0) {
-        load_stage(col_begin);
-        store_stage(0);
+    // transposed-read addresses: lane as a source points at pixel
+    // 8*(lane/32) + 4h + (lane%16)/4 of the step, channel 16*((lane/16)%2) +
+    // 4*(lane%4) of its 32-row block; steps ks add 16 pixels (2 row groups)
+    const int ksrc = 8 * (lane >> 5) + ((lane & 15) >> 2);
+    const int csrc = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    int fa[MI][2], fb[NI][2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi)
+            fa[mi][h] = wtile_off(ksrc + 4 * h, wm * MI * MT + mi * MT + csrc, NLA);
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+            fb[ni][h] = wtile_off(ksrc + 4 * h, wn * NI * MT + ni * MT + csrc, NLB);
     }
-    __syncthreads();
 
-    const int arow = wm * MI * MT + (lane & 31);
-    const int brow = wn * NI * MT + (lane & 31);
-    const int kl = (lane >> 5) * 8;
-
-    for (int s = 0; s < nst; ++s) {
-        const int cur = s & 1;
-        if (s + 1 < nst)
-            load_stage(col_begin + (s + 1) * TKP);
-        bf16x8 fa[KS][MI], fb[KS][NI];
+    auto compute = [&](const u32x4* As, const u32x4* Bs, auto&& after) {
+        const char* a = (const char*)As;
+        const char* b = (const char*)Bs;
+        bf16x8 xa[2][MI], xb[2][NI];
+        auto read = [&](int ks, int buf) {
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi) {
+                const short4v lo = lds_read_tr16(a + fa[mi][0] + ks * 2 * NLA * 1024);
+                const short4v hi = lds_read_tr16(a + fa[mi][1] + ks * 2 * NLA * 1024);
+                xa[buf][mi] = __builtin_bit_cast(
+                    bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+            }
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni) {
+                const short4v lo = lds_read_tr16(b + fb[ni][0] + ks * 2 * NLB * 1024);
+                const short4v hi = lds_read_tr16(b + fb[ni][1] + ks * 2 * NLB * 1024);
+                xb[buf][ni] = __builtin_bit_cast(
+                    bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+            }
+        };
+        read(0, 0);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-            for (int mi = 0; mi < MI; ++mi)
-                fa[ks][mi] = lds_frag(&As[cur][arow + mi * MT][ks * 16 + kl]);
-#pragma unroll
-            for (int ni = 0; ni < NI; ++ni)
-                fb[ks][ni] = lds_frag(&Bs[cur][brow + ni * MT][ks * 16 + kl]);
-        }
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
+            if (ks + 1 < KS)
+                read(ks + 1, (ks + 1) & 1);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
                 for (int ni = 0; ni < NI; ++ni)
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks][mi], fb[ks][ni],
-                                                                        acc[mi][ni], 0, 0, 0);
-        if (s + 1 < nst)
-            store_stage(cur ^ 1);
-        __syncthreads();
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        xa[ks & 1][mi], xb[ks & 1][ni], acc[mi][ni], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            after(ks);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+
+    const int nst = col_end > col_begin ? (col_end - col_begin + TKP - 1) / TKP : 0;
+    if (nst > 0)
+        issue(0, A0, B0);
+    if (NS > 2 && nst > 1)
+        issue(1, A1, B1);
+    for (int s0 = 0; s0 < nst; s0 += NS) {
+#pragma unroll
+        for (int h = 0; h < NS; ++h) {
+            const int s = s0 + h;
+            if (s >= nst)
+                break;
+            u32x4* Ac = h == 0 ? A0 : (h == 1 ? A1 : A2);
+            u32x4* Bc = h == 0 ? B0 : (h == 1 ? B1 : B2);
+            const int hnx = (h + NS - 1) % NS;
+            u32x4* An = hnx == 0 ? A0 : (hnx == 1 ? A1 : A2);
+            u32x4* Bn = hnx == 0 ? B0 : (hnx == 1 ? B1 : B2);
+            if (NS > 2 && s + 1 < nst)
+                wait_all_but_next();
+            else
+                wait_vmcnt<0>();
+            stage_barrier();
+            const int t = s + NS - 1;
+            const bool more = t < nst;
+            if (more)
+                pixels(t);
+            compute(Ac, Bc, [&](int part) {
+                if (more)
+                    issue_part(An, Bn, part);
+            });
+        }
     }
 
-    // Partial result P[split][g*Kg + m][r], r = (u, v, c) over Rw (lanes along r)
+    // Partial result P[split][g*Kg + m][r], lanes along r
     const __amdgpu_buffer_rsrc_t rp = make_rsrc(p.P, p.P_bytes);
     const int pbase = split * p.K * p.Rw;
 #pragma unroll
     for (int ni = 0; ni < NI; ++ni) {
-        const int r = r0 + brow + ni * MT;
+        const int r = r0 + wn * NI * MT + ni * MT + (lane & 31);
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
@@ -934,7 +990,7 @@ hipError_t launch_wg(const WgradBf16Params& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * 32, TN = WN * NI * 32;
     const int64_t tiles = (int64_t)((p.Rw + TN - 1) / TN) * ((p.Kg + TM - 1) / TM) * p.G * p.splits;
-    hipLaunchKernelGGL((conv_wgrad_bf16_kernel<WM, WN, MI, NI>), dim3((unsigned)tiles),
+    hipLaunchKernelGGL((conv_wgrad_bf16_kernel<WM, WN, MI, NI, 3>), dim3((unsigned)tiles),
                        dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();
 }
@@ -971,17 +1027,17 @@ hipError_t launch_conv_gemm_bf16(const GemmBf16Params& p, int epi, int tile, int
                    : launch_gemm_pipe<1, false>(p, tile, pipe, s);
 }
 
+int bf16_wgrad_tile_m(int tile) { return tile == BWTILE_96x256 ? 96 : 128; }
+
 hipError_t launch_conv_wgrad_bf16(const WgradBf16Params& p, int tile, hipStream_t s)
 {
-    if (p.Cgp % 8 != 0 || p.Kgp % 8 != 0)
+    if (p.Cgp % 8 != 0 || p.Kgp % 8 != 0 || p.cols_per_split % kBf16WgradTK != 0)
         return hipErrorInvalidValue;
     switch (tile) {
-    case WTILE_128x128:
-        return launch_wg<2, 2, 2, 2>(p, s);
-    case WTILE_96x128:
-        return launch_wg<1, 4, 3, 1>(p, s);
-    case WTILE_64x128:
-        return launch_wg<2, 2, 1, 2>(p, s);
+    case BWTILE_128x256:
+        return launch_wg<2, 2, 2, 4>(p, s);
+    case BWTILE_96x256:
+        return launch_wg<1, 4, 3, 2>(p, s);
     default:
         return hipErrorInvalidValue;
     }

@@ -219,7 +219,16 @@ struct WgradBf16Params {
     int Ncol, cols_per_split, splits;
     FastDiv div_ohw, div_ow;
 };
-constexpr int kBf16WgradTK = 32;  // output pixels per weight-gradient stage
+constexpr int kBf16WgradTK = 64;  // output pixels per weight-gradient stage
+// bf16 weight-gradient tiles (output channels x reduction indices r)
+enum Bf16WgradTile {
+    BWTILE_128x256 = 0,  // 4 waves as 2x2, each 64x128
+    BWTILE_96x256 = 1,   // 4 waves as 1x4, each 96x64
+    BWTILE_COUNT
+};
+int bf16_wgrad_tile_m(int tile);
+constexpr int kBf16WgradTN = 256;
+// cols_per_split must be a multiple of kBf16WgradTK
 hipError_t launch_conv_wgrad_bf16(const WgradBf16Params& p, int tile, hipStream_t s);
 
 // dW[k][c][t] = (accumulate ? dW : 0) + sum_s P[s][k][t*Cgp + c] for c < Cg,

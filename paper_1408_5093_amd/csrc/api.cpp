@@ -64,9 +64,11 @@ struct ConvPlan {
     size_t off_d, off_sums, off_wt, off_part;
     size_t ws_fwd, ws_data, ws_weights, ws_both;
     // bf16 operands: channel-contiguous staging with each group's channels
-    // padded to a multiple of 8 (Cgp, Kgp); padded reduction lengths of the
-    // forward (Rp) and data-gradient (Rtp) GEMMs; weight-gradient columns Rw
-    int Cgp, Kgp, Rp, Rtp, Rw;
+    // padded to a multiple of 8 (Cgp, Kgp), or a single group of at most 4
+    // channels padded to Cgp in {1, 2, 4} with 8 / Cgp taps per 16-byte chunk
+    // (tpc; kw rounded up to kwp); padded reduction lengths of the forward
+    // (Rp) and data-gradient (Rtp) GEMMs; weight-gradient columns Rw
+    int Cgp, Kgp, Rp, Rtp, Rw, tpc, kwp;
     // zero-bordered bf16 staging: the input on an XHp x XWp grid (real pixels
     // at (ph, pw)), the top gradient on a DHp x DWp grid (real pixels at
     // (dtb, dlb)); the data-gradient gather reads the latter from (doh0, dow0)
@@ -250,15 +252,29 @@ int pick_bf16_tile(int M, int forced)
 int plan_bf16(ConvPlan* p)
 {
     ConvPlan& q = *p;
+    // Channels per staged group.  A 16-byte chunk of the reduction is 8
+    // channels of one tap, or, for one group of at most 4 channels, 8 / Cgp
+    // horizontally adjacent taps of Cgp channels: 8 consecutive staged
+    // elements, 16-byte aligned when the horizontal stride and the staged
+    // width are multiples of the taps per chunk (CaffeNet's conv1: 3 -> 4
+    // channels instead of 8).
     q.Cgp = round_up(q.Cg, 8);
+    if (q.G == 1)
+        for (int c = 1; c <= 4; c *= 2)
+            if (c >= q.Cg && q.sw % (8 / c) == 0) {
+                q.Cgp = c;
+                break;
+            }
+    q.tpc = q.Cgp < 8 ? 8 / q.Cgp : 1;
+    q.kwp = round_up(q.kw, q.tpc);
     q.Kgp = round_up(q.Kg, 8);
-    const int khw = q.kh * q.kw;
+    const int khw = q.kh * q.kwp;
     // The staged copies carry the gathers' zero padding as a border: the
     // input's covers every forward tap, the top gradient's every tap of the
     // phase-stacked data-gradient gather (whose padding Th - 1 - a0h may be
     // negative: then the gather starts doh0 rows into the grid instead).
     q.XHp = std::max(q.ph + q.H, (q.Ho - 1) * q.sh + q.kh);
-    q.XWp = std::max(q.pw + q.W, (q.Wo - 1) * q.sw + q.kw);
+    q.XWp = round_up(std::max(q.pw + q.W, (q.Wo - 1) * q.sw + q.kwp), q.tpc);
     const int php = q.Th - 1 - q.a0h, pwp = q.Tw - 1 - q.a0w;
     q.dtb = std::max(php, 0);
     q.dlb = std::max(pwp, 0);
@@ -801,8 +817,8 @@ int run_forward_bf16(const ConvPlan& q, const void* bottom, const void* weight, 
     LAUNCH(launch_stage_nhwc_bf16((const uint16_t*)bottom, xh, q.N, q.C, q.H, q.W, q.Cg, q.Cgp,
                                   Ctot, q.XHp, q.XWp, q.ph, q.pw, s),
            "bf16 staging launch");
-    LAUNCH(launch_pack_weights_bf16((const uint16_t*)weight, wp, q.K, q.Cg, q.Cgp, q.kh * q.kw,
-                                    q.Rp, s),
+    LAUNCH(launch_pack_weights_bf16((const uint16_t*)weight, wp, q.K, q.Cg, q.Cgp, q.kh, q.kw,
+                                    q.kwp, q.Rp, s),
            "bf16 weight pack launch");
     GemmBf16Params p = {};
     p.A = wp;
@@ -813,9 +829,13 @@ int run_forward_bf16(const ConvPlan& q, const void* bottom, const void* weight, 
     p.X_bytes = nbytes((int64_t)q.N * q.XHp * q.XWp * Ctot, 2);
     p.Y_bytes = nbytes(q.top_elems, 4);
     p.N = q.N; p.IHp = q.XHp; p.IWp = q.XWp; p.Ctot = Ctot; p.Cgp = q.Cgp;
-    p.Cg8 = q.Cgp / 8; p.KC = q.kh * q.kw * p.Cg8;
-    p.div_cg8 = make_fastdiv((uint32_t)p.Cg8); p.div_kw = make_fastdiv((uint32_t)q.kw);
-    p.kh = q.kh; p.kw = q.kw; p.sh = q.sh; p.sw = q.sw; p.oh0 = 0; p.ow0 = 0;
+    // chunks per tap group, tap groups per kernel row, elements per tap group
+    p.Cg8 = q.Cgp >= 8 ? q.Cgp / 8 : 1;
+    p.kw = q.kwp / q.tpc;
+    p.vstr = q.Cgp >= 8 ? Ctot : 8;
+    p.KC = q.kh * p.kw * p.Cg8;
+    p.div_cg8 = make_fastdiv((uint32_t)p.Cg8); p.div_kw = make_fastdiv((uint32_t)p.kw);
+    p.kh = q.kh; p.sh = q.sh; p.sw = q.sw; p.oh0 = 0; p.ow0 = 0;
     p.OH = q.Ho; p.OW = q.Wo;
     p.M = q.Kg; p.Rp = q.Rp; p.G = q.G;
     p.Ncol = q.N * q.Ho * q.Wo;
@@ -845,7 +865,7 @@ int run_data_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom_mask
     p.X_bytes = nbytes((int64_t)q.N * q.DHp * q.DWp * Ktot, 2);
     p.Y_bytes = nbytes(q.bottom_elems, 4);
     p.N = q.N; p.IHp = q.DHp; p.IWp = q.DWp; p.Ctot = Ktot; p.Cgp = q.Kgp;
-    p.Cg8 = q.Kgp / 8; p.KC = q.Th * q.Tw * p.Cg8;
+    p.Cg8 = q.Kgp / 8; p.KC = q.Th * q.Tw * p.Cg8; p.vstr = Ktot;
     p.div_cg8 = make_fastdiv((uint32_t)p.Cg8); p.div_kw = make_fastdiv((uint32_t)q.Tw);
     p.kh = q.Th; p.kw = q.Tw; p.sh = 1; p.sw = 1; p.oh0 = q.doh0; p.ow0 = q.dow0;
     p.OH = q.Ah; p.OW = q.Aw;
@@ -879,7 +899,7 @@ int run_weights_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom,
     p.N = q.N; p.IHp = q.XHp; p.IWp = q.XWp; p.Ctot = Ctot; p.Cgp = q.Cgp;
     p.K = q.K; p.Kg = q.Kg; p.Kgp = q.Kgp; p.Ktot = q.G * q.Kgp;
     p.DHp = q.DHp; p.DWp = q.DWp; p.dtb = q.dtb; p.dlb = q.dlb;
-    p.kh = q.kh; p.kw = q.kw; p.sh = q.sh; p.sw = q.sw;
+    p.kh = q.kh; p.kw = q.kwp; p.sh = q.sh; p.sw = q.sw;
     p.OH = q.Ho; p.OW = q.Wo;
     p.Rw = q.Rw; p.G = q.G;
     p.Ncol = q.N * q.Ho * q.Wo;
@@ -888,7 +908,7 @@ int run_weights_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom,
     p.div_ohw = make_fastdiv((uint32_t)(q.Ho * q.Wo));
     p.div_ow = make_fastdiv((uint32_t)q.Wo);
     LAUNCH(launch_conv_wgrad_bf16(p, q.wgrad_tile, s), "bf16 weight-gradient launch");
-    LAUNCH(launch_wgrad_reduce_perm(part, weight_diff, q.K, q.Rw, q.Cgp, q.Cg, q.kh * q.kw,
+    LAUNCH(launch_wgrad_reduce_perm(part, weight_diff, q.K, q.Rw, q.Cgp, q.Cg, q.kh, q.kw, q.kwp,
                                     q.splits, accumulate, s),
            "bf16 reduce launch");
     return CAFFE_OK;

@@ -80,10 +80,10 @@ struct MfmaBf16<16> {
 // whether the LDS serves 8 or 16 lanes of 16 bytes per cycle.
 //
 // A rows are contiguous in global memory.  A B row is one output column:
-// its chunk kc sits at tap (u, v) = (kc / Cg8 / kw, kc / Cg8 % kw), channels
-// 8*(kc % Cg8) .. +7, at a byte offset from the column's pixel that does not
-// depend on the column, so each lane walks its one chunk index per stage and
-// adds the offset to the pixel base of each of its columns.  Past the last
+// its chunk kc = (u, vg, c8) sits at a byte offset from the column's pixel
+// that does not depend on the column (see GemmBf16Params), so each lane
+// walks its one chunk index per stage and adds the offset to the pixel base
+// of each of its columns.  Past the last
 // chunk the offset is out of range (the copy lands zeros).  Columns past
 // Ncol re-read the last column; their results are never stored.
 __device__ __forceinline__ void copy16_lds(__amdgpu_buffer_rsrc_t r, u32x4* dst, uint32_t voff,
@@ -199,11 +199,11 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
     // byte offset of this lane's chunk of stage t from a column's pixel
     auto b_delta = [&](int t) -> uint32_t {
         const int kc = t * CH + ck;
-        const int tap = (int)fdiv((uint32_t)kc, p.div_cg8);
-        const int c8 = kc - tap * p.Cg8;
-        const int u = (int)fdiv((uint32_t)tap, p.div_kw);
-        const int v = tap - u * p.kw;
-        const uint32_t d = (uint32_t)((u * p.IWp + v) * p.Ctot + 8 * c8) * 2u;
+        const int tg = (int)fdiv((uint32_t)kc, p.div_cg8);
+        const int c8 = kc - tg * p.Cg8;
+        const int u = (int)fdiv((uint32_t)tg, p.div_kw);
+        const int vg = tg - u * p.kw;
+        const uint32_t d = (uint32_t)(u * p.IWp * p.Ctot + vg * p.vstr + 8 * c8) * 2u;
         return kc < p.KC ? d : kOob;
     };
     // The copies of one stage, NA + NB per wave, go out in KS parts, one
@@ -670,15 +670,15 @@ conv_wgrad_bf16_kernel(const WgradBf16Params p)
     }
 }
 
-// dW[k][c][t] = (accumulate ? dW : 0) + sum_s P[s][k][t*Cgp + c]  (c < Cg, t < khw):
-// the split partials added in a fixed order, as wgrad_reduce_kernel does, with
-// lanes along the partials' (u, v, c) order.
+// dW[k][c][u][v] = (accumulate ? dW : 0) + sum_s P[s][k][(u*kwp + v)*Cgp + c]
+// (c < Cg, u < kh, v < kw): the split partials added in a fixed order, as
+// wgrad_reduce_kernel does, with lanes along the partials' (u, v, c) order.
 constexpr int kPermParts = 8;
 constexpr int kPermCols = 32;
 
 __global__ void __launch_bounds__(kPermParts * kPermCols)
 wgrad_reduce_perm_kernel(const float* __restrict__ P, float* __restrict__ dW, int K, int Rw,
-                         int Cgp, int Cg, int khw, int splits, int accumulate)
+                         int Cgp, int Cg, int kh, int kw, int kwp, int splits, int accumulate)
 {
     __shared__ float part[kPermParts][kPermCols + 1];
     const int col = threadIdx.x % kPermCols;
@@ -712,8 +712,10 @@ wgrad_reduce_perm_kernel(const float* __restrict__ P, float* __restrict__ dW, in
         const int r = e - k * Rw;
         const int tap = r / Cgp;
         const int c = r - tap * Cgp;
-        if (c < Cg && tap < khw) {
-            float* o = dW + ((size_t)k * Cg + c) * khw + tap;
+        const int u = tap / kwp;
+        const int v = tap - u * kwp;
+        if (c < Cg && u < kh && v < kw) {
+            float* o = dW + (((size_t)k * Cg + c) * kh + u) * kw + v;
             *o = accumulate ? *o + t : t;
         }
     }
@@ -786,6 +788,44 @@ stage_nhwc_bf16_kernel(const bf16_t* __restrict__ X, bf16_t* __restrict__ Xp, in
                        ((uint32_t)tile[8 * c8 + 2 * k + 1][pl] << 16);
             *(u32x4*)&Xp[((size_t)n * HWp + pw) * Ctot + cp] = v;
         }
+    }
+}
+
+// NCHW bf16 -> zero-bordered pixel-interleaved bf16 for one group of Cgp = 1,
+// 2 or 4 channels (c < Cg real, the rest 0): thread q writes the 16-byte
+// chunk of padded pixels TPC*q .. TPC*q + TPC - 1 (TPC = 8 / Cgp; Hp*Wp is a
+// multiple of TPC), its lanes reading consecutive pixel groups of each plane.
+template <int CGP>
+__global__ void __launch_bounds__(256)
+stage_narrow_bf16_kernel(const bf16_t* __restrict__ X, bf16_t* __restrict__ Xp, int N, int Cg,
+                         int H, int W, int Hp, int Wp, int tb, int lb)
+{
+    constexpr int TPC = 8 / CGP;
+    const int HWp = Hp * Wp;
+    const int per_image = HWp / TPC;
+    const long total = (long)N * per_image;
+    for (long q = blockIdx.x * (long)blockDim.x + threadIdx.x; q < total;
+         q += (long)gridDim.x * blockDim.x) {
+        const int n = (int)(q / per_image);
+        const int p0 = (int)(q - (long)n * per_image) * TPC;
+        uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int t = 0; t < TPC; ++t) {
+            const int pix = p0 + t;
+            const int hp = pix / Wp;
+            const int h = hp - tb;
+            const int x = pix - hp * Wp - lb;
+            const bool inside = (unsigned)h < (unsigned)H && (unsigned)x < (unsigned)W;
+#pragma unroll
+            for (int c = 0; c < CGP; ++c) {
+                bf16_t v = 0;
+                if (inside && c < Cg)
+                    v = X[(((size_t)n * Cg + c) * H + h) * W + x];
+                const int e = t * CGP + c;  // element of the chunk
+                w[e >> 1] |= (uint32_t)v << (16 * (e & 1));
+            }
+        }
+        *(u32x4*)&Xp[(size_t)q * 8] = u32x4{w[0], w[1], w[2], w[3]};
     }
 }
 
@@ -882,11 +922,11 @@ bias_reduce_kernel(const float* __restrict__ sums, float* __restrict__ db, int T
         db[k] = accumulate ? db[k] + red[0] : red[0];
 }
 
-// Forward weights: Wp[o][(u*kw + v)*Cgp + c] = W[o][c][u][v], zero for c >= Cg
-// and for r >= khw*Cgp (rows padded to Rp).
+// Forward weights: Wp[o][(u*kwp + v)*Cgp + c] = W[o][c][u][v], zero for
+// c >= Cg, v >= kw and r >= kh*kwp*Cgp (rows padded to Rp).
 __global__ void __launch_bounds__(256)
 pack_weights_bf16_kernel(const bf16_t* __restrict__ W, bf16_t* __restrict__ Wp, int K, int Cg,
-                         int Cgp, int khw, int Rp)
+                         int Cgp, int kh, int kw, int kwp, int Rp)
 {
     const long total = (long)K * Rp;
     for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < total;
@@ -895,10 +935,12 @@ pack_weights_bf16_kernel(const bf16_t* __restrict__ W, bf16_t* __restrict__ Wp, 
         const int r = (int)(e - (long)o * Rp);
         const int t = r / Cgp;
         const int c = r - t * Cgp;
-        bf16_t v = 0;
-        if (t < khw && c < Cg)
-            v = W[((long)o * Cg + c) * khw + t];
-        Wp[e] = v;
+        const int u = t / kwp;
+        const int v = t - u * kwp;
+        bf16_t x = 0;
+        if (u < kh && v < kw && c < Cg)
+            x = W[(((long)o * Cg + c) * kh + u) * kw + v];
+        Wp[e] = x;
     }
 }
 
@@ -1018,8 +1060,11 @@ hipError_t launch_conv_gemm_bf16(const GemmBf16Params& p, int epi, int tile, int
 {
     if (p.Ncol == 0)
         return hipSuccess;
-    if (p.Rp % kBf16TK != 0 || p.Cgp % 8 != 0 || p.Ctot % 8 != 0 || p.Cg8 * 8 != p.Cgp ||
-        p.KC * 8 > p.Rp || p.KC != p.kh * p.kw * p.Cg8)
+    const bool wide = p.Cgp % 8 == 0 && p.Ctot % 8 == 0 && p.Cg8 * 8 == p.Cgp && p.vstr == p.Ctot;
+    const bool narrow = (p.Cgp == 1 || p.Cgp == 2 || p.Cgp == 4) && p.Ctot == p.Cgp && p.G == 1 &&
+                        p.Cg8 == 1 && p.vstr == 8;
+    if (p.Rp % kBf16TK != 0 || !(wide || narrow) || p.KC * 8 > p.Rp ||
+        p.KC != p.kh * p.kw * p.Cg8)
         return hipErrorInvalidValue;
     if (epi == 0)
         return launch_gemm_pipe<0, false>(p, tile, pipe, s);
@@ -1031,7 +1076,8 @@ int bf16_wgrad_tile_m(int tile) { return tile == BWTILE_96x256 ? 96 : 128; }
 
 hipError_t launch_conv_wgrad_bf16(const WgradBf16Params& p, int tile, hipStream_t s)
 {
-    if (p.Cgp % 8 != 0 || p.Kgp % 8 != 0 || p.cols_per_split % kBf16WgradTK != 0)
+    const bool narrow = (p.Cgp == 1 || p.Cgp == 2 || p.Cgp == 4) && p.Ctot == p.Cgp && p.G == 1;
+    if ((p.Cgp % 8 != 0 && !narrow) || p.Kgp % 8 != 0 || p.cols_per_split % kBf16WgradTK != 0)
         return hipErrorInvalidValue;
     switch (tile) {
     case BWTILE_128x256:
@@ -1044,14 +1090,15 @@ hipError_t launch_conv_wgrad_bf16(const WgradBf16Params& p, int tile, hipStream_
 }
 
 hipError_t launch_wgrad_reduce_perm(const float* P, float* dW, int K, int Rw, int Cgp, int Cg,
-                                    int khw, int splits, int accumulate, hipStream_t s)
+                                    int kh, int kw, int kwp, int splits, int accumulate,
+                                    hipStream_t s)
 {
     const int count = K * Rw;
     if (count == 0)
         return hipSuccess;
     hipLaunchKernelGGL(wgrad_reduce_perm_kernel, dim3((count + kPermCols - 1) / kPermCols),
-                       dim3(kPermParts * kPermCols), 0, s, P, dW, K, Rw, Cgp, Cg, khw, splits,
-                       accumulate);
+                       dim3(kPermParts * kPermCols), 0, s, P, dW, K, Rw, Cgp, Cg, kh, kw, kwp,
+                       splits, accumulate);
     return hipGetLastError();
 }
 
@@ -1061,6 +1108,20 @@ hipError_t launch_stage_nhwc_bf16(const uint16_t* X, uint16_t* Xp, int N, int C,
 {
     if (N == 0)
         return hipSuccess;
+    if (Ctot < 8) {  // one group of 1, 2 or 4 channels
+        const long chunks = (long)N * Hp * Wp * Ctot / 8;
+        const dim3 grid(grid_1d(chunks));
+        if (Ctot == 4)
+            hipLaunchKernelGGL(stage_narrow_bf16_kernel<4>, grid, dim3(256), 0, s, X, Xp, N, Cg, H,
+                               W, Hp, Wp, tb, lb);
+        else if (Ctot == 2)
+            hipLaunchKernelGGL(stage_narrow_bf16_kernel<2>, grid, dim3(256), 0, s, X, Xp, N, Cg, H,
+                               W, Hp, Wp, tb, lb);
+        else
+            hipLaunchKernelGGL(stage_narrow_bf16_kernel<1>, grid, dim3(256), 0, s, X, Xp, N, Cg, H,
+                               W, Hp, Wp, tb, lb);
+        return hipGetLastError();
+    }
     const int ct = Ctot <= 8 ? 8 : Ctot <= 16 ? 16 : Ctot <= 32 ? 32 : 64;
     const int pt = ct == 8 ? stage_tile_pixels<8>() : ct == 16 ? stage_tile_pixels<16>()
                  : ct == 32 ? stage_tile_pixels<32>() : stage_tile_pixels<64>();
@@ -1114,13 +1175,13 @@ hipError_t launch_bias_reduce(const float* sums, float* db, int T, int K, int ac
 }
 
 hipError_t launch_pack_weights_bf16(const uint16_t* W, uint16_t* Wp, int K, int Cg, int Cgp,
-                                    int khw, int Rp, hipStream_t s)
+                                    int kh, int kw, int kwp, int Rp, hipStream_t s)
 {
     const long total = (long)K * Rp;
     if (total == 0)
         return hipSuccess;
     hipLaunchKernelGGL(pack_weights_bf16_kernel, dim3(grid_1d(total)), dim3(256), 0, s, W, Wp, K,
-                       Cg, Cgp, khw, Rp);
+                       Cg, Cgp, kh, kw, kwp, Rp);
     return hipGetLastError();
 }
 

@@ -171,10 +171,18 @@ enum Bf16Pipe {
 };
 
 // Implicit GEMM over a channel-contiguous, zero-bordered bf16 gather source
-// X[N][IHp][IWp][Ctot] whose group g owns channels g*Cgp .. g*Cgp + Cgp - 1
-// (Cgp a multiple of 8).  The reduction r = (u, v, c) over kh x kw x Cgp
-// runs in 16-byte chunks of 8 channels, KC = kh*kw*Cgp/8 of them; A is
-// [G*M][Rp] bf16 (Rp >= 8*KC a multiple of kBf16TK, zero past 8*KC).
+// X[N][IHp][IWp][Ctot] whose group g owns channels g*Cgp .. g*Cgp + Cgp - 1.
+// The reduction r = (u, v, c) over kh x kwp x Cgp runs in 16-byte chunks of 8
+// consecutive elements, KC = kh * kwg * Cg8 of them:
+//  - Cgp a multiple of 8: a chunk is 8 channels of one tap; Cg8 = Cgp / 8
+//    chunks per tap, kwg = kw taps per kernel row, vstr = Ctot;
+//  - Cgp in {1, 2, 4} (one group, Ctot = Cgp): a chunk is 8 / Cgp
+//    horizontally adjacent taps of all Cgp channels (the staged row is
+//    contiguous along (v, c)); Cg8 = 1, kwg = kwp / (8 / Cgp) tap groups per
+//    kernel row, vstr = 8.
+// Chunk kc = (u, vg, c8) (c8 fastest) lies (u*IWp*Ctot + vg*vstr + 8*c8)
+// elements from its column's pixel.  A is [G*M][Rp] bf16 (Rp >= 8*KC a
+// multiple of kBf16TK, zero past 8*KC and at taps past kw).
 //   C_g[m][col] = sum_r A[g*M + m][r] * X[n][i*sh + oh0 + u][j*sw + ow0 + v][g*Cgp + c]
 // for col = (n, i, j) in N x OH x OW: the borders of X stand for the
 // convolution's zero padding, so every gathered position lies inside it.
@@ -187,8 +195,8 @@ struct GemmBf16Params {
     float* Y;
     const float* bias;
     uint32_t A_bytes, X_bytes, Y_bytes;
-    int N, IHp, IWp, Ctot, Cgp, Cg8, KC;
-    int kh, kw, sh, sw, oh0, ow0;
+    int N, IHp, IWp, Ctot, Cgp, Cg8, KC, vstr;
+    int kh, kw, sh, sw, oh0, ow0;  // kw: tap groups per kernel row (kwg)
     int OH, OW;
     int M, Rp, G, Ncol;
     int relu;
@@ -203,9 +211,10 @@ hipError_t launch_conv_gemm_bf16(const GemmBf16Params& p, int epi, int tile, int
 // Split-K weight gradient over channel-contiguous, zero-bordered bf16
 // operands (D laid out [N][DHp][DWp][Ktot] with the real pixels at offset
 // (dtb, dlb); X as in GemmBf16Params with oh0 = ow0 = 0):
-//   P[s][g*Kg + m][(u*kw + v)*Cgp + c] =
+//   P[s][g*Kg + m][(u*kwp + v)*Cgp + c] =
 //       sum_{col in split s} D[n][i + dtb][j + dlb][g*Kgp + m] * X[n][i*sh + u][j*sw + v][g*Cgp + c]
-// with col = (n, i, j) and Rw = kh*kw*Cgp columns per output channel.
+// with col = (n, i, j) and Rw = kh*kwp*Cgp columns per output channel (kw
+// below holds kwp: kw rounded up to the taps of a chunk).
 struct WgradBf16Params {
     const uint16_t* D;
     const uint16_t* X;
@@ -231,14 +240,16 @@ constexpr int kBf16WgradTN = 256;
 // cols_per_split must be a multiple of kBf16WgradTK
 hipError_t launch_conv_wgrad_bf16(const WgradBf16Params& p, int tile, hipStream_t s);
 
-// dW[k][c][t] = (accumulate ? dW : 0) + sum_s P[s][k][t*Cgp + c] for c < Cg,
-// t < khw (fixed order).
+// dW[k][c][u][v] = (accumulate ? dW : 0) + sum_s P[s][k][(u*kwp + v)*Cgp + c]
+// for c < Cg, u < kh, v < kw (fixed order).
 hipError_t launch_wgrad_reduce_perm(const float* P, float* dW, int K, int Rw, int Cgp, int Cg,
-                                    int khw, int splits, int accumulate, hipStream_t s);
+                                    int kh, int kw, int kwp, int splits, int accumulate,
+                                    hipStream_t s);
 
 // Xp[n][hp][wp][g*Cgp + c] = X[n][g*Cg + c][hp - tb][wp - lb] inside the H x W
 // image (c < Cg), else 0: the zero-bordered channel-contiguous copy, Hp x Wp
-// pixels per image; Ctot = G*Cgp.
+// pixels per image; Ctot = G*Cgp, a multiple of 8, or Cgp in {1, 2, 4} with
+// G = 1 and Hp*Wp a multiple of 8 / Cgp.
 hipError_t launch_stage_nhwc_bf16(const uint16_t* X, uint16_t* Xp, int N, int C, int H, int W,
                                   int Cg, int Cgp, int Ctot, int Hp, int Wp, int tb, int lb,
                                   hipStream_t s);
@@ -256,9 +267,10 @@ hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, f
 hipError_t launch_bias_reduce(const float* sums, float* db, int T, int K, int accumulate,
                               hipStream_t s);
 
-// Wp[o][(u*kw + v)*Cgp + c] = W[o][c][u][v] (0 for c >= Cg and past khw*Cgp).
+// Wp[o][(u*kwp + v)*Cgp + c] = W[o][c][u][v] (0 for c >= Cg, v >= kw and
+// past kh*kwp*Cgp).
 hipError_t launch_pack_weights_bf16(const uint16_t* W, uint16_t* Wp, int K, int Cg, int Cgp,
-                                    int khw, int Rp, hipStream_t s);
+                                    int kh, int kw, int kwp, int Rp, hipStream_t s);
 
 // Wt[g][(c, fh, fw)][(th*Tw + tw)*Kgp + k] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)]
 // (0 past the kernel edge, for k >= Kg and past Th*Tw*Kgp).

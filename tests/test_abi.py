@@ -120,11 +120,15 @@ def test_workspace_sizes():
         desc.relu = 1
 
 def test_workspace_sizes_bf16():
-    # bf16 operands are staged channel-contiguous, each group's channels padded
-    # to a multiple of 8, next to the packed weights (rows padded to 32)
+    # bf16 operands are staged channel-contiguous on a zero-bordered grid next
+    # to the packed weights (rows padded to 64).  A single group of 3 channels
+    # with an even horizontal stride is padded to 4 channels, two taps per
+    # 16-byte chunk: conv1's 11 taps per kernel row round up to 12, its staged
+    # width to 228 (the last tap pair reads one column past the image)
     d = cc.conv_desc((256, 3, 227, 227), (96, 3, 11, 11), 4, 0, 1, True, cc.CAFFE_BF16)
-    xh = 256 * 227 * 227 * 8 * 2
-    assert cc.conv_workspace_size(d, cc.PASS_FORWARD) >= xh + 96 * 992 * 2
+    xh = 256 * 227 * 228 * 4 * 2
+    assert cc.conv_workspace_size(d, cc.PASS_FORWARD) >= xh + 96 * 576 * 2
+    assert cc.conv_workspace_size(d, cc.PASS_FORWARD) < 256 * 227 * 227 * 8 * 2
     dh = 256 * 55 * 55 * 96 * 2
     both = cc.conv_workspace_size(d, cc.PASS_BACKWARD)
     assert both >= dh + xh

@@ -90,6 +90,17 @@ def test_tile_shapes_each_chooser_branch_bf16():
         run_case(2, C, 29, 31, 6, k, k, s, s, 1, 2, 1, True)
 
 
+def test_narrow_channel_packing_bf16():
+    # one group of at most 4 channels staged as Cgp = 1, 2 or 4 channels with
+    # 8 / Cgp taps per 16-byte chunk when the horizontal stride allows it
+    # (kernel widths that are not multiples of the taps per chunk, vertical
+    # strides that differ from the horizontal one); 3 channels with an odd
+    # horizontal stride keep 8-channel chunks
+    for C, sh, sw, kh, kw in [(3, 4, 4, 11, 11), (4, 1, 2, 3, 3), (2, 3, 4, 5, 7),
+                              (1, 2, 8, 4, 9), (3, 2, 1, 5, 5), (2, 1, 2, 1, 1)]:
+        run_case(2, C, 23, 37, 10, kh, kw, sh, sw, 1, 2, 1, True)
+
+
 def test_channel_padding_and_long_reductions_bf16():
     # channels per group that are not multiples of 8 (zero padding), and
     # channel counts spanning several 32-deep stages per tap

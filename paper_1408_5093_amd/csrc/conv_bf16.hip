@@ -761,17 +761,19 @@ stage_nhwc_bf16_kernel(const bf16_t* __restrict__ X, bf16_t* __restrict__ Xp, in
     const int w = pix - hp * Wp - lb;
     const bool inside = pix < HWp && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
     const size_t src = (size_t)n * C * H * W + (size_t)h * W + w;
-#pragma unroll 4
+    // all of the thread's loads are issued before the first LDS store
+    bf16_t v[NQ];
+#pragma unroll
     for (int q = 0; q < NQ; ++q) {
         const int c = (tid + 256 * q) / PT;
         const int cp = c0 + c;
         const int g = cp / Cgp;
         const int cl = cp - g * Cgp;
-        bf16_t v = 0;
-        if (inside && cp < Ctot && cl < Cg)
-            v = X[src + (size_t)(g * Cg + cl) * H * W];
-        tile[c][px] = v;
+        v[q] = inside && cp < Ctot && cl < Cg ? X[src + (size_t)(g * Cg + cl) * H * W] : 0;
     }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+        tile[(tid + 256 * q) / PT][px] = v[q];
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < NW; ++q) {
@@ -859,24 +861,29 @@ diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
     const bool inside = pix < HWp && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
     const size_t plane = (size_t)H * W;
     const size_t src = (size_t)n * K * plane + (size_t)h * W + w;
-#pragma unroll 4
+    // all loads first (the wave sums below would otherwise wait on each)
+    float d[16];
+#pragma unroll
     for (int q = 0; q < 16; ++q) {
-        const int cl = cw + 4 * q;
-        const int cp = c0 + cl;
+        const int cp = c0 + cw + 4 * q;
         const int g = cp / Kgp;
         const int k = cp - g * Kgp;
-        const bool ok = cp < Ktot && k < Kg;
-        float d = 0.f;
-        if (ok && inside) {
-            const size_t idx = src + (size_t)(g * Kg + k) * plane;
-            d = G[idx];
-            if (relu && !(Y[idx] > 0.f))
-                d = 0.f;
-        }
-        tile[cl][px] = f32_to_bf16_rne(d);
+        const bool ok = cp < Ktot && k < Kg && inside;
+        const size_t idx = src + (size_t)(g * Kg + k) * plane;
+        d[q] = ok ? G[idx] : 0.f;
+        if (relu && ok && !(Y[idx] > 0.f))
+            d[q] = 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+        const int cl = cw + 4 * q;
+        tile[cl][px] = f32_to_bf16_rne(d[q]);
         if (sums) {
-            const float sm = wave_sum(d);
-            if (px == 0 && ok)
+            const int cp = c0 + cl;
+            const int g = cp / Kgp;
+            const int k = cp - g * Kgp;
+            const float sm = wave_sum(d[q]);
+            if (px == 0 && cp < Ktot && k < Kg)
                 sums[(size_t)(g * Kg + k) * T + n * ptiles + pt] = sm;
         }
     }

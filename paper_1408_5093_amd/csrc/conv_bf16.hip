@@ -832,76 +832,90 @@ stage_narrow_bf16_kernel(const bf16_t* __restrict__ X, bf16_t* __restrict__ Xp, 
 }
 
 // Top-gradient staging: Dh = bf16(relu ? G [Y > 0] : G) channel-contiguous on
-// the zero-bordered Hp x Wp grid, one block per (image, 64 padded channels,
-// 64 bordered pixels).  Each wave also sums the fp32 masked gradient of its
-// channels over the block's pixels (a fixed butterfly; the border adds 0)
-// into sums[(g*Kg + k) * T + n * ptiles + pt]: the bias-gradient partials,
-// T = N * ptiles per channel.
+// the zero-bordered Hp x Wp grid, one block per (image, 64 padded channels)
+// walking the image's bordered pixels 64 at a time.  Each thread also adds up
+// the fp32 masked gradient of its 16 channels at its pixels; one wave sum per
+// channel at the end (a fixed butterfly after a fixed per-lane order; the
+// border adds 0) gives sums[(g*Kg + k) * N + n], the image's bias-gradient
+// partial.
 __global__ void __launch_bounds__(256)
 diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
-                      bf16_t* __restrict__ Dh, float* __restrict__ sums, int K, int H, int W,
-                      int Kg, int Kgp, int Ktot, int Hp, int Wp, int tb, int lb, int relu,
-                      int ptiles, int ctiles, int T)
+                      bf16_t* __restrict__ Dh, float* __restrict__ sums, int N, int K, int H,
+                      int W, int Kg, int Kgp, int Ktot, int Hp, int Wp, int tb, int lb, int relu,
+                      int ctiles)
 {
     __shared__ bf16_t tile[64][66];
-    const int n = blockIdx.x / (ptiles * ctiles);
-    const int rem = blockIdx.x - n * ptiles * ctiles;
-    const int ct = rem / ptiles;
-    const int pt = rem - ct * ptiles;
-    const int c0 = ct * 64;
-    const int p0 = pt * 64;
+    const int n = blockIdx.x / ctiles;
+    const int c0 = (blockIdx.x - n * ctiles) * 64;
     const int HWp = Hp * Wp;
     const int tid = threadIdx.x;
     const int px = tid & 63;
     const int cw = tid >> 6;
-    const int pix = p0 + px;
-    const int hp = pix / Wp;
-    const int h = hp - tb;
-    const int w = pix - hp * Wp - lb;
-    const bool inside = pix < HWp && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
     const size_t plane = (size_t)H * W;
-    const size_t src = (size_t)n * K * plane + (size_t)h * W + w;
-    // all loads first (the wave sums below would otherwise wait on each)
-    float d[16];
+    // this thread's 16 channels (cw + 4q) and whether they exist
+    size_t cbase[16];
+    bool cok[16];
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
         const int cp = c0 + cw + 4 * q;
         const int g = cp / Kgp;
         const int k = cp - g * Kgp;
-        const bool ok = cp < Ktot && k < Kg && inside;
-        const size_t idx = src + (size_t)(g * Kg + k) * plane;
-        d[q] = ok ? G[idx] : 0.f;
-        if (relu && ok && !(Y[idx] > 0.f))
-            d[q] = 0.f;
+        cok[q] = cp < Ktot && k < Kg;
+        cbase[q] = ((size_t)n * K + g * Kg + k) * plane;
     }
+    float acc[16];
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-        const int cl = cw + 4 * q;
-        tile[cl][px] = f32_to_bf16_rne(d[q]);
-        if (sums) {
-            const int cp = c0 + cl;
-            const int g = cp / Kgp;
-            const int k = cp - g * Kgp;
-            const float sm = wave_sum(d[q]);
-            if (px == 0 && cp < Ktot && k < Kg)
-                sums[(size_t)(g * Kg + k) * T + n * ptiles + pt] = sm;
+    for (int q = 0; q < 16; ++q)
+        acc[q] = 0.f;
+    for (int p0 = 0; p0 < HWp; p0 += 64) {
+        const int pix = p0 + px;
+        const int hp = pix / Wp;
+        const int h = hp - tb;
+        const int w = pix - hp * Wp - lb;
+        const bool inside = pix < HWp && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+        const size_t off = (size_t)h * W + w;
+        // all loads first, then the conversions
+        float d[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            const bool ok = cok[q] && inside;
+            d[q] = ok ? G[cbase[q] + off] : 0.f;
+            if (relu && ok && !(Y[cbase[q] + off] > 0.f))
+                d[q] = 0.f;
         }
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            acc[q] += d[q];
+            tile[cw + 4 * q][px] = f32_to_bf16_rne(d[q]);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const int id = tid + 256 * q;
+            const int pl = id >> 3;
+            const int c8 = id & 7;
+            const int pw = p0 + pl;
+            const int cp = c0 + 8 * c8;
+            if (pw < HWp && cp < Ktot) {
+                u32x4 v;
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    v[k] = (uint32_t)tile[8 * c8 + 2 * k][pl] |
+                           ((uint32_t)tile[8 * c8 + 2 * k + 1][pl] << 16);
+                *(u32x4*)&Dh[((size_t)n * HWp + pw) * Ktot + cp] = v;
+            }
+        }
+        __syncthreads();
     }
-    __syncthreads();
+    if (sums) {
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-        const int id = tid + 256 * q;
-        const int pl = id >> 3;
-        const int c8 = id & 7;
-        const int pw = p0 + pl;
-        const int cp = c0 + 8 * c8;
-        if (pw < HWp && cp < Ktot) {
-            u32x4 v;
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-                v[k] = (uint32_t)tile[8 * c8 + 2 * k][pl] |
-                       ((uint32_t)tile[8 * c8 + 2 * k + 1][pl] << 16);
-            *(u32x4*)&Dh[((size_t)n * HWp + pw) * Ktot + cp] = v;
+        for (int q = 0; q < 16; ++q) {
+            const float sm = wave_sum(acc[q]);
+            if (px == 0 && cok[q]) {
+                const int cp = c0 + cw + 4 * q;
+                const int g = cp / Kgp;
+                sums[(size_t)(g * Kg + cp - g * Kgp) * N + n] = sm;
+            }
         }
     }
 }
@@ -1156,7 +1170,7 @@ hipError_t launch_stage_nhwc_bf16(const uint16_t* X, uint16_t* Xp, int N, int C,
     return hipGetLastError();
 }
 
-int diff_prep_terms(int N, int HWp) { return N * ((HWp + 63) / 64); }
+int diff_prep_terms(int N, int /*HWp*/) { return N; }
 
 hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, float* sums, int N,
                                  int K, int H, int W, int Kg, int Kgp, int Ktot, int Hp, int Wp,
@@ -1164,11 +1178,9 @@ hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, f
 {
     if (N == 0)
         return hipSuccess;
-    const int ptiles = (Hp * Wp + 63) / 64;
     const int ctiles = (Ktot + 63) / 64;
-    hipLaunchKernelGGL(diff_prep_bf16_kernel, dim3((unsigned)((int64_t)ptiles * ctiles * N)),
-                       dim3(256), 0, s, G, Y, Dh, sums, K, H, W, Kg, Kgp, Ktot, Hp, Wp, tb, lb,
-                       relu, ptiles, ctiles, N * ptiles);
+    hipLaunchKernelGGL(diff_prep_bf16_kernel, dim3((unsigned)((int64_t)ctiles * N)), dim3(256), 0,
+                       s, G, Y, Dh, sums, N, K, H, W, Kg, Kgp, Ktot, Hp, Wp, tb, lb, relu, ctiles);
     return hipGetLastError();
 }
 

@@ -389,8 +389,13 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
             wb[ni] = p.psw * (b + p.a0w) - p.opw;
             cb[ni] = (n * p.Cout + g * p.Cg_out) * OutHW;
         }
+        // per MT-row block: every position (and, masked, every bf16 bottom
+        // value) first, then the stores (a load after a store to another
+        // buffer could not be moved above it, so each would wait alone)
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
+            uint32_t off[Op::kRegs][NI];
+            float y[Op::kRegs][NI];
 #pragma unroll
             for (int q = 0; q < Op::kRegs; ++q) {
                 const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
@@ -410,16 +415,23 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
                                           (uint32_t)((unsigned)w >= (unsigned)p.OutW))
                                          << 31;
                     const uint32_t idx = (uint32_t)(cb[ni] + c * OutHW + h * p.OutW + w);
-                    float v = acc[mi][ni][q];
-                    if constexpr (MASK) {
-                        // backward of the ReLU whose (bf16) output is this
-                        // layer's bottom: keep the gradient where it was > 0
-                        const float y = bf16_to_f32(buf_ld_u16(rom, (idx * 2u) | bad));
-                        v = y > 0.f ? v : 0.f;
-                    }
-                    buf_st_f32(v, ry, (idx * 4u) | bad);
+                    off[q][ni] = idx | bad;
+                    // backward of the ReLU whose (bf16) output is this
+                    // layer's bottom: keep the gradient where it was > 0
+                    if constexpr (MASK)
+                        y[q][ni] = bf16_to_f32(buf_ld_u16(rom, (idx * 2u) | bad));
                 }
             }
+#pragma unroll
+            for (int q = 0; q < Op::kRegs; ++q)
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni) {
+                    float v = acc[mi][ni][q];
+                    if constexpr (MASK)
+                        v = y[q][ni] > 0.f ? v : 0.f;
+                    const uint32_t o = off[q][ni];
+                    buf_st_f32(v, ry, ((o & ~kOob) * 4u) | (o & kOob));
+                }
         }
     }
 }

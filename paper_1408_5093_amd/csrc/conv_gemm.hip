@@ -502,8 +502,14 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
             wb[ni] = p.psw * (b + p.a0w) - p.opw;
             cb[ni] = (n * p.Cout + g * p.Cg_out) * OutHW;
         }
+        // per MT-row block: every position (and, masked, every value of the
+        // ReLU output) first, then the stores (a load after a store to
+        // another buffer could not be moved above it, so each would wait
+        // alone)
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
+            uint32_t off[Op::kRegs][NI];
+            float y[Op::kRegs][NI];
 #pragma unroll
             for (int q = 0; q < Op::kRegs; ++q) {
                 const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
@@ -522,18 +528,22 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
                                           (uint32_t)((unsigned)h >= (unsigned)p.OutH) |
                                           (uint32_t)((unsigned)w >= (unsigned)p.OutW))
                                          << 31;
-                    const uint32_t off =
-                        ((uint32_t)(cb[ni] + c * OutHW + h * p.OutW + w) * 4u) | bad;
-                    float v = acc[mi][ni][q];
-                    if constexpr (MASK) {
-                        // backward of the ReLU that produced the gather target:
-                        // keep the gradient only where that output was > 0
-                        const float y = buf_ld_f32(rom, off);
-                        v = y > 0.f ? v : 0.f;
-                    }
-                    buf_st_f32(v, ry, off);
+                    off[q][ni] = ((uint32_t)(cb[ni] + c * OutHW + h * p.OutW + w) * 4u) | bad;
+                    // backward of the ReLU that produced the gather target:
+                    // keep the gradient only where that output was > 0
+                    if constexpr (MASK)
+                        y[q][ni] = buf_ld_f32(rom, off[q][ni]);
                 }
             }
+#pragma unroll
+            for (int q = 0; q < Op::kRegs; ++q)
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni) {
+                    float v = acc[mi][ni][q];
+                    if constexpr (MASK)
+                        v = y[q][ni] > 0.f ? v : 0.f;
+                    buf_st_f32(v, ry, off[q][ni]);
+                }
         }
     }
 }

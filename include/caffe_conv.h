@@ -138,7 +138,17 @@ enum caffe_backward_flags {
      * a ReLU whose output is this layer's bottom, fused into the data
      * gradient.  Needs bottom (in CAFFE_BF16 mode the mask is taken from
      * the bf16 bottom). */
-    CAFFE_BACKWARD_MASK_BOTTOM_DIFF = 2
+    CAFFE_BACKWARD_MASK_BOTTOM_DIFF = 2,
+    /* CAFFE_BF16 mode: the workspace still holds the staged copy of bottom
+     * written by the last caffe_conv_forward call with the same descriptor,
+     * bottom and workspace, and none of them has changed since (the
+     * training-step order: forward, then backward on a workspace of its
+     * own).  The weight gradient then reads that copy instead of staging
+     * bottom again; the staged copy sits at the start of both passes'
+     * workspaces.  No effect in CAFFE_F32 mode, which stages nothing; a
+     * workspace that does not hold the forward's copy gives a wrong
+     * weight gradient. */
+    CAFFE_BACKWARD_BOTTOM_STAGED = 4
 };
 
 /* The whole backward pass of the layer in one call: the ReLU mask is applied

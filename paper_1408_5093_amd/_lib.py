@@ -22,6 +22,7 @@ CAFFE_BF16 = 1
 
 BACKWARD_TOP_DIFF_MASKED = 1
 BACKWARD_MASK_BOTTOM_DIFF = 2
+BACKWARD_BOTTOM_STAGED = 4
 POOL_RELU_INPUT = 1
 
 PASS_FORWARD = 0

@@ -75,7 +75,8 @@ struct ConvPlan {
     int XHp, XWp, DHp, DWp, dtb, dlb, doh0, dow0;
     int fwd_pipe, dgrad_pipe;       // bf16 GEMM pipelines (Bf16Pipe)
     size_t off_xh_fwd, off_wp_fwd;  // forward: [Xh][Wp]
-    size_t off_dh, off_xh;          // backward: [Dh][Xh][sums][Wt][partials]
+    size_t off_dh, off_xh;          // backward: [Xh][Dh][sums][Wt][partials] (Xh where the
+                                    // forward left it)
     // inner-product shape (1x1 kernel on 1x1 spatial, one group, fp32): dense
     // split-K GEMMs with rows = samples (forward, data gradient) or outputs
     // (weight gradient)
@@ -335,9 +336,9 @@ int plan_bf16(ConvPlan* p)
     const size_t sums_bytes = align_up((size_t)terms * q.K * 4, kWsAlign);
     if ((int64_t)sums_bytes > kMaxTensorBytes)
         return fail(CAFFE_ERR_UNSUPPORTED, "bias partials reach 2^31 bytes");
-    q.off_dh = 0;
-    q.off_xh = align_up(dh, kWsAlign);
-    q.off_sums = q.off_xh + align_up(xh, kWsAlign);
+    q.off_xh = 0;
+    q.off_dh = align_up(xh, kWsAlign);
+    q.off_sums = q.off_dh + align_up(dh, kWsAlign);
     q.off_wt = q.off_sums + sums_bytes;
     q.off_part = q.off_wt + align_up(wt, kWsAlign);
     q.ws_data = q.off_part;
@@ -880,15 +881,16 @@ int run_data_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom_mask
     return CAFFE_OK;
 }
 
-int run_weights_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom,
+int run_weights_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom, bool staged,
                      float* weight_diff, int accumulate, char* ws, hipStream_t s)
 {
     uint16_t* xh = (uint16_t*)(ws + q.off_xh);
     float* part = (float*)(ws + q.off_part);
     const int Ctot = q.G * q.Cgp;
-    LAUNCH(launch_stage_nhwc_bf16((const uint16_t*)bottom, xh, q.N, q.C, q.H, q.W, q.Cg, q.Cgp,
-                                  Ctot, q.XHp, q.XWp, q.ph, q.pw, s),
-           "bf16 staging launch");
+    if (!staged)
+        LAUNCH(launch_stage_nhwc_bf16((const uint16_t*)bottom, xh, q.N, q.C, q.H, q.W, q.Cg,
+                                      q.Cgp, Ctot, q.XHp, q.XWp, q.ph, q.pw, s),
+               "bf16 staging launch");
     WgradBf16Params p = {};
     p.D = dh;
     p.X = xh;
@@ -915,8 +917,9 @@ int run_weights_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom,
 }
 
 int backward_bf16(const ConvPlan& q, const float* top_diff, const float* top, bool masked,
-                  bool mask_bottom, const void* bottom, const void* weight, float* bottom_diff,
-                  float* weight_diff, float* bias_diff, int accumulate, char* ws, hipStream_t s)
+                  bool mask_bottom, bool staged, const void* bottom, const void* weight,
+                  float* bottom_diff, float* weight_diff, float* bias_diff, int accumulate,
+                  char* ws, hipStream_t s)
 {
     if (!bottom_diff && !weight_diff) {
         if (bias_diff)
@@ -934,7 +937,7 @@ int backward_bf16(const ConvPlan& q, const float* top_diff, const float* top, bo
     if (bottom_diff)
         CHECK(run_data_bf16(q, dh, mask_bottom ? bottom : nullptr, weight, bottom_diff, ws, s));
     if (weight_diff)
-        CHECK(run_weights_bf16(q, dh, bottom, weight_diff, accumulate, ws, s));
+        CHECK(run_weights_bf16(q, dh, bottom, staged, weight_diff, accumulate, ws, s));
     if (bias_diff)
         LAUNCH(launch_bias_reduce(sums, bias_diff, diff_prep_terms(q.N, q.DHp * q.DWp), q.K,
                                   accumulate, s),
@@ -1017,8 +1020,10 @@ int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, cons
     CHECK(plan_conv(desc, &q));
     if (accumulate != 0 && accumulate != 1)
         return fail(CAFFE_ERR_INVALID_ARG, "accumulate must be 0 or 1");
-    if (flags & ~(CAFFE_BACKWARD_TOP_DIFF_MASKED | CAFFE_BACKWARD_MASK_BOTTOM_DIFF))
+    if (flags & ~(CAFFE_BACKWARD_TOP_DIFF_MASKED | CAFFE_BACKWARD_MASK_BOTTOM_DIFF |
+                  CAFFE_BACKWARD_BOTTOM_STAGED))
         return fail(CAFFE_ERR_INVALID_ARG, "unknown backward flags 0x%x", flags);
+    const bool staged = (flags & CAFFE_BACKWARD_BOTTOM_STAGED) != 0;
     const bool masked = (flags & CAFFE_BACKWARD_TOP_DIFF_MASKED) != 0;
     const bool mask_bottom = (flags & CAFFE_BACKWARD_MASK_BOTTOM_DIFF) != 0 && bottom_diff;
     CHECK(check_conv_ptrs(q, top_diff, true, true, "top_diff"));
@@ -1038,8 +1043,8 @@ int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, cons
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
     if (q.dtype == CAFFE_BF16)
-        return backward_bf16(q, top_diff, top, masked, mask_bottom, bottom, weight, bottom_diff,
-                             weight_diff, bias_diff, accumulate, ws, s);
+        return backward_bf16(q, top_diff, top, masked, mask_bottom, staged, bottom, weight,
+                             bottom_diff, weight_diff, bias_diff, accumulate, ws, s);
     if (q.dense)
         return backward_dense(q, top_diff, top, masked, mask_bottom, (const float*)bottom,
                               (const float*)weight, bottom_diff, weight_diff, bias_diff,

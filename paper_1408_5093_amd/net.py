@@ -12,7 +12,8 @@ call; this module only owns buffers and the call order.
 """
 import torch
 
-from . import (BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED, CAFFE_BF16, CAFFE_F32,
+from . import (BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED,
+               CAFFE_BF16, CAFFE_F32,
                PASS_BACKWARD, PASS_FORWARD, POOL_RELU_INPUT, Workspace, caffe_conv_backward,
                caffe_conv_forward, cast_f32_to_bf16, conv_desc, conv_out_shape,
                conv_workspace_size, lrn_backward, lrn_forward, maxpool_backward, maxpool_forward,
@@ -41,6 +42,7 @@ class ConvStack:
         # 1x1 image) takes it flattened, channels (c, h, w) -- a view
         self.out_shape = []
         ws_need = 0
+        ws_layer = []
         for l, L in enumerate(self.layers):
             d = conv_desc((N, L.C, L.H, L.W), (L.K, L.C // L.g, L.k, L.k), L.s, L.p, L.g, L.relu,
                           dt)
@@ -55,8 +57,9 @@ class ConvStack:
             self.dbottom.append(torch.empty((N, L.C, L.H, L.W), dtype=torch.float32, device=dev))
             self.bottom_op.append(torch.empty((N, L.C, L.H, L.W), dtype=op, device=dev)
                                   if bf16 else None)
-            ws_need = max(ws_need, conv_workspace_size(d, PASS_BACKWARD),
-                          conv_workspace_size(d, PASS_FORWARD))
+            need_l = max(conv_workspace_size(d, PASS_BACKWARD), conv_workspace_size(d, PASS_FORWARD))
+            ws_need = max(ws_need, need_l)
+            ws_layer.append(need_l)
             cur = (N, L.K, Ho, Wo)
             stages = []
             for kind, prm in self.glue.get(l, []):
@@ -78,7 +81,14 @@ class ConvStack:
                 flat = nx.H == 1 and nx.W == 1 and cur[1] * cur[2] * cur[3] == nx.C
                 if cur != (N, nx.C, nx.H, nx.W) and not flat:
                     raise ValueError(f"layer {l} output {cur} does not feed layer {l + 1}")
-        self.ws = Workspace(dev).get(ws_need)
+        # bf16: a workspace per layer, so that its backward reads the input
+        # its forward staged there (BACKWARD_BOTTOM_STAGED); fp32 stages
+        # nothing and all layers share one
+        if bf16:
+            self.ws_of = [Workspace(dev).get(n) for n in ws_layer]
+        else:
+            self.ws = Workspace(dev).get(ws_need)
+            self.ws_of = [self.ws] * len(ws_layer)
         self.bottom = [None] * len(self.layers)
         # Fused ReLU backward passes.  A ReLU output that feeds a max-pool gets
         # its backward folded into the pool's routing (CAFFE_POOL_RELU_INPUT);
@@ -131,7 +141,8 @@ class ConvStack:
             if self.bf16:
                 src = cast_f32_to_bf16(cur, out=self.bottom_op[l], stream=s)
             self._mark(("fwd", l, "begin"), s)
-            caffe_conv_forward(self.descs[l], src, self.W[l], self.b[l], self.top[l], self.ws, s)
+            caffe_conv_forward(self.descs[l], src, self.W[l], self.b[l], self.top[l], self.ws_of[l],
+                               s)
             self._mark(("fwd", l, "end"), s)
             cur = self.top[l]
             if self.fused[l]:
@@ -185,10 +196,12 @@ class ConvStack:
                 flags |= BACKWARD_TOP_DIFF_MASKED
             if self.mask_bottom[l] and want_dx:
                 flags |= BACKWARD_MASK_BOTTOM_DIFF
+            if self.bf16:
+                flags |= BACKWARD_BOTTOM_STAGED
             self._mark(("bwd", l, "begin"), s)
             caffe_conv_backward(self.descs[l], g, self.top[l] if L.relu else None, bottom,
                                 self.W[l], self.dbottom[l] if want_dx else None, self.dW[l],
-                                self.db[l], 0, flags, self.ws, s)
+                                self.db[l], 0, flags, self.ws_of[l], s)
             self._mark(("bwd", l, "end"), s)
             g = self.dbottom[l]
         return self.dbottom[0]

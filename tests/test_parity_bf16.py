@@ -113,6 +113,40 @@ def test_backward_flags_bf16(flags):
     run_case(2, 8, 13, 13, 24, 3, 3, 1, 1, 1, 1, 2, True, flags=flags)
 
 
+@pytest.mark.parametrize("case", [(2, 3, 29, 31, 16, 11, 11, 4, 4, 0, 0, 1, True),
+                                  (2, 8, 13, 13, 24, 3, 3, 1, 1, 1, 1, 2, True),
+                                  (3, 20, 9, 10, 30, 5, 5, 1, 1, 2, 2, 1, False)])
+def test_backward_reuses_forward_staging_bf16(case):
+    """BACKWARD_BOTTOM_STAGED: a backward on the workspace the forward
+    staged its input into gives bitwise the gradients of a plain backward on
+    a fresh workspace (the same kernels in the same order read the same
+    staged copy); in fp32 mode the flag changes nothing."""
+    N, C, H, W, K, kh, kw, sh, sw, ph, pw, g, relu = case
+    print(f"staged bottom case {case}", flush=True)
+    rng = np.random.default_rng([79, N, C, K, kh])
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    w = (rng.standard_normal((K, C // g, kh, kw)) * 0.3).astype(np.float32)
+    b = (rng.standard_normal(K) * 0.5).astype(np.float32)
+    for op in (torch.bfloat16, torch.float32):
+        dt = cc.CAFFE_BF16 if op == torch.bfloat16 else cc.CAFFE_F32
+        d = cc.conv_desc(x.shape, w.shape, (sh, sw), (ph, pw), g, relu, dt)
+        Ho, Wo = cc.conv_out_shape(d)
+        xb, wb, bt = _t(x, op), _t(w, op), _t(b)
+        gd = _t(rng.standard_normal((N, K, Ho, Wo)))
+        need = max(cc.conv_workspace_size(d, cc.PASS_FORWARD),
+                   cc.conv_workspace_size(d, cc.PASS_BACKWARD))
+        buf = cc.Workspace(DEV).get(need)
+        top = torch.empty((N, K, Ho, Wo), dtype=torch.float32, device=DEV)
+        cc.caffe_conv_forward(d, xb, wb, bt, top, buf)
+        ref = cc.conv_backward(xb, wb, gd, top if relu else None, (sh, sw), (ph, pw), g, relu)
+        outs = tuple(torch.empty_like(t) for t in ref)
+        cc.caffe_conv_backward(d, gd, top if relu else None, xb, wb, *outs, 0,
+                               cc.BACKWARD_BOTTOM_STAGED, buf)
+        torch.cuda.synchronize()
+        for name, u, v in zip(("dx", "dw", "db"), outs, ref):
+            assert torch.equal(u, v), (op, name)
+
+
 def test_empty_batch_bf16():
     x = torch.empty((0, 4, 9, 9), device=DEV, dtype=torch.bfloat16)
     w = torch.randn((6, 2, 3, 3), device=DEV).to(torch.bfloat16)

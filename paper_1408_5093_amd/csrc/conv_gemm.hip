@@ -436,50 +436,49 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     // buffer, dropped by the hardware): short-circuit tests here become
     // divergent branches and make the compiler copy every accumulator out of
     // the AGPRs at once.
+    // the wave's 64 columns, one per lane, rows regrouped by WaveRows
+    typedef WaveRows<MT> WR;
+    static_assert(NI * MT == 64, "a wave covers 64 columns");
+    constexpr int NR = WR::kRows;
+    const int wcol = n0 + wn * NI * MT + lane;
     if constexpr (EPI >= 2) {
         // split partial P[split][g][m][col], lanes along col
+        const uint32_t cbad = (uint32_t)(wcol >= p.Ncol) << 31;
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
-            for (int ni = 0; ni < NI; ++ni) {
-                const int col = n0 + bcol + ni * MT;
-                const uint32_t cbad = (uint32_t)(col >= p.Ncol) << 31;
-                __builtin_amdgcn_sched_barrier(0);
+            for (int q = 0; q < Op::kRegs; ++q) {
+                float v[NR];
+                wave_rows<MT>(acc[mi], q, v);
 #pragma unroll
-                for (int q = 0; q < Op::kRegs; ++q) {
-                    const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
+                for (int h = 0; h < NR; ++h) {
+                    const int m = m0 + wm * MI * MT + mi * MT + WR::row(q, h);
                     const uint32_t off =
-                        ((uint32_t)(((split * p.G + g) * M + m) * p.Ncol + col) * 4u) | cbad |
+                        ((uint32_t)(((split * p.G + g) * M + m) * p.Ncol + wcol) * 4u) | cbad |
                         ((uint32_t)(m >= M) << 31);
-                    buf_st_f32(acc[mi][ni][q], ry, off);
+                    buf_st_f32(v[h], ry, off);
                 }
             }
         }
     } else if constexpr (EPI == 0) {
-        int cbase[NI];
-        uint32_t cbad[NI];
-#pragma unroll
-        for (int ni = 0; ni < NI; ++ni) {
-            const int col = n0 + bcol + ni * MT;
-            const int n = col / OHW;
-            const int pix = col - n * OHW;
-            cbase[ni] = n * p.Cout * OHW + pix;
-            cbad[ni] = (uint32_t)(col >= p.Ncol) << 31;
-        }
+        const int n = wcol / OHW;
+        const int pix = wcol - n * OHW;
+        const int cbase = n * p.Cout * OHW + pix;
+        const uint32_t cbad = (uint32_t)(wcol >= p.Ncol) << 31;
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
-            for (int ni = 0; ni < NI; ++ni) {
-                __builtin_amdgcn_sched_barrier(0);
+            for (int q = 0; q < Op::kRegs; ++q) {
+                float z[NR];
+                wave_rows<MT>(acc[mi], q, z);
 #pragma unroll
-                for (int q = 0; q < Op::kRegs; ++q) {
-                    const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
+                for (int h = 0; h < NR; ++h) {
+                    const int m = m0 + wm * MI * MT + mi * MT + WR::row(q, h);
                     const int oc = g * M + m;
-                    const float z = acc[mi][ni][q];
                     // ReLU: non-positive values (NaN included) become 0; without
                     // ReLU every value passes unchanged
-                    const float v = z > 0.f ? z : (p.relu ? 0.f : z);
-                    const uint32_t off = ((uint32_t)(cbase[ni] + oc * OHW) * 4u) | cbad[ni] |
+                    const float v = z[h] > 0.f ? z[h] : (p.relu ? 0.f : z[h]);
+                    const uint32_t off = ((uint32_t)(cbase + oc * OHW) * 4u) | cbad |
                                          ((uint32_t)(m >= M) << 31);
                     buf_st_f32(v, ry, off);
                 }
@@ -489,61 +488,58 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
         const int pss = p.psh * p.psw;
         const int OutHW = p.OutH * p.OutW;
         const __amdgpu_buffer_rsrc_t rom = make_rsrc(MASK ? p.Omask : p.Y, p.Y_bytes);
-        int cb[NI], hb[NI], wb[NI];
-#pragma unroll
-        for (int ni = 0; ni < NI; ++ni) {
-            const int col = n0 + bcol + ni * MT;
-            const bool cok = col < p.Ncol;
-            const int n = cok ? col / OHW : 0;
-            const int pix = col - n * OHW;
-            const int a = pix / p.OW;
-            const int b = pix - a * p.OW;
-            hb[ni] = cok ? p.psh * (a + p.a0h) - p.oph : -(1 << 28);
-            wb[ni] = p.psw * (b + p.a0w) - p.opw;
-            cb[ni] = (n * p.Cout + g * p.Cg_out) * OutHW;
-        }
+        const bool cok = wcol < p.Ncol;
+        const int n = cok ? wcol / OHW : 0;
+        const int pix = wcol - n * OHW;
+        const int a = pix / p.OW;
+        const int b = pix - a * p.OW;
+        const int hb = cok ? p.psh * (a + p.a0h) - p.oph : -(1 << 28);
+        const int wb = p.psw * (b + p.a0w) - p.opw;
+        const int cb = (n * p.Cout + g * p.Cg_out) * OutHW;
         // per MT-row block: every position (and, masked, every value of the
         // ReLU output) first, then the stores (a load after a store to
         // another buffer could not be moved above it, so each would wait
         // alone)
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
-            uint32_t off[Op::kRegs][NI];
-            float y[Op::kRegs][NI];
+            uint32_t off[Op::kRegs][NR];
+            float y[Op::kRegs][NR];
 #pragma unroll
             for (int q = 0; q < Op::kRegs; ++q) {
-                const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
-                int c = m, fh = 0, fw = 0;
-                if (pss != 1) {
-                    c = m / pss;
-                    const int fr = m - c * pss;
-                    fh = fr / p.psw;
-                    fw = fr - fh * p.psw;
-                }
 #pragma unroll
-                for (int ni = 0; ni < NI; ++ni) {
-                    const int h = hb[ni] + fh;
-                    const int w = wb[ni] + fw;
+                for (int h = 0; h < NR; ++h) {
+                    const int m = m0 + wm * MI * MT + mi * MT + WR::row(q, h);
+                    int c = m, fh = 0, fw = 0;
+                    if (pss != 1) {
+                        c = m / pss;
+                        const int fr = m - c * pss;
+                        fh = fr / p.psw;
+                        fw = fr - fh * p.psw;
+                    }
+                    const int hh = hb + fh;
+                    const int ww = wb + fw;
                     const uint32_t bad = ((uint32_t)(m >= M) |
-                                          (uint32_t)((unsigned)h >= (unsigned)p.OutH) |
-                                          (uint32_t)((unsigned)w >= (unsigned)p.OutW))
+                                          (uint32_t)((unsigned)hh >= (unsigned)p.OutH) |
+                                          (uint32_t)((unsigned)ww >= (unsigned)p.OutW))
                                          << 31;
-                    off[q][ni] = ((uint32_t)(cb[ni] + c * OutHW + h * p.OutW + w) * 4u) | bad;
+                    off[q][h] = ((uint32_t)(cb + c * OutHW + hh * p.OutW + ww) * 4u) | bad;
                     // backward of the ReLU that produced the gather target:
                     // keep the gradient only where that output was > 0
                     if constexpr (MASK)
-                        y[q][ni] = buf_ld_f32(rom, off[q][ni]);
+                        y[q][h] = buf_ld_f32(rom, off[q][h]);
                 }
             }
 #pragma unroll
-            for (int q = 0; q < Op::kRegs; ++q)
+            for (int q = 0; q < Op::kRegs; ++q) {
+                float v[NR];
+                wave_rows<MT>(acc[mi], q, v);
 #pragma unroll
-                for (int ni = 0; ni < NI; ++ni) {
-                    float v = acc[mi][ni][q];
+                for (int h = 0; h < NR; ++h) {
                     if constexpr (MASK)
-                        v = y[q][ni] > 0.f ? v : 0.f;
-                    buf_st_f32(v, ry, off[q][ni]);
+                        v[h] = y[q][h] > 0.f ? v[h] : 0.f;
+                    buf_st_f32(v[h], ry, off[q][h]);
                 }
+            }
         }
     }
 }
@@ -867,21 +863,26 @@ dense_gemm_nt_kernel(const ConvGemmParams p)
         }
     }
 
-    // split partial P[split][m][col], lanes along col
+    // split partial P[split][m][col]: the wave's 64 columns, one per lane,
+    // rows regrouped by WaveRows
     const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y, p.Y_bytes);
+    typedef WaveRows<MT> WR;
+    static_assert(NI * MT == 64, "a wave covers 64 columns");
+    constexpr int NR = WR::kRows;
+    const int col = n0 + bcol0 + lane;
+    const uint32_t cbad = (uint32_t)(col >= p.Ncol) << 31;
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
-        for (int ni = 0; ni < NI; ++ni) {
-            const int col = n0 + bcol0 + ni * MT + fi;
-            const uint32_t cbad = (uint32_t)(col >= p.Ncol) << 31;
-            __builtin_amdgcn_sched_barrier(0);
+        for (int q = 0; q < Op::kRegs; ++q) {
+            float v[NR];
+            wave_rows<MT>(acc[mi], q, v);
 #pragma unroll
-            for (int q = 0; q < Op::kRegs; ++q) {
-                const int m = m0 + arow0 + mi * MT + Op::row(q, lane);
+            for (int h = 0; h < NR; ++h) {
+                const int m = m0 + arow0 + mi * MT + WR::row(q, h);
                 const uint32_t off = ((uint32_t)((split * M + m) * p.Ncol + col) * 4u) | cbad |
                                      ((uint32_t)(m >= M) << 31);
-                buf_st_f32(acc[mi][ni][q], ry, off);
+                buf_st_f32(v[h], ry, off);
             }
         }
     }

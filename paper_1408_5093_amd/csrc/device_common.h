@@ -71,6 +71,75 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t x, const FastDiv& f)
     return (uint32_t)(((uint64_t)x * f.mul) >> f.shift);
 }
 
+// MFMA results regrouped as output rows across the lanes.  A wave's NI
+// accumulator blocks of MT columns (NI * MT == 64) hold, in register q,
+//   MT = 32: row 8*(q/4) + q%4 + 4*(lane/32) of column 32*ni + lane%32,
+//   MT = 16: row 4*(lane/16) + q of column 16*ni + lane%16.
+// Lane swaps regroup them so that value h of get(acc, q) is row row(q, h)
+// of column `lane` (0..63): a store of one value per lane then writes 64
+// consecutive columns of one row instead of 32 columns of two rows.  Used by
+// the fp32 GEMM epilogues (the CaffeNet fp32 step runs ~1% faster with it;
+// the bf16 step ran 2% slower, so the bf16 kernels keep the MFMA layout).
+//   v_permlane32_swap(x, y): x.lanes[32,64) <-> y.lanes[0,32)
+//   v_permlane16_swap(x, y): x.lanes[16,32) <-> y.lanes[0,16), x.lanes[48,64) <-> y.lanes[32,48)
+template <int MT>
+struct WaveRows;
+
+template <>
+struct WaveRows<32> {
+    static constexpr int kRows = 2;
+    static __device__ __forceinline__ int row(int q, int h) { return 8 * (q >> 2) + (q & 3) + 4 * h; }
+    // x[ni] = register q of accumulator block ni
+    static __device__ __forceinline__ void get(const float* x, float* out)
+    {
+        const auto s = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x[0]),
+                                                        __builtin_bit_cast(uint32_t, x[1]), false,
+                                                        false);
+        out[0] = __builtin_bit_cast(float, (uint32_t)s[0]);
+        out[1] = __builtin_bit_cast(float, (uint32_t)s[1]);
+    }
+};
+
+template <>
+struct WaveRows<16> {
+    static constexpr int kRows = 4;
+    static __device__ __forceinline__ int row(int q, int h) { return q + 4 * h; }
+    // a 4 x 4 transpose of 16-lane groups: register ni, group j holds row
+    // group j of columns 16*ni ..; the result h holds row group h of all 64
+    static __device__ __forceinline__ void get(const float* x, float* out)
+    {
+        const auto s02 = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x[0]),
+                                                          __builtin_bit_cast(uint32_t, x[2]), false,
+                                                          false);
+        const auto s13 = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x[1]),
+                                                          __builtin_bit_cast(uint32_t, x[3]), false,
+                                                          false);
+        const auto t01 = __builtin_amdgcn_permlane16_swap((uint32_t)s02[0], (uint32_t)s13[0],
+                                                          false, false);
+        const auto t23 = __builtin_amdgcn_permlane16_swap((uint32_t)s02[1], (uint32_t)s13[1],
+                                                          false, false);
+        out[0] = __builtin_bit_cast(float, (uint32_t)t01[0]);
+        out[1] = __builtin_bit_cast(float, (uint32_t)t01[1]);
+        out[2] = __builtin_bit_cast(float, (uint32_t)t23[0]);
+        out[3] = __builtin_bit_cast(float, (uint32_t)t23[1]);
+    }
+};
+
+// Register q of the NI accumulator blocks of row block `acc` (an array of NI
+// MFMA accumulators), regrouped as WaveRows rows.  The registers are passed
+// to the swaps by value: read through a pointer to the accumulator array
+// inside the swap helper, every q got the swaps of q = 0 (checked with a
+// probe of known values).
+template <int MT, int NI, typename Acc>
+__device__ __forceinline__ void wave_rows(const Acc (&acc)[NI], int q, float* out)
+{
+    float x[NI];
+#pragma unroll
+    for (int ni = 0; ni < NI; ++ni)
+        x[ni] = acc[ni][q];
+    WaveRows<MT>::get(x, out);
+}
+
 __device__ __forceinline__ float wave_sum(float v)
 {
     for (int off = 32; off > 0; off >>= 1)

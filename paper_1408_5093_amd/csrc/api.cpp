@@ -53,8 +53,12 @@ struct ConvPlan {
     int64_t bottom_elems, top_elems, weight_elems;
     // data gradient (phase-stacked)
     int Th, Tw, a0h, a0w, Ah, Aw, Mt, Rt;
-    // weight gradient split-K
+    // weight gradient split-K; the quad-order kernel reads a per-column table
+    // of ncol_pad entries at off_coltab
     int splits, cols_per_split, wgrad_tile;
+    bool wgrad_quad;
+    int ncol_pad, xpad;
+    size_t off_coltab;
     // reduction order of the implicit GEMMs: tap-major r = (u, v, c) when the
     // gathered channels per group fill whole pipeline stages
     int fwd_tile, dgrad_tile;
@@ -440,6 +444,19 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     q.blocked = env_tile("CAFFE_CONV_BLOCKED") != 0;
     q.xcd_order = env_tile("CAFFE_CONV_XCD_ORDER") != 0;
     q.wgrad_xcd_order = env_tile("CAFFE_CONV_WGRAD_XCD_ORDER") > 0;
+    // quad-order weight gradient: its scalar offsets (tap planes, rows of the
+    // tile) ride on lane offsets of up to the tensor's size, so both sums
+    // must stay below 2^31 with a tile's rows past the end
+    {
+        const int64_t ihw = (int64_t)q.H * q.W, ohw = (int64_t)q.Ho * q.Wo;
+        q.xpad = q.ph * q.W + q.pw;
+        const int64_t xlim = q.bottom_elems * 4 + 4 * (int64_t)q.xpad + (q.C + 512) * ihw * 4;
+        const int64_t dlim = q.top_elems * 4 + (q.K + 512) * ohw * 4;
+        q.wgrad_quad = env_tile("CAFFE_CONV_WGRAD_QUAD") != 0 &&
+                       wgrad_quad_supported(q.Cg, q.kh, q.kw) && xlim < kMaxTensorBytes &&
+                       dlim < kMaxTensorBytes;
+        q.ncol_pad = (int)((ncol + 15) / 16 * 16);
+    }
     q.fwd_tap = q.Cg % gemm_tile_k(q.fwd_tile) == 0;
     q.dgrad_tap = q.Kg % gemm_tile_k(q.dgrad_tile) == 0;
     q.ws_fwd = align_up(q.weight_elems * 4, kWsAlign);  // the packed weights
@@ -512,7 +529,8 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     q.off_wt = q.off_sums + sums_bytes;
     q.off_part = q.off_wt + wt_bytes;
     q.ws_data = q.off_part + align_up(dpart, kWsAlign);
-    q.ws_weights = q.off_part + align_up(part_bytes, kWsAlign);
+    q.off_coltab = q.off_part + align_up(part_bytes, kWsAlign);
+    q.ws_weights = q.off_coltab + (q.wgrad_quad ? align_up((size_t)q.ncol_pad * 12, kWsAlign) : 0);
     q.ws_both = std::max(q.ws_data, q.ws_weights);
     return CAFFE_OK;
 }
@@ -693,7 +711,18 @@ int run_weights(const ConvPlan& q, const float* dsrc, const void* bottom, float*
     p.div_ohw = make_fastdiv((uint32_t)(q.Ho * q.Wo));
     p.div_ow = make_fastdiv((uint32_t)q.Wo);
     p.xcd_order = q.wgrad_xcd_order;
-    LAUNCH(launch_conv_wgrad_f32(p, q.wgrad_tile, s), "weight-gradient launch");
+    if (q.wgrad_quad) {
+        uint32_t* tab = (uint32_t*)(ws + q.off_coltab);
+        LAUNCH(launch_wgrad_col_table(tab, (int)p.Ncol, q.ncol_pad, q.C, q.H, q.W, q.K, q.Ho,
+                                      q.Wo, q.kh, q.kw, q.sh, q.sw, q.ph, q.pw, s),
+               "weight-gradient column table launch");
+        p.T = tab;
+        p.T_bytes = nbytes((int64_t)q.ncol_pad * 3, 4);
+        p.xpad = q.xpad;
+        LAUNCH(launch_conv_wgrad_quad_f32(p, q.wgrad_tile, s), "weight-gradient launch");
+    } else {
+        LAUNCH(launch_conv_wgrad_f32(p, q.wgrad_tile, s), "weight-gradient launch");
+    }
     // dW = sum of the split partials; db = sum of the split bias partials
     LAUNCH(launch_wgrad_reduce(part, weight_diff, (int)q.weight_elems, q.splits, sums, bias_diff,
                                q.splits, q.K, accumulate, s),

@@ -28,11 +28,6 @@ namespace caffe_hip {
 
 typedef uint16_t bf16_t;
 
-__device__ __forceinline__ u32x4 buf_ld_b128(__amdgpu_buffer_rsrc_t r, uint32_t byte_off)
-{
-    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
-}
-
 __device__ __forceinline__ bf16x8 lds_frag(const bf16_t* p)
 {
     return __builtin_bit_cast(bf16x8, *(const u32x4*)p);

@@ -286,6 +286,293 @@ conv_wgrad_f32_kernel(const WgradParams p)
     }
 }
 
+// ------------------------------------------------------------ quad order
+// Layers with Cg % 4 == 0 and a kernel of kh*kw < 32 taps run the same
+// split-K GEMM with its tap dimension in the order
+//   r' = ((c / 4) * kh*kw + u*kw + v) * 4 + c % 4
+// (four channels of one tap side by side).  A thread's loader rows are
+// r' = r0 + rw + 16 q with rw = 4 * wave + lane / 16, so c % 4 is the lane's
+// (a fixed channel-plane offset) and r' / 4 = r0 / 4 + wave + 4 q is
+// wave-uniform: each B load takes the column's window base in the lane
+// offset and the tap's offset in the scalar offset, and its bounds test is
+// one bit of the column's tap mask.  A rows m0 + rw + 16 q split the same
+// way.  The columns' bases and masks come from a table written once per call
+// (wgrad_col_table_kernel), so a stage decodes no pixel indices.  The
+// epilogue maps r' back to r = c*kh*kw + u*kw + v.
+//
+// LDS tiles hold each wave's MFMA row blocks interleaved in pairs
+// (position 2*(m % 32) + block parity), so one 8-byte read fetches the
+// fragments of two blocks at an immediate offset.
+
+// Position of tile row m = 32 * sub + l within its LDS row, for a tile whose
+// waves own slabs of NSUB 32-row blocks.
+template <int NSUB>
+__device__ __forceinline__ int quad_lds_pos(int sub, int l)
+{
+    const int slab = sub / NSUB, mi = sub % NSUB;
+    const bool pair = (mi | 1) < NSUB;
+    return slab * NSUB * 32 + (mi / 2) * 64 + (pair ? 2 * l + (mi & 1) : l);
+}
+
+template <int WM, int WN, int MI, int NI, int KH, int KW>
+__global__ void __launch_bounds__(64 * WM * WN)
+conv_wgrad_quad_f32_kernel(const WgradParams p)
+{
+    constexpr int MT = 32;
+    constexpr int NT = 64 * WM * WN;
+    constexpr int TM = WM * MI * MT;
+    constexpr int TN = WN * NI * MT;
+    constexpr int TK = 16;
+    constexpr int RS = NT / TK;  // loader rows per pass
+    constexpr int EA = TM / RS;  // A elements per thread per stage
+    constexpr int EB = TN / RS;  // B elements per thread per stage
+    constexpr int KHW = KH * KW;
+    static_assert(RS == 16 && TM % 32 == 0 && TN % 32 == 0, "quad loader mapping");
+    static_assert(KHW < 32, "one mask bit per tap");
+
+    // rows of 8-byte aligned length; the stride (2 mod 32 words) keeps the
+    // loader's 8-byte writes conflict-free
+    __shared__ float As[2][TK][TM + 2];
+    __shared__ float Bs[2][TK][TN + 2];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave % WM;
+    const int wn = wave / WM;
+    const int n_rt = (p.R + TN - 1) / TN;
+    const int n_mt = (p.Kg + TM - 1) / TM;
+    const int per_xcd = gridDim.x >> 3;
+    const int T = p.xcd_order ? (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3) : blockIdx.x;
+    if (T >= n_rt * n_mt * p.G * p.splits)
+        return;
+    const int rt = T % n_rt;
+    const int mt = (T / n_rt) % n_mt;
+    const int g = (T / (n_rt * n_mt)) % p.G;
+    const int split = T / (n_rt * n_mt * p.G);
+    const int m0 = mt * TM;
+    const int r0 = rt * TN;
+    const int IW = p.IW, IHW = p.IH * p.IW;
+    const int OHW = p.OH * p.OW;
+    const int col_begin = split * p.cols_per_split;
+    const int col_end = min(p.Ncol, col_begin + p.cols_per_split);
+
+    const __amdgpu_buffer_rsrc_t rd = make_rsrc(p.D, p.D_bytes);
+    // X through a base p.xpad elements early: every window base in the table
+    // is then >= 0 and every tap offset below is >= 0
+    const __amdgpu_buffer_rsrc_t rx =
+        make_rsrc((const char*)p.X - 4 * (size_t)p.xpad, p.X_bytes + 4u * (uint32_t)p.xpad);
+    const __amdgpu_buffer_rsrc_t rtab = make_rsrc(p.T, p.T_bytes);
+
+    const int kc = tid % TK;  // reduction column within a stage
+    const int rw = tid / TK;  // loader row within one pass
+
+    // A row m0 + rw + RS*q of group g: lane part rw*OHW, the rest uniform.
+    // Rows past Kg and taps past R only feed accumulators the epilogue never
+    // stores; their loads stay inside the tensors or read 0.
+    const uint32_t a_lane4 = (uint32_t)(rw * OHW) * 4u;
+    const uint32_t a_soff4 = (uint32_t)((g * p.Kg + m0) * OHW) * 4u;
+    const uint32_t b_lane4 = (uint32_t)((lane >> 4) * IHW) * 4u;
+    uint32_t b_soff[EB];
+    uint32_t b_bit[EB];
+#pragma unroll
+    for (int q = 0; q < EB; ++q) {
+        const int tg = r0 / 4 + wave + 4 * q;
+        const int cb = tg / KHW;
+        const int t = tg - cb * KHW;
+        const int u = t / KW;
+        const int v = t - u * KW;
+        b_soff[q] = (uint32_t)((g * p.Cg + 4 * cb) * IHW + u * IW + v) * 4u;
+        b_bit[q] = (uint32_t)t;
+    }
+
+    float rA[EA], rB[EB];
+    typedef uint32_t u32x3 __attribute__((ext_vector_type(3)));
+    auto load_entry = [&](int cbase) {
+        return __builtin_bit_cast(
+            u32x3, __builtin_amdgcn_raw_buffer_load_b96(rtab, (uint32_t)(cbase + kc) * 12u, 0, 0));
+    };
+    auto load_stage = [&](const u32x3& e) {
+        const uint32_t db4 = e[2] + a_lane4;
+#pragma unroll
+        for (int q = 0; q < EA; ++q)
+            rA[q] = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(
+                           rd, db4, (int)(a_soff4 + (uint32_t)(RS * q * OHW) * 4u), 0));
+        const uint32_t xb4 = e[0] + b_lane4;
+        const uint32_t nok = e[1];
+#pragma unroll
+        for (int q = 0; q < EB; ++q)
+            rB[q] = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(rx, xb4 | ((nok >> b_bit[q]) << 31),
+                                                            (int)b_soff[q], 0));
+    };
+
+    // Loader row rw + RS*q is row 32*(q/2) + rw + 16*(q%2) of the tile;
+    // rows q and q + 2 of a block pair sit side by side.
+    auto store_rows = [&](float* row, const float* vals, auto nsub_tag, auto e_tag) {
+        constexpr int NSUB = decltype(nsub_tag)::value;
+        constexpr int E = decltype(e_tag)::value;
+#pragma unroll
+        for (int q = 0; q < E; ++q) {
+            const int sub = q / 2;
+            const int mi = sub % NSUB;
+            const int pos = quad_lds_pos<NSUB>(sub, rw + 16 * (q % 2));
+            if ((mi | 1) < NSUB) {
+                if ((mi & 1) == 0)
+                    *(float2*)&row[pos] = make_float2(vals[q], vals[q + 2]);
+            } else {
+                row[pos] = vals[q];
+            }
+        }
+    };
+    auto store_stage = [&](int buf) {
+        store_rows(&As[buf][kc][0], rA, std::integral_constant<int, MI>{},
+                   std::integral_constant<int, EA>{});
+        store_rows(&Bs[buf][kc][0], rB, std::integral_constant<int, NI>{},
+                   std::integral_constant<int, EB>{});
+    };
+
+    floatx16 acc[MI][NI];
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+            acc[mi][ni] = floatx16{};
+
+    // bias-gradient partials, as in conv_wgrad_f32_kernel
+    const bool want_db = p.dbp != nullptr && rt == 0;
+    const int db_pos = quad_lds_pos<MI>(tid / 32, tid % 32);
+    float dsum = 0.f;
+
+    const int nst = col_end > col_begin ? (col_end - col_begin + TK - 1) / TK : 0;
+    u32x3 e_next = {0u, 0u, 0u};  // table entries of the next stage
+    if (nst > 0) {
+        load_stage(load_entry(col_begin));
+        if (nst > 1)
+            e_next = load_entry(col_begin + TK);
+        store_stage(0);
+    }
+    __syncthreads();
+
+    const int kl = lane >> 5;
+    const int l32 = lane & 31;
+    for (int s = 0; s < nst; ++s) {
+        const int cur = s & 1;
+        if (s + 1 < nst) {
+            load_stage(e_next);
+            // (unconditional: past the split it reads unused entries, or 0
+            // past the table, and the stores below wait for the data only)
+            e_next = load_entry(col_begin + (s + 2) * TK);
+        }
+        if (want_db && tid < TM) {
+#pragma unroll
+            for (int k = 0; k < TK; ++k)
+                dsum += As[cur][k][db_pos];
+        }
+        constexpr int KS = TK / 2;
+        constexpr int PF = 2;
+        float fa[PF + 1][MI], fb[PF + 1][NI];
+        auto read_frags = [&](const float* row, float* f, auto nsub_tag, int slab) {
+            constexpr int NSUB = decltype(nsub_tag)::value;
+#pragma unroll
+            for (int mi = 0; mi < NSUB; mi += 2) {
+                const int pos = quad_lds_pos<NSUB>(slab * NSUB + mi, l32);
+                if (mi + 1 < NSUB) {
+                    const float2 v = *(const float2*)&row[pos];
+                    f[mi] = v.x;
+                    f[mi + 1] = v.y;
+                } else {
+                    f[mi] = row[pos];
+                }
+            }
+        };
+        auto read_frag = [&](int ks, int slot) {
+            read_frags(&As[cur][2 * ks + kl][0], fa[slot], std::integral_constant<int, MI>{}, wm);
+            read_frags(&Bs[cur][2 * ks + kl][0], fb[slot], std::integral_constant<int, NI>{}, wn);
+        };
+#pragma unroll
+        for (int ks = 0; ks < PF; ++ks)
+            read_frag(ks, ks);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            if (ks + PF < KS)
+                read_frag(ks + PF, (ks + PF) % (PF + 1));
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni)
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                        fa[ks % (PF + 1)][mi], fb[ks % (PF + 1)][ni], acc[mi][ni], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (s + 1 < nst)
+            store_stage(cur ^ 1);
+        __syncthreads();
+    }
+
+    if (want_db) {
+        const int m = m0 + tid;
+        if (tid < TM && m < p.Kg)
+            p.dbp[split * p.K + g * p.Kg + m] = dsum;
+    }
+
+    // Partial P[split][g*Kg + m][r], r = c*KHW + t for r' = (cb*KHW + t)*4 + c % 4.
+    const __amdgpu_buffer_rsrc_t rp = make_rsrc(p.P, p.P_bytes);
+    const int pbase = split * p.K * p.R;
+#pragma unroll
+    for (int ni = 0; ni < NI; ++ni) {
+        const int rq = r0 + wn * NI * MT + ni * MT + l32;
+        const int tg = rq >> 2;
+        const int cb = tg / KHW;
+        const int r = (4 * cb + (rq & 3)) * KHW + (tg - cb * KHW);
+        const bool rok = rq < p.R;
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) {
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                const int m = m0 + wm * MI * MT + mi * MT + 8 * (q >> 2) + 4 * kl + (q & 3);
+                const bool ok = rok && m < p.Kg;
+                const uint32_t off = ok ? (uint32_t)(pbase + (g * p.Kg + m) * p.R + r) * 4u : kOob;
+                buf_st_f32(acc[mi][ni][q], rp, off);
+            }
+        }
+    }
+}
+
+// One thread per column: see launch_wgrad_col_table.
+__global__ void __launch_bounds__(256)
+wgrad_col_table_kernel(uint32_t* __restrict__ T, int ncol, int ncol_pad, int C, int IH, int IW,
+                       int K, int OH, int OW, int kh, int kw, int sh, int sw, int ph, int pw)
+{
+    const int col = blockIdx.x * 256 + threadIdx.x;
+    if (col >= ncol_pad)
+        return;
+    uint32_t e[3] = {kOob, ~0u, kOob};
+    if (col < ncol) {
+        const int OHW = OH * OW;
+        const int n = col / OHW;
+        const int pix = col - n * OHW;
+        const int i = pix / OW;
+        const int j = pix - i * OW;
+        const int ih0 = i * sh - ph;
+        const int iw0 = j * sw - pw;
+        uint32_t nok = 0;
+        for (int u = 0; u < kh; ++u)
+            for (int v = 0; v < kw; ++v)
+                if ((unsigned)(ih0 + u) >= (unsigned)IH || (unsigned)(iw0 + v) >= (unsigned)IW)
+                    nok |= 1u << (u * kw + v);
+        const int64_t xb = (int64_t)n * C * IH * IW + (int64_t)(ih0 + ph) * IW + (iw0 + pw);
+        e[0] = (uint32_t)(xb * 4);
+        e[1] = nok;
+        e[2] = (uint32_t)(((int64_t)n * K * OHW + pix) * 4);
+    }
+    T[3 * col] = e[0];
+    T[3 * col + 1] = e[1];
+    T[3 * col + 2] = e[2];
+}
+
 // ------------------------------------------------------------------ launch
 namespace {
 constexpr int kTK = 16;
@@ -345,6 +632,65 @@ hipError_t launch_conv_wgrad_f32(const WgradParams& p, int tile, hipStream_t s)
     default:
         return hipErrorInvalidValue;
     }
+}
+
+namespace {
+template <int WM, int WN, int MI, int NI, int KH, int KW>
+hipError_t launch_wq(const WgradParams& p, hipStream_t s)
+{
+    constexpr int TM = WM * MI * 32, TN = WN * NI * 32;
+    const int64_t tiles =
+        (int64_t)((p.R + TN - 1) / TN) * ((p.Kg + TM - 1) / TM) * p.G * p.splits;
+    const int64_t per_xcd = (tiles + 7) / 8;
+    hipLaunchKernelGGL((conv_wgrad_quad_f32_kernel<WM, WN, MI, NI, KH, KW>),
+                       dim3((unsigned)(per_xcd * 8)), dim3(64 * WM * WN), 0, s, p);
+    return hipGetLastError();
+}
+
+template <int WM, int WN, int MI, int NI>
+hipError_t launch_wqg(const WgradParams& p, hipStream_t s)
+{
+    if (p.kh == 3 && p.kw == 3)
+        return launch_wq<WM, WN, MI, NI, 3, 3>(p, s);
+    if (p.kh == 5 && p.kw == 5)
+        return launch_wq<WM, WN, MI, NI, 5, 5>(p, s);
+    return hipErrorInvalidValue;
+}
+}  // namespace
+
+bool wgrad_quad_supported(int Cg, int kh, int kw)
+{
+    return Cg % 4 == 0 && ((kh == 3 && kw == 3) || (kh == 5 && kw == 5));
+}
+
+hipError_t launch_conv_wgrad_quad_f32(const WgradParams& p, int tile, hipStream_t s)
+{
+    if (!wgrad_quad_supported(p.Cg, p.kh, p.kw) || p.T == nullptr || p.xpad < 0)
+        return hipErrorInvalidValue;
+    switch (tile) {
+    case WTILE_128x128:
+        return launch_wqg<2, 2, 2, 2>(p, s);
+    case WTILE_96x128:
+        return launch_wqg<1, 4, 3, 1>(p, s);
+    case WTILE_64x128:
+        return launch_wqg<2, 2, 1, 2>(p, s);
+    default:
+        return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_wgrad_col_table(uint32_t* T, int ncol, int ncol_pad, int C, int IH, int IW,
+                                  int K, int OH, int OW, int kh, int kw, int sh, int sw, int ph,
+                                  int pw, hipStream_t s)
+{
+    if (ncol_pad <= 0)
+        return hipSuccess;
+    if (ncol_pad % 16 != 0 || ncol_pad < ncol || kh * kw >= 32)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(wgrad_col_table_kernel, dim3((unsigned)((ncol_pad + 255) / 256)), dim3(256),
+                       0, s, T, ncol, ncol_pad, C, IH, IW, K, OH, OW, kh, kw, sh, sw, ph,
+                       pw);
+    return hipGetLastError();
 }
 
 FastDiv make_fastdiv(uint32_t d)

@@ -40,6 +40,11 @@ __device__ __forceinline__ float buf_ld_f32(__amdgpu_buffer_rsrc_t r, uint32_t b
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0));
 }
 
+__device__ __forceinline__ u32x4 buf_ld_b128(__amdgpu_buffer_rsrc_t r, uint32_t byte_off)
+{
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
+}
+
 __device__ __forceinline__ uint16_t buf_ld_u16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off)
 {
     return __builtin_amdgcn_raw_buffer_load_b16(r, byte_off, 0, 0);

@@ -101,6 +101,11 @@ struct WgradParams {
     int Ncol, cols_per_split, splits;
     FastDiv div_ohw, div_ow;
     int xcd_order;  // XCD-contiguous tile order (else linear)
+    // quad-order kernel only: the per-column table (see
+    // launch_wgrad_col_table) and the element shift of X's resource base
+    const void* T;
+    uint32_t T_bytes;
+    int xpad;
 };
 
 // Tile shapes a launcher may pick; see conv_gemm.hip.
@@ -147,6 +152,20 @@ int wgrad_tile_m(int tile);
 int wgrad_tile_n(int tile);
 int wgrad_tile_k();
 hipError_t launch_conv_wgrad_f32(const WgradParams& p, int tile, hipStream_t s);
+
+// Quad-order weight gradient (see conv_wgrad.hip): Cg % 4 == 0 and a 3x3 or
+// 5x5 kernel; reads p.T, written by launch_wgrad_col_table for the same
+// geometry.  Partials in the layout launch_conv_wgrad_f32 writes.
+bool wgrad_quad_supported(int Cg, int kh, int kw);
+hipError_t launch_conv_wgrad_quad_f32(const WgradParams& p, int tile, hipStream_t s);
+// Three words per output column col < ncol_pad (ncol_pad a multiple of 16):
+// {byte offset of the column's window origin in X plus xpad = ph*IW + pw
+// elements, mask of the window's taps u*kw + v that lie outside the image,
+// byte offset of the column in D's channel 0}; columns past ncol get
+// {2^31, ~0, 2^31}.
+hipError_t launch_wgrad_col_table(uint32_t* T, int ncol, int ncol_pad, int C, int IH, int IW,
+                                  int K, int OH, int OW, int kh, int kw, int sh, int sw, int ph,
+                                  int pw, hipStream_t s);
 
 // ---- bf16 operands (conv_bf16.hip) ----
 // Reduction depth of a bf16 implicit-GEMM stage (8 chunks of 8 bf16: 128

@@ -241,3 +241,42 @@ def test_split_k_masked_bottom_and_default_plan(monkeypatch):
     assert_close(_np(dx), dx_ref * (x > 0), TOL_F32, "masked data gradient")
     monkeypatch.delenv("CAFFE_CONV_DGRAD_SPLITS")
     run_case(1, 64, 6, 6, 64, 5, 5, 1, 1, 2, 2, 1, True)
+
+
+# Weight gradients in the quad tap order (Cg % 4 == 0, 3x3 or 5x5 kernels):
+# several tap tiles with a ragged tail, each row tile height, groups, strides,
+# pads up to the kernel size and a ragged column count.
+QUAD_CASES = [
+    # N, C, H, W, K, kh, kw, sh, sw, ph, pw, g
+    (2, 36, 11, 9, 70, 3, 3, 1, 1, 1, 1, 1),      # R = 324: 3 tap tiles, ragged rows
+    (3, 8, 13, 12, 192, 3, 3, 2, 2, 1, 1, 2),     # stride 2, Kg = 96 (96-row tile)
+    (2, 16, 9, 10, 128, 5, 5, 1, 1, 2, 2, 1),     # 128-row tile
+    (1, 24, 7, 7, 128, 5, 5, 1, 1, 4, 4, 2),      # pad = kernel - 1, Kg = 64
+    (5, 4, 6, 5, 10, 3, 3, 1, 1, 0, 0, 1),        # unpadded, 60 columns
+    (2, 12, 8, 9, 21, 3, 3, 1, 2, 3, 0, 3),       # uneven stride and pad, 3 groups
+]
+
+
+@pytest.mark.parametrize("case", QUAD_CASES)
+def test_weight_gradient_quad_order(case, monkeypatch):
+    """The quad-order kernel against the oracle, and bit for bit against the
+    channel-major kernel (same sums, same order; only the tile columns are
+    permuted)."""
+    monkeypatch.setenv("CAFFE_CONV_WGRAD_QUAD", "1")
+    N, C, H, W, K, kh, kw, sh, sw, ph, pw, g = case
+    rng = np.random.default_rng([91, N, C, H, W, K])
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    w = (rng.standard_normal((K, C // g, kh, kw)) * 0.3).astype(np.float32)
+    top = np.maximum(rng.standard_normal((N, K, (H + 2 * ph - kh) // sh + 1,
+                                          (W + 2 * pw - kw) // sw + 1)), 0).astype(np.float32)
+    gd = rng.standard_normal(top.shape).astype(np.float32)
+    _, dw_ref, db_ref = oracle.conv_backward(x, w, gd, top=top, stride=(sh, sw), pad=(ph, pw),
+                                             group=g, relu=True, need=("dw", "db"))
+    args = (_t(x), _t(w), _t(gd), _t(top), (sh, sw), (ph, pw), g, True)
+    _, dw, db = cc.conv_backward(*args, need=("dw", "db"))
+    assert_close(_np(dw), dw_ref, TOL_F32, "weight gradient")
+    assert_close(_np(db), db_ref, TOL_F32, "bias gradient")
+    monkeypatch.setenv("CAFFE_CONV_WGRAD_QUAD", "0")
+    _, dw0, db0 = cc.conv_backward(*args, need=("dw", "db"))
+    torch.cuda.synchronize()
+    assert torch.equal(dw, dw0) and torch.equal(db, db0)

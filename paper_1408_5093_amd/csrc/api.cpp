@@ -63,6 +63,10 @@ struct ConvPlan {
     // gathered channels per group fill whole pipeline stages
     int fwd_tile, dgrad_tile;
     bool fwd_tap, dgrad_tap;
+    // channel-major forward: tap-offset table of fwd_rpad entries
+    bool fwd_taps;
+    int fwd_rpad;
+    size_t off_taps_fwd;
     int blocked, xcd_order, wgrad_xcd_order;  // reduction and tile orders (see kernels.h)
     // workspace layout (byte offsets), per pass
     size_t off_d, off_sums, off_wt, off_part;
@@ -379,6 +383,7 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
                     kMaxSpatial);
 
     ConvPlan& q = *p;
+    q = ConvPlan{};
     q.N = d->N; q.C = d->C; q.H = d->H; q.W = d->W; q.K = d->K;
     q.kh = d->kernel_h; q.kw = d->kernel_w; q.sh = d->stride_h; q.sw = d->stride_w;
     q.ph = d->pad_h; q.pw = d->pad_w; q.G = d->group; q.relu = d->relu; q.dtype = d->dtype;
@@ -516,6 +521,14 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
         return fail(CAFFE_ERR_UNSUPPORTED, "split partials reach 2^31 bytes");
     q.off_fwd_part = q.ws_fwd;
     q.ws_fwd += align_up(fpart, kWsAlign);
+    // channel-major forward gather: a tap-offset table (the kernel adds its
+    // entries to lane offsets of up to X's size, hence the 2^30 bound)
+    q.fwd_taps = !q.fwd_tap && q.bottom_elems * q.esize < (int64_t(1) << 30) &&
+                 env_tile("CAFFE_CONV_TAP_TABLE") != 0;
+    q.fwd_rpad = round_up(q.R, gemm_tile_k(q.fwd_tile));
+    q.off_taps_fwd = q.ws_fwd;
+    if (q.fwd_taps)
+        q.ws_fwd += align_up((size_t)q.fwd_rpad * 4, kWsAlign);
 
     // Workspace: [masked top diff][bias partial sums][transformed weights]
     // [weight or data-gradient partials].  The masked top diff is written
@@ -605,6 +618,12 @@ int run_forward(const ConvPlan& q, const void* bottom, const void* weight, const
     p.Cout = q.K; p.OutH = q.Ho; p.OutW = q.Wo;
     p.blocked = q.blocked;
     p.xcd_order = q.xcd_order;
+    if (q.fwd_taps) {
+        uint32_t* taps = (uint32_t*)(ws + q.off_taps_fwd);
+        LAUNCH(launch_tap_table(taps, q.fwd_rpad, q.R, q.kh, q.kw, q.H * q.W, q.W, p.X_bytes, s),
+               "tap table launch");
+        p.taps = taps;
+    }
     if (q.fwd_splits > 1) {
         float* part = (float*)(ws + q.off_fwd_part);
         ConvGemmParams pp = p;

@@ -249,7 +249,33 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     // time, carrying v into u and u into c).
     constexpr int STEP = NW / NC;
     static_assert(STEP * NC == NW, "B copy rows advance by a whole step");
+    // With a tap table and every window inside the image, a copy's tap
+    // offset is a table entry, moved to the scalar offset with one lane
+    // read: lane i < 16 of tap_v holds entry kbase + wave / NC + i of the
+    // next stage to copy (the wave's rows are kbase + wave / NC + STEP*q).
+    // Rows past R read the entry X_bytes: out of range.
+    const bool use_taps = p.taps != nullptr && b_all_inside;
+    const __amdgpu_buffer_rsrc_t rtap =
+        make_rsrc(p.taps, p.taps ? (uint32_t)((R + TK - 1) / TK * TK) * 4u : 0u);
+    const uint32_t b_voff4 = ((uint32_t)b_base * 4u) | b_cbad;
+    uint32_t tap_v = 0;
+    auto load_taps = [&](int kbase) {
+        tap_v = __builtin_amdgcn_raw_buffer_load_b32(
+            rtap, (uint32_t)(kbase + wave / NC + (lane & 15)) * 4u, 0, 0);
+    };
     auto copy_b_any = [&](BTile& dst, int kbase) {
+        if (use_taps) {
+            // all lane reads first: a scalar offset read right after the
+            // lane read that writes it costs wait states per copy
+            uint32_t soff[NB];
+#pragma unroll
+            for (int q = 0; q < NB; ++q)
+                soff[q] = (uint32_t)__builtin_amdgcn_readlane((int)tap_v, STEP * q);
+#pragma unroll
+            for (int q = 0; q < NB; ++q)
+                copy_to_lds(rx, &dst[b_row(q)][b_nc * 64], b_voff4, soff[q]);
+            return;
+        }
         int r = kbase + b_row(0);
         int c = r / khw;
         int u = (r - c * khw) / kw;
@@ -340,12 +366,17 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     }
 
     copy_a(As0, s_begin * TK);
-    if constexpr (EPI == 2)
+    if constexpr (EPI == 2) {
         copy_b_dense(Bs0, s_begin * TK);
-    else if constexpr (TAP)
+    } else if constexpr (TAP) {
         copy_b_tap(Bs0, tu, tv, tc);
-    else
+    } else {
+        if (use_taps)
+            load_taps(s_begin * TK);
         copy_b_any(Bs0, s_begin * TK);
+        if (use_taps)
+            load_taps((s_begin + 1) * TK);
+    }
     __builtin_amdgcn_s_waitcnt(kVmcnt0);
     __syncthreads();
 
@@ -392,6 +423,8 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
                     copy_b_tap(Bn, tu, tv, tc);
                 } else {
                     copy_b_any(Bn, (s + 1) * TK);
+                    if (use_taps)  // (past the end it reads 0, unused)
+                        load_taps((s + 2) * TK);
                 }
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -588,6 +621,34 @@ hipError_t launch_pack_weights(const float* W, float* Wp, int G, int M, int Cg, 
         blocks = 4096;
     hipLaunchKernelGGL(pack_weights_kernel, dim3((unsigned)blocks), dim3(256), 0, s, W, Wp, G, M,
                        Cg, khw, tk, order);
+    return hipGetLastError();
+}
+
+__global__ void __launch_bounds__(256)
+tap_table_kernel(uint32_t* __restrict__ T, int rpad, int R, int kh, int kw, int IHW, int IW,
+                 uint32_t oob)
+{
+    const int r = blockIdx.x * 256 + threadIdx.x;
+    if (r >= rpad)
+        return;
+    uint32_t e = oob;
+    if (r < R) {
+        const int khw = kh * kw;
+        const int c = r / khw;
+        const int t = r - c * khw;
+        const int u = t / kw;
+        e = (uint32_t)(c * IHW + u * IW + (t - u * kw)) * 4u;
+    }
+    T[r] = e;
+}
+
+hipError_t launch_tap_table(uint32_t* T, int rpad, int R, int kh, int kw, int IHW, int IW,
+                            uint32_t oob, hipStream_t s)
+{
+    if (rpad <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(tap_table_kernel, dim3((unsigned)((rpad + 255) / 256)), dim3(256), 0, s, T,
+                       rpad, R, kh, kw, IHW, IW, oob);
     return hipGetLastError();
 }
 

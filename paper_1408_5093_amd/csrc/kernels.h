@@ -47,6 +47,10 @@ struct ConvGemmParams {
     int blocked;    // channel-blocked reduction order (else tap-major), with tap_major
     int xcd_order;  // XCD-contiguous tile order (else linear)
     int splits, stages_per_split;  // dense split-K GEMM only
+    // channel-major gathered operand (r = (c, u, v)) only, optional: byte
+    // offsets (c*IH*IW + u*IW + v) * 4 of the taps r < R, then X_bytes up to
+    // a whole number of stages (see launch_tap_table)
+    const uint32_t* taps;
 };
 
 // Dense split-K GEMM on the same core (the inner-product layer):
@@ -135,6 +139,11 @@ constexpr int kGemmMinTK = 16;
 // its partial P[split][g][m][col] to p.Y (see launch_conv_split_reduce_*).
 hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool tap_major,
                                 hipStream_t s);
+
+// Tap offsets of the channel-major order r = c*kh*kw + u*kw + v:
+// T[r] = (c*IHW + u*IW + v) * 4 for r < R, T[r] = oob for R <= r < rpad.
+hipError_t launch_tap_table(uint32_t* T, int rpad, int R, int kh, int kw, int IHW, int IW,
+                            uint32_t oob, hipStream_t s);
 
 // Forward weights W[G*M][Cg][khw] -> Wp[g][r][m] in the reduction order
 // r = ((c / tk) * khw + t) * tk + c % tk (order > 0), r = t * Cg + c

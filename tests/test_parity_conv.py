@@ -280,3 +280,26 @@ def test_weight_gradient_quad_order(case, monkeypatch):
     _, dw0, db0 = cc.conv_backward(*args, need=("dw", "db"))
     torch.cuda.synchronize()
     assert torch.equal(dw, dw0) and torch.equal(db, db0)
+
+
+@pytest.mark.parametrize("case", [
+    (2, 3, 35, 35, 16, 11, 11, 4, 4, 0, 0, 1),    # every window inside: table offsets
+    (2, 5, 23, 21, 40, 4, 4, 3, 3, 1, 1, 1),      # padded: inner waves on the table
+    (3, 6, 9, 9, 10, 3, 3, 1, 1, 0, 0, 2),        # groups, ragged columns
+])
+def test_forward_tap_table(case, monkeypatch):
+    """The channel-major forward with its tap-offset table against the
+    oracle, and bit for bit against the scalar tap walk."""
+    N, C, H, W, K, kh, kw, sh, sw, ph, pw, g = case
+    rng = np.random.default_rng([93, N, C, H, W, K])
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    w = (rng.standard_normal((K, C // g, kh, kw)) * 0.3).astype(np.float32)
+    b = rng.standard_normal(K).astype(np.float32)
+    y_ref = oracle.conv_forward(x, w, b, (sh, sw), (ph, pw), g, True)
+    monkeypatch.setenv("CAFFE_CONV_TAP_TABLE", "1")
+    y = cc.conv_forward(_t(x), _t(w), _t(b), (sh, sw), (ph, pw), g, True)
+    assert_close(_np(y), y_ref, TOL_F32, "forward")
+    monkeypatch.setenv("CAFFE_CONV_TAP_TABLE", "0")
+    y0 = cc.conv_forward(_t(x), _t(w), _t(b), (sh, sw), (ph, pw), g, True)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y0)

@@ -149,16 +149,14 @@ void plan_splits(int M, int ncol, int R, int tile, int cus, int forced, int* spl
 }
 
 // Tile for a GEMM with M rows: the least padding of M; ties go to the first
-// tile of the pass's preference order (measured: the forward pass favours
-// 64-row tiles over 96-row ones, the data gradient the reverse).  `forced`
-// >= 0 picks a tile (profiling only).
-int pick_tile(int M, bool forward, int forced)
+// tile of the preference order (measured on CaffeNet's 192-row GEMMs at
+// N=256: 64-row tiles beat 96-row ones by 4% in the forward pass and by 13%
+// in the data gradient).  `forced` >= 0 picks a tile (profiling only).
+int pick_tile(int M, int forced)
 {
     if (forced >= 0 && forced < TILE_COUNT)
         return forced;
-    static const int fwd_order[] = {TILE_128x128, TILE_64x256, TILE_96x256, TILE_48x256};
-    static const int bwd_order[] = {TILE_128x128, TILE_96x256, TILE_64x256, TILE_48x256};
-    const int* order = forward ? fwd_order : bwd_order;
+    static const int order[] = {TILE_128x128, TILE_64x256, TILE_96x256, TILE_48x256};
     int best = order[0];
     double best_waste = 1e30;
     for (int i = 0; i < 4; ++i) {
@@ -182,7 +180,7 @@ int pick_dense_tile(int M, int forced)
         return forced;
     if ((double)((M + 127) / 128 * 128) <= 1.05 * M)
         return TILE_128x128;
-    return pick_tile(M, true, -1);
+    return pick_tile(M, -1);
 }
 
 // Weight-gradient tile: the least padding of Kg, then the taller tile.
@@ -441,8 +439,8 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     if (part_bytes > kMaxTensorBytes)
         return fail(CAFFE_ERR_UNSUPPORTED, "weight-gradient partials reach 2^31 bytes");
 
-    q.fwd_tile = pick_tile(q.Kg, true, env_tile("CAFFE_CONV_FWD_TILE"));
-    q.dgrad_tile = pick_tile(q.Mt, false, env_tile("CAFFE_CONV_DGRAD_TILE"));
+    q.fwd_tile = pick_tile(q.Kg, env_tile("CAFFE_CONV_FWD_TILE"));
+    q.dgrad_tile = pick_tile(q.Mt, env_tile("CAFFE_CONV_DGRAD_TILE"));
     // defaults from measurement: the channel-blocked order and the XCD tile
     // order help the forward / data-gradient GEMMs; the weight gradient keeps
     // the linear tile order (its split partials gain nothing from it)

@@ -303,3 +303,19 @@ def test_forward_tap_table(case, monkeypatch):
     y0 = cc.conv_forward(_t(x), _t(w), _t(b), (sh, sw), (ph, pw), g, True)
     torch.cuda.synchronize()
     assert torch.equal(y, y0)
+
+
+@pytest.mark.parametrize("tile", [-1, 1, 3])
+def test_data_gradient_192_rows_masked(tile, monkeypatch):
+    """192 gathered rows per group (conv4/conv5's data gradient): the default
+    tile choice, the 96-row and the 64-row tiles, with the bottom mask."""
+    monkeypatch.setenv("CAFFE_CONV_DGRAD_TILE", str(tile))
+    rng = np.random.default_rng(23)
+    N, C, H, W, K, g = 2, 384, 7, 6, 32, 2
+    x = np.maximum(rng.standard_normal((N, C, H, W)), 0).astype(np.float32)
+    w = (rng.standard_normal((K, C // g, 3, 3)) * 0.1).astype(np.float32)
+    gd = rng.standard_normal((N, K, H, W)).astype(np.float32)
+    dx_ref, _, _ = oracle.conv_backward(x, w, gd, stride=1, pad=1, group=g, need=("dx",))
+    dx, _, _ = cc.conv_backward(_t(x), _t(w), _t(gd), None, 1, 1, g, False, need=("dx",),
+                                flags=cc.BACKWARD_MASK_BOTTOM_DIFF)
+    assert_close(_np(dx), dx_ref * (x > 0), TOL_F32, "masked data gradient")

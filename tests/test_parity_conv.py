@@ -89,9 +89,10 @@ def test_data_gradient_phase_stacked_row_heights():
         run_case(2, C, 29, 31, 6, k, k, s, s, 1, 2, 1, True)
 
 
-def test_empty_batch():
-    x = torch.empty((0, 4, 9, 9), device=DEV)
-    w = torch.randn((6, 2, 3, 3), device=DEV)
+@pytest.mark.parametrize("C", [4, 8])  # 8: 4 channels per group, the quad-order weight gradient
+def test_empty_batch(C):
+    x = torch.empty((0, C, 9, 9), device=DEV)
+    w = torch.randn((6, C // 2, 3, 3), device=DEV)
     y = cc.conv_forward(x, w, torch.zeros(6, device=DEV), 1, 1, 2, True)
     assert y.shape == (0, 6, 9, 9)
     g = torch.empty(y.shape, device=DEV)

@@ -686,6 +686,7 @@ int run_data(const ConvPlan& q, const float* dsrc, const float* bottom_mask, con
     p.Cg_out = q.Cg;
     p.blocked = q.blocked;
     p.xcd_order = q.xcd_order;
+    p.div_pss = make_fastdiv((uint32_t)(q.sh * q.sw)); p.div_psw = make_fastdiv((uint32_t)q.sw);
     if (q.dgrad_splits > 1) {
         float* part = (float*)(ws + q.off_part);
         ConvGemmParams pp = p;
@@ -889,6 +890,8 @@ int run_forward_bf16(const ConvPlan& q, const void* bottom, const void* weight, 
     p.relu = q.relu;
     p.Cout = q.K; p.OutH = q.Ho; p.OutW = q.Wo;
     p.xcd_order = q.xcd_order;
+    p.div_ohw = make_fastdiv((uint32_t)(q.Ho * q.Wo)); p.div_ow = make_fastdiv((uint32_t)q.Wo);
+    p.div_pss = make_fastdiv(1); p.div_psw = make_fastdiv(1);
     LAUNCH(launch_conv_gemm_bf16(p, 0, q.fwd_tile, q.fwd_pipe, s), "bf16 forward launch");
     return CAFFE_OK;
 }
@@ -922,6 +925,8 @@ int run_data_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom_mask
     p.psh = q.sh; p.psw = q.sw; p.a0h = q.a0h; p.a0w = q.a0w; p.oph = q.ph; p.opw = q.pw;
     p.Cg_out = q.Cg;
     p.xcd_order = q.xcd_order;
+    p.div_ohw = make_fastdiv((uint32_t)(q.Ah * q.Aw)); p.div_ow = make_fastdiv((uint32_t)q.Aw);
+    p.div_pss = make_fastdiv((uint32_t)(q.sh * q.sw)); p.div_psw = make_fastdiv((uint32_t)q.sw);
     LAUNCH(launch_conv_gemm_bf16(p, 1, q.dgrad_tile, q.dgrad_pipe, s),
            "bf16 data-gradient launch");
     return CAFFE_OK;

@@ -346,7 +346,7 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni) {
             const int col = n0 + brow + ni * MT;
-            const int n = col / OHW;
+            const int n = (int)fdiv((uint32_t)col, p.div_ohw);
             const int pix = col - n * OHW;
             cbase[ni] = n * p.Cout * OHW + pix;
             cbad[ni] = (uint32_t)(col >= p.Ncol) << 31;
@@ -376,9 +376,9 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
         for (int ni = 0; ni < NI; ++ni) {
             const int col = n0 + brow + ni * MT;
             const bool cok = col < p.Ncol;
-            const int n = cok ? col / OHW : 0;
+            const int n = cok ? (int)fdiv((uint32_t)col, p.div_ohw) : 0;
             const int pix = col - n * OHW;
-            const int a = pix / p.OW;
+            const int a = (int)fdiv((uint32_t)pix, p.div_ow);
             const int b = pix - a * p.OW;
             hb[ni] = cok ? p.psh * (a + p.a0h) - p.oph : -(1 << 28);
             wb[ni] = p.psw * (b + p.a0w) - p.opw;
@@ -396,9 +396,9 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
                 const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
                 int c = m, fh = 0, fw = 0;
                 if (pss != 1) {
-                    c = m / pss;
+                    c = (int)fdiv((uint32_t)m, p.div_pss);
                     const int fr = m - c * pss;
-                    fh = fr / p.psw;
+                    fh = (int)fdiv((uint32_t)fr, p.div_psw);
                     fw = fr - fh * p.psw;
                 }
 #pragma unroll

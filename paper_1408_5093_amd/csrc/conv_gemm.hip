@@ -544,9 +544,9 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
                     const int m = m0 + wm * MI * MT + mi * MT + WR::row(q, h);
                     int c = m, fh = 0, fw = 0;
                     if (pss != 1) {
-                        c = m / pss;
+                        c = (int)fdiv((uint32_t)m, p.div_pss);
                         const int fr = m - c * pss;
-                        fh = fr / p.psw;
+                        fh = (int)fdiv((uint32_t)fr, p.div_psw);
                         fw = fr - fh * p.psw;
                     }
                     const int hh = hb + fh;

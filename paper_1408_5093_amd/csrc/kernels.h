@@ -47,6 +47,7 @@ struct ConvGemmParams {
     int blocked;    // channel-blocked reduction order (else tap-major), with tap_major
     int xcd_order;  // XCD-contiguous tile order (else linear)
     int splits, stages_per_split;  // dense split-K GEMM only
+    FastDiv div_pss, div_psw;  // epi 1: phases psh*psw and psw
     // channel-major gathered operand (r = (c, u, v)) only, optional: byte
     // offsets (c*IH*IW + u*IW + v) * 4 of the taps r < R, then X_bytes up to
     // a whole number of stages (see launch_tap_table)
@@ -232,6 +233,9 @@ struct GemmBf16Params {
     int psh, psw, a0h, a0w, oph, opw, Cg_out;
     int xcd_order;
     FastDiv div_cg8, div_kw;
+    // epilogue divisions: output pixels per image and per row (epi 0 and 1),
+    // phases psh*psw and psw (epi 1)
+    FastDiv div_ohw, div_ow, div_pss, div_psw;
 };
 hipError_t launch_conv_gemm_bf16(const GemmBf16Params& p, int epi, int tile, int pipe,
                                  hipStream_t s);

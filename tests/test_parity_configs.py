@@ -149,3 +149,25 @@ def _glue_dy(net, l, st):
     if i + 1 < len(stages):
         return stages[i + 1]["dx"]
     return net.dbottom[l + 1].view(st["y"].shape)
+
+
+def test_caffenet_step_side_stream_matches_one_stream():
+    """The fp32 backward with the weight gradients on a side stream gives the
+    single-stream results bit for bit (same kernels, same inputs), over three
+    steps in a row."""
+    N = 8
+    inp = wl.caffenet_step(N)
+    x = torch.from_numpy(inp["x"]).to(DEV)
+    g = torch.from_numpy(inp["top_diff"]).to(DEV)
+    nets = [ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(),
+                      split_backward=split) for split in (True, False)]
+    for _ in range(3):
+        for net in nets:
+            net.forward(x)
+            net.backward(g)
+        torch.cuda.synchronize()
+        a, b = nets
+        for l in range(len(wl.CAFFENET)):
+            assert torch.equal(a.top[l], b.top[l])
+            assert torch.equal(a.dW[l], b.dW[l]) and torch.equal(a.db[l], b.db[l])
+            assert torch.equal(a.dbottom[l], b.dbottom[l])

@@ -75,6 +75,12 @@ def test_cast_bf16_round_to_nearest_even():
     # torch's own float -> bfloat16 conversion also rounds to nearest even
     ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
     np.testing.assert_array_equal(got, ref)
+    # eight values per thread and step, then the tail one by one
+    for n in (1, 7, 8, 9, 23, 4096 + 5):
+        bn = cc.cast_f32_to_bf16(_t(x[:n]))
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(bn.view(torch.int16).cpu().numpy().view(np.uint16),
+                                      wl.to_bf16_bits(x[:n]))
 
 
 def test_maxpool_relu_input_flag():

@@ -839,22 +839,31 @@ stage_narrow_bf16_kernel(const bf16_t* __restrict__ X, bf16_t* __restrict__ Xp, 
 }
 
 // Top-gradient staging: Dh = bf16(relu ? G [Y > 0] : G) channel-contiguous on
-// the zero-bordered Hp x Wp grid, one block per (image, 64 padded channels)
-// walking the image's bordered pixels 64 at a time.  Each thread also adds up
-// the fp32 masked gradient of its 16 channels at its pixels; one wave sum per
-// channel at the end (a fixed butterfly after a fixed per-lane order; the
-// border adds 0) gives sums[(g*Kg + k) * N + n], the image's bias-gradient
-// partial.
+// the zero-bordered Hp x Wp grid.  One block per (image, 64 padded channels,
+// run of kDiffPrepPixels bordered pixels), walking its run 64 pixels at a
+// time: each thread loads one pixel of 16 channels (all loads of a step
+// issued before any is used), the block transposes them through LDS and
+// writes 16-byte channel chunks.  Each thread also adds up the fp32 masked
+// gradient of its 16 channels; one wave sum per channel at the end (a fixed
+// butterfly after a fixed per-lane order; the border adds 0) gives
+// sums[(g*Kg + k) * T + n * runs + run] (T = N * runs), the partial
+// bias gradient of that run of the image.
+constexpr int kDiffPrepPixels = 512;
+
 __global__ void __launch_bounds__(256)
 diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
                       bf16_t* __restrict__ Dh, float* __restrict__ sums, int N, int K, int H,
                       int W, int Kg, int Kgp, int Ktot, int Hp, int Wp, int tb, int lb, int relu,
-                      int ctiles)
+                      int ctiles, int runs)
 {
     __shared__ bf16_t tile[64][66];
-    const int n = blockIdx.x / ctiles;
-    const int c0 = (blockIdx.x - n * ctiles) * 64;
+    const int run = blockIdx.x % runs;
+    const int nc = blockIdx.x / runs;
+    const int n = nc / ctiles;
+    const int c0 = (nc - n * ctiles) * 64;
     const int HWp = Hp * Wp;
+    const int p_begin = run * kDiffPrepPixels;
+    const int p_end = min(HWp, p_begin + kDiffPrepPixels);
     const int tid = threadIdx.x;
     const int px = tid & 63;
     const int cw = tid >> 6;
@@ -874,26 +883,26 @@ diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
 #pragma unroll
     for (int q = 0; q < 16; ++q)
         acc[q] = 0.f;
-    for (int p0 = 0; p0 < HWp; p0 += 64) {
+    for (int p0 = p_begin; p0 < p_end; p0 += 64) {
         const int pix = p0 + px;
         const int hp = pix / Wp;
         const int h = hp - tb;
         const int w = pix - hp * Wp - lb;
-        const bool inside = pix < HWp && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+        const bool inside = pix < p_end && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
         const size_t off = (size_t)h * W + w;
-        // all loads first, then the conversions
-        float d[16];
+        // every load of the step first (the ReLU output too), then the uses
+        float d[16], y[16];
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
             const bool ok = cok[q] && inside;
             d[q] = ok ? G[cbase[q] + off] : 0.f;
-            if (relu && ok && !(Y[cbase[q] + off] > 0.f))
-                d[q] = 0.f;
+            y[q] = relu && ok ? Y[cbase[q] + off] : 1.f;
         }
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
-            acc[q] += d[q];
-            tile[cw + 4 * q][px] = f32_to_bf16_rne(d[q]);
+            const float v = y[q] > 0.f ? d[q] : 0.f;  // (a NaN output masks too)
+            acc[q] += v;
+            tile[cw + 4 * q][px] = f32_to_bf16_rne(v);
         }
         __syncthreads();
 #pragma unroll
@@ -903,7 +912,7 @@ diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
             const int c8 = id & 7;
             const int pw = p0 + pl;
             const int cp = c0 + 8 * c8;
-            if (pw < HWp && cp < Ktot) {
+            if (pw < p_end && cp < Ktot) {
                 u32x4 v;
 #pragma unroll
                 for (int k = 0; k < 4; ++k)
@@ -915,13 +924,14 @@ diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
         __syncthreads();
     }
     if (sums) {
+        const size_t T = (size_t)N * runs;
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
             const float sm = wave_sum(acc[q]);
             if (px == 0 && cok[q]) {
                 const int cp = c0 + cw + 4 * q;
                 const int g = cp / Kgp;
-                sums[(size_t)(g * Kg + cp - g * Kgp) * N + n] = sm;
+                sums[(size_t)(g * Kg + cp - g * Kgp) * T + (size_t)n * runs + run] = sm;
             }
         }
     }
@@ -1177,7 +1187,10 @@ hipError_t launch_stage_nhwc_bf16(const uint16_t* X, uint16_t* Xp, int N, int C,
     return hipGetLastError();
 }
 
-int diff_prep_terms(int N, int /*HWp*/) { return N; }
+int diff_prep_terms(int N, int HWp)
+{
+    return N * std::max(1, (HWp + kDiffPrepPixels - 1) / kDiffPrepPixels);
+}
 
 hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, float* sums, int N,
                                  int K, int H, int W, int Kg, int Kgp, int Ktot, int Hp, int Wp,
@@ -1186,8 +1199,10 @@ hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, f
     if (N == 0)
         return hipSuccess;
     const int ctiles = (Ktot + 63) / 64;
-    hipLaunchKernelGGL(diff_prep_bf16_kernel, dim3((unsigned)((int64_t)ctiles * N)), dim3(256), 0,
-                       s, G, Y, Dh, sums, N, K, H, W, Kg, Kgp, Ktot, Hp, Wp, tb, lb, relu, ctiles);
+    const int runs = diff_prep_terms(N, Hp * Wp) / N;
+    hipLaunchKernelGGL(diff_prep_bf16_kernel, dim3((unsigned)((int64_t)ctiles * N * runs)),
+                       dim3(256), 0, s, G, Y, Dh, sums, N, K, H, W, Kg, Kgp, Ktot, Hp, Wp, tb, lb,
+                       relu, ctiles, runs);
     return hipGetLastError();
 }
 

@@ -289,7 +289,8 @@ hipError_t launch_stage_nhwc_bf16(const uint16_t* X, uint16_t* Xp, int N, int C,
 // Dh[n][hp][wp][g*Kgp + k] = bf16(relu ? G [Y > 0] : G)[n][g*Kg + k][hp - tb][wp - lb]
 // inside the H x W grid (k < Kg), else 0.  sums (may be null): the fp32
 // bias-gradient partials, sums[k*T + t] for T = diff_prep_terms(N, Hp*Wp)
-// terms per output channel (one per image).
+// terms per output channel (one per run of 512 bordered pixels of an image,
+// t = image * runs + run).
 int diff_prep_terms(int N, int HWp);
 hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, float* sums, int N,
                                  int K, int H, int W, int Kg, int Kgp, int Ktot, int Hp, int Wp,

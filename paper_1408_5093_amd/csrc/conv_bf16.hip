@@ -1040,13 +1040,13 @@ hipError_t launch_gemm_tile(const GemmBf16Params& p, int tile, hipStream_t s)
 {
     switch (tile) {
     case BTILE_128x256:
-        return launch_gemm<32, 1, 4, 4, 2, NS, EPI, MASK>(p, s);
+        return launch_gemm<32, 2, 4, 2, 2, NS, EPI, MASK>(p, s);
     case BTILE_96x256:
-        return launch_gemm<32, 1, 4, 3, 2, NS, EPI, MASK>(p, s);
+        return launch_gemm<32, 1, 8, 3, 1, NS, EPI, MASK>(p, s);
     case BTILE_64x256:
         return launch_gemm<32, 1, 4, 2, 2, NS, EPI, MASK>(p, s);
     case BTILE_48x256:
-        return launch_gemm<16, 1, 4, 3, 4, NS, EPI, MASK>(p, s);
+        return launch_gemm<16, 1, 8, 3, 2, NS, EPI, MASK>(p, s);
     default:
         return hipErrorInvalidValue;
     }

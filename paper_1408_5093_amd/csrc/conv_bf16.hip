@@ -475,7 +475,8 @@ conv_wgrad_bf16_kernel(const WgradBf16Params p)
     constexpr int EA = TKP / 8 / NW;   // row groups (8 pixels) per wave
     constexpr int NC = EA * (NLA + NLB);
     constexpr int CPP = (NC + KS - 1) / KS;
-    static_assert(NW == 4 && TM <= 128 && TN % 64 == 0 && EA == 2, "tile shape");
+    static_assert((NW == 4 || NW == 8) && TM <= 128 && TN % 64 == 0 && EA * NW * 8 == TKP,
+                  "tile shape");
     static_assert(NS == 2 || NS == 3, "buffers");
 
     __shared__ u32x4 A0[TKP * NLA * 8], A1[TKP * NLA * 8], A2[NS > 2 ? TKP * NLA * 8 : 1];
@@ -504,8 +505,8 @@ conv_wgrad_bf16_kernel(const WgradBf16Params p)
     const __amdgpu_buffer_rsrc_t rd = make_rsrc(p.D, p.D_bytes);
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, p.X_bytes);
 
-    // copies: this wave's row groups 2*wave + e (pixels 16*wave + 8e + lane/8
-    // of a stage), lane's chunk of a line (lane % 8) ^ chunk_swz(pixel).  Byte
+    // copies: this wave's row groups EA*wave + e (pixels 8*(EA*wave + e) +
+    // lane/8 of a stage), lane's chunk of a line (lane % 8) ^ chunk_swz(pixel).  Byte
     // offsets from a pixel: rows past Kg and columns past Rw are read (inside
     // the buffer or as zeros past its end) but feed only results that are
     // never stored, so they need no mask.
@@ -533,7 +534,7 @@ conv_wgrad_bf16_kernel(const WgradBf16Params p)
     auto pixels = [&](int t) {
 #pragma unroll
         for (int e = 0; e < EA; ++e) {
-            const int col = col_begin + t * TKP + 16 * wave + 8 * e + cr;
+            const int col = col_begin + t * TKP + 8 * (EA * wave + e) + cr;
             const int n = (int)fdiv((uint32_t)col, p.div_ohw);
             const int pix = col - n * OHW;
             const int i = (int)fdiv((uint32_t)pix, p.div_ow);
@@ -1119,9 +1120,9 @@ hipError_t launch_conv_wgrad_bf16(const WgradBf16Params& p, int tile, hipStream_
         return hipErrorInvalidValue;
     switch (tile) {
     case BWTILE_128x256:
-        return launch_wg<2, 2, 2, 4>(p, s);
+        return launch_wg<2, 4, 2, 2>(p, s);
     case BWTILE_96x256:
-        return launch_wg<1, 4, 3, 2>(p, s);
+        return launch_wg<1, 8, 3, 1>(p, s);
     default:
         return hipErrorInvalidValue;
     }

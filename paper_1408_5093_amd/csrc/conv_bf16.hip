@@ -868,9 +868,15 @@ diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
     const int tid = threadIdx.x;
     const int px = tid & 63;
     const int cw = tid >> 6;
-    const size_t plane = (size_t)H * W;
-    // this thread's 16 channels (cw + 4q) and whether they exist
-    size_t cbase[16];
+    const int plane = H * W;
+    // G and Y through buffer resources (both < 2^31 bytes): a missing channel
+    // or a border pixel is an out-of-range offset and reads 0
+    const uint32_t gbytes = (uint32_t)((size_t)N * K * plane * 4);
+    const __amdgpu_buffer_rsrc_t rg = make_rsrc(G, gbytes);
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(Y, relu ? gbytes : 0u);
+    // this thread's 16 channels (cw + 4q): byte offsets of their planes,
+    // 2^31 for a channel that does not exist
+    uint32_t cb4[16];
     bool cok[16];
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
@@ -878,7 +884,7 @@ diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
         const int g = cp / Kgp;
         const int k = cp - g * Kgp;
         cok[q] = cp < Ktot && k < Kg;
-        cbase[q] = ((size_t)n * K + g * Kg + k) * plane;
+        cb4[q] = cok[q] ? (uint32_t)((n * K + g * Kg + k) * plane) * 4u : kOob;
     }
     float acc[16];
 #pragma unroll
@@ -890,18 +896,22 @@ diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
         const int h = hp - tb;
         const int w = pix - hp * Wp - lb;
         const bool inside = pix < p_end && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
-        const size_t off = (size_t)h * W + w;
+        const uint32_t off4 = inside ? (uint32_t)(h * W + w) * 4u : 0u;
+        const uint32_t obad = inside ? 0u : kOob;
         // every load of the step first (the ReLU output too), then the uses
         float d[16], y[16];
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            const bool ok = cok[q] && inside;
-            d[q] = ok ? G[cbase[q] + off] : 0.f;
-            y[q] = relu && ok ? Y[cbase[q] + off] : 1.f;
+        for (int q = 0; q < 16; ++q)
+            d[q] = buf_ld_f32(rg, (cb4[q] + off4) | obad);
+        if (relu) {
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+                y[q] = buf_ld_f32(ry, (cb4[q] + off4) | obad);
         }
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
-            const float v = y[q] > 0.f ? d[q] : 0.f;  // (a NaN output masks too)
+            // (a NaN output masks too)
+            const float v = !relu || y[q] > 0.f ? d[q] : 0.f;
             acc[q] += v;
             tile[cw + 4 * q][px] = f32_to_bf16_rne(v);
         }

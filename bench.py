@@ -227,8 +227,9 @@ def lenet_training(wl, ConvStack, steps, warmup, stream, N=64):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
-              "the data-parallel design is described in DESIGN.md", file=sys.stderr)
+        print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}); the library "
+              "runs one GPU's share of a data-parallel step and does no collectives",
+              file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

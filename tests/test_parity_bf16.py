@@ -249,3 +249,23 @@ def test_caffenet_bf16_training_step_full_size():
                             images=images, filters=[L.K // 2], tol=TOL_BF16,
                             what=f"bf16 step {L.name} vs fp32 operands",
                             dx_mask=(xl > 0) if net.mask_bottom[l] else None)
+
+
+def test_backward_side_stream_fork_bf16(monkeypatch):
+    """A combined bf16 backward runs its weight gradient on the library's
+    second stream: bitwise the gradients of the one-stream order, on the
+    caller's stream once the call returns (three calls in a row)."""
+    rng = np.random.default_rng(83)
+    N, C, H, W, K, g = 3, 16, 11, 12, 40, 2
+    x = _t(rng.standard_normal((N, C, H, W)), torch.bfloat16)
+    w = _t(rng.standard_normal((K, C // g, 3, 3)) * 0.3, torch.bfloat16)
+    y = cc.conv_forward(x, w, _t(rng.standard_normal(K)), 1, 1, g, True)
+    gds = [_t(rng.standard_normal(y.shape)) for _ in range(3)]
+    out = {}
+    for fork in ("1", "0"):
+        monkeypatch.setenv("CAFFE_BACKWARD_FORK", fork)
+        out[fork] = [cc.conv_backward(x, w, gd, y, 1, 1, g, True) for gd in gds]
+    torch.cuda.synchronize()
+    for a, b in zip(out["1"], out["0"]):
+        for u, v in zip(a, b):
+            assert torch.equal(u, v)

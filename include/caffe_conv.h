@@ -49,9 +49,10 @@
  * stream), then returns: the results are ready when the stream reaches that
  * point.  Device faults therefore surface at the caller's next
  * synchronisation.  Calls on different streams that share no output or
- * workspace memory may run concurrently; the library holds no mutable global
- * state.  Results are bitwise reproducible run to run for the same
- * arguments (no atomics; every sum has a fixed order).
+ * workspace memory may run concurrently; the library's only global state is
+ * one auxiliary stream per device, created on first use by
+ * caffe_conv_backward.  Results are bitwise reproducible run to run for the
+ * same arguments (no atomics; every sum has a fixed order).
  *
  * Errors.  Every call returns CAFFE_OK (0) or a negative caffe_status and
  * then has enqueued nothing.  caffe_status_string() names a code;
@@ -156,7 +157,12 @@ enum caffe_backward_flags {
  * bias_diff may be NULL to skip it; bottom is required iff weight_diff is
  * given or flags has CAFFE_BACKWARD_MASK_BOTTOM_DIFF, weight iff bottom_diff
  * is given.  accumulate applies to weight_diff and bias_diff only; flags is a
- * set of caffe_backward_flags. */
+ * set of caffe_backward_flags.  In CAFFE_BF16 mode with both bottom_diff and
+ * weight_diff, the weight gradient runs on the device's auxiliary stream
+ * (default priority), which waits for `stream` after the top gradient is
+ * staged and which `stream` waits for before the call returns: the results
+ * are ordered on `stream` as always.  Not while `stream` is being captured
+ * into a graph, and not with the environment variable CAFFE_BACKWARD_FORK=0. */
 int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, const float* top,
                         const void* bottom, const void* weight, float* bottom_diff,
                         float* weight_diff, float* bias_diff, int32_t accumulate, int32_t flags,

@@ -222,16 +222,17 @@ class ConvStack:
             if split and (self.top_masked[l] or not L.relu):
                 ready = torch.cuda.Event()
                 ready.record(s)
-                self.side.wait_event(ready)
-                self._mark(("wgt", l, "begin"), self.side)
-                caffe_conv_backward(self.descs[l], g, top, bottom, self.W[l], None, self.dW[l],
-                                    self.db[l], 0, flags, self.ws_side, self.side)
-                self._mark(("wgt", l, "end"), self.side)
+                # the data gradient (on the critical path) goes out first
                 if want_dx:
                     self._mark(("bwd", l, "begin"), s)
                     caffe_conv_backward(self.descs[l], g, top, bottom, self.W[l],
                                         self.dbottom[l], None, None, 0, flags, self.ws_of[l], s)
                     self._mark(("bwd", l, "end"), s)
+                self.side.wait_event(ready)
+                self._mark(("wgt", l, "begin"), self.side)
+                caffe_conv_backward(self.descs[l], g, top, bottom, self.W[l], None, self.dW[l],
+                                    self.db[l], 0, flags, self.ws_side, self.side)
+                self._mark(("wgt", l, "end"), self.side)
             else:
                 self._mark(("bwd", l, "begin"), s)
                 caffe_conv_backward(self.descs[l], g, top, bottom, self.W[l],

@@ -676,8 +676,13 @@ lrn_pool_backward_kernel(const float* __restrict__ a_in, const float* __restrict
     __shared__ int32_t ms[kFuseCh][kFusePos];
     const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
     const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
-    const int strip = blockIdx.x % nstrips;
-    const int rest = blockIdx.x / nstrips;
+    // Workgroups are dispatched round-robin over the 8 XCDs, each with its own
+    // L2; neighbouring strips and channel chunks share halo rows and channels,
+    // so each XCD takes one contiguous range of the block order.
+    const int xcd = blockIdx.x & 7, per = gridDim.x >> 3, extra = gridDim.x & 7;
+    const int blk = xcd * per + min(xcd, extra) + (blockIdx.x >> 3);
+    const int strip = blk % nstrips;
+    const int rest = blk / nstrips;
     const int c0 = (rest % nchunks) * kFuseCh;
     const int n = rest / nchunks;
     const int y_lo = strip * yrows;

@@ -54,10 +54,20 @@
  * caffe_conv_backward.  Results are bitwise reproducible run to run for the
  * same arguments (no atomics; every sum has a fixed order).
  *
- * Errors.  Every call returns CAFFE_OK (0) or a negative caffe_status and
- * then has enqueued nothing.  caffe_status_string() names a code;
- * caffe_last_error() returns a thread-local message describing the last
- * failure on the calling thread.
+ * Errors.  Every call returns CAFFE_OK (0) or a negative caffe_status.  A
+ * call that fails its argument checks (every code but CAFFE_ERR_HIP) has
+ * enqueued nothing.  CAFFE_ERR_HIP means the HIP runtime refused a launch or
+ * a stream operation part-way through: the kernels the call had already
+ * enqueued on `stream` stay enqueued (the call's outputs are then undefined),
+ * and work it had forked to the auxiliary stream has finished before the
+ * call returns.  caffe_status_string() names a code; caffe_last_error()
+ * returns a thread-local message describing the last failure on the calling
+ * thread.
+ *
+ * Tuning.  Tile shapes, split counts and kernel variants are chosen from the
+ * descriptor alone.  Environment variables named CAFFE_CONV_*, CAFFE_FC_*,
+ * CAFFE_BF16_* and CAFFE_BACKWARD_FORK override those choices for profiling
+ * and tests, and are read only while CAFFE_PROFILE_OVERRIDES=1 is set.
  */
 #ifndef CAFFE_CONV_H
 #define CAFFE_CONV_H
@@ -106,6 +116,10 @@ int caffe_conv_out_shape(const caffe_conv_desc* desc, int32_t* Ho, int32_t* Wo);
 /* Bytes of device workspace that `pass` (a caffe_conv_pass) needs for this
  * descriptor; 0 is a valid answer.  Host-only. */
 int caffe_conv_workspace_size(const caffe_conv_desc* desc, int32_t pass, size_t* bytes);
+
+/* The same query returning the size: SIZE_MAX for an invalid descriptor or
+ * pass (caffe_last_error() then says why).  Host-only. */
+size_t caffe_conv_workspace_bytes(const caffe_conv_desc* desc, int32_t pass);
 
 /* Forward pass (Sec. 3.2): top = [relu](weight (*) bottom + bias).
  * bias may be NULL (no bias).  top is overwritten. */
@@ -162,7 +176,8 @@ enum caffe_backward_flags {
  * (default priority), which waits for `stream` after the top gradient is
  * staged and which `stream` waits for before the call returns: the results
  * are ordered on `stream` as always.  Not while `stream` is being captured
- * into a graph, and not with the environment variable CAFFE_BACKWARD_FORK=0. */
+ * into a graph, and not with CAFFE_BACKWARD_FORK=0 (read only while
+ * CAFFE_PROFILE_OVERRIDES=1). */
 int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, const float* top,
                         const void* bottom, const void* weight, float* bottom_diff,
                         float* weight_diff, float* bias_diff, int32_t accumulate, int32_t flags,
@@ -170,6 +185,9 @@ int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, cons
 
 /* Static name of a status code ("CAFFE_OK", ...). */
 const char* caffe_status_string(int32_t status);
+
+/* The same name under the convolution layer's prefix. */
+const char* caffe_conv_status_string(int32_t status);
 
 /* Thread-local text of the last error raised on this thread ("" if none). */
 const char* caffe_last_error(void);

@@ -44,6 +44,7 @@ EXPORTS = (
     "caffe_lrn_forward", "caffe_lrn_backward", "caffe_cast_f32_to_bf16",
     "caffe_sgd_learning_rate", "caffe_softmax_loss", "caffe_sgd_update",
     "caffe_pool_lrn_forward", "caffe_lrn_pool_backward", "caffe_sgd_update_device_lr",
+    "caffe_conv_workspace_bytes", "caffe_conv_status_string",
 )
 
 
@@ -121,8 +122,11 @@ def load():
         f = getattr(lib, name)
         f.argtypes = args
         f.restype = ctypes.c_int
-    lib.caffe_status_string.argtypes = [i32]
-    lib.caffe_status_string.restype = ctypes.c_char_p
+    for name in ("caffe_status_string", "caffe_conv_status_string"):
+        getattr(lib, name).argtypes = [i32]
+        getattr(lib, name).restype = ctypes.c_char_p
+    lib.caffe_conv_workspace_bytes.argtypes = [cdp, i32]
+    lib.caffe_conv_workspace_bytes.restype = sz
     lib.caffe_last_error.argtypes = []
     lib.caffe_last_error.restype = ctypes.c_char_p
     lib.caffe_version.argtypes = []

@@ -203,10 +203,21 @@ int pick_wgrad_tile(int Kg, int forced)
     return best;
 }
 
-// Profiling override of a tuning choice (tile index, block target): an
-// integer from the environment, -1 when unset.
+// Profiling override of a tuning choice (tile index, split count, kernel
+// variant): an integer from the environment, -1 when unset.  The variables
+// are read only while CAFFE_PROFILE_OVERRIDES=1 is set, so that a stray
+// CAFFE_* variable cannot change what a default call runs (the kernel, the
+// split count and with it the summation order).
+bool overrides_enabled()
+{
+    const char* v = getenv("CAFFE_PROFILE_OVERRIDES");
+    return v && v[0] == '1' && v[1] == '\0';
+}
+
 int env_tile(const char* name)
 {
+    if (!overrides_enabled())
+        return -1;
     const char* v = getenv(name);
     return v && *v ? atoi(v) : -1;
 }
@@ -1024,6 +1035,12 @@ int join_side(hipStream_t s, Fork& f, int st_a, int st_b)
 {
     const hipError_t e1 = hipEventRecord(f.done, f.side);
     const hipError_t e2 = e1 == hipSuccess ? hipStreamWaitEvent(s, f.done, 0) : e1;
+    if (e2 != hipSuccess) {
+        // s cannot be made to wait for the side stream: drain the side stream
+        // here, so that no kernel of this call still reads or writes the
+        // caller's buffers or workspace once the error is returned
+        (void)hipStreamSynchronize(f.side);
+    }
     hipEventDestroy(f.start);
     hipEventDestroy(f.done);
     if (st_a != CAFFE_OK)
@@ -1231,6 +1248,16 @@ const char* caffe_status_string(int32_t status)
     case CAFFE_ERR_HIP: return "CAFFE_ERR_HIP";
     default: return "CAFFE_ERR_UNKNOWN";
     }
+}
+
+const char* caffe_conv_status_string(int32_t status) { return caffe_status_string(status); }
+
+size_t caffe_conv_workspace_bytes(const caffe_conv_desc* desc, int32_t pass)
+{
+    size_t bytes = 0;
+    if (caffe_conv_workspace_size(desc, pass, &bytes) != CAFFE_OK)
+        return SIZE_MAX;
+    return bytes;
 }
 
 const char* caffe_last_error(void) { return g_err; }

@@ -136,7 +136,10 @@ class ConvStack:
                 self.fused[l] = pool_lrn_supported(st[0]["in_shape"], p["kernel"], p["stride"],
                                                    p.get("pad", 0), r["size"], r["alpha"],
                                                    r["beta"], r["k"])
-        # when a list, (tag, event) pairs are recorded around every conv call
+        # when a list, (tag, event) pairs are recorded around every conv call:
+        # tag = (kind, layer, "begin" | "end") with kind "fwd" (forward),
+        # "bwd" (data gradient), "wgt" (weight and bias gradients) or "both"
+        # (both gradients in one call)
         self.events = None
 
     def _mark(self, tag, s):
@@ -234,11 +237,14 @@ class ConvStack:
                                     self.db[l], 0, flags, self.ws_side, self.side)
                 self._mark(("wgt", l, "end"), self.side)
             else:
-                self._mark(("bwd", l, "begin"), s)
+                # one call for both gradients ("both"), or for the weight
+                # gradient alone ("wgt") when no data gradient is wanted
+                tag = "both" if want_dx else "wgt"
+                self._mark((tag, l, "begin"), s)
                 caffe_conv_backward(self.descs[l], g, top, bottom, self.W[l],
                                     self.dbottom[l] if want_dx else None, self.dW[l], self.db[l],
                                     0, flags, self.ws_of[l], s)
-                self._mark(("bwd", l, "end"), s)
+                self._mark((tag, l, "end"), s)
             g = self.dbottom[l]
         if split:
             # the next forward overwrites what the side stream reads

@@ -16,3 +16,12 @@ def pytest_configure(config):
 @pytest.fixture(scope="session")
 def golden_dir():
     return os.path.join(ROOT, "tests", "golden")
+
+
+@pytest.fixture
+def overrides(monkeypatch):
+    """monkeypatch with the library's tuning overrides switched on
+    (CAFFE_PROFILE_OVERRIDES=1): tests that force a kernel variant, tile or
+    split count set the CAFFE_* variables through it."""
+    monkeypatch.setenv("CAFFE_PROFILE_OVERRIDES", "1")
+    return monkeypatch

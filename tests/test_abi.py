@@ -38,6 +38,39 @@ def test_status_strings():
                        (-3, b"CAFFE_ERR_WORKSPACE"), (-4, b"CAFFE_ERR_UNSUPPORTED"),
                        (-5, b"CAFFE_ERR_HIP")]:
         assert lib.caffe_status_string(code) == name
+        assert lib.caffe_conv_status_string(code) == name
+    assert lib.caffe_conv_status_string(-99) == b"CAFFE_ERR_UNKNOWN"
+
+
+def test_workspace_bytes_matches_workspace_size():
+    """caffe_conv_workspace_bytes returns what caffe_conv_workspace_size
+    stores, and SIZE_MAX for an invalid descriptor or pass."""
+    lib = cc.load()
+    size_max = ctypes.c_size_t(-1).value
+    for dt in (cc.CAFFE_F32, cc.CAFFE_BF16):
+        d = cc.conv_desc((256, 96, 27, 27), (256, 48, 5, 5), 1, 2, 2, True, dt)
+        for pass_ in range(4):
+            assert lib.caffe_conv_workspace_bytes(ctypes.byref(d), pass_) == \
+                cc.conv_workspace_size(d, pass_)
+        assert lib.caffe_conv_workspace_bytes(ctypes.byref(d), 9) == size_max
+    bad = _desc(group=3)
+    assert lib.caffe_conv_workspace_bytes(ctypes.byref(bad), 0) == size_max
+    assert lib.caffe_conv_workspace_bytes(None, 0) == size_max
+    assert lib.caffe_last_error() != b""
+
+
+def test_tuning_overrides_need_the_switch(monkeypatch):
+    """A CAFFE_* tuning variable changes nothing unless
+    CAFFE_PROFILE_OVERRIDES=1: the quad-order weight gradient's column table
+    (part of conv2's weight-gradient workspace) is planned either way, and
+    only the switch lets CAFFE_CONV_WGRAD_QUAD=0 drop it."""
+    d = cc.conv_desc((256, 96, 27, 27), (256, 48, 5, 5), 1, 2, 2, True)
+    default = cc.conv_workspace_size(d, cc.PASS_BACKWARD_WEIGHTS)
+    monkeypatch.delenv("CAFFE_PROFILE_OVERRIDES", raising=False)
+    monkeypatch.setenv("CAFFE_CONV_WGRAD_QUAD", "0")
+    assert cc.conv_workspace_size(d, cc.PASS_BACKWARD_WEIGHTS) == default
+    monkeypatch.setenv("CAFFE_PROFILE_OVERRIDES", "1")
+    assert cc.conv_workspace_size(d, cc.PASS_BACKWARD_WEIGHTS) < default
 
 
 @pytest.mark.parametrize("x,w,s,p,g,out", [

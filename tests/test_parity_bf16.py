@@ -251,7 +251,7 @@ def test_caffenet_bf16_training_step_full_size():
                             dx_mask=(xl > 0) if net.mask_bottom[l] else None)
 
 
-def test_backward_side_stream_fork_bf16(monkeypatch):
+def test_backward_side_stream_fork_bf16(overrides):
     """A combined bf16 backward runs its weight gradient on the library's
     second stream: bitwise the gradients of the one-stream order, on the
     caller's stream once the call returns (three calls in a row)."""
@@ -263,7 +263,7 @@ def test_backward_side_stream_fork_bf16(monkeypatch):
     gds = [_t(rng.standard_normal(y.shape)) for _ in range(3)]
     out = {}
     for fork in ("1", "0"):
-        monkeypatch.setenv("CAFFE_BACKWARD_FORK", fork)
+        overrides.setenv("CAFFE_BACKWARD_FORK", fork)
         out[fork] = [cc.conv_backward(x, w, gd, y, 1, 1, g, True) for gd in gds]
     torch.cuda.synchronize()
     for a, b in zip(out["1"], out["0"]):

@@ -217,21 +217,21 @@ SPLIT_CASES = [
 @pytest.mark.parametrize("case", SPLIT_CASES)
 @pytest.mark.parametrize("splits", [2, 5])
 @pytest.mark.parametrize("blocked", ["1", "0"])
-def test_split_k(case, splits, blocked, monkeypatch):
+def test_split_k(case, splits, blocked, overrides):
     """Forced split counts (profiling overrides) on both reduction orders:
     each split starts its walk mid-reduction, the reduce applies the
     epilogue."""
-    monkeypatch.setenv("CAFFE_CONV_FWD_SPLITS", str(splits))
-    monkeypatch.setenv("CAFFE_CONV_DGRAD_SPLITS", str(splits))
-    monkeypatch.setenv("CAFFE_CONV_BLOCKED", blocked)
+    overrides.setenv("CAFFE_CONV_FWD_SPLITS", str(splits))
+    overrides.setenv("CAFFE_CONV_DGRAD_SPLITS", str(splits))
+    overrides.setenv("CAFFE_CONV_BLOCKED", blocked)
     run_case(*case, relu=True, bias=True)
     run_case(*case, relu=False, bias=False, seed=1)
 
 
-def test_split_k_masked_bottom_and_default_plan(monkeypatch):
+def test_split_k_masked_bottom_and_default_plan(overrides):
     # the bottom mask applied by the data-gradient reduce; then a shape whose
     # own plan splits (one image, a long reduction)
-    monkeypatch.setenv("CAFFE_CONV_DGRAD_SPLITS", "3")
+    overrides.setenv("CAFFE_CONV_DGRAD_SPLITS", "3")
     rng = np.random.default_rng(31)
     x = np.maximum(rng.standard_normal((2, 16, 10, 10)), 0).astype(np.float32)
     w = rng.standard_normal((32, 16, 3, 3)).astype(np.float32)
@@ -240,7 +240,7 @@ def test_split_k_masked_bottom_and_default_plan(monkeypatch):
     dx, _, _ = cc.conv_backward(_t(x), _t(w), _t(g), None, 1, 1, 1, False, need=("dx",),
                                 flags=cc.BACKWARD_MASK_BOTTOM_DIFF)
     assert_close(_np(dx), dx_ref * (x > 0), TOL_F32, "masked data gradient")
-    monkeypatch.delenv("CAFFE_CONV_DGRAD_SPLITS")
+    overrides.delenv("CAFFE_CONV_DGRAD_SPLITS")
     run_case(1, 64, 6, 6, 64, 5, 5, 1, 1, 2, 2, 1, True)
 
 
@@ -259,11 +259,11 @@ QUAD_CASES = [
 
 
 @pytest.mark.parametrize("case", QUAD_CASES)
-def test_weight_gradient_quad_order(case, monkeypatch):
+def test_weight_gradient_quad_order(case, overrides):
     """The quad-order kernel against the oracle, and bit for bit against the
     channel-major kernel (same sums, same order; only the tile columns are
     permuted)."""
-    monkeypatch.setenv("CAFFE_CONV_WGRAD_QUAD", "1")
+    overrides.setenv("CAFFE_CONV_WGRAD_QUAD", "1")
     N, C, H, W, K, kh, kw, sh, sw, ph, pw, g = case
     rng = np.random.default_rng([91, N, C, H, W, K])
     x = rng.standard_normal((N, C, H, W)).astype(np.float32)
@@ -277,7 +277,7 @@ def test_weight_gradient_quad_order(case, monkeypatch):
     _, dw, db = cc.conv_backward(*args, need=("dw", "db"))
     assert_close(_np(dw), dw_ref, TOL_F32, "weight gradient")
     assert_close(_np(db), db_ref, TOL_F32, "bias gradient")
-    monkeypatch.setenv("CAFFE_CONV_WGRAD_QUAD", "0")
+    overrides.setenv("CAFFE_CONV_WGRAD_QUAD", "0")
     _, dw0, db0 = cc.conv_backward(*args, need=("dw", "db"))
     torch.cuda.synchronize()
     assert torch.equal(dw, dw0) and torch.equal(db, db0)
@@ -288,7 +288,7 @@ def test_weight_gradient_quad_order(case, monkeypatch):
     (2, 5, 23, 21, 40, 4, 4, 3, 3, 1, 1, 1),      # padded: inner waves on the table
     (3, 6, 9, 9, 10, 3, 3, 1, 1, 0, 0, 2),        # groups, ragged columns
 ])
-def test_forward_tap_table(case, monkeypatch):
+def test_forward_tap_table(case, overrides):
     """The channel-major forward with its tap-offset table against the
     oracle, and bit for bit against the scalar tap walk."""
     N, C, H, W, K, kh, kw, sh, sw, ph, pw, g = case
@@ -297,20 +297,20 @@ def test_forward_tap_table(case, monkeypatch):
     w = (rng.standard_normal((K, C // g, kh, kw)) * 0.3).astype(np.float32)
     b = rng.standard_normal(K).astype(np.float32)
     y_ref = oracle.conv_forward(x, w, b, (sh, sw), (ph, pw), g, True)
-    monkeypatch.setenv("CAFFE_CONV_TAP_TABLE", "1")
+    overrides.setenv("CAFFE_CONV_TAP_TABLE", "1")
     y = cc.conv_forward(_t(x), _t(w), _t(b), (sh, sw), (ph, pw), g, True)
     assert_close(_np(y), y_ref, TOL_F32, "forward")
-    monkeypatch.setenv("CAFFE_CONV_TAP_TABLE", "0")
+    overrides.setenv("CAFFE_CONV_TAP_TABLE", "0")
     y0 = cc.conv_forward(_t(x), _t(w), _t(b), (sh, sw), (ph, pw), g, True)
     torch.cuda.synchronize()
     assert torch.equal(y, y0)
 
 
 @pytest.mark.parametrize("tile", [-1, 1, 3])
-def test_data_gradient_192_rows_masked(tile, monkeypatch):
+def test_data_gradient_192_rows_masked(tile, overrides):
     """192 gathered rows per group (conv4/conv5's data gradient): the default
     tile choice, the 96-row and the 64-row tiles, with the bottom mask."""
-    monkeypatch.setenv("CAFFE_CONV_DGRAD_TILE", str(tile))
+    overrides.setenv("CAFFE_CONV_DGRAD_TILE", str(tile))
     rng = np.random.default_rng(23)
     N, C, H, W, K, g = 2, 384, 7, 6, 32, 2
     x = np.maximum(rng.standard_normal((N, C, H, W)), 0).astype(np.float32)

@@ -127,6 +127,24 @@ int caffe_conv_forward(const caffe_conv_desc* desc, const void* bottom, const vo
                        const float* bias, float* top, void* workspace, size_t ws_bytes,
                        void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * caffe_conv_forward with its workspace taken from a static device array the
+ * library owns, CAFFE_CONV_NOALLOC_SCRATCH_BYTES per device (each GPU the
+ * library runs on keeps its copy until the process ends).  The call
+ * allocates nothing; the caller still provides bottom, weight, bias and top.
+ * Returns CAFFE_ERR_WORKSPACE when the forward pass needs more workspace
+ * than that (caffe_conv_workspace_size with CAFFE_PASS_FORWARD tells in
+ * advance), e.g. bf16 operands at CaffeNet conv1's size, whose staged input
+ * alone is larger.  The first call on a device looks up the array's address
+ * (a one-time set-up; nothing is allocated).  Every call on one device uses
+ * the same array, and nothing in it needs to start at zero: calls that may
+ * overlap in time on one device (different streams, or several host threads)
+ * race on it, so the caller serialises them. */
+#define CAFFE_CONV_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int caffe_conv_forward_noalloc(const caffe_conv_desc* desc, const void* bottom,
+                               const void* weight, const float* bias, float* top, void* stream);
+
 /* Backward pass w.r.t. the input (Sec. 3.2): bottom_diff = adjoint(D).
  * top is the forward output and is required iff desc->relu; it is read only
  * for the mask [top > 0].  bottom_diff is overwritten. */

@@ -15,7 +15,7 @@ import torch
 
 from . import _lib
 from ._lib import (  # noqa: F401
-    CAFFE_ERR_UNSUPPORTED, BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF,
+    CAFFE_ERR_UNSUPPORTED, CAFFE_ERR_WORKSPACE, NOALLOC_SCRATCH_BYTES, BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF,
     BACKWARD_TOP_DIFF_MASKED, CAFFE_BF16, CAFFE_F32, CAFFE_LR_EXP,
     CAFFE_LR_FIXED, CAFFE_LR_INV, CAFFE_LR_STEP, LrSchedule, PASS_BACKWARD,
     PASS_BACKWARD_DATA, PASS_BACKWARD_WEIGHTS, PASS_FORWARD, POOL_RELU_INPUT, CaffeError, ConvDesc,

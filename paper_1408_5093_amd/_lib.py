@@ -30,6 +30,8 @@ PASS_BACKWARD_DATA = 1
 PASS_BACKWARD_WEIGHTS = 2
 PASS_BACKWARD = 3
 
+NOALLOC_SCRATCH_BYTES = 64 << 20  # CAFFE_CONV_NOALLOC_SCRATCH_BYTES
+
 CAFFE_LR_FIXED = 0
 CAFFE_LR_STEP = 1
 CAFFE_LR_EXP = 2
@@ -44,7 +46,7 @@ EXPORTS = (
     "caffe_lrn_forward", "caffe_lrn_backward", "caffe_cast_f32_to_bf16",
     "caffe_sgd_learning_rate", "caffe_softmax_loss", "caffe_sgd_update",
     "caffe_pool_lrn_forward", "caffe_lrn_pool_backward", "caffe_sgd_update_device_lr",
-    "caffe_conv_workspace_bytes", "caffe_conv_status_string",
+    "caffe_conv_workspace_bytes", "caffe_conv_status_string", "caffe_conv_forward_noalloc",
 )
 
 
@@ -100,6 +102,7 @@ def load():
         "caffe_conv_out_shape": [cdp, pi32, pi32],
         "caffe_conv_workspace_size": [cdp, i32, ctypes.POINTER(sz)],
         "caffe_conv_forward": [cdp, vp, vp, vp, vp, vp, sz, vp],
+        "caffe_conv_forward_noalloc": [cdp, vp, vp, vp, vp, vp],
         "caffe_conv_backward_data": [cdp, vp, vp, vp, vp, vp, sz, vp],
         "caffe_conv_backward_weights": [cdp, vp, vp, vp, vp, vp, i32, vp, sz, vp],
         "caffe_conv_backward": [cdp, vp, vp, vp, vp, vp, vp, vp, i32, i32, vp, sz, vp],

@@ -1158,6 +1158,27 @@ int caffe_conv_forward(const caffe_conv_desc* desc, const void* bottom, const vo
     return run_forward(q, bottom, weight, bias, top, (char*)workspace, (hipStream_t)stream);
 }
 
+int caffe_conv_forward_noalloc(const caffe_conv_desc* desc, const void* bottom,
+                               const void* weight, const float* bias, float* top, void* stream)
+{
+    static_assert(CAFFE_CONV_NOALLOC_SCRATCH_BYTES == caffe_hip::kStaticScratchBytes,
+                  "header and library agree on the scratch size");
+    ConvPlan q;
+    CHECK(plan_conv(desc, &q));
+    if (q.ws_fwd > caffe_hip::kStaticScratchBytes)
+        return fail(CAFFE_ERR_WORKSPACE,
+                    "the forward pass needs %zu bytes of workspace; the static scratch holds %zu",
+                    q.ws_fwd, caffe_hip::kStaticScratchBytes);
+    void* ws = nullptr;
+    if (q.ws_fwd > 0) {
+        const hipError_t e = caffe_hip::static_scratch_address(&ws);
+        if (e != hipSuccess)
+            return hip_fail(e, "static scratch lookup");
+    }
+    // the same checks and kernels as caffe_conv_forward, on the static buffer
+    return caffe_conv_forward(desc, bottom, weight, bias, top, ws, q.ws_fwd, stream);
+}
+
 int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, const float* top,
                         const void* bottom, const void* weight, float* bottom_diff,
                         float* weight_diff, float* bias_diff, int32_t accumulate, int32_t flags,

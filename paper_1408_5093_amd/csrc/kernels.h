@@ -15,6 +15,12 @@ struct FastDiv {
 };
 FastDiv make_fastdiv(uint32_t d);
 
+// Bytes of the library's static per-device scratch array (the workspace of
+// caffe_conv_forward_noalloc) and the current device's address of it, looked
+// up on the first call on each device.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+hipError_t static_scratch_address(void** ptr);
+
 // Implicit GEMM whose reduction index r = (c, u, v) walks a kh x kw window of
 // a gather source X[N][Cin][IH][IW] and whose column index walks the output
 // grid (n, i, j) in N x OH x OW:

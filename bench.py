@@ -10,19 +10,25 @@ before the timed region starts.
 
 Prints one JSON line.  `value` is the convolution FLOPs of a step (forward +
 data gradient + weight gradient, 2 per multiply-add) divided by the wall
-time of the whole step, glue included.
+time of the whole step, glue included.  The same line carries the other
+workloads as objects of their own: the LeNet conv pair (N=64), CaffeNet
+conv1's forward pass and conv2-5's forward passes (N=256), and the conv1-5
+step at N=512 with bfloat16 operands.
 """
 import argparse
 import json
 import os
-import platform
 import sys
+import threading
 import time
 
 METRIC = ("conv-stack TFLOP/s (% of MFMA peak) + images/sec, CaffeNet conv1-5 fwd+bwd, N=256")
-FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
+FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix peak (256 CUs at 2.4 GHz)
 BF16_MFMA_PEAK_TFLOPS = 2516.6  # MI355X dense bf16 matrix peak (no sparsity)
+SPEC_SCLK_MHZ = 2400.0
 HBM_PEAK_GBS = 8000.0
+PAPER_CONTEXT = ("over 40 million images per day, about 2.5 ms per image, on one NVIDIA K40 or "
+                 "Titan (whole system; model, batch and pass not stated): context, not a target")
 
 
 def parse():
@@ -31,8 +37,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--batch", type=int, default=256)
-    ap.add_argument("--bf16", action="store_true", help="bfloat16 operands (N=512 workload)")
-    ap.add_argument("--cpu-images", type=int, default=192,
+    ap.add_argument("--bf16", action="store_true",
+                    help="time the bfloat16 step (N=512 workload) as the headline (profiling)")
+    ap.add_argument("--cpu-images", type=int, default=256,
                     help="images in the CPU-oracle baseline sample (0 = skip)")
     ap.add_argument("--network-steps", type=int, default=-1,
                     help="steps of the whole-network step (conv1-5, pool5, fc6-fc8) timed "
@@ -40,26 +47,173 @@ def parse():
     ap.add_argument("--network-only", action="store_true",
                     help="time only the whole-network step (profiling); the JSON line then "
                          "carries its images/s as the value")
+    ap.add_argument("--configs", choices=("all", "none"), default="all",
+                    help="also time the LeNet pair, conv1 forward, conv2-5 forward and bf16 "
+                         "workloads (none: the headline step only, for profiling)")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="only the warm-up and timed steps of the headline workload: no "
+                         "serialized pass, clock sampling, other workloads or CPU baseline (for "
+                         "kernel traces and counter runs, whose per-step figures then cover the "
+                         "timed steps alone)")
+    ap.add_argument("--one-stream", action="store_true",
+                    help="issue the fp32 weight gradients on the caller's stream in the timed "
+                         "steps too (measurement of the overlap)")
     ap.add_argument("--calibrate-copy-mb", type=int, default=0,
                     help="first run one plain device copy of this many MiB (a known-size "
                          "reference for the HBM byte counters)")
     return ap.parse_args()
 
 
-def traffic_record(kernel_source):
-    """HBM bytes per launch of the dominant kernel, as measured with the
+# ------------------------------------------------------------ accounting
+def call_flops(kind, L, N):
+    """FLOPs of one library call: one pass, or two for a combined backward."""
+    return (2 if kind == "both" else 1) * L.flops(N)
+
+
+def kernel_of(kind, L, bf16):
+    """The GEMM kernel(s) a call of this kind runs for layer L."""
+    if bf16:
+        return {"fwd": "conv_gemm_bf16_kernel (forward)",
+                "bwd": "conv_gemm_bf16_kernel (data gradient)",
+                "wgt": "conv_wgrad_bf16_kernel",
+                "both": "conv_gemm_bf16_kernel (data gradient) + conv_wgrad_bf16_kernel"}[kind]
+    if L.H == 1 and L.W == 1 and L.k == 1:
+        return "dense_gemm (inner product)"
+    quad = (L.C // L.g) % 4 == 0 and L.k in (3, 5)
+    wgt = "conv_wgrad_quad_f32_kernel" if quad else "conv_wgrad_f32_kernel"
+    return {"fwd": "conv_gemm_f32_kernel (forward)",
+            "bwd": "conv_gemm_f32_kernel (data gradient)",
+            "wgt": wgt,
+            "both": f"conv_gemm_f32_kernel (data gradient) + {wgt}"}[kind]
+
+
+def timed_steps(step, stream, steps, net=None):
+    """Run `steps` steps between two events on `stream`; with `net`, also
+    the mean duration of every library call (events around each call, on
+    the stream it is issued on) and the time covered by at least one call."""
+    import torch
+    import numpy as np
+    if net is not None:
+        net.events = []
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record(stream)
+    for _ in range(steps):
+        step()
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = start.elapsed_time(end) / steps
+    if net is None:
+        return ms, wall, None, None
+    acc, spans = {}, []
+    evs, net.events = net.events, None
+    for i in range(0, len(evs), 2):
+        (tb, eb), (te, ee) = evs[i], evs[i + 1]
+        assert tb[:2] == te[:2] and tb[2] == "begin" and te[2] == "end"
+        acc.setdefault(tb[:2], []).append(eb.elapsed_time(ee))
+        spans.append((start.elapsed_time(eb), start.elapsed_time(ee)))
+    covered, reach = 0.0, float("-inf")
+    for b0, b1 in sorted(spans):
+        if b1 > reach:
+            covered += b1 - max(b0, reach)
+            reach = b1
+    return ms, wall, {k: float(np.mean(v)) for k, v in acc.items()}, covered / steps
+
+
+def roofline(call_ms, layers, N, peak, bf16, sclk=None):
+    """Roofline record of the dominant call: the call with the largest mean
+    duration per step in the timed region (each runs one GEMM kernel, plus
+    small table/reduce kernels counted in its duration)."""
+    key = max(call_ms, key=call_ms.get)
+    kind, l = key
+    L = layers[l]
+    flops = call_flops(kind, L, N)
+    ach = flops / (call_ms[key] * 1e-3) / 1e12
+    rec = {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+           "frac": ach / peak, "traffic": None, "call": f"{kind}_{L.name}",
+           "kernel": f"{kernel_of(kind, L, bf16)}, {L.name}",
+           "kernel_ms": call_ms[key], "flops_per_launch": flops}
+    if sclk:
+        p = peak * sclk / SPEC_SCLK_MHZ
+        rec["peak_at_observed_sclk"] = p
+        rec["frac_at_observed_sclk"] = ach / p
+    return rec
+
+
+def traffic_record(call, batch, bf16):
+    """HBM bytes per launch of a call's GEMM kernel, as measured with the
     FETCH_SIZE / WRITE_SIZE counters and committed under profiles/ -- or None
-    when the kernel's source has changed since that measurement."""
+    when none was measured for it or its source has changed since."""
     import hashlib
     here = os.path.dirname(os.path.abspath(__file__))
     try:
-        rec = json.load(open(os.path.join(here, "profiles", "traffic.json")))
-        src = open(os.path.join(here, kernel_source), "rb").read()
+        recs = json.load(open(os.path.join(here, "profiles", "traffic.json")))
     except (OSError, ValueError):
         return None
-    if rec.get("source_sha256") != hashlib.sha256(src).hexdigest():
+    for rec in recs.get("kernels", []):
+        if rec.get("call") != call or rec.get("batch") != batch or rec.get("bf16", False) != bf16:
+            continue
+        try:
+            src = open(os.path.join(here, rec["source"]), "rb").read()
+        except (OSError, KeyError):
+            return None
+        if rec.get("source_sha256") != hashlib.sha256(src).hexdigest():
+            return None
+        return rec
+    return None
+
+
+def observed_sclk(work, bus_id):
+    """Median graphics clock (MHz, mean over the XCDs) that the SMU reports
+    while `work` runs and the device is at least 90% busy, sampled every
+    20 ms through amdsmi for the device on PCI bus `bus_id`.  The SMU
+    refreshes these metrics about once a second, so `work` should run for
+    a few seconds.  None when amdsmi or the device cannot be read."""
+    try:
+        import amdsmi
+        amdsmi.amdsmi_init()
+    except Exception:
+        work()
         return None
-    return rec
+    try:
+        handle = None
+        for h in amdsmi.amdsmi_get_processor_handles():
+            bdf = amdsmi.amdsmi_get_gpu_device_bdf(h)
+            if int(bdf.split(":")[1], 16) == bus_id:
+                handle = h
+        if handle is None:
+            work()
+            return None
+        samples, stop = [], threading.Event()
+
+        def poll():
+            while not stop.is_set():
+                try:
+                    m = amdsmi.amdsmi_get_gpu_metrics_info(handle)
+                    clks = [float(c) for c in m.get("current_gfxclks", []) if isinstance(c, (int, float))]
+                    if clks and float(m.get("average_gfx_activity", 0)) >= 90:
+                        samples.append(sum(clks) / len(clks))
+                except Exception:
+                    pass
+                time.sleep(0.02)
+
+        t = threading.Thread(target=poll, daemon=True)
+        t.start()
+        work()
+        stop.set()
+        t.join()
+        samples.sort()
+        return samples[len(samples) // 2] if samples else None
+    except Exception:
+        return None
+    finally:
+        try:
+            amdsmi.amdsmi_shut_down()
+        except Exception:
+            pass
 
 
 def caffenet_glue(wl):
@@ -67,6 +221,7 @@ def caffenet_glue(wl):
             1: [("pool", wl.CAFFENET_POOL), ("lrn", wl.CAFFENET_LRN)]}
 
 
+# ------------------------------------------------------------ CPU baseline
 def cpu_baseline(inp, wl, n_img):
     """The oracle, as it stands, on the first n_img images of the same batch:
     forward and backward of conv1..5 with the same glue."""
@@ -107,49 +262,41 @@ def cpu_baseline(inp, wl, n_img):
                 break
     except OSError:
         pass
+    n_all = inp["x"].shape[0]
+    which = "all" if n_img >= n_all else f"the first {n_img}"
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
             "kind": "oracle", "images_per_s": n_img / dt, "seconds": dt, "cpu": cpu,
-            "sample": f"CaffeNet conv1-5 fwd + bwd (with pool/LRN glue) on the first {n_img} "
-                      f"of the step's 256 seeded images, plain fp64 loops, OpenMP"}
+            "sample": f"CaffeNet conv1-5 fwd + bwd (with pool/LRN glue) on {which} {n_img} of the "
+                      f"step's {n_all} seeded images (full batch: {n_img >= n_all}), plain fp64 "
+                      f"loops, OpenMP"}
 
 
+# ------------------------------------------------------------ other workloads
 def network_step(wl, ConvStack, N, steps, warmup, stream):
     """The whole CaffeNet chain -- conv1-5 with their glue, max-pool after
     conv5, the fc6-fc8 inner products -- forward and backward from a
     synthetic fc8 top gradient: images/s and per-layer call times."""
-    import numpy as np
     import torch
     print(f"[bench] whole-network step N={N}", file=sys.stderr, flush=True)
     inp = wl.caffenet_net_step(N)
     net = ConvStack(wl.CAFFENET_NET, N, inp["W"], inp["b"], glue=wl.CAFFENET_NET_GLUE)
     x = torch.from_numpy(inp["x"]).cuda()
     g = torch.from_numpy(inp["top_diff"]).cuda()
+
+    def step():
+        net.forward(x, stream)
+        net.backward(g, stream)
+
     for _ in range(warmup):
-        net.forward(x, stream)
-        net.backward(g, stream)
-    torch.cuda.synchronize()
-    net.events = []
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for _ in range(steps):
-        net.forward(x, stream)
-        net.backward(g, stream)
-    end.record(stream)
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / steps
-    acc = {}
-    evs, net.events = net.events, None
-    for i in range(0, len(evs), 2):
-        (tb, eb), (_, ee) = evs[i], evs[i + 1]
-        acc.setdefault(tb[:2], []).append(eb.elapsed_time(ee))
+        step()
+    ms, _, call_ms, _ = timed_steps(step, stream, steps, net)
     flops = sum(3 * L.flops(N) for L in wl.CAFFENET_NET)
     return {"workload": ("CaffeNet conv1-5 + max-pool + fc6-fc8 (ReLU on fc6, fc7) forward + "
                          "data, weight and bias gradients"),
             "global_batch": N, "ms_per_step": ms, "images_per_s": N / (ms * 1e-3),
             "tflops": flops / (ms * 1e-3) / 1e12, "flops_per_step": flops,
-            "breakdown_ms": {f"{k[0]}_{wl.CAFFENET_NET[k[1]].name}": round(float(np.mean(v)), 4)
-                             for k, v in sorted(acc.items())}}
+            "breakdown_ms": {f"{k[0]}_{wl.CAFFENET_NET[k[1]].name}": round(v, 4)
+                             for k, v in sorted(call_ms.items())}}
 
 
 def shard_step(wl, ConvStack, steps, warmup, stream, N=32):
@@ -162,19 +309,14 @@ def shard_step(wl, ConvStack, steps, warmup, stream, N=32):
     net = ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(wl))
     x = torch.from_numpy(inp["x"]).cuda()
     g = torch.from_numpy(inp["top_diff"]).cuda()
+
+    def step():
+        net.forward(x, stream)
+        net.backward(g, stream)
+
     for _ in range(warmup):
-        net.forward(x, stream)
-        net.backward(g, stream)
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for _ in range(steps):
-        net.forward(x, stream)
-        net.backward(g, stream)
-    end.record(stream)
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / steps
+        step()
+    ms, _, _, _ = timed_steps(step, stream, steps)
     flops = sum(3 * L.flops(N) for L in wl.CAFFENET)
     return {"workload": "CaffeNet conv1-5 training step on a 32-image shard", "global_batch": N,
             "ms_per_step": ms, "images_per_s": N / (ms * 1e-3),
@@ -196,32 +338,138 @@ def lenet_training(wl, ConvStack, steps, warmup, stream, N=64):
     y = torch.from_numpy(inp["labels"][0]).cuda()
     for _ in range(warmup):
         tr.step(x, y, stream)
-    torch.cuda.synchronize()
-
-    def timed(fn):
-        start = torch.cuda.Event(enable_timing=True)
-        end = torch.cuda.Event(enable_timing=True)
-        start.record(stream)
-        for _ in range(steps):
-            fn()
-        end.record(stream)
-        torch.cuda.synchronize()
-        return start.elapsed_time(end) / steps
-
-    ms_eager = timed(lambda: tr.step(x, y, stream))
+    ms_eager, _, _, _ = timed_steps(lambda: tr.step(x, y, stream), stream, steps)
     # the same iteration captured once as a HIP graph and replayed (the
     # per-launch host cost of ~40 small kernels is what the eager loop pays)
     tr.capture(x, y)
     for _ in range(warmup):
         tr.replay()
-    torch.cuda.synchronize()
-    ms = timed(tr.replay)
+    ms, _, _, _ = timed_steps(tr.replay, stream, steps)
     return {"workload": ("LeNet training iteration: conv1, max-pool, conv2, max-pool, ip1 + ReLU, "
                          "ip2, softmax loss, backward, SGD (momentum 0.9, decay 5e-4, inv "
                          "schedule), replayed as one captured HIP graph"),
             "global_batch": N, "ms_per_step": ms, "images_per_s": N / (ms * 1e-3),
             "ms_per_step_eager": ms_eager, "images_per_s_eager": N / (ms_eager * 1e-3),
             "final_loss": float(tr.loss.item())}
+
+
+def rate_record(workload, N, ms, flops, peak, dtype, **extra):
+    r = {"workload": workload, "global_batch": N, "dtype": dtype, "ms_per_step": ms,
+         "tflops": flops / (ms * 1e-3) / 1e12, "flops_per_step": flops,
+         "pct_mfma_peak": 100.0 * flops / (ms * 1e-3) / 1e12 / peak,
+         "images_per_s": N / (ms * 1e-3)}
+    r.update(extra)
+    return r
+
+
+def lenet_pair(wl, ConvStack, steps, warmup, stream, N=64):
+    """LeNet conv pair (conv1, 2x2/2 max-pool, conv2), fp32, N=64: forward
+    and backward (data, weight and bias gradients of both layers) from an
+    N(0, 1) top gradient."""
+    import torch
+    print(f"[bench] LeNet conv pair N={N}", file=sys.stderr, flush=True)
+    inp = wl.lenet_pair(N)
+    net = ConvStack(wl.LENET, N, inp["W"], inp["b"], glue={0: [("pool", wl.LENET_POOL)]})
+    x = torch.from_numpy(inp["x"]).cuda()
+    g = torch.from_numpy(inp["top_diff"]).cuda()
+
+    def step():
+        net.forward(x, stream)
+        net.backward(g, stream)
+
+    for _ in range(warmup):
+        step()
+    ms, _, _, _ = timed_steps(step, stream, steps)
+    flops = sum(3 * L.flops(N) for L in wl.LENET)
+    return rate_record("LeNet conv pair: conv1 20x5x5, 2x2/2 max-pool, conv2 50x5x5, forward + "
+                       "data, weight and bias gradients", N, ms, flops, FP32_MFMA_PEAK_TFLOPS,
+                       "f32")
+
+
+def forward_only(cc, layers, inputs, steps, warmup, stream, N):
+    """Forward passes of `layers` on their own seeded inputs: per layer and
+    in all, each call timed on its own between events."""
+    import torch
+    per = {}
+    total_ms, total_flops = 0.0, 0
+    for L, inp in zip(layers, inputs):
+        d = cc.conv_desc((N, L.C, L.H, L.W), (L.K, L.C // L.g, L.k, L.k), L.s, L.p, L.g, L.relu)
+        Ho, Wo = cc.conv_out_shape(d)
+        x = torch.from_numpy(inp["x"]).cuda()
+        w = torch.from_numpy(inp["W"]).cuda()
+        b = torch.from_numpy(inp["b"]).cuda()
+        y = torch.empty((N, L.K, Ho, Wo), device="cuda")
+        ws = cc.Workspace().get(cc.conv_workspace_size(d, cc.PASS_FORWARD))
+
+        def call():
+            cc.caffe_conv_forward(d, x, w, b, y, ws, stream)
+
+        for _ in range(warmup):
+            call()
+        ms, _, _, _ = timed_steps(call, stream, steps)
+        flops = L.flops(N)
+        per[L.name] = {"ms": ms, "tflops": flops / (ms * 1e-3) / 1e12,
+                       "pct_mfma_peak": 100.0 * flops / (ms * 1e-3) / 1e12 / FP32_MFMA_PEAK_TFLOPS}
+        total_ms += ms
+        total_flops += flops
+        del x, w, b, y, ws
+    return total_ms, total_flops, per
+
+
+def conv1_forward(cc, wl, steps, warmup, stream, N=256):
+    print(f"[bench] CaffeNet conv1 forward N={N}", file=sys.stderr, flush=True)
+    ms, flops, _ = forward_only(cc, wl.CAFFENET[:1], [wl.caffenet_conv1_fwd(N)], steps, warmup,
+                                stream, N)
+    return rate_record("CaffeNet conv1 forward: 3x227x227 -> 96x55x55, 11x11 stride 4, bias + "
+                       "fused ReLU", N, ms, flops, FP32_MFMA_PEAK_TFLOPS, "f32")
+
+
+def conv25_forward(cc, wl, steps, warmup, stream, N=256):
+    print(f"[bench] CaffeNet conv2-5 forward N={N}", file=sys.stderr, flush=True)
+    ms, flops, per = forward_only(cc, wl.CAFFENET[1:],
+                                  [wl.caffenet_conv25_layer(l, N) for l in range(1, 5)], steps,
+                                  warmup, stream, N)
+    return rate_record("CaffeNet conv2-5 forward, each layer on its own half-normal input, bias "
+                       "0.1 + fused ReLU (ms_per_step = the four calls back to back)", N, ms, flops,
+                       FP32_MFMA_PEAK_TFLOPS, "f32", per_layer=per)
+
+
+def conv_step(cc, wl, ConvStack, N, bf16, steps, warmup, stream, one_stream=False,
+              serialized=True):
+    """The conv1-5 training step: per-step time, per-call durations, the
+    roofline of the dominant call, and (fp32) the same calls issued one
+    stream (each call alone on the device)."""
+    import torch
+    workload = wl.CAFFENET_STEP_BF16 if bf16 else wl.CAFFENET_STEP
+    print(f"[bench] generating seeded inputs N={N}{' bf16' if bf16 else ''}", file=sys.stderr,
+          flush=True)
+    inp = wl.caffenet_step(N, workload)
+    if bf16:
+        inp["x"] = wl.round_bf16(inp["x"])
+    net = ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(wl), bf16=bf16)
+    net.serial = one_stream
+    x = torch.from_numpy(inp["x"]).cuda()
+    g = torch.from_numpy(inp["top_diff"]).cuda()
+
+    def step():
+        net.forward(x, stream)
+        net.backward(g, stream)
+
+    print(f"[bench] warmup {warmup}", file=sys.stderr, flush=True)
+    for _ in range(warmup):
+        step()
+    ms, wall, call_ms, covered = timed_steps(step, stream, steps, net)
+    print(f"[bench] {steps} steps, {ms:.3f} ms/step", file=sys.stderr, flush=True)
+    out = {"inp": inp, "net": net, "x": x, "g": g, "step": step, "ms": ms, "wall": wall,
+           "call_ms": call_ms, "covered": covered}
+    if serialized and not bf16 and not one_stream:
+        net.serial = True
+        for _ in range(2):
+            step()
+        _, _, out["call_ms_serial"], _ = timed_steps(step, stream, steps, net)
+        net.serial = False
+        print("[bench] serialized calls timed", file=sys.stderr, flush=True)
+    return out
 
 
 def main():
@@ -232,7 +480,6 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
     import paper_1408_5093_amd as cc
@@ -243,9 +490,8 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(3)
+    stream = torch.cuda.current_stream()
     if args.network_only:
-        from paper_1408_5093_amd import workloads as wl
-        stream = torch.cuda.current_stream()
         r = network_step(wl, ConvStack, args.batch, args.steps, args.warmup, stream)
         print(json.dumps({"metric": "CaffeNet whole-network training images/s", "value":
                           r["images_per_s"], "unit": "images/s", "n_gpus": 1, "steps": args.steps,
@@ -255,16 +501,6 @@ def main():
                               "workload": r["workload"], "global_batch": args.batch},
                           "network": r}), flush=True)
         return
-    N = args.batch if not args.bf16 or args.batch != 256 else 512
-    workload = wl.CAFFENET_STEP_BF16 if args.bf16 else wl.CAFFENET_STEP
-    print(f"[bench] generating seeded inputs N={N}", file=sys.stderr, flush=True)
-    inp = wl.caffenet_step(N, workload)
-    if args.bf16:
-        inp["x"] = wl.round_bf16(inp["x"])
-    net = ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(wl), bf16=args.bf16)
-    x = torch.from_numpy(inp["x"]).cuda()
-    g = torch.from_numpy(inp["top_diff"]).cuda()
-    stream = torch.cuda.current_stream()
     if args.calibrate_copy_mb > 0:
         n = args.calibrate_copy_mb * (1 << 20) // 4
         src = torch.ones(n, device="cuda")
@@ -273,70 +509,54 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    def step():
-        net.forward(x, stream)
-        net.backward(g, stream)
-
-    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    # timed region: events around every convolution call, on the library's stream
-    net.events = []
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    start.record(stream)
-    for _ in range(args.steps):
-        step()
-    end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    ms_step = start.elapsed_time(end) / args.steps
-    print(f"[bench] {args.steps} steps, {ms_step:.3f} ms/step", file=sys.stderr, flush=True)
-
-    # per-call durations (ms), averaged over the timed steps
-    # (the weight-gradient calls, "wgt", run on a second stream beside the
-    # data gradients: conv_ms is the time covered by at least one call)
-    acc = {}
-    spans = []
-    evs = net.events
-    net.events = None
-    for i in range(0, len(evs), 2):
-        (tag_b, eb), (tag_e, ee) = evs[i], evs[i + 1]
-        assert tag_b[:2] == tag_e[:2] and tag_b[2] == "begin" and tag_e[2] == "end"
-        acc.setdefault(tag_b[:2], []).append(eb.elapsed_time(ee))
-        spans.append((start.elapsed_time(eb), start.elapsed_time(ee)))
-    call_ms = {k: float(np.mean(v)) for k, v in acc.items()}
-    covered, reach = 0.0, float("-inf")
-    for b0, b1 in sorted(spans):
-        if b1 > reach:
-            covered += b1 - max(b0, reach)
-            reach = b1
-
+    bf16 = args.bf16
+    N = args.batch if not bf16 or args.batch != 256 else 512
+    peak = BF16_MFMA_PEAK_TFLOPS if bf16 else FP32_MFMA_PEAK_TFLOPS
+    if args.headline_only:
+        args.configs, args.network_steps, args.cpu_images = "none", 0, 0
+    run = conv_step(cc, wl, ConvStack, N, bf16, args.steps, args.warmup, stream,
+                    one_stream=args.one_stream, serialized=not args.headline_only)
+    ms_step, call_ms = run["ms"], run["call_ms"]
     flops_step = sum(3 * L.flops(N) for L in wl.CAFFENET)
-    conv_ms = covered / args.steps
-    peak = BF16_MFMA_PEAK_TFLOPS if args.bf16 else FP32_MFMA_PEAK_TFLOPS
     tflops = flops_step / (ms_step * 1e-3) / 1e12
 
-    # roofline of the dominant single-kernel call: the slowest forward (one
-    # implicit-GEMM launch per call)
-    fwd = {k: v for k, v in call_ms.items() if k[0] == "fwd"}
-    kdom = max(fwd, key=fwd.get)
-    Ldom = wl.CAFFENET[kdom[1]]
-    ach = Ldom.flops(N) / (fwd[kdom] * 1e-3) / 1e12
-    rec = traffic_record("paper_1408_5093_amd/csrc/conv_gemm.hip")
-    traffic = None
-    if rec and rec.get("layer") == Ldom.name and rec.get("batch") == N and not args.bf16:
-        traffic = rec["bytes_per_launch"]
-    roofline = {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
-                "frac": ach / peak, "traffic": traffic,
-                "kernel": f"conv_gemm (forward, {Ldom.name})",
-                "kernel_ms": fwd[kdom], "flops_per_launch": Ldom.flops(N)}
+    # graphics clock while the same steps run again (not part of the timed region)
+    props = torch.cuda.get_device_properties(0)
+    nsclk = max(1, int(2.5 / (ms_step * 1e-3)))
 
-    breakdown = {f"{k[0]}_{wl.CAFFENET[k[1]].name}": round(v, 4) for k, v in sorted(call_ms.items())}
+    def clock_work():
+        for i in range(nsclk):
+            run["step"]()
+            if i % 20 == 19:  # keep the host close to the device
+                torch.cuda.synchronize()
+        torch.cuda.synchronize()
+
+    sclk = None
+    if not args.headline_only:
+        sclk = observed_sclk(clock_work, getattr(props, "pci_bus_id", -1))
+        print(f"[bench] observed sclk {sclk} MHz", file=sys.stderr, flush=True)
+
+    roof = roofline(call_ms, wl.CAFFENET, N, peak, bf16, sclk)
+    roof["traffic"] = (traffic_record(roof["call"], N, bf16) or {}).get("bytes_per_launch")
+    roof["duration_source"] = ("HIP events around the call on the stream it is issued on, mean "
+                               "over the timed steps (the call's small table and reduce kernels "
+                               "included)")
+    ser = run.get("call_ms_serial")
+    if ser:
+        key = next(k for k in ser if f"{k[0]}_{wl.CAFFENET[k[1]].name}" == roof["call"])
+        a = call_flops(key[0], wl.CAFFENET[key[1]], N) / (ser[key] * 1e-3) / 1e12
+        roof["serialized"] = {"kernel_ms": ser[key], "achieved": a, "frac": a / peak}
+        dom = roofline(ser, wl.CAFFENET, N, peak, bf16, sclk)
+        roof["dominant_serialized"] = {k: dom[k] for k in ("call", "kernel", "kernel_ms",
+                                                           "achieved", "frac")}
+        roof["note"] = ("kernel_ms is the call's duration in the timed steps, where the weight "
+                        "gradients run on a second stream beside the data gradients and both "
+                        "stretch; 'serialized' times the same calls issued one after another on "
+                        "one stream")
+
+    def names(d):
+        return {f"{k[0]}_{wl.CAFFENET[k[1]].name}": round(v, 4) for k, v in sorted(d.items())}
+
     out = {
         "metric": METRIC,
         "value": tflops,
@@ -348,32 +568,61 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if args.bf16 else "f32",
+        "dtype": "bf16" if bf16 else "f32",
         "data": "synthetic (seeded N(0,50) pixels, N(0,0.01) weights, N(0,1e-3) top gradient)",
         "config": {"workload": ("CaffeNet conv1-5 training step: forward (bias+ReLU) + data, "
                                 "weight and bias gradients, 3x3/2 max-pool + LRN(5) glue after "
                                 "conv1 and conv2"),
                    "global_batch": N, "image": "3x227x227",
-                   "operands": "bf16" if args.bf16 else "fp32", "accumulate": "fp32"},
+                   "operands": "bf16" if bf16 else "fp32", "accumulate": "fp32",
+                   "weight_gradient_stream": "caller's" if args.one_stream else "second"},
         "images_per_s": N / (ms_step * 1e-3),
         "pct_mfma_peak": 100.0 * tflops / peak,
-        "conv_tflops_in_conv_calls": flops_step / (conv_ms * 1e-3) / 1e12,
-        "conv_calls_ms_per_step": conv_ms,
+        "observed_sclk_mhz": sclk,
+        "pct_mfma_peak_at_observed_sclk": (100.0 * tflops / (peak * sclk / SPEC_SCLK_MHZ)
+                                           if sclk else None),
+        "conv_tflops_in_conv_calls": flops_step / (run["covered"] * 1e-3) / 1e12,
+        "conv_calls_ms_per_step": run["covered"],
         "flops_per_step": flops_step,
-        "wall_s": wall,
-        "breakdown_ms": breakdown,
-        "roofline": roofline,
+        "wall_s": run["wall"],
+        "breakdown_ms": names(call_ms),
+        "roofline": roof,
         "cpu_baseline": None,
+        "paper_context": PAPER_CONTEXT,
     }
+    if ser:
+        out["breakdown_ms_serialized"] = names(ser)
+    inp = run["inp"]
+    del run
+    torch.cuda.empty_cache()
+
+    if args.configs == "all" and not bf16:
+        out["lenet_pair"] = lenet_pair(wl, ConvStack, 10 * args.steps, args.warmup, stream)
+        out["conv1_forward"] = conv1_forward(cc, wl, 2 * args.steps, args.warmup, stream)
+        out["conv2_5_forward"] = conv25_forward(cc, wl, 2 * args.steps, args.warmup, stream)
+        torch.cuda.empty_cache()
+        b = conv_step(cc, wl, ConvStack, 512, True, args.steps, args.warmup, stream,
+                      serialized=False)
+        bflops = sum(3 * L.flops(512) for L in wl.CAFFENET)
+        br = rate_record("CaffeNet conv1-5 training step with bfloat16 inputs and weights, fp32 "
+                         "accumulation and outputs, same glue", 512, b["ms"], bflops,
+                         BF16_MFMA_PEAK_TFLOPS, "bf16", breakdown_ms=names(b["call_ms"]))
+        br["roofline"] = roofline(b["call_ms"], wl.CAFFENET, 512, BF16_MFMA_PEAK_TFLOPS, True,
+                                  sclk)
+        br["roofline"]["traffic"] = (traffic_record(br["roofline"]["call"], 512, True)
+                                     or {}).get("bytes_per_launch")
+        out["bf16_step_n512"] = br
+        del b
+        torch.cuda.empty_cache()
     nsteps = args.steps if args.network_steps < 0 else args.network_steps
-    if nsteps > 0 and not args.bf16:
+    if nsteps > 0 and not bf16:
         out["network"] = network_step(wl, ConvStack, N, nsteps, args.warmup, stream)
         out["lenet_training"] = lenet_training(wl, ConvStack, 10 * nsteps, args.warmup, stream)
         out["shard_n32"] = shard_step(wl, ConvStack, nsteps, args.warmup, stream)
     if args.cpu_images > 0:
-        print(f"[bench] CPU oracle baseline on {args.cpu_images} images", file=sys.stderr,
-              flush=True)
-        out["cpu_baseline"] = cpu_baseline(inp, wl, args.cpu_images)
+        n = min(args.cpu_images, N)
+        print(f"[bench] CPU oracle baseline on {n} images", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(inp, wl, n)
     print(json.dumps(out), flush=True)
 
 

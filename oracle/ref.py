@@ -5,6 +5,7 @@ before the call and every result is float64.  The C library states the
 definitions it implements (Caffe, Sec. 3.2 layer forward/backward roles; the
 textbook strided, padded, grouped cross-correlation for convolution).
 """
+import contextlib
 import ctypes
 
 import numpy as np
@@ -12,13 +13,28 @@ import numpy as np
 from .build import ensure_built
 
 _lib = None
+_lib_path = None  # another build of caffe_ref.c (see library())
 _dp = ctypes.POINTER(ctypes.c_double)
+
+
+@contextlib.contextmanager
+def library(path):
+    """Inside the block, every wrapper below calls the oracle library built
+    at `path` instead of libcaffe_ref.so (the planted-mistake tests build
+    altered copies of caffe_ref.c and run the pins against them)."""
+    global _lib, _lib_path
+    saved = _lib, _lib_path
+    _lib, _lib_path = None, path
+    try:
+        yield
+    finally:
+        _lib, _lib_path = saved
 
 
 def _load():
     global _lib
     if _lib is None:
-        lib = ctypes.CDLL(ensure_built())
+        lib = ctypes.CDLL(_lib_path or ensure_built())
         i = ctypes.c_int
         d = ctypes.c_double
         lib.caffe_ref_num_threads.restype = i

@@ -105,6 +105,10 @@ class ConvStack:
         if self.split_backward:
             self.side = torch.cuda.Stream(device=dev)
             self.ws_side = Workspace(dev).get(max(ws_weights, 1))
+        # serial = True keeps the separate data- and weight-gradient calls but
+        # issues both on the caller's stream (measurement: each call then has
+        # the device to itself; the results are the same bits)
+        self.serial = False
         self.bottom = [None] * len(self.layers)
         # Fused ReLU backward passes.  A ReLU output that feeds a max-pool gets
         # its backward folded into the pool's routing (CAFFE_POOL_RELU_INPUT);
@@ -231,11 +235,15 @@ class ConvStack:
                     caffe_conv_backward(self.descs[l], g, top, bottom, self.W[l],
                                         self.dbottom[l], None, None, 0, flags, self.ws_of[l], s)
                     self._mark(("bwd", l, "end"), s)
-                self.side.wait_event(ready)
-                self._mark(("wgt", l, "begin"), self.side)
+                if self.serial:
+                    wstream, wspace = s, self.ws_of[l]
+                else:
+                    wstream, wspace = self.side, self.ws_side
+                    wstream.wait_event(ready)
+                self._mark(("wgt", l, "begin"), wstream)
                 caffe_conv_backward(self.descs[l], g, top, bottom, self.W[l], None, self.dW[l],
-                                    self.db[l], 0, flags, self.ws_side, self.side)
-                self._mark(("wgt", l, "end"), self.side)
+                                    self.db[l], 0, flags, wspace, wstream)
+                self._mark(("wgt", l, "end"), wstream)
             else:
                 # one call for both gradients ("both"), or for the weight
                 # gradient alone ("wgt") when no data gradient is wanted

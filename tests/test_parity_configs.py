@@ -98,6 +98,15 @@ def test_caffenet_network_step_full_size():
     _run_and_check_step(net, wl.CAFFENET_NET, inp, images=[0, 200])
 
 
+def _tile_filters(L):
+    """One filter in every 64 rows of every group (the weight-gradient row
+    tiles are 64, 96 or 128 rows) and each group's last filter."""
+    Kg = L.K // L.g
+    if L.H == 1 and L.W == 1:  # inner products: first and last
+        return [0, L.K - 1]
+    return sorted({t * Kg + m for t in range(L.g) for m in list(range(0, Kg, 64)) + [Kg - 1]})
+
+
 def _run_and_check_step(net, layers, inp, images):
     x = torch.from_numpy(inp["x"]).to(DEV)
     g = torch.from_numpy(inp["top_diff"]).to(DEV)
@@ -109,7 +118,7 @@ def _run_and_check_step(net, layers, inp, images):
         gl = _np(net.layer_top_diff(l, g))
         check_layer_sampled(L, xl, inp["W"][l], inp["b"][l], _np(net.top[l]), gl,
                             _np(net.dbottom[l]), _np(net.dW[l]), _np(net.db[l]), images=images,
-                            filters=[0, L.K - 1], what=f"step {L.name}",
+                            filters=_tile_filters(L), what=f"step {L.name}",
                             dx_mask=(xl > 0) if net.mask_bottom[l] else None)
         for st in net.stages[l]:
             xin = _np(st["x"])[images]

@@ -532,13 +532,20 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
         // per MT-row block: every position (and, masked, every value of the
         // ReLU output) first, then the stores (a load after a store to
         // another buffer could not be moved above it, so each would wait
-        // alone)
+        // alone).  Masked, a 32-row block goes in two halves of its
+        // registers: the mask values and offsets of a whole block beside the
+        // accumulators took the kernel past 128 VGPRs (three waves per SIMD
+        // instead of four).
+        constexpr int QC = MASK && Op::kRegs > 8 ? Op::kRegs / 2 : Op::kRegs;
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
-            uint32_t off[Op::kRegs][NR];
-            float y[Op::kRegs][NR];
 #pragma unroll
-            for (int q = 0; q < Op::kRegs; ++q) {
+          for (int q0 = 0; q0 < Op::kRegs; q0 += QC) {
+            uint32_t off[QC][NR];
+            float y[QC][NR];
+#pragma unroll
+            for (int qq = 0; qq < QC; ++qq) {
+                const int q = q0 + qq;
 #pragma unroll
                 for (int h = 0; h < NR; ++h) {
                     const int m = m0 + wm * MI * MT + mi * MT + WR::row(q, h);
@@ -555,24 +562,25 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
                                           (uint32_t)((unsigned)hh >= (unsigned)p.OutH) |
                                           (uint32_t)((unsigned)ww >= (unsigned)p.OutW))
                                          << 31;
-                    off[q][h] = ((uint32_t)(cb + c * OutHW + hh * p.OutW + ww) * 4u) | bad;
+                    off[qq][h] = ((uint32_t)(cb + c * OutHW + hh * p.OutW + ww) * 4u) | bad;
                     // backward of the ReLU that produced the gather target:
                     // keep the gradient only where that output was > 0
                     if constexpr (MASK)
-                        y[q][h] = buf_ld_f32(rom, off[q][h]);
+                        y[qq][h] = buf_ld_f32(rom, off[qq][h]);
                 }
             }
 #pragma unroll
-            for (int q = 0; q < Op::kRegs; ++q) {
+            for (int qq = 0; qq < QC; ++qq) {
                 float v[NR];
-                wave_rows<MT>(acc[mi], q, v);
+                wave_rows<MT>(acc[mi], q0 + qq, v);
 #pragma unroll
                 for (int h = 0; h < NR; ++h) {
                     if constexpr (MASK)
-                        v[h] = y[q][h] > 0.f ? v[h] : 0.f;
-                    buf_st_f32(v[h], ry, off[q][h]);
+                        v[h] = y[qq][h] > 0.f ? v[h] : 0.f;
+                    buf_st_f32(v[h], ry, off[qq][h]);
                 }
             }
+          }
         }
     }
 }

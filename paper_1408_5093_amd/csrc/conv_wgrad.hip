@@ -315,7 +315,7 @@ __device__ __forceinline__ int quad_lds_pos(int sub, int l)
 }
 
 template <int WM, int WN, int MI, int NI, int KH, int KW>
-__global__ void __launch_bounds__(64 * WM * WN)
+__global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(4)))
 conv_wgrad_quad_f32_kernel(const WgradParams p)
 {
     constexpr int MT = 32;
@@ -457,6 +457,15 @@ conv_wgrad_quad_f32_kernel(const WgradParams p)
 
     const int kl = lane >> 5;
     const int l32 = lane & 31;
+    // Column blocks of this wave that hold taps below R (wave-uniform): the
+    // last tap tile of a layer whose R is not a multiple of TN runs no MFMAs
+    // for blocks wholly past R, which leaves their SIMD time to the other
+    // resident workgroups (CaffeNet conv2: 48 of the last tile's 128 taps are
+    // real).  The stage loop below is instantiated once per count.
+    const int nbv = __builtin_amdgcn_readfirstlane(
+        min(max((p.R - (r0 + wn * NI * MT) + MT - 1) / MT, 0), NI));
+    auto stage_loop = [&](auto nb_tag) {
+    constexpr int NB = decltype(nb_tag)::value;
     for (int s = 0; s < nst; ++s) {
         const int cur = s & 1;
         if (s + 1 < nst) {
@@ -502,7 +511,7 @@ conv_wgrad_quad_f32_kernel(const WgradParams p)
 #pragma unroll
             for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-                for (int ni = 0; ni < NI; ++ni)
+                for (int ni = 0; ni < NB; ++ni)
                     acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x2f32(
                         fa[ks % (PF + 1)][mi], fb[ks % (PF + 1)][ni], acc[mi][ni], 0, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
@@ -511,6 +520,13 @@ conv_wgrad_quad_f32_kernel(const WgradParams p)
             store_stage(cur ^ 1);
         __syncthreads();
     }
+    };
+    if (nbv == NI)
+        stage_loop(std::integral_constant<int, NI>{});
+    else if (NI > 1 && nbv == 1)
+        stage_loop(std::integral_constant<int, 1>{});
+    else
+        stage_loop(std::integral_constant<int, 0>{});
 
     if (want_db) {
         const int m = m0 + tid;

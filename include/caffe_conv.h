@@ -106,7 +106,8 @@ enum caffe_conv_pass {
     CAFFE_PASS_FORWARD = 0,
     CAFFE_PASS_BACKWARD_DATA = 1,
     CAFFE_PASS_BACKWARD_WEIGHTS = 2,
-    CAFFE_PASS_BACKWARD = 3 /* caffe_conv_backward: data and weights together */
+    CAFFE_PASS_BACKWARD = 3, /* caffe_conv_backward: data and weights together */
+    CAFFE_PASS_BACKWARD_POOL_LRN = 4 /* caffe_conv_backward_pool_lrn (caffe_layers.h) */
 };
 
 /* Output spatial size (formula above).  Host-only; never touches a GPU.

@@ -36,6 +36,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "caffe_conv.h"
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -100,6 +102,33 @@ int caffe_pool_lrn_forward(const caffe_pool_desc* pool, const caffe_lrn_desc* lr
 int caffe_lrn_pool_backward(const caffe_pool_desc* pool, const caffe_lrn_desc* lrn,
                             const float* pooled, const float* top, const float* top_diff,
                             const int32_t* mask, float* bottom_diff, void* stream);
+
+/* The backward pass of a convolution layer whose output feeds max pooling
+ * followed by LRN (CaffeNet's conv1 and conv2 with their glue): the layer's
+ * top gradient is the glue's backward, caffe_lrn_pool_backward(pool, lrn,
+ * pooled, lrn_top, lrn_top_diff, pool_mask), and the rest is
+ * caffe_conv_backward(desc, that gradient, top, bottom, weight, bottom_diff,
+ * weight_diff, bias_diff, accumulate, flags, ...) -- the same results,
+ * without the top gradient ever stored in float.  `pool` must describe the
+ * pooling of this layer's top (N, K, Ho, Wo) and `lrn` the pooled blob, with
+ * the support conditions of caffe_lrn_pool_backward.  pool_mask holds the
+ * winners of the forward pooling; with CAFFE_POOL_RELU_INPUT there the
+ * gradient is already masked by the layer's ReLU (pass
+ * CAFFE_BACKWARD_TOP_DIFF_MASKED), otherwise `top` is read for the mask when
+ * desc->relu.  Workspace: caffe_conv_workspace_size with
+ * CAFFE_PASS_BACKWARD_POOL_LRN.
+ * In CAFFE_BF16 mode with K / group a multiple of 16, the glue's backward
+ * writes the bfloat16 staging of the top gradient (and the bias-gradient
+ * partials of its float values) directly: one pass instead of writing the
+ * float gradient and reading it back.  Otherwise the float gradient goes to
+ * the workspace first. */
+int caffe_conv_backward_pool_lrn(const caffe_conv_desc* desc, const caffe_pool_desc* pool,
+                                 const caffe_lrn_desc* lrn, const float* pooled,
+                                 const float* lrn_top, const float* lrn_top_diff,
+                                 const int32_t* pool_mask, const float* top, const void* bottom,
+                                 const void* weight, float* bottom_diff, float* weight_diff,
+                                 float* bias_diff, int32_t accumulate, int32_t flags,
+                                 void* workspace, size_t ws_bytes, void* stream);
 
 /* out[i] = bfloat16(in[i]) rounded to nearest even, i < count.  The input for
  * CAFFE_BF16 convolutions. */

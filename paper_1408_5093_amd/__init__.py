@@ -18,7 +18,8 @@ from ._lib import (  # noqa: F401
     CAFFE_ERR_UNSUPPORTED, CAFFE_ERR_WORKSPACE, NOALLOC_SCRATCH_BYTES, BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF,
     BACKWARD_TOP_DIFF_MASKED, CAFFE_BF16, CAFFE_F32, CAFFE_LR_EXP,
     CAFFE_LR_FIXED, CAFFE_LR_INV, CAFFE_LR_STEP, LrSchedule, PASS_BACKWARD,
-    PASS_BACKWARD_DATA, PASS_BACKWARD_WEIGHTS, PASS_FORWARD, POOL_RELU_INPUT, CaffeError, ConvDesc,
+    PASS_BACKWARD_DATA, PASS_BACKWARD_POOL_LRN, PASS_BACKWARD_WEIGHTS, PASS_FORWARD,
+    POOL_RELU_INPUT, CaffeError, ConvDesc,
     LrnDesc, PoolDesc, check, load, LIB_PATH,
 )
 
@@ -27,7 +28,7 @@ __all__ = [
     "conv_backward_data", "conv_backward_weights", "maxpool_forward", "maxpool_backward",
     "lrn_forward", "lrn_backward", "cast_f32_to_bf16", "Workspace", "CaffeError",
     "sgd_learning_rate", "softmax_loss", "sgd_update", "pool_lrn_forward", "lrn_pool_backward",
-    "pool_lrn_supported",
+    "pool_lrn_supported", "caffe_conv_backward_pool_lrn",
 ]
 
 
@@ -312,6 +313,26 @@ def lrn_pool_backward(x_shape, pooled, top, top_diff, mask, kernel, stride, pad=
                                          _ptr(top), _ptr(top_diff), _ptr(mask), _ptr(out),
                                          _stream(stream)))
     return out
+
+
+def caffe_conv_backward_pool_lrn(desc, pool, lrn, pooled, lrn_top, lrn_top_diff, pool_mask, top,
+                                 bottom, weight, bottom_diff, weight_diff, bias_diff,
+                                 accumulate=0, flags=0, workspace=None, stream=None):
+    """caffe_conv_backward_pool_lrn: the layer's backward from the gradient
+    of the LRN that follows its max-pool (pool, lrn: PoolDesc, LrnDesc)."""
+    t = _op_dtype(desc)
+    for x, n in ((pooled, "pooled"), (lrn_top, "lrn_top"), (lrn_top_diff, "lrn_top_diff"),
+                 (top, "top"), (bottom_diff, "bottom_diff"), (weight_diff, "weight_diff"),
+                 (bias_diff, "bias_diff")):
+        _dev(x, n, torch.float32)
+    _dev(pool_mask, "pool_mask", torch.int32)
+    _dev(bottom, "bottom", t), _dev(weight, "weight", t)
+    ws_bytes = 0 if workspace is None else workspace.numel()
+    check(load().caffe_conv_backward_pool_lrn(
+        ctypes.byref(desc), ctypes.byref(pool), ctypes.byref(lrn), _ptr(pooled), _ptr(lrn_top),
+        _ptr(lrn_top_diff), _ptr(pool_mask), _ptr(top), _ptr(bottom), _ptr(weight),
+        _ptr(bottom_diff), _ptr(weight_diff), _ptr(bias_diff), int(accumulate), int(flags),
+        _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def cast_f32_to_bf16(x, out=None, stream=None):

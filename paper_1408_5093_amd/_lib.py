@@ -29,6 +29,7 @@ PASS_FORWARD = 0
 PASS_BACKWARD_DATA = 1
 PASS_BACKWARD_WEIGHTS = 2
 PASS_BACKWARD = 3
+PASS_BACKWARD_POOL_LRN = 4
 
 NOALLOC_SCRATCH_BYTES = 64 << 20  # CAFFE_CONV_NOALLOC_SCRATCH_BYTES
 
@@ -47,6 +48,7 @@ EXPORTS = (
     "caffe_sgd_learning_rate", "caffe_softmax_loss", "caffe_sgd_update",
     "caffe_pool_lrn_forward", "caffe_lrn_pool_backward", "caffe_sgd_update_device_lr",
     "caffe_conv_workspace_bytes", "caffe_conv_status_string", "caffe_conv_forward_noalloc",
+    "caffe_conv_backward_pool_lrn",
 )
 
 
@@ -114,6 +116,8 @@ def load():
         "caffe_cast_f32_to_bf16": [vp, vp, i64, vp],
         "caffe_pool_lrn_forward": [pdp, ldp, vp, vp, vp, vp, i32, vp],
         "caffe_lrn_pool_backward": [pdp, ldp, vp, vp, vp, vp, vp, vp],
+        "caffe_conv_backward_pool_lrn": [cdp, pdp, ldp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                         i32, i32, vp, sz, vp],
         "caffe_sgd_learning_rate": [ctypes.POINTER(LrSchedule), i64,
                                     ctypes.POINTER(ctypes.c_float)],
         "caffe_softmax_loss": [vp, vp, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp],

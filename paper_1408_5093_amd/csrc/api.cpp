@@ -1052,6 +1052,11 @@ int join_side(hipStream_t s, Fork& f, int st_a, int st_b)
     return CAFFE_OK;
 }
 
+int backward_bf16_staged(const ConvPlan& q, const float* sums, int terms, bool mask_bottom,
+                         bool staged, const void* bottom, const void* weight, float* bottom_diff,
+                         float* weight_diff, float* bias_diff, int accumulate, char* ws,
+                         hipStream_t s);
+
 int backward_bf16(const ConvPlan& q, const float* top_diff, const float* top, bool masked,
                   bool mask_bottom, bool staged, const void* bottom, const void* weight,
                   float* bottom_diff, float* weight_diff, float* bias_diff, int accumulate,
@@ -1070,6 +1075,19 @@ int backward_bf16(const ConvPlan& q, const float* top_diff, const float* top, bo
                                  q.Wo, q.Kg, q.Kgp, q.G * q.Kgp, q.DHp, q.DWp, q.dtb, q.dlb,
                                  q.relu && !masked, s),
            "bf16 top-gradient staging launch");
+    return backward_bf16_staged(q, sums, diff_prep_terms(q.N, q.DHp * q.DWp), mask_bottom, staged,
+                                bottom, weight, bottom_diff, weight_diff, bias_diff, accumulate, ws,
+                                s);
+}
+
+// The bf16 backward once the top gradient is staged at off_dh and its
+// bias-gradient partials sit in `sums` (`terms` per channel).
+int backward_bf16_staged(const ConvPlan& q, const float* sums, int terms, bool mask_bottom,
+                         bool staged, const void* bottom, const void* weight, float* bottom_diff,
+                         float* weight_diff, float* bias_diff, int accumulate, char* ws,
+                         hipStream_t s)
+{
+    const uint16_t* dh = (const uint16_t*)(ws + q.off_dh);
     Fork f;
     if (bottom_diff && weight_diff && fork_side(s, &f)) {
         // (disjoint workspace regions: Wt for the data gradient; the staged
@@ -1086,10 +1104,21 @@ int backward_bf16(const ConvPlan& q, const float* top_diff, const float* top, bo
             CHECK(run_weights_bf16(q, dh, bottom, staged, weight_diff, accumulate, ws, s));
     }
     if (bias_diff)
-        LAUNCH(launch_bias_reduce(sums, bias_diff, diff_prep_terms(q.N, q.DHp * q.DWp), q.K,
-                                  accumulate, s),
+        LAUNCH(launch_bias_reduce(sums, bias_diff, terms, q.K, accumulate, s),
                "bias reduce launch");
     return CAFFE_OK;
+}
+
+// caffe_conv_backward_pool_lrn: the bf16 staging is written by the fused
+// glue backward when a 16-channel block lies in one group; its bias partials
+// (at most one per image, row strip and channel) go after the backward's
+// workspace.  Otherwise the fp32 top gradient goes there.
+bool pool_lrn_staged(const ConvPlan& q) { return q.dtype == CAFFE_BF16 && q.Kg % 16 == 0; }
+
+size_t pool_lrn_extra(const ConvPlan& q)
+{
+    const int64_t elems = pool_lrn_staged(q) ? (int64_t)q.N * q.Ho * q.K : q.top_elems;
+    return align_up((size_t)elems * 4, kWsAlign);
 }
 
 int check_conv_ptrs(const ConvPlan& q, const void* p, bool needed, bool is_blob, const char* name)
@@ -1132,6 +1161,9 @@ int caffe_conv_workspace_size(const caffe_conv_desc* desc, int32_t pass, size_t*
         return CAFFE_OK;
     case CAFFE_PASS_BACKWARD:
         *bytes = q.ws_both;
+        return CAFFE_OK;
+    case CAFFE_PASS_BACKWARD_POOL_LRN:
+        *bytes = q.ws_both + pool_lrn_extra(q);
         return CAFFE_OK;
     default:
         return fail(CAFFE_ERR_INVALID_ARG, "unknown pass %d", pass);
@@ -1256,6 +1288,81 @@ int caffe_conv_backward_weights(const caffe_conv_desc* desc, const float* top_di
     CHECK(check_conv_ptrs(q, weight_diff, true, false, "weight_diff"));
     return caffe_conv_backward(desc, top_diff, top, bottom, nullptr, nullptr, weight_diff,
                                bias_diff, accumulate, 0, workspace, ws_bytes, stream);
+}
+
+static int check_pool_lrn(const caffe_pool_desc* pd, const caffe_lrn_desc* ld, int* Ho, int* Wo);
+
+int caffe_conv_backward_pool_lrn(const caffe_conv_desc* desc, const caffe_pool_desc* pool,
+                                 const caffe_lrn_desc* lrn, const float* pooled,
+                                 const float* lrn_top, const float* lrn_top_diff,
+                                 const int32_t* pool_mask, const float* top, const void* bottom,
+                                 const void* weight, float* bottom_diff, float* weight_diff,
+                                 float* bias_diff, int32_t accumulate, int32_t flags,
+                                 void* workspace, size_t ws_bytes, void* stream)
+{
+    ConvPlan q;
+    CHECK(plan_conv(desc, &q));
+    int PHo, PWo;
+    CHECK(check_pool_lrn(pool, lrn, &PHo, &PWo));
+    if (pool->N != q.N || pool->C != q.K || pool->H != q.Ho || pool->W != q.Wo)
+        return fail(CAFFE_ERR_INVALID_ARG, "the pooled blob (%d, %d, %d, %d) is not the "
+                    "convolution's top (%d, %d, %d, %d)", pool->N, pool->C, pool->H, pool->W, q.N,
+                    q.K, q.Ho, q.Wo);
+    if (accumulate != 0 && accumulate != 1)
+        return fail(CAFFE_ERR_INVALID_ARG, "accumulate must be 0 or 1");
+    if (flags & ~(CAFFE_BACKWARD_TOP_DIFF_MASKED | CAFFE_BACKWARD_MASK_BOTTOM_DIFF |
+                  CAFFE_BACKWARD_BOTTOM_STAGED))
+        return fail(CAFFE_ERR_INVALID_ARG, "unknown backward flags 0x%x", flags);
+    const bool masked = (flags & CAFFE_BACKWARD_TOP_DIFF_MASKED) != 0;
+    const bool mask_bottom = (flags & CAFFE_BACKWARD_MASK_BOTTOM_DIFF) != 0 && bottom_diff;
+    CHECK(check_conv_ptrs(q, pooled, true, true, "pooled"));
+    CHECK(check_conv_ptrs(q, lrn_top, true, true, "lrn_top"));
+    CHECK(check_conv_ptrs(q, lrn_top_diff, true, true, "lrn_top_diff"));
+    CHECK(check_conv_ptrs(q, pool_mask, true, true, "pool_mask"));
+    CHECK(check_conv_ptrs(q, top, q.relu != 0 && !masked, true, "top"));
+    CHECK(check_conv_ptrs(q, bottom, weight_diff != nullptr || mask_bottom, true, "bottom"));
+    CHECK(check_conv_ptrs(q, weight, bottom_diff != nullptr, false, "weight"));
+    CHECK(check_conv_ptrs(q, bottom_diff, false, true, "bottom_diff"));
+    CHECK(check_conv_ptrs(q, weight_diff, false, false, "weight_diff"));
+    CHECK(check_conv_ptrs(q, bias_diff, false, false, "bias_diff"));
+    CHECK(check_ws(workspace, ws_bytes, q.ws_both + pool_lrn_extra(q)));
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    const float* relu_top = q.relu && !masked ? top : nullptr;
+    if (!pool_lrn_staged(q)) {
+        // the glue's backward into the workspace, then the layer's backward
+        // on that gradient (already masked when relu_top was applied)
+        float* gbuf = (float*)(ws + q.ws_both);
+        LAUNCH(launch_lrn_pool_backward(pooled, lrn_top, lrn_top_diff, pool_mask, gbuf, q.N, q.K,
+                                        q.Ho, q.Wo, PHo, PWo, pool->kernel_h, pool->kernel_w,
+                                        pool->stride_h, pool->stride_w, pool->pad_h, pool->pad_w,
+                                        lrn->local_size, lrn->alpha, lrn->beta, lrn->k, s),
+               "fused LRN + pool backward launch");
+        return caffe_conv_backward(desc, gbuf, top, bottom, weight, bottom_diff, weight_diff,
+                                   bias_diff, accumulate, flags, workspace, q.ws_both, stream);
+    }
+    if (q.N == 0) {
+        if (bias_diff && !accumulate)
+            LAUNCH(launch_fill_zero(bias_diff, q.K, s), "zero fill launch");
+        if (weight_diff && !accumulate)
+            LAUNCH(launch_fill_zero(weight_diff, q.weight_elems, s), "zero fill launch");
+        return CAFFE_OK;
+    }
+    // the glue's backward written straight into the bf16 top-gradient
+    // staging, with its bias-gradient partials
+    float* sums = (float*)(ws + q.ws_both);
+    LAUNCH(launch_lrn_pool_backward_bf16(pooled, lrn_top, lrn_top_diff, pool_mask, relu_top,
+                                         (uint16_t*)(ws + q.off_dh), sums, q.N, q.K, q.Ho, q.Wo,
+                                         PHo, PWo, pool->kernel_h, pool->kernel_w, pool->stride_h,
+                                         pool->stride_w, pool->pad_h, pool->pad_w, lrn->local_size,
+                                         lrn->alpha, lrn->beta, lrn->k, q.Kg, q.Kgp, q.G * q.Kgp,
+                                         q.DHp, q.DWp, q.dtb, q.dlb, s),
+           "fused LRN + pool backward staging launch");
+    const int strips = lrn_pool_backward_strips(q.Ho, PHo, PWo, pool->kernel_h, pool->stride_h,
+                                                pool->pad_h);
+    return backward_bf16_staged(q, sums, q.N * strips, mask_bottom,
+                                (flags & CAFFE_BACKWARD_BOTTOM_STAGED) != 0, bottom, weight,
+                                bottom_diff, weight_diff, bias_diff, accumulate, ws, s);
 }
 
 const char* caffe_status_string(int32_t status)

@@ -359,6 +359,20 @@ hipError_t launch_lrn_backward(const float* x, const float* y, const float* dy, 
 // LRN sizes 3 and 5; the geometry must pass pool_lrn_fusable
 // (hipErrorInvalidValue otherwise).
 bool pool_lrn_fusable(int H, int W, int OH, int OW, int kh, int sh, int ph, int size);
+// Row strips of the fused LRN + max-pool backward (0: not fusable).
+int lrn_pool_backward_strips(int H, int OH, int OW, int kh, int sh, int ph);
+// The fused backward written as the bf16 top-gradient staging of the
+// convolution below (channels in groups of Kg, each padded to Kgp, Ktot in
+// all, on a DHp x DWp grid with the image at (tb, lb)), plus the grid's zero
+// border and the bias-gradient partials sums[c * T + n * strips + strip]
+// (T = N * strips).  relu_top (may be null): mask by [relu_top > 0].
+hipError_t launch_lrn_pool_backward_bf16(const float* pooled, const float* top,
+                                         const float* top_diff, const int32_t* mask,
+                                         const float* relu_top, uint16_t* Dh, float* sums, int N,
+                                         int C, int H, int W, int OH, int OW, int kh, int kw,
+                                         int sh, int sw, int ph, int pw, int size, float alpha,
+                                         float beta, float k, int Kg, int Kgp, int Ktot, int DHp,
+                                         int DWp, int tb, int lb, hipStream_t s);
 hipError_t launch_lrn_pool_backward(const float* pooled, const float* top, const float* top_diff,
                                     const int32_t* mask, float* dx, int N, int C, int H, int W,
                                     int OH, int OW, int kh, int kw, int sh, int sw, int ph, int pw,

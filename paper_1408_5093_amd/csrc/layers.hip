@@ -660,6 +660,145 @@ hipError_t launch_lrn_backward(const float* x, const float* y, const float* dy, 
 constexpr int kFuseCh = 16;      // channels owned by a block
 constexpr int kFusePos = 256;    // pooled positions staged per block (one per thread)
 
+// One block of the fused backward: image n, channels c0 .. c0 + 15, input
+// rows y_lo .. y_hi, and the pooled rows i_lo .. i_hi whose windows reach
+// them.
+struct FuseBlock {
+    int n, c0, strip, y_lo, y_hi, i_lo, i_hi;
+};
+
+__device__ __forceinline__ FuseBlock fuse_block(int H, int OH, int kh, int sh, int ph, int yrows,
+                                                int nstrips, int nchunks)
+{
+    // Workgroups are dispatched round-robin over the 8 XCDs, each with its own
+    // L2; neighbouring strips and channel chunks share halo rows and channels,
+    // so each XCD takes one contiguous range of the block order.
+    const int xcd = blockIdx.x & 7, per = gridDim.x >> 3, extra = gridDim.x & 7;
+    const int blk = xcd * per + min(xcd, extra) + (blockIdx.x >> 3);
+    FuseBlock f;
+    f.strip = blk % nstrips;
+    const int rest = blk / nstrips;
+    f.c0 = (rest % nchunks) * kFuseCh;
+    f.n = rest / nchunks;
+    f.y_lo = f.strip * yrows;
+    f.y_hi = min(H, f.y_lo + yrows) - 1;
+    f.i_lo = max(0, (f.y_lo + ph - kh + sh) / sh);
+    f.i_hi = min(OH - 1, (f.y_hi + ph) / sh);
+    return f;
+}
+
+// Phase 1: the pooled gradient (LRN backward) of the block's 16 channels at
+// every staged pooled position, and the winners, into LDS.
+template <int SIZE>
+__device__ __forceinline__ void fuse_stage_pooled_grad(
+    const FuseBlock& f, const float* __restrict__ a_in, const float* __restrict__ b_in,
+    const float* __restrict__ g_in, const int32_t* __restrict__ mask,
+    float (&gs)[kFuseCh][kFusePos], int32_t (&ms)[kFuseCh][kFusePos], int N, int C, int OH, int OW,
+    float alpha_over_n, float beta, float k)
+{
+    constexpr int PRE = (SIZE - 1) / 2;
+    constexpr int POST = SIZE - 1 - PRE;
+    constexpr int NR = kFuseCh + SIZE - 1;   // ratios: channels c0 - POST .. c0 + 15 + PRE
+    constexpr int NA = NR + SIZE - 1;        // inputs: channels c0 - POST - PRE .. + NA - 1
+    const int npos = (f.i_hi - f.i_lo + 1) * OW;
+    const int OHW = OH * OW;
+    const int c0 = f.c0;
+    const int pos = threadIdx.x;
+    if (pos >= npos)
+        return;
+    const int pix = (f.i_lo + pos / OW) * OW + (pos - (pos / OW) * OW);
+    const uint32_t bytes = (uint32_t)(N * C * OHW) * 4u;
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_in, bytes);
+    const __amdgpu_buffer_rsrc_t rb = make_rsrc(b_in, bytes);
+    const __amdgpu_buffer_rsrc_t rg = make_rsrc(g_in, bytes);
+    const __amdgpu_buffer_rsrc_t rm = make_rsrc(mask, bytes);
+    const uint32_t base4 = (uint32_t)(f.n * C * OHW + pix) * 4u;
+    const uint32_t hw4 = (uint32_t)OHW * 4u;
+    auto off = [&](int ch) {
+        return (base4 + (uint32_t)ch * hw4) | ((uint32_t)((unsigned)ch >= (unsigned)C) << 31);
+    };
+    float a[NA], g[NR], b[NR];
+#pragma unroll
+    for (int q = 0; q < NA; ++q)
+        a[q] = buf_ld_f32(ra, off(c0 - POST - PRE + q));
+#pragma unroll
+    for (int q = 0; q < NR; ++q) {
+        g[q] = buf_ld_f32(rg, off(c0 - POST + q));
+        b[q] = buf_ld_f32(rb, off(c0 - POST + q));
+    }
+    float r[NR], sc[kFuseCh];
+#pragma unroll
+    for (int q = 0; q < NR; ++q) {
+        float sq = 0.f;
+#pragma unroll
+        for (int t = 0; t < SIZE; ++t)
+            sq += a[q + t] * a[q + t];
+        const float s = k + alpha_over_n * sq;
+        r[q] = g[q] * b[q] * __builtin_amdgcn_rcpf(s);
+        if (q >= POST && q < POST + kFuseCh)
+            sc[q - POST] = s;
+    }
+    const float coef = 2.f * alpha_over_n * beta;
+#pragma unroll
+    for (int t = 0; t < kFuseCh; ++t) {
+        float cross = 0.f;
+#pragma unroll
+        for (int q = 0; q < SIZE; ++q)
+            cross += r[t + q];
+        gs[t][pos] = g[t + POST] * pow_neg(sc[t], beta) - coef * a[t + POST + PRE] * cross;
+        // (channels past C stage zeros; phase 2 never reads them)
+        ms[t][pos] = (int32_t)__builtin_bit_cast(uint32_t, buf_ld_f32(rm, off(c0 + t)));
+    }
+}
+
+// Phase 2 for one input position (h, w) and staged channel t: the sum, in
+// row-major window order, of the pooled gradients of the covering windows
+// whose winner it is.
+template <int KS, int SS>
+__device__ __forceinline__ float fuse_gather(const FuseBlock& f,
+                                             const float (&gs)[kFuseCh][kFusePos],
+                                             const int32_t (&ms)[kFuseCh][kFusePos], int t,
+                                             int h, int w, int W, int OH, int OW, int kh, int kw,
+                                             int sh, int sw, int ph, int pw)
+{
+    const int hw = h * W + w;
+    const int i0 = max(0, (h + ph - kh + sh) / sh);
+    const int i1 = min(OH - 1, (h + ph) / sh);
+    const int j0 = max(0, (w + pw - kw + sw) / sw);
+    const int j1 = min(OW - 1, (w + pw) / sw);
+    float sum = 0.f;
+    if constexpr (KS > 0) {
+        // the covering windows (at most T x T), read first with their
+        // indices clamped into the staged rows, then added in row-major
+        // order where valid and routed here
+        constexpr int T = (KS + SS - 1) / SS;
+        int m[T][T];
+        float g[T][T];
+#pragma unroll
+        for (int di = 0; di < T; ++di)
+#pragma unroll
+            for (int dj = 0; dj < T; ++dj) {
+                const int o = (min(i0 + di, f.i_hi) - f.i_lo) * OW + min(j0 + dj, OW - 1);
+                m[di][dj] = ms[t][o];
+                g[di][dj] = gs[t][o];
+            }
+#pragma unroll
+        for (int di = 0; di < T; ++di)
+#pragma unroll
+            for (int dj = 0; dj < T; ++dj)
+                if (i0 + di <= i1 && j0 + dj <= j1 && m[di][dj] == hw)
+                    sum += g[di][dj];
+    } else {
+        for (int ii = i0; ii <= i1; ++ii)
+            for (int jj = j0; jj <= j1; ++jj) {
+                const int o = (ii - f.i_lo) * OW + jj;
+                if (ms[t][o] == hw)
+                    sum += gs[t][o];
+            }
+    }
+    return sum;
+}
+
 template <int KS, int SS, int SIZE>
 __global__ void __launch_bounds__(256)
 lrn_pool_backward_kernel(const float* __restrict__ a_in, const float* __restrict__ b_in,
@@ -668,136 +807,157 @@ lrn_pool_backward_kernel(const float* __restrict__ a_in, const float* __restrict
                          int kh_, int kw_, int sh_, int sw_, int ph, int pw, int yrows,
                          int nstrips, int nchunks, float alpha_over_n, float beta, float k)
 {
-    constexpr int PRE = (SIZE - 1) / 2;
-    constexpr int POST = SIZE - 1 - PRE;
-    constexpr int NR = kFuseCh + SIZE - 1;   // ratios: channels c0 - POST .. c0 + 15 + PRE
-    constexpr int NA = NR + SIZE - 1;        // inputs: channels c0 - POST - PRE .. + NA - 1
     __shared__ float gs[kFuseCh][kFusePos];
     __shared__ int32_t ms[kFuseCh][kFusePos];
     const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
     const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
-    // Workgroups are dispatched round-robin over the 8 XCDs, each with its own
-    // L2; neighbouring strips and channel chunks share halo rows and channels,
-    // so each XCD takes one contiguous range of the block order.
-    const int xcd = blockIdx.x & 7, per = gridDim.x >> 3, extra = gridDim.x & 7;
-    const int blk = xcd * per + min(xcd, extra) + (blockIdx.x >> 3);
-    const int strip = blk % nstrips;
-    const int rest = blk / nstrips;
-    const int c0 = (rest % nchunks) * kFuseCh;
-    const int n = rest / nchunks;
-    const int y_lo = strip * yrows;
-    const int y_hi = min(H, y_lo + yrows) - 1;
-    // pooled rows whose windows reach input rows y_lo .. y_hi
-    const int i_lo = max(0, (y_lo + ph - kh + sh) / sh);
-    const int i_hi = min(OH - 1, (y_hi + ph) / sh);
-    const int npos = (i_hi - i_lo + 1) * OW;
-    const int OHW = OH * OW, HW = H * W;
-    // phase 1: the pooled gradient (LRN backward) of the block's 16 channels at
-    // every staged pooled position, and the winners, into LDS
-    const int pos = threadIdx.x;
-    if (pos < npos) {
-        const int pix = (i_lo + pos / OW) * OW + (pos - (pos / OW) * OW);
-        const uint32_t bytes = (uint32_t)(N * C * OHW) * 4u;
-        const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_in, bytes);
-        const __amdgpu_buffer_rsrc_t rb = make_rsrc(b_in, bytes);
-        const __amdgpu_buffer_rsrc_t rg = make_rsrc(g_in, bytes);
-        const __amdgpu_buffer_rsrc_t rm = make_rsrc(mask, bytes);
-        const uint32_t base4 = (uint32_t)(n * C * OHW + pix) * 4u;
-        const uint32_t hw4 = (uint32_t)OHW * 4u;
-        auto off = [&](int ch) {
-            return (base4 + (uint32_t)ch * hw4) | ((uint32_t)((unsigned)ch >= (unsigned)C) << 31);
-        };
-        float a[NA], g[NR], b[NR];
-#pragma unroll
-        for (int q = 0; q < NA; ++q)
-            a[q] = buf_ld_f32(ra, off(c0 - POST - PRE + q));
-#pragma unroll
-        for (int q = 0; q < NR; ++q) {
-            g[q] = buf_ld_f32(rg, off(c0 - POST + q));
-            b[q] = buf_ld_f32(rb, off(c0 - POST + q));
-        }
-        float r[NR], sc[kFuseCh];
-#pragma unroll
-        for (int q = 0; q < NR; ++q) {
-            float sq = 0.f;
-#pragma unroll
-            for (int t = 0; t < SIZE; ++t)
-                sq += a[q + t] * a[q + t];
-            const float s = k + alpha_over_n * sq;
-            r[q] = g[q] * b[q] * __builtin_amdgcn_rcpf(s);
-            if (q >= POST && q < POST + kFuseCh)
-                sc[q - POST] = s;
-        }
-        const float coef = 2.f * alpha_over_n * beta;
-#pragma unroll
-        for (int t = 0; t < kFuseCh; ++t) {
-            float cross = 0.f;
-#pragma unroll
-            for (int q = 0; q < SIZE; ++q)
-                cross += r[t + q];
-            gs[t][pos] = g[t + POST] * pow_neg(sc[t], beta) - coef * a[t + POST + PRE] * cross;
-            // (channels past C stage zeros; phase 2 never reads them)
-            ms[t][pos] = (int32_t)__builtin_bit_cast(uint32_t, buf_ld_f32(rm, off(c0 + t)));
-        }
-    }
+    const FuseBlock f = fuse_block(H, OH, kh, sh, ph, yrows, nstrips, nchunks);
+    fuse_stage_pooled_grad<SIZE>(f, a_in, b_in, g_in, mask, gs, ms, N, C, OH, OW, alpha_over_n,
+                                 beta, k);
     __syncthreads();
-    // phase 2: each input position of rows y_lo .. y_hi adds, in row-major
-    // window order, the pooled gradients of the covering windows whose winner
-    // it is
-    // Thread -> one input column w (threads past the last full group of W
-    // columns idle) and every g-th row of each channel; the covering windows'
-    // column range is fixed per thread.
+    // phase 2: thread -> one input column w (threads past the last full group
+    // of W columns idle) and every g-th row of each channel
     const int groups = 256 / W;             // W <= 256 (the staged rows hold >= 1 row)
     const int grp = threadIdx.x / W;
     const int w = threadIdx.x - grp * W;
     if (grp >= groups)
         return;
-    const int ny = y_hi - y_lo + 1;
-    const int j0 = max(0, (w + pw - kw + sw) / sw);
-    const int j1 = min(OW - 1, (w + pw) / sw);
+    const int ny = f.y_hi - f.y_lo + 1;
+    const int HW = H * W;
     for (int t = 0; t < kFuseCh; ++t) {
-        const int ch = c0 + t;
+        const int ch = f.c0 + t;
         if (ch >= C)
             break;
-        float* dplane = dx + ((size_t)n * C + ch) * HW;
+        float* dplane = dx + ((size_t)f.n * C + ch) * HW;
         for (int hh = grp; hh < ny; hh += groups) {
-            const int h = y_lo + hh;
-            const int hw = h * W + w;
-            const int i0 = max(0, (h + ph - kh + sh) / sh);
-            const int i1 = min(OH - 1, (h + ph) / sh);
-            float sum = 0.f;
-            if constexpr (KS > 0) {
-                // the covering windows (at most T x T), read first with their
-                // indices clamped into the staged rows, then added in
-                // row-major order where valid and routed here
-                constexpr int T = (KS + SS - 1) / SS;
-                int m[T][T];
-                float g[T][T];
-#pragma unroll
-                for (int di = 0; di < T; ++di)
-#pragma unroll
-                    for (int dj = 0; dj < T; ++dj) {
-                        const int o = (min(i0 + di, i_hi) - i_lo) * OW + min(j0 + dj, OW - 1);
-                        m[di][dj] = ms[t][o];
-                        g[di][dj] = gs[t][o];
-                    }
-#pragma unroll
-                for (int di = 0; di < T; ++di)
-#pragma unroll
-                    for (int dj = 0; dj < T; ++dj)
-                        if (i0 + di <= i1 && j0 + dj <= j1 && m[di][dj] == hw)
-                            sum += g[di][dj];
-            } else {
-                for (int ii = i0; ii <= i1; ++ii)
-                    for (int jj = j0; jj <= j1; ++jj) {
-                        const int o = (ii - i_lo) * OW + jj;
-                        if (ms[t][o] == hw)
-                            sum += gs[t][o];
-                    }
-            }
-            dplane[hw] = sum;
+            const int h = f.y_lo + hh;
+            dplane[h * W + w] = fuse_gather<KS, SS>(f, gs, ms, t, h, w, W, OH, OW, kh, kw, sh, sw,
+                                                    ph, pw);
         }
     }
+}
+
+// The same backward written straight into the bf16 top-gradient staging of
+// the convolution below the pool (the layer whose output the pool read):
+// Dh[n][h + tb][w + lb][g * Kgp + k] = bf16(D[n][g * Kg + k][h][w]) with
+// D = the gathered gradient, times [relu_top > 0] when `relu_top` (the
+// convolution's output) is given: the ReLU's backward, when the pool did not
+// fold it.  A block's 16 channels lie in one
+// group (Kg % 16 == 0), so each input position stores them as two 16-byte
+// chunks.  The fp32 values are also summed per channel over the block's
+// positions (each thread its own positions in row order, then a fixed
+// pairwise tree over the threads): sums[(g * Kg + k) * T + n * nstrips +
+// strip], T = N * nstrips, the bias-gradient partials.  The staging grid's
+// border is written by dh_zero_border_kernel.
+template <int KS, int SS, int SIZE>
+__global__ void __launch_bounds__(256)
+lrn_pool_backward_bf16_kernel(const float* __restrict__ a_in, const float* __restrict__ b_in,
+                              const float* __restrict__ g_in, const int32_t* __restrict__ mask,
+                              const float* __restrict__ relu_top, uint16_t* __restrict__ Dh,
+                              float* __restrict__ sums, int N, int C, int H, int W, int OH, int OW,
+                              int kh_, int kw_, int sh_, int sw_, int ph, int pw, int yrows,
+                              int nstrips, int nchunks, float alpha_over_n, float beta, float k,
+                              int Kg, int Kgp, int Ktot, int DHp, int DWp, int tb, int lb)
+{
+    __shared__ float gs[kFuseCh][kFusePos];
+    __shared__ int32_t ms[kFuseCh][kFusePos];
+    const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
+    const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
+    const FuseBlock f = fuse_block(H, OH, kh, sh, ph, yrows, nstrips, nchunks);
+    fuse_stage_pooled_grad<SIZE>(f, a_in, b_in, g_in, mask, gs, ms, N, C, OH, OW, alpha_over_n,
+                                 beta, k);
+    __syncthreads();
+    const int groups = 256 / W;
+    const int grp = threadIdx.x / W;
+    const int w = threadIdx.x - grp * W;
+    const int ny = f.y_hi - f.y_lo + 1;
+    const int HW = H * W;
+    const int g = f.c0 / Kg;
+    const int cp0 = g * Kgp + (f.c0 - g * Kg);
+    const uint32_t tbytes = relu_top ? (uint32_t)(N * C * HW) * 4u : 0u;
+    const __amdgpu_buffer_rsrc_t rt = make_rsrc(relu_top, tbytes);
+    float bsum[kFuseCh];
+#pragma unroll
+    for (int t = 0; t < kFuseCh; ++t)
+        bsum[t] = 0.f;
+    if (grp < groups) {
+        for (int hh = grp; hh < ny; hh += groups) {
+            const int h = f.y_lo + hh;
+            uint32_t packed[kFuseCh / 2];
+#pragma unroll
+            for (int t = 0; t < kFuseCh; t += 2) {
+                float v[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    v[u] = fuse_gather<KS, SS>(f, gs, ms, t + u, h, w, W, OH, OW, kh, kw, sh, sw,
+                                               ph, pw);
+                    if (relu_top) {
+                        // (a NaN output masks too)
+                        const uint32_t o = (uint32_t)(((f.n * C + f.c0 + t + u) * H + h) * W + w);
+                        v[u] = buf_ld_f32(rt, o * 4u) > 0.f ? v[u] : 0.f;
+                    }
+                    bsum[t + u] += v[u];
+                }
+                packed[t / 2] = (uint32_t)f32_to_bf16_rne(v[0]) |
+                                ((uint32_t)f32_to_bf16_rne(v[1]) << 16);
+            }
+            u32x4* dst = (u32x4*)&Dh[(((size_t)f.n * DHp + h + tb) * DWp + w + lb) * Ktot + cp0];
+            dst[0] = u32x4{packed[0], packed[1], packed[2], packed[3]};
+            dst[1] = u32x4{packed[4], packed[5], packed[6], packed[7]};
+        }
+    }
+    // bias-gradient partials: one fixed pairwise tree per channel (LDS reused)
+    __syncthreads();
+    float* red = &gs[0][0];
+    const size_t T = (size_t)N * nstrips;
+    for (int t = 0; t < kFuseCh; ++t) {
+        red[threadIdx.x] = bsum[t];
+        __syncthreads();
+        for (int half = 128; half > 0; half >>= 1) {
+            if (threadIdx.x < half)
+                red[threadIdx.x] += red[threadIdx.x + half];
+            __syncthreads();
+        }
+        if (threadIdx.x == 0 && f.c0 + t < C)
+            sums[(size_t)(f.c0 + t) * T + (size_t)f.n * nstrips + f.strip] = red[0];
+        __syncthreads();
+    }
+}
+
+// Zeros of the bf16 top-gradient staging grid outside the image: the rows
+// above and below it and the columns left and right of it, every channel, as
+// 16-byte stores.  One thread per (image, border pixel, 8-channel chunk).
+__global__ void __launch_bounds__(256)
+dh_zero_border_kernel(uint16_t* __restrict__ Dh, int N, int DHp, int DWp, int tb, int lb, int H,
+                      int W, int Ktot, long total)
+{
+    const long e = blockIdx.x * 256L + threadIdx.x;
+    if (e >= total)
+        return;
+    const int chunks = Ktot / 8;
+    const int border = DHp * DWp - H * W;
+    const int c8 = (int)(e % chunks);
+    const long pe = e / chunks;
+    const int b = (int)(pe % border);
+    const int n = (int)(pe / border);
+    // border pixels in row-major order: tb full rows, then H rows of the
+    // (DWp - W) side pixels, then the full rows below
+    const int side = DWp - W;
+    int hp, wp;
+    if (b < tb * DWp) {
+        hp = b / DWp;
+        wp = b - hp * DWp;
+    } else if (b < tb * DWp + H * side) {
+        const int r = b - tb * DWp;
+        hp = tb + r / side;
+        const int j = r - (r / side) * side;
+        wp = j < lb ? j : W + j;
+    } else {
+        const int r = b - tb * DWp - H * side;
+        hp = tb + H + r / DWp;
+        wp = r - (r / DWp) * DWp;
+    }
+    *(u32x4*)&Dh[(((size_t)n * DHp + hp) * DWp + wp) * Ktot + 8 * c8] = u32x4{0u, 0u, 0u, 0u};
 }
 
 // The backward's strip: `yrows` input rows whose covering pooled rows (at
@@ -852,6 +1012,55 @@ hipError_t launch_lrn_pool_backward(const float* pooled, const float* top, const
             FUSED_BWD(0, 0, 3);
     }
 #undef FUSED_BWD
+    return hipGetLastError();
+}
+
+int lrn_pool_backward_strips(int H, int OH, int OW, int kh, int sh, int ph)
+{
+    const int yrows = fused_backward_yrows(H, OH, OW, kh, sh, ph);
+    return yrows > 0 ? (H + yrows - 1) / yrows : 0;
+}
+
+hipError_t launch_lrn_pool_backward_bf16(const float* pooled, const float* top,
+                                         const float* top_diff, const int32_t* mask,
+                                         const float* relu_top, uint16_t* Dh, float* sums, int N,
+                                         int C, int H, int W, int OH, int OW, int kh, int kw,
+                                         int sh, int sw, int ph, int pw, int size, float alpha,
+                                         float beta, float k, int Kg, int Kgp, int Ktot, int DHp,
+                                         int DWp, int tb, int lb, hipStream_t s)
+{
+    if ((long)N * C * H * W == 0)
+        return hipSuccess;
+    const int yrows = fused_backward_yrows(H, OH, OW, kh, sh, ph);
+    if (yrows == 0 || (size != 3 && size != 5) || Kg % kFuseCh != 0 || Ktot % 8 != 0 ||
+        tb < 0 || lb < 0 || DHp < tb + H || DWp < lb + W)
+        return hipErrorInvalidValue;
+    const long border = (long)N * (DHp * DWp - H * W) * (Ktot / 8);
+    if (border > 0)
+        hipLaunchKernelGGL(dh_zero_border_kernel, dim3((unsigned)((border + 255) / 256)), dim3(256),
+                           0, s, Dh, N, DHp, DWp, tb, lb, H, W, Ktot, border);
+    const int nstrips = (H + yrows - 1) / yrows;
+    const int nchunks = C / kFuseCh;
+    const dim3 g((unsigned)((long)N * nchunks * nstrips));
+    const float an = alpha / size;
+#define FUSED_BWD16(KS_, SS_, SZ_)                                                                \
+    hipLaunchKernelGGL((lrn_pool_backward_bf16_kernel<KS_, SS_, SZ_>), g, dim3(256), 0, s,       \
+                       pooled, top, top_diff, mask, relu_top, Dh, sums, N, C, H, W, OH, OW, kh,  \
+                       kw, sh, sw, ph, pw, yrows, nstrips, nchunks, an, beta, k, Kg, Kgp, Ktot,  \
+                       DHp, DWp, tb, lb)
+    const bool k32 = kh == 3 && kw == 3 && sh == 2 && sw == 2;
+    if (size == 5) {
+        if (k32)
+            FUSED_BWD16(3, 2, 5);
+        else
+            FUSED_BWD16(0, 0, 5);
+    } else {
+        if (k32)
+            FUSED_BWD16(3, 2, 3);
+        else
+            FUSED_BWD16(0, 0, 3);
+    }
+#undef FUSED_BWD16
     return hipGetLastError();
 }
 

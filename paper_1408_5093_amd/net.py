@@ -15,8 +15,9 @@ import torch
 
 from . import (BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED,
                CAFFE_BF16, CAFFE_F32,
-               PASS_BACKWARD, PASS_BACKWARD_WEIGHTS, PASS_FORWARD, POOL_RELU_INPUT, Workspace,
-               caffe_conv_backward, caffe_conv_forward, cast_f32_to_bf16, conv_desc, conv_out_shape,
+               PASS_BACKWARD, PASS_BACKWARD_POOL_LRN, PASS_BACKWARD_WEIGHTS, PASS_FORWARD,
+               POOL_RELU_INPUT, Workspace, caffe_conv_backward, caffe_conv_backward_pool_lrn,
+               caffe_conv_forward, cast_f32_to_bf16, conv_desc, conv_out_shape, lrn_desc,
                conv_workspace_size, lrn_backward, lrn_forward, maxpool_backward, maxpool_forward,
                lrn_pool_backward, pool_desc, pool_lrn_forward, pool_lrn_supported,
                pool_out_shape, sgd_learning_rate, sgd_update, softmax_loss)
@@ -28,7 +29,7 @@ class ConvStack:
     bfloat16 operands (fp32 accumulation and outputs); glue stays fp32."""
 
     def __init__(self, layers, N, weights, biases, glue=None, bf16=False, device="cuda",
-                 fuse_glue=True, split_backward=True):
+                 fuse_glue=True, split_backward=True, fuse_staging=True):
         self.layers = list(layers)
         self.N = N
         self.bf16 = bf16
@@ -60,6 +61,9 @@ class ConvStack:
             self.bottom_op.append(torch.empty((N, L.C, L.H, L.W), dtype=op, device=dev)
                                   if bf16 else None)
             need_l = max(conv_workspace_size(d, PASS_BACKWARD), conv_workspace_size(d, PASS_FORWARD))
+            glue_l = [kind for kind, _ in self.glue.get(l, [])]
+            if bf16 and fuse_staging and glue_l == ["pool", "lrn"]:
+                need_l = max(need_l, conv_workspace_size(d, PASS_BACKWARD_POOL_LRN))
             ws_need = max(ws_need, need_l)
             ws_layer.append(need_l)
             ws_weights = max(ws_weights, conv_workspace_size(d, PASS_BACKWARD_WEIGHTS))
@@ -140,6 +144,19 @@ class ConvStack:
                 self.fused[l] = pool_lrn_supported(st[0]["in_shape"], p["kernel"], p["stride"],
                                                    p.get("pad", 0), r["size"], r["alpha"],
                                                    r["beta"], r["k"])
+        # bf16: a layer whose output goes through the fused max-pool + LRN
+        # hands the glue's backward to its own backward call, which writes
+        # the bf16 staging of its top gradient directly (the float gradient
+        # is never stored); dbottom of the glue stage is then not written
+        self.fuse_staging = [bf16 and fuse_staging and self.fused[l] for l in range(n)]
+        for l in range(n):
+            if self.fuse_staging[l]:
+                pst, lst = self.stages[l]
+                p, r = pst["prm"], lst["prm"]
+                pst["pool_desc"] = pool_desc(pst["in_shape"], p["kernel"], p["stride"],
+                                             p.get("pad", 0))
+                lst["lrn_desc"] = lrn_desc(pst["y"].shape, r["size"], r["alpha"], r["beta"],
+                                           r["k"])
         # when a list, (tag, event) pairs are recorded around every conv call:
         # tag = (kind, layer, "begin" | "end") with kind "fwd" (forward),
         # "bwd" (data gradient), "wgt" (weight and bias gradients) or "both"
@@ -202,6 +219,9 @@ class ConvStack:
         for l in range(len(self.layers) - 1, -1, -1):
             L = self.layers[l]
             g = g.view(self.out_shape[l])
+            if self.fuse_staging[l]:
+                g = self._backward_pool_lrn(l, g, s, l > 0 or data_grad_bottom)
+                continue
             if self.fused[l]:
                 pst, lst = self.stages[l]
                 p, r = pst["prm"], lst["prm"]
@@ -259,10 +279,31 @@ class ConvStack:
             s.wait_stream(self.side)
         return self.dbottom[0]
 
+    def _backward_pool_lrn(self, l, g, s, want_dx):
+        """Layer l's backward from the gradient g of the LRN after its max-pool
+        (one call: the glue's backward staged as the bf16 top gradient)."""
+        pst, lst = self.stages[l]
+        L = self.layers[l]
+        flags = BACKWARD_BOTTOM_STAGED
+        if self.top_masked[l]:
+            flags |= BACKWARD_TOP_DIFF_MASKED
+        if self.mask_bottom[l] and want_dx:
+            flags |= BACKWARD_MASK_BOTTOM_DIFF
+        self._mark(("both" if want_dx else "wgt", l, "begin"), s)
+        caffe_conv_backward_pool_lrn(self.descs[l], pst["pool_desc"], lst["lrn_desc"], pst["y"],
+                                     lst["y"], g, pst["mask"], self.top[l] if L.relu else None,
+                                     self.bottom_op[l], self.W[l],
+                                     self.dbottom[l] if want_dx else None, self.dW[l],
+                                     self.db[l], 0, flags, self.ws_of[l], s)
+        self._mark(("both" if want_dx else "wgt", l, "end"), s)
+        return self.dbottom[l]
+
     def layer_top_diff(self, l, top_diff_last):
         """Gradient that layer l received in the last backward (after its glue)."""
         if l == len(self.layers) - 1:
             return top_diff_last
+        if self.fuse_staging[l]:
+            raise ValueError(f"layer {l}'s top gradient is staged in bf16 only (fuse_staging)")
         st = self.stages[l]
         return st[0]["dx"] if st else self.dbottom[l + 1].view(self.top[l].shape)
 

@@ -226,7 +226,11 @@ def test_caffenet_bf16_training_step_full_size():
     on the tensors the GPU consumed (sampled images and filters)."""
     N = 512
     inp = wl.caffenet_step(N, wl.CAFFENET_STEP_BF16)
-    net = ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(), bf16=True)
+    # (unfused staging: the glue's float gradient is stored, so the check can
+    # read each layer's top gradient; the fused step is compared with this one
+    # in test_caffenet_bf16_step_fused_staging_matches)
+    net = ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(), bf16=True,
+                    fuse_staging=False)
     x = torch.from_numpy(inp["x"]).to(DEV)
     g = torch.from_numpy(inp["top_diff"]).to(DEV)
     net.forward(x)
@@ -269,3 +273,27 @@ def test_backward_side_stream_fork_bf16(overrides):
     for a, b in zip(out["1"], out["0"]):
         for u, v in zip(a, b):
             assert torch.equal(u, v)
+
+
+def test_caffenet_bf16_step_fused_staging_matches():
+    """The bf16 step at N=512 with conv1's and conv2's top gradients staged
+    by the fused glue backward (the default) against the unfused step: every
+    data and weight gradient bit for bit (the staged bf16 gradient is the
+    same), every bias gradient within 1e-6, over two steps."""
+    N = 512
+    inp = wl.caffenet_step(N, wl.CAFFENET_STEP_BF16)
+    x = torch.from_numpy(inp["x"]).to(DEV)
+    g = torch.from_numpy(inp["top_diff"]).to(DEV)
+    nets = [ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(), bf16=True,
+                      fuse_staging=f) for f in (True, False)]
+    assert nets[0].fuse_staging[:2] == [True, True] and not any(nets[1].fuse_staging)
+    for _ in range(2):
+        for net in nets:
+            net.forward(x)
+            net.backward(g)
+        torch.cuda.synchronize()
+        a, b = nets
+        for l in range(len(wl.CAFFENET)):
+            assert torch.equal(a.dbottom[l], b.dbottom[l]), f"layer {l} data gradient"
+            assert torch.equal(a.dW[l], b.dW[l]), f"layer {l} weight gradient"
+            assert_close(_np(a.db[l]), _np(b.db[l]), 1e-6, f"layer {l} bias gradient")

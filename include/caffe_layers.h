@@ -130,6 +130,16 @@ int caffe_conv_backward_pool_lrn(const caffe_conv_desc* desc, const caffe_pool_d
                                  float* bias_diff, int32_t accumulate, int32_t flags,
                                  void* workspace, size_t ws_bytes, void* stream);
 
+/* The backward pass of a rectified-linear layer (Sec. 3.2 lists ReLU among
+ * Caffe's layers): bottom_diff[i] = top[i] > 0 ? top_diff[i] : 0 for
+ * i < count, where top is the layer's forward output (a NaN top gives 0).
+ * bottom_diff may be top_diff (in place).  A network uses it where a ReLU's
+ * backward is not folded into a neighbouring layer's kernels, e.g. to mask a
+ * convolution's top gradient once before its data and weight gradients run
+ * as separate calls. */
+int caffe_relu_backward(const float* top, const float* top_diff, float* bottom_diff,
+                        int64_t count, void* stream);
+
 /* out[i] = bfloat16(in[i]) rounded to nearest even, i < count.  The input for
  * CAFFE_BF16 convolutions. */
 int caffe_cast_f32_to_bf16(const float* in, uint16_t* out, int64_t count, void* stream);

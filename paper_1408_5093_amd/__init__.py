@@ -28,7 +28,7 @@ __all__ = [
     "conv_backward_data", "conv_backward_weights", "maxpool_forward", "maxpool_backward",
     "lrn_forward", "lrn_backward", "cast_f32_to_bf16", "Workspace", "CaffeError",
     "sgd_learning_rate", "softmax_loss", "sgd_update", "pool_lrn_forward", "lrn_pool_backward",
-    "pool_lrn_supported", "caffe_conv_backward_pool_lrn",
+    "pool_lrn_supported", "caffe_conv_backward_pool_lrn", "relu_backward",
 ]
 
 
@@ -333,6 +333,20 @@ def caffe_conv_backward_pool_lrn(desc, pool, lrn, pooled, lrn_top, lrn_top_diff,
         _ptr(lrn_top_diff), _ptr(pool_mask), _ptr(top), _ptr(bottom), _ptr(weight),
         _ptr(bottom_diff), _ptr(weight_diff), _ptr(bias_diff), int(accumulate), int(flags),
         _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def relu_backward(top, top_diff, out=None, stream=None):
+    """bottom_diff = top_diff [top > 0] (the ReLU layer's backward)."""
+    for t, n in ((top, "top"), (top_diff, "top_diff")):
+        _dev(t, n, torch.float32)
+    if top.shape != top_diff.shape:
+        raise ValueError("top and top_diff differ in shape")
+    if out is None:
+        out = torch.empty_like(top_diff)
+    _dev(out, "bottom_diff", torch.float32)
+    check(load().caffe_relu_backward(_ptr(top), _ptr(top_diff), _ptr(out), top.numel(),
+                                     _stream(stream)))
+    return out
 
 
 def cast_f32_to_bf16(x, out=None, stream=None):

@@ -48,7 +48,7 @@ EXPORTS = (
     "caffe_sgd_learning_rate", "caffe_softmax_loss", "caffe_sgd_update",
     "caffe_pool_lrn_forward", "caffe_lrn_pool_backward", "caffe_sgd_update_device_lr",
     "caffe_conv_workspace_bytes", "caffe_conv_status_string", "caffe_conv_forward_noalloc",
-    "caffe_conv_backward_pool_lrn",
+    "caffe_conv_backward_pool_lrn", "caffe_relu_backward",
 )
 
 
@@ -114,6 +114,7 @@ def load():
         "caffe_lrn_forward": [ldp, vp, vp, vp],
         "caffe_lrn_backward": [ldp, vp, vp, vp, vp, vp],
         "caffe_cast_f32_to_bf16": [vp, vp, i64, vp],
+        "caffe_relu_backward": [vp, vp, vp, i64, vp],
         "caffe_pool_lrn_forward": [pdp, ldp, vp, vp, vp, vp, i32, vp],
         "caffe_lrn_pool_backward": [pdp, ldp, vp, vp, vp, vp, vp, vp],
         "caffe_conv_backward_pool_lrn": [cdp, pdp, ldp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,

@@ -1557,6 +1557,22 @@ int caffe_lrn_pool_backward(const caffe_pool_desc* pd, const caffe_lrn_desc* ld,
     return CAFFE_OK;
 }
 
+int caffe_relu_backward(const float* top, const float* top_diff, float* bottom_diff,
+                        int64_t count, void* stream)
+{
+    if (count < 0)
+        return fail(CAFFE_ERR_INVALID_ARG, "count must be >= 0");
+    if (count * 4 > kMaxTensorBytes)
+        return fail(CAFFE_ERR_UNSUPPORTED, "a tensor reaches 2^31 bytes");
+    const bool nz = count > 0;
+    CHECK(check_ptr(top, nz, "top"));
+    CHECK(check_ptr(top_diff, nz, "top_diff"));
+    CHECK(check_ptr(bottom_diff, nz, "bottom_diff"));
+    LAUNCH(launch_relu_mask(top_diff, top, bottom_diff, count, (hipStream_t)stream),
+           "ReLU backward launch");
+    return CAFFE_OK;
+}
+
 int caffe_cast_f32_to_bf16(const float* in, uint16_t* out, int64_t count, void* stream)
 {
     if (count < 0)

@@ -845,9 +845,9 @@ lrn_pool_backward_kernel(const float* __restrict__ a_in, const float* __restrict
 // fold it.  A block's 16 channels lie in one
 // group (Kg % 16 == 0), so each input position stores them as two 16-byte
 // chunks.  The fp32 values are also summed per channel over the block's
-// positions (each thread its own positions in row order, then a fixed
-// pairwise tree over the threads): sums[(g * Kg + k) * T + n * nstrips +
-// strip], T = N * nstrips, the bias-gradient partials.  The staging grid's
+// positions (each thread its own positions in row order, a fixed butterfly
+// over each wave, then the four waves in order): sums[(g * Kg + k) * T +
+// n * nstrips + strip], T = N * nstrips, the bias-gradient partials.  The staging grid's
 // border is written by dh_zero_border_kernel.
 template <int KS, int SS, int SIZE>
 __global__ void __launch_bounds__(256)
@@ -906,21 +906,22 @@ lrn_pool_backward_bf16_kernel(const float* __restrict__ a_in, const float* __res
             dst[1] = u32x4{packed[4], packed[5], packed[6], packed[7]};
         }
     }
-    // bias-gradient partials: one fixed pairwise tree per channel (LDS reused)
-    __syncthreads();
-    float* red = &gs[0][0];
-    const size_t T = (size_t)N * nstrips;
+    // bias-gradient partials: per channel a wave butterfly (fixed), then the
+    // four waves' sums added in wave order
+    __shared__ float red[kFuseCh][4];
+    const int wave = threadIdx.x >> 6;
+#pragma unroll
     for (int t = 0; t < kFuseCh; ++t) {
-        red[threadIdx.x] = bsum[t];
-        __syncthreads();
-        for (int half = 128; half > 0; half >>= 1) {
-            if (threadIdx.x < half)
-                red[threadIdx.x] += red[threadIdx.x + half];
-            __syncthreads();
-        }
-        if (threadIdx.x == 0 && f.c0 + t < C)
-            sums[(size_t)(f.c0 + t) * T + (size_t)f.n * nstrips + f.strip] = red[0];
-        __syncthreads();
+        const float v = wave_sum(bsum[t]);
+        if ((threadIdx.x & 63) == 0)
+            red[t][wave] = v;
+    }
+    __syncthreads();
+    const int t = threadIdx.x;
+    if (t < kFuseCh && f.c0 + t < C) {
+        const size_t T = (size_t)N * nstrips;
+        sums[(size_t)(f.c0 + t) * T + (size_t)f.n * nstrips + f.strip] =
+            ((red[t][0] + red[t][1]) + red[t][2]) + red[t][3];
     }
 }
 

@@ -19,7 +19,7 @@ from . import (BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_D
                POOL_RELU_INPUT, Workspace, caffe_conv_backward, caffe_conv_backward_pool_lrn,
                caffe_conv_forward, cast_f32_to_bf16, conv_desc, conv_out_shape, lrn_desc,
                conv_workspace_size, lrn_backward, lrn_forward, maxpool_backward, maxpool_forward,
-               lrn_pool_backward, pool_desc, pool_lrn_forward, pool_lrn_supported,
+               lrn_pool_backward, pool_desc, pool_lrn_forward, pool_lrn_supported, relu_backward,
                pool_out_shape, sgd_learning_rate, sgd_update, softmax_loss)
 
 
@@ -101,10 +101,11 @@ class ConvStack:
         # workspace) while the data gradient and the glue below it go on in
         # the caller's stream: the GEMMs fill each other's idle compute units
         # and the bandwidth-bound glue hides behind them (CaffeNet conv1-5,
-        # N=256: 9.80 -> 9.39 ms per step).  The top layer's gradient still
-        # needs the ReLU mask, which one combined call applies once (split,
-        # the two calls would each apply it: measured no faster).  bf16 keeps
-        # one call: both passes read the top gradient it stages once.
+        # N=256: 9.80 -> 9.39 ms per step).  A layer whose top gradient
+        # arrives unmasked (the top layer) runs its ReLU's backward as a pass
+        # of its own first, so that both calls take the masked gradient.
+        # bf16 keeps one call: both passes read the top gradient it stages
+        # once.
         self.split_backward = split_backward and not bf16
         if self.split_backward:
             self.side = torch.cuda.Stream(device=dev)
@@ -133,6 +134,11 @@ class ConvStack:
             elif not st and l + 1 < n:
                 self.mask_bottom[l + 1] = True
                 self.top_masked[l] = True
+        # masked top gradients of the layers whose ReLU backward runs as its
+        # own pass (split backward only)
+        self.dtop_relu = [torch.empty_like(self.top[l])
+                          if self.split_backward and L.relu and not self.top_masked[l] else None
+                          for l, L in enumerate(self.layers)]
         # A max-pool directly followed by an LRN runs as one fused pass each
         # way (the pooled gradient never stored) when the kernels take the
         # geometry; the LRN stage then has no "dx".
@@ -246,7 +252,10 @@ class ConvStack:
             if self.bf16:
                 flags |= BACKWARD_BOTTOM_STAGED
             top = self.top[l] if L.relu else None
-            if split and (self.top_masked[l] or not L.relu):
+            if split and self.dtop_relu[l] is not None:
+                g = relu_backward(self.top[l], g, out=self.dtop_relu[l], stream=s)
+                flags |= BACKWARD_TOP_DIFF_MASKED
+            if split and (flags & BACKWARD_TOP_DIFF_MASKED or not L.relu):
                 ready = torch.cuda.Event()
                 ready.record(s)
                 # the data gradient (on the critical path) goes out first

@@ -155,3 +155,18 @@ def test_pool_lrn_fused_unsupported_and_empty():
     dx = cc.lrn_pool_backward(x.shape, pooled, y, torch.zeros_like(y), mask, 3, 2, 0, 5)
     torch.cuda.synchronize()
     assert dx.shape == x.shape
+
+
+def test_relu_backward():
+    """bottom_diff = top_diff [top > 0] (exact select; NaN top gives 0), in
+    place too, and with a length that is not a multiple of 4."""
+    rng = np.random.default_rng(31)
+    for n in (1, 7, 4099, 100000):
+        top = torch.from_numpy(rng.standard_normal(n).astype(np.float32)).to(DEV)
+        top[0] = float("nan")
+        g = torch.from_numpy(rng.standard_normal(n).astype(np.float32)).to(DEV)
+        ref = torch.where(top > 0, g, torch.zeros_like(g))
+        assert torch.equal(cc.relu_backward(top, g), ref)
+        g2 = g.clone()
+        cc.relu_backward(top, g2, out=g2)
+        assert torch.equal(g2, ref)

@@ -57,7 +57,7 @@ struct ConvPlan {
     // weight gradient split-K; the quad-order kernel reads a per-column table
     // of ncol_pad entries at off_coltab
     int splits, cols_per_split, wgrad_tile;
-    bool wgrad_quad;
+    bool wgrad_quad, wgrad_dma;
     int ncol_pad, xpad;
     size_t off_coltab;
     // reduction order of the implicit GEMMs: tap-major r = (u, v, c) when the
@@ -472,6 +472,9 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
                        wgrad_quad_supported(q.Cg, q.kh, q.kw) && xlim < kMaxTensorBytes &&
                        dlim < kMaxTensorBytes;
         q.ncol_pad = (int)((ncol + 15) / 16 * 16);
+        // the quad order with both operands copied by LDS DMA (the same
+        // table and conditions; splits are whole 16-column stages)
+        q.wgrad_dma = q.wgrad_quad && env_tile("CAFFE_CONV_WGRAD_DMA") != 0;
     }
     q.fwd_tap = q.Cg % gemm_tile_k(q.fwd_tile) == 0;
     q.dgrad_tap = q.Kg % gemm_tile_k(q.dgrad_tile) == 0;
@@ -750,7 +753,10 @@ int run_weights(const ConvPlan& q, const float* dsrc, const void* bottom, float*
         p.T = tab;
         p.T_bytes = nbytes((int64_t)q.ncol_pad * 3, 4);
         p.xpad = q.xpad;
-        LAUNCH(launch_conv_wgrad_quad_f32(p, q.wgrad_tile, s), "weight-gradient launch");
+        if (q.wgrad_dma)
+            LAUNCH(launch_conv_wgrad_dma_f32(p, q.wgrad_tile, s), "weight-gradient launch");
+        else
+            LAUNCH(launch_conv_wgrad_quad_f32(p, q.wgrad_tile, s), "weight-gradient launch");
     } else {
         LAUNCH(launch_conv_wgrad_f32(p, q.wgrad_tile, s), "weight-gradient launch");
     }

@@ -557,6 +557,256 @@ conv_wgrad_quad_f32_kernel(const WgradParams p)
     }
 }
 
+// ----------------------------------------------------------- LDS-DMA order
+// The quad-order GEMM with both operands copied global -> LDS by the buffer
+// unit (one wave instruction writes 64 consecutive floats), with lanes along
+// the reduction index: no register staging, no LDS stores, no waits on the
+// loads before the stores.
+//
+// LDS holds each operand as [tile row][16 columns of the stage], one 64-byte
+// row per tile row, its four 16-byte chunks permuted: logical chunk c of row
+// R sits in slot c ^ wchunk_swz(R).  A fragment read (ds_read_b128: 16 rows,
+// one chunk) then touches distinct banks whether the LDS serves 16 lanes of
+// 64 banks or 8 lanes of 32 banks per cycle.  The MFMA k index is permuted
+// within a stage: lane group kl (lane / 32) takes the stage's columns
+// 8 kl + step, so one 16-byte read gives a lane's values for four steps; A
+// and B use the same permutation, so each step's sum is unchanged.
+//
+// A copy moves four tile rows (16 lanes each): lane L holds row 4j + L / 16,
+// slot (L / 4) % 4, element L % 4, i.e. the logical column
+// 4 ((L / 4 % 4) ^ wchunk_swz(4j + L / 16)) + L % 4.  Copy j = wave + 4q of a
+// wave has j % 4 = wave, and wchunk_swz depends on the row only through its
+// bits 1..3, so a lane's column is the same in every copy of every stage: it
+// loads one column-table entry per stage.
+__device__ __forceinline__ int wchunk_swz(int r)
+{
+    return ((r >> 2) & 1) | ((((r >> 1) ^ (r >> 3)) & 1) << 1);
+}
+
+template <int WM, int WN, int MI, int NI, int KH, int KW>
+__global__ void __launch_bounds__(64 * WM * WN)
+conv_wgrad_dma_f32_kernel(const WgradParams p)
+{
+    constexpr int MT = 32;
+    constexpr int NW = WM * WN;
+    constexpr int TM = WM * MI * MT;
+    constexpr int TN = WN * NI * MT;
+    constexpr int TK = 16;
+    constexpr int CA = TM / 4;             // A copies per stage
+    constexpr int CB = TN / 4;             // B copies per stage
+    constexpr int NA = CA / NW, NB = CB / NW;
+    constexpr int KHW = KH * KW;
+    static_assert(NW == 4 && CA % NW == 0 && CB % NW == 0, "copy mapping: wave = copy % 4");
+    static_assert(KHW < 32, "one mask bit per tap");
+
+    __shared__ float As0[TM * TK], As1[TM * TK];
+    __shared__ float Bs0[TN * TK], Bs1[TN * TK];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave % WM;
+    const int wn = wave / WM;
+    const int n_rt = (p.R + TN - 1) / TN;
+    const int n_mt = (p.Kg + TM - 1) / TM;
+    const int per_xcd = gridDim.x >> 3;
+    const int T = p.xcd_order ? (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3) : blockIdx.x;
+    if (T >= n_rt * n_mt * p.G * p.splits)
+        return;
+    const int rt = T % n_rt;
+    const int mt = (T / n_rt) % n_mt;
+    const int g = (T / (n_rt * n_mt)) % p.G;
+    const int split = T / (n_rt * n_mt * p.G);
+    const int m0 = mt * TM;
+    const int r0 = rt * TN;
+    const int IW = p.IW, IHW = p.IH * p.IW;
+    const int OHW = p.OH * p.OW;
+    const int col_begin = split * p.cols_per_split;
+    const int col_end = min(p.Ncol, col_begin + p.cols_per_split);
+
+    const __amdgpu_buffer_rsrc_t rd = make_rsrc(p.D, p.D_bytes);
+    // X through a base p.xpad elements early, as in the quad kernel
+    const __amdgpu_buffer_rsrc_t rx =
+        make_rsrc((const char*)p.X - 4 * (size_t)p.xpad, p.X_bytes + 4u * (uint32_t)p.xpad);
+    const __amdgpu_buffer_rsrc_t rtab = make_rsrc(p.T, p.T_bytes);
+
+    // this lane's place in every copy: row 4j + rg, logical column kcol
+    const int rg = lane >> 4;
+    const int kcol = 4 * (((lane >> 2) & 3) ^ wchunk_swz(4 * wave + rg)) + (lane & 3);
+    // A copy q: rows m0 + 4j .. + 3 of group g, j = wave + 4q (scalar part),
+    // the lane's row rg in its lane offset
+    const uint32_t a_lane4 = (uint32_t)(rg * OHW) * 4u;
+    // B copy q: quad rows r0 + 4j .. + 3 = channels 4 cb .. 4 cb + 3 (the
+    // lane's c % 4 = rg) of tap t: offset and mask bit uniform
+    const uint32_t b_lane4 = (uint32_t)(rg * IHW) * 4u;
+    uint32_t b_soff[NB], b_bit[NB];
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+        const int tg = r0 / 4 + wave + NW * q;
+        const int cb = tg / KHW;
+        const int t = tg - cb * KHW;
+        const int u = t / KW;
+        const int v = t - u * KW;
+        b_soff[q] = (uint32_t)((g * p.Cg + 4 * cb) * IHW + u * IW + v) * 4u;
+        b_bit[q] = (uint32_t)t;
+    }
+    const uint32_t a_soff0 = (uint32_t)((g * p.Kg + m0 + 4 * wave) * OHW) * 4u;
+    const uint32_t a_step4 = (uint32_t)(4 * NW * OHW) * 4u;
+
+    typedef uint32_t u32x3 __attribute__((ext_vector_type(3)));
+    auto load_entry = [&](int cbase) {
+        return __builtin_bit_cast(
+            u32x3,
+            __builtin_amdgcn_raw_buffer_load_b96(rtab, (uint32_t)(cbase + kcol) * 12u, 0, 0));
+    };
+    auto copy_stage = [&](float* As, float* Bs, const u32x3& e) {
+        const uint32_t da = e[2] + a_lane4;
+#pragma unroll
+        for (int q = 0; q < NA; ++q)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rd, (lds_void*)&As[16 * 4 * (wave + NW * q)],
+                                                     4, da, a_soff0 + q * a_step4, 0, 0);
+        const uint32_t xb = e[0] + b_lane4;
+#pragma unroll
+        for (int q = 0; q < NB; ++q)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)&Bs[16 * 4 * (wave + NW * q)],
+                                                     4, xb | ((e[1] >> b_bit[q]) << 31),
+                                                     b_soff[q], 0, 0);
+    };
+
+    floatx16 acc[MI][NI];
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+            acc[mi][ni] = floatx16{};
+
+    // bias-gradient partials: the first tap tile's threads t < TM add up row t
+    const bool want_db = p.dbp != nullptr && rt == 0;
+    float dsum = 0.f;
+
+    // fragment reads: tile row R of a 32-row block, chunks 2 kl and 2 kl + 1
+    const int l32 = lane & 31;
+    const int kl = lane >> 5;
+    int fa[MI][2], fb[NI][2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) {
+            const int R = wm * MI * MT + mi * MT + l32;
+            fa[mi][h] = R * TK + 4 * ((2 * kl + h) ^ wchunk_swz(R));
+        }
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) {
+            const int R = wn * NI * MT + ni * MT + l32;
+            fb[ni][h] = R * TK + 4 * ((2 * kl + h) ^ wchunk_swz(R));
+        }
+    }
+    // column blocks of this wave that hold taps below R (as in the quad kernel)
+    const int nbv = __builtin_amdgcn_readfirstlane(
+        min(max((p.R - (r0 + wn * NI * MT) + MT - 1) / MT, 0), NI));
+
+    const int nst = col_end > col_begin ? (col_end - col_begin + TK - 1) / TK : 0;
+    u32x3 e_next = {0u, 0u, 0u};
+    if (nst > 0) {
+        copy_stage(As0, Bs0, load_entry(col_begin));
+        e_next = load_entry(col_begin + TK);
+    }
+    __builtin_amdgcn_s_waitcnt(kVmcnt0);
+    __syncthreads();
+
+    auto stage_loop = [&](auto nb_tag) {
+    constexpr int NB_ = decltype(nb_tag)::value;
+    for (int s0 = 0; s0 < nst; s0 += 2) {
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb) {
+            const int s = s0 + hb;
+            if (s >= nst)
+                break;
+            float* Ac = hb ? As1 : As0;
+            float* Bc = hb ? Bs1 : Bs0;
+            float* An = hb ? As0 : As1;
+            float* Bn = hb ? Bs0 : Bs1;
+            if (s + 1 < nst) {
+                copy_stage(An, Bn, e_next);
+                // (past the split it reads unused entries, or 0 past the table)
+                e_next = load_entry(col_begin + (s + 2) * TK);
+            }
+            if (want_db && tid < TM) {
+                // row tid in the order of its logical chunks
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const floatx4 v =
+                        *(const floatx4*)&Ac[tid * TK + 4 * (c ^ wchunk_swz(tid))];
+                    dsum += v[0];
+                    dsum += v[1];
+                    dsum += v[2];
+                    dsum += v[3];
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            floatx4 xa[2][MI], xb[2][NI];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+#pragma unroll
+                for (int mi = 0; mi < MI; ++mi)
+                    xa[h][mi] = *(const floatx4*)&Ac[fa[mi][h]];
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni)
+                    xb[h][ni] = *(const floatx4*)&Bc[fb[ni][h]];
+            }
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+                        for (int ni = 0; ni < NB_; ++ni)
+                            acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                                xa[h][mi][i], xb[h][ni][i], acc[mi][ni], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            // the next stage's copies have landed, for every wave
+            __builtin_amdgcn_s_waitcnt(kVmcnt0);
+            __syncthreads();
+        }
+    }
+    };
+    if (nbv == NI)
+        stage_loop(std::integral_constant<int, NI>{});
+    else if (NI > 1 && nbv == 1)
+        stage_loop(std::integral_constant<int, 1>{});
+    else
+        stage_loop(std::integral_constant<int, 0>{});
+
+    if (want_db) {
+        const int m = m0 + tid;
+        if (tid < TM && m < p.Kg)
+            p.dbp[split * p.K + g * p.Kg + m] = dsum;
+    }
+
+    // Partial P[split][g*Kg + m][r], r = c*KHW + t for r' = (cb*KHW + t)*4 + c % 4.
+    const __amdgpu_buffer_rsrc_t rp = make_rsrc(p.P, p.P_bytes);
+    const int pbase = split * p.K * p.R;
+#pragma unroll
+    for (int ni = 0; ni < NI; ++ni) {
+        const int rq = r0 + wn * NI * MT + ni * MT + l32;
+        const int tg = rq >> 2;
+        const int cb = tg / KHW;
+        const int r = (4 * cb + (rq & 3)) * KHW + (tg - cb * KHW);
+        const bool rok = rq < p.R;
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) {
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                const int m = m0 + wm * MI * MT + mi * MT + 8 * (q >> 2) + 4 * kl + (q & 3);
+                const bool ok = rok && m < p.Kg;
+                const uint32_t off = ok ? (uint32_t)(pbase + (g * p.Kg + m) * p.R + r) * 4u : kOob;
+                buf_st_f32(acc[mi][ni][q], rp, off);
+            }
+        }
+    }
+}
+
 // One thread per column: see launch_wgrad_col_table.
 __global__ void __launch_bounds__(256)
 wgrad_col_table_kernel(uint32_t* __restrict__ T, int ncol, int ncol_pad, int C, int IH, int IW,
@@ -673,6 +923,47 @@ hipError_t launch_wqg(const WgradParams& p, hipStream_t s)
     return hipErrorInvalidValue;
 }
 }  // namespace
+
+namespace {
+template <int WM, int WN, int MI, int NI, int KH, int KW>
+hipError_t launch_wd(const WgradParams& p, hipStream_t s)
+{
+    constexpr int TM = WM * MI * 32, TN = WN * NI * 32;
+    const int64_t tiles =
+        (int64_t)((p.R + TN - 1) / TN) * ((p.Kg + TM - 1) / TM) * p.G * p.splits;
+    const int64_t per_xcd = (tiles + 7) / 8;
+    hipLaunchKernelGGL((conv_wgrad_dma_f32_kernel<WM, WN, MI, NI, KH, KW>),
+                       dim3((unsigned)(per_xcd * 8)), dim3(64 * WM * WN), 0, s, p);
+    return hipGetLastError();
+}
+
+template <int WM, int WN, int MI, int NI>
+hipError_t launch_wdg(const WgradParams& p, hipStream_t s)
+{
+    if (p.kh == 3 && p.kw == 3)
+        return launch_wd<WM, WN, MI, NI, 3, 3>(p, s);
+    if (p.kh == 5 && p.kw == 5)
+        return launch_wd<WM, WN, MI, NI, 5, 5>(p, s);
+    return hipErrorInvalidValue;
+}
+}  // namespace
+
+hipError_t launch_conv_wgrad_dma_f32(const WgradParams& p, int tile, hipStream_t s)
+{
+    if (!wgrad_quad_supported(p.Cg, p.kh, p.kw) || p.T == nullptr || p.xpad < 0 ||
+        p.cols_per_split % 16 != 0)
+        return hipErrorInvalidValue;
+    switch (tile) {
+    case WTILE_128x128:
+        return launch_wdg<2, 2, 2, 2>(p, s);
+    case WTILE_96x128:
+        return launch_wdg<1, 4, 3, 1>(p, s);
+    case WTILE_64x128:
+        return launch_wdg<2, 2, 1, 2>(p, s);
+    default:
+        return hipErrorInvalidValue;
+    }
+}
 
 bool wgrad_quad_supported(int Cg, int kh, int kw)
 {

@@ -174,6 +174,9 @@ hipError_t launch_conv_wgrad_f32(const WgradParams& p, int tile, hipStream_t s);
 // geometry.  Partials in the layout launch_conv_wgrad_f32 writes.
 bool wgrad_quad_supported(int Cg, int kh, int kw);
 hipError_t launch_conv_wgrad_quad_f32(const WgradParams& p, int tile, hipStream_t s);
+// The same GEMM with both operands copied global -> LDS by LDS DMA (same
+// table, same conditions, cols_per_split a multiple of 16).
+hipError_t launch_conv_wgrad_dma_f32(const WgradParams& p, int tile, hipStream_t s);
 // Three words per output column col < ncol_pad (ncol_pad a multiple of 16):
 // {byte offset of the column's window origin in X plus xpad = ph*IW + pw
 // elements, mask of the window's taps u*kw + v that lie outside the image,

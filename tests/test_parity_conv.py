@@ -260,10 +260,11 @@ QUAD_CASES = [
 
 @pytest.mark.parametrize("case", QUAD_CASES)
 def test_weight_gradient_quad_order(case, overrides):
-    """The quad-order kernel against the oracle, and bit for bit against the
-    channel-major kernel (same sums, same order; only the tile columns are
-    permuted)."""
+    """The quad-order kernel (register-staged copies) against the oracle, and
+    bit for bit against the channel-major kernel (same sums, same order; only
+    the tile columns are permuted)."""
     overrides.setenv("CAFFE_CONV_WGRAD_QUAD", "1")
+    overrides.setenv("CAFFE_CONV_WGRAD_DMA", "0")
     N, C, H, W, K, kh, kw, sh, sw, ph, pw, g = case
     rng = np.random.default_rng([91, N, C, H, W, K])
     x = rng.standard_normal((N, C, H, W)).astype(np.float32)
@@ -320,3 +321,33 @@ def test_data_gradient_192_rows_masked(tile, overrides):
     dx, _, _ = cc.conv_backward(_t(x), _t(w), _t(gd), None, 1, 1, g, False, need=("dx",),
                                 flags=cc.BACKWARD_MASK_BOTTOM_DIFF)
     assert_close(_np(dx), dx_ref * (x > 0), TOL_F32, "masked data gradient")
+
+
+@pytest.mark.parametrize("case", QUAD_CASES)
+def test_weight_gradient_dma_copies(case, overrides):
+    """The quad-order GEMM with LDS-DMA copies (the default where the quad
+    order applies) against the oracle, against the register-staged kernel to
+    rounding (it sums each stage's columns in another order), and bit for bit
+    from one run to the next; split-K ranges of one stage and of many."""
+    N, C, H, W, K, kh, kw, sh, sw, ph, pw, g = case
+    rng = np.random.default_rng([92, N, C, H, W, K])
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    w = (rng.standard_normal((K, C // g, kh, kw)) * 0.3).astype(np.float32)
+    top = np.maximum(rng.standard_normal((N, K, (H + 2 * ph - kh) // sh + 1,
+                                          (W + 2 * pw - kw) // sw + 1)), 0).astype(np.float32)
+    gd = rng.standard_normal(top.shape).astype(np.float32)
+    _, dw_ref, db_ref = oracle.conv_backward(x, w, gd, top=top, stride=(sh, sw), pad=(ph, pw),
+                                             group=g, relu=True, need=("dw", "db"))
+    args = (_t(x), _t(w), _t(gd), _t(top), (sh, sw), (ph, pw), g, True)
+    for blocks in ("2048", "16"):
+        overrides.setenv("CAFFE_CONV_WGRAD_BLOCKS", blocks)
+        overrides.setenv("CAFFE_CONV_WGRAD_DMA", "1")
+        _, dw, db = cc.conv_backward(*args, need=("dw", "db"))
+        _, dw2, db2 = cc.conv_backward(*args, need=("dw", "db"))
+        overrides.setenv("CAFFE_CONV_WGRAD_DMA", "0")
+        _, dw0, db0 = cc.conv_backward(*args, need=("dw", "db"))
+        torch.cuda.synchronize()
+        assert_close(_np(dw), dw_ref, TOL_F32, f"weight gradient ({blocks} blocks)")
+        assert_close(_np(db), db_ref, TOL_F32, f"bias gradient ({blocks} blocks)")
+        assert torch.equal(dw, dw2) and torch.equal(db, db2)
+        assert_close(_np(dw), _np(dw0), 1e-5, "DMA vs register-staged copies")

@@ -79,8 +79,9 @@ def kernel_of(kind, L, bf16):
                 "both": "conv_gemm_bf16_kernel (data gradient) + conv_wgrad_bf16_kernel"}[kind]
     if L.H == 1 and L.W == 1 and L.k == 1:
         return "dense_gemm (inner product)"
+    # (the quad-order layers run the LDS-DMA variant of the quad kernel)
     quad = (L.C // L.g) % 4 == 0 and L.k in (3, 5)
-    wgt = "conv_wgrad_quad_f32_kernel" if quad else "conv_wgrad_f32_kernel"
+    wgt = "conv_wgrad_dma_f32_kernel" if quad else "conv_wgrad_f32_kernel"
     return {"fwd": "conv_gemm_f32_kernel (forward)",
             "bwd": "conv_gemm_f32_kernel (data gradient)",
             "wgt": wgt,

@@ -297,3 +297,15 @@ def test_caffenet_bf16_step_fused_staging_matches():
             assert torch.equal(a.dbottom[l], b.dbottom[l]), f"layer {l} data gradient"
             assert torch.equal(a.dW[l], b.dW[l]), f"layer {l} weight gradient"
             assert_close(_np(a.db[l]), _np(b.db[l]), 1e-6, f"layer {l} bias gradient")
+
+
+@pytest.mark.parametrize("tile", range(4))
+def test_forced_gemm_tiles_bf16(tile, overrides):
+    """Every bf16 GEMM tile, forced for the forward and the data gradient,
+    on row counts that leave a partial row tile and columns that leave a
+    partial column tile (several tiles each way)."""
+    overrides.setenv("CAFFE_BF16_FWD_TILE", str(tile))
+    overrides.setenv("CAFFE_BF16_DGRAD_TILE", str(tile))
+    run_case(3, 16, 14, 15, 200, 3, 3, 1, 1, 1, 1, 1, True)   # 200 rows, 630 columns
+    run_case(2, 24, 21, 22, 36, 5, 5, 1, 1, 2, 2, 2, False)   # grouped, 5x5 taps
+    run_case(2, 3, 45, 47, 40, 11, 11, 4, 4, 0, 0, 1, True)   # stride 4, 48 phase rows

@@ -31,11 +31,16 @@
  *
  * Types.  `desc->dtype` selects the operand type of `bottom` and `weight`:
  * CAFFE_F32 (float) or CAFFE_BF16 (bfloat16 stored as uint16_t; the caller
- * rounds to nearest-even).  Everything else (bias, top, top_diff, every
- * gradient) is float in both modes, and every product is accumulated in
- * float.  In CAFFE_BF16 mode `top_diff` (after the ReLU mask) is rounded to
- * bfloat16 (nearest-even) before it enters a product; bias_diff sums the
- * unrounded float values.
+ * rounds to nearest-even).  CAFFE_BF16_F32_BOTTOM is CAFFE_BF16 with a float
+ * `bottom` that the library rounds to bfloat16 (nearest-even) as it copies it
+ * into its workspace, so the products, results and gradients are those of
+ * CAFFE_BF16 on the rounded bottom (CAFFE_BACKWARD_MASK_BOTTOM_DIFF keeps
+ * the gradient where the rounded value is > 0): it saves the caller a
+ * separate rounding pass over the layer's input.  Everything else (bias, top,
+ * top_diff, every gradient) is float in all modes, and every product is
+ * accumulated in float.  In both bf16 modes `top_diff` (after the ReLU mask)
+ * is rounded to bfloat16 (nearest-even) before it enters a product;
+ * bias_diff sums the unrounded float values.
  *
  * Memory and ownership.  Every tensor pointer is a device pointer (HIP
  * device memory of the current device), allocated and owned by the caller,
@@ -88,7 +93,11 @@ typedef enum caffe_status {
     CAFFE_ERR_HIP = -5          /* the HIP runtime refused a launch                  */
 } caffe_status;
 
-typedef enum caffe_dtype { CAFFE_F32 = 0, CAFFE_BF16 = 1 } caffe_dtype;
+typedef enum caffe_dtype {
+    CAFFE_F32 = 0,
+    CAFFE_BF16 = 1,
+    CAFFE_BF16_F32_BOTTOM = 2 /* bf16 weight, float bottom rounded by the library */
+} caffe_dtype;
 
 /* Layer geometry: the parameters Caffe's convolution layer is defined by. */
 typedef struct caffe_conv_desc {

@@ -117,7 +117,7 @@ int caffe_lrn_pool_backward(const caffe_pool_desc* pool, const caffe_lrn_desc* l
  * CAFFE_BACKWARD_TOP_DIFF_MASKED), otherwise `top` is read for the mask when
  * desc->relu.  Workspace: caffe_conv_workspace_size with
  * CAFFE_PASS_BACKWARD_POOL_LRN.
- * In CAFFE_BF16 mode with K / group a multiple of 16, the glue's backward
+ * In the bf16 modes with K / group a multiple of 16, the glue's backward
  * writes the bfloat16 staging of the top gradient (and the bias-gradient
  * partials of its float values) directly: one pass instead of writing the
  * float gradient and reading it back.  Otherwise the float gradient goes to

@@ -16,7 +16,7 @@ import torch
 from . import _lib
 from ._lib import (  # noqa: F401
     CAFFE_ERR_UNSUPPORTED, CAFFE_ERR_WORKSPACE, NOALLOC_SCRATCH_BYTES, BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF,
-    BACKWARD_TOP_DIFF_MASKED, CAFFE_BF16, CAFFE_F32, CAFFE_LR_EXP,
+    BACKWARD_TOP_DIFF_MASKED, CAFFE_BF16, CAFFE_BF16_F32_BOTTOM, CAFFE_F32, CAFFE_LR_EXP,
     CAFFE_LR_FIXED, CAFFE_LR_INV, CAFFE_LR_STEP, LrSchedule, PASS_BACKWARD,
     PASS_BACKWARD_DATA, PASS_BACKWARD_POOL_LRN, PASS_BACKWARD_WEIGHTS, PASS_FORWARD,
     POOL_RELU_INPUT, CaffeError, ConvDesc,
@@ -96,13 +96,19 @@ class Workspace:
 
 
 def _op_dtype(desc):
+    """dtype of the weight (and of the bottom, see _bottom_dtype)."""
+    return torch.bfloat16 if desc.dtype in (CAFFE_BF16, CAFFE_BF16_F32_BOTTOM) else torch.float32
+
+
+def _bottom_dtype(desc):
     return torch.bfloat16 if desc.dtype == CAFFE_BF16 else torch.float32
 
 
 # ----------------------------------------------------- C-ABI-shaped calls
 def caffe_conv_forward(desc, bottom, weight, bias, top, workspace=None, stream=None):
     t = _op_dtype(desc)
-    _dev(bottom, "bottom", t), _dev(weight, "weight", t), _dev(bias, "bias", torch.float32)
+    _dev(bottom, "bottom", _bottom_dtype(desc)), _dev(weight, "weight", t)
+    _dev(bias, "bias", torch.float32)
     _dev(top, "top", torch.float32)
     ws_bytes = 0 if workspace is None else workspace.numel()
     check(load().caffe_conv_forward(ctypes.byref(desc), _ptr(bottom), _ptr(weight), _ptr(bias),
@@ -115,7 +121,7 @@ def caffe_conv_backward(desc, top_diff, top, bottom, weight, bottom_diff, weight
     for x, n in ((top_diff, "top_diff"), (top, "top"), (bottom_diff, "bottom_diff"),
                  (weight_diff, "weight_diff"), (bias_diff, "bias_diff")):
         _dev(x, n, torch.float32)
-    _dev(bottom, "bottom", t), _dev(weight, "weight", t)
+    _dev(bottom, "bottom", _bottom_dtype(desc)), _dev(weight, "weight", t)
     ws_bytes = 0 if workspace is None else workspace.numel()
     check(load().caffe_conv_backward(ctypes.byref(desc), _ptr(top_diff), _ptr(top), _ptr(bottom),
                                      _ptr(weight), _ptr(bottom_diff), _ptr(weight_diff),
@@ -135,7 +141,7 @@ def caffe_conv_backward_data(desc, top_diff, top, weight, bottom_diff, workspace
 def caffe_conv_backward_weights(desc, top_diff, top, bottom, weight_diff, bias_diff, accumulate=0,
                                 workspace=None, stream=None):
     _dev(top_diff, "top_diff", torch.float32), _dev(top, "top", torch.float32)
-    _dev(bottom, "bottom", _op_dtype(desc)), _dev(weight_diff, "weight_diff", torch.float32)
+    _dev(bottom, "bottom", _bottom_dtype(desc)), _dev(weight_diff, "weight_diff", torch.float32)
     _dev(bias_diff, "bias_diff", torch.float32)
     ws_bytes = 0 if workspace is None else workspace.numel()
     check(load().caffe_conv_backward_weights(ctypes.byref(desc), _ptr(top_diff), _ptr(top),
@@ -145,8 +151,16 @@ def caffe_conv_backward_weights(desc, top_diff, top, bottom, weight_diff, bias_d
 
 
 # ------------------------------------------------------ allocating helpers
+def _dtype_of(x, w):
+    """The descriptor dtype for a bottom x and weight w: bf16 weights with a
+    float bottom take CAFFE_BF16_F32_BOTTOM (the library rounds the bottom)."""
+    if w.dtype == torch.bfloat16:
+        return CAFFE_BF16 if x.dtype == torch.bfloat16 else CAFFE_BF16_F32_BOTTOM
+    return CAFFE_F32
+
+
 def conv_forward(x, w, b=None, stride=1, pad=0, group=1, relu=False, out=None, ws=None):
-    dtype = CAFFE_BF16 if x.dtype == torch.bfloat16 else CAFFE_F32
+    dtype = _dtype_of(x, w)
     d = conv_desc(x.shape, w.shape, stride, pad, group, relu, dtype)
     Ho, Wo = conv_out_shape(d)
     if out is None:
@@ -160,7 +174,7 @@ def conv_forward(x, w, b=None, stride=1, pad=0, group=1, relu=False, out=None, w
 def conv_backward(x, w, top_diff, top=None, stride=1, pad=0, group=1, relu=False,
                   need=("dx", "dw", "db"), accumulate=0, outs=None, ws=None, flags=0):
     """Returns (dx, dw, db), None where not requested."""
-    dtype = CAFFE_BF16 if x.dtype == torch.bfloat16 else CAFFE_F32
+    dtype = _dtype_of(x, w)
     d = conv_desc(x.shape, w.shape, stride, pad, group, relu, dtype)
     dev = top_diff.device
     if outs is None:
@@ -326,7 +340,7 @@ def caffe_conv_backward_pool_lrn(desc, pool, lrn, pooled, lrn_top, lrn_top_diff,
                  (bias_diff, "bias_diff")):
         _dev(x, n, torch.float32)
     _dev(pool_mask, "pool_mask", torch.int32)
-    _dev(bottom, "bottom", t), _dev(weight, "weight", t)
+    _dev(bottom, "bottom", _bottom_dtype(desc)), _dev(weight, "weight", t)
     ws_bytes = 0 if workspace is None else workspace.numel()
     check(load().caffe_conv_backward_pool_lrn(
         ctypes.byref(desc), ctypes.byref(pool), ctypes.byref(lrn), _ptr(pooled), _ptr(lrn_top),

@@ -19,6 +19,7 @@ CAFFE_ERR_HIP = -5
 
 CAFFE_F32 = 0
 CAFFE_BF16 = 1
+CAFFE_BF16_F32_BOTTOM = 2
 
 BACKWARD_TOP_DIFF_MASKED = 1
 BACKWARD_MASK_BOTTOM_DIFF = 2

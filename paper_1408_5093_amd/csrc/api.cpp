@@ -101,6 +101,11 @@ struct ConvPlan {
     size_t fc_off_d, fc_off_dt, fc_off_pb;   // backward: [D][D^T][partials]
 };
 
+// bf16 products (CAFFE_BF16 and CAFFE_BF16_F32_BOTTOM), and a float bottom
+// (CAFFE_F32, and CAFFE_BF16_F32_BOTTOM, which rounds it while staging)
+bool is_bf16(const ConvPlan& q) { return q.dtype != CAFFE_F32; }
+bool bottom_f32(const ConvPlan& q) { return q.dtype != CAFFE_BF16; }
+
 // Split-K plan of a dense GEMM with M rows, ncol columns and a reduction of R
 // on `cus` compute units.  Workgroups are dealt evenly to the units and a
 // unit works through its share at its MFMA rate, so the GEMM takes about
@@ -383,7 +388,7 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
         return fail(CAFFE_ERR_UNSUPPORTED, "group must be <= 65535");
     if (d->relu != 0 && d->relu != 1)
         return fail(CAFFE_ERR_INVALID_ARG, "relu must be 0 or 1");
-    if (d->dtype != CAFFE_F32 && d->dtype != CAFFE_BF16)
+    if (d->dtype != CAFFE_F32 && d->dtype != CAFFE_BF16 && d->dtype != CAFFE_BF16_F32_BOTTOM)
         return fail(CAFFE_ERR_UNSUPPORTED, "unknown dtype %d", d->dtype);
     if (d->H + 2 * (int64_t)d->pad_h < d->kernel_h || d->W + 2 * (int64_t)d->pad_w < d->kernel_w)
         return fail(CAFFE_ERR_INVALID_ARG, "kernel larger than the padded input");
@@ -402,7 +407,7 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     q.Wo = (q.W + 2 * q.pw - q.kw) / q.sw + 1;
     q.Cg = q.C / q.G;
     q.Kg = q.K / q.G;
-    q.esize = q.dtype == CAFFE_BF16 ? 2 : 4;
+    q.esize = is_bf16(q) ? 2 : 4;
 
     const int64_t R = (int64_t)q.Cg * q.kh * q.kw;
     q.bottom_elems = (int64_t)q.N * q.C * q.H * q.W;
@@ -484,7 +489,7 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     q.fwd_splits = q.dgrad_splits = 1;
     q.fwd_sps = q.dgrad_sps = 0;
     q.off_fwd_part = 0;
-    if (q.dtype == CAFFE_BF16)
+    if (is_bf16(q))
         return plan_bf16(&q);
 
     q.dense = q.H == 1 && q.W == 1 && q.kh == 1 && q.kw == 1 && q.ph == 0 && q.pw == 0 &&
@@ -881,7 +886,7 @@ int run_forward_bf16(const ConvPlan& q, const void* bottom, const void* weight, 
     uint16_t* xh = (uint16_t*)(ws + q.off_xh_fwd);
     uint16_t* wp = (uint16_t*)(ws + q.off_wp_fwd);
     const int Ctot = q.G * q.Cgp;
-    LAUNCH(launch_stage_nhwc_bf16((const uint16_t*)bottom, xh, q.N, q.C, q.H, q.W, q.Cg, q.Cgp,
+    LAUNCH(launch_stage_nhwc_bf16(bottom, bottom_f32(q), xh, q.N, q.C, q.H, q.W, q.Cg, q.Cgp,
                                   Ctot, q.XHp, q.XWp, q.ph, q.pw, s),
            "bf16 staging launch");
     LAUNCH(launch_pack_weights_bf16((const uint16_t*)weight, wp, q.K, q.Cg, q.Cgp, q.kh, q.kw,
@@ -928,7 +933,8 @@ int run_data_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom_mask
     GemmBf16Params p = {};
     p.A = wt;
     p.X = dh;
-    p.Omask = (const uint16_t*)bottom_mask;
+    p.Omask = bottom_mask;
+    p.omask_f32 = bottom_f32(q);
     p.Y = bottom_diff;
     p.A_bytes = nbytes((int64_t)q.G * q.Mt * q.Rtp, 2);
     p.X_bytes = nbytes((int64_t)q.N * q.DHp * q.DWp * Ktot, 2);
@@ -958,7 +964,7 @@ int run_weights_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom, 
     float* part = (float*)(ws + q.off_part);
     const int Ctot = q.G * q.Cgp;
     if (!staged)
-        LAUNCH(launch_stage_nhwc_bf16((const uint16_t*)bottom, xh, q.N, q.C, q.H, q.W, q.Cg,
+        LAUNCH(launch_stage_nhwc_bf16(bottom, bottom_f32(q), xh, q.N, q.C, q.H, q.W, q.Cg,
                                       q.Cgp, Ctot, q.XHp, q.XWp, q.ph, q.pw, s),
                "bf16 staging launch");
     WgradBf16Params p = {};
@@ -1119,7 +1125,7 @@ int backward_bf16_staged(const ConvPlan& q, const float* sums, int terms, bool m
 // glue backward when a 16-channel block lies in one group; its bias partials
 // (at most one per image, row strip and channel) go after the backward's
 // workspace.  Otherwise the fp32 top gradient goes there.
-bool pool_lrn_staged(const ConvPlan& q) { return q.dtype == CAFFE_BF16 && q.Kg % 16 == 0; }
+bool pool_lrn_staged(const ConvPlan& q) { return is_bf16(q) && q.Kg % 16 == 0; }
 
 size_t pool_lrn_extra(const ConvPlan& q)
 {
@@ -1187,7 +1193,7 @@ int caffe_conv_forward(const caffe_conv_desc* desc, const void* bottom, const vo
     CHECK(check_conv_ptrs(q, bias, false, false, "bias"));
     CHECK(check_conv_ptrs(q, top, true, true, "top"));
     CHECK(check_ws(workspace, ws_bytes, q.ws_fwd));
-    if (q.dtype == CAFFE_BF16)
+    if (is_bf16(q))
         return run_forward_bf16(q, bottom, weight, bias, top, (char*)workspace,
                                 (hipStream_t)stream);
     if (q.dense)
@@ -1248,7 +1254,7 @@ int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, cons
     CHECK(check_ws(workspace, ws_bytes, need));
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    if (q.dtype == CAFFE_BF16)
+    if (is_bf16(q))
         return backward_bf16(q, top_diff, top, masked, mask_bottom, staged, bottom, weight,
                              bottom_diff, weight_diff, bias_diff, accumulate, ws, s);
     if (q.dense)

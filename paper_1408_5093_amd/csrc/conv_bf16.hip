@@ -122,7 +122,7 @@ constexpr int bf16_gemm_blocks_per_cu(int tm, int tn, int ns)
     return (160 * 1024) / ((tm + tn) * kBf16TK * 2 * ns);
 }
 
-template <int MT, int WM, int WN, int MI, int NI, int NS, int EPI, bool MASK>
+template <int MT, int WM, int WN, int MI, int NI, int NS, int EPI, int MASK>
 __global__ void __launch_bounds__(64 * WM * WN,
                                   bf16_gemm_blocks_per_cu(WM * MI * MT, WN * NI * MT, NS))
 conv_gemm_bf16_kernel(const GemmBf16Params p)
@@ -370,7 +370,10 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
     } else {
         const int pss = p.psh * p.psw;
         const int OutHW = p.OutH * p.OutW;
-        const __amdgpu_buffer_rsrc_t rom = make_rsrc(p.Omask, MASK ? p.Y_bytes / 2 : 0u);
+        // the bottom mask (MASK 1: bf16 values, MASK 2: float values taken
+        // as the bf16 they round to)
+        const __amdgpu_buffer_rsrc_t rom =
+            make_rsrc(p.Omask, MASK == 1 ? p.Y_bytes / 2 : (MASK == 2 ? p.Y_bytes : 0u));
         int cb[NI], hb[NI], wb[NI];
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni) {
@@ -413,8 +416,10 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
                     off[q][ni] = idx | bad;
                     // backward of the ReLU whose (bf16) output is this
                     // layer's bottom: keep the gradient where it was > 0
-                    if constexpr (MASK)
+                    if constexpr (MASK == 1)
                         y[q][ni] = bf16_to_f32(buf_ld_u16(rom, (idx * 2u) | bad));
+                    else if constexpr (MASK == 2)
+                        y[q][ni] = buf_ld_f32(rom, (idx * 4u) | bad);
                 }
             }
 #pragma unroll
@@ -422,8 +427,12 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
 #pragma unroll
                 for (int ni = 0; ni < NI; ++ni) {
                     float v = acc[mi][ni][q];
-                    if constexpr (MASK)
+                    // (a float rounds to a positive bf16 exactly when it is
+                    // above 2^-134, the tie that rounds to even 0; NaN never)
+                    if constexpr (MASK == 1)
                         v = y[q][ni] > 0.f ? v : 0.f;
+                    else if constexpr (MASK == 2)
+                        v = y[q][ni] > 0x1p-134f ? v : 0.f;
                     const uint32_t o = off[q][ni];
                     buf_st_f32(v, ry, ((o & ~kOob) * 4u) | (o & kOob));
                 }
@@ -741,9 +750,13 @@ constexpr int stage_tile_pixels()
     return 4096 / CT < 256 ? 4096 / CT : 256;
 }
 
-template <int CT>
+// A staged value: bf16 as given, or a float rounded to nearest-even.
+__device__ __forceinline__ bf16_t to_bf16(bf16_t v) { return v; }
+__device__ __forceinline__ bf16_t to_bf16(float v) { return f32_to_bf16_rne(v); }
+
+template <int CT, typename T>
 __global__ void __launch_bounds__(256)
-stage_nhwc_bf16_kernel(const bf16_t* __restrict__ X, bf16_t* __restrict__ Xp, int C, int H, int W,
+stage_nhwc_bf16_kernel(const T* __restrict__ X, bf16_t* __restrict__ Xp, int C, int H, int W,
                        int Cg, int Cgp, int Ctot, int Hp, int Wp, int tb, int lb, int ptiles,
                        int ctiles)
 {
@@ -777,7 +790,8 @@ stage_nhwc_bf16_kernel(const bf16_t* __restrict__ X, bf16_t* __restrict__ Xp, in
         const int cp = c0 + c;
         const int g = cp / Cgp;
         const int cl = cp - g * Cgp;
-        v[q] = inside && cp < Ctot && cl < Cg ? X[src + (size_t)(g * Cg + cl) * H * W] : 0;
+        v[q] = inside && cp < Ctot && cl < Cg ? to_bf16(X[src + (size_t)(g * Cg + cl) * H * W])
+                                              : (bf16_t)0;
     }
 #pragma unroll
     for (int q = 0; q < NQ; ++q)
@@ -805,9 +819,9 @@ stage_nhwc_bf16_kernel(const bf16_t* __restrict__ X, bf16_t* __restrict__ Xp, in
 // 2 or 4 channels (c < Cg real, the rest 0): thread q writes the 16-byte
 // chunk of padded pixels TPC*q .. TPC*q + TPC - 1 (TPC = 8 / Cgp; Hp*Wp is a
 // multiple of TPC), its lanes reading consecutive pixel groups of each plane.
-template <int CGP>
+template <int CGP, typename T>
 __global__ void __launch_bounds__(256)
-stage_narrow_bf16_kernel(const bf16_t* __restrict__ X, bf16_t* __restrict__ Xp, int N, int Cg,
+stage_narrow_bf16_kernel(const T* __restrict__ X, bf16_t* __restrict__ Xp, int N, int Cg,
                          int H, int W, int Hp, int Wp, int tb, int lb)
 {
     constexpr int TPC = 8 / CGP;
@@ -830,7 +844,7 @@ stage_narrow_bf16_kernel(const bf16_t* __restrict__ X, bf16_t* __restrict__ Xp, 
             for (int c = 0; c < CGP; ++c) {
                 bf16_t v = 0;
                 if (inside && c < Cg)
-                    v = X[(((size_t)n * Cg + c) * H + h) * W + x];
+                    v = to_bf16(X[(((size_t)n * Cg + c) * H + h) * W + x]);
                 const int e = t * CGP + c;  // element of the chunk
                 w[e >> 1] |= (uint32_t)v << (16 * (e & 1));
             }
@@ -1035,7 +1049,7 @@ unsigned grid_1d(long total)
     return (unsigned)(blocks > 4096 ? 4096 : (blocks < 1 ? 1 : blocks));
 }
 
-template <int MT, int WM, int WN, int MI, int NI, int NS, int EPI, bool MASK>
+template <int MT, int WM, int WN, int MI, int NI, int NS, int EPI, int MASK>
 hipError_t launch_gemm(const GemmBf16Params& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * MT, TN = WN * NI * MT;
@@ -1046,7 +1060,7 @@ hipError_t launch_gemm(const GemmBf16Params& p, hipStream_t s)
     return hipGetLastError();
 }
 
-template <int NS, int EPI, bool MASK>
+template <int NS, int EPI, int MASK>
 hipError_t launch_gemm_tile(const GemmBf16Params& p, int tile, hipStream_t s)
 {
     switch (tile) {
@@ -1063,7 +1077,7 @@ hipError_t launch_gemm_tile(const GemmBf16Params& p, int tile, hipStream_t s)
     }
 }
 
-template <int EPI, bool MASK>
+template <int EPI, int MASK>
 hipError_t launch_gemm_pipe(const GemmBf16Params& p, int tile, int pipe, hipStream_t s)
 {
     switch (pipe) {
@@ -1116,9 +1130,11 @@ hipError_t launch_conv_gemm_bf16(const GemmBf16Params& p, int epi, int tile, int
         p.KC != p.kh * p.kw * p.Cg8)
         return hipErrorInvalidValue;
     if (epi == 0)
-        return launch_gemm_pipe<0, false>(p, tile, pipe, s);
-    return p.Omask ? launch_gemm_pipe<1, true>(p, tile, pipe, s)
-                   : launch_gemm_pipe<1, false>(p, tile, pipe, s);
+        return launch_gemm_pipe<0, 0>(p, tile, pipe, s);
+    if (!p.Omask)
+        return launch_gemm_pipe<1, 0>(p, tile, pipe, s);
+    return p.omask_f32 ? launch_gemm_pipe<1, 2>(p, tile, pipe, s)
+                       : launch_gemm_pipe<1, 1>(p, tile, pipe, s);
 }
 
 int bf16_wgrad_tile_m(int tile) { return tile == BWTILE_96x256 ? 96 : 128; }
@@ -1151,24 +1167,22 @@ hipError_t launch_wgrad_reduce_perm(const float* P, float* dW, int K, int Rw, in
     return hipGetLastError();
 }
 
-hipError_t launch_stage_nhwc_bf16(const uint16_t* X, uint16_t* Xp, int N, int C, int H, int W,
-                                  int Cg, int Cgp, int Ctot, int Hp, int Wp, int tb, int lb,
-                                  hipStream_t s)
+template <typename T>
+hipError_t launch_stage(const T* X, uint16_t* Xp, int N, int C, int H, int W, int Cg, int Cgp,
+                        int Ctot, int Hp, int Wp, int tb, int lb, hipStream_t s)
 {
-    if (N == 0)
-        return hipSuccess;
     if (Ctot < 8) {  // one group of 1, 2 or 4 channels
         const long chunks = (long)N * Hp * Wp * Ctot / 8;
         const dim3 grid(grid_1d(chunks));
         if (Ctot == 4)
-            hipLaunchKernelGGL(stage_narrow_bf16_kernel<4>, grid, dim3(256), 0, s, X, Xp, N, Cg, H,
-                               W, Hp, Wp, tb, lb);
+            hipLaunchKernelGGL((stage_narrow_bf16_kernel<4, T>), grid, dim3(256), 0, s, X, Xp, N,
+                               Cg, H, W, Hp, Wp, tb, lb);
         else if (Ctot == 2)
-            hipLaunchKernelGGL(stage_narrow_bf16_kernel<2>, grid, dim3(256), 0, s, X, Xp, N, Cg, H,
-                               W, Hp, Wp, tb, lb);
+            hipLaunchKernelGGL((stage_narrow_bf16_kernel<2, T>), grid, dim3(256), 0, s, X, Xp, N,
+                               Cg, H, W, Hp, Wp, tb, lb);
         else
-            hipLaunchKernelGGL(stage_narrow_bf16_kernel<1>, grid, dim3(256), 0, s, X, Xp, N, Cg, H,
-                               W, Hp, Wp, tb, lb);
+            hipLaunchKernelGGL((stage_narrow_bf16_kernel<1, T>), grid, dim3(256), 0, s, X, Xp, N,
+                               Cg, H, W, Hp, Wp, tb, lb);
         return hipGetLastError();
     }
     const int ct = Ctot <= 8 ? 8 : Ctot <= 16 ? 16 : Ctot <= 32 ? 32 : 64;
@@ -1178,8 +1192,8 @@ hipError_t launch_stage_nhwc_bf16(const uint16_t* X, uint16_t* Xp, int N, int C,
     const int ctiles = (Ctot + ct - 1) / ct;
     const dim3 grid((unsigned)((int64_t)ptiles * ctiles * N));
 #define CAFFE_STAGE_LAUNCH(CT)                                                                    \
-    hipLaunchKernelGGL(stage_nhwc_bf16_kernel<CT>, grid, dim3(256), 0, s, X, Xp, C, H, W, Cg, Cgp, \
-                       Ctot, Hp, Wp, tb, lb, ptiles, ctiles)
+    hipLaunchKernelGGL((stage_nhwc_bf16_kernel<CT, T>), grid, dim3(256), 0, s, X, Xp, C, H, W, Cg, \
+                       Cgp, Ctot, Hp, Wp, tb, lb, ptiles, ctiles)
     switch (ct) {
     case 8:
         CAFFE_STAGE_LAUNCH(8);
@@ -1196,6 +1210,17 @@ hipError_t launch_stage_nhwc_bf16(const uint16_t* X, uint16_t* Xp, int N, int C,
     }
 #undef CAFFE_STAGE_LAUNCH
     return hipGetLastError();
+}
+
+hipError_t launch_stage_nhwc_bf16(const void* X, int x_f32, uint16_t* Xp, int N, int C, int H,
+                                  int W, int Cg, int Cgp, int Ctot, int Hp, int Wp, int tb, int lb,
+                                  hipStream_t s)
+{
+    if (N == 0)
+        return hipSuccess;
+    if (x_f32)
+        return launch_stage((const float*)X, Xp, N, C, H, W, Cg, Cgp, Ctot, Hp, Wp, tb, lb, s);
+    return launch_stage((const uint16_t*)X, Xp, N, C, H, W, Cg, Cgp, Ctot, Hp, Wp, tb, lb, s);
 }
 
 int diff_prep_terms(int N, int HWp)

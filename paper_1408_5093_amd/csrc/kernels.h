@@ -227,11 +227,13 @@ enum Bf16Pipe {
 // for col = (n, i, j) in N x OH x OW: the borders of X stand for the
 // convolution's zero padding, so every gathered position lies inside it.
 // Epilogues as ConvGemmParams (epi 0 forward, epi 1 phase-stacked data
-// gradient); Omask (epi 1, may be null) is a bf16 tensor laid out like Y.
+// gradient); Omask (epi 1, may be null) is a tensor laid out like Y of bf16
+// values, or of floats (omask_f32) that count as the bf16 they round to.
 struct GemmBf16Params {
     const uint16_t* A;
     const uint16_t* X;
-    const uint16_t* Omask;
+    const void* Omask;
+    int omask_f32;
     float* Y;
     const float* bias;
     uint32_t A_bytes, X_bytes, Y_bytes;
@@ -293,9 +295,10 @@ hipError_t launch_wgrad_reduce_perm(const float* P, float* dW, int K, int Rw, in
 // Xp[n][hp][wp][g*Cgp + c] = X[n][g*Cg + c][hp - tb][wp - lb] inside the H x W
 // image (c < Cg), else 0: the zero-bordered channel-contiguous copy, Hp x Wp
 // pixels per image; Ctot = G*Cgp, a multiple of 8, or Cgp in {1, 2, 4} with
-// G = 1 and Hp*Wp a multiple of 8 / Cgp.
-hipError_t launch_stage_nhwc_bf16(const uint16_t* X, uint16_t* Xp, int N, int C, int H, int W,
-                                  int Cg, int Cgp, int Ctot, int Hp, int Wp, int tb, int lb,
+// G = 1 and Hp*Wp a multiple of 8 / Cgp.  X holds bf16 values, or floats
+// (x_f32) that are rounded to bf16 (nearest-even) on the way.
+hipError_t launch_stage_nhwc_bf16(const void* X, int x_f32, uint16_t* Xp, int N, int C, int H,
+                                  int W, int Cg, int Cgp, int Ctot, int Hp, int Wp, int tb, int lb,
                                   hipStream_t s);
 
 // Dh[n][hp][wp][g*Kgp + k] = bf16(relu ? G [Y > 0] : G)[n][g*Kg + k][hp - tb][wp - lb]

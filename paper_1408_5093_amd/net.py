@@ -14,10 +14,10 @@ call; this module only owns buffers and the call order.
 import torch
 
 from . import (BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED,
-               CAFFE_BF16, CAFFE_F32,
+               CAFFE_BF16_F32_BOTTOM, CAFFE_F32,
                PASS_BACKWARD, PASS_BACKWARD_POOL_LRN, PASS_BACKWARD_WEIGHTS, PASS_FORWARD,
                POOL_RELU_INPUT, Workspace, caffe_conv_backward, caffe_conv_backward_pool_lrn,
-               caffe_conv_forward, cast_f32_to_bf16, conv_desc, conv_out_shape, lrn_desc,
+               caffe_conv_forward, conv_desc, conv_out_shape, lrn_desc,
                conv_workspace_size, lrn_backward, lrn_forward, maxpool_backward, maxpool_forward,
                lrn_pool_backward, pool_desc, pool_lrn_forward, pool_lrn_supported, relu_backward,
                pool_out_shape, sgd_learning_rate, sgd_update, softmax_loss)
@@ -26,7 +26,9 @@ from . import (BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_D
 class ConvStack:
     """layers: sequence of workloads.ConvLayer.  glue: {l: [("pool", {...}) | ("lrn", {...})]}
     applied in order to the output of layer l.  bf16=True runs the convolutions on
-    bfloat16 operands (fp32 accumulation and outputs); glue stays fp32."""
+    bfloat16 operands (fp32 accumulation and outputs): bf16 weights, and each
+    layer's float input rounded by the library as it stages it
+    (CAFFE_BF16_F32_BOTTOM); glue stays fp32."""
 
     def __init__(self, layers, N, weights, biases, glue=None, bf16=False, device="cuda",
                  fuse_glue=True, split_backward=True, fuse_staging=True):
@@ -35,10 +37,10 @@ class ConvStack:
         self.bf16 = bf16
         self.glue = glue or {}
         dev = torch.device(device)
-        dt = CAFFE_BF16 if bf16 else CAFFE_F32
+        dt = CAFFE_BF16_F32_BOTTOM if bf16 else CAFFE_F32
         op = torch.bfloat16 if bf16 else torch.float32
         self.descs, self.W, self.b, self.dW, self.db = [], [], [], [], []
-        self.top, self.dtop_glue, self.dbottom, self.bottom_op = [], [], [], []
+        self.top, self.dtop_glue, self.dbottom = [], [], []
         self.stages = []  # per layer: list of glue stage dicts
         # shape of layer l's output after its glue; an inner-product layer (a
         # 1x1 image) takes it flattened, channels (c, h, w) -- a view
@@ -58,8 +60,6 @@ class ConvStack:
             self.db.append(torch.empty(L.K, dtype=torch.float32, device=dev))
             self.top.append(torch.empty((N, L.K, Ho, Wo), dtype=torch.float32, device=dev))
             self.dbottom.append(torch.empty((N, L.C, L.H, L.W), dtype=torch.float32, device=dev))
-            self.bottom_op.append(torch.empty((N, L.C, L.H, L.W), dtype=op, device=dev)
-                                  if bf16 else None)
             need_l = max(conv_workspace_size(d, PASS_BACKWARD), conv_workspace_size(d, PASS_FORWARD))
             glue_l = [kind for kind, _ in self.glue.get(l, [])]
             if bf16 and fuse_staging and glue_l == ["pool", "lrn"]:
@@ -183,11 +183,8 @@ class ConvStack:
             L = self.layers[l]
             cur = cur.view(self.N, L.C, L.H, L.W)
             self.bottom[l] = cur
-            src = cur
-            if self.bf16:
-                src = cast_f32_to_bf16(cur, out=self.bottom_op[l], stream=s)
             self._mark(("fwd", l, "begin"), s)
-            caffe_conv_forward(self.descs[l], src, self.W[l], self.b[l], self.top[l], self.ws_of[l],
+            caffe_conv_forward(self.descs[l], cur, self.W[l], self.b[l], self.top[l], self.ws_of[l],
                                s)
             self._mark(("fwd", l, "end"), s)
             cur = self.top[l]
@@ -243,7 +240,7 @@ class ConvStack:
                     g = lrn_backward(st["x"], st["y"], g, p["size"], p["alpha"], p["beta"],
                                      p["k"], out=st["dx"], stream=s)
             want_dx = l > 0 or data_grad_bottom
-            bottom = self.bottom_op[l] if self.bf16 else self.bottom[l]
+            bottom = self.bottom[l]
             flags = 0
             if self.top_masked[l]:
                 flags |= BACKWARD_TOP_DIFF_MASKED
@@ -301,7 +298,7 @@ class ConvStack:
         self._mark(("both" if want_dx else "wgt", l, "begin"), s)
         caffe_conv_backward_pool_lrn(self.descs[l], pst["pool_desc"], lst["lrn_desc"], pst["y"],
                                      lst["y"], g, pst["mask"], self.top[l] if L.relu else None,
-                                     self.bottom_op[l], self.W[l],
+                                     self.bottom[l], self.W[l],
                                      self.dbottom[l] if want_dx else None, self.dW[l],
                                      self.db[l], 0, flags, self.ws_of[l], s)
         self._mark(("both" if want_dx else "wgt", l, "end"), s)

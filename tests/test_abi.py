@@ -101,7 +101,7 @@ def _desc(**kw):
 @pytest.mark.parametrize("field,value,code", [
     ("C", 0, -1), ("H", -1, -1), ("K", 0, -1), ("N", -1, -1), ("kernel_h", 0, -1),
     ("stride_w", 0, -1), ("pad_h", -1, -1), ("group", 0, -1), ("group", 3, -1),
-    ("K", 7, -1), ("relu", 2, -1), ("dtype", 7, -4), ("kernel_h", 12, -1),
+    ("K", 7, -1), ("relu", 2, -1), ("dtype", 7, -4), ("dtype", 3, -4), ("kernel_h", 12, -1),
     ("H", 20000, -4), ("pad_w", 17000, -4),
 ])
 def test_invalid_descriptor(field, value, code):
@@ -115,6 +115,17 @@ def test_invalid_descriptor(field, value, code):
     assert lib.caffe_conv_forward(ctypes.byref(d), P(0x1000), P(0x2000), None, P(0x3000), None, 0,
                                   None) == code
     assert lib.caffe_last_error() != b""
+
+
+def test_float_bottom_bf16_dtype_plans_like_bf16():
+    """CAFFE_BF16_F32_BOTTOM takes a float bottom but plans the bf16 path:
+    the same workspace sizes as CAFFE_BF16 for every pass."""
+    for x, w, s, p, g in [((256, 3, 227, 227), (96, 3, 11, 11), 4, 0, 1),
+                          ((8, 96, 27, 27), (256, 48, 5, 5), 1, 2, 2)]:
+        d1 = cc.conv_desc(x, w, s, p, g, True, cc.CAFFE_BF16)
+        d2 = cc.conv_desc(x, w, s, p, g, True, cc.CAFFE_BF16_F32_BOTTOM)
+        for pas in range(5):
+            assert cc.conv_workspace_size(d1, pas) == cc.conv_workspace_size(d2, pas)
 
 
 def test_null_desc_and_outputs():

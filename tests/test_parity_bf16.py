@@ -239,8 +239,7 @@ def test_caffenet_bf16_training_step_full_size():
     images = [0, N - 1]
     for l, L in enumerate(wl.CAFFENET):
         xl = _np(net.bottom[l])          # the fp32 input
-        xr = _np(net.bottom_op[l])       # the bf16 operand the layer multiplied
-        np.testing.assert_array_equal(xr[images], wl.round_bf16(xl[images]))
+        xr = wl.round_bf16(xl)           # the bf16 operand the layer multiplies
         wr = _np(net.W[l])
         gl = _np(net.layer_top_diff(l, g))
         top = _np(net.top[l])
@@ -309,3 +308,52 @@ def test_forced_gemm_tiles_bf16(tile, overrides):
     run_case(3, 16, 14, 15, 200, 3, 3, 1, 1, 1, 1, 1, True)   # 200 rows, 630 columns
     run_case(2, 24, 21, 22, 36, 5, 5, 1, 1, 2, 2, 2, False)   # grouped, 5x5 taps
     run_case(2, 3, 45, 47, 40, 11, 11, 4, 4, 0, 0, 1, True)   # stride 4, 48 phase rows
+
+
+@pytest.mark.parametrize("case", [
+    (2, 3, 45, 47, 40, 11, 11, 4, 4, 0, 0, 1, True),   # 3 channels: narrow staging
+    (2, 16, 14, 15, 64, 3, 3, 1, 1, 1, 1, 2, True),    # grouped, padded
+    (3, 20, 9, 10, 30, 5, 5, 1, 1, 2, 2, 1, False),    # channels not a multiple of 8
+])
+def test_float_bottom_rounded_by_the_library(case):
+    """CAFFE_BF16_F32_BOTTOM: a float bottom that the library rounds while
+    staging gives bitwise what CAFFE_BF16 gives on the bottom rounded by
+    torch (nearest-even): top, and every gradient with the bottom mask and
+    with and without the forward's staged copy.  Some bottom values sit
+    exactly half-way between two bf16 values and some round to +-0, so the
+    rounding and the mask's sign rule are both exercised."""
+    N, C, H, W, K, kh, kw, sh, sw, ph, pw, g, relu = case
+    print(f"float bottom case {case}", flush=True)
+    rng = np.random.default_rng([84, N, C, K, kh])
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    bits = x.view(np.uint32)
+    bits[:, :, 0, :] = (bits[:, :, 0, :] & 0xFFFF0000) | 0x8000   # ties
+    x[:, :, 1, :4] = np.array([1e-39, -1e-39, 2e-45, -2e-45], np.float32)  # to +-0 / denormals
+    w = (rng.standard_normal((K, C // g, kh, kw)) * 0.3).astype(np.float32)
+    b = (rng.standard_normal(K) * 0.5).astype(np.float32)
+    xf = _t(x)
+    xb = xf.to(torch.bfloat16)
+    wb = _t(w, torch.bfloat16)
+    bt = _t(b)
+    outs = []
+    for dt, xin in ((cc.CAFFE_BF16, xb), (cc.CAFFE_BF16_F32_BOTTOM, xf)):
+        d = cc.conv_desc(x.shape, w.shape, (sh, sw), (ph, pw), g, relu, dt)
+        Ho, Wo = cc.conv_out_shape(d)
+        need = max(cc.conv_workspace_size(d, p) for p in range(4))
+        buf = cc.Workspace(DEV).get(need)
+        top = torch.empty((N, K, Ho, Wo), device=DEV)
+        cc.caffe_conv_forward(d, xin, wb, bt, top, buf)
+        gd = _t(np.random.default_rng(85).standard_normal((N, K, Ho, Wo)))
+        res = [top.clone()]
+        for flags in (cc.BACKWARD_MASK_BOTTOM_DIFF,
+                      cc.BACKWARD_MASK_BOTTOM_DIFF | cc.BACKWARD_BOTTOM_STAGED):
+            dx = torch.empty(x.shape, device=DEV)
+            dw = torch.empty(w.shape, device=DEV)
+            db = torch.empty(K, device=DEV)
+            cc.caffe_conv_backward(d, gd, top if relu else None, xin, wb, dx, dw, db, 0, flags,
+                                   buf)
+            res += [dx, dw, db]
+        torch.cuda.synchronize()
+        outs.append(res)
+    for a, c in zip(*outs):
+        assert torch.equal(a, c)

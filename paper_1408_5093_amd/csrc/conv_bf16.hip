@@ -754,6 +754,94 @@ constexpr int stage_tile_pixels()
 __device__ __forceinline__ bf16_t to_bf16(bf16_t v) { return v; }
 __device__ __forceinline__ bf16_t to_bf16(float v) { return f32_to_bf16_rne(v); }
 
+// Row-chunk staging (groups of a multiple of 8 channels, so that Cgp = Cg and
+// the staged channels are the blob's; rows of at most kStageRowPixels pixels):
+// a block takes image n, channels c0 .. c0 + 63 and padded rows
+// r0 .. r0 + RH - 1.  The real rows among them are one contiguous run of
+// RP = rows * W pixels in every channel plane, so the loads are whole runs,
+// one pixel per thread and channel (no line is shared with another block but
+// at the run's ends); the block transposes them through LDS and writes every
+// padded pixel of its rows, border zeros included, as 16-byte chunks of 8
+// channels.
+constexpr int kStageRowPixels = 256;
+
+template <typename T>
+__device__ __forceinline__ T load_elem(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff);
+template <>
+__device__ __forceinline__ float load_elem<float>(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                                  uint32_t soff)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+template <>
+__device__ __forceinline__ bf16_t load_elem<bf16_t>(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                                    uint32_t soff)
+{
+    return __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
+}
+constexpr int kStageRowCh = 64;
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+stage_rows_bf16_kernel(const T* __restrict__ X, bf16_t* __restrict__ Xp, int C, int H, int W,
+                       int Cg, int Cgp, int Ctot, int Hp, int Wp, int tb, int lb, int RH,
+                       int rchunks, int ctiles)
+{
+    constexpr int CT = kStageRowCh;
+    constexpr int C8 = CT / 8;
+    __shared__ bf16_t tile[CT][kStageRowPixels + 2];
+    // block -> (n, channel tile, row chunk), row chunks fastest
+    const int n = blockIdx.x / (rchunks * ctiles);
+    const int rem = blockIdx.x - n * rchunks * ctiles;
+    const int ct = rem / rchunks;
+    const int r0 = (rem - ct * rchunks) * RH;
+    const int r1 = min(Hp, r0 + RH);
+    const int c0 = ct * CT;
+    const int h0 = max(0, r0 - tb);
+    const int h1 = min(H, r1 - tb);
+    const int RP = h1 > h0 ? (h1 - h0) * W : 0;
+    const int tid = threadIdx.x;
+    if (tid < RP) {
+        // the image's planes through one buffer resource: channel c0 + c is
+        // the scalar offset (c0 + c) * H * W elements, out of range (0) past
+        // the last channel
+        const uint32_t plane = (uint32_t)(H * W) * (uint32_t)sizeof(T);
+        const __amdgpu_buffer_rsrc_t rx =
+            make_rsrc(X + (size_t)n * C * H * W, (uint32_t)C * plane);
+        const uint32_t voff = (uint32_t)(h0 * W + tid) * (uint32_t)sizeof(T);
+        // every load of the thread in flight before the first is used
+        T v[CT];
+#pragma unroll
+        for (int c = 0; c < CT; ++c)
+            v[c] = load_elem<T>(rx, voff, (uint32_t)(c0 + c) * plane);
+#pragma unroll
+        for (int c = 0; c < CT; ++c)
+            tile[c][tid] = to_bf16(v[c]);
+    }
+    __syncthreads();
+    const int npix = (r1 - r0) * Wp;
+    for (int id = tid; id < npix * C8; id += 256) {
+        const int c8 = id % C8;
+        const int pl = id / C8;
+        const int cp = c0 + 8 * c8;
+        if (cp >= Ctot)
+            continue;
+        const int hp = r0 + pl / Wp;
+        const int wp = pl - (pl / Wp) * Wp;
+        const int h = hp - tb;
+        const int w = wp - lb;
+        u32x4 out = {0u, 0u, 0u, 0u};
+        if ((unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W) {
+            const int q = (h - h0) * W + w;
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                out[k] = (uint32_t)tile[8 * c8 + 2 * k][q] |
+                         ((uint32_t)tile[8 * c8 + 2 * k + 1][q] << 16);
+        }
+        *(u32x4*)&Xp[(((size_t)n * Hp + hp) * Wp + wp) * Ctot + cp] = out;
+    }
+}
+
 template <int CT, typename T>
 __global__ void __launch_bounds__(256)
 stage_nhwc_bf16_kernel(const T* __restrict__ X, bf16_t* __restrict__ Xp, int C, int H, int W,
@@ -821,36 +909,43 @@ stage_nhwc_bf16_kernel(const T* __restrict__ X, bf16_t* __restrict__ Xp, int C, 
 // multiple of TPC), its lanes reading consecutive pixel groups of each plane.
 template <int CGP, typename T>
 __global__ void __launch_bounds__(256)
-stage_narrow_bf16_kernel(const T* __restrict__ X, bf16_t* __restrict__ Xp, int N, int Cg,
-                         int H, int W, int Hp, int Wp, int tb, int lb)
+stage_narrow_bf16_kernel(const T* __restrict__ X, bf16_t* __restrict__ Xp, int Cg, int H, int W,
+                         int Hp, int Wp, int tb, int lb, FastDiv div_wp)
 {
     constexpr int TPC = 8 / CGP;
-    const int HWp = Hp * Wp;
-    const int per_image = HWp / TPC;
-    const long total = (long)N * per_image;
-    for (long q = blockIdx.x * (long)blockDim.x + threadIdx.x; q < total;
-         q += (long)gridDim.x * blockDim.x) {
-        const int n = (int)(q / per_image);
-        const int p0 = (int)(q - (long)n * per_image) * TPC;
-        uint32_t w[4] = {0u, 0u, 0u, 0u};
+    // grid: x over the image's chunks, y over the images
+    const int n = blockIdx.y;
+    const int per_image = Hp * Wp / TPC;
+    const int q = blockIdx.x * 256 + threadIdx.x;
+    if (q >= per_image)
+        return;
+    // the image's planes through one buffer resource: channel c is the
+    // scalar offset c * H * W elements, out of range (0) from channel Cg on,
+    // and a pixel outside the image takes the out-of-range lane offset
+    const uint32_t plane = (uint32_t)(H * W) * (uint32_t)sizeof(T);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + (size_t)n * Cg * H * W, (uint32_t)Cg * plane);
+    T v[TPC][CGP];
 #pragma unroll
-        for (int t = 0; t < TPC; ++t) {
-            const int pix = p0 + t;
-            const int hp = pix / Wp;
-            const int h = hp - tb;
-            const int x = pix - hp * Wp - lb;
-            const bool inside = (unsigned)h < (unsigned)H && (unsigned)x < (unsigned)W;
+    for (int t = 0; t < TPC; ++t) {
+        const int pix = q * TPC + t;
+        const int hp = (int)fdiv((uint32_t)pix, div_wp);
+        const int h = hp - tb;
+        const int x = pix - hp * Wp - lb;
+        const bool inside = (unsigned)h < (unsigned)H && (unsigned)x < (unsigned)W;
+        const uint32_t voff = inside ? (uint32_t)(h * W + x) * (uint32_t)sizeof(T) : kOob;
 #pragma unroll
-            for (int c = 0; c < CGP; ++c) {
-                bf16_t v = 0;
-                if (inside && c < Cg)
-                    v = to_bf16(X[(((size_t)n * Cg + c) * H + h) * W + x]);
-                const int e = t * CGP + c;  // element of the chunk
-                w[e >> 1] |= (uint32_t)v << (16 * (e & 1));
-            }
-        }
-        *(u32x4*)&Xp[(size_t)q * 8] = u32x4{w[0], w[1], w[2], w[3]};
+        for (int c = 0; c < CGP; ++c)
+            v[t][c] = load_elem<T>(rx, voff, (uint32_t)c * plane);
     }
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int t = 0; t < TPC; ++t)
+#pragma unroll
+        for (int c = 0; c < CGP; ++c) {
+            const int e = t * CGP + c;  // element of the chunk
+            w[e >> 1] |= (uint32_t)to_bf16(v[t][c]) << (16 * (e & 1));
+        }
+    *(u32x4*)&Xp[((size_t)n * per_image + q) * 8] = u32x4{w[0], w[1], w[2], w[3]};
 }
 
 // Top-gradient staging: Dh = bf16(relu ? G [Y > 0] : G) channel-contiguous on
@@ -1172,17 +1267,39 @@ hipError_t launch_stage(const T* X, uint16_t* Xp, int N, int C, int H, int W, in
                         int Ctot, int Hp, int Wp, int tb, int lb, hipStream_t s)
 {
     if (Ctot < 8) {  // one group of 1, 2 or 4 channels
-        const long chunks = (long)N * Hp * Wp * Ctot / 8;
-        const dim3 grid(grid_1d(chunks));
-        if (Ctot == 4)
-            hipLaunchKernelGGL((stage_narrow_bf16_kernel<4, T>), grid, dim3(256), 0, s, X, Xp, N,
-                               Cg, H, W, Hp, Wp, tb, lb);
-        else if (Ctot == 2)
-            hipLaunchKernelGGL((stage_narrow_bf16_kernel<2, T>), grid, dim3(256), 0, s, X, Xp, N,
-                               Cg, H, W, Hp, Wp, tb, lb);
-        else
-            hipLaunchKernelGGL((stage_narrow_bf16_kernel<1, T>), grid, dim3(256), 0, s, X, Xp, N,
-                               Cg, H, W, Hp, Wp, tb, lb);
+        // (the channel offsets stay below 2^32 bytes, range-checked)
+        if ((int64_t)Ctot * H * W * (int64_t)sizeof(T) >= (int64_t(1) << 32))
+            return hipErrorInvalidValue;
+        const int per_image = Hp * Wp * Ctot / 8;
+        const FastDiv dwp = make_fastdiv((uint32_t)Wp);
+        // (images in launches of at most 65535: the grid's y extent)
+        for (int n0 = 0; n0 < N; n0 += 65535) {
+            const dim3 grid((unsigned)((per_image + 255) / 256), (unsigned)std::min(N - n0, 65535));
+            const T* Xn = X + (size_t)n0 * Cg * H * W;
+            uint16_t* Xpn = Xp + (size_t)n0 * per_image * 8;
+            if (Ctot == 4)
+                hipLaunchKernelGGL((stage_narrow_bf16_kernel<4, T>), grid, dim3(256), 0, s, Xn,
+                                   Xpn, Cg, H, W, Hp, Wp, tb, lb, dwp);
+            else if (Ctot == 2)
+                hipLaunchKernelGGL((stage_narrow_bf16_kernel<2, T>), grid, dim3(256), 0, s, Xn,
+                                   Xpn, Cg, H, W, Hp, Wp, tb, lb, dwp);
+            else
+                hipLaunchKernelGGL((stage_narrow_bf16_kernel<1, T>), grid, dim3(256), 0, s, Xn,
+                                   Xpn, Cg, H, W, Hp, Wp, tb, lb, dwp);
+        }
+        return hipGetLastError();
+    }
+    // (the channel offsets, up to one tile past the last channel, stay below
+    // 2^32 bytes: range-checked, never wrapped)
+    const bool offsets_fit = ((int64_t)C + kStageRowCh) * H * W * (int64_t)sizeof(T) <
+                             (int64_t(1) << 32);
+    if (W <= kStageRowPixels && Ctot >= 32 && Cgp == Cg && offsets_fit) {
+        const int RH = kStageRowPixels / W;
+        const int rchunks = (Hp + RH - 1) / RH;
+        const int ctiles = (Ctot + kStageRowCh - 1) / kStageRowCh;
+        hipLaunchKernelGGL((stage_rows_bf16_kernel<T>),
+                           dim3((unsigned)((int64_t)N * rchunks * ctiles)), dim3(256), 0, s, X, Xp,
+                           C, H, W, Cg, Cgp, Ctot, Hp, Wp, tb, lb, RH, rchunks, ctiles);
         return hipGetLastError();
     }
     const int ct = Ctot <= 8 ? 8 : Ctot <= 16 ? 16 : Ctot <= 32 ? 32 : 64;

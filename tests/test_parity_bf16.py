@@ -357,3 +357,13 @@ def test_float_bottom_rounded_by_the_library(case):
         outs.append(res)
     for a, c in zip(*outs):
         assert torch.equal(a, c)
+
+
+@pytest.mark.parametrize("tile", range(2))
+def test_forced_wgrad_tiles_bf16(tile, overrides):
+    """Every bf16 weight-gradient tile, forced, on channel counts that leave
+    partial row and column tiles (narrow packing included)."""
+    overrides.setenv("CAFFE_BF16_WGRAD_TILE", str(tile))
+    run_case(3, 16, 14, 15, 200, 3, 3, 1, 1, 1, 1, 1, True)   # 200 rows, 144 columns
+    run_case(2, 24, 21, 22, 36, 5, 5, 1, 1, 2, 2, 2, False)   # grouped, 300 columns
+    run_case(2, 3, 45, 47, 40, 11, 11, 4, 4, 0, 0, 1, True)   # narrow: 528 columns

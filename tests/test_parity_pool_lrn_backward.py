@@ -31,6 +31,8 @@ CASES = [
     (2, 8, 15, 15, 32, 3, 1, 1, 1, False, True),   # float operands
     (2, 3, 59, 59, 32, 11, 4, 0, 1, True, True),   # conv1's stride-4 geometry, staged
     (2, 16, 27, 27, 64, 5, 1, 2, 2, True, True),   # conv2's geometry, staged
+    (2, 16, 27, 27, 64, 5, 1, 2, 2, "f32", True),  # the same from a float bottom
+    (2, 8, 13, 17, 64, 3, 1, 1, 2, "f32", False),  # float bottom, ReLU mask from top
 ]
 POOL = dict(kernel=3, stride=2, pad=0)
 LRN = dict(size=5, alpha=1e-4, beta=0.75, k=1.0)
@@ -45,8 +47,12 @@ def test_backward_pool_lrn(case):
     N, C, H, W, K, k, s, p, g, bf16, relu_input = case
     print(f"backward_pool_lrn {case}", flush=True)
     rng = np.random.default_rng([1408, 5093, 90, sum(case[:9])])
+    # bf16 == "f32": bf16 weights and a float bottom the library rounds
+    # (CAFFE_BF16_F32_BOTTOM)
+    f32_bottom = bf16 == "f32"
     op = torch.bfloat16 if bf16 else torch.float32
-    x = torch.from_numpy(rng.standard_normal((N, C, H, W)).astype(np.float32)).to(DEV).to(op)
+    x = torch.from_numpy(rng.standard_normal((N, C, H, W)).astype(np.float32)).to(DEV)
+    x = x if f32_bottom else x.to(op)
     w = torch.from_numpy((rng.standard_normal((K, C // g, k, k)) * 0.2).astype(np.float32))
     w = w.to(DEV).to(op)
     b = torch.from_numpy(rng.standard_normal(K).astype(np.float32) * 0.1).to(DEV)
@@ -55,7 +61,8 @@ def test_backward_pool_lrn(case):
     pooled, mask, lrn_top = cc.pool_lrn_forward(top, flags=flags_pool, **POOL, **LRN)
     gl = torch.from_numpy(rng.standard_normal(lrn_top.shape).astype(np.float32)).to(DEV)
 
-    d = cc.conv_desc(x.shape, w.shape, s, p, g, True, cc.CAFFE_BF16 if bf16 else cc.CAFFE_F32)
+    dt = cc.CAFFE_BF16_F32_BOTTOM if f32_bottom else cc.CAFFE_BF16 if bf16 else cc.CAFFE_F32
+    d = cc.conv_desc(x.shape, w.shape, s, p, g, True, dt)
     pd = cc.pool_desc(top.shape, POOL["kernel"], POOL["stride"], POOL["pad"])
     ld = cc.lrn_desc(pooled.shape, **LRN)
     flags = cc.BACKWARD_TOP_DIFF_MASKED if relu_input else 0
@@ -86,8 +93,9 @@ def test_backward_pool_lrn(case):
     assert_close(gg, gref, TOL_F32, "glue backward vs the oracle")
     # the convolution against the oracle on the operands the GPU multiplied
     gmul = _np(gtop.to(torch.bfloat16)) if bf16 else gg
-    dx_r, dw_r, _ = oracle.conv_backward(_np(x), _np(w), gmul, stride=s, pad=p, group=g)
-    _, _, db_r = oracle.conv_backward(_np(x), _np(w), gg, stride=s, pad=p, group=g, need=("db",))
+    xm = _np(x.to(torch.bfloat16)) if f32_bottom else _np(x)   # the bottom multiplied
+    dx_r, dw_r, _ = oracle.conv_backward(xm, _np(w), gmul, stride=s, pad=p, group=g)
+    _, _, db_r = oracle.conv_backward(xm, _np(w), gg, stride=s, pad=p, group=g, need=("db",))
     assert_close(_np(dx), dx_r, TOL_F32, "data gradient vs the oracle")
     assert_close(_np(dw), dw_r, TOL_F32, "weight gradient vs the oracle")
     assert_close(_np(db), db_r, TOL_F32, "bias gradient vs the oracle")

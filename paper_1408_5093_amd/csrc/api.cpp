@@ -78,6 +78,11 @@ struct ConvPlan {
     // (tpc; kw rounded up to kwp); padded reduction lengths of the forward
     // (Rp) and data-gradient (Rtp) GEMMs; weight-gradient columns Rw
     int Cgp, Kgp, Rp, Rtp, Rw, tpc, kwp;
+    // space-to-depth staging of a strided layer (s2d = its stride S, else 0):
+    // S x S pixel blocks of the input become channels (Cgp from C * S * S),
+    // and the layer a stride-1 one with gkh x kwp kernel taps of the blocks
+    // (gkh = ceil(kh / S), kwp = ceil(kw / S)); without it gkh = kh
+    int s2d, gkh;
     // zero-bordered bf16 staging: the input on an XHp x XWp grid (real pixels
     // at (ph, pw)), the top gradient on a DHp x DWp grid (real pixels at
     // (dtb, dlb)); the data-gradient gather reads the latter from (doh0, dow0)
@@ -292,14 +297,40 @@ int plan_bf16(ConvPlan* p)
             }
     q.tpc = q.Cgp < 8 ? 8 / q.Cgp : 1;
     q.kwp = round_up(q.kw, q.tpc);
+    q.gkh = q.kh;
+    q.s2d = 0;
     q.Kgp = round_up(q.Kg, 8);
-    const int khw = q.kh * q.kwp;
     // The staged copies carry the gathers' zero padding as a border: the
     // input's covers every forward tap, the top gradient's every tap of the
     // phase-stacked data-gradient gather (whose padding Th - 1 - a0h may be
     // negative: then the gather starts doh0 rows into the grid instead).
     q.XHp = std::max(q.ph + q.H, (q.Ho - 1) * q.sh + q.kh);
     q.XWp = round_up(std::max(q.pw + q.W, (q.Wo - 1) * q.sw + q.kwp), q.tpc);
+    // A strided layer with few channels (CaffeNet's conv1: 3 channels,
+    // stride 4) staged space-to-depth when that pads its reduction less:
+    // conv1's 11 x 11 x 3 taps become 3 x 3 taps of 48 channels, 432 staged
+    // reduction elements (448 padded) instead of 11 x 12 x 4 = 528 (576).
+    {
+        const int S = q.sh;
+        const int cs = round_up(q.C * S * S, 8);
+        const int gkh = (q.kh + S - 1) / S, gkw = (q.kw + S - 1) / S;
+        const int xhp = q.Ho + gkh - 1, xwp = q.Wo + gkw - 1;
+        const int64_t r_plain = ((int64_t)q.kh * q.kwp * q.Cgp + kBf16TK - 1) / kBf16TK;
+        const int64_t r_s2d = ((int64_t)gkh * gkw * cs + kBf16TK - 1) / kBf16TK;
+        if (q.G == 1 && S >= 2 && q.sw == S && q.kh >= S && q.kw >= S && q.C * S * S <= 64 &&
+            r_s2d < r_plain && xhp <= 65535 && q.N <= 65535 &&
+            (int64_t)q.C * S * xwp * S * 2 <= 64 * 1024 &&
+            (int64_t)q.C * q.H * q.W * 4 < (int64_t(1) << 31)) {
+            q.s2d = S;
+            q.Cgp = cs;
+            q.tpc = 1;
+            q.gkh = gkh;
+            q.kwp = gkw;
+            q.XHp = xhp;
+            q.XWp = xwp;
+        }
+    }
+    const int khw = q.gkh * q.kwp;
     const int php = q.Th - 1 - q.a0h, pwp = q.Tw - 1 - q.a0w;
     q.dtb = std::max(php, 0);
     q.dlb = std::max(pwp, 0);
@@ -878,6 +909,16 @@ int backward_dense(const ConvPlan& q, const float* top_diff, const float* top, b
 }
 
 // ---- bf16 operands
+// The input's bf16 staging (plain or space-to-depth) at xh.
+hipError_t stage_bottom_bf16(const ConvPlan& q, const void* bottom, uint16_t* xh, hipStream_t s)
+{
+    if (q.s2d)
+        return launch_stage_s2d_bf16(bottom, bottom_f32(q), xh, q.N, q.C, q.H, q.W, q.s2d, q.ph,
+                                     q.pw, q.XHp, q.XWp, q.Cgp, s);
+    return launch_stage_nhwc_bf16(bottom, bottom_f32(q), xh, q.N, q.C, q.H, q.W, q.Cg, q.Cgp,
+                                  q.G * q.Cgp, q.XHp, q.XWp, q.ph, q.pw, s);
+}
+
 int run_forward_bf16(const ConvPlan& q, const void* bottom, const void* weight, const float* bias,
                      float* top, char* ws, hipStream_t s)
 {
@@ -886,11 +927,9 @@ int run_forward_bf16(const ConvPlan& q, const void* bottom, const void* weight, 
     uint16_t* xh = (uint16_t*)(ws + q.off_xh_fwd);
     uint16_t* wp = (uint16_t*)(ws + q.off_wp_fwd);
     const int Ctot = q.G * q.Cgp;
-    LAUNCH(launch_stage_nhwc_bf16(bottom, bottom_f32(q), xh, q.N, q.C, q.H, q.W, q.Cg, q.Cgp,
-                                  Ctot, q.XHp, q.XWp, q.ph, q.pw, s),
-           "bf16 staging launch");
+    LAUNCH(stage_bottom_bf16(q, bottom, xh, s), "bf16 staging launch");
     LAUNCH(launch_pack_weights_bf16((const uint16_t*)weight, wp, q.K, q.Cg, q.Cgp, q.kh, q.kw,
-                                    q.kwp, q.Rp, s),
+                                    q.kwp, q.s2d ? q.s2d : 1, q.Rp, s),
            "bf16 weight pack launch");
     GemmBf16Params p = {};
     p.A = wp;
@@ -905,9 +944,11 @@ int run_forward_bf16(const ConvPlan& q, const void* bottom, const void* weight, 
     p.Cg8 = q.Cgp >= 8 ? q.Cgp / 8 : 1;
     p.kw = q.kwp / q.tpc;
     p.vstr = q.Cgp >= 8 ? Ctot : 8;
-    p.KC = q.kh * p.kw * p.Cg8;
+    p.KC = q.gkh * p.kw * p.Cg8;
     p.div_cg8 = make_fastdiv((uint32_t)p.Cg8); p.div_kw = make_fastdiv((uint32_t)p.kw);
-    p.kh = q.kh; p.sh = q.sh; p.sw = q.sw; p.oh0 = 0; p.ow0 = 0;
+    p.kh = q.gkh; p.oh0 = 0; p.ow0 = 0;
+    p.sh = q.s2d ? 1 : q.sh;
+    p.sw = q.s2d ? 1 : q.sw;
     p.OH = q.Ho; p.OW = q.Wo;
     p.M = q.Kg; p.Rp = q.Rp; p.G = q.G;
     p.Ncol = q.N * q.Ho * q.Wo;
@@ -964,9 +1005,7 @@ int run_weights_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom, 
     float* part = (float*)(ws + q.off_part);
     const int Ctot = q.G * q.Cgp;
     if (!staged)
-        LAUNCH(launch_stage_nhwc_bf16(bottom, bottom_f32(q), xh, q.N, q.C, q.H, q.W, q.Cg,
-                                      q.Cgp, Ctot, q.XHp, q.XWp, q.ph, q.pw, s),
-               "bf16 staging launch");
+        LAUNCH(stage_bottom_bf16(q, bottom, xh, s), "bf16 staging launch");
     WgradBf16Params p = {};
     p.D = dh;
     p.X = xh;
@@ -977,7 +1016,9 @@ int run_weights_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom, 
     p.N = q.N; p.IHp = q.XHp; p.IWp = q.XWp; p.Ctot = Ctot; p.Cgp = q.Cgp;
     p.K = q.K; p.Kg = q.Kg; p.Kgp = q.Kgp; p.Ktot = q.G * q.Kgp;
     p.DHp = q.DHp; p.DWp = q.DWp; p.dtb = q.dtb; p.dlb = q.dlb;
-    p.kh = q.kh; p.kw = q.kwp; p.sh = q.sh; p.sw = q.sw;
+    p.kh = q.gkh; p.kw = q.kwp;
+    p.sh = q.s2d ? 1 : q.sh;
+    p.sw = q.s2d ? 1 : q.sw;
     p.OH = q.Ho; p.OW = q.Wo;
     p.Rw = q.Rw; p.G = q.G;
     p.Ncol = q.N * q.Ho * q.Wo;
@@ -987,7 +1028,7 @@ int run_weights_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom, 
     p.div_ow = make_fastdiv((uint32_t)q.Wo);
     LAUNCH(launch_conv_wgrad_bf16(p, q.wgrad_tile, s), "bf16 weight-gradient launch");
     LAUNCH(launch_wgrad_reduce_perm(part, weight_diff, q.K, q.Rw, q.Cgp, q.Cg, q.kh, q.kw, q.kwp,
-                                    q.splits, accumulate, s),
+                                    q.s2d ? q.s2d : 1, q.splits, accumulate, s),
            "bf16 reduce launch");
     return CAFFE_OK;
 }

@@ -687,15 +687,18 @@ conv_wgrad_bf16_kernel(const WgradBf16Params p)
     }
 }
 
-// dW[k][c][u][v] = (accumulate ? dW : 0) + sum_s P[s][k][(u*kwp + v)*Cgp + c]
+// dW[k][c][u][v] = (accumulate ? dW : 0) + sum_s P[s][k][(bu*kwp + bv)*Cgp + cp]
 // (c < Cg, u < kh, v < kw): the split partials added in a fixed order, as
-// wgrad_reduce_kernel does, with lanes along the partials' (u, v, c) order.
+// wgrad_reduce_kernel does, with lanes along the partials' (bu, bv, cp)
+// order.  Plain staging (S = 1): (bu, bv, cp) = (u, v, c).  Space-to-depth
+// staging by S: u = S*bu + fu, v = S*bv + fv, cp = (fu*S + fv)*Cg + c.
 constexpr int kPermParts = 8;
 constexpr int kPermCols = 32;
 
 __global__ void __launch_bounds__(kPermParts * kPermCols)
 wgrad_reduce_perm_kernel(const float* __restrict__ P, float* __restrict__ dW, int K, int Rw,
-                         int Cgp, int Cg, int kh, int kw, int kwp, int splits, int accumulate)
+                         int Cgp, int Cg, int kh, int kw, int kwp, int S, int splits,
+                         int accumulate)
 {
     __shared__ float part[kPermParts][kPermCols + 1];
     const int col = threadIdx.x % kPermCols;
@@ -728,10 +731,15 @@ wgrad_reduce_perm_kernel(const float* __restrict__ P, float* __restrict__ dW, in
         const int k = e / Rw;
         const int r = e - k * Rw;
         const int tap = r / Cgp;
-        const int c = r - tap * Cgp;
-        const int u = tap / kwp;
-        const int v = tap - u * kwp;
-        if (c < Cg && u < kh && v < kw) {
+        const int cp = r - tap * Cgp;
+        const int bu = tap / kwp;
+        const int bv = tap - bu * kwp;
+        const int f = cp / Cg;
+        const int c = cp - f * Cg;
+        const int fu = f / S;
+        const int u = S * bu + fu;
+        const int v = S * bv + f - fu * S;
+        if (f < S * S && u < kh && v < kw) {
             float* o = dW + (((size_t)k * Cg + c) * kh + u) * kw + v;
             *o = accumulate ? *o + t : t;
         }
@@ -1080,11 +1088,13 @@ bias_reduce_kernel(const float* __restrict__ sums, float* __restrict__ db, int T
         db[k] = accumulate ? db[k] + red[0] : red[0];
 }
 
-// Forward weights: Wp[o][(u*kwp + v)*Cgp + c] = W[o][c][u][v], zero for
-// c >= Cg, v >= kw and r >= kh*kwp*Cgp (rows padded to Rp).
+// Forward weights in the staged reduction order, rows padded to Rp:
+// Wp[o][(bu*kwp + bv)*Cgp + cp] = W[o][c][u][v] with (u, v, c) as in
+// wgrad_reduce_perm_kernel (S = 1: (bu, bv, cp) = (u, v, c)), zero where u, v
+// or c falls outside the kernel or the channels and for r >= the staged taps.
 __global__ void __launch_bounds__(256)
 pack_weights_bf16_kernel(const bf16_t* __restrict__ W, bf16_t* __restrict__ Wp, int K, int Cg,
-                         int Cgp, int kh, int kw, int kwp, int Rp)
+                         int Cgp, int kh, int kw, int kwp, int S, int Rp)
 {
     const long total = (long)K * Rp;
     for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < total;
@@ -1092,11 +1102,16 @@ pack_weights_bf16_kernel(const bf16_t* __restrict__ W, bf16_t* __restrict__ Wp, 
         const int o = (int)(e / Rp);
         const int r = (int)(e - (long)o * Rp);
         const int t = r / Cgp;
-        const int c = r - t * Cgp;
-        const int u = t / kwp;
-        const int v = t - u * kwp;
+        const int cp = r - t * Cgp;
+        const int bu = t / kwp;
+        const int bv = t - bu * kwp;
+        const int f = cp / Cg;
+        const int c = cp - f * Cg;
+        const int fu = f / S;
+        const int u = S * bu + fu;
+        const int v = S * bv + f - fu * S;
         bf16_t x = 0;
-        if (u < kh && v < kw && c < Cg)
+        if (f < S * S && u < kh && v < kw)
             x = W[(((long)o * Cg + c) * kh + u) * kw + v];
         Wp[e] = x;
     }
@@ -1250,14 +1265,14 @@ hipError_t launch_conv_wgrad_bf16(const WgradBf16Params& p, int tile, hipStream_
 }
 
 hipError_t launch_wgrad_reduce_perm(const float* P, float* dW, int K, int Rw, int Cgp, int Cg,
-                                    int kh, int kw, int kwp, int splits, int accumulate,
+                                    int kh, int kw, int kwp, int S, int splits, int accumulate,
                                     hipStream_t s)
 {
     const int count = K * Rw;
     if (count == 0)
         return hipSuccess;
     hipLaunchKernelGGL(wgrad_reduce_perm_kernel, dim3((count + kPermCols - 1) / kPermCols),
-                       dim3(kPermParts * kPermCols), 0, s, P, dW, K, Rw, Cgp, Cg, kh, kw, kwp,
+                       dim3(kPermParts * kPermCols), 0, s, P, dW, K, Rw, Cgp, Cg, kh, kw, kwp, S,
                        splits, accumulate);
     return hipGetLastError();
 }
@@ -1369,13 +1384,116 @@ hipError_t launch_bias_reduce(const float* sums, float* db, int T, int K, int ac
 }
 
 hipError_t launch_pack_weights_bf16(const uint16_t* W, uint16_t* Wp, int K, int Cg, int Cgp,
-                                    int kh, int kw, int kwp, int Rp, hipStream_t s)
+                                    int kh, int kw, int kwp, int S, int Rp, hipStream_t s)
 {
     const long total = (long)K * Rp;
     if (total == 0)
         return hipSuccess;
     hipLaunchKernelGGL(pack_weights_bf16_kernel, dim3(grid_1d(total)), dim3(256), 0, s, W, Wp, K,
-                       Cg, Cgp, kh, kw, kwp, Rp);
+                       Cg, Cgp, kh, kw, kwp, S, Rp);
+    return hipGetLastError();
+}
+
+// Space-to-depth staging by S (a strided layer as a stride-1 one):
+// Xp[n][a][b][(fu*S + fv)*C + c] = X[n][c][S*a + fu - ph][S*b + fv - pw] (0
+// outside the image and for channels past C*S*S, up to Csp).  One block per
+// (RA staged rows, image n): the S*RA source rows of every channel go to LDS
+// with lanes along the row (coalesced, eight loads in flight per thread),
+// then each thread writes 16-byte chunks of 8 staged channels, lanes along
+// (pixel, chunk).
+template <typename T>
+__global__ void __launch_bounds__(256)
+stage_s2d_bf16_kernel(const T* __restrict__ X, bf16_t* __restrict__ Xp, int C, int H, int W,
+                      int S, int ph, int pw, int XHp, int XWp, int Csp, int RA, FastDiv div_c8,
+                      FastDiv div_xwp)
+{
+    extern __shared__ bf16_t srows[];  // [C][S * RA][XWp * S]
+    __shared__ int ctab[64];           // staged channel -> its (c, fu) row and fv in srows
+    const int tid = threadIdx.x;
+    const int a0 = blockIdx.x * RA;
+    const int na = min(RA, XHp - a0);
+    const int n = blockIdx.y;
+    const int RW = XWp * S;
+    const int SR = S * RA;              // source rows per channel
+    const int Cs = C * S * S;
+    if (tid < Csp) {
+        int t = -1;
+        if (tid < Cs) {
+            const int f = tid / C;
+            const int c = tid - f * C;
+            const int fu = f / S;
+            t = (c * SR + fu) * RW + (f - fu * S);
+        }
+        ctab[tid] = t;
+    }
+    const uint32_t plane = (uint32_t)(H * W) * (uint32_t)sizeof(T);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + (size_t)n * C * H * W, (uint32_t)C * plane);
+    // source rows rr = c * SR + r, eight at a time, lanes along the row
+    const int nrows = C * SR;
+    for (int rr0 = 0; rr0 < nrows; rr0 += 8) {
+        for (int x = tid; x < RW; x += 256) {
+            const int w = x - pw;
+            const bool win = (unsigned)w < (unsigned)W;
+            T v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int rr = rr0 + u;  // (uniform)
+                const int c = rr / SR;
+                const int h = S * a0 + (rr - c * SR) - ph;
+                const bool in = rr < nrows && win && (unsigned)h < (unsigned)H;
+                const uint32_t voff =
+                    in ? (uint32_t)c * plane + (uint32_t)(h * W + w) * (uint32_t)sizeof(T) : kOob;
+                v[u] = load_elem<T>(rx, voff, 0u);
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (rr0 + u < nrows)
+                    srows[(rr0 + u) * RW + x] = to_bf16(v[u]);
+        }
+    }
+    __syncthreads();
+    // 16-byte chunks of 8 staged channels, lanes along (pixel, chunk)
+    const int C8 = Csp / 8;
+    for (int id = tid; id < na * XWp * C8; id += 256) {
+        const int pl = (int)fdiv((uint32_t)id, div_c8);  // (row of the block, b)
+        const int q = id - pl * C8;
+        const int ra = (int)fdiv((uint32_t)pl, div_xwp);
+        const int b = pl - ra * XWp;
+        const int base = S * (ra * RW + b);
+        uint32_t wv[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int t0 = ctab[8 * q + 2 * k], t1 = ctab[8 * q + 2 * k + 1];
+            const uint32_t lo = t0 >= 0 ? srows[t0 + base] : 0u;
+            const uint32_t hi = t1 >= 0 ? srows[t1 + base] : 0u;
+            wv[k] = lo | (hi << 16);
+        }
+        *(u32x4*)&Xp[(((size_t)n * XHp + a0 + ra) * XWp + b) * Csp + 8 * q] =
+            u32x4{wv[0], wv[1], wv[2], wv[3]};
+    }
+}
+
+hipError_t launch_stage_s2d_bf16(const void* X, int x_f32, uint16_t* Xp, int N, int C, int H,
+                                 int W, int S, int ph, int pw, int XHp, int XWp, int Csp,
+                                 hipStream_t s)
+{
+    if (N == 0)
+        return hipSuccess;
+    // staged rows per block: about 32 KB of source rows in LDS
+    const size_t row_lds = (size_t)C * S * XWp * S * 2;
+    if (row_lds > 64 * 1024 || Csp % 8 != 0 || C * S * S > Csp || Csp > 64 || N > 65535 ||
+        (int64_t)C * H * W * 4 >= (int64_t(1) << 31))
+        return hipErrorInvalidValue;
+    const int RA = (int)std::max<size_t>(1, std::min<size_t>(8, (32 * 1024) / row_lds));
+    const dim3 grid((unsigned)((XHp + RA - 1) / RA), (unsigned)N);
+    const size_t lds = row_lds * RA;
+    const FastDiv dc8 = make_fastdiv((uint32_t)(Csp / 8)), dxw = make_fastdiv((uint32_t)XWp);
+    if (x_f32)
+        hipLaunchKernelGGL(stage_s2d_bf16_kernel<float>, grid, dim3(256), lds, s,
+                           (const float*)X, Xp, C, H, W, S, ph, pw, XHp, XWp, Csp, RA, dc8, dxw);
+    else
+        hipLaunchKernelGGL(stage_s2d_bf16_kernel<bf16_t>, grid, dim3(256), lds, s,
+                           (const bf16_t*)X, Xp, C, H, W, S, ph, pw, XHp, XWp, Csp, RA, dc8, dxw);
     return hipGetLastError();
 }
 

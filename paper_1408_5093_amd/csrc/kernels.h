@@ -286,10 +286,11 @@ constexpr int kBf16WgradTN = 256;
 // cols_per_split must be a multiple of kBf16WgradTK
 hipError_t launch_conv_wgrad_bf16(const WgradBf16Params& p, int tile, hipStream_t s);
 
-// dW[k][c][u][v] = (accumulate ? dW : 0) + sum_s P[s][k][(u*kwp + v)*Cgp + c]
-// for c < Cg, u < kh, v < kw (fixed order).
+// dW[k][c][u][v] = (accumulate ? dW : 0) + sum_s P[s][k][(bu*kwp + bv)*Cgp + cp]
+// for c < Cg, u < kh, v < kw (fixed order), (bu, bv, cp) from (u, v, c) as in
+// launch_pack_weights_bf16.
 hipError_t launch_wgrad_reduce_perm(const float* P, float* dW, int K, int Rw, int Cgp, int Cg,
-                                    int kh, int kw, int kwp, int splits, int accumulate,
+                                    int kh, int kw, int kwp, int S, int splits, int accumulate,
                                     hipStream_t s);
 
 // Xp[n][hp][wp][g*Cgp + c] = X[n][g*Cg + c][hp - tb][wp - lb] inside the H x W
@@ -315,10 +316,20 @@ hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, f
 hipError_t launch_bias_reduce(const float* sums, float* db, int T, int K, int accumulate,
                               hipStream_t s);
 
-// Wp[o][(u*kwp + v)*Cgp + c] = W[o][c][u][v] (0 for c >= Cg, v >= kw and
-// past kh*kwp*Cgp).
+// Wp[o][(bu*kwp + bv)*Cgp + cp] = W[o][c][u][v], 0 outside the kernel and the
+// channels and past the staged taps; plain staging (S = 1): (bu, bv, cp) =
+// (u, v, c); space-to-depth by S: u = S*bu + fu, v = S*bv + fv,
+// cp = (fu*S + fv)*Cg + c.
 hipError_t launch_pack_weights_bf16(const uint16_t* W, uint16_t* Wp, int K, int Cg, int Cgp,
-                                    int kh, int kw, int kwp, int Rp, hipStream_t s);
+                                    int kh, int kw, int kwp, int S, int Rp, hipStream_t s);
+// Space-to-depth staging by S of one group of C channels:
+// Xp[n][a][b][(fu*S + fv)*C + c] = X[n][c][S*a + fu - ph][S*b + fv - pw] (0
+// outside the image and for staged channels past C*S*S, up to Csp, a
+// multiple of 8), XHp x XWp staged pixels per image.  X holds bf16 values, or
+// floats (x_f32) rounded to bf16 on the way.
+hipError_t launch_stage_s2d_bf16(const void* X, int x_f32, uint16_t* Xp, int N, int C, int H,
+                                 int W, int S, int ph, int pw, int XHp, int XWp, int Csp,
+                                 hipStream_t s);
 
 // Wt[g][(c, fh, fw)][(th*Tw + tw)*Kgp + k] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)]
 // (0 past the kernel edge, for k >= Kg and past Th*Tw*Kgp).

@@ -167,12 +167,17 @@ def test_workspace_sizes_bf16():
     # bf16 operands are staged channel-contiguous on a zero-bordered grid next
     # to the packed weights (rows padded to 64).  A single group of 3 channels
     # with an even horizontal stride is padded to 4 channels, two taps per
-    # 16-byte chunk: conv1's 11 taps per kernel row round up to 12, its staged
-    # width to 228 (the last tap pair reads one column past the image)
+    # 16-byte chunk: 5 taps per kernel row round up to 6, the staged width to
+    # 64 (the last tap pair reads one column past the image)
+    d1 = cc.conv_desc((8, 3, 63, 63), (16, 3, 5, 5), 2, 0, 1, True, cc.CAFFE_BF16)
+    assert cc.conv_workspace_size(d1, cc.PASS_FORWARD) >= 8 * 63 * 64 * 4 * 2 + 16 * 128 * 2
+    # conv1 (stride 4) is staged space-to-depth: 4 x 4 pixel blocks of its 3
+    # channels become 48 channels of a 57 x 57 grid, its 11 x 11 kernel 3 x 3
+    # taps of them (432 reduction elements, rows padded to 448)
     d = cc.conv_desc((256, 3, 227, 227), (96, 3, 11, 11), 4, 0, 1, True, cc.CAFFE_BF16)
-    xh = 256 * 227 * 228 * 4 * 2
-    assert cc.conv_workspace_size(d, cc.PASS_FORWARD) >= xh + 96 * 576 * 2
-    assert cc.conv_workspace_size(d, cc.PASS_FORWARD) < 256 * 227 * 227 * 8 * 2
+    xh = 256 * 57 * 57 * 48 * 2
+    assert cc.conv_workspace_size(d, cc.PASS_FORWARD) >= xh + 96 * 448 * 2
+    assert cc.conv_workspace_size(d, cc.PASS_FORWARD) < 256 * 227 * 228 * 4 * 2
     dh = 256 * 55 * 55 * 96 * 2
     both = cc.conv_workspace_size(d, cc.PASS_BACKWARD)
     assert both >= dh + xh

@@ -168,9 +168,11 @@ class ConvStack:
         # "bwd" (data gradient), "wgt" (weight and bias gradients) or "both"
         # (both gradients in one call)
         self.events = None
+        # with a set of (kind, layer) keys, only those calls are marked
+        self.mark_only = None
 
     def _mark(self, tag, s):
-        if self.events is not None:
+        if self.events is not None and (self.mark_only is None or tag[:2] in self.mark_only):
             ev = torch.cuda.Event(enable_timing=True)
             ev.record(s)
             self.events.append((tag, ev))

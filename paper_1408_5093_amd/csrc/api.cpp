@@ -99,6 +99,13 @@ struct ConvPlan {
     // (data gradient)
     int fwd_splits, fwd_sps, dgrad_splits, dgrad_sps;
     size_t off_fwd_part;
+    // tail splits of the forward and data-gradient GEMMs (splits 1: none):
+    // the tiles from T on cut into `splits` reduction ranges of sps stages,
+    // their partials at the split partials' offset
+    struct Tail {
+        int T, splits, sps, c0;
+        int64_t bytes;
+    } fwd_tail, dgrad_tail;
     bool dense;
     int fc_tile_f, fc_tile_d, fc_tile_w;
     int fc_splits_f, fc_sps_f, fc_splits_d, fc_sps_d, fc_splits_w, fc_sps_w;
@@ -157,6 +164,81 @@ void plan_splits(int M, int ncol, int R, int tile, int cus, int forced, int* spl
         best = std::min<int64_t>(forced, nst);
     *sps = (int)((nst + best - 1) / best);
     *splits = (int)((nst + *sps - 1) / *sps);
+}
+
+// Tail split of a GEMM with G groups of M x ncol outputs on a tile and a
+// reduction of R (one workgroup per tile otherwise).  When the tiles do not
+// deal evenly to the `cus` compute units, some units run one workgroup more
+// than the rest while the others idle (CaffeNet N=256: conv5's forward and
+// conv3's data gradient have 676 128 x 128 tiles, 2.64 per unit, and run
+// ~20% longer than conv3's forward with 1014, 3.96 per unit).  The last
+// tiles past whole rounds of the units -- whole column tiles of the last
+// group -- are then cut into s reduction ranges, one workgroup each, whose
+// partials a reduce adds: every unit gets about the same work.  The model:
+// workgroup b runs on unit b % cus, a unit's time is the sum of its
+// workgroups' stages; s (2..8) is taken when the modelled time with the
+// partial sums' traffic (written and read once at ~4 TB/s, plus ~6 us for
+// the reduce) beats the plain grid's by 1.5% or more (measured alone at
+// N=256: conv5's forward 0.362 -> 0.348 ms with 3 ranges, conv3's data
+// gradient 0.719 -> 0.661, conv2's forward 0.929 -> 0.908 with 2, conv2's
+// data gradient 1.032 -> 0.993 with 4; conv1's data gradient, which the
+// model leaves whole, 0.630 -> 0.652 with 2).
+void plan_tail(int M, int64_t ncol, int R, int tile, int G, int cus, int forced, int forced_cus,
+               ConvPlan::Tail* t)
+{
+    *t = ConvPlan::Tail{0, 1, 0, 0, 0};
+    const int tm = gemm_tile_m(tile), tn = gemm_tile_n(tile), tk = gemm_tile_k(tile);
+    const int64_t n_mt = (M + tm - 1) / tm, n_ct = (ncol + tn - 1) / tn;
+    const int64_t n_tiles = n_mt * n_ct * G;
+    const int64_t nst = (R + tk - 1) / tk;
+    if (forced_cus > 0)  // profiling and tests only
+        cus = forced_cus;
+    cus = std::max(1, cus);
+    if (forced == 0 || n_tiles < cus || nst < 8 || M <= 0)
+        return;
+    const int64_t past = n_tiles % cus;
+    if (past == 0 && forced < 0)
+        return;
+    // whole column tiles of the last group
+    const int64_t n_tail = std::max<int64_t>(n_mt, (past + n_mt - 1) / n_mt * n_mt);
+    if (n_tail > n_mt * n_ct)
+        return;
+    const int64_t full = n_tiles - n_tail;
+    const double t_stage = 2.0 * tm * tn * tk / (0.8 * 157.3e12 / 256);
+    auto unit_time = [&](int64_t s) {  // the busiest unit's stages
+        const int64_t sps = (nst + s - 1) / s;
+        int64_t worst = 0;
+        for (int64_t c = 0; c < cus; ++c) {
+            const int64_t nf = full > c ? (full - 1 - c) / cus + 1 : 0;
+            // partial workgroups b = full .. full + n_tail * s - 1 on unit c
+            const int64_t lo = full, hi = full + n_tail * s;
+            const int64_t first = lo + ((c - lo % cus) % cus + cus) % cus;
+            const int64_t np = first < hi ? (hi - 1 - first) / cus + 1 : 0;
+            worst = std::max(worst, nf * nst + np * sps);
+        }
+        return worst;
+    };
+    const double plain = (double)((n_tiles + cus - 1) / cus) * nst * t_stage;
+    double best_t = plain * 0.985;
+    int64_t best = 0;
+    for (int64_t s = 2; s <= 8; ++s) {
+        const int64_t sps = (nst + s - 1) / s;
+        if (sps < 4 || (s - 1) * sps >= nst)
+            continue;
+        const int64_t bytes = s * (int64_t)M * (ncol - (n_ct - n_tail / n_mt) * tn) * 4;
+        const double tt = unit_time(s) * t_stage + 2.0 * bytes / 4e12 + 6e-6;
+        if (forced > 1 ? s == forced : tt < best_t) {
+            best_t = tt;
+            best = s;
+        }
+    }
+    if (best < 2)
+        return;
+    t->T = (int)full;
+    t->splits = (int)best;
+    t->sps = (int)((nst + best - 1) / best);
+    t->c0 = (int)((n_ct - n_tail / n_mt) * tn);
+    t->bytes = best * (int64_t)M * (ncol - t->c0) * 4;
 }
 
 // Tile for a GEMM with M rows: the least padding of M; ties go to the first
@@ -564,9 +646,22 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
                 &q.fwd_splits, &q.fwd_sps, q.G);
     plan_splits(q.Mt, (int)dcols, q.Rt, q.dgrad_tile, cus, env_tile("CAFFE_CONV_DGRAD_SPLITS"),
                 &q.dgrad_splits, &q.dgrad_sps, q.G);
-    const int64_t fpart = q.fwd_splits > 1 ? (int64_t)q.fwd_splits * q.top_elems * 4 : 0;
-    const int64_t dpart =
-        q.dgrad_splits > 1 ? (int64_t)q.dgrad_splits * q.G * q.Mt * dcols * 4 : 0;
+    // tail splits where the grid is not split already
+    const int tail_forced = env_tile("CAFFE_CONV_TAIL_SPLITS");
+    const int tail_cus = env_tile("CAFFE_CONV_TAIL_UNITS");
+    q.fwd_tail = ConvPlan::Tail{0, 1, 0, 0, 0};
+    q.dgrad_tail = ConvPlan::Tail{0, 1, 0, 0, 0};
+    if (q.fwd_splits == 1)
+        plan_tail(q.Kg, (int64_t)q.N * q.Ho * q.Wo, q.R, q.fwd_tile, q.G, cus, tail_forced,
+                  tail_cus, &q.fwd_tail);
+    if (q.dgrad_splits == 1)
+        plan_tail(q.Mt, dcols, q.Rt, q.dgrad_tile, q.G, cus, tail_forced, tail_cus,
+                  &q.dgrad_tail);
+    const int64_t fpart = q.fwd_splits > 1 ? (int64_t)q.fwd_splits * q.top_elems * 4
+                                           : q.fwd_tail.bytes;
+    const int64_t dpart = q.dgrad_splits > 1
+                              ? (int64_t)q.dgrad_splits * q.G * q.Mt * dcols * 4
+                              : q.dgrad_tail.bytes;
     if (fpart > kMaxTensorBytes || dpart > kMaxTensorBytes)
         return fail(CAFFE_ERR_UNSUPPORTED, "split partials reach 2^31 bytes");
     q.off_fwd_part = q.ws_fwd;
@@ -686,6 +781,20 @@ int run_forward(const ConvPlan& q, const void* bottom, const void* weight, const
                "forward reduce launch");
         return CAFFE_OK;
     }
+    if (q.fwd_tail.splits > 1) {
+        float* part = (float*)(ws + q.off_fwd_part);
+        p.tail_T = q.fwd_tail.T;
+        p.tail_splits = q.fwd_tail.splits;
+        p.tail_sps = q.fwd_tail.sps;
+        p.tail_c0 = q.fwd_tail.c0;
+        p.Pt = part;
+        p.Pt_bytes = nbytes(q.fwd_tail.bytes, 1);
+        LAUNCH(launch_conv_gemm_f32(p, 0, q.fwd_tile, q.fwd_tap, s), "forward launch");
+        LAUNCH(launch_conv_split_reduce_fwd(part, q.fwd_tail.splits, p, top, s, q.G - 1,
+                                            q.fwd_tail.c0),
+               "forward tail reduce launch");
+        return CAFFE_OK;
+    }
     LAUNCH(launch_conv_gemm_f32(p, 0, q.fwd_tile, q.fwd_tap, s), "forward launch");
     return CAFFE_OK;
 }
@@ -752,6 +861,21 @@ int run_data(const ConvPlan& q, const float* dsrc, const float* bottom_mask, con
         LAUNCH(launch_conv_split_reduce_dgrad(part, q.dgrad_splits, p, bottom_mask, bottom_diff,
                                               s),
                "data-gradient reduce launch");
+        return CAFFE_OK;
+    }
+    if (q.dgrad_tail.splits > 1) {
+        float* part = (float*)(ws + q.off_part);
+        p.tail_T = q.dgrad_tail.T;
+        p.tail_splits = q.dgrad_tail.splits;
+        p.tail_sps = q.dgrad_tail.sps;
+        p.tail_c0 = q.dgrad_tail.c0;
+        p.Pt = part;
+        p.Pt_bytes = nbytes(q.dgrad_tail.bytes, 1);
+        LAUNCH(launch_conv_gemm_f32(p, 1, q.dgrad_tile, q.dgrad_tap, s),
+               "data-gradient launch");
+        LAUNCH(launch_conv_split_reduce_dgrad(part, q.dgrad_tail.splits, p, bottom_mask,
+                                              bottom_diff, s, q.G - 1, q.dgrad_tail.c0),
+               "data-gradient tail reduce launch");
         return CAFFE_OK;
     }
     LAUNCH(launch_conv_gemm_f32(p, 1, q.dgrad_tile, q.dgrad_tap, s), "data-gradient launch");

@@ -294,16 +294,17 @@ hipError_t launch_split_reduce(const float* P, int splits, int count, int ncol, 
 // Split convolution GEMM epilogues: one thread per GEMM output (g, m, col),
 // col fastest (coalesced partial reads); the partials of an output are added
 // in split order after the bias.
+// The region: groups g0 .. g0 + Gt - 1, columns c0 .. c0 + Nc - 1.
 __global__ void __launch_bounds__(256)
-conv_split_reduce_fwd_kernel(const float* __restrict__ P, int splits, int G, int M, int Ncol,
-                             int OHW, int Cout, const float* __restrict__ bias, int relu,
-                             float* __restrict__ Y)
+conv_split_reduce_fwd_kernel(const float* __restrict__ P, int splits, int g0, int Gt, int M,
+                             int c0, int Nc, int OHW, int Cout, const float* __restrict__ bias,
+                             int relu, float* __restrict__ Y)
 {
-    const int64_t count = (int64_t)G * M * Ncol;
+    const int64_t count = (int64_t)Gt * M * Nc;
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count;
          e += (int64_t)gridDim.x * blockDim.x) {
-        const int col = (int)(e % Ncol);
-        const int gm = (int)(e / Ncol);            // g * M + m = output channel
+        const int col = c0 + (int)(e % Nc);
+        const int gm = g0 * M + (int)(e / Nc);     // g * M + m = output channel
         float t = bias ? bias[gm] : 0.f;
         for (int q = 0; q < splits; ++q)
             t += P[(int64_t)q * count + e];
@@ -314,17 +315,17 @@ conv_split_reduce_fwd_kernel(const float* __restrict__ P, int splits, int G, int
 }
 
 __global__ void __launch_bounds__(256)
-conv_split_reduce_dgrad_kernel(const float* __restrict__ P, int splits, int G, int M, int Ncol,
-                               int OHW, int OW, int psh, int psw, int a0h, int a0w, int oph,
-                               int opw, int Cout, int Cg_out, int OutH, int OutW,
-                               const float* __restrict__ mask, float* __restrict__ dX)
+conv_split_reduce_dgrad_kernel(const float* __restrict__ P, int splits, int g0, int Gt, int M,
+                               int c0, int Nc, int OHW, int OW, int psh, int psw, int a0h,
+                               int a0w, int oph, int opw, int Cout, int Cg_out, int OutH,
+                               int OutW, const float* __restrict__ mask, float* __restrict__ dX)
 {
-    const int64_t count = (int64_t)G * M * Ncol;
+    const int64_t count = (int64_t)Gt * M * Nc;
     const int pss = psh * psw;
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count;
          e += (int64_t)gridDim.x * blockDim.x) {
-        const int col = (int)(e % Ncol);
-        const int gm = (int)(e / Ncol);
+        const int col = c0 + (int)(e % Nc);
+        const int gm = g0 * M + (int)(e / Nc);
         const int g = gm / M;
         const int m = gm - g * M;
         const int c = m / pss;
@@ -350,31 +351,38 @@ conv_split_reduce_dgrad_kernel(const float* __restrict__ P, int splits, int G, i
 }
 
 hipError_t launch_conv_split_reduce_fwd(const float* P, int splits, const ConvGemmParams& q,
-                                        float* Y, hipStream_t s)
+                                        float* Y, hipStream_t s, int g0, int c0)
 {
-    const int64_t count = (int64_t)q.G * q.M * q.Ncol;
+    if (g0 < 0 || g0 > q.G || c0 < 0 || c0 > q.Ncol)
+        return hipErrorInvalidValue;
+    const int Gt = q.G - g0, Nc = q.Ncol - c0;
+    const int64_t count = (int64_t)Gt * q.M * Nc;
     if (count == 0)
         return hipSuccess;
     int64_t blocks = (count + 255) / 256;
     if (blocks > 8192)
         blocks = 8192;
     hipLaunchKernelGGL(conv_split_reduce_fwd_kernel, dim3((unsigned)blocks), dim3(256), 0, s, P,
-                       splits, q.G, q.M, q.Ncol, q.OH * q.OW, q.Cout, q.bias, q.relu, Y);
+                       splits, g0, Gt, q.M, c0, Nc, q.OH * q.OW, q.Cout, q.bias, q.relu, Y);
     return hipGetLastError();
 }
 
 hipError_t launch_conv_split_reduce_dgrad(const float* P, int splits, const ConvGemmParams& q,
-                                          const float* mask, float* dX, hipStream_t s)
+                                          const float* mask, float* dX, hipStream_t s, int g0,
+                                          int c0)
 {
-    const int64_t count = (int64_t)q.G * q.M * q.Ncol;
+    if (g0 < 0 || g0 > q.G || c0 < 0 || c0 > q.Ncol)
+        return hipErrorInvalidValue;
+    const int Gt = q.G - g0, Nc = q.Ncol - c0;
+    const int64_t count = (int64_t)Gt * q.M * Nc;
     if (count == 0)
         return hipSuccess;
     int64_t blocks = (count + 255) / 256;
     if (blocks > 8192)
         blocks = 8192;
     hipLaunchKernelGGL(conv_split_reduce_dgrad_kernel, dim3((unsigned)blocks), dim3(256), 0, s, P,
-                       splits, q.G, q.M, q.Ncol, q.OH * q.OW, q.OW, q.psh, q.psw, q.a0h, q.a0w,
-                       q.oph, q.opw, q.Cout, q.Cg_out, q.OutH, q.OutW, mask, dX);
+                       splits, g0, Gt, q.M, c0, Nc, q.OH * q.OW, q.OW, q.psh, q.psw, q.a0h,
+                       q.a0w, q.oph, q.opw, q.Cout, q.Cg_out, q.OutH, q.OutW, mask, dX);
     return hipGetLastError();
 }
 

@@ -115,18 +115,54 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     // run together on one XCD and share its L2.
     const int n_mt = (p.M + TM - 1) / TM;
     const int n_ct = (p.Ncol + TN - 1) / TN;
-    const int per_xcd = gridDim.x >> 3;
-    const int T = p.xcd_order ? (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3) : blockIdx.x;
+    const int n_tiles = n_mt * n_ct * p.G;
+    const bool has_tail = EPI < 2 && p.tail_splits > 1;
+    int T = blockIdx.x;
+    if (p.xcd_order) {
+        const int x = blockIdx.x & 7, i = blockIdx.x >> 3;
+        if (has_tail) {
+            // each XCD takes a contiguous run of the whole tiles, then an
+            // eighth of the tail's work items, which fill its units last
+            const int n_items = (n_tiles - p.tail_T) * p.tail_splits;
+            const int fq = (p.tail_T + 7) >> 3, tq = (n_items + 7) >> 3;
+            if (i < fq) {
+                const int f = x * fq + i;
+                T = f < p.tail_T ? f : INT_MAX;
+            } else {
+                const int j = x * tq + (i - fq);
+                T = j < n_items ? p.tail_T + j : INT_MAX;
+            }
+        } else {
+            T = x * (int)(gridDim.x >> 3) + i;
+        }
+    }
     // EPI 2 (dense) and EPI 3 (gathered convolution operands) store split-K
     // partials: the reduction is cut into p.splits ranges of
-    // p.stages_per_split stages, the split index varying slowest
-    const int n_split = EPI >= 2 ? p.splits : 1;
-    if (T >= n_mt * n_ct * p.G * n_split)
-        return;
-    const int mt = T % n_mt;
-    const int ct = (T / n_mt) % n_ct;
-    const int g = (T / (n_mt * n_ct)) % p.G;
-    const int split = T / (n_mt * n_ct * p.G);
+    // p.stages_per_split stages, the split index varying slowest.  EPI 0 and
+    // 1 may cut only their last tiles (a tail split, see ConvGemmParams):
+    // work item T >= tail_T takes reduction range (T - tail_T) % tail_splits
+    // of tile tail_T + (T - tail_T) / tail_splits.
+    int tile = T, split = 0;
+    bool tail = false;
+    if constexpr (EPI >= 2) {
+        if (T >= n_tiles * p.splits)
+            return;
+        tile = T % n_tiles;
+        split = T / n_tiles;
+    } else {
+        if (has_tail && T >= p.tail_T) {
+            const int j = T - p.tail_T;
+            const int jt = j / p.tail_splits;
+            tile = p.tail_T + jt;
+            split = j - jt * p.tail_splits;
+            tail = true;
+        }
+        if (tile >= n_tiles)
+            return;
+    }
+    const int mt = tile % n_mt;
+    const int ct = (tile / n_mt) % n_ct;
+    const int g = tile / (n_mt * n_ct);
     const int m0 = mt * TM;
     const int n0 = ct * TN;
     const int M = p.M, R = p.R;
@@ -329,8 +365,9 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     for (int mi = 0; mi < MI; ++mi) {
         typename Op::acc_t init{};
         if constexpr (EPI == 0) {
+            // (a tail split's partials leave the bias to the reduce)
             const __amdgpu_buffer_rsrc_t rbias =
-                make_rsrc(p.bias, p.bias ? (uint32_t)(p.G * M) * 4u : 0u);
+                make_rsrc(p.bias, p.bias && !tail ? (uint32_t)(p.G * M) * 4u : 0u);
 #pragma unroll
             for (int q = 0; q < Op::kRegs; ++q) {
                 const int m = m0 + wm * MI * MT + mi * MT + Op::row(q, lane);
@@ -343,14 +380,16 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     }
 
     const int nst_all = (R + TK - 1) / TK;
-    const int s_begin = EPI >= 2 ? split * p.stages_per_split : 0;
-    const int nst = EPI >= 2 ? min(nst_all, s_begin + p.stages_per_split) : nst_all;
+    const bool splitk = EPI >= 2 || tail;
+    const int sps = EPI >= 2 ? p.stages_per_split : p.tail_sps;
+    const int s_begin = splitk ? split * sps : 0;
+    const int nst = splitk ? min(nst_all, s_begin + sps) : nst_all;
     // blocked walk state: stage s covers tap (tu, tv) of channels tc .. tc + TK - 1.
     // It is updated in the loop body itself: captured by reference in a
     // lambda, it was kept in scratch memory, and the scratch accesses' waits
     // also stalled on the next stage's global loads.
     int tu = 0, tv = 0, tc = 0;
-    if constexpr (EPI == 3 && TAP) {
+    if constexpr (EPI != 2 && TAP) {
         // the walk state of the split's first stage
         if (p.blocked) {  // stage s: channels (s / khw) * TK.., tap s % khw
             const int t = s_begin % khw;
@@ -474,6 +513,31 @@ conv_gemm_f32_kernel(const ConvGemmParams p)
     static_assert(NI * MT == 64, "a wave covers 64 columns");
     constexpr int NR = WR::kRows;
     const int wcol = n0 + wn * NI * MT + lane;
+    if constexpr (EPI < 2) {
+        if (tail) {
+            // tail-split partial Pt[split][m][col - tail_c0] (the last group's)
+            const __amdgpu_buffer_rsrc_t rp = make_rsrc(p.Pt, p.Pt_bytes);
+            const int Nc = p.Ncol - p.tail_c0;
+            const uint32_t cbad = (uint32_t)(wcol >= p.Ncol) << 31;
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi) {
+#pragma unroll
+                for (int q = 0; q < Op::kRegs; ++q) {
+                    float v[NR];
+                    wave_rows<MT>(acc[mi], q, v);
+#pragma unroll
+                    for (int h = 0; h < NR; ++h) {
+                        const int m = m0 + wm * MI * MT + mi * MT + WR::row(q, h);
+                        const uint32_t off =
+                            ((uint32_t)((split * M + m) * Nc + wcol - p.tail_c0) * 4u) | cbad |
+                            ((uint32_t)(m >= M) << 31);
+                        buf_st_f32(v[h], rp, off);
+                    }
+                }
+            }
+            return;
+        }
+    }
     if constexpr (EPI >= 2) {
         // split partial P[split][g][m][col], lanes along col
         const uint32_t cbad = (uint32_t)(wcol >= p.Ncol) << 31;
@@ -679,9 +743,16 @@ template <int MT, int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH
 hipError_t launch_one(const ConvGemmParams& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * MT, TN = WN * NI * MT;
-    const int64_t tiles = (int64_t)((p.Ncol + TN - 1) / TN) * ((p.M + TM - 1) / TM) * p.G *
-                          (EPI >= 2 ? p.splits : 1);
-    const int64_t per_xcd = (tiles + 7) / 8;  // 8 XCDs; see the kernel's tile order
+    int64_t tiles = (int64_t)((p.Ncol + TN - 1) / TN) * ((p.M + TM - 1) / TM) * p.G;
+    int64_t per_xcd;  // 8 XCDs; see the kernel's tile order
+    if (EPI < 2 && p.tail_splits > 1) {
+        const int64_t items = (tiles - p.tail_T) * p.tail_splits;
+        per_xcd = (p.tail_T + 7) / 8 + (items + 7) / 8;
+    } else {
+        if (EPI >= 2)
+            tiles *= p.splits;
+        per_xcd = (tiles + 7) / 8;
+    }
     hipLaunchKernelGGL(
         (conv_gemm_f32_kernel<MT, WM, WN, MI, NI, TK, KH, KW, SH, SW, EPI, TAP, MASK>),
         dim3((unsigned)(per_xcd * 8)), dim3(64 * WM * WN), 0, s, p);
@@ -1021,6 +1092,20 @@ hipError_t launch_conv_gemm_f32(const ConvGemmParams& p, int epi, int tile, bool
         return hipSuccess;
     if (tile < 0 || tile >= TILE_COUNT || (tap_major && p.Cin_g % kTiles[tile].tk != 0))
         return hipErrorInvalidValue;
+    if ((epi == 0 || epi == 1) && p.tail_splits > 1) {
+        // the tail: whole column tiles of the last group, each range non-empty
+        const TileShape& t = kTiles[tile];
+        const int tm = t.wm * t.mi * t.mt, tn = t.wn * t.ni * t.mt;
+        const int n_mt = (p.M + tm - 1) / tm, n_ct = (p.Ncol + tn - 1) / tn;
+        const int n_tiles = n_mt * n_ct * p.G;
+        const int nst = (p.R + t.tk - 1) / t.tk;
+        if (p.tail_T < (p.G - 1) * n_mt * n_ct || p.tail_T >= n_tiles || p.tail_T % n_mt != 0 ||
+            p.tail_c0 != (p.tail_T / n_mt) % n_ct * tn || p.tail_sps < 1 ||
+            (int64_t)(p.tail_splits - 1) * p.tail_sps >= nst ||
+            (int64_t)p.tail_splits * p.M * (p.Ncol - p.tail_c0) * 4 > (int64_t)p.Pt_bytes ||
+            p.Pt == nullptr)
+            return hipErrorInvalidValue;
+    }
     if (epi == 0)
         return launch_tile<0, false>(p, tile, tap_major, s);
     if (epi == 3) {

@@ -54,6 +54,14 @@ struct ConvGemmParams {
     int xcd_order;  // XCD-contiguous tile order (else linear)
     int splits, stages_per_split;  // dense split-K GEMM only
     FastDiv div_pss, div_psw;  // epi 1: phases psh*psw and psw
+    // epi 0 / 1, tail_splits > 1: the tiles from tail_T on (whole column
+    // tiles of the last group, its columns from tail_c0 on) run as
+    // tail_splits reduction ranges of tail_sps stages, each storing its
+    // partial Pt[split][m][col - tail_c0] (Ncol - tail_c0 columns) for
+    // launch_conv_split_reduce_* over that region to finish
+    int tail_T, tail_splits, tail_sps, tail_c0;
+    float* Pt;
+    uint32_t Pt_bytes;
     // channel-major gathered operand (r = (c, u, v)) only, optional: byte
     // offsets (c*IH*IW + u*IW + v) * 4 of the taps r < R, then X_bytes up to
     // a whole number of stages (see launch_tap_table)
@@ -90,10 +98,13 @@ hipError_t launch_split_reduce(const float* P, int splits, int count, int ncol, 
 //   [psh (a + a0h) - oph + fh][psw (b + a0w) - opw + fw] = sum_s P[s][g][m][col]
 //   (pix = a * OW + b; positions outside the image are dropped), times
 //   [mask > 0] where mask is non-null.
+// With g0 / c0, only the outputs of groups g0.. and columns c0.. (the region
+// a tail split covers), from P[split][g - g0][m][col - c0].
 hipError_t launch_conv_split_reduce_fwd(const float* P, int splits, const ConvGemmParams& q,
-                                        float* Y, hipStream_t s);
+                                        float* Y, hipStream_t s, int g0 = 0, int c0 = 0);
 hipError_t launch_conv_split_reduce_dgrad(const float* P, int splits, const ConvGemmParams& q,
-                                          const float* mask, float* dX, hipStream_t s);
+                                          const float* mask, float* dX, hipStream_t s,
+                                          int g0 = 0, int c0 = 0);
 
 // Split-K weight gradient:
 //   P[s][g*Kg + m][r] = sum_{col in split s} D[n][g*Kg + m][i][j] * X[n][g*Cg + c][i*sh - ph + u][j*sw - pw + v]

@@ -228,6 +228,21 @@ def test_split_k(case, splits, blocked, overrides):
     run_case(*case, relu=False, bias=False, seed=1)
 
 
+@pytest.mark.parametrize("case", SPLIT_CASES)
+@pytest.mark.parametrize("splits,units", [(2, 1), (3, 2)])
+def test_tail_split(case, splits, units, overrides):
+    """Tail splits (the last column tiles of the last group cut into
+    reduction ranges, their partials finished by a reduce over that region),
+    forced by the profiling overrides as if the device had `units` compute
+    units: the forward and data gradient match the oracle with and without
+    bias, ReLU and the blocked order."""
+    overrides.setenv("CAFFE_CONV_TAIL_SPLITS", str(splits))
+    overrides.setenv("CAFFE_CONV_TAIL_UNITS", str(units))
+    run_case(*case, relu=True, bias=True)
+    overrides.setenv("CAFFE_CONV_BLOCKED", "0")
+    run_case(*case, relu=False, bias=False, seed=1)
+
+
 def test_split_k_masked_bottom_and_default_plan(overrides):
     # the bottom mask applied by the data-gradient reduce; then a shape whose
     # own plan splits (one image, a long reduction)

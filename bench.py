@@ -111,11 +111,21 @@ def timed_steps(step, stream, steps, net=None):
         return ms, wall, None, None
     acc, spans = {}, []
     evs, net.events = net.events, None
-    for i in range(0, len(evs), 2):
-        (tb, eb), (te, ee) = evs[i], evs[i + 1]
-        assert tb[:2] == te[:2] and tb[2] == "begin" and te[2] == "end"
-        acc.setdefault(tb[:2], []).append(eb.elapsed_time(ee))
-        spans.append((start.elapsed_time(eb), start.elapsed_time(ee)))
+    # a call's span runs from its "begin" event to the latest of its "end"
+    # events (one per stream its work is ordered on)
+    calls, open_ = [], {}
+    for tag, ev in evs:
+        if tag[2] == "begin":
+            open_[tag[:2]] = [tag[:2], ev, []]
+            calls.append(open_[tag[:2]])
+        else:
+            open_[tag[:2]][2].append(ev)
+    for key, eb, ends in calls:
+        assert ends, key
+        d = max(eb.elapsed_time(ee) for ee in ends)
+        acc.setdefault(key, []).append(d)
+        b0 = start.elapsed_time(eb)
+        spans.append((b0, b0 + d))
     covered, reach = 0.0, float("-inf")
     for b0, b1 in sorted(spans):
         if b1 > reach:

@@ -211,6 +211,26 @@ int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, cons
                         float* weight_diff, float* bias_diff, int32_t accumulate, int32_t flags,
                         void* workspace, size_t ws_bytes, void* stream);
 
+/* caffe_conv_backward with the weight-side outputs (weight_diff and
+ * bias_diff) ordered on weight_stream instead of `stream` (the same call
+ * when the two are equal).  weight_stream first waits for all work enqueued
+ * on `stream` before the call, then, in the bf16 modes, for the top-gradient
+ * staging the call enqueues there, and takes the weight and bias gradients
+ * while `stream` goes on with the data gradient (bottom_diff, ordered on
+ * `stream`); nothing joins the two streams, so a network can run one
+ * layer's weight gradient beside the next layers' data gradients and glue.
+ * In CAFFE_F32 mode both passes share the workspace's partial sums and run
+ * on `stream`, which weight_stream then waits for.  The workspace stays in
+ * use until both streams have passed the call's work; the caller joins the
+ * streams before reusing it or reading weight_diff on `stream`.  The
+ * default-priority stream rule of the backward's auxiliary stream applies
+ * to weight_stream as well. */
+int caffe_conv_backward_ex(const caffe_conv_desc* desc, const float* top_diff, const float* top,
+                           const void* bottom, const void* weight, float* bottom_diff,
+                           float* weight_diff, float* bias_diff, int32_t accumulate,
+                           int32_t flags, void* workspace, size_t ws_bytes, void* stream,
+                           void* weight_stream);
+
 /* Static name of a status code ("CAFFE_OK", ...). */
 const char* caffe_status_string(int32_t status);
 

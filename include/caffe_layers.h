@@ -130,6 +130,19 @@ int caffe_conv_backward_pool_lrn(const caffe_conv_desc* desc, const caffe_pool_d
                                  float* bias_diff, int32_t accumulate, int32_t flags,
                                  void* workspace, size_t ws_bytes, void* stream);
 
+/* caffe_conv_backward_pool_lrn with the weight-side outputs ordered on
+ * weight_stream, as caffe_conv_backward_ex (caffe_conv.h) describes: the
+ * glue's backward and the data gradient on `stream`, the weight and bias
+ * gradients on weight_stream after the staging, the streams not joined. */
+int caffe_conv_backward_pool_lrn_ex(const caffe_conv_desc* desc, const caffe_pool_desc* pool,
+                                    const caffe_lrn_desc* lrn, const float* pooled,
+                                    const float* lrn_top, const float* lrn_top_diff,
+                                    const int32_t* pool_mask, const float* top,
+                                    const void* bottom, const void* weight, float* bottom_diff,
+                                    float* weight_diff, float* bias_diff, int32_t accumulate,
+                                    int32_t flags, void* workspace, size_t ws_bytes, void* stream,
+                                    void* weight_stream);
+
 /* The backward pass of a rectified-linear layer (Sec. 3.2 lists ReLU among
  * Caffe's layers): bottom_diff[i] = top[i] > 0 ? top_diff[i] : 0 for
  * i < count, where top is the layer's forward output (a NaN top gives 0).

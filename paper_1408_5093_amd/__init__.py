@@ -116,17 +116,22 @@ def caffe_conv_forward(desc, bottom, weight, bias, top, workspace=None, stream=N
 
 
 def caffe_conv_backward(desc, top_diff, top, bottom, weight, bottom_diff, weight_diff, bias_diff,
-                        accumulate=0, flags=0, workspace=None, stream=None):
+                        accumulate=0, flags=0, workspace=None, stream=None, weight_stream=None):
+    """caffe_conv_backward, or with weight_stream caffe_conv_backward_ex (the
+    weight and bias gradients ordered on that stream, not joined)."""
     t = _op_dtype(desc)
     for x, n in ((top_diff, "top_diff"), (top, "top"), (bottom_diff, "bottom_diff"),
                  (weight_diff, "weight_diff"), (bias_diff, "bias_diff")):
         _dev(x, n, torch.float32)
     _dev(bottom, "bottom", _bottom_dtype(desc)), _dev(weight, "weight", t)
     ws_bytes = 0 if workspace is None else workspace.numel()
-    check(load().caffe_conv_backward(ctypes.byref(desc), _ptr(top_diff), _ptr(top), _ptr(bottom),
-                                     _ptr(weight), _ptr(bottom_diff), _ptr(weight_diff),
-                                     _ptr(bias_diff), int(accumulate), int(flags), _ptr(workspace),
-                                     ws_bytes, _stream(stream)))
+    args = (ctypes.byref(desc), _ptr(top_diff), _ptr(top), _ptr(bottom), _ptr(weight),
+            _ptr(bottom_diff), _ptr(weight_diff), _ptr(bias_diff), int(accumulate), int(flags),
+            _ptr(workspace), ws_bytes, _stream(stream))
+    if weight_stream is None:
+        check(load().caffe_conv_backward(*args))
+    else:
+        check(load().caffe_conv_backward_ex(*args, _stream(weight_stream)))
 
 
 def caffe_conv_backward_data(desc, top_diff, top, weight, bottom_diff, workspace=None, stream=None):
@@ -331,9 +336,11 @@ def lrn_pool_backward(x_shape, pooled, top, top_diff, mask, kernel, stride, pad=
 
 def caffe_conv_backward_pool_lrn(desc, pool, lrn, pooled, lrn_top, lrn_top_diff, pool_mask, top,
                                  bottom, weight, bottom_diff, weight_diff, bias_diff,
-                                 accumulate=0, flags=0, workspace=None, stream=None):
+                                 accumulate=0, flags=0, workspace=None, stream=None,
+                                 weight_stream=None):
     """caffe_conv_backward_pool_lrn: the layer's backward from the gradient
-    of the LRN that follows its max-pool (pool, lrn: PoolDesc, LrnDesc)."""
+    of the LRN that follows its max-pool (pool, lrn: PoolDesc, LrnDesc); with
+    weight_stream, caffe_conv_backward_pool_lrn_ex."""
     t = _op_dtype(desc)
     for x, n in ((pooled, "pooled"), (lrn_top, "lrn_top"), (lrn_top_diff, "lrn_top_diff"),
                  (top, "top"), (bottom_diff, "bottom_diff"), (weight_diff, "weight_diff"),
@@ -342,11 +349,14 @@ def caffe_conv_backward_pool_lrn(desc, pool, lrn, pooled, lrn_top, lrn_top_diff,
     _dev(pool_mask, "pool_mask", torch.int32)
     _dev(bottom, "bottom", _bottom_dtype(desc)), _dev(weight, "weight", t)
     ws_bytes = 0 if workspace is None else workspace.numel()
-    check(load().caffe_conv_backward_pool_lrn(
-        ctypes.byref(desc), ctypes.byref(pool), ctypes.byref(lrn), _ptr(pooled), _ptr(lrn_top),
-        _ptr(lrn_top_diff), _ptr(pool_mask), _ptr(top), _ptr(bottom), _ptr(weight),
-        _ptr(bottom_diff), _ptr(weight_diff), _ptr(bias_diff), int(accumulate), int(flags),
-        _ptr(workspace), ws_bytes, _stream(stream)))
+    args = (ctypes.byref(desc), ctypes.byref(pool), ctypes.byref(lrn), _ptr(pooled),
+            _ptr(lrn_top), _ptr(lrn_top_diff), _ptr(pool_mask), _ptr(top), _ptr(bottom),
+            _ptr(weight), _ptr(bottom_diff), _ptr(weight_diff), _ptr(bias_diff), int(accumulate),
+            int(flags), _ptr(workspace), ws_bytes, _stream(stream))
+    if weight_stream is None:
+        check(load().caffe_conv_backward_pool_lrn(*args))
+    else:
+        check(load().caffe_conv_backward_pool_lrn_ex(*args, _stream(weight_stream)))
 
 
 def relu_backward(top, top_diff, out=None, stream=None):

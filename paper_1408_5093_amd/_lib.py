@@ -49,7 +49,8 @@ EXPORTS = (
     "caffe_sgd_learning_rate", "caffe_softmax_loss", "caffe_sgd_update",
     "caffe_pool_lrn_forward", "caffe_lrn_pool_backward", "caffe_sgd_update_device_lr",
     "caffe_conv_workspace_bytes", "caffe_conv_status_string", "caffe_conv_forward_noalloc",
-    "caffe_conv_backward_pool_lrn", "caffe_relu_backward",
+    "caffe_conv_backward_pool_lrn", "caffe_relu_backward", "caffe_conv_backward_ex",
+    "caffe_conv_backward_pool_lrn_ex",
 )
 
 
@@ -109,6 +110,7 @@ def load():
         "caffe_conv_backward_data": [cdp, vp, vp, vp, vp, vp, sz, vp],
         "caffe_conv_backward_weights": [cdp, vp, vp, vp, vp, vp, i32, vp, sz, vp],
         "caffe_conv_backward": [cdp, vp, vp, vp, vp, vp, vp, vp, i32, i32, vp, sz, vp],
+        "caffe_conv_backward_ex": [cdp, vp, vp, vp, vp, vp, vp, vp, i32, i32, vp, sz, vp, vp],
         "caffe_pool_out_shape": [pdp, pi32, pi32],
         "caffe_maxpool_forward": [pdp, vp, vp, vp, i32, vp],
         "caffe_maxpool_backward": [pdp, vp, vp, vp, vp],
@@ -120,6 +122,8 @@ def load():
         "caffe_lrn_pool_backward": [pdp, ldp, vp, vp, vp, vp, vp, vp],
         "caffe_conv_backward_pool_lrn": [cdp, pdp, ldp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                          i32, i32, vp, sz, vp],
+        "caffe_conv_backward_pool_lrn_ex": [cdp, pdp, ldp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                            vp, i32, i32, vp, sz, vp, vp],
         "caffe_sgd_learning_rate": [ctypes.POINTER(LrSchedule), i64,
                                     ctypes.POINTER(ctypes.c_float)],
         "caffe_softmax_loss": [vp, vp, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp],

@@ -1229,20 +1229,37 @@ int join_side(hipStream_t s, Fork& f, int st_a, int st_b)
     return CAFFE_OK;
 }
 
+// Work enqueued on `follower` after this call follows everything enqueued on
+// `s` so far.
+int stream_follow(hipStream_t follower, hipStream_t s)
+{
+    hipEvent_t ev = nullptr;
+    hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+    if (e == hipSuccess) {
+        e = hipEventRecord(ev, s);
+        if (e == hipSuccess)
+            e = hipStreamWaitEvent(follower, ev, 0);
+        hipEventDestroy(ev);
+    }
+    if (e != hipSuccess)
+        return hip_fail(e, "stream ordering");
+    return CAFFE_OK;
+}
+
 int backward_bf16_staged(const ConvPlan& q, const float* sums, int terms, bool mask_bottom,
                          bool staged, const void* bottom, const void* weight, float* bottom_diff,
                          float* weight_diff, float* bias_diff, int accumulate, char* ws,
-                         hipStream_t s);
+                         hipStream_t s, hipStream_t wst);
 
 int backward_bf16(const ConvPlan& q, const float* top_diff, const float* top, bool masked,
                   bool mask_bottom, bool staged, const void* bottom, const void* weight,
                   float* bottom_diff, float* weight_diff, float* bias_diff, int accumulate,
-                  char* ws, hipStream_t s)
+                  char* ws, hipStream_t s, hipStream_t wst)
 {
     if (!bottom_diff && !weight_diff) {
         if (bias_diff)
-            return run_bias_only(q, top_diff, top, masked, bias_diff, accumulate, ws, s);
-        return CAFFE_OK;
+            CHECK(run_bias_only(q, top_diff, top, masked, bias_diff, accumulate, ws, s));
+        return wst ? stream_follow(wst, s) : CAFFE_OK;
     }
     uint16_t* dh = (uint16_t*)(ws + q.off_dh);
     float* sums = (float*)(ws + q.off_sums);
@@ -1254,7 +1271,7 @@ int backward_bf16(const ConvPlan& q, const float* top_diff, const float* top, bo
            "bf16 top-gradient staging launch");
     return backward_bf16_staged(q, sums, diff_prep_terms(q.N, q.DHp * q.DWp), mask_bottom, staged,
                                 bottom, weight, bottom_diff, weight_diff, bias_diff, accumulate, ws,
-                                s);
+                                s, wst);
 }
 
 // The bf16 backward once the top gradient is staged at off_dh and its
@@ -1262,9 +1279,24 @@ int backward_bf16(const ConvPlan& q, const float* top_diff, const float* top, bo
 int backward_bf16_staged(const ConvPlan& q, const float* sums, int terms, bool mask_bottom,
                          bool staged, const void* bottom, const void* weight, float* bottom_diff,
                          float* weight_diff, float* bias_diff, int accumulate, char* ws,
-                         hipStream_t s)
+                         hipStream_t s, hipStream_t wst)
 {
     const uint16_t* dh = (const uint16_t*)(ws + q.off_dh);
+    if (wst) {
+        // the caller's weight stream takes the weight and bias gradients
+        // once the staging on s is done, and nothing joins it here (the two
+        // passes use disjoint workspace regions, as in the fork below)
+        CHECK(stream_follow(wst, s));
+        if (bottom_diff)
+            CHECK(run_data_bf16(q, dh, mask_bottom ? bottom : nullptr, weight, bottom_diff, ws,
+                                s));
+        if (weight_diff)
+            CHECK(run_weights_bf16(q, dh, bottom, staged, weight_diff, accumulate, ws, wst));
+        if (bias_diff)
+            LAUNCH(launch_bias_reduce(sums, bias_diff, terms, q.K, accumulate, wst),
+                   "bias reduce launch");
+        return CAFFE_OK;
+    }
     Fork f;
     if (bottom_diff && weight_diff && fork_side(s, &f)) {
         // (disjoint workspace regions: Wt for the data gradient; the staged
@@ -1393,6 +1425,17 @@ int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, cons
                         float* weight_diff, float* bias_diff, int32_t accumulate, int32_t flags,
                         void* workspace, size_t ws_bytes, void* stream)
 {
+    return caffe_conv_backward_ex(desc, top_diff, top, bottom, weight, bottom_diff, weight_diff,
+                                  bias_diff, accumulate, flags, workspace, ws_bytes, stream,
+                                  stream);
+}
+
+int caffe_conv_backward_ex(const caffe_conv_desc* desc, const float* top_diff, const float* top,
+                           const void* bottom, const void* weight, float* bottom_diff,
+                           float* weight_diff, float* bias_diff, int32_t accumulate,
+                           int32_t flags, void* workspace, size_t ws_bytes, void* stream,
+                           void* weight_stream)
+{
     ConvPlan q;
     CHECK(plan_conv(desc, &q));
     if (accumulate != 0 && accumulate != 1)
@@ -1418,14 +1461,18 @@ int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, cons
                                                    : std::min(q.ws_data, q.ws_weights);
     CHECK(check_ws(workspace, ws_bytes, need));
     hipStream_t s = (hipStream_t)stream;
+    // a weight stream other than `stream` takes the weight-side outputs
+    hipStream_t wst = weight_stream != stream ? (hipStream_t)weight_stream : nullptr;
     char* ws = (char*)workspace;
     if (is_bf16(q))
         return backward_bf16(q, top_diff, top, masked, mask_bottom, staged, bottom, weight,
-                             bottom_diff, weight_diff, bias_diff, accumulate, ws, s);
-    if (q.dense)
-        return backward_dense(q, top_diff, top, masked, mask_bottom, (const float*)bottom,
-                              (const float*)weight, bottom_diff, weight_diff, bias_diff,
-                              accumulate, ws, s);
+                             bottom_diff, weight_diff, bias_diff, accumulate, ws, s, wst);
+    if (q.dense) {
+        CHECK(backward_dense(q, top_diff, top, masked, mask_bottom, (const float*)bottom,
+                             (const float*)weight, bottom_diff, weight_diff, bias_diff,
+                             accumulate, ws, s));
+        return wst ? stream_follow(wst, s) : CAFFE_OK;
+    }
     const float* dsrc = top_diff;
     if (q.relu && !masked && (bottom_diff || weight_diff) && q.top_elems > 0) {
         // D = top_diff [top > 0], shared by both gradients
@@ -1441,7 +1488,9 @@ int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, cons
         CHECK(run_weights(q, dsrc, bottom, weight_diff, bias_diff, accumulate, ws, s));
     else if (bias_diff)
         CHECK(run_bias_only(q, top_diff, top, masked, bias_diff, accumulate, ws, s));
-    return CAFFE_OK;
+    // (fp32: both passes share the workspace's partial-sum region, so they
+    // run in turn on `stream`)
+    return wst ? stream_follow(wst, s) : CAFFE_OK;
 }
 
 int caffe_conv_backward_data(const caffe_conv_desc* desc, const float* top_diff, const float* top,
@@ -1476,6 +1525,21 @@ int caffe_conv_backward_pool_lrn(const caffe_conv_desc* desc, const caffe_pool_d
                                  const void* weight, float* bottom_diff, float* weight_diff,
                                  float* bias_diff, int32_t accumulate, int32_t flags,
                                  void* workspace, size_t ws_bytes, void* stream)
+{
+    return caffe_conv_backward_pool_lrn_ex(desc, pool, lrn, pooled, lrn_top, lrn_top_diff,
+                                           pool_mask, top, bottom, weight, bottom_diff,
+                                           weight_diff, bias_diff, accumulate, flags, workspace,
+                                           ws_bytes, stream, stream);
+}
+
+int caffe_conv_backward_pool_lrn_ex(const caffe_conv_desc* desc, const caffe_pool_desc* pool,
+                                    const caffe_lrn_desc* lrn, const float* pooled,
+                                    const float* lrn_top, const float* lrn_top_diff,
+                                    const int32_t* pool_mask, const float* top,
+                                    const void* bottom, const void* weight, float* bottom_diff,
+                                    float* weight_diff, float* bias_diff, int32_t accumulate,
+                                    int32_t flags, void* workspace, size_t ws_bytes, void* stream,
+                                    void* weight_stream)
 {
     ConvPlan q;
     CHECK(plan_conv(desc, &q));
@@ -1515,15 +1579,17 @@ int caffe_conv_backward_pool_lrn(const caffe_conv_desc* desc, const caffe_pool_d
                                         pool->stride_h, pool->stride_w, pool->pad_h, pool->pad_w,
                                         lrn->local_size, lrn->alpha, lrn->beta, lrn->k, s),
                "fused LRN + pool backward launch");
-        return caffe_conv_backward(desc, gbuf, top, bottom, weight, bottom_diff, weight_diff,
-                                   bias_diff, accumulate, flags, workspace, q.ws_both, stream);
+        return caffe_conv_backward_ex(desc, gbuf, top, bottom, weight, bottom_diff, weight_diff,
+                                      bias_diff, accumulate, flags, workspace, q.ws_both, stream,
+                                      weight_stream);
     }
+    hipStream_t wst = weight_stream != stream ? (hipStream_t)weight_stream : nullptr;
     if (q.N == 0) {
         if (bias_diff && !accumulate)
             LAUNCH(launch_fill_zero(bias_diff, q.K, s), "zero fill launch");
         if (weight_diff && !accumulate)
             LAUNCH(launch_fill_zero(weight_diff, q.weight_elems, s), "zero fill launch");
-        return CAFFE_OK;
+        return wst ? stream_follow(wst, s) : CAFFE_OK;
     }
     // the glue's backward written straight into the bf16 top-gradient
     // staging, with its bias-gradient partials
@@ -1539,7 +1605,7 @@ int caffe_conv_backward_pool_lrn(const caffe_conv_desc* desc, const caffe_pool_d
                                                 pool->pad_h);
     return backward_bf16_staged(q, sums, q.N * strips, mask_bottom,
                                 (flags & CAFFE_BACKWARD_BOTTOM_STAGED) != 0, bottom, weight,
-                                bottom_diff, weight_diff, bias_diff, accumulate, ws, s);
+                                bottom_diff, weight_diff, bias_diff, accumulate, ws, s, wst);
 }
 
 const char* caffe_status_string(int32_t status)

@@ -104,11 +104,16 @@ class ConvStack:
         # N=256: 9.80 -> 9.39 ms per step).  A layer whose top gradient
         # arrives unmasked (the top layer) runs its ReLU's backward as a pass
         # of its own first, so that both calls take the masked gradient.
-        # bf16 keeps one call: both passes read the top gradient it stages
-        # once.
+        # bf16 keeps one call per layer (both passes read the top gradient it
+        # stages once) and hands the call the side stream for the weight
+        # side (caffe_conv_backward_ex): the weight and bias gradients run
+        # there, not joined per layer, beside the next layers' staging, glue
+        # and data gradients.
         self.split_backward = split_backward and not bf16
-        if self.split_backward:
+        self.weight_side = split_backward and bf16
+        if self.split_backward or self.weight_side:
             self.side = torch.cuda.Stream(device=dev)
+        if self.split_backward:
             self.ws_side = Workspace(dev).get(max(ws_weights, 1))
         # serial = True keeps the separate data- and weight-gradient calls but
         # issues both on the caller's stream (measurement: each call then has
@@ -217,15 +222,17 @@ class ConvStack:
         (dbottom[0] only when data_grad_bottom)."""
         s = stream or torch.cuda.current_stream()
         # (a captured graph keeps to one stream)
-        split = self.split_backward and not torch.cuda.is_current_stream_capturing()
-        if split:
+        capturing = torch.cuda.is_current_stream_capturing()
+        split = self.split_backward and not capturing
+        wside = self.side if self.weight_side and not capturing else None
+        if split or wside is not None:
             self.side.wait_stream(s)
         g = top_diff
         for l in range(len(self.layers) - 1, -1, -1):
             L = self.layers[l]
             g = g.view(self.out_shape[l])
             if self.fuse_staging[l]:
-                g = self._backward_pool_lrn(l, g, s, l > 0 or data_grad_bottom)
+                g = self._backward_pool_lrn(l, g, s, l > 0 or data_grad_bottom, wside)
                 continue
             if self.fused[l]:
                 pst, lst = self.stages[l]
@@ -279,15 +286,17 @@ class ConvStack:
                 self._mark((tag, l, "begin"), s)
                 caffe_conv_backward(self.descs[l], g, top, bottom, self.W[l],
                                     self.dbottom[l] if want_dx else None, self.dW[l], self.db[l],
-                                    0, flags, self.ws_of[l], s)
+                                    0, flags, self.ws_of[l], s, weight_stream=wside)
                 self._mark((tag, l, "end"), s)
+                if wside is not None:  # (the call ends with the later of the two)
+                    self._mark((tag, l, "end"), wside)
             g = self.dbottom[l]
-        if split:
+        if split or wside is not None:
             # the next forward overwrites what the side stream reads
             s.wait_stream(self.side)
         return self.dbottom[0]
 
-    def _backward_pool_lrn(self, l, g, s, want_dx):
+    def _backward_pool_lrn(self, l, g, s, want_dx, wside=None):
         """Layer l's backward from the gradient g of the LRN after its max-pool
         (one call: the glue's backward staged as the bf16 top gradient)."""
         pst, lst = self.stages[l]
@@ -302,8 +311,11 @@ class ConvStack:
                                      lst["y"], g, pst["mask"], self.top[l] if L.relu else None,
                                      self.bottom[l], self.W[l],
                                      self.dbottom[l] if want_dx else None, self.dW[l],
-                                     self.db[l], 0, flags, self.ws_of[l], s)
+                                     self.db[l], 0, flags, self.ws_of[l], s,
+                                     weight_stream=wside)
         self._mark(("both" if want_dx else "wgt", l, "end"), s)
+        if wside is not None:  # (the call ends with the later of the two)
+            self._mark(("both" if want_dx else "wgt", l, "end"), wside)
         return self.dbottom[l]
 
     def layer_top_diff(self, l, top_diff_last):

@@ -274,6 +274,67 @@ def test_backward_side_stream_fork_bf16(overrides):
             assert torch.equal(u, v)
 
 
+@pytest.mark.parametrize("bf16", [True, False])
+def test_backward_weight_stream(bf16):
+    """caffe_conv_backward_ex: the weight and bias gradients ordered on a
+    second stream of the caller's, not joined -- bitwise the gradients of
+    caffe_conv_backward, over three calls in a row on one workspace with the
+    streams joined only at the end."""
+    rng = np.random.default_rng(89)
+    N, C, H, W, K, g = 3, 16, 11, 12, 40, 2
+    op = torch.bfloat16 if bf16 else torch.float32
+    x = _t(rng.standard_normal((N, C, H, W)), op)
+    w = _t(rng.standard_normal((K, C // g, 3, 3)) * 0.3, op)
+    y = cc.conv_forward(x, w, _t(rng.standard_normal(K)), 1, 1, g, True)
+    d = cc.conv_desc(x.shape, w.shape, 1, 1, g, True, cc.CAFFE_BF16 if bf16 else cc.CAFFE_F32)
+    gds = [_t(rng.standard_normal(y.shape)) for _ in range(3)]
+    ws = cc.Workspace().get(cc.conv_workspace_size(d, cc.PASS_BACKWARD))
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    outs = {}
+    for mode in ("one", "two"):
+        res = []
+        for gd in gds:
+            dx = torch.empty(x.shape, device=DEV)
+            dw = torch.empty(w.shape, device=DEV)
+            db = torch.empty(K, device=DEV)
+            if mode == "two":
+                # (the workspace is reused: the previous call's weight side first)
+                main.wait_stream(side)
+            cc.caffe_conv_backward(d, gd, y, x, w, dx, dw, db, 0, 0, ws,
+                                   weight_stream=side if mode == "two" else None)
+            res.append((dx, dw, db))
+        main.wait_stream(side)
+        torch.cuda.synchronize()
+        outs[mode] = res
+    for a, b in zip(outs["one"], outs["two"]):
+        for u, v in zip(a, b):
+            assert torch.equal(u, v)
+
+
+def test_caffenet_bf16_step_weight_stream_matches():
+    """The bf16 step at N=512 with every layer's weight and bias gradients
+    on the network's second stream (the default) against the one-stream step:
+    every gradient bit for bit, over two steps."""
+    N = 512
+    inp = wl.caffenet_step(N, wl.CAFFENET_STEP_BF16)
+    x = torch.from_numpy(inp["x"]).to(DEV)
+    g = torch.from_numpy(inp["top_diff"]).to(DEV)
+    nets = [ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(), bf16=True,
+                      split_backward=f) for f in (True, False)]
+    assert nets[0].weight_side and not nets[1].weight_side
+    for _ in range(2):
+        for net in nets:
+            net.forward(x)
+            net.backward(g)
+        torch.cuda.synchronize()
+        a, b = nets
+        for l in range(len(wl.CAFFENET)):
+            assert torch.equal(a.dbottom[l], b.dbottom[l]), f"layer {l} data gradient"
+            assert torch.equal(a.dW[l], b.dW[l]), f"layer {l} weight gradient"
+            assert torch.equal(a.db[l], b.db[l]), f"layer {l} bias gradient"
+
+
 def test_caffenet_bf16_step_fused_staging_matches():
     """The bf16 step at N=512 with conv1's and conv2's top gradients staged
     by the fused glue backward (the default) against the unfused step: every

@@ -968,12 +968,14 @@ stage_narrow_bf16_kernel(const T* __restrict__ X, bf16_t* __restrict__ Xp, int C
 // bias gradient of that run of the image.
 constexpr int kDiffPrepPixels = 512;
 
+template <bool RELU>
 __global__ void __launch_bounds__(256)
 diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
                       bf16_t* __restrict__ Dh, float* __restrict__ sums, int N, int K, int H,
-                      int W, int Kg, int Kgp, int Ktot, int Hp, int Wp, int tb, int lb, int relu,
+                      int W, int Kg, int Kgp, int Ktot, int Hp, int Wp, int tb, int lb,
                       int ctiles, int runs)
 {
+    constexpr bool relu = RELU;
     __shared__ bf16_t tile[64][66];
     const int run = blockIdx.x % runs;
     const int nc = blockIdx.x / runs;
@@ -990,7 +992,7 @@ diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
     // or a border pixel is an out-of-range offset and reads 0
     const uint32_t gbytes = (uint32_t)((size_t)N * K * plane * 4);
     const __amdgpu_buffer_rsrc_t rg = make_rsrc(G, gbytes);
-    const __amdgpu_buffer_rsrc_t ry = make_rsrc(Y, relu ? gbytes : 0u);
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(Y, RELU ? gbytes : 0u);
     // this thread's 16 channels (cw + 4q): byte offsets of their planes,
     // 2^31 for a channel that does not exist
     uint32_t cb4[16];
@@ -1007,23 +1009,43 @@ diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
 #pragma unroll
     for (int q = 0; q < 16; ++q)
         acc[q] = 0.f;
-    for (int p0 = p_begin; p0 < p_end; p0 += 64) {
+    // the byte offset of this thread's pixel in step p0 (out of range on the
+    // border and past the run)
+    auto step_off = [&](int p0) -> uint32_t {
         const int pix = p0 + px;
         const int hp = pix / Wp;
         const int h = hp - tb;
         const int w = pix - hp * Wp - lb;
         const bool inside = pix < p_end && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
-        const uint32_t off4 = inside ? (uint32_t)(h * W + w) * 4u : 0u;
-        const uint32_t obad = inside ? 0u : kOob;
-        // every load of the step first (the ReLU output too), then the uses
-        float d[16], y[16];
+        return inside ? (uint32_t)(h * W + w) * 4u : kOob;
+    };
+    // Each step's loads go out before the previous step is transposed and
+    // stored (two steps in flight per thread); the ReLU output's too.
+    float d[16], y[16];
+    {
+        const uint32_t o = step_off(p_begin);
 #pragma unroll
         for (int q = 0; q < 16; ++q)
-            d[q] = buf_ld_f32(rg, (cb4[q] + off4) | obad);
-        if (relu) {
+            d[q] = buf_ld_f32(rg, (cb4[q] + o) | (o & kOob));
+        if constexpr (RELU) {
 #pragma unroll
             for (int q = 0; q < 16; ++q)
-                y[q] = buf_ld_f32(ry, (cb4[q] + off4) | obad);
+                y[q] = buf_ld_f32(ry, (cb4[q] + o) | (o & kOob));
+        }
+    }
+    for (int p0 = p_begin; p0 < p_end; p0 += 64) {
+        float dn[16], yn[16];
+        const bool more = p0 + 64 < p_end;
+        if (more) {
+            const uint32_t o = step_off(p0 + 64);
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+                dn[q] = buf_ld_f32(rg, (cb4[q] + o) | (o & kOob));
+            if constexpr (RELU) {
+#pragma unroll
+                for (int q = 0; q < 16; ++q)
+                    yn[q] = buf_ld_f32(ry, (cb4[q] + o) | (o & kOob));
+            }
         }
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
@@ -1050,6 +1072,14 @@ diff_prep_bf16_kernel(const float* __restrict__ G, const float* __restrict__ Y,
             }
         }
         __syncthreads();
+        if (more) {
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                d[q] = dn[q];
+                if constexpr (RELU)
+                    y[q] = yn[q];
+            }
+        }
     }
     if (sums) {
         const size_t T = (size_t)N * runs;
@@ -1368,9 +1398,13 @@ hipError_t launch_diff_prep_bf16(const float* G, const float* Y, uint16_t* Dh, f
         return hipSuccess;
     const int ctiles = (Ktot + 63) / 64;
     const int runs = diff_prep_terms(N, Hp * Wp) / N;
-    hipLaunchKernelGGL(diff_prep_bf16_kernel, dim3((unsigned)((int64_t)ctiles * N * runs)),
-                       dim3(256), 0, s, G, Y, Dh, sums, N, K, H, W, Kg, Kgp, Ktot, Hp, Wp, tb, lb,
-                       relu, ctiles, runs);
+    const dim3 grid((unsigned)((int64_t)ctiles * N * runs));
+    if (relu)
+        hipLaunchKernelGGL(diff_prep_bf16_kernel<true>, grid, dim3(256), 0, s, G, Y, Dh, sums, N,
+                           K, H, W, Kg, Kgp, Ktot, Hp, Wp, tb, lb, ctiles, runs);
+    else
+        hipLaunchKernelGGL(diff_prep_bf16_kernel<false>, grid, dim3(256), 0, s, G, Y, Dh, sums, N,
+                           K, H, W, Kg, Kgp, Ktot, Hp, Wp, tb, lb, ctiles, runs);
     return hipGetLastError();
 }
 

@@ -191,7 +191,13 @@ enum caffe_backward_flags {
      * workspaces.  No effect in CAFFE_F32 mode, which stages nothing; a
      * workspace that does not hold the forward's copy gives a wrong
      * weight gradient. */
-    CAFFE_BACKWARD_BOTTOM_STAGED = 4
+    CAFFE_BACKWARD_BOTTOM_STAGED = 4,
+    /* bf16 modes: the workspace holds this layer's staged top gradient and
+     * its bias-gradient partial sums, written by the layer above's
+     * caffe_conv_backward_into (which named this descriptor and workspace
+     * as `below`); top_diff is not read (it may be NULL) and counts as
+     * masked.  CAFFE_ERR_INVALID_ARG in CAFFE_F32 mode. */
+    CAFFE_BACKWARD_TOP_STAGED = 16
 };
 
 /* The whole backward pass of the layer in one call: the ReLU mask is applied
@@ -230,6 +236,33 @@ int caffe_conv_backward_ex(const caffe_conv_desc* desc, const float* top_diff, c
                            float* weight_diff, float* bias_diff, int32_t accumulate,
                            int32_t flags, void* workspace, size_t ws_bytes, void* stream,
                            void* weight_stream);
+
+/* caffe_conv_backward_ex whose data gradient is not stored as a float
+ * bottom_diff but written, rounded to bf16 (nearest even), as the staged top
+ * gradient of the convolution `below` -- the layer whose top is this layer's
+ * bottom -- in below's backward workspace (below_workspace, at least
+ * caffe_conv_workspace_size(below, CAFFE_PASS_BACKWARD) bytes), together with
+ * the partial sums below's bias gradient adds up, and with the zero border
+ * below's data gradient gathers from.  With CAFFE_BACKWARD_MASK_BOTTOM_DIFF
+ * the values are masked first, as bottom_diff would be.  below's backward
+ * then takes CAFFE_BACKWARD_TOP_STAGED (on a stream ordered after `stream`)
+ * and reads no float top gradient: the pass that would write, read back and
+ * stage it is gone.  Requirements (else CAFFE_ERR_UNSUPPORTED): bf16 modes
+ * for both layers, stride 1 with the data gradient's grid the image itself,
+ * a multiple of 4 channels per group here and no channel padding in below's
+ * staging (a multiple of 8 channels per group); below's N, K, Ho, Wo must be
+ * this layer's N, C, H, W (CAFFE_ERR_INVALID_ARG). */
+/* 1 when caffe_conv_backward_into can stage desc's data gradient for
+ * `below` (the requirements above), else 0 (also for an invalid descriptor;
+ * caffe_last_error() then says why).  Host-only. */
+int caffe_conv_stage_below_supported(const caffe_conv_desc* desc, const caffe_conv_desc* below);
+
+int caffe_conv_backward_into(const caffe_conv_desc* desc, const float* top_diff, const float* top,
+                             const void* bottom, const void* weight, float* weight_diff,
+                             float* bias_diff, int32_t accumulate, int32_t flags,
+                             void* workspace, size_t ws_bytes, const caffe_conv_desc* below,
+                             void* below_workspace, size_t below_ws_bytes, void* stream,
+                             void* weight_stream);
 
 /* Static name of a status code ("CAFFE_OK", ...). */
 const char* caffe_status_string(int32_t status);

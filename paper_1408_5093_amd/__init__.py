@@ -15,8 +15,8 @@ import torch
 
 from . import _lib
 from ._lib import (  # noqa: F401
-    CAFFE_ERR_UNSUPPORTED, CAFFE_ERR_WORKSPACE, NOALLOC_SCRATCH_BYTES, BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF,
-    BACKWARD_TOP_DIFF_MASKED, CAFFE_BF16, CAFFE_BF16_F32_BOTTOM, CAFFE_F32, CAFFE_LR_EXP,
+    CAFFE_ERR_UNSUPPORTED, CAFFE_ERR_WORKSPACE, NOALLOC_SCRATCH_BYTES, BACKWARD_BOTTOM_STAGED,
+    BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED, BACKWARD_TOP_STAGED, CAFFE_BF16, CAFFE_BF16_F32_BOTTOM, CAFFE_F32, CAFFE_LR_EXP,
     CAFFE_LR_FIXED, CAFFE_LR_INV, CAFFE_LR_STEP, LrSchedule, PASS_BACKWARD,
     PASS_BACKWARD_DATA, PASS_BACKWARD_POOL_LRN, PASS_BACKWARD_WEIGHTS, PASS_FORWARD,
     POOL_RELU_INPUT, CaffeError, ConvDesc,
@@ -29,6 +29,7 @@ __all__ = [
     "lrn_forward", "lrn_backward", "cast_f32_to_bf16", "Workspace", "CaffeError",
     "sgd_learning_rate", "softmax_loss", "sgd_update", "pool_lrn_forward", "lrn_pool_backward",
     "pool_lrn_supported", "caffe_conv_backward_pool_lrn", "relu_backward",
+    "caffe_conv_backward_into", "conv_stage_below_supported",
 ]
 
 
@@ -132,6 +133,30 @@ def caffe_conv_backward(desc, top_diff, top, bottom, weight, bottom_diff, weight
         check(load().caffe_conv_backward(*args))
     else:
         check(load().caffe_conv_backward_ex(*args, _stream(weight_stream)))
+
+
+def caffe_conv_backward_into(desc, top_diff, top, bottom, weight, weight_diff, bias_diff,
+                             accumulate, flags, workspace, below, below_workspace, stream=None,
+                             weight_stream=None):
+    """caffe_conv_backward_into: the data gradient staged as the top gradient
+    of the layer `below` (a ConvDesc) in its workspace."""
+    t = _op_dtype(desc)
+    for x, n in ((top_diff, "top_diff"), (top, "top"), (weight_diff, "weight_diff"),
+                 (bias_diff, "bias_diff")):
+        _dev(x, n, torch.float32)
+    _dev(bottom, "bottom", _bottom_dtype(desc)), _dev(weight, "weight", t)
+    ws_bytes = 0 if workspace is None else workspace.numel()
+    bws_bytes = 0 if below_workspace is None else below_workspace.numel()
+    check(load().caffe_conv_backward_into(
+        ctypes.byref(desc), _ptr(top_diff), _ptr(top), _ptr(bottom), _ptr(weight),
+        _ptr(weight_diff), _ptr(bias_diff), int(accumulate), int(flags), _ptr(workspace),
+        ws_bytes, ctypes.byref(below), _ptr(below_workspace), bws_bytes, _stream(stream),
+        _stream(weight_stream if weight_stream is not None else stream)))
+
+
+def conv_stage_below_supported(desc, below):
+    """Whether caffe_conv_backward_into can stage desc's data gradient for below."""
+    return bool(load().caffe_conv_stage_below_supported(ctypes.byref(desc), ctypes.byref(below)))
 
 
 def caffe_conv_backward_data(desc, top_diff, top, weight, bottom_diff, workspace=None, stream=None):

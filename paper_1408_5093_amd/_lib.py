@@ -24,6 +24,7 @@ CAFFE_BF16_F32_BOTTOM = 2
 BACKWARD_TOP_DIFF_MASKED = 1
 BACKWARD_MASK_BOTTOM_DIFF = 2
 BACKWARD_BOTTOM_STAGED = 4
+BACKWARD_TOP_STAGED = 16
 POOL_RELU_INPUT = 1
 
 PASS_FORWARD = 0
@@ -50,7 +51,8 @@ EXPORTS = (
     "caffe_pool_lrn_forward", "caffe_lrn_pool_backward", "caffe_sgd_update_device_lr",
     "caffe_conv_workspace_bytes", "caffe_conv_status_string", "caffe_conv_forward_noalloc",
     "caffe_conv_backward_pool_lrn", "caffe_relu_backward", "caffe_conv_backward_ex",
-    "caffe_conv_backward_pool_lrn_ex",
+    "caffe_conv_backward_pool_lrn_ex", "caffe_conv_backward_into",
+    "caffe_conv_stage_below_supported",
 )
 
 
@@ -111,6 +113,9 @@ def load():
         "caffe_conv_backward_weights": [cdp, vp, vp, vp, vp, vp, i32, vp, sz, vp],
         "caffe_conv_backward": [cdp, vp, vp, vp, vp, vp, vp, vp, i32, i32, vp, sz, vp],
         "caffe_conv_backward_ex": [cdp, vp, vp, vp, vp, vp, vp, vp, i32, i32, vp, sz, vp, vp],
+        "caffe_conv_backward_into": [cdp, vp, vp, vp, vp, vp, vp, i32, i32, vp, sz, cdp, vp, sz,
+                                     vp, vp],
+        "caffe_conv_stage_below_supported": [cdp, cdp],
         "caffe_pool_out_shape": [pdp, pi32, pi32],
         "caffe_maxpool_forward": [pdp, vp, vp, vp, i32, vp],
         "caffe_maxpool_backward": [pdp, vp, vp, vp, vp],

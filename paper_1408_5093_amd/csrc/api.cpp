@@ -99,6 +99,15 @@ struct ConvPlan {
     // (data gradient)
     int fwd_splits, fwd_sps, dgrad_splits, dgrad_sps;
     size_t off_fwd_part;
+    // bf16 data gradient written as the staged top gradient of the layer
+    // below (caffe_conv_backward_into), else null
+    struct StageTarget {
+        uint16_t* Sh;
+        float* Ssum;
+        uint32_t Sh_bytes, Ssum_bytes;
+        int Hp, Wp, tb, lb, Ktot, T;
+    };
+    const StageTarget* below;
     // tail splits of the forward and data-gradient GEMMs (splits 1: none):
     // the tiles from T on cut into `splits` reduction ranges of sps stages,
     // their partials at the split partials' offset
@@ -469,7 +478,10 @@ int plan_bf16(ConvPlan* p)
     q.ws_fwd = q.off_wp_fwd + align_up(wp, kWsAlign);
     // bias-gradient partials of the top-gradient staging (and room for the
     // per-image sums of the bias-only pass)
-    const int64_t terms = std::max<int64_t>(diff_prep_terms(q.N, q.DHp * q.DWp), q.N);
+    // (or the partial sums a layer above stages with its data gradient)
+    const int64_t terms =
+        std::max<int64_t>(std::max<int64_t>(diff_prep_terms(q.N, q.DHp * q.DWp), q.N),
+                          stage_below_terms((int64_t)q.N * q.Ho * q.Wo));
     const size_t sums_bytes = align_up((size_t)terms * q.K * 4, kWsAlign);
     if ((int64_t)sums_bytes > kMaxTensorBytes)
         return fail(CAFFE_ERR_UNSUPPORTED, "bias partials reach 2^31 bytes");
@@ -1090,6 +1102,10 @@ int run_data_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom_mask
 {
     if (q.bottom_elems == 0)
         return CAFFE_OK;
+    if (q.below)  // its border first (the epilogue writes the image's pixels)
+        LAUNCH(launch_dh_zero_border(q.below->Sh, q.N, q.below->Hp, q.below->Wp, q.below->tb,
+                                     q.below->lb, q.H, q.W, q.below->Ktot, s),
+               "staging border launch");
     uint16_t* wt = (uint16_t*)(ws + q.off_wt);
     LAUNCH(launch_dgrad_weights_bf16((const uint16_t*)weight, wt, q.G, q.Kg, q.Kgp, q.Cg, q.kh,
                                      q.kw, q.sh, q.sw, q.Th, q.Tw, q.Rtp, s),
@@ -1117,6 +1133,16 @@ int run_data_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom_mask
     p.xcd_order = q.xcd_order;
     p.div_ohw = make_fastdiv((uint32_t)(q.Ah * q.Aw)); p.div_ow = make_fastdiv((uint32_t)q.Aw);
     p.div_pss = make_fastdiv((uint32_t)(q.sh * q.sw)); p.div_psw = make_fastdiv((uint32_t)q.sw);
+    if (q.below) {
+        const ConvPlan::StageTarget& b = *q.below;
+        p.Y = nullptr;
+        p.Sh = b.Sh; p.Ssum = b.Ssum; p.Sh_bytes = b.Sh_bytes; p.Ssum_bytes = b.Ssum_bytes;
+        p.s_Hp = b.Hp; p.s_Wp = b.Wp; p.s_tb = b.tb; p.s_lb = b.lb; p.s_Ktot = b.Ktot;
+        p.s_T = b.T;
+        LAUNCH(launch_conv_gemm_bf16(p, 2, q.dgrad_tile, q.dgrad_pipe, s),
+               "bf16 data-gradient staging launch");
+        return CAFFE_OK;
+    }
     LAUNCH(launch_conv_gemm_bf16(p, 1, q.dgrad_tile, q.dgrad_pipe, s),
            "bf16 data-gradient launch");
     return CAFFE_OK;
@@ -1252,17 +1278,25 @@ int backward_bf16_staged(const ConvPlan& q, const float* sums, int terms, bool m
                          hipStream_t s, hipStream_t wst);
 
 int backward_bf16(const ConvPlan& q, const float* top_diff, const float* top, bool masked,
-                  bool mask_bottom, bool staged, const void* bottom, const void* weight,
-                  float* bottom_diff, float* weight_diff, float* bias_diff, int accumulate,
-                  char* ws, hipStream_t s, hipStream_t wst)
+                  bool top_staged, bool mask_bottom, bool staged, const void* bottom,
+                  const void* weight, float* bottom_diff, float* weight_diff, float* bias_diff,
+                  int accumulate, char* ws, hipStream_t s, hipStream_t wst)
 {
-    if (!bottom_diff && !weight_diff) {
-        if (bias_diff)
+    float* sums = (float*)(ws + q.off_sums);
+    // the top gradient and its bias partials staged by the layer above
+    const int staged_terms = stage_below_terms((int64_t)q.N * q.Ho * q.Wo);
+    if (!bottom_diff && !weight_diff && !q.below) {
+        if (bias_diff && top_staged)
+            LAUNCH(launch_bias_reduce(sums, bias_diff, staged_terms, q.K, accumulate, s),
+                   "bias reduce launch");
+        else if (bias_diff)
             CHECK(run_bias_only(q, top_diff, top, masked, bias_diff, accumulate, ws, s));
         return wst ? stream_follow(wst, s) : CAFFE_OK;
     }
+    if (top_staged)
+        return backward_bf16_staged(q, sums, staged_terms, mask_bottom, staged, bottom, weight,
+                                    bottom_diff, weight_diff, bias_diff, accumulate, ws, s, wst);
     uint16_t* dh = (uint16_t*)(ws + q.off_dh);
-    float* sums = (float*)(ws + q.off_sums);
     // D = bf16(top_diff [top > 0]) staged channel-contiguous; the fp32 plane
     // sums give the bias gradient
     LAUNCH(launch_diff_prep_bf16(top_diff, top, dh, bias_diff ? sums : nullptr, q.N, q.K, q.Ho,
@@ -1282,12 +1316,13 @@ int backward_bf16_staged(const ConvPlan& q, const float* sums, int terms, bool m
                          hipStream_t s, hipStream_t wst)
 {
     const uint16_t* dh = (const uint16_t*)(ws + q.off_dh);
+    const bool want_data = bottom_diff || q.below;
     if (wst) {
         // the caller's weight stream takes the weight and bias gradients
         // once the staging on s is done, and nothing joins it here (the two
         // passes use disjoint workspace regions, as in the fork below)
         CHECK(stream_follow(wst, s));
-        if (bottom_diff)
+        if (want_data)
             CHECK(run_data_bf16(q, dh, mask_bottom ? bottom : nullptr, weight, bottom_diff, ws,
                                 s));
         if (weight_diff)
@@ -1298,7 +1333,7 @@ int backward_bf16_staged(const ConvPlan& q, const float* sums, int terms, bool m
         return CAFFE_OK;
     }
     Fork f;
-    if (bottom_diff && weight_diff && fork_side(s, &f)) {
+    if (want_data && weight_diff && fork_side(s, &f)) {
         // (disjoint workspace regions: Wt for the data gradient; the staged
         // bottom and the partials for the weight gradient)
         const int sw = run_weights_bf16(q, dh, bottom, staged, weight_diff, accumulate, ws, f.side);
@@ -1306,7 +1341,7 @@ int backward_bf16_staged(const ConvPlan& q, const float* sums, int terms, bool m
             run_data_bf16(q, dh, mask_bottom ? bottom : nullptr, weight, bottom_diff, ws, s);
         CHECK(join_side(s, f, sw, sd));
     } else {
-        if (bottom_diff)
+        if (want_data)
             CHECK(run_data_bf16(q, dh, mask_bottom ? bottom : nullptr, weight, bottom_diff, ws,
                                 s));
         if (weight_diff)
@@ -1430,43 +1465,94 @@ int caffe_conv_backward(const caffe_conv_desc* desc, const float* top_diff, cons
                                   stream);
 }
 
-int caffe_conv_backward_ex(const caffe_conv_desc* desc, const float* top_diff, const float* top,
-                           const void* bottom, const void* weight, float* bottom_diff,
-                           float* weight_diff, float* bias_diff, int32_t accumulate,
-                           int32_t flags, void* workspace, size_t ws_bytes, void* stream,
-                           void* weight_stream)
+}  // extern "C"
+
+namespace {
+
+// Whether layer q's data gradient can be staged as the top gradient of the
+// layer qb below it (see caffe_conv_backward_into): CAFFE_OK, else the error.
+int check_stage_below(const ConvPlan& q, const ConvPlan& qb)
+{
+    if (!is_bf16(q) || !is_bf16(qb))
+        return fail(CAFFE_ERR_UNSUPPORTED, "a staged data gradient needs bf16 modes");
+    if (qb.N != q.N || qb.K != q.C || qb.Ho != q.H || qb.Wo != q.W)
+        return fail(CAFFE_ERR_INVALID_ARG, "the layer below's top (%d, %d, %d, %d) is not this "
+                    "layer's bottom (%d, %d, %d, %d)", qb.N, qb.K, qb.Ho, qb.Wo, q.N, q.C, q.H,
+                    q.W);
+    // stride 1 with the image as the GEMM's grid, no padded channels below
+    if (q.sh != 1 || q.sw != 1 || q.Ah != q.H || q.Aw != q.W || q.a0h != q.ph ||
+        q.a0w != q.pw || q.Cg % 4 != 0 || qb.Kgp != qb.Kg ||
+        (q.dgrad_tile != BTILE_128x256 && q.dgrad_tile != BTILE_64x256))
+        return fail(CAFFE_ERR_UNSUPPORTED, "this layer's data gradient cannot be staged for the "
+                    "layer below (stride %dx%d, %d channels per group)", q.sh, q.sw, q.Cg);
+    return CAFFE_OK;
+}
+
+// caffe_conv_backward_ex, and with `below` caffe_conv_backward_into (its
+// data gradient staged into the layer below's workspace instead of stored).
+int backward_impl(const caffe_conv_desc* desc, const float* top_diff, const float* top,
+                  const void* bottom, const void* weight, float* bottom_diff, float* weight_diff,
+                  float* bias_diff, int32_t accumulate, int32_t flags, void* workspace,
+                  size_t ws_bytes, void* stream, void* weight_stream,
+                  const caffe_conv_desc* below, void* below_ws, size_t below_ws_bytes)
 {
     ConvPlan q;
     CHECK(plan_conv(desc, &q));
     if (accumulate != 0 && accumulate != 1)
         return fail(CAFFE_ERR_INVALID_ARG, "accumulate must be 0 or 1");
     if (flags & ~(CAFFE_BACKWARD_TOP_DIFF_MASKED | CAFFE_BACKWARD_MASK_BOTTOM_DIFF |
-                  CAFFE_BACKWARD_BOTTOM_STAGED))
+                  CAFFE_BACKWARD_BOTTOM_STAGED | CAFFE_BACKWARD_TOP_STAGED))
         return fail(CAFFE_ERR_INVALID_ARG, "unknown backward flags 0x%x", flags);
     const bool staged = (flags & CAFFE_BACKWARD_BOTTOM_STAGED) != 0;
-    const bool masked = (flags & CAFFE_BACKWARD_TOP_DIFF_MASKED) != 0;
-    const bool mask_bottom = (flags & CAFFE_BACKWARD_MASK_BOTTOM_DIFF) != 0 && bottom_diff;
-    CHECK(check_conv_ptrs(q, top_diff, true, true, "top_diff"));
+    const bool top_staged = (flags & CAFFE_BACKWARD_TOP_STAGED) != 0;
+    const bool masked = (flags & CAFFE_BACKWARD_TOP_DIFF_MASKED) != 0 || top_staged;
+    if (top_staged && !is_bf16(q))
+        return fail(CAFFE_ERR_INVALID_ARG, "CAFFE_BACKWARD_TOP_STAGED needs a bf16 mode");
+    // the stage target: the layer below, whose top is this layer's bottom
+    ConvPlan qb;
+    ConvPlan::StageTarget target;
+    if (below) {
+        CHECK(plan_conv(below, &qb));
+        CHECK(check_stage_below(q, qb));
+        CHECK(check_ws(below_ws, below_ws_bytes, qb.ws_both));
+        if (bottom_diff)
+            return fail(CAFFE_ERR_INVALID_ARG, "bottom_diff is staged for the layer below: pass "
+                        "NULL");
+        target.Sh = (uint16_t*)((char*)below_ws + qb.off_dh);
+        target.Ssum = (float*)((char*)below_ws + qb.off_sums);
+        target.Hp = qb.DHp;
+        target.Wp = qb.DWp;
+        target.tb = qb.dtb;
+        target.lb = qb.dlb;
+        target.Ktot = qb.G * qb.Kgp;
+        target.T = stage_below_terms((int64_t)qb.N * qb.Ho * qb.Wo);
+        target.Sh_bytes = nbytes((int64_t)qb.N * qb.DHp * qb.DWp * target.Ktot, 2);
+        target.Ssum_bytes = nbytes((int64_t)target.T * qb.K, 4);
+        q.below = &target;
+    }
+    const bool want_dx = bottom_diff || below;
+    const bool mask_bottom = (flags & CAFFE_BACKWARD_MASK_BOTTOM_DIFF) != 0 && want_dx;
+    CHECK(check_conv_ptrs(q, top_diff, !top_staged, true, "top_diff"));
     CHECK(check_conv_ptrs(q, top, q.relu != 0 && !masked, true, "top"));
     CHECK(check_conv_ptrs(q, bottom, weight_diff != nullptr || mask_bottom, true, "bottom"));
-    CHECK(check_conv_ptrs(q, weight, bottom_diff != nullptr, false, "weight"));
+    CHECK(check_conv_ptrs(q, weight, want_dx, false, "weight"));
     CHECK(check_conv_ptrs(q, bottom_diff, false, true, "bottom_diff"));
     CHECK(check_conv_ptrs(q, weight_diff, false, false, "weight_diff"));
     CHECK(check_conv_ptrs(q, bias_diff, false, false, "bias_diff"));
     // the pass sizes of caffe_conv_workspace_size: both gradients, data only,
     // weights (with or without the bias) only; the bias alone fits either
-    const size_t need = bottom_diff && weight_diff ? q.ws_both
-                        : bottom_diff              ? q.ws_data
-                        : weight_diff              ? q.ws_weights
-                                                   : std::min(q.ws_data, q.ws_weights);
+    const size_t need = want_dx && weight_diff ? q.ws_both
+                        : want_dx              ? q.ws_data
+                        : weight_diff          ? q.ws_weights
+                                               : std::min(q.ws_data, q.ws_weights);
     CHECK(check_ws(workspace, ws_bytes, need));
     hipStream_t s = (hipStream_t)stream;
     // a weight stream other than `stream` takes the weight-side outputs
     hipStream_t wst = weight_stream != stream ? (hipStream_t)weight_stream : nullptr;
     char* ws = (char*)workspace;
     if (is_bf16(q))
-        return backward_bf16(q, top_diff, top, masked, mask_bottom, staged, bottom, weight,
-                             bottom_diff, weight_diff, bias_diff, accumulate, ws, s, wst);
+        return backward_bf16(q, top_diff, top, masked, top_staged, mask_bottom, staged, bottom,
+                             weight, bottom_diff, weight_diff, bias_diff, accumulate, ws, s, wst);
     if (q.dense) {
         CHECK(backward_dense(q, top_diff, top, masked, mask_bottom, (const float*)bottom,
                              (const float*)weight, bottom_diff, weight_diff, bias_diff,
@@ -1491,6 +1577,43 @@ int caffe_conv_backward_ex(const caffe_conv_desc* desc, const float* top_diff, c
     // (fp32: both passes share the workspace's partial-sum region, so they
     // run in turn on `stream`)
     return wst ? stream_follow(wst, s) : CAFFE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int caffe_conv_backward_ex(const caffe_conv_desc* desc, const float* top_diff, const float* top,
+                           const void* bottom, const void* weight, float* bottom_diff,
+                           float* weight_diff, float* bias_diff, int32_t accumulate,
+                           int32_t flags, void* workspace, size_t ws_bytes, void* stream,
+                           void* weight_stream)
+{
+    return backward_impl(desc, top_diff, top, bottom, weight, bottom_diff, weight_diff, bias_diff,
+                         accumulate, flags, workspace, ws_bytes, stream, weight_stream, nullptr,
+                         nullptr, 0);
+}
+
+int caffe_conv_stage_below_supported(const caffe_conv_desc* desc, const caffe_conv_desc* below)
+{
+    ConvPlan q, qb;
+    if (plan_conv(desc, &q) != CAFFE_OK || !below || plan_conv(below, &qb) != CAFFE_OK)
+        return 0;
+    return check_stage_below(q, qb) == CAFFE_OK ? 1 : 0;
+}
+
+int caffe_conv_backward_into(const caffe_conv_desc* desc, const float* top_diff, const float* top,
+                             const void* bottom, const void* weight, float* weight_diff,
+                             float* bias_diff, int32_t accumulate, int32_t flags,
+                             void* workspace, size_t ws_bytes, const caffe_conv_desc* below,
+                             void* below_workspace, size_t below_ws_bytes, void* stream,
+                             void* weight_stream)
+{
+    if (!below)
+        return fail(CAFFE_ERR_INVALID_ARG, "below is NULL");
+    return backward_impl(desc, top_diff, top, bottom, weight, nullptr, weight_diff, bias_diff,
+                         accumulate, flags, workspace, ws_bytes, stream, weight_stream, below,
+                         below_workspace, below_ws_bytes);
 }
 
 int caffe_conv_backward_data(const caffe_conv_desc* desc, const float* top_diff, const float* top,

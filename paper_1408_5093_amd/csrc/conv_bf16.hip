@@ -367,6 +367,94 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
                 }
             }
         }
+    } else if constexpr (EPI == 2) {
+        // The data gradient as the layer below's staged top gradient (stride
+        // 1: the GEMM's column grid is the image, row m is channel
+        // g*Cg_out + m) and the bias gradient's partial sums of each wave's
+        // 64 columns.  A lane holds four consecutive channels of one pixel
+        // per register quad: one 8-byte store.
+        static_assert(MT == 32 && WN == 4 && NI * MT == 64, "stage-below epilogue layout");
+        const int OutHW = p.OutH * p.OutW;
+        const __amdgpu_buffer_rsrc_t rom =
+            make_rsrc(p.Omask, MASK == 1 ? p.Y_bytes / 2 : (MASK == 2 ? p.Y_bytes : 0u));
+        const __amdgpu_buffer_rsrc_t rsh = make_rsrc(p.Sh, p.Sh_bytes);
+        const __amdgpu_buffer_rsrc_t rss = make_rsrc(p.Ssum, p.Ssum_bytes);
+        int mb[NI], sb[NI];
+        uint32_t pbad[NI];
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) {
+            const int col = n0 + brow + ni * MT;
+            const bool cok = col < p.Ncol;
+            const int n = cok ? (int)fdiv((uint32_t)col, p.div_ohw) : 0;
+            const int pix = col - n * OHW;
+            const int a = (int)fdiv((uint32_t)pix, p.div_ow);
+            const int b = pix - a * p.OW;
+            const int h = a + p.a0h - p.oph, w = b + p.a0w - p.opw;
+            const bool ok = cok && (unsigned)h < (unsigned)p.OutH && (unsigned)w < (unsigned)p.OutW;
+            pbad[ni] = ok ? 0u : kOob;
+            mb[ni] = (n * p.Cout + g * p.Cg_out) * OutHW + h * p.OutW + w;
+            sb[ni] = ((n * p.s_Hp + h + p.s_tb) * p.s_Wp + w + p.s_lb) * p.s_Ktot + g * p.Cg_out;
+        }
+        const int lrow0 = m0 + wm * MI * MT;
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) {
+            // the mask values of the block first, then the values and stores
+            float y[Op::kRegs][NI];
+#pragma unroll
+            for (int q = 0; q < Op::kRegs; ++q) {
+                const int m = lrow0 + mi * MT + Op::row(q, lane);
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni) {
+                    const uint32_t bad = pbad[ni] | ((uint32_t)(m >= M) << 31);
+                    const uint32_t idx = (uint32_t)(mb[ni] + m * OutHW);
+                    if constexpr (MASK == 1)
+                        y[q][ni] = bf16_to_f32(buf_ld_u16(rom, (idx * 2u) | bad));
+                    else if constexpr (MASK == 2)
+                        y[q][ni] = buf_ld_f32(rom, (idx * 4u) | bad);
+                    else
+                        y[q][ni] = 1.f;
+                }
+            }
+#pragma unroll
+            for (int qa = 0; qa < Op::kRegs / 4; ++qa) {
+                float csum[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni) {
+                    uint32_t w2[2] = {0u, 0u};
+#pragma unroll
+                    for (int b = 0; b < 4; ++b) {
+                        const int q = 4 * qa + b;
+                        float v = acc[mi][ni][q];
+                        if constexpr (MASK == 1)
+                            v = y[q][ni] > 0.f ? v : 0.f;
+                        else if constexpr (MASK == 2)
+                            v = y[q][ni] > 0x1p-134f ? v : 0.f;
+                        // (positions outside the image add nothing)
+                        v = pbad[ni] ? 0.f : v;
+                        csum[b] += v;
+                        w2[b >> 1] |= (uint32_t)f32_to_bf16_rne(v) << (16 * (b & 1));
+                    }
+                    // rows m .. m + 3 of this quad; a quad past M stores nothing
+                    const int m = lrow0 + mi * MT + Op::row(4 * qa, lane);
+                    const uint32_t off = ((uint32_t)(sb[ni] + m) * 2u) | pbad[ni] |
+                                         ((uint32_t)(m >= M) << 31);
+                    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w2[0], w2[1]}, rsh, off, 0, 0);
+                }
+                // the wave's column sums: over the 32 lanes of each half
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    float t = csum[b];
+#pragma unroll
+                    for (int o = 16; o > 0; o >>= 1)
+                        t += __shfl_xor(t, o, 64);
+                    const int m = lrow0 + mi * MT + Op::row(4 * qa + b, lane);
+                    const uint32_t off =
+                        ((uint32_t)((g * p.Cg_out + m) * p.s_T + 4 * ct + wn) * 4u) |
+                        ((uint32_t)((lane & 31) != 0 || m >= M) << 31);
+                    buf_st_f32(t, rss, off);
+                }
+            }
+        }
     } else {
         const int pss = p.psh * p.psw;
         const int OutHW = p.OutH * p.OutW;
@@ -1230,6 +1318,23 @@ hipError_t launch_gemm_pipe(const GemmBf16Params& p, int tile, int pipe, hipStre
     }
 }
 
+// epi 2: the tiles of 32-row blocks with four waves of 64 columns
+template <int MASK>
+hipError_t launch_stage_below(const GemmBf16Params& p, int tile, int pipe, hipStream_t s)
+{
+    const bool three = pipe == BPIPE_3;
+    switch (tile) {
+    case BTILE_128x256:
+        return three ? launch_gemm<32, 2, 4, 2, 2, 3, 2, MASK>(p, s)
+                     : launch_gemm<32, 2, 4, 2, 2, 2, 2, MASK>(p, s);
+    case BTILE_64x256:
+        return three ? launch_gemm<32, 1, 4, 2, 2, 3, 2, MASK>(p, s)
+                     : launch_gemm<32, 1, 4, 2, 2, 2, 2, MASK>(p, s);
+    default:
+        return hipErrorInvalidValue;
+    }
+}
+
 template <int WM, int WN, int MI, int NI>
 hipError_t launch_wg(const WgradBf16Params& p, hipStream_t s)
 {
@@ -1271,11 +1376,29 @@ hipError_t launch_conv_gemm_bf16(const GemmBf16Params& p, int epi, int tile, int
         return hipErrorInvalidValue;
     if (epi == 0)
         return launch_gemm_pipe<0, 0>(p, tile, pipe, s);
+    if (epi == 2) {
+        // stride 1, the column grid the image itself, whole quads of rows
+        if (p.psh != 1 || p.psw != 1 || p.OH != p.OutH || p.OW != p.OutW ||
+            p.a0h != p.oph || p.a0w != p.opw || p.M != p.Cg_out || p.M % 4 != 0 ||
+            p.Cg_out % 4 != 0 || p.s_Ktot % 4 != 0 || !p.Sh || !p.Ssum ||
+            p.s_T < stage_below_terms(p.Ncol) || p.s_tb < 0 || p.s_lb < 0 ||
+            p.s_Hp < p.s_tb + p.OutH || p.s_Wp < p.s_lb + p.OutW ||
+            (int64_t)p.G * p.Cg_out > p.s_Ktot ||
+            (int64_t)p.N * p.s_Hp * p.s_Wp * p.s_Ktot * 2 > (int64_t)p.Sh_bytes ||
+            (int64_t)p.G * p.Cg_out * p.s_T * 4 > (int64_t)p.Ssum_bytes)
+            return hipErrorInvalidValue;
+        if (!p.Omask)
+            return launch_stage_below<0>(p, tile, pipe, s);
+        return p.omask_f32 ? launch_stage_below<2>(p, tile, pipe, s)
+                           : launch_stage_below<1>(p, tile, pipe, s);
+    }
     if (!p.Omask)
         return launch_gemm_pipe<1, 0>(p, tile, pipe, s);
     return p.omask_f32 ? launch_gemm_pipe<1, 2>(p, tile, pipe, s)
                        : launch_gemm_pipe<1, 1>(p, tile, pipe, s);
 }
+
+int stage_below_terms(int64_t ncol) { return (int)(4 * ((ncol + 255) / 256)); }
 
 int bf16_wgrad_tile_m(int tile) { return tile == BWTILE_96x256 ? 96 : 128; }
 

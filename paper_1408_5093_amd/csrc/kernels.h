@@ -260,9 +260,27 @@ struct GemmBf16Params {
     // epilogue divisions: output pixels per image and per row (epi 0 and 1),
     // phases psh*psw and psw (epi 1)
     FastDiv div_ohw, div_ow, div_pss, div_psw;
+    // epi 2 (a stride-1 data gradient whose output grid is the image, taken
+    // as the top gradient of the layer below): instead of Y, each value v of
+    // channel c = g*Cg_out + m at pixel (n, h, w), masked as in epi 1, goes
+    // to Sh[n][h + s_tb][w + s_lb][c] as bf16 (nearest even) -- the layer
+    // below's staged top gradient, s_Ktot channels -- and each wave's sum of
+    // its 64 columns' float values to Ssum[c * s_T + 4 * column tile + wave
+    // column] (the bias gradient's partial sums, s_T per channel)
+    uint16_t* Sh;
+    float* Ssum;
+    uint32_t Sh_bytes, Ssum_bytes;
+    int s_Hp, s_Wp, s_tb, s_lb, s_Ktot, s_T;
 };
 hipError_t launch_conv_gemm_bf16(const GemmBf16Params& p, int epi, int tile, int pipe,
                                  hipStream_t s);
+// Terms per channel of the epi 2 bias partial sums for an image grid of
+// ncol pixels (4 per 256-column tile).
+int stage_below_terms(int64_t ncol);
+// Zero the border (every pixel outside rows tb .. tb + H - 1 and columns
+// lb .. lb + W - 1) of an N x DHp x DWp x Ktot bf16 staging.
+hipError_t launch_dh_zero_border(uint16_t* Dh, int N, int DHp, int DWp, int tb, int lb, int H,
+                                 int W, int Ktot, hipStream_t s);
 
 // Split-K weight gradient over channel-contiguous, zero-bordered bf16
 // operands (D laid out [N][DHp][DWp][Ktot] with the real pixels at offset

@@ -962,6 +962,18 @@ dh_zero_border_kernel(uint16_t* __restrict__ Dh, int N, int DHp, int DWp, int tb
     *(u32x4*)&Dh[(((size_t)n * DHp + hp) * DWp + wp) * Ktot + 8 * c8] = u32x4{0u, 0u, 0u, 0u};
 }
 
+hipError_t launch_dh_zero_border(uint16_t* Dh, int N, int DHp, int DWp, int tb, int lb, int H,
+                                 int W, int Ktot, hipStream_t s)
+{
+    if (Ktot % 8 != 0 || tb < 0 || lb < 0 || DHp < tb + H || DWp < lb + W)
+        return hipErrorInvalidValue;
+    const long border = (long)N * (DHp * DWp - H * W) * (Ktot / 8);
+    if (border > 0)
+        hipLaunchKernelGGL(dh_zero_border_kernel, dim3((unsigned)((border + 255) / 256)), dim3(256),
+                           0, s, Dh, N, DHp, DWp, tb, lb, H, W, Ktot, border);
+    return hipGetLastError();
+}
+
 // The backward's strip: `yrows` input rows whose covering pooled rows (at
 // most 256 positions) are staged; 0 when even one row does not fit.
 static int fused_backward_yrows(int H, int OH, int OW, int kh, int sh, int ph)
@@ -1037,10 +1049,9 @@ hipError_t launch_lrn_pool_backward_bf16(const float* pooled, const float* top,
     if (yrows == 0 || (size != 3 && size != 5) || Kg % kFuseCh != 0 || Ktot % 8 != 0 ||
         tb < 0 || lb < 0 || DHp < tb + H || DWp < lb + W)
         return hipErrorInvalidValue;
-    const long border = (long)N * (DHp * DWp - H * W) * (Ktot / 8);
-    if (border > 0)
-        hipLaunchKernelGGL(dh_zero_border_kernel, dim3((unsigned)((border + 255) / 256)), dim3(256),
-                           0, s, Dh, N, DHp, DWp, tb, lb, H, W, Ktot, border);
+    const hipError_t e = launch_dh_zero_border(Dh, N, DHp, DWp, tb, lb, H, W, Ktot, s);
+    if (e != hipSuccess)
+        return e;
     const int nstrips = (H + yrows - 1) / yrows;
     const int nchunks = C / kFuseCh;
     const dim3 g((unsigned)((long)N * nchunks * nstrips));

@@ -14,7 +14,8 @@ call; this module only owns buffers and the call order.
 import torch
 
 from . import (BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED,
-               CAFFE_BF16_F32_BOTTOM, CAFFE_F32,
+               BACKWARD_TOP_STAGED, CAFFE_BF16_F32_BOTTOM, CAFFE_F32, caffe_conv_backward_into,
+               conv_stage_below_supported,
                PASS_BACKWARD, PASS_BACKWARD_POOL_LRN, PASS_BACKWARD_WEIGHTS, PASS_FORWARD,
                POOL_RELU_INPUT, Workspace, caffe_conv_backward, caffe_conv_backward_pool_lrn,
                caffe_conv_forward, conv_desc, conv_out_shape, lrn_desc,
@@ -31,7 +32,7 @@ class ConvStack:
     (CAFFE_BF16_F32_BOTTOM); glue stays fp32."""
 
     def __init__(self, layers, N, weights, biases, glue=None, bf16=False, device="cuda",
-                 fuse_glue=True, split_backward=True, fuse_staging=True):
+                 fuse_glue=True, split_backward=True, fuse_staging=True, chain_staging=True):
         self.layers = list(layers)
         self.N = N
         self.bf16 = bf16
@@ -111,6 +112,18 @@ class ConvStack:
         # and data gradients.
         self.split_backward = split_backward and not bf16
         self.weight_side = split_backward and bf16
+        # bf16: a layer whose bottom is the previous layer's top (no glue in
+        # between) writes its data gradient straight into that layer's staged
+        # top gradient (caffe_conv_backward_into) where the library supports
+        # the pair, so the float gradient is neither stored nor staged again
+        n_l = len(self.layers)
+        self.stage_into = [False] * n_l
+        if bf16 and chain_staging:
+            for l in range(1, n_l):
+                self.stage_into[l] = (not self.glue.get(l - 1) and not self.glue.get(l) and
+                                      conv_stage_below_supported(self.descs[l],
+                                                                 self.descs[l - 1]))
+        self.top_from_above = [l + 1 < n_l and self.stage_into[l + 1] for l in range(n_l)]
         if self.split_backward or self.weight_side:
             self.side = torch.cuda.Stream(device=dev)
         if self.split_backward:
@@ -230,9 +243,13 @@ class ConvStack:
         g = top_diff
         for l in range(len(self.layers) - 1, -1, -1):
             L = self.layers[l]
-            g = g.view(self.out_shape[l])
+            if g is not None:
+                g = g.view(self.out_shape[l])
             if self.fuse_staging[l]:
                 g = self._backward_pool_lrn(l, g, s, l > 0 or data_grad_bottom, wside)
+                continue
+            if self.stage_into[l] or self.top_from_above[l]:
+                g = self._backward_staged(l, g, s, wside)
                 continue
             if self.fused[l]:
                 pst, lst = self.stages[l]
@@ -296,6 +313,38 @@ class ConvStack:
             s.wait_stream(self.side)
         return self.dbottom[0]
 
+    def _backward_staged(self, l, g, s, wside):
+        """bf16 layer l with its top gradient staged by the layer above and/or
+        its data gradient staged into the layer below; returns the float top
+        gradient of the layer below, or None when it is staged."""
+        L = self.layers[l]
+        flags = BACKWARD_BOTTOM_STAGED
+        if self.top_masked[l]:
+            flags |= BACKWARD_TOP_DIFF_MASKED
+        if self.top_from_above[l]:
+            flags |= BACKWARD_TOP_STAGED
+            g = None
+        else:
+            g = g.view(self.out_shape[l])
+        if self.mask_bottom[l]:
+            flags |= BACKWARD_MASK_BOTTOM_DIFF
+        top = self.top[l] if L.relu else None
+        self._mark(("both", l, "begin"), s)
+        if self.stage_into[l]:
+            caffe_conv_backward_into(self.descs[l], g, top, self.bottom[l], self.W[l], self.dW[l],
+                                     self.db[l], 0, flags, self.ws_of[l], self.descs[l - 1],
+                                     self.ws_of[l - 1], s, weight_stream=wside)
+            out = None
+        else:
+            caffe_conv_backward(self.descs[l], g, top, self.bottom[l], self.W[l],
+                                self.dbottom[l], self.dW[l], self.db[l], 0, flags, self.ws_of[l],
+                                s, weight_stream=wside)
+            out = self.dbottom[l]
+        self._mark(("both", l, "end"), s)
+        if wside is not None:  # (the call ends with the later of the two)
+            self._mark(("both", l, "end"), wside)
+        return out
+
     def _backward_pool_lrn(self, l, g, s, want_dx, wside=None):
         """Layer l's backward from the gradient g of the LRN after its max-pool
         (one call: the glue's backward staged as the bf16 top gradient)."""
@@ -322,8 +371,9 @@ class ConvStack:
         """Gradient that layer l received in the last backward (after its glue)."""
         if l == len(self.layers) - 1:
             return top_diff_last
-        if self.fuse_staging[l]:
-            raise ValueError(f"layer {l}'s top gradient is staged in bf16 only (fuse_staging)")
+        if self.fuse_staging[l] or self.top_from_above[l]:
+            raise ValueError(f"layer {l}'s top gradient is staged in bf16 only (fuse_staging, "
+                             "chain_staging)")
         st = self.stages[l]
         return st[0]["dx"] if st else self.dbottom[l + 1].view(self.top[l].shape)
 

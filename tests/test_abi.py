@@ -246,8 +246,11 @@ def test_pointer_checks_before_any_launch():
     # accumulate flag, unknown backward flags
     assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 2, 0,
                P(0x100000), ws, None) == -1
-    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0, 8,
+    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0, 32,
                P(0x100000), ws, None) == -1
+    # the staged top gradient is a bf16 mode's
+    assert bwd(P(0x1000), P(0x1800), P(0x2000), P(0x3000), P(0x4000), P(0x5000), P(0x6000), 0,
+               16, P(0x100000), ws, None) == -1
     # weight gradient needs bottom; data gradient needs weight; a masked
     # bottom gradient needs bottom
     assert bwd(P(0x1000), P(0x1800), None, P(0x3000), None, P(0x5000), None, 0, 0,

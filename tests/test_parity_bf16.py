@@ -230,7 +230,7 @@ def test_caffenet_bf16_training_step_full_size():
     # read each layer's top gradient; the fused step is compared with this one
     # in test_caffenet_bf16_step_fused_staging_matches)
     net = ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(), bf16=True,
-                    fuse_staging=False)
+                    fuse_staging=False, chain_staging=False)
     x = torch.from_numpy(inp["x"]).to(DEV)
     g = torch.from_numpy(inp["top_diff"]).to(DEV)
     net.forward(x)
@@ -330,7 +330,8 @@ def test_caffenet_bf16_step_weight_stream_matches():
         torch.cuda.synchronize()
         a, b = nets
         for l in range(len(wl.CAFFENET)):
-            assert torch.equal(a.dbottom[l], b.dbottom[l]), f"layer {l} data gradient"
+            if not a.stage_into[l]:  # (a staged data gradient is not stored)
+                assert torch.equal(a.dbottom[l], b.dbottom[l]), f"layer {l} data gradient"
             assert torch.equal(a.dW[l], b.dW[l]), f"layer {l} weight gradient"
             assert torch.equal(a.db[l], b.db[l]), f"layer {l} bias gradient"
 
@@ -354,7 +355,94 @@ def test_caffenet_bf16_step_fused_staging_matches():
         torch.cuda.synchronize()
         a, b = nets
         for l in range(len(wl.CAFFENET)):
-            assert torch.equal(a.dbottom[l], b.dbottom[l]), f"layer {l} data gradient"
+            if not a.stage_into[l]:
+                assert torch.equal(a.dbottom[l], b.dbottom[l]), f"layer {l} data gradient"
+            assert torch.equal(a.dW[l], b.dW[l]), f"layer {l} weight gradient"
+            assert_close(_np(a.db[l]), _np(b.db[l]), 1e-6, f"layer {l} bias gradient")
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32_bottom"])
+@pytest.mark.parametrize("ga", [1, 2])
+def test_backward_into_layer_below(dt, ga):
+    """caffe_conv_backward_into: layer B's data gradient (masked by B's bottom,
+    the ReLU output of layer A) staged straight into A's top-gradient staging,
+    then A's backward with CAFFE_BACKWARD_TOP_STAGED -- against B storing its
+    float data gradient and A staging it: A's data and weight gradients bit
+    for bit, A's bias gradient within 1e-6, B's weight and bias gradients
+    bit for bit; twice, the second time into a workspace that held other
+    values."""
+    rng = np.random.default_rng([97, ga, dt == "bf16"])
+    mode = cc.CAFFE_BF16 if dt == "bf16" else cc.CAFFE_BF16_F32_BOTTOM
+    N, C, H, W, KA, KB = 2, 16, 10, 9, 128, 40
+    x = _t(rng.standard_normal((N, C, H, W)), torch.bfloat16)
+    wa = _t(rng.standard_normal((KA, C // ga, 3, 3)) * 0.2, torch.bfloat16)
+    wb = _t(rng.standard_normal((KB, KA // 2, 3, 3)) * 0.2, torch.bfloat16)
+    ba, bb = _t(rng.standard_normal(KA) * 0.1), _t(rng.standard_normal(KB) * 0.1)
+    da = cc.conv_desc(x.shape, wa.shape, 1, 1, ga, True, cc.CAFFE_BF16)
+    ya = torch.empty((N, KA, H, W), device=DEV)
+    wsa0 = cc.Workspace(DEV).get(max(cc.conv_workspace_size(da, p) for p in range(4)))
+    cc.caffe_conv_forward(da, x, wa, ba, ya, wsa0)
+    xb = ya.to(torch.bfloat16) if mode == cc.CAFFE_BF16 else ya
+    db_ = cc.conv_desc(xb.shape, wb.shape, 1, 1, 2, True, mode)
+    assert cc.conv_stage_below_supported(db_, da)
+    yb = torch.empty((N, KB, H, W), device=DEV)
+    wsb = cc.Workspace(DEV).get(max(cc.conv_workspace_size(db_, p) for p in range(4)))
+    cc.caffe_conv_forward(db_, xb, wb, bb, yb, wsb)
+    gd = _t(rng.standard_normal(yb.shape))
+    nA = cc.conv_workspace_size(da, cc.PASS_BACKWARD)
+    out = {}
+    for way in ("stored", "staged", "staged"):
+        wsa = torch.full((nA,), 0x7F, dtype=torch.uint8, device=DEV)
+        # A's forward staging of its bottom (what BACKWARD_BOTTOM_STAGED reads)
+        cc.caffe_conv_forward(da, x, wa, ba, ya, wsa)
+        dwb, dbb = torch.empty(wb.shape, device=DEV), torch.empty(KB, device=DEV)
+        dxa, dwa, dba = (torch.empty(x.shape, device=DEV), torch.empty(wa.shape, device=DEV),
+                         torch.empty(KA, device=DEV))
+        fb = cc.BACKWARD_MASK_BOTTOM_DIFF
+        fa = cc.BACKWARD_BOTTOM_STAGED
+        if way == "stored":
+            dxb = torch.empty(xb.shape, device=DEV, dtype=torch.float32)
+            cc.caffe_conv_backward(db_, gd, yb, xb, wb, dxb, dwb, dbb, 0, fb, wsb)
+            cc.caffe_conv_backward(da, dxb, ya, x, wa, dxa, dwa, dba, 0,
+                                   fa | cc.BACKWARD_TOP_DIFF_MASKED, wsa)
+        else:
+            cc.caffe_conv_backward_into(db_, gd, yb, xb, wb, dwb, dbb, 0, fb, wsb, da, wsa)
+            cc.caffe_conv_backward(da, None, ya, x, wa, dxa, dwa, dba, 0,
+                                   fa | cc.BACKWARD_TOP_STAGED, wsa)
+        torch.cuda.synchronize()
+        out.setdefault(way, []).append((dxa, dwa, dba, dwb, dbb))
+    ref = out["stored"][0]
+    for got in out["staged"]:
+        assert torch.equal(got[0], ref[0]), "A data gradient"
+        assert torch.equal(got[1], ref[1]), "A weight gradient"
+        assert_close(_np(got[2]), _np(ref[2]), 1e-6, "A bias gradient")
+        assert torch.equal(got[3], ref[3]) and torch.equal(got[4], ref[4]), "B gradients"
+
+
+def test_caffenet_bf16_step_chained_staging_matches():
+    """The bf16 step at N=512 with conv5's and conv4's data gradients staged
+    straight into conv4's and conv3's top-gradient staging (the default)
+    against the step that stores and stages them: the stored data gradients,
+    every weight gradient bit for bit (the staged bf16 values are the same),
+    the bias gradients within 1e-6 (their partial sums are taken in another
+    order), over two steps."""
+    N = 512
+    inp = wl.caffenet_step(N, wl.CAFFENET_STEP_BF16)
+    x = torch.from_numpy(inp["x"]).to(DEV)
+    g = torch.from_numpy(inp["top_diff"]).to(DEV)
+    nets = [ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(), bf16=True,
+                      chain_staging=f) for f in (True, False)]
+    assert nets[0].stage_into == [False, False, False, True, True]
+    assert not any(nets[1].stage_into)
+    for _ in range(2):
+        for net in nets:
+            net.forward(x)
+            net.backward(g)
+        torch.cuda.synchronize()
+        a, b = nets
+        for l in range(len(wl.CAFFENET)):
+            if not a.stage_into[l]:
+                assert torch.equal(a.dbottom[l], b.dbottom[l]), f"layer {l} data gradient"
             assert torch.equal(a.dW[l], b.dW[l]), f"layer {l} weight gradient"
             assert_close(_np(a.db[l]), _np(b.db[l]), 1e-6, f"layer {l} bias gradient")
 

@@ -137,6 +137,21 @@ int caffe_conv_forward(const caffe_conv_desc* desc, const void* bottom, const vo
                        const float* bias, float* top, void* workspace, size_t ws_bytes,
                        void* stream);
 
+/* Flags of caffe_conv_forward_ex. */
+enum caffe_forward_flags {
+    /* bf16 modes: the workspace already holds bottom's staged bf16 copy,
+     * written by caffe_pool_lrn_forward_into (caffe_layers.h) for this
+     * descriptor and workspace; the call does not stage bottom again (bottom
+     * may be NULL) and the later backward's CAFFE_BACKWARD_BOTTOM_STAGED
+     * reads that copy.  CAFFE_ERR_INVALID_ARG in CAFFE_F32 mode. */
+    CAFFE_FORWARD_BOTTOM_STAGED = 1
+};
+
+/* caffe_conv_forward with caffe_forward_flags. */
+int caffe_conv_forward_ex(const caffe_conv_desc* desc, const void* bottom, const void* weight,
+                          const float* bias, float* top, void* workspace, size_t ws_bytes,
+                          int32_t flags, void* stream);
+
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc):
  * caffe_conv_forward with its workspace taken from a static device array the

@@ -92,6 +92,26 @@ int caffe_pool_lrn_forward(const caffe_pool_desc* pool, const caffe_lrn_desc* lr
                            const float* bottom, float* pooled, int32_t* mask, float* top,
                            int32_t flags, void* stream);
 
+/* caffe_pool_lrn_forward whose LRN output (top, still written) also goes,
+ * rounded to bf16 (nearest even), to the staged bottom of the convolution
+ * `next` that takes it as input, border included, in next's forward
+ * workspace (next_workspace, at least caffe_conv_workspace_size(next,
+ * CAFFE_PASS_FORWARD) bytes): next's forward then takes
+ * CAFFE_FORWARD_BOTTOM_STAGED (caffe_conv_forward_ex) and skips the pass
+ * that would read top back and stage it.  next's N, C, H, W must be the
+ * LRN's (CAFFE_ERR_INVALID_ARG); next must be in a bf16 mode with groups of
+ * a multiple of 16 channels that need no padding, the LRN of size 3 or 5
+ * (caffe_pool_lrn_stage_supported, else CAFFE_ERR_UNSUPPORTED). */
+int caffe_pool_lrn_forward_into(const caffe_pool_desc* pool, const caffe_lrn_desc* lrn,
+                                const float* bottom, float* pooled, int32_t* mask, float* top,
+                                int32_t flags, const caffe_conv_desc* next, void* next_workspace,
+                                size_t next_ws_bytes, void* stream);
+
+/* 1 when caffe_pool_lrn_forward_into can stage for `next`, else 0.
+ * Host-only. */
+int caffe_pool_lrn_stage_supported(const caffe_pool_desc* pool, const caffe_lrn_desc* lrn,
+                                   const caffe_conv_desc* next);
+
 /* The backward of that pair in one pass: bottom_diff as caffe_lrn_backward
  * (pooled, top, top_diff) followed by caffe_maxpool_backward (with `mask`)
  * would write it, without storing the pooled gradient (each block stages the

@@ -16,7 +16,8 @@ import torch
 from . import _lib
 from ._lib import (  # noqa: F401
     CAFFE_ERR_UNSUPPORTED, CAFFE_ERR_WORKSPACE, NOALLOC_SCRATCH_BYTES, BACKWARD_BOTTOM_STAGED,
-    BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED, BACKWARD_TOP_STAGED, CAFFE_BF16, CAFFE_BF16_F32_BOTTOM, CAFFE_F32, CAFFE_LR_EXP,
+    BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED, BACKWARD_TOP_STAGED,
+    FORWARD_BOTTOM_STAGED, CAFFE_BF16, CAFFE_BF16_F32_BOTTOM, CAFFE_F32, CAFFE_LR_EXP,
     CAFFE_LR_FIXED, CAFFE_LR_INV, CAFFE_LR_STEP, LrSchedule, PASS_BACKWARD,
     PASS_BACKWARD_DATA, PASS_BACKWARD_POOL_LRN, PASS_BACKWARD_WEIGHTS, PASS_FORWARD,
     POOL_RELU_INPUT, CaffeError, ConvDesc,
@@ -29,7 +30,7 @@ __all__ = [
     "lrn_forward", "lrn_backward", "cast_f32_to_bf16", "Workspace", "CaffeError",
     "sgd_learning_rate", "softmax_loss", "sgd_update", "pool_lrn_forward", "lrn_pool_backward",
     "pool_lrn_supported", "caffe_conv_backward_pool_lrn", "relu_backward",
-    "caffe_conv_backward_into", "conv_stage_below_supported",
+    "caffe_conv_backward_into", "conv_stage_below_supported", "pool_lrn_stage_supported",
 ]
 
 
@@ -106,14 +107,19 @@ def _bottom_dtype(desc):
 
 
 # ----------------------------------------------------- C-ABI-shaped calls
-def caffe_conv_forward(desc, bottom, weight, bias, top, workspace=None, stream=None):
+def caffe_conv_forward(desc, bottom, weight, bias, top, workspace=None, stream=None, flags=0):
+    """caffe_conv_forward, or with flags caffe_conv_forward_ex."""
     t = _op_dtype(desc)
     _dev(bottom, "bottom", _bottom_dtype(desc)), _dev(weight, "weight", t)
     _dev(bias, "bias", torch.float32)
     _dev(top, "top", torch.float32)
     ws_bytes = 0 if workspace is None else workspace.numel()
-    check(load().caffe_conv_forward(ctypes.byref(desc), _ptr(bottom), _ptr(weight), _ptr(bias),
-                                    _ptr(top), _ptr(workspace), ws_bytes, _stream(stream)))
+    args = (ctypes.byref(desc), _ptr(bottom), _ptr(weight), _ptr(bias), _ptr(top),
+            _ptr(workspace), ws_bytes)
+    if flags:
+        check(load().caffe_conv_forward_ex(*args, int(flags), _stream(stream)))
+    else:
+        check(load().caffe_conv_forward(*args, _stream(stream)))
 
 
 def caffe_conv_backward(desc, top_diff, top, bottom, weight, bottom_diff, weight_diff, bias_diff,
@@ -328,8 +334,10 @@ def pool_lrn_supported(x_shape, kernel, stride, pad=0, size=5, alpha=1e-4, beta=
 
 
 def pool_lrn_forward(x, kernel, stride, pad=0, size=5, alpha=1e-4, beta=0.75, k=1.0,
-                     pooled=None, mask=None, out=None, flags=0, stream=None):
-    """Max-pool then LRN in one pass; returns (pooled, mask, out)."""
+                     pooled=None, mask=None, out=None, flags=0, stream=None, stage_for=None):
+    """Max-pool then LRN in one pass; returns (pooled, mask, out).  With
+    stage_for=(conv desc, its forward workspace), caffe_pool_lrn_forward_into:
+    the output is also staged as that convolution's bf16 bottom."""
     _dev(x, "bottom", torch.float32)
     pd, ld, shape = _pool_lrn_descs(x.shape, kernel, stride, pad, size, alpha, beta, k)
     pooled = torch.empty(shape, dtype=torch.float32, device=x.device) if pooled is None else pooled
@@ -338,9 +346,23 @@ def pool_lrn_forward(x, kernel, stride, pad=0, size=5, alpha=1e-4, beta=0.75, k=
     for t, n in ((pooled, "pooled"), (out, "top")):
         _dev(t, n, torch.float32)
     _dev(mask, "mask", torch.int32)
-    check(load().caffe_pool_lrn_forward(ctypes.byref(pd), ctypes.byref(ld), _ptr(x), _ptr(pooled),
-                                        _ptr(mask), _ptr(out), int(flags), _stream(stream)))
+    args = (ctypes.byref(pd), ctypes.byref(ld), _ptr(x), _ptr(pooled), _ptr(mask), _ptr(out),
+            int(flags))
+    if stage_for is None:
+        check(load().caffe_pool_lrn_forward(*args, _stream(stream)))
+    else:
+        nd, nws = stage_for
+        check(load().caffe_pool_lrn_forward_into(*args, ctypes.byref(nd), _ptr(nws),
+                                                 0 if nws is None else nws.numel(),
+                                                 _stream(stream)))
     return pooled, mask, out
+
+
+def pool_lrn_stage_supported(x_shape, kernel, stride, pad, size, alpha, beta, k, next_desc):
+    """Whether pool_lrn_forward can stage its output for the convolution next_desc."""
+    pd, ld, _ = _pool_lrn_descs(x_shape, kernel, stride, pad, size, alpha, beta, k)
+    return bool(load().caffe_pool_lrn_stage_supported(ctypes.byref(pd), ctypes.byref(ld),
+                                                      ctypes.byref(next_desc)))
 
 
 def lrn_pool_backward(x_shape, pooled, top, top_diff, mask, kernel, stride, pad=0, size=5,

@@ -25,6 +25,7 @@ BACKWARD_TOP_DIFF_MASKED = 1
 BACKWARD_MASK_BOTTOM_DIFF = 2
 BACKWARD_BOTTOM_STAGED = 4
 BACKWARD_TOP_STAGED = 16
+FORWARD_BOTTOM_STAGED = 1
 POOL_RELU_INPUT = 1
 
 PASS_FORWARD = 0
@@ -52,7 +53,8 @@ EXPORTS = (
     "caffe_conv_workspace_bytes", "caffe_conv_status_string", "caffe_conv_forward_noalloc",
     "caffe_conv_backward_pool_lrn", "caffe_relu_backward", "caffe_conv_backward_ex",
     "caffe_conv_backward_pool_lrn_ex", "caffe_conv_backward_into",
-    "caffe_conv_stage_below_supported",
+    "caffe_conv_stage_below_supported", "caffe_conv_forward_ex", "caffe_pool_lrn_forward_into",
+    "caffe_pool_lrn_stage_supported",
 )
 
 
@@ -108,6 +110,7 @@ def load():
         "caffe_conv_out_shape": [cdp, pi32, pi32],
         "caffe_conv_workspace_size": [cdp, i32, ctypes.POINTER(sz)],
         "caffe_conv_forward": [cdp, vp, vp, vp, vp, vp, sz, vp],
+        "caffe_conv_forward_ex": [cdp, vp, vp, vp, vp, vp, sz, i32, vp],
         "caffe_conv_forward_noalloc": [cdp, vp, vp, vp, vp, vp],
         "caffe_conv_backward_data": [cdp, vp, vp, vp, vp, vp, sz, vp],
         "caffe_conv_backward_weights": [cdp, vp, vp, vp, vp, vp, i32, vp, sz, vp],
@@ -124,6 +127,8 @@ def load():
         "caffe_cast_f32_to_bf16": [vp, vp, i64, vp],
         "caffe_relu_backward": [vp, vp, vp, i64, vp],
         "caffe_pool_lrn_forward": [pdp, ldp, vp, vp, vp, vp, i32, vp],
+        "caffe_pool_lrn_forward_into": [pdp, ldp, vp, vp, vp, vp, i32, cdp, vp, sz, vp],
+        "caffe_pool_lrn_stage_supported": [pdp, ldp, cdp],
         "caffe_lrn_pool_backward": [pdp, ldp, vp, vp, vp, vp, vp, vp],
         "caffe_conv_backward_pool_lrn": [cdp, pdp, ldp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                          i32, i32, vp, sz, vp],

@@ -1046,6 +1046,15 @@ int backward_dense(const ConvPlan& q, const float* top_diff, const float* top, b
 
 // ---- bf16 operands
 // The input's bf16 staging (plain or space-to-depth) at xh.
+// Whether the LRN forward can write convolution qn's bf16 bottom staging:
+// the plain channel-contiguous layout with unpadded groups, in whole
+// 16-channel chunks.
+bool caffe_hip_stage_from_lrn_ok(const ConvPlan& qn, int lrn_size)
+{
+    return is_bf16(qn) && !qn.s2d && qn.Cgp == qn.Cg && qn.C % 16 == 0 &&
+           (lrn_size == 3 || lrn_size == 5) && qn.ph >= 0 && qn.pw >= 0;
+}
+
 hipError_t stage_bottom_bf16(const ConvPlan& q, const void* bottom, uint16_t* xh, hipStream_t s)
 {
     if (q.s2d)
@@ -1056,14 +1065,15 @@ hipError_t stage_bottom_bf16(const ConvPlan& q, const void* bottom, uint16_t* xh
 }
 
 int run_forward_bf16(const ConvPlan& q, const void* bottom, const void* weight, const float* bias,
-                     float* top, char* ws, hipStream_t s)
+                     float* top, char* ws, hipStream_t s, bool bottom_staged = false)
 {
     if (q.top_elems == 0)
         return CAFFE_OK;
     uint16_t* xh = (uint16_t*)(ws + q.off_xh_fwd);
     uint16_t* wp = (uint16_t*)(ws + q.off_wp_fwd);
     const int Ctot = q.G * q.Cgp;
-    LAUNCH(stage_bottom_bf16(q, bottom, xh, s), "bf16 staging launch");
+    if (!bottom_staged)
+        LAUNCH(stage_bottom_bf16(q, bottom, xh, s), "bf16 staging launch");
     LAUNCH(launch_pack_weights_bf16((const uint16_t*)weight, wp, q.K, q.Cg, q.Cgp, q.kh, q.kw,
                                     q.kwp, q.s2d ? q.s2d : 1, q.Rp, s),
            "bf16 weight pack launch");
@@ -1418,16 +1428,28 @@ int caffe_conv_forward(const caffe_conv_desc* desc, const void* bottom, const vo
                        const float* bias, float* top, void* workspace, size_t ws_bytes,
                        void* stream)
 {
+    return caffe_conv_forward_ex(desc, bottom, weight, bias, top, workspace, ws_bytes, 0, stream);
+}
+
+int caffe_conv_forward_ex(const caffe_conv_desc* desc, const void* bottom, const void* weight,
+                          const float* bias, float* top, void* workspace, size_t ws_bytes,
+                          int32_t flags, void* stream)
+{
     ConvPlan q;
     CHECK(plan_conv(desc, &q));
-    CHECK(check_conv_ptrs(q, bottom, true, true, "bottom"));
+    if (flags & ~CAFFE_FORWARD_BOTTOM_STAGED)
+        return fail(CAFFE_ERR_INVALID_ARG, "unknown forward flags 0x%x", flags);
+    const bool bottom_staged = (flags & CAFFE_FORWARD_BOTTOM_STAGED) != 0;
+    if (bottom_staged && !is_bf16(q))
+        return fail(CAFFE_ERR_INVALID_ARG, "CAFFE_FORWARD_BOTTOM_STAGED needs a bf16 mode");
+    CHECK(check_conv_ptrs(q, bottom, !bottom_staged, true, "bottom"));
     CHECK(check_conv_ptrs(q, weight, true, false, "weight"));
     CHECK(check_conv_ptrs(q, bias, false, false, "bias"));
     CHECK(check_conv_ptrs(q, top, true, true, "top"));
     CHECK(check_ws(workspace, ws_bytes, q.ws_fwd));
     if (is_bf16(q))
         return run_forward_bf16(q, bottom, weight, bias, top, (char*)workspace,
-                                (hipStream_t)stream);
+                                (hipStream_t)stream, bottom_staged);
     if (q.dense)
         return run_dense_forward(q, (const float*)bottom, (const float*)weight, bias, top,
                                  (char*)workspace, (hipStream_t)stream);
@@ -1901,6 +1923,57 @@ int caffe_pool_lrn_forward(const caffe_pool_desc* pd, const caffe_lrn_desc* ld,
                               ld->beta, ld->k, (hipStream_t)stream),
            "LRN forward launch");
     return CAFFE_OK;
+}
+
+int caffe_pool_lrn_forward_into(const caffe_pool_desc* pd, const caffe_lrn_desc* ld,
+                                const float* bottom, float* pooled, int32_t* mask, float* top,
+                                int32_t flags, const caffe_conv_desc* next, void* next_workspace,
+                                size_t next_ws_bytes, void* stream)
+{
+    if (flags & ~CAFFE_POOL_RELU_INPUT)
+        return fail(CAFFE_ERR_INVALID_ARG, "unknown pooling flags 0x%x", flags);
+    int Ho, Wo;
+    CHECK(check_pool_lrn(pd, ld, &Ho, &Wo));
+    ConvPlan qn;
+    if (!next)
+        return fail(CAFFE_ERR_INVALID_ARG, "next is NULL");
+    CHECK(plan_conv(next, &qn));
+    if (qn.N != ld->N || qn.C != ld->C || qn.H != ld->H || qn.W != ld->W)
+        return fail(CAFFE_ERR_INVALID_ARG, "the convolution's bottom (%d, %d, %d, %d) is not the "
+                    "LRN's top (%d, %d, %d, %d)", qn.N, qn.C, qn.H, qn.W, ld->N, ld->C, ld->H,
+                    ld->W);
+    if (!caffe_hip_stage_from_lrn_ok(qn, ld->local_size))
+        return fail(CAFFE_ERR_UNSUPPORTED, "the LRN's top cannot be staged for this convolution "
+                    "(bf16 mode, channel groups of a multiple of 16 unpadded, LRN size 3 or 5)");
+    CHECK(check_ws(next_workspace, next_ws_bytes, qn.ws_fwd));
+    const bool nz = pd->N > 0;
+    CHECK(check_ptr(bottom, nz, "bottom"));
+    CHECK(check_ptr(pooled, nz, "pooled"));
+    CHECK(check_ptr(mask, false, "mask"));
+    CHECK(check_ptr(top, nz, "top"));
+    hipStream_t s = (hipStream_t)stream;
+    LAUNCH(launch_maxpool_forward(bottom, pooled, mask, pd->N * pd->C, pd->H, pd->W, Ho, Wo,
+                                  pd->kernel_h, pd->kernel_w, pd->stride_h, pd->stride_w,
+                                  pd->pad_h, pd->pad_w, (flags & CAFFE_POOL_RELU_INPUT) ? 1 : 0,
+                                  s),
+           "max-pool forward launch");
+    uint16_t* xh = (uint16_t*)((char*)next_workspace + qn.off_xh_fwd);
+    LAUNCH(launch_lrn_forward_stage(pooled, top, ld->N, ld->C, ld->H, ld->W, ld->local_size,
+                                    ld->alpha, ld->beta, ld->k, xh, qn.XHp, qn.XWp, qn.ph, qn.pw,
+                                    s),
+           "LRN forward and staging launch");
+    return CAFFE_OK;
+}
+
+int caffe_pool_lrn_stage_supported(const caffe_pool_desc* pd, const caffe_lrn_desc* ld,
+                                   const caffe_conv_desc* next)
+{
+    int Ho, Wo;
+    ConvPlan qn;
+    if (check_pool_lrn(pd, ld, &Ho, &Wo) != CAFFE_OK || !next || plan_conv(next, &qn) != CAFFE_OK)
+        return 0;
+    return qn.N == ld->N && qn.C == ld->C && qn.H == ld->H && qn.W == ld->W &&
+           caffe_hip_stage_from_lrn_ok(qn, ld->local_size);
 }
 
 int caffe_lrn_pool_backward(const caffe_pool_desc* pd, const caffe_lrn_desc* ld,

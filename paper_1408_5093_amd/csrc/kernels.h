@@ -396,6 +396,13 @@ hipError_t launch_maxpool_forward(const float* x, float* y, int32_t* mask, int N
 hipError_t launch_maxpool_backward(const float* dy, const int32_t* mask, float* dx, int NC, int H,
                                    int W, int OH, int OW, int kh, int kw, int sh, int sw, int ph,
                                    int pw, hipStream_t s);
+// launch_lrn_forward whose output also goes, rounded to bf16, to the
+// zero-bordered staging Xp[n][h + tb][w + lb][c] (Hp x Wp pixels of C
+// channels, border written too) of a convolution that takes it as its
+// bottom; C a multiple of 16, size 3 or 5.
+hipError_t launch_lrn_forward_stage(const float* x, float* y, int N, int C, int H, int W,
+                                    int size, float alpha, float beta, float k, uint16_t* Xp,
+                                    int Hp, int Wp, int tb, int lb, hipStream_t s);
 hipError_t launch_lrn_forward(const float* x, float* y, int N, int C, int HW, int size,
                               float alpha, float beta, float k, hipStream_t s);
 hipError_t launch_lrn_backward(const float* x, const float* y, const float* dy, float* dx, int N,

@@ -443,13 +443,22 @@ __device__ __forceinline__ float pow_neg(float s, float beta)
     return __builtin_amdgcn_exp2f(-beta * __builtin_amdgcn_logf(s));
 }
 
+// The output's bf16 staging for a convolution that takes it as its bottom
+// (LrnStage): Xp[n][h + tb][w + lb][c] on an Hp x Wp grid of C channels.
+struct LrnStage {
+    uint16_t* Xp;
+    int W, Hp, Wp, tb, lb;
+};
+
 // One thread per (n, chunk of CH channels, pixel); lanes run along pixels.
 // Every input of the chunk and its halo is loaded up front (independent
-// loads), then the outputs are formed from registers.
-template <int SIZE, int CH>
+// loads), then the outputs are formed from registers.  STAGE: the chunk's
+// outputs also go to the staging, rounded to bf16 (two 16-byte stores).
+template <int SIZE, int CH, bool STAGE = false>
 __global__ void __launch_bounds__(256)
 lrn_forward_kernel(const float* __restrict__ x, float* __restrict__ y, int N, int C, int HW,
-                   int nchunks, FastDiv div_hw, float alpha_over_n, float beta, float k)
+                   int nchunks, FastDiv div_hw, float alpha_over_n, float beta, float k,
+                   LrnStage st = LrnStage{})
 {
     constexpr int PRE = (SIZE - 1) / 2;
     constexpr int NA = CH + SIZE - 1;
@@ -475,13 +484,32 @@ lrn_forward_kernel(const float* __restrict__ x, float* __restrict__ y, int N, in
 #pragma unroll
     for (int q = 0; q < NA; ++q)
         a[q] = buf_ld_f32(rx, off(c0 - PRE + q));
+    uint32_t packed[CH / 2];
 #pragma unroll
     for (int t = 0; t < CH; ++t) {
+        // explicit fused multiply-adds: every instantiation rounds alike
         float sq = 0.f;
 #pragma unroll
         for (int q = 0; q < SIZE; ++q)
-            sq += a[t + q] * a[t + q];
-        buf_st_f32(a[t + PRE] * pow_neg(k + alpha_over_n * sq, beta), ry, off(c0 + t));
+            sq = __builtin_fmaf(a[t + q], a[t + q], sq);
+        const float out = a[t + PRE] * pow_neg(__builtin_fmaf(alpha_over_n, sq, k), beta);
+        buf_st_f32(out, ry, off(c0 + t));
+        if constexpr (STAGE) {
+            const uint32_t h16 = f32_to_bf16_rne(out);
+            packed[t >> 1] = (t & 1) ? (packed[t >> 1] | (h16 << 16)) : h16;
+        }
+    }
+    if constexpr (STAGE) {
+        static_assert(CH % 8 == 0, "whole 16-byte chunks");
+        // (C is a multiple of CH: the chunk lies inside the image's channels)
+        const int h = pix / st.W;
+        const int w = pix - h * st.W;
+        uint16_t* dst =
+            st.Xp + (((size_t)n * st.Hp + h + st.tb) * st.Wp + w + st.lb) * C + c0;
+#pragma unroll
+        for (int j = 0; j < CH / 8; ++j)
+            *(u32x4*)(dst + 8 * j) = u32x4{packed[4 * j], packed[4 * j + 1], packed[4 * j + 2],
+                                           packed[4 * j + 3]};
     }
 }
 
@@ -622,6 +650,33 @@ hipError_t launch_lrn_forward(const float* x, float* y, int N, int C, int HW, in
     else
         hipLaunchKernelGGL(lrn_forward_any_kernel, dim3(grid_exact((long)N * C * HW)), dim3(256),
                            0, s, x, y, N, C, HW, size, an, beta, k);
+    return hipGetLastError();
+}
+
+hipError_t launch_lrn_forward_stage(const float* x, float* y, int N, int C, int H, int W,
+                                    int size, float alpha, float beta, float k, uint16_t* Xp,
+                                    int Hp, int Wp, int tb, int lb, hipStream_t s)
+{
+    if ((long)N * C * H * W == 0)
+        return hipSuccess;
+    if (C % kLrnChunk != 0 || (size != 5 && size != 3) || tb < 0 || lb < 0 || Hp < tb + H ||
+        Wp < lb + W || (((uintptr_t)Xp) & 15) != 0)
+        return hipErrorInvalidValue;
+    const hipError_t e = launch_dh_zero_border(Xp, N, Hp, Wp, tb, lb, H, W, C, s);
+    if (e != hipSuccess)
+        return e;
+    const int HW = H * W;
+    const float an = alpha / size;
+    const int nch = C / kLrnChunk;
+    const long threads = (long)N * nch * HW;
+    const FastDiv d = make_fastdiv((uint32_t)HW);
+    const LrnStage st{Xp, W, Hp, Wp, tb, lb};
+    if (size == 5)
+        hipLaunchKernelGGL((lrn_forward_kernel<5, kLrnChunk, true>), dim3(grid_exact(threads)),
+                           dim3(256), 0, s, x, y, N, C, HW, nch, d, an, beta, k, st);
+    else
+        hipLaunchKernelGGL((lrn_forward_kernel<3, kLrnChunk, true>), dim3(grid_exact(threads)),
+                           dim3(256), 0, s, x, y, N, C, HW, nch, d, an, beta, k, st);
     return hipGetLastError();
 }
 

@@ -14,8 +14,8 @@ call; this module only owns buffers and the call order.
 import torch
 
 from . import (BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED,
-               BACKWARD_TOP_STAGED, CAFFE_BF16_F32_BOTTOM, CAFFE_F32, caffe_conv_backward_into,
-               conv_stage_below_supported,
+               BACKWARD_TOP_STAGED, CAFFE_BF16_F32_BOTTOM, CAFFE_F32, FORWARD_BOTTOM_STAGED,
+               caffe_conv_backward_into, conv_stage_below_supported, pool_lrn_stage_supported,
                PASS_BACKWARD, PASS_BACKWARD_POOL_LRN, PASS_BACKWARD_WEIGHTS, PASS_FORWARD,
                POOL_RELU_INPUT, Workspace, caffe_conv_backward, caffe_conv_backward_pool_lrn,
                caffe_conv_forward, conv_desc, conv_out_shape, lrn_desc,
@@ -32,7 +32,8 @@ class ConvStack:
     (CAFFE_BF16_F32_BOTTOM); glue stays fp32."""
 
     def __init__(self, layers, N, weights, biases, glue=None, bf16=False, device="cuda",
-                 fuse_glue=True, split_backward=True, fuse_staging=True, chain_staging=True):
+                 fuse_glue=True, split_backward=True, fuse_staging=True, chain_staging=True,
+                 lrn_staging=True):
         self.layers = list(layers)
         self.N = N
         self.bf16 = bf16
@@ -173,6 +174,19 @@ class ConvStack:
         # the bf16 staging of its top gradient directly (the float gradient
         # is never stored); dbottom of the glue stage is then not written
         self.fuse_staging = [bf16 and fuse_staging and self.fused[l] for l in range(n)]
+        # bf16: a fused max-pool + LRN that feeds the next convolution also
+        # writes that layer's bf16 staging as it forms the LRN output
+        # (caffe_pool_lrn_forward_into), and the layer's forward then skips
+        # its own staging pass (CAFFE_FORWARD_BOTTOM_STAGED)
+        self.bottom_staged = [False] * n
+        if bf16 and lrn_staging:
+            for l in range(1, n):
+                if self.fused[l - 1]:
+                    pst, lst = self.stages[l - 1]
+                    p, r = pst["prm"], lst["prm"]
+                    self.bottom_staged[l] = pool_lrn_stage_supported(
+                        pst["in_shape"], p["kernel"], p["stride"], p.get("pad", 0), r["size"],
+                        r["alpha"], r["beta"], r["k"], self.descs[l])
         for l in range(n):
             if self.fuse_staging[l]:
                 pst, lst = self.stages[l]
@@ -199,13 +213,14 @@ class ConvStack:
         """x: (N, C, H, W) float32 device tensor.  Returns the last layer's top."""
         s = stream or torch.cuda.current_stream()
         cur = x
-        for l in range(len(self.layers)):
+        n_l = len(self.layers)
+        for l in range(n_l):
             L = self.layers[l]
             cur = cur.view(self.N, L.C, L.H, L.W)
             self.bottom[l] = cur
             self._mark(("fwd", l, "begin"), s)
             caffe_conv_forward(self.descs[l], cur, self.W[l], self.b[l], self.top[l], self.ws_of[l],
-                               s)
+                               s, flags=FORWARD_BOTTOM_STAGED if self.bottom_staged[l] else 0)
             self._mark(("fwd", l, "end"), s)
             cur = self.top[l]
             if self.fused[l]:
@@ -214,7 +229,10 @@ class ConvStack:
                 pst["x"], lst["x"] = cur, pst["y"]
                 pool_lrn_forward(cur, p["kernel"], p["stride"], p.get("pad", 0), r["size"],
                                  r["alpha"], r["beta"], r["k"], pooled=pst["y"], mask=pst["mask"],
-                                 out=lst["y"], flags=self.pool_flags[l], stream=s)
+                                 out=lst["y"], flags=self.pool_flags[l], stream=s,
+                                 stage_for=((self.descs[l + 1], self.ws_of[l + 1])
+                                            if l + 1 < n_l and self.bottom_staged[l + 1]
+                                            else None))
                 cur = lst["y"]
                 continue
             for st in self.stages[l]:

@@ -259,6 +259,10 @@ def test_pointer_checks_before_any_launch():
                P(0x100000), ws, None) == -1
     assert bwd(P(0x1000), P(0x1800), None, P(0x3000), P(0x4000), None, None, 0, 2,
                P(0x100000), ws, None) == -1
+    # forward flags: unknown ones, and a staged bottom is a bf16 mode's
+    fx = lambda fl: lib.caffe_conv_forward_ex(ctypes.byref(d), P(0x1000), P(0x2000), None,
+                                              P(0x3000), P(0x100000), ws, fl, None)
+    assert fx(2) == -1 and fx(cc.FORWARD_BOTTOM_STAGED) == -1
     bd = lib.caffe_conv_backward_data
     assert bd(ctypes.byref(d), P(0x1000), P(0x1800), P(0x2000), None, P(0x100000), ws, None) == -1
     bw = lib.caffe_conv_backward_weights
@@ -281,6 +285,20 @@ def test_glue_validation():
     assert lib.caffe_lrn_forward(ctypes.byref(ld), P(0x1000), P(0x2000), None) == -1
     ld = cc.lrn_desc((2, 3, 5, 5), 5, k=0.0)
     assert lib.caffe_lrn_forward(ctypes.byref(ld), P(0x1000), P(0x2000), None) == -1
+    # an LRN output staged for the next convolution: the shapes must meet,
+    # the convolution must run on bf16 operands with whole 16-channel groups
+    pd2 = cc.pool_desc((2, 96, 55, 55), 3, 2)
+    ld2 = cc.lrn_desc((2, 96, 27, 27), 5)
+    nxt = lambda C, dt: cc.conv_desc((2, C, 27, 27), (256, C // 2, 5, 5), 1, 2, 2, True, dt)
+    into = lambda nd: lib.caffe_pool_lrn_forward_into(
+        ctypes.byref(pd2), ctypes.byref(ld2), P(0x1000), P(0x2000), None, P(0x3000), 0,
+        ctypes.byref(nd), P(0x100000), 1 << 30, None)
+    assert lib.caffe_pool_lrn_stage_supported(ctypes.byref(pd2), ctypes.byref(ld2),
+                                              ctypes.byref(nxt(96, cc.CAFFE_BF16_F32_BOTTOM)))
+    for nd, code in [(nxt(96, cc.CAFFE_F32), -4), (nxt(192, cc.CAFFE_BF16_F32_BOTTOM), -1)]:
+        assert not lib.caffe_pool_lrn_stage_supported(ctypes.byref(pd2), ctypes.byref(ld2),
+                                                      ctypes.byref(nd))
+        assert into(nd) == code
     assert lib.caffe_cast_f32_to_bf16(P(0x1000), P(0x2000), -1, None) == -1
     assert lib.caffe_cast_f32_to_bf16(P(0x1002), P(0x2000), 5, None) == -2
 

@@ -447,6 +447,80 @@ def test_caffenet_bf16_step_chained_staging_matches():
             assert_close(_np(a.db[l]), _np(b.db[l]), 1e-6, f"layer {l} bias gradient")
 
 
+@pytest.mark.parametrize("case", [
+    # N, C, H, W, pool k/s, LRN size, next K, kernel, pad, group
+    (2, 32, 13, 13, 3, 2, 5, 24, 3, 1, 2),     # grouped, 16 channels a group, 6x6 image
+    (3, 48, 24, 19, 3, 2, 3, 40, 5, 2, 1),     # LRN size 3, ragged pixel count
+    (1, 96, 55, 55, 3, 2, 5, 64, 5, 2, 2),     # the conv1 -> conv2 geometry, one image
+])
+def test_lrn_forward_into_next_staging(case):
+    """A max-pool + LRN whose output is staged as the next bf16 convolution's
+    bottom (caffe_pool_lrn_forward_into), then that convolution run on the
+    staged bottom (CAFFE_FORWARD_BOTTOM_STAGED) and its weight gradient on
+    the same staging (CAFFE_BACKWARD_BOTTOM_STAGED): every output bit for
+    bit against the separate passes.  The staging workspace starts filled
+    with large finite values, so a border the fused pass fails to zero shows
+    up in the convolution's output."""
+    N, C, H, W, pk, ps, size, K, kk, pad, g = case
+    print(f"lrn staging case {case}", flush=True)
+    rng = np.random.default_rng([91, *case])
+    x = _t(np.maximum(rng.standard_normal((N, C, H, W)), 0))
+    prm = (pk, ps, 0, size, 1e-4 * 50, 0.75, 1.0)
+    Hp, Wp = cc.pool_out_shape(cc.pool_desc((N, C, H, W), pk, ps, 0))
+    nd = cc.conv_desc((N, C, Hp, Wp), (K, C // g, kk, kk), 1, pad, g, True,
+                      cc.CAFFE_BF16_F32_BOTTOM)
+    assert cc.pool_lrn_stage_supported(x.shape, *prm, nd)
+    w = _t(rng.standard_normal((K, C // g, kk, kk)) * 0.2, torch.bfloat16)
+    b = _t(rng.standard_normal(K) * 0.3)
+    ws_n = max(cc.conv_workspace_size(nd, cc.PASS_FORWARD),
+               cc.conv_workspace_size(nd, cc.PASS_BACKWARD))
+    ws = [torch.full((ws_n,), 0x7E, dtype=torch.uint8, device=DEV) for _ in range(2)]
+    outs = []
+    for staged in (False, True):
+        pooled, mask, y = cc.pool_lrn_forward(x, *prm, stage_for=(nd, ws[1]) if staged else None)
+        Ho, Wo = cc.conv_out_shape(nd)
+        top = torch.empty((N, K, Ho, Wo), device=DEV)
+        cc.caffe_conv_forward(nd, y, w, b, top, ws[staged],
+                              flags=cc.FORWARD_BOTTOM_STAGED if staged else 0)
+        gd = _t(np.random.default_rng(5).standard_normal(top.shape))
+        dW, db = torch.empty(w.shape, device=DEV), torch.empty(K, device=DEV)
+        cc.caffe_conv_backward(nd, gd, top, y, w, None, dW, db, flags=cc.BACKWARD_BOTTOM_STAGED,
+                               workspace=ws[staged])
+        torch.cuda.synchronize()
+        outs.append((pooled, mask, y, top, dW, db))
+    for name, a, c in zip(("pooled", "mask", "lrn", "top", "dW", "db"), *outs):
+        assert torch.equal(a, c), name
+    assert torch.isfinite(outs[1][3]).all()
+
+
+def test_caffenet_bf16_step_lrn_staging_matches():
+    """The bf16 step at N=512 with the LRN after conv1 and conv2 staging conv2's
+    and conv3's bf16 bottoms as it forms its output (the default) against the
+    step whose convolutions stage their own bottoms: every top, data, weight
+    and bias gradient bit for bit (the staged values are the same roundings of
+    the same floats), over two steps."""
+    N = 512
+    inp = wl.caffenet_step(N, wl.CAFFENET_STEP_BF16)
+    x = torch.from_numpy(inp["x"]).to(DEV)
+    g = torch.from_numpy(inp["top_diff"]).to(DEV)
+    nets = [ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(), bf16=True,
+                      lrn_staging=f) for f in (True, False)]
+    assert nets[0].bottom_staged == [False, True, True, False, False]
+    assert not any(nets[1].bottom_staged)
+    for _ in range(2):
+        for net in nets:
+            net.forward(x)
+            net.backward(g)
+        torch.cuda.synchronize()
+        a, b = nets
+        for l in range(len(wl.CAFFENET)):
+            assert torch.equal(a.top[l], b.top[l]), f"layer {l} top"
+            if not a.stage_into[l]:
+                assert torch.equal(a.dbottom[l], b.dbottom[l]), f"layer {l} data gradient"
+            assert torch.equal(a.dW[l], b.dW[l]), f"layer {l} weight gradient"
+            assert torch.equal(a.db[l], b.db[l]), f"layer {l} bias gradient"
+
+
 @pytest.mark.parametrize("tile", range(4))
 def test_forced_gemm_tiles_bf16(tile, overrides):
     """Every bf16 GEMM tile, forced for the forward and the data gradient,

@@ -1234,9 +1234,9 @@ bool fork_side(hipStream_t s, Fork* f)
     if (hipEventCreateWithFlags(&f->done, hipEventDisableTiming) != hipSuccess ||
         hipEventRecord(f->start, s) != hipSuccess ||
         hipStreamWaitEvent(f->side, f->start, 0) != hipSuccess) {
-        hipEventDestroy(f->start);
+        (void)hipEventDestroy(f->start);
         if (f->done)
-            hipEventDestroy(f->done);
+            (void)hipEventDestroy(f->done);
         return false;
     }
     return true;
@@ -1254,8 +1254,8 @@ int join_side(hipStream_t s, Fork& f, int st_a, int st_b)
         // caller's buffers or workspace once the error is returned
         (void)hipStreamSynchronize(f.side);
     }
-    hipEventDestroy(f.start);
-    hipEventDestroy(f.done);
+    (void)hipEventDestroy(f.start);
+    (void)hipEventDestroy(f.done);
     if (st_a != CAFFE_OK)
         return st_a;
     if (st_b != CAFFE_OK)
@@ -1275,7 +1275,7 @@ int stream_follow(hipStream_t follower, hipStream_t s)
         e = hipEventRecord(ev, s);
         if (e == hipSuccess)
             e = hipStreamWaitEvent(follower, ev, 0);
-        hipEventDestroy(ev);
+        (void)hipEventDestroy(ev);
     }
     if (e != hipSuccess)
         return hip_fail(e, "stream ordering");

@@ -445,9 +445,14 @@ __device__ __forceinline__ float pow_neg(float s, float beta)
 
 // The output's bf16 staging for a convolution that takes it as its bottom
 // (LrnStage): Xp[n][h + tb][w + lb][c] on an Hp x Wp grid of C channels.
+// Work mapping of the staging variant: a wave takes 64 pixels of one
+// chunk; a block, `wpb` chunks of the same 64 pixels; the `nb` blocks of a
+// pixel group (image n, pixels 64 grp ..) sit 8 ids apart, so that they run
+// on one XCD and each staged pixel's channels are written through one L2.
 struct LrnStage {
     uint16_t* Xp;
     int W, Hp, Wp, tb, lb;
+    int npg, nb, wpb;  // pixel groups per image, blocks per group, waves per block
 };
 
 // One thread per (n, chunk of CH channels, pixel); lanes run along pixels.
@@ -462,13 +467,28 @@ lrn_forward_kernel(const float* __restrict__ x, float* __restrict__ y, int N, in
 {
     constexpr int PRE = (SIZE - 1) / 2;
     constexpr int NA = CH + SIZE - 1;
-    const int e = blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= N * nchunks * HW)
-        return;
-    const int rest = udiv(e, div_hw);
-    const int pix = e - rest * HW;
-    const int n = rest / nchunks;
-    const int c0 = (rest - n * nchunks) * CH;
+    int n, c0, pix;
+    if constexpr (STAGE) {
+        const int xcd = blockIdx.x & 7;
+        const int r = blockIdx.x >> 3;
+        const int j = r % st.nb;
+        const int pg = (r / st.nb) * 8 + xcd;
+        if (pg >= N * st.npg)
+            return;
+        n = pg / st.npg;
+        pix = (pg - n * st.npg) * 64 + (threadIdx.x & 63);
+        c0 = (j * st.wpb + (threadIdx.x >> 6)) * CH;
+        if (pix >= HW)
+            return;
+    } else {
+        const int e = blockIdx.x * blockDim.x + threadIdx.x;
+        if (e >= N * nchunks * HW)
+            return;
+        const int rest = udiv(e, div_hw);
+        pix = e - rest * HW;
+        n = rest / nchunks;
+        c0 = (rest - n * nchunks) * CH;
+    }
     // Range-checked buffer accesses: a channel outside [0, C) gets an offset
     // with bit 31 set, which reads 0 / drops the store, so every load is
     // unconditional and all of them are in flight together.
@@ -668,15 +688,24 @@ hipError_t launch_lrn_forward_stage(const float* x, float* y, int N, int C, int 
     const int HW = H * W;
     const float an = alpha / size;
     const int nch = C / kLrnChunk;
-    const long threads = (long)N * nch * HW;
     const FastDiv d = make_fastdiv((uint32_t)HW);
-    const LrnStage st{Xp, W, Hp, Wp, tb, lb};
+    // waves per block: the largest divisor of the chunk count up to 4
+    int wpb = 4;
+    while (nch % wpb != 0)
+        --wpb;
+    const int npg = (HW + 63) / 64;
+    const int nb = nch / wpb;
+    const long groups8 = ((long)N * npg + 7) / 8;
+    if (groups8 * 8 * nb > INT_MAX)
+        return hipErrorInvalidValue;
+    const LrnStage st{Xp, W, Hp, Wp, tb, lb, npg, nb, wpb};
+    const dim3 grid((unsigned)(groups8 * 8 * nb)), block(64 * wpb);
     if (size == 5)
-        hipLaunchKernelGGL((lrn_forward_kernel<5, kLrnChunk, true>), dim3(grid_exact(threads)),
-                           dim3(256), 0, s, x, y, N, C, HW, nch, d, an, beta, k, st);
+        hipLaunchKernelGGL((lrn_forward_kernel<5, kLrnChunk, true>), grid, block, 0, s, x, y, N, C,
+                           HW, nch, d, an, beta, k, st);
     else
-        hipLaunchKernelGGL((lrn_forward_kernel<3, kLrnChunk, true>), dim3(grid_exact(threads)),
-                           dim3(256), 0, s, x, y, N, C, HW, nch, d, an, beta, k, st);
+        hipLaunchKernelGGL((lrn_forward_kernel<3, kLrnChunk, true>), grid, block, 0, s, x, y, N, C,
+                           HW, nch, d, an, beta, k, st);
     return hipGetLastError();
 }
 

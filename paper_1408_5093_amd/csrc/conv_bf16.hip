@@ -420,7 +420,7 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
                 float csum[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int ni = 0; ni < NI; ++ni) {
-                    uint32_t w2[2] = {0u, 0u};
+                    float vq[4];
 #pragma unroll
                     for (int b = 0; b < 4; ++b) {
                         const int q = 4 * qa + b;
@@ -432,8 +432,10 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
                         // (positions outside the image add nothing)
                         v = pbad[ni] ? 0.f : v;
                         csum[b] += v;
-                        w2[b >> 1] |= (uint32_t)f32_to_bf16_rne(v) << (16 * (b & 1));
+                        vq[b] = v;
                     }
+                    const uint32_t w2[2] = {f32x2_to_bf16x2_rne(vq[0], vq[1]),
+                                            f32x2_to_bf16x2_rne(vq[2], vq[3])};
                     // rows m .. m + 3 of this quad; a quad past M stores nothing
                     const int m = lrow0 + mi * MT + Op::row(4 * qa, lane);
                     const uint32_t off = ((uint32_t)(sb[ni] + m) * 2u) | pbad[ni] |
@@ -849,6 +851,12 @@ constexpr int stage_tile_pixels()
 // A staged value: bf16 as given, or a float rounded to nearest-even.
 __device__ __forceinline__ bf16_t to_bf16(bf16_t v) { return v; }
 __device__ __forceinline__ bf16_t to_bf16(float v) { return f32_to_bf16_rne(v); }
+// two staged values packed, the first in the low half
+__device__ __forceinline__ uint32_t to_bf16x2(bf16_t a, bf16_t b)
+{
+    return (uint32_t)a | ((uint32_t)b << 16);
+}
+__device__ __forceinline__ uint32_t to_bf16x2(float a, float b) { return f32x2_to_bf16x2_rne(a, b); }
 
 // Row-chunk staging (groups of a multiple of 8 channels, so that Cgp = Cg and
 // the staged channels are the blob's; rows of at most kStageRowPixels pixels):
@@ -1033,14 +1041,10 @@ stage_narrow_bf16_kernel(const T* __restrict__ X, bf16_t* __restrict__ Xp, int C
         for (int c = 0; c < CGP; ++c)
             v[t][c] = load_elem<T>(rx, voff, (uint32_t)c * plane);
     }
-    uint32_t w[4] = {0u, 0u, 0u, 0u};
+    uint32_t w[4];
 #pragma unroll
-    for (int t = 0; t < TPC; ++t)
-#pragma unroll
-        for (int c = 0; c < CGP; ++c) {
-            const int e = t * CGP + c;  // element of the chunk
-            w[e >> 1] |= (uint32_t)to_bf16(v[t][c]) << (16 * (e & 1));
-        }
+    for (int e = 0; e < 8; e += 2)  // elements e, e + 1 of the chunk: (tap, channel) pairs
+        w[e >> 1] = to_bf16x2(v[e / CGP][e % CGP], v[(e + 1) / CGP][(e + 1) % CGP]);
     *(u32x4*)&Xp[((size_t)n * per_image + q) * 8] = u32x4{w[0], w[1], w[2], w[3]};
 }
 

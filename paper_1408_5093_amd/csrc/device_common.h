@@ -56,14 +56,20 @@ __device__ __forceinline__ void buf_st_f32(float v, __amdgpu_buffer_rsrc_t r, ui
     __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, byte_off, 0, 0);
 }
 
-// float -> bfloat16 bits, round to nearest even (NaN kept quiet).
+// float -> bfloat16 bits, round to nearest even (a NaN stays a quiet NaN):
+// gfx950's conversion instruction, one per value or per pair.
+typedef __bf16 bf16x2_cvt __attribute__((ext_vector_type(2)));
+typedef float f32x2_cvt __attribute__((ext_vector_type(2)));
+
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f)
 {
-    uint32_t u = __builtin_bit_cast(uint32_t, f);
-    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu))
-        return (uint16_t)((u >> 16) | 0x0040u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
+    return __builtin_bit_cast(uint16_t, (__bf16)f);
+}
+
+// (lo, hi) -> their bfloat16 bits packed, lo in the low half
+__device__ __forceinline__ uint32_t f32x2_to_bf16x2_rne(float lo, float hi)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_cvt{lo, hi}, bf16x2_cvt));
 }
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t h)

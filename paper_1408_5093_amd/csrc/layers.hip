@@ -505,6 +505,7 @@ lrn_forward_kernel(const float* __restrict__ x, float* __restrict__ y, int N, in
     for (int q = 0; q < NA; ++q)
         a[q] = buf_ld_f32(rx, off(c0 - PRE + q));
     uint32_t packed[CH / 2];
+    float even = 0.f;
 #pragma unroll
     for (int t = 0; t < CH; ++t) {
         // explicit fused multiply-adds: every instantiation rounds alike
@@ -515,8 +516,10 @@ lrn_forward_kernel(const float* __restrict__ x, float* __restrict__ y, int N, in
         const float out = a[t + PRE] * pow_neg(__builtin_fmaf(alpha_over_n, sq, k), beta);
         buf_st_f32(out, ry, off(c0 + t));
         if constexpr (STAGE) {
-            const uint32_t h16 = f32_to_bf16_rne(out);
-            packed[t >> 1] = (t & 1) ? (packed[t >> 1] | (h16 << 16)) : h16;
+            if (t & 1)
+                packed[t >> 1] = f32x2_to_bf16x2_rne(even, out);
+            else
+                even = out;
         }
     }
     if constexpr (STAGE) {
@@ -884,6 +887,68 @@ __device__ __forceinline__ float fuse_gather(const FuseBlock& f,
     return sum;
 }
 
+// Phase 2 for the 3x3 / stride-2 window, four input positions at a time:
+// the positions (2a + dy - ph, 2b + dx - pw), dy, dx in {0, 1}, are covered
+// only by windows among rows a - 1, a and columns b - 1, b (row a - 1 only
+// for dy = 0, column b - 1 only for dx = 0), so the four records are read
+// once for all four, and each position adds its routed gradients in the
+// row-major window order of fuse_gather: the same sums, a quarter of the
+// LDS reads and of the index arithmetic.
+struct QuadMap {
+    int a_lo, nar, b_lo, nbc, groups, grp, bc;
+};
+
+__device__ __forceinline__ QuadMap quad_map(const FuseBlock& f, int W, int ph, int pw)
+{
+    QuadMap q;
+    q.a_lo = (f.y_lo + ph) >> 1;
+    q.nar = ((f.y_hi + ph) >> 1) - q.a_lo + 1;
+    q.b_lo = pw >> 1;
+    q.nbc = ((W - 1 + pw) >> 1) - q.b_lo + 1;   // <= 129 for W <= 256
+    q.groups = 256 / q.nbc;
+    q.grp = threadIdx.x / q.nbc;
+    q.bc = threadIdx.x - q.grp * q.nbc;
+    return q;
+}
+
+__device__ __forceinline__ void fuse_gather_quad(const FuseBlock& f,
+                                                 const float (&gs)[kFuseCh][kFusePos],
+                                                 const int32_t (&ms)[kFuseCh][kFusePos],
+                                                 int t, int a, int b, int W, int OH, int OW,
+                                                 int ph, int pw, float (&out)[2][2])
+{
+    float g[2][2];
+    int m[2][2];
+    bool ok[2][2];
+#pragma unroll
+    for (int di = 0; di < 2; ++di)
+#pragma unroll
+        for (int dj = 0; dj < 2; ++dj) {
+            const int i = a - 1 + di, j = b - 1 + dj;
+            ok[di][dj] = i >= 0 && i < OH && j >= 0 && j < OW;
+            // (clamped into the staged rows: a window a position outside
+            // the strip would need is read but never used)
+            const int o = (min(max(i, f.i_lo), f.i_hi) - f.i_lo) * OW + min(max(j, 0), OW - 1);
+            g[di][dj] = gs[t][o];
+            m[di][dj] = ms[t][o];
+        }
+#pragma unroll
+    for (int dy = 0; dy < 2; ++dy)
+#pragma unroll
+        for (int dx = 0; dx < 2; ++dx) {
+            const int hw = (2 * a + dy - ph) * W + 2 * b + dx - pw;
+            float sum = 0.f;
+#pragma unroll
+            for (int di = dy; di < 2; ++di)
+#pragma unroll
+                for (int dj = dx; dj < 2; ++dj) {
+                    if (ok[di][dj] && m[di][dj] == hw)
+                        sum += g[di][dj];
+                }
+            out[dy][dx] = sum;
+        }
+}
+
 template <int KS, int SS, int SIZE>
 __global__ void __launch_bounds__(256)
 lrn_pool_backward_kernel(const float* __restrict__ a_in, const float* __restrict__ b_in,
@@ -900,6 +965,33 @@ lrn_pool_backward_kernel(const float* __restrict__ a_in, const float* __restrict
     fuse_stage_pooled_grad<SIZE>(f, a_in, b_in, g_in, mask, gs, ms, N, C, OH, OW, alpha_over_n,
                                  beta, k);
     __syncthreads();
+    if constexpr (KS == 3 && SS == 2) {
+        // phase 2: thread -> one column pair b and every g-th row pair a
+        const QuadMap qm = quad_map(f, W, ph, pw);
+        if (qm.grp >= qm.groups)
+            return;
+        const int HW = H * W;
+        for (int t = 0; t < kFuseCh; ++t) {
+            const int ch = f.c0 + t;
+            if (ch >= C)
+                break;
+            float* dplane = dx + ((size_t)f.n * C + ch) * HW;
+            for (int ar = qm.grp; ar < qm.nar; ar += qm.groups) {
+                const int a = qm.a_lo + ar, b = qm.b_lo + qm.bc;
+                float q[2][2];
+                fuse_gather_quad(f, gs, ms, t, a, b, W, OH, OW, ph, pw, q);
+#pragma unroll
+                for (int dy = 0; dy < 2; ++dy)
+#pragma unroll
+                    for (int ex = 0; ex < 2; ++ex) {
+                        const int h = 2 * a + dy - ph, w = 2 * b + ex - pw;
+                        if (h >= f.y_lo && h <= f.y_hi && w >= 0 && w < W)
+                            dplane[h * W + w] = q[dy][ex];
+                    }
+            }
+        }
+        return;
+    }
     // phase 2: thread -> one input column w (threads past the last full group
     // of W columns idle) and every g-th row of each channel
     const int groups = 256 / W;             // W <= 256 (the staged rows hold >= 1 row)
@@ -916,8 +1008,8 @@ lrn_pool_backward_kernel(const float* __restrict__ a_in, const float* __restrict
         float* dplane = dx + ((size_t)f.n * C + ch) * HW;
         for (int hh = grp; hh < ny; hh += groups) {
             const int h = f.y_lo + hh;
-            dplane[h * W + w] = fuse_gather<KS, SS>(f, gs, ms, t, h, w, W, OH, OW, kh, kw, sh, sw,
-                                                    ph, pw);
+            dplane[h * W + w] = fuse_gather<KS, SS>(f, gs, ms, t, h, w, W, OH, OW, kh, kw,
+                                                          sh, sw, ph, pw);
         }
     }
 }
@@ -965,7 +1057,64 @@ lrn_pool_backward_bf16_kernel(const float* __restrict__ a_in, const float* __res
 #pragma unroll
     for (int t = 0; t < kFuseCh; ++t)
         bsum[t] = 0.f;
-    if (grp < groups) {
+    if constexpr (KS == 3 && SS == 2) {
+        // thread -> one column pair b and every g-th row pair a; each of
+        // the four positions stores its 16 channels as two 16-byte chunks
+        const QuadMap qm = quad_map(f, W, ph, pw);
+        for (int ar = qm.grp; qm.grp < qm.groups && ar < qm.nar; ar += qm.groups) {
+            const int a = qm.a_lo + ar, b = qm.b_lo + qm.bc;
+            bool in[2][2];
+#pragma unroll
+            for (int dy = 0; dy < 2; ++dy)
+#pragma unroll
+                for (int ex = 0; ex < 2; ++ex) {
+                    const int h = 2 * a + dy - ph, w = 2 * b + ex - pw;
+                    in[dy][ex] = h >= f.y_lo && h <= f.y_hi && w >= 0 && w < W;
+                }
+            uint32_t packed[2][2][kFuseCh / 2];
+#pragma unroll
+            for (int t = 0; t < kFuseCh; t += 2) {
+                float q[2][2][2];
+                fuse_gather_quad(f, gs, ms, t, a, b, W, OH, OW, ph, pw, q[0]);
+                fuse_gather_quad(f, gs, ms, t + 1, a, b, W, OH, OW, ph, pw, q[1]);
+#pragma unroll
+                for (int dy = 0; dy < 2; ++dy)
+#pragma unroll
+                    for (int ex = 0; ex < 2; ++ex) {
+                        float v[2] = {q[0][dy][ex], q[1][dy][ex]};
+                        if (relu_top) {
+                            const int h = 2 * a + dy - ph, w = 2 * b + ex - pw;
+#pragma unroll
+                            for (int u = 0; u < 2; ++u) {
+                                // (a NaN output masks too)
+                                const uint32_t o =
+                                    ((uint32_t)(((f.n * C + f.c0 + t + u) * H + h) * W + w) * 4u) |
+                                    ((uint32_t)!in[dy][ex] << 31);
+                                v[u] = buf_ld_f32(rt, o) > 0.f ? v[u] : 0.f;
+                            }
+                        }
+                        if (in[dy][ex]) {
+                            bsum[t] += v[0];
+                            bsum[t + 1] += v[1];
+                        }
+                        packed[dy][ex][t / 2] = f32x2_to_bf16x2_rne(v[0], v[1]);
+                    }
+            }
+#pragma unroll
+            for (int dy = 0; dy < 2; ++dy)
+#pragma unroll
+                for (int ex = 0; ex < 2; ++ex) {
+                    if (!in[dy][ex])
+                        continue;
+                    const int h = 2 * a + dy - ph, w = 2 * b + ex - pw;
+                    u32x4* dst =
+                        (u32x4*)&Dh[(((size_t)f.n * DHp + h + tb) * DWp + w + lb) * Ktot + cp0];
+                    const uint32_t* pk = packed[dy][ex];
+                    dst[0] = u32x4{pk[0], pk[1], pk[2], pk[3]};
+                    dst[1] = u32x4{pk[4], pk[5], pk[6], pk[7]};
+                }
+        }
+    } else if (grp < groups) {
         for (int hh = grp; hh < ny; hh += groups) {
             const int h = f.y_lo + hh;
             uint32_t packed[kFuseCh / 2];
@@ -974,8 +1123,8 @@ lrn_pool_backward_bf16_kernel(const float* __restrict__ a_in, const float* __res
                 float v[2];
 #pragma unroll
                 for (int u = 0; u < 2; ++u) {
-                    v[u] = fuse_gather<KS, SS>(f, gs, ms, t + u, h, w, W, OH, OW, kh, kw, sh, sw,
-                                               ph, pw);
+                    v[u] = fuse_gather<KS, SS>(f, gs, ms, t + u, h, w, W, OH, OW, kh, kw,
+                                                     sh, sw, ph, pw);
                     if (relu_top) {
                         // (a NaN output masks too)
                         const uint32_t o = (uint32_t)(((f.n * C + f.c0 + t + u) * H + h) * W + w);
@@ -983,8 +1132,7 @@ lrn_pool_backward_bf16_kernel(const float* __restrict__ a_in, const float* __res
                     }
                     bsum[t + u] += v[u];
                 }
-                packed[t / 2] = (uint32_t)f32_to_bf16_rne(v[0]) |
-                                ((uint32_t)f32_to_bf16_rne(v[1]) << 16);
+                packed[t / 2] = f32x2_to_bf16x2_rne(v[0], v[1]);
             }
             u32x4* dst = (u32x4*)&Dh[(((size_t)f.n * DHp + h + tb) * DWp + w + lb) * Ktot + cp0];
             dst[0] = u32x4{packed[0], packed[1], packed[2], packed[3]};
@@ -1174,10 +1322,10 @@ cast_f32_bf16_kernel(const float* __restrict__ x, uint16_t* __restrict__ y, int6
         const float4 a = ((const float4*)x)[2 * i];
         const float4 b = ((const float4*)x)[2 * i + 1];
         u32x4 o;
-        o[0] = (uint32_t)f32_to_bf16_rne(a.x) | ((uint32_t)f32_to_bf16_rne(a.y) << 16);
-        o[1] = (uint32_t)f32_to_bf16_rne(a.z) | ((uint32_t)f32_to_bf16_rne(a.w) << 16);
-        o[2] = (uint32_t)f32_to_bf16_rne(b.x) | ((uint32_t)f32_to_bf16_rne(b.y) << 16);
-        o[3] = (uint32_t)f32_to_bf16_rne(b.z) | ((uint32_t)f32_to_bf16_rne(b.w) << 16);
+        o[0] = f32x2_to_bf16x2_rne(a.x, a.y);
+        o[1] = f32x2_to_bf16x2_rne(a.z, a.w);
+        o[2] = f32x2_to_bf16x2_rne(b.x, b.y);
+        o[3] = f32x2_to_bf16x2_rne(b.z, b.w);
         ((u32x4*)y)[i] = o;
     }
     for (int64_t e = 8 * n8 + t0; e < count; e += stride)

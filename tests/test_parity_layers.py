@@ -144,6 +144,29 @@ def test_pool_lrn_fused(shape, pk, ps, pp, size, alpha, beta, k, relu_input):
     assert_close(_np(dx), _np(dx2), 1e-6, "fused vs separate backward")
 
 
+@pytest.mark.parametrize("shape,pk,ps,pp,size,alpha,beta,k",
+                         [c for c in FUSED if c[1:3] == (3, 2)])
+def test_pool_lrn_backward_empty_windows(shape, pk, ps, pp, size, alpha, beta, k):
+    """The fused backward (3x3 / stride 2: four input positions per thread
+    from one read of their covering windows) on a ReLU input where about half
+    the windows hold no winner: against the separate LRN and pool backward
+    passes and the oracle."""
+    print(f"fused backward, empty windows {shape} pool {pk}/{ps}/{pp}", flush=True)
+    rng = np.random.default_rng([6, *shape, pp])
+    x = np.maximum(rng.standard_normal(shape) - 1.5, 0).astype(np.float32)
+    pooled, mask, y = cc.pool_lrn_forward(_t(x), pk, ps, pp, size, alpha, beta, k,
+                                          flags=cc.POOL_RELU_INPUT)
+    assert (_np(mask) == -1).mean() > 0.2
+    g = rng.standard_normal(tuple(y.shape)).astype(np.float32)
+    dx = cc.lrn_pool_backward(shape, pooled, y, _t(g), mask, pk, ps, pp, size, alpha, beta, k)
+    dp2 = cc.lrn_backward(pooled, y, _t(g), size, alpha, beta, k)
+    dx2 = cc.maxpool_backward(shape, dp2, mask, pk, ps, pp)
+    assert_close(_np(dx), _np(dx2), 1e-6, "fused vs separate backward")
+    dp_ref = oracle.lrn_backward(_np(pooled), g, size, alpha, beta, k)
+    dx_ref = oracle.maxpool_backward(x, dp_ref, pk, ps, pp) * (x > 0)
+    assert_close(_np(dx), dx_ref, TOL_F32, "fused backward vs the oracle")
+
+
 def test_pool_lrn_fused_unsupported_and_empty():
     # 3 staged pooled rows of 200 columns exceed 256 positions
     assert not cc.pool_lrn_supported((1, 4, 401, 401), 3, 2, 0, 5)

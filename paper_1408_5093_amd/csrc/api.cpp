@@ -69,6 +69,7 @@ struct ConvPlan {
     int fwd_rpad;
     size_t off_taps_fwd;
     int blocked, xcd_order, wgrad_xcd_order;  // reduction and tile orders (see kernels.h)
+    bool wgrad_unit_order;                    // bf16 weight gradient: units per XCD
     // workspace layout (byte offsets), per pass
     size_t off_d, off_sums, off_wt, off_part;
     size_t ws_fwd, ws_data, ws_weights, ws_both;
@@ -456,6 +457,19 @@ int plan_bf16(ConvPlan* p)
     int64_t splits = (target + tiles - 1) / tiles;
     const int64_t max_splits = std::max<int64_t>(1, ncol / (8 * tk));
     const int64_t max_by_bytes = std::max<int64_t>(1, kMaxTensorBytes / (rw * q.K * 4));
+    // Unit order (see WgradBf16Params::unit_order) where a (group, split)
+    // unit holds at least 7 tiles: measured on the CaffeNet layers at N=512,
+    // each unit's slab then comes from HBM once instead of once per tile
+    // (conv3-5: 4-6x fewer bytes); with fewer tiles per unit (conv1, conv2)
+    // the linear order was as fast or faster.  The split count then becomes
+    // a multiple of 8 / gcd(G, 8), so that every XCD takes as many units.
+    const int64_t per_unit = tiles / q.G;
+    const int uo = env_tile("CAFFE_BF16_WGRAD_UNIT_ORDER");
+    q.wgrad_unit_order = uo >= 0 ? uo != 0 : per_unit >= 7;
+    if (q.wgrad_unit_order) {
+        const int64_t m = q.G % 8 == 0 ? 1 : q.G % 4 == 0 ? 2 : q.G % 2 == 0 ? 4 : 8;
+        splits = std::max<int64_t>(m, (splits + m / 2) / m * m);
+    }
     splits = std::max<int64_t>(1, std::min(std::min(splits, max_splits), max_by_bytes));
     int64_t cps = (ncol + splits - 1) / splits;
     cps = std::max<int64_t>(tk, (cps + tk - 1) / tk * tk);
@@ -1186,6 +1200,7 @@ int run_weights_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom, 
     p.splits = q.splits;
     p.div_ohw = make_fastdiv((uint32_t)(q.Ho * q.Wo));
     p.div_ow = make_fastdiv((uint32_t)q.Wo);
+    p.unit_order = q.wgrad_unit_order ? 1 : 0;
     LAUNCH(launch_conv_wgrad_bf16(p, q.wgrad_tile, s), "bf16 weight-gradient launch");
     LAUNCH(launch_wgrad_reduce_perm(part, weight_diff, q.K, q.Rw, q.Cgp, q.Cg, q.kh, q.kw, q.kwp,
                                     q.s2d ? q.s2d : 1, q.splits, accumulate, s),

@@ -588,7 +588,15 @@ conv_wgrad_bf16_kernel(const WgradBf16Params p)
     const int wn = wave / WM;
     const int n_rt = (p.Rw + TN - 1) / TN;
     const int n_mt = (p.Kg + TM - 1) / TM;
-    const int T = blockIdx.x;
+    int T = blockIdx.x;
+    if (p.unit_order) {
+        // workgroups are dealt round-robin over the 8 XCDs: slot s of XCD x
+        // takes block s % U of unit (s / U) * 8 + x
+        const int U = n_rt * n_mt;
+        const int slot = blockIdx.x >> 3;
+        const int unit = (slot / U) * 8 + (blockIdx.x & 7);
+        T = unit * U + slot % U;
+    }
     if (T >= n_rt * n_mt * p.G * p.splits)
         return;
     const int rt = T % n_rt;
@@ -1343,7 +1351,12 @@ template <int WM, int WN, int MI, int NI>
 hipError_t launch_wg(const WgradBf16Params& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * 32, TN = WN * NI * 32;
-    const int64_t tiles = (int64_t)((p.Rw + TN - 1) / TN) * ((p.Kg + TM - 1) / TM) * p.G * p.splits;
+    const int64_t per_unit = (int64_t)((p.Rw + TN - 1) / TN) * ((p.Kg + TM - 1) / TM);
+    const int64_t units = (int64_t)p.G * p.splits;
+    // unit order: whole rounds of 8 units (the blocks past the last unit exit)
+    const int64_t tiles = p.unit_order ? (units + 7) / 8 * 8 * per_unit : units * per_unit;
+    if (tiles > INT_MAX)
+        return hipErrorInvalidValue;
     hipLaunchKernelGGL((conv_wgrad_bf16_kernel<WM, WN, MI, NI, 3>), dim3((unsigned)tiles),
                        dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();

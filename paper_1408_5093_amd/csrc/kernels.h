@@ -301,6 +301,11 @@ struct WgradBf16Params {
     int Rw, G;
     int Ncol, cols_per_split, splits;
     FastDiv div_ohw, div_ow;
+    // 1: the blocks of one (group, split) unit -- every row and column tile,
+    // all reading the same top-gradient and input slab -- run on one XCD,
+    // units dealt round-robin over the 8 XCDs, so that the slab is fetched
+    // from HBM once into that XCD's L2
+    int unit_order;
 };
 constexpr int kBf16WgradTK = 64;  // output pixels per weight-gradient stage
 // bf16 weight-gradient tiles (output channels x reduction indices r); with

@@ -521,6 +521,38 @@ def test_caffenet_bf16_step_lrn_staging_matches():
             assert torch.equal(a.db[l], b.db[l]), f"layer {l} bias gradient"
 
 
+@pytest.mark.parametrize("case", [
+    # N, C, H, W, K, k, pad, group, blocks (the split target; 0: the default)
+    (4, 256, 13, 13, 128, 3, 1, 1, 0),     # one split: one unit, seven empty ones exit
+    (48, 256, 13, 13, 256, 3, 1, 2, 72),   # 2 groups x 8 splits: two units per XCD
+    (24, 256, 13, 11, 192, 3, 1, 2, 108),  # 96-row tiles, 2 groups x 6 splits, ragged
+])
+def test_wgrad_unit_order_bf16(case, overrides):
+    """The bf16 weight gradient with each (group, split) unit's tiles on one
+    XCD against the linear tile order at the same split count: the same
+    partial sums in the same order, so the same bits; and the oracle on the
+    rounded operands."""
+    N, C, H, W, K, k, pad, g, blocks = case
+    print(f"bf16 wgrad unit order {case}", flush=True)
+    rng = np.random.default_rng([79, *case])
+    xr = wl.round_bf16(rng.standard_normal((N, C, H, W)).astype(np.float32))
+    wr = wl.round_bf16((rng.standard_normal((K, C // g, k, k)) * 0.2).astype(np.float32))
+    gd = wl.round_bf16(rng.standard_normal((N, K, H + 2 * pad - k + 1,
+                                            W + 2 * pad - k + 1)).astype(np.float32))
+    xb, wb = _t(xr, torch.bfloat16), _t(wr, torch.bfloat16)
+    if blocks:
+        overrides.setenv("CAFFE_CONV_WGRAD_BLOCKS", str(blocks))
+    dws = []
+    for order in ("1", "0"):
+        overrides.setenv("CAFFE_BF16_WGRAD_UNIT_ORDER", order)
+        _, dw, _ = cc.conv_backward(xb, wb, _t(gd), None, 1, pad, g, need=("dw",))
+        torch.cuda.synchronize()
+        dws.append(dw)
+    assert torch.equal(dws[0], dws[1])
+    _, dw_ref, _ = oracle.conv_backward(xr, wr, gd, stride=1, pad=pad, group=g, need=("dw",))
+    assert_close(_np(dws[0]), dw_ref, TOL_F32, "weight gradient (rounded operands)")
+
+
 @pytest.mark.parametrize("tile", range(4))
 def test_forced_gemm_tiles_bf16(tile, overrides):
     """Every bf16 GEMM tile, forced for the forward and the data gradient,

@@ -586,6 +586,12 @@ int plan_conv(const caffe_conv_desc* d, ConvPlan* p)
     int64_t splits = (target + tiles - 1) / tiles;
     const int64_t max_splits = std::max<int64_t>(1, ncol / (8 * tk));
     const int64_t max_by_bytes = std::max<int64_t>(1, kMaxTensorBytes / (q.weight_elems * 4));
+    // unit order (WgradParams::unit_order): splits a multiple of 8 / gcd(G, 8)
+    q.wgrad_unit_order = env_tile("CAFFE_CONV_WGRAD_UNIT_ORDER") > 0;
+    if (q.wgrad_unit_order) {
+        const int64_t m = q.G % 8 == 0 ? 1 : q.G % 4 == 0 ? 2 : q.G % 2 == 0 ? 4 : 8;
+        splits = std::max<int64_t>(m, (splits + m / 2) / m * m);
+    }
     splits = std::max<int64_t>(1, std::min(std::min(splits, max_splits), max_by_bytes));
     int64_t cps = (ncol + splits - 1) / splits;
     cps = std::max<int64_t>(tk, (cps + tk - 1) / tk * tk);
@@ -931,6 +937,7 @@ int run_weights(const ConvPlan& q, const float* dsrc, const void* bottom, float*
     p.div_ohw = make_fastdiv((uint32_t)(q.Ho * q.Wo));
     p.div_ow = make_fastdiv((uint32_t)q.Wo);
     p.xcd_order = q.wgrad_xcd_order;
+    p.unit_order = q.wgrad_unit_order ? 1 : 0;
     if (q.wgrad_quad) {
         uint32_t* tab = (uint32_t*)(ws + q.off_coltab);
         LAUNCH(launch_wgrad_col_table(tab, (int)p.Ncol, q.ncol_pad, q.C, q.H, q.W, q.K, q.Ho,

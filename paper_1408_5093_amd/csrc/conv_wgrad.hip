@@ -17,6 +17,28 @@
 
 namespace caffe_hip {
 
+// The logical tile of this workgroup (workgroup L runs on XCD L % 8):
+// linear; XCD-contiguous (tile (L % 8) * per_xcd + L / 8, per_xcd = the
+// grid / 8); or unit order, where slot s = L / 8 of XCD x takes tile s % U of
+// unit (s / U) * 8 + x, U = per_unit the tiles of one (group, split) unit.
+__device__ __forceinline__ int wgrad_tile_index(const WgradParams& p, int per_unit)
+{
+    if (p.unit_order) {
+        const int slot = blockIdx.x >> 3;
+        return ((slot / per_unit) * 8 + (blockIdx.x & 7)) * per_unit + slot % per_unit;
+    }
+    const int per_xcd = gridDim.x >> 3;
+    return p.xcd_order ? (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3) : blockIdx.x;
+}
+
+// Workgroups of a weight-gradient launch: whole rounds of 8 XCDs of tiles,
+// or of units in unit order (the workgroups past the last tile exit).
+static int64_t wgrad_grid(const WgradParams& p, int64_t per_unit)
+{
+    const int64_t units = (int64_t)p.G * p.splits;
+    return p.unit_order ? (units + 7) / 8 * 8 * per_unit : (units * per_unit + 7) / 8 * 8;
+}
+
 template <int WM, int WN, int MI, int NI, int TK, int KH, int KW, int SH, int SW>
 __global__ void __launch_bounds__(64 * WM * WN)
 conv_wgrad_f32_kernel(const WgradParams p)
@@ -46,13 +68,12 @@ conv_wgrad_f32_kernel(const WgradParams p)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave % WM;
     const int wn = wave / WM;
-    // XCD-contiguous tile order (workgroup L runs on XCD L % 8; tile
-    // T = (L % 8) * per_xcd + L / 8).  Tap tiles vary fastest, then row tiles:
-    // the workgroups sharing a split's diff rows run together on one XCD.
+    // Tap tiles vary fastest, then row tiles (see wgrad_tile_index): in the
+    // XCD-contiguous and unit orders the workgroups sharing a split's diff
+    // rows run together on one XCD.
     const int n_rt = (p.R + TN - 1) / TN;
     const int n_mt = (p.Kg + TM - 1) / TM;
-    const int per_xcd = gridDim.x >> 3;
-    const int T = p.xcd_order ? (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3) : blockIdx.x;
+    const int T = wgrad_tile_index(p, n_rt * n_mt);
     if (T >= n_rt * n_mt * p.G * p.splits)
         return;
     const int rt = T % n_rt;
@@ -342,8 +363,7 @@ conv_wgrad_quad_f32_kernel(const WgradParams p)
     const int wn = wave / WM;
     const int n_rt = (p.R + TN - 1) / TN;
     const int n_mt = (p.Kg + TM - 1) / TM;
-    const int per_xcd = gridDim.x >> 3;
-    const int T = p.xcd_order ? (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3) : blockIdx.x;
+    const int T = wgrad_tile_index(p, n_rt * n_mt);
     if (T >= n_rt * n_mt * p.G * p.splits)
         return;
     const int rt = T % n_rt;
@@ -609,8 +629,7 @@ conv_wgrad_dma_f32_kernel(const WgradParams p)
     const int wn = wave / WM;
     const int n_rt = (p.R + TN - 1) / TN;
     const int n_mt = (p.Kg + TM - 1) / TM;
-    const int per_xcd = gridDim.x >> 3;
-    const int T = p.xcd_order ? (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3) : blockIdx.x;
+    const int T = wgrad_tile_index(p, n_rt * n_mt);
     if (T >= n_rt * n_mt * p.G * p.splits)
         return;
     const int rt = T % n_rt;
@@ -856,11 +875,11 @@ template <int WM, int WN, int MI, int NI, int KH, int KW, int SH, int SW>
 hipError_t launch_w(const WgradParams& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * 32, TN = WN * NI * 32;
-    const int64_t tiles =
-        (int64_t)((p.R + TN - 1) / TN) * ((p.Kg + TM - 1) / TM) * p.G * p.splits;
-    const int64_t per_xcd = (tiles + 7) / 8;  // 8 XCDs; see the kernel's tile order
+    const int64_t grid = wgrad_grid(p, (int64_t)((p.R + TN - 1) / TN) * ((p.Kg + TM - 1) / TM));
+    if (grid > INT_MAX)
+        return hipErrorInvalidValue;
     hipLaunchKernelGGL((conv_wgrad_f32_kernel<WM, WN, MI, NI, kTK, KH, KW, SH, SW>),
-                       dim3((unsigned)(per_xcd * 8)), dim3(64 * WM * WN), 0, s, p);
+                       dim3((unsigned)grid), dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();
 }
 
@@ -905,11 +924,11 @@ template <int WM, int WN, int MI, int NI, int KH, int KW>
 hipError_t launch_wq(const WgradParams& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * 32, TN = WN * NI * 32;
-    const int64_t tiles =
-        (int64_t)((p.R + TN - 1) / TN) * ((p.Kg + TM - 1) / TM) * p.G * p.splits;
-    const int64_t per_xcd = (tiles + 7) / 8;
+    const int64_t grid = wgrad_grid(p, (int64_t)((p.R + TN - 1) / TN) * ((p.Kg + TM - 1) / TM));
+    if (grid > INT_MAX)
+        return hipErrorInvalidValue;
     hipLaunchKernelGGL((conv_wgrad_quad_f32_kernel<WM, WN, MI, NI, KH, KW>),
-                       dim3((unsigned)(per_xcd * 8)), dim3(64 * WM * WN), 0, s, p);
+                       dim3((unsigned)grid), dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();
 }
 
@@ -929,11 +948,11 @@ template <int WM, int WN, int MI, int NI, int KH, int KW>
 hipError_t launch_wd(const WgradParams& p, hipStream_t s)
 {
     constexpr int TM = WM * MI * 32, TN = WN * NI * 32;
-    const int64_t tiles =
-        (int64_t)((p.R + TN - 1) / TN) * ((p.Kg + TM - 1) / TM) * p.G * p.splits;
-    const int64_t per_xcd = (tiles + 7) / 8;
+    const int64_t grid = wgrad_grid(p, (int64_t)((p.R + TN - 1) / TN) * ((p.Kg + TM - 1) / TM));
+    if (grid > INT_MAX)
+        return hipErrorInvalidValue;
     hipLaunchKernelGGL((conv_wgrad_dma_f32_kernel<WM, WN, MI, NI, KH, KW>),
-                       dim3((unsigned)(per_xcd * 8)), dim3(64 * WM * WN), 0, s, p);
+                       dim3((unsigned)grid), dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();
 }
 

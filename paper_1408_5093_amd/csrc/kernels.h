@@ -52,6 +52,10 @@ struct ConvGemmParams {
     int psh, psw, a0h, a0w, oph, opw, Cg_out;
     int blocked;    // channel-blocked reduction order (else tap-major), with tap_major
     int xcd_order;  // XCD-contiguous tile order (else linear)
+    // 1: unit order instead (every row and column tile of one (group, split)
+    // unit on one XCD, units dealt round-robin over the XCDs; the grid is
+    // whole rounds of 8 units, see wgrad_grid)
+    int unit_order;
     int splits, stages_per_split;  // dense split-K GEMM only
     FastDiv div_pss, div_psw;  // epi 1: phases psh*psw and psw
     // epi 0 / 1, tail_splits > 1: the tiles from tail_T on (whole column
@@ -123,6 +127,10 @@ struct WgradParams {
     int Ncol, cols_per_split, splits;
     FastDiv div_ohw, div_ow;
     int xcd_order;  // XCD-contiguous tile order (else linear)
+    // 1: unit order instead (every row and column tile of one (group, split)
+    // unit on one XCD, units dealt round-robin over the XCDs; the grid is
+    // whole rounds of 8 units, see wgrad_grid)
+    int unit_order;
     // quad-order kernel only: the per-column table (see
     // launch_wgrad_col_table) and the element shift of X's resource base
     const void* T;

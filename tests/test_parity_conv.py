@@ -243,6 +243,36 @@ def test_tail_split(case, splits, units, overrides):
     run_case(*case, relu=False, bias=False, seed=1)
 
 
+@pytest.mark.parametrize("case", [
+    # N, C, H, W, K, k, pad, group, blocks (the split target): which weight-
+    # gradient kernel runs follows from the shape (3x3 / 5x5 LDS-DMA, any-tap)
+    (12, 64, 13, 13, 128, 3, 1, 2, 48),    # 2 groups x 8 splits
+    (6, 48, 14, 11, 96, 5, 2, 1, 80),      # one group, 7 splits (the most), ragged
+    (5, 3, 23, 23, 32, 7, 0, 1, 0),        # the any-tap kernel, default splits
+])
+def test_wgrad_unit_order(case, overrides):
+    """The fp32 weight gradient with each (group, split) unit's tiles on one
+    XCD against the linear order at the same split count: the same partials
+    in the same order, so the same bits; and the oracle."""
+    N, C, H, W, K, k, pad, g, blocks = case
+    print(f"wgrad unit order {case}", flush=True)
+    rng = np.random.default_rng([80, *case])
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    w = rng.standard_normal((K, C // g, k, k)).astype(np.float32)
+    gd = rng.standard_normal((N, K, H + 2 * pad - k + 1, W + 2 * pad - k + 1)).astype(np.float32)
+    if blocks:
+        overrides.setenv("CAFFE_CONV_WGRAD_BLOCKS", str(blocks))
+    dws = []
+    for order in ("1", "0"):
+        overrides.setenv("CAFFE_CONV_WGRAD_UNIT_ORDER", order)
+        _, dw, _ = cc.conv_backward(_t(x), _t(w), _t(gd), None, 1, pad, g, need=("dw",))
+        torch.cuda.synchronize()
+        dws.append(dw)
+    assert torch.equal(dws[0], dws[1])
+    _, dw_ref, _ = oracle.conv_backward(x, w, gd, stride=1, pad=pad, group=g, need=("dw",))
+    assert_close(_np(dws[0]), dw_ref, TOL_F32, "weight gradient")
+
+
 def test_split_k_masked_bottom_and_default_plan(overrides):
     # the bottom mask applied by the data-gradient reduce; then a shape whose
     # own plan splits (one image, a long reduction)

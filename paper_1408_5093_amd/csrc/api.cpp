@@ -70,6 +70,7 @@ struct ConvPlan {
     size_t off_taps_fwd;
     int blocked, xcd_order, wgrad_xcd_order;  // reduction and tile orders (see kernels.h)
     bool wgrad_unit_order;                    // bf16 weight gradient: units per XCD
+    int dgrad_blocked;                        // bf16 data gradient: channel-blocked order
     // workspace layout (byte offsets), per pass
     size_t off_d, off_sums, off_wt, off_part;
     size_t ws_fwd, ws_data, ws_weights, ws_both;
@@ -480,6 +481,13 @@ int plan_bf16(ConvPlan* p)
     if (part_bytes > kMaxTensorBytes)
         return fail(CAFFE_ERR_UNSUPPORTED, "weight-gradient partials reach 2^31 bytes");
 
+    // data gradient in the channel-blocked reduction order (64-channel blocks
+    // of the top gradient outer, taps inner) where the channels allow it
+    {
+        const int bo = env_tile("CAFFE_BF16_DGRAD_BLOCKED");
+        const bool ok = q.Kgp % 64 == 0 && q.Th * q.Tw > 1;
+        q.dgrad_blocked = ok && bo != 0 ? 1 : 0;
+    }
     q.fwd_tile = pick_bf16_tile(q.Kg, env_tile("CAFFE_BF16_FWD_TILE"));
     q.dgrad_tile = pick_bf16_tile(q.Mt, env_tile("CAFFE_BF16_DGRAD_TILE"));
     const int pipe = env_tile("CAFFE_BF16_PIPE");
@@ -1139,7 +1147,7 @@ int run_data_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom_mask
                "staging border launch");
     uint16_t* wt = (uint16_t*)(ws + q.off_wt);
     LAUNCH(launch_dgrad_weights_bf16((const uint16_t*)weight, wt, q.G, q.Kg, q.Kgp, q.Cg, q.kh,
-                                     q.kw, q.sh, q.sw, q.Th, q.Tw, q.Rtp, s),
+                                     q.kw, q.sh, q.sw, q.Th, q.Tw, q.Rtp, q.dgrad_blocked, s),
            "bf16 weight transform launch");
     const int Ktot = q.G * q.Kgp;
     GemmBf16Params p = {};
@@ -1162,6 +1170,9 @@ int run_data_bf16(const ConvPlan& q, const uint16_t* dh, const void* bottom_mask
     p.psh = q.sh; p.psw = q.sw; p.a0h = q.a0h; p.a0w = q.a0w; p.oph = q.ph; p.opw = q.pw;
     p.Cg_out = q.Cg;
     p.xcd_order = q.xcd_order;
+    p.blocked = q.dgrad_blocked;
+    p.ntap = q.Th * q.Tw;
+    p.div_ntap = make_fastdiv((uint32_t)p.ntap);
     p.div_ohw = make_fastdiv((uint32_t)(q.Ah * q.Aw)); p.div_ow = make_fastdiv((uint32_t)q.Aw);
     p.div_pss = make_fastdiv((uint32_t)(q.sh * q.sw)); p.div_psw = make_fastdiv((uint32_t)q.sw);
     if (q.below) {

@@ -194,6 +194,16 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
     // byte offset of this lane's chunk of stage t from a column's pixel
     auto b_delta = [&](int t) -> uint32_t {
         const int kc = t * CH + ck;
+        if (p.blocked) {
+            // stage t: 64-channel block t / ntap of tap t % ntap
+            const int cb = (int)fdiv((uint32_t)t, p.div_ntap);
+            const int tap = t - cb * p.ntap;
+            const int u = (int)fdiv((uint32_t)tap, p.div_kw);
+            const int vg = tap - u * p.kw;
+            const uint32_t d =
+                (uint32_t)(u * p.IWp * p.Ctot + vg * p.vstr + 8 * (cb * CH + ck)) * 2u;
+            return kc < p.KC ? d : kOob;
+        }
         const int tg = (int)fdiv((uint32_t)kc, p.div_cg8);
         const int c8 = kc - tg * p.Cg8;
         const int u = (int)fdiv((uint32_t)tg, p.div_kw);
@@ -1253,7 +1263,8 @@ pack_weights_bf16_kernel(const bf16_t* __restrict__ W, bf16_t* __restrict__ Wp, 
 // zero past the kernel edge, for k >= Kg and for r >= Th*Tw*Kgp (rows padded to Rtp).
 __global__ void __launch_bounds__(256)
 dgrad_weights_bf16_kernel(const bf16_t* __restrict__ W, bf16_t* __restrict__ Wt, int G, int Kg,
-                          int Kgp, int Cg, int kh, int kw, int sh, int sw, int Th, int Tw, int Rtp)
+                          int Kgp, int Cg, int kh, int kw, int sh, int sw, int Th, int Tw, int Rtp,
+                          int blocked)
 {
     const int Mt = Cg * sh * sw;
     const long total = (long)G * Mt * Rtp;
@@ -1263,8 +1274,16 @@ dgrad_weights_bf16_kernel(const bf16_t* __restrict__ W, bf16_t* __restrict__ Wt,
         const long gm = e / Rtp;
         const int m = (int)(gm % Mt);
         const int g = (int)(gm / Mt);
-        const int t = r / Kgp;
-        const int k = r - t * Kgp;
+        int t, k;
+        if (blocked) {  // ((k / 64)*Th*Tw + t)*64 + k % 64
+            const int b = r / (Th * Tw * 64);
+            const int rem = r - b * Th * Tw * 64;
+            t = rem >> 6;
+            k = b * 64 + (rem & 63);
+        } else {
+            t = r / Kgp;
+            k = r - t * Kgp;
+        }
         bf16_t v = 0;
         if (t < Th * Tw && k < Kg) {
             const int th = t / Tw, tw = t - th * Tw;
@@ -1673,13 +1692,15 @@ hipError_t launch_stage_s2d_bf16(const void* X, int x_f32, uint16_t* Xp, int N, 
 
 hipError_t launch_dgrad_weights_bf16(const uint16_t* W, uint16_t* Wt, int G, int Kg, int Kgp,
                                      int Cg, int kh, int kw, int sh, int sw, int Th, int Tw,
-                                     int Rtp, hipStream_t s)
+                                     int Rtp, int blocked, hipStream_t s)
 {
     const long total = (long)G * Cg * sh * sw * Rtp;
     if (total == 0)
         return hipSuccess;
+    if (blocked && Kgp % 64 != 0)
+        return hipErrorInvalidValue;
     hipLaunchKernelGGL(dgrad_weights_bf16_kernel, dim3(grid_1d(total)), dim3(256), 0, s, W, Wt, G,
-                       Kg, Kgp, Cg, kh, kw, sh, sw, Th, Tw, Rtp);
+                       Kg, Kgp, Cg, kh, kw, sh, sw, Th, Tw, Rtp, blocked);
     return hipGetLastError();
 }
 

@@ -265,6 +265,12 @@ struct GemmBf16Params {
     int psh, psw, a0h, a0w, oph, opw, Cg_out;
     int xcd_order;
     FastDiv div_cg8, div_kw;
+    // blocked: the reduction runs over 64-channel blocks outer, taps inner
+    // (stage t = block t / ntap of tap t % ntap; A packed in that order), so
+    // that the workgroups of one XCD share fewer staged rows at a time
+    // (needs Cgp % 64 == 0 and one tap per tap group)
+    int blocked, ntap;
+    FastDiv div_ntap;
     // epilogue divisions: output pixels per image and per row (epi 0 and 1),
     // phases psh*psw and psw (epi 1)
     FastDiv div_ohw, div_ow, div_pss, div_psw;
@@ -374,10 +380,11 @@ hipError_t launch_stage_s2d_bf16(const void* X, int x_f32, uint16_t* Xp, int N, 
                                  hipStream_t s);
 
 // Wt[g][(c, fh, fw)][(th*Tw + tw)*Kgp + k] = W[g*Kg + k][c][fh + sh*(Th-1-th)][fw + sw*(Tw-1-tw)]
-// (0 past the kernel edge, for k >= Kg and past Th*Tw*Kgp).
+// (0 past the kernel edge, for k >= Kg and past Th*Tw*Kgp); blocked (Kgp % 64
+// == 0): the index ((k / 64)*Th*Tw + th*Tw + tw)*64 + k % 64 instead.
 hipError_t launch_dgrad_weights_bf16(const uint16_t* W, uint16_t* Wt, int G, int Kg, int Kgp,
                                      int Cg, int kh, int kw, int sh, int sw, int Th, int Tw,
-                                     int Rtp, hipStream_t s);
+                                     int Rtp, int blocked, hipStream_t s);
 
 // D = relu ? G * [Y > 0] : G (written to D unless D is null) and, unless
 // plane_sums is null, plane_sums[p] = sum of D over plane p (fixed order).

@@ -553,6 +553,19 @@ def test_wgrad_unit_order_bf16(case, overrides):
     assert_close(_np(dws[0]), dw_ref, TOL_F32, "weight gradient (rounded operands)")
 
 
+@pytest.mark.parametrize("blocked", ["0", "1"])
+def test_dgrad_channel_blocked_bf16(blocked, overrides):
+    """The data gradient with the reduction in 64-channel blocks outer, taps
+    inner (the default where the top gradient's channels per group are a
+    multiple of 64) and in the tap-major order: each against the oracle,
+    with several channel blocks, 3x3 and 5x5 taps, groups and the masked
+    bottom gradient."""
+    overrides.setenv("CAFFE_BF16_DGRAD_BLOCKED", blocked)
+    run_case(2, 32, 13, 11, 128, 3, 3, 1, 1, 1, 1, 1, True)        # 2 blocks, 9 taps
+    run_case(2, 48, 11, 12, 256, 5, 5, 1, 1, 2, 2, 2, False)       # 2 groups x 2 blocks
+    run_case(3, 16, 9, 9, 192, 3, 3, 1, 1, 1, 1, 1, True, flags=cc.BACKWARD_MASK_BOTTOM_DIFF)
+
+
 @pytest.mark.parametrize("tile", range(4))
 def test_forced_gemm_tiles_bf16(tile, overrides):
     """Every bf16 GEMM tile, forced for the forward and the data gradient,

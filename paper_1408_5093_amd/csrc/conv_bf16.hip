@@ -184,9 +184,9 @@ conv_gemm_bf16_kernel(const GemmBf16Params p)
 #pragma unroll
     for (int q = 0; q < NB; ++q) {
         const int col = min(n0 + RPI * (wave + NW * q) + cr, p.Ncol - 1);
-        const int n = col / OHW;
+        const int n = (int)fdiv((uint32_t)col, p.div_ohw);
         const int pix = col - n * OHW;
-        const int i = pix / p.OW;
+        const int i = (int)fdiv((uint32_t)pix, p.div_ow);
         const int j = pix - i * p.OW;
         b_pix[q] = (uint32_t)(((n * p.IHp + i * p.sh + p.oh0) * p.IWp + j * p.sw + p.ow0) *
                                   p.Ctot + g * p.Cgp) * 2u;

@@ -115,7 +115,10 @@ int caffe_pool_lrn_stage_supported(const caffe_pool_desc* pool, const caffe_lrn_
 /* The backward of that pair in one pass: bottom_diff as caffe_lrn_backward
  * (pooled, top, top_diff) followed by caffe_maxpool_backward (with `mask`)
  * would write it, without storing the pooled gradient (each block stages the
- * pooled gradient of its input rows' covering windows in LDS).
+ * pooled gradient of its input rows' covering windows in LDS).  top must be
+ * the LRN's forward output for `pooled` (caffe_pool_lrn_forward's): the
+ * pass forms it again from `pooled` as the forward kernel does, with the
+ * same bits, instead of reading it.
  * CAFFE_ERR_UNSUPPORTED unless lrn->local_size is 3 or 5, W <= 256 and
  * min(Ho, (kernel_h - 1) / stride_h + 2) * Wo <= 256 (a block stages at most
  * 256 pooled positions, one per thread). */

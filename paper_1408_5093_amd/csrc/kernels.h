@@ -434,6 +434,8 @@ hipError_t launch_lrn_backward(const float* x, const float* y, const float* dy, 
 bool pool_lrn_fusable(int H, int W, int OH, int OW, int kh, int sh, int ph, int size);
 // Row strips of the fused LRN + max-pool backward (0: not fusable).
 int lrn_pool_backward_strips(int H, int OH, int OW, int kh, int sh, int ph);
+// (Both fused backward launchers take the LRN's output `top` for the
+// interface only: the kernels form it again from `pooled`, bit for bit.)
 // The fused backward written as the bf16 top-gradient staging of the
 // convolution below (channels in groups of Kg, each padded to Kgp, Ktot in
 // all, on a DHp x DWp grid with the image at (tb, lb)), plus the grid's zero

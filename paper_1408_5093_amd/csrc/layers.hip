@@ -777,10 +777,14 @@ __device__ __forceinline__ FuseBlock fuse_block(int H, int OH, int kh, int sh, i
 
 // Phase 1: the pooled gradient (LRN backward) of the block's 16 channels at
 // every staged pooled position, and the winners, into LDS.
+// The LRN's output b = a s^-beta is not read: it is formed again from the
+// pooled inputs exactly as the forward kernel forms it (the same fused
+// multiply-adds, the same hardware exp2 / log2), so it has the same bits,
+// and the pass reads a fifth fewer bytes.
 template <int SIZE>
 __device__ __forceinline__ void fuse_stage_pooled_grad(
-    const FuseBlock& f, const float* __restrict__ a_in, const float* __restrict__ b_in,
-    const float* __restrict__ g_in, const int32_t* __restrict__ mask,
+    const FuseBlock& f, const float* __restrict__ a_in, const float* __restrict__ g_in,
+    const int32_t* __restrict__ mask,
     float (&gs)[kFuseCh][kFusePos], int32_t (&ms)[kFuseCh][kFusePos], int N, int C, int OH, int OW,
     float alpha_over_n, float beta, float k)
 {
@@ -797,7 +801,6 @@ __device__ __forceinline__ void fuse_stage_pooled_grad(
     const int pix = (f.i_lo + pos / OW) * OW + (pos - (pos / OW) * OW);
     const uint32_t bytes = (uint32_t)(N * C * OHW) * 4u;
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_in, bytes);
-    const __amdgpu_buffer_rsrc_t rb = make_rsrc(b_in, bytes);
     const __amdgpu_buffer_rsrc_t rg = make_rsrc(g_in, bytes);
     const __amdgpu_buffer_rsrc_t rm = make_rsrc(mask, bytes);
     const uint32_t base4 = (uint32_t)(f.n * C * OHW + pix) * 4u;
@@ -805,26 +808,27 @@ __device__ __forceinline__ void fuse_stage_pooled_grad(
     auto off = [&](int ch) {
         return (base4 + (uint32_t)ch * hw4) | ((uint32_t)((unsigned)ch >= (unsigned)C) << 31);
     };
-    float a[NA], g[NR], b[NR];
+    float a[NA], g[NR];
 #pragma unroll
     for (int q = 0; q < NA; ++q)
         a[q] = buf_ld_f32(ra, off(c0 - POST - PRE + q));
 #pragma unroll
-    for (int q = 0; q < NR; ++q) {
+    for (int q = 0; q < NR; ++q)
         g[q] = buf_ld_f32(rg, off(c0 - POST + q));
-        b[q] = buf_ld_f32(rb, off(c0 - POST + q));
-    }
-    float r[NR], sc[kFuseCh];
+    float r[NR], pc[kFuseCh];
 #pragma unroll
     for (int q = 0; q < NR; ++q) {
+        // channel c0 - POST + q: its scale s, s^-beta and output b
         float sq = 0.f;
 #pragma unroll
         for (int t = 0; t < SIZE; ++t)
-            sq += a[q + t] * a[q + t];
-        const float s = k + alpha_over_n * sq;
-        r[q] = g[q] * b[q] * __builtin_amdgcn_rcpf(s);
+            sq = __builtin_fmaf(a[q + t], a[q + t], sq);
+        const float s = __builtin_fmaf(alpha_over_n, sq, k);
+        const float p = pow_neg(s, beta);
+        const float b = a[q + PRE] * p;
+        r[q] = g[q] * b * __builtin_amdgcn_rcpf(s);
         if (q >= POST && q < POST + kFuseCh)
-            sc[q - POST] = s;
+            pc[q - POST] = p;
     }
     const float coef = 2.f * alpha_over_n * beta;
 #pragma unroll
@@ -833,7 +837,7 @@ __device__ __forceinline__ void fuse_stage_pooled_grad(
 #pragma unroll
         for (int q = 0; q < SIZE; ++q)
             cross += r[t + q];
-        gs[t][pos] = g[t + POST] * pow_neg(sc[t], beta) - coef * a[t + POST + PRE] * cross;
+        gs[t][pos] = g[t + POST] * pc[t] - coef * a[t + POST + PRE] * cross;
         // (channels past C stage zeros; phase 2 never reads them)
         ms[t][pos] = (int32_t)__builtin_bit_cast(uint32_t, buf_ld_f32(rm, off(c0 + t)));
     }
@@ -951,9 +955,8 @@ __device__ __forceinline__ void fuse_gather_quad(const FuseBlock& f,
 
 template <int KS, int SS, int SIZE>
 __global__ void __launch_bounds__(256)
-lrn_pool_backward_kernel(const float* __restrict__ a_in, const float* __restrict__ b_in,
-                         const float* __restrict__ g_in, const int32_t* __restrict__ mask,
-                         float* __restrict__ dx, int N, int C, int H, int W, int OH, int OW,
+lrn_pool_backward_kernel(const float* __restrict__ a_in, const float* __restrict__ g_in,
+                         const int32_t* __restrict__ mask, float* __restrict__ dx, int N, int C, int H, int W, int OH, int OW,
                          int kh_, int kw_, int sh_, int sw_, int ph, int pw, int yrows,
                          int nstrips, int nchunks, float alpha_over_n, float beta, float k)
 {
@@ -962,8 +965,8 @@ lrn_pool_backward_kernel(const float* __restrict__ a_in, const float* __restrict
     const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
     const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
     const FuseBlock f = fuse_block(H, OH, kh, sh, ph, yrows, nstrips, nchunks);
-    fuse_stage_pooled_grad<SIZE>(f, a_in, b_in, g_in, mask, gs, ms, N, C, OH, OW, alpha_over_n,
-                                 beta, k);
+    fuse_stage_pooled_grad<SIZE>(f, a_in, g_in, mask, gs, ms, N, C, OH, OW, alpha_over_n, beta,
+                                 k);
     __syncthreads();
     if constexpr (KS == 3 && SS == 2) {
         // phase 2: thread -> one column pair b and every g-th row pair a
@@ -1028,9 +1031,8 @@ lrn_pool_backward_kernel(const float* __restrict__ a_in, const float* __restrict
 // border is written by dh_zero_border_kernel.
 template <int KS, int SS, int SIZE>
 __global__ void __launch_bounds__(256)
-lrn_pool_backward_bf16_kernel(const float* __restrict__ a_in, const float* __restrict__ b_in,
-                              const float* __restrict__ g_in, const int32_t* __restrict__ mask,
-                              const float* __restrict__ relu_top, uint16_t* __restrict__ Dh,
+lrn_pool_backward_bf16_kernel(const float* __restrict__ a_in, const float* __restrict__ g_in,
+                              const int32_t* __restrict__ mask, const float* __restrict__ relu_top, uint16_t* __restrict__ Dh,
                               float* __restrict__ sums, int N, int C, int H, int W, int OH, int OW,
                               int kh_, int kw_, int sh_, int sw_, int ph, int pw, int yrows,
                               int nstrips, int nchunks, float alpha_over_n, float beta, float k,
@@ -1041,8 +1043,8 @@ lrn_pool_backward_bf16_kernel(const float* __restrict__ a_in, const float* __res
     const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
     const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
     const FuseBlock f = fuse_block(H, OH, kh, sh, ph, yrows, nstrips, nchunks);
-    fuse_stage_pooled_grad<SIZE>(f, a_in, b_in, g_in, mask, gs, ms, N, C, OH, OW, alpha_over_n,
-                                 beta, k);
+    fuse_stage_pooled_grad<SIZE>(f, a_in, g_in, mask, gs, ms, N, C, OH, OW, alpha_over_n, beta,
+                                 k);
     __syncthreads();
     const int groups = 256 / W;
     const int grp = threadIdx.x / W;
@@ -1243,8 +1245,8 @@ hipError_t launch_lrn_pool_backward(const float* pooled, const float* top, const
     const float an = alpha / size;
 #define FUSED_BWD(KS_, SS_, SZ_)                                                                  \
     hipLaunchKernelGGL((lrn_pool_backward_kernel<KS_, SS_, SZ_>), g, dim3(256), 0, s, pooled,    \
-                       top, top_diff, mask, dx, N, C, H, W, OH, OW, kh, kw, sh, sw, ph, pw,     \
-                       yrows, nstrips, nchunks, an, beta, k)
+                       top_diff, mask, dx, N, C, H, W, OH, OW, kh, kw, sh, sw, ph, pw, yrows,   \
+                       nstrips, nchunks, an, beta, k)
     const bool k32 = kh == 3 && kw == 3 && sh == 2 && sw == 2;
     if (size == 5) {
         if (k32)
@@ -1290,9 +1292,9 @@ hipError_t launch_lrn_pool_backward_bf16(const float* pooled, const float* top,
     const float an = alpha / size;
 #define FUSED_BWD16(KS_, SS_, SZ_)                                                                \
     hipLaunchKernelGGL((lrn_pool_backward_bf16_kernel<KS_, SS_, SZ_>), g, dim3(256), 0, s,       \
-                       pooled, top, top_diff, mask, relu_top, Dh, sums, N, C, H, W, OH, OW, kh,  \
-                       kw, sh, sw, ph, pw, yrows, nstrips, nchunks, an, beta, k, Kg, Kgp, Ktot,  \
-                       DHp, DWp, tb, lb)
+                       pooled, top_diff, mask, relu_top, Dh, sums, N, C, H, W, OH, OW, kh, kw,   \
+                       sh, sw, ph, pw, yrows, nstrips, nchunks, an, beta, k, Kg, Kgp, Ktot, DHp, \
+                       DWp, tb, lb)
     const bool k32 = kh == 3 && kw == 3 && sh == 2 && sw == 2;
     if (size == 5) {
         if (k32)

@@ -62,7 +62,13 @@ enum caffe_pool_flags {
      * records mask -1 (no winner), so the backward pass also applies that
      * ReLU's backward (it routes nothing where the ReLU's output was 0).
      * top is unchanged. */
-    CAFFE_POOL_RELU_INPUT = 1
+    CAFFE_POOL_RELU_INPUT = 1,
+    /* caffe_pool_lrn_forward_into only: the LRN's float output is not
+     * written (top may be NULL); its staged bf16 copy is.  For callers whose
+     * only other reader of that output is the fused backward
+     * (caffe_conv_backward_pool_lrn, caffe_lrn_pool_backward), which forms
+     * it again from `pooled`. */
+    CAFFE_POOL_LRN_STAGE_ONLY = 2
 };
 
 /* mask may be NULL when no backward pass will follow; flags is a set of

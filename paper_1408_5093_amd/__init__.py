@@ -20,7 +20,7 @@ from ._lib import (  # noqa: F401
     FORWARD_BOTTOM_STAGED, CAFFE_BF16, CAFFE_BF16_F32_BOTTOM, CAFFE_F32, CAFFE_LR_EXP,
     CAFFE_LR_FIXED, CAFFE_LR_INV, CAFFE_LR_STEP, LrSchedule, PASS_BACKWARD,
     PASS_BACKWARD_DATA, PASS_BACKWARD_POOL_LRN, PASS_BACKWARD_WEIGHTS, PASS_FORWARD,
-    POOL_RELU_INPUT, CaffeError, ConvDesc,
+    POOL_LRN_STAGE_ONLY, POOL_RELU_INPUT, CaffeError, ConvDesc,
     LrnDesc, PoolDesc, check, load, LIB_PATH,
 )
 

@@ -27,6 +27,7 @@ BACKWARD_BOTTOM_STAGED = 4
 BACKWARD_TOP_STAGED = 16
 FORWARD_BOTTOM_STAGED = 1
 POOL_RELU_INPUT = 1
+POOL_LRN_STAGE_ONLY = 2
 
 PASS_FORWARD = 0
 PASS_BACKWARD_DATA = 1

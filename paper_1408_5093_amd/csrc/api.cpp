@@ -1963,8 +1963,9 @@ int caffe_pool_lrn_forward_into(const caffe_pool_desc* pd, const caffe_lrn_desc*
                                 int32_t flags, const caffe_conv_desc* next, void* next_workspace,
                                 size_t next_ws_bytes, void* stream)
 {
-    if (flags & ~CAFFE_POOL_RELU_INPUT)
+    if (flags & ~(CAFFE_POOL_RELU_INPUT | CAFFE_POOL_LRN_STAGE_ONLY))
         return fail(CAFFE_ERR_INVALID_ARG, "unknown pooling flags 0x%x", flags);
+    const bool write_top = !(flags & CAFFE_POOL_LRN_STAGE_ONLY);
     int Ho, Wo;
     CHECK(check_pool_lrn(pd, ld, &Ho, &Wo));
     ConvPlan qn;
@@ -1983,7 +1984,7 @@ int caffe_pool_lrn_forward_into(const caffe_pool_desc* pd, const caffe_lrn_desc*
     CHECK(check_ptr(bottom, nz, "bottom"));
     CHECK(check_ptr(pooled, nz, "pooled"));
     CHECK(check_ptr(mask, false, "mask"));
-    CHECK(check_ptr(top, nz, "top"));
+    CHECK(check_ptr(top, nz && write_top, "top"));
     hipStream_t s = (hipStream_t)stream;
     LAUNCH(launch_maxpool_forward(bottom, pooled, mask, pd->N * pd->C, pd->H, pd->W, Ho, Wo,
                                   pd->kernel_h, pd->kernel_w, pd->stride_h, pd->stride_w,
@@ -1991,9 +1992,9 @@ int caffe_pool_lrn_forward_into(const caffe_pool_desc* pd, const caffe_lrn_desc*
                                   s),
            "max-pool forward launch");
     uint16_t* xh = (uint16_t*)((char*)next_workspace + qn.off_xh_fwd);
-    LAUNCH(launch_lrn_forward_stage(pooled, top, ld->N, ld->C, ld->H, ld->W, ld->local_size,
-                                    ld->alpha, ld->beta, ld->k, xh, qn.XHp, qn.XWp, qn.ph, qn.pw,
-                                    s),
+    LAUNCH(launch_lrn_forward_stage(pooled, write_top ? top : nullptr, ld->N, ld->C, ld->H,
+                                    ld->W, ld->local_size, ld->alpha, ld->beta, ld->k, xh, qn.XHp,
+                                    qn.XWp, qn.ph, qn.pw, s),
            "LRN forward and staging launch");
     return CAFFE_OK;
 }

@@ -494,7 +494,8 @@ lrn_forward_kernel(const float* __restrict__ x, float* __restrict__ y, int N, in
     // unconditional and all of them are in flight together.
     const uint32_t bytes = (uint32_t)(N * C * HW) * 4u;
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, bytes);
-    const __amdgpu_buffer_rsrc_t ry = make_rsrc(y, bytes);
+    // (staging without y: an empty range, every store of y dropped)
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(y, y ? bytes : 0u);
     const uint32_t base4 = (uint32_t)(n * C * HW + pix) * 4u;
     const uint32_t hw4 = (uint32_t)HW * 4u;
     auto off = [&](int ch) {

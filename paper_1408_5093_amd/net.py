@@ -17,7 +17,8 @@ from . import (BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_D
                BACKWARD_TOP_STAGED, CAFFE_BF16_F32_BOTTOM, CAFFE_F32, FORWARD_BOTTOM_STAGED,
                caffe_conv_backward_into, conv_stage_below_supported, pool_lrn_stage_supported,
                PASS_BACKWARD, PASS_BACKWARD_POOL_LRN, PASS_BACKWARD_WEIGHTS, PASS_FORWARD,
-               POOL_RELU_INPUT, Workspace, caffe_conv_backward, caffe_conv_backward_pool_lrn,
+               POOL_LRN_STAGE_ONLY, POOL_RELU_INPUT, Workspace, caffe_conv_backward,
+               caffe_conv_backward_pool_lrn,
                caffe_conv_forward, conv_desc, conv_out_shape, lrn_desc,
                conv_workspace_size, lrn_backward, lrn_forward, maxpool_backward, maxpool_forward,
                lrn_pool_backward, pool_desc, pool_lrn_forward, pool_lrn_supported, relu_backward,
@@ -33,7 +34,7 @@ class ConvStack:
 
     def __init__(self, layers, N, weights, biases, glue=None, bf16=False, device="cuda",
                  fuse_glue=True, split_backward=True, fuse_staging=True, chain_staging=True,
-                 lrn_staging=True):
+                 lrn_staging=True, lrn_stage_only=True):
         self.layers = list(layers)
         self.N = N
         self.bf16 = bf16
@@ -187,6 +188,10 @@ class ConvStack:
                     self.bottom_staged[l] = pool_lrn_stage_supported(
                         pst["in_shape"], p["kernel"], p["stride"], p.get("pad", 0), r["size"],
                         r["alpha"], r["beta"], r["k"], self.descs[l])
+        # ... and then writes only that staging, not its float output, when the
+        # glue's backward is the fused one that forms the output again
+        self.lrn_stage_only = [lrn_stage_only and l + 1 < n and self.bottom_staged[l + 1] and
+                               self.fuse_staging[l] for l in range(n)]
         for l in range(n):
             if self.fuse_staging[l]:
                 pst, lst = self.stages[l]
@@ -229,7 +234,9 @@ class ConvStack:
                 pst["x"], lst["x"] = cur, pst["y"]
                 pool_lrn_forward(cur, p["kernel"], p["stride"], p.get("pad", 0), r["size"],
                                  r["alpha"], r["beta"], r["k"], pooled=pst["y"], mask=pst["mask"],
-                                 out=lst["y"], flags=self.pool_flags[l], stream=s,
+                                 out=lst["y"], stream=s,
+                                 flags=self.pool_flags[l] |
+                                 (POOL_LRN_STAGE_ONLY if self.lrn_stage_only[l] else 0),
                                  stage_for=((self.descs[l + 1], self.ws_of[l + 1])
                                             if l + 1 < n_l and self.bottom_staged[l + 1]
                                             else None))

@@ -293,6 +293,9 @@ def test_glue_validation():
     into = lambda nd: lib.caffe_pool_lrn_forward_into(
         ctypes.byref(pd2), ctypes.byref(ld2), P(0x1000), P(0x2000), None, P(0x3000), 0,
         ctypes.byref(nd), P(0x100000), 1 << 30, None)
+    # the stage-only flag belongs to the staging call
+    assert lib.caffe_pool_lrn_forward(ctypes.byref(pd2), ctypes.byref(ld2), P(0x1000), P(0x2000),
+                                      None, P(0x3000), cc.POOL_LRN_STAGE_ONLY, None) == -1
     assert lib.caffe_pool_lrn_stage_supported(ctypes.byref(pd2), ctypes.byref(ld2),
                                               ctypes.byref(nxt(96, cc.CAFFE_BF16_F32_BOTTOM)))
     for nd, code in [(nxt(96, cc.CAFFE_F32), -4), (nxt(192, cc.CAFFE_BF16_F32_BOTTOM), -1)]:

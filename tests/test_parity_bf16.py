@@ -458,9 +458,10 @@ def test_lrn_forward_into_next_staging(case):
     bottom (caffe_pool_lrn_forward_into), then that convolution run on the
     staged bottom (CAFFE_FORWARD_BOTTOM_STAGED) and its weight gradient on
     the same staging (CAFFE_BACKWARD_BOTTOM_STAGED): every output bit for
-    bit against the separate passes.  The staging workspace starts filled
-    with large finite values, so a border the fused pass fails to zero shows
-    up in the convolution's output."""
+    bit against the separate passes, also with CAFFE_POOL_LRN_STAGE_ONLY (the
+    LRN's float output then left untouched).  The staging workspace starts
+    filled with large finite values, so a border the fused pass fails to
+    zero shows up in the convolution's output."""
     N, C, H, W, pk, ps, size, K, kk, pad, g = case
     print(f"lrn staging case {case}", flush=True)
     rng = np.random.default_rng([91, *case])
@@ -476,20 +477,29 @@ def test_lrn_forward_into_next_staging(case):
                cc.conv_workspace_size(nd, cc.PASS_BACKWARD))
     ws = [torch.full((ws_n,), 0x7E, dtype=torch.uint8, device=DEV) for _ in range(2)]
     outs = []
-    for staged in (False, True):
-        pooled, mask, y = cc.pool_lrn_forward(x, *prm, stage_for=(nd, ws[1]) if staged else None)
+    ws.append(torch.full((ws_n,), 0x7E, dtype=torch.uint8, device=DEV))
+    for mode in (0, 1, 2):  # separate staging, staged by the LRN, staged only
+        staged = mode > 0
+        y0 = torch.full((N, C, Hp, Wp), float("nan"), device=DEV)
+        pooled, mask, y = cc.pool_lrn_forward(x, *prm, out=y0,
+                                              stage_for=(nd, ws[mode]) if staged else None,
+                                              flags=cc.POOL_LRN_STAGE_ONLY if mode == 2 else 0)
+        if mode == 2:
+            assert torch.isnan(y).all(), "the float output was written"
+            y = outs[0][2]  # (the float bottom is not read: the staging is)
         Ho, Wo = cc.conv_out_shape(nd)
         top = torch.empty((N, K, Ho, Wo), device=DEV)
-        cc.caffe_conv_forward(nd, y, w, b, top, ws[staged],
+        cc.caffe_conv_forward(nd, y, w, b, top, ws[mode],
                               flags=cc.FORWARD_BOTTOM_STAGED if staged else 0)
         gd = _t(np.random.default_rng(5).standard_normal(top.shape))
         dW, db = torch.empty(w.shape, device=DEV), torch.empty(K, device=DEV)
         cc.caffe_conv_backward(nd, gd, top, y, w, None, dW, db, flags=cc.BACKWARD_BOTTOM_STAGED,
-                               workspace=ws[staged])
+                               workspace=ws[mode])
         torch.cuda.synchronize()
         outs.append((pooled, mask, y, top, dW, db))
-    for name, a, c in zip(("pooled", "mask", "lrn", "top", "dW", "db"), *outs):
-        assert torch.equal(a, c), name
+    for other in outs[1:]:
+        for name, a, c in zip(("pooled", "mask", "lrn", "top", "dW", "db"), outs[0], other):
+            assert torch.equal(a, c), name
     assert torch.isfinite(outs[1][3]).all()
 
 

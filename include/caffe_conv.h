@@ -212,7 +212,11 @@ enum caffe_backward_flags {
      * caffe_conv_backward_into (which named this descriptor and workspace
      * as `below`); top_diff is not read (it may be NULL) and counts as
      * masked.  CAFFE_ERR_INVALID_ARG in CAFFE_F32 mode. */
-    CAFFE_BACKWARD_TOP_STAGED = 16
+    CAFFE_BACKWARD_TOP_STAGED = 16,
+    /* caffe_conv_backward_pool_lrn(_ex) (caffe_layers.h) only: pool_mask
+     * holds one byte per pooled value, as caffe_pool_lrn_forward writes it
+     * with CAFFE_POOL_MASK_OFFSETS. */
+    CAFFE_BACKWARD_POOL_MASK_OFFSETS = 32
 };
 
 /* The whole backward pass of the layer in one call: the ReLU mask is applied

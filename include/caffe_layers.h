@@ -68,7 +68,15 @@ enum caffe_pool_flags {
      * only other reader of that output is the fused backward
      * (caffe_conv_backward_pool_lrn, caffe_lrn_pool_backward), which forms
      * it again from `pooled`. */
-    CAFFE_POOL_LRN_STAGE_ONLY = 2
+    CAFFE_POOL_LRN_STAGE_ONLY = 2,
+    /* caffe_pool_lrn_forward and caffe_pool_lrn_forward_into only: mask
+     * (an int32_t pointer by type) receives one byte per pooled value, the
+     * winner's offset du * kernel_w + dv within its window (255: no winner)
+     * instead of its plane index: a quarter of the bytes to write and read.
+     * Only caffe_conv_backward_pool_lrn with CAFFE_BACKWARD_POOL_MASK_OFFSETS
+     * reads such a mask.  CAFFE_ERR_UNSUPPORTED for windows of more than 255
+     * taps. */
+    CAFFE_POOL_MASK_OFFSETS = 4
 };
 
 /* mask may be NULL when no backward pass will follow; flags is a set of

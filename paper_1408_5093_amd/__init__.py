@@ -16,11 +16,12 @@ import torch
 from . import _lib
 from ._lib import (  # noqa: F401
     CAFFE_ERR_UNSUPPORTED, CAFFE_ERR_WORKSPACE, NOALLOC_SCRATCH_BYTES, BACKWARD_BOTTOM_STAGED,
-    BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED, BACKWARD_TOP_STAGED,
+    BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_POOL_MASK_OFFSETS, BACKWARD_TOP_DIFF_MASKED,
+    BACKWARD_TOP_STAGED,
     FORWARD_BOTTOM_STAGED, CAFFE_BF16, CAFFE_BF16_F32_BOTTOM, CAFFE_F32, CAFFE_LR_EXP,
     CAFFE_LR_FIXED, CAFFE_LR_INV, CAFFE_LR_STEP, LrSchedule, PASS_BACKWARD,
     PASS_BACKWARD_DATA, PASS_BACKWARD_POOL_LRN, PASS_BACKWARD_WEIGHTS, PASS_FORWARD,
-    POOL_LRN_STAGE_ONLY, POOL_RELU_INPUT, CaffeError, ConvDesc,
+    POOL_LRN_STAGE_ONLY, POOL_MASK_OFFSETS, POOL_RELU_INPUT, CaffeError, ConvDesc,
     LrnDesc, PoolDesc, check, load, LIB_PATH,
 )
 
@@ -340,12 +341,13 @@ def pool_lrn_forward(x, kernel, stride, pad=0, size=5, alpha=1e-4, beta=0.75, k=
     the output is also staged as that convolution's bf16 bottom."""
     _dev(x, "bottom", torch.float32)
     pd, ld, shape = _pool_lrn_descs(x.shape, kernel, stride, pad, size, alpha, beta, k)
+    mdt = torch.uint8 if flags & POOL_MASK_OFFSETS else torch.int32
     pooled = torch.empty(shape, dtype=torch.float32, device=x.device) if pooled is None else pooled
-    mask = torch.empty(shape, dtype=torch.int32, device=x.device) if mask is None else mask
+    mask = torch.empty(shape, dtype=mdt, device=x.device) if mask is None else mask
     out = torch.empty(shape, dtype=torch.float32, device=x.device) if out is None else out
     for t, n in ((pooled, "pooled"), (out, "top")):
         _dev(t, n, torch.float32)
-    _dev(mask, "mask", torch.int32)
+    _dev(mask, "mask", mdt)
     args = (ctypes.byref(pd), ctypes.byref(ld), _ptr(x), _ptr(pooled), _ptr(mask), _ptr(out),
             int(flags))
     if stage_for is None:
@@ -393,7 +395,8 @@ def caffe_conv_backward_pool_lrn(desc, pool, lrn, pooled, lrn_top, lrn_top_diff,
                  (top, "top"), (bottom_diff, "bottom_diff"), (weight_diff, "weight_diff"),
                  (bias_diff, "bias_diff")):
         _dev(x, n, torch.float32)
-    _dev(pool_mask, "pool_mask", torch.int32)
+    _dev(pool_mask, "pool_mask",
+         torch.uint8 if flags & BACKWARD_POOL_MASK_OFFSETS else torch.int32)
     _dev(bottom, "bottom", _bottom_dtype(desc)), _dev(weight, "weight", t)
     ws_bytes = 0 if workspace is None else workspace.numel()
     args = (ctypes.byref(desc), ctypes.byref(pool), ctypes.byref(lrn), _ptr(pooled),

@@ -25,9 +25,11 @@ BACKWARD_TOP_DIFF_MASKED = 1
 BACKWARD_MASK_BOTTOM_DIFF = 2
 BACKWARD_BOTTOM_STAGED = 4
 BACKWARD_TOP_STAGED = 16
+BACKWARD_POOL_MASK_OFFSETS = 32
 FORWARD_BOTTOM_STAGED = 1
 POOL_RELU_INPUT = 1
 POOL_LRN_STAGE_ONLY = 2
+POOL_MASK_OFFSETS = 4
 
 PASS_FORWARD = 0
 PASS_BACKWARD_DATA = 1

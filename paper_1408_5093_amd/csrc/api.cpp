@@ -1730,8 +1730,12 @@ int caffe_conv_backward_pool_lrn_ex(const caffe_conv_desc* desc, const caffe_poo
     if (accumulate != 0 && accumulate != 1)
         return fail(CAFFE_ERR_INVALID_ARG, "accumulate must be 0 or 1");
     if (flags & ~(CAFFE_BACKWARD_TOP_DIFF_MASKED | CAFFE_BACKWARD_MASK_BOTTOM_DIFF |
-                  CAFFE_BACKWARD_BOTTOM_STAGED))
+                  CAFFE_BACKWARD_BOTTOM_STAGED | CAFFE_BACKWARD_POOL_MASK_OFFSETS))
         return fail(CAFFE_ERR_INVALID_ARG, "unknown backward flags 0x%x", flags);
+    const int mask_u8 = (flags & CAFFE_BACKWARD_POOL_MASK_OFFSETS) ? 1 : 0;
+    if (mask_u8 && pool->kernel_h * pool->kernel_w > 255)
+        return fail(CAFFE_ERR_UNSUPPORTED, "byte winner offsets need windows of at most 255 taps");
+    flags &= ~CAFFE_BACKWARD_POOL_MASK_OFFSETS;
     const bool masked = (flags & CAFFE_BACKWARD_TOP_DIFF_MASKED) != 0;
     const bool mask_bottom = (flags & CAFFE_BACKWARD_MASK_BOTTOM_DIFF) != 0 && bottom_diff;
     CHECK(check_conv_ptrs(q, pooled, true, true, "pooled"));
@@ -1755,7 +1759,8 @@ int caffe_conv_backward_pool_lrn_ex(const caffe_conv_desc* desc, const caffe_poo
         LAUNCH(launch_lrn_pool_backward(pooled, lrn_top, lrn_top_diff, pool_mask, gbuf, q.N, q.K,
                                         q.Ho, q.Wo, PHo, PWo, pool->kernel_h, pool->kernel_w,
                                         pool->stride_h, pool->stride_w, pool->pad_h, pool->pad_w,
-                                        lrn->local_size, lrn->alpha, lrn->beta, lrn->k, s),
+                                        lrn->local_size, lrn->alpha, lrn->beta, lrn->k, s,
+                                        mask_u8),
                "fused LRN + pool backward launch");
         return caffe_conv_backward_ex(desc, gbuf, top, bottom, weight, bottom_diff, weight_diff,
                                       bias_diff, accumulate, flags, workspace, q.ws_both, stream,
@@ -1777,7 +1782,7 @@ int caffe_conv_backward_pool_lrn_ex(const caffe_conv_desc* desc, const caffe_poo
                                          PHo, PWo, pool->kernel_h, pool->kernel_w, pool->stride_h,
                                          pool->stride_w, pool->pad_h, pool->pad_w, lrn->local_size,
                                          lrn->alpha, lrn->beta, lrn->k, q.Kg, q.Kgp, q.G * q.Kgp,
-                                         q.DHp, q.DWp, q.dtb, q.dlb, s),
+                                         q.DHp, q.DWp, q.dtb, q.dlb, s, mask_u8),
            "fused LRN + pool backward staging launch");
     const int strips = lrn_pool_backward_strips(q.Ho, PHo, PWo, pool->kernel_h, pool->stride_h,
                                                 pool->pad_h);
@@ -1938,10 +1943,13 @@ int caffe_pool_lrn_forward(const caffe_pool_desc* pd, const caffe_lrn_desc* ld,
                            const float* bottom, float* pooled, int32_t* mask, float* top,
                            int32_t flags, void* stream)
 {
-    if (flags & ~CAFFE_POOL_RELU_INPUT)
+    if (flags & ~(CAFFE_POOL_RELU_INPUT | CAFFE_POOL_MASK_OFFSETS))
         return fail(CAFFE_ERR_INVALID_ARG, "unknown pooling flags 0x%x", flags);
     int Ho, Wo;
     CHECK(check_pool_lrn(pd, ld, &Ho, &Wo));
+    const int mask_u8 = (flags & CAFFE_POOL_MASK_OFFSETS) ? 1 : 0;
+    if (mask_u8 && pd->kernel_h * pd->kernel_w > 255)
+        return fail(CAFFE_ERR_UNSUPPORTED, "byte winner offsets need windows of at most 255 taps");
     const bool nz = pd->N > 0;
     CHECK(check_ptr(bottom, nz, "bottom"));
     CHECK(check_ptr(pooled, nz, "pooled"));
@@ -1950,7 +1958,7 @@ int caffe_pool_lrn_forward(const caffe_pool_desc* pd, const caffe_lrn_desc* ld,
     LAUNCH(launch_maxpool_forward(bottom, pooled, mask, pd->N * pd->C, pd->H, pd->W, Ho, Wo,
                                   pd->kernel_h, pd->kernel_w, pd->stride_h, pd->stride_w,
                                   pd->pad_h, pd->pad_w, (flags & CAFFE_POOL_RELU_INPUT) ? 1 : 0,
-                                  (hipStream_t)stream),
+                                  (hipStream_t)stream, mask_u8),
            "max-pool forward launch");
     LAUNCH(launch_lrn_forward(pooled, top, ld->N, ld->C, ld->H * ld->W, ld->local_size, ld->alpha,
                               ld->beta, ld->k, (hipStream_t)stream),
@@ -1963,11 +1971,14 @@ int caffe_pool_lrn_forward_into(const caffe_pool_desc* pd, const caffe_lrn_desc*
                                 int32_t flags, const caffe_conv_desc* next, void* next_workspace,
                                 size_t next_ws_bytes, void* stream)
 {
-    if (flags & ~(CAFFE_POOL_RELU_INPUT | CAFFE_POOL_LRN_STAGE_ONLY))
+    if (flags & ~(CAFFE_POOL_RELU_INPUT | CAFFE_POOL_LRN_STAGE_ONLY | CAFFE_POOL_MASK_OFFSETS))
         return fail(CAFFE_ERR_INVALID_ARG, "unknown pooling flags 0x%x", flags);
     const bool write_top = !(flags & CAFFE_POOL_LRN_STAGE_ONLY);
     int Ho, Wo;
     CHECK(check_pool_lrn(pd, ld, &Ho, &Wo));
+    const int mask_u8 = (flags & CAFFE_POOL_MASK_OFFSETS) ? 1 : 0;
+    if (mask_u8 && pd->kernel_h * pd->kernel_w > 255)
+        return fail(CAFFE_ERR_UNSUPPORTED, "byte winner offsets need windows of at most 255 taps");
     ConvPlan qn;
     if (!next)
         return fail(CAFFE_ERR_INVALID_ARG, "next is NULL");
@@ -1989,7 +2000,7 @@ int caffe_pool_lrn_forward_into(const caffe_pool_desc* pd, const caffe_lrn_desc*
     LAUNCH(launch_maxpool_forward(bottom, pooled, mask, pd->N * pd->C, pd->H, pd->W, Ho, Wo,
                                   pd->kernel_h, pd->kernel_w, pd->stride_h, pd->stride_w,
                                   pd->pad_h, pd->pad_w, (flags & CAFFE_POOL_RELU_INPUT) ? 1 : 0,
-                                  s),
+                                  s, mask_u8),
            "max-pool forward launch");
     uint16_t* xh = (uint16_t*)((char*)next_workspace + qn.off_xh_fwd);
     LAUNCH(launch_lrn_forward_stage(pooled, write_top ? top : nullptr, ld->N, ld->C, ld->H,

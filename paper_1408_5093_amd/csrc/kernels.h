@@ -410,9 +410,12 @@ hipError_t launch_fill_zero(float* out, int64_t count, hipStream_t s);
 // Glue layers (layers.hip).
 // relu_input: windows whose maximum is not > 0 record mask -1 (no winner),
 // so the backward pass routes them nothing.
+// (mask_u8: mask is bytes, each winner's offset du * kw + dv in its window,
+// 255 for none)
 hipError_t launch_maxpool_forward(const float* x, float* y, int32_t* mask, int NC, int H, int W,
                                   int OH, int OW, int kh, int kw, int sh, int sw, int ph, int pw,
-                                  int relu_input, hipStream_t s);
+                                  int relu_input, hipStream_t s,
+                                  int mask_u8 = 0);
 hipError_t launch_maxpool_backward(const float* dy, const int32_t* mask, float* dx, int NC, int H,
                                    int W, int OH, int OW, int kh, int kw, int sh, int sw, int ph,
                                    int pw, hipStream_t s);
@@ -435,7 +438,8 @@ bool pool_lrn_fusable(int H, int W, int OH, int OW, int kh, int sh, int ph, int 
 // Row strips of the fused LRN + max-pool backward (0: not fusable).
 int lrn_pool_backward_strips(int H, int OH, int OW, int kh, int sh, int ph);
 // (Both fused backward launchers take the LRN's output `top` for the
-// interface only: the kernels form it again from `pooled`, bit for bit.)
+// interface only: the kernels form it again from `pooled`, bit for bit.
+// mask_u8: the mask as launch_maxpool_forward writes it with mask_u8.)
 // The fused backward written as the bf16 top-gradient staging of the
 // convolution below (channels in groups of Kg, each padded to Kgp, Ktot in
 // all, on a DHp x DWp grid with the image at (tb, lb)), plus the grid's zero
@@ -447,11 +451,13 @@ hipError_t launch_lrn_pool_backward_bf16(const float* pooled, const float* top,
                                          int C, int H, int W, int OH, int OW, int kh, int kw,
                                          int sh, int sw, int ph, int pw, int size, float alpha,
                                          float beta, float k, int Kg, int Kgp, int Ktot, int DHp,
-                                         int DWp, int tb, int lb, hipStream_t s);
+                                         int DWp, int tb, int lb, hipStream_t s,
+                                         int mask_u8 = 0);
 hipError_t launch_lrn_pool_backward(const float* pooled, const float* top, const float* top_diff,
                                     const int32_t* mask, float* dx, int N, int C, int H, int W,
                                     int OH, int OW, int kh, int kw, int sh, int sw, int ph, int pw,
-                                    int size, float alpha, float beta, float k, hipStream_t s);
+                                    int size, float alpha, float beta, float k, hipStream_t s,
+                                    int mask_u8 = 0);
 hipError_t launch_cast_f32_bf16(const float* x, uint16_t* y, int64_t count, hipStream_t s);
 
 // ---- solver (solver.hip)

@@ -27,7 +27,8 @@ template <int KS, int SS>
 __global__ void __launch_bounds__(256)
 maxpool_forward_kernel(const float* __restrict__ x, float* __restrict__ y,
                        int32_t* __restrict__ mask, int NC, int H, int W, int OH, int OW, int kh_,
-                       int kw_, int sh_, int sw_, int ph, int pw, FastDiv div_ow, int relu_input)
+                       int kw_, int sh_, int sw_, int ph, int pw, FastDiv div_ow, int relu_input,
+                       int mask_u8)
 {
     constexpr int PPT = kPoolPlanesPerThread;
     const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
@@ -44,7 +45,7 @@ maxpool_forward_kernel(const float* __restrict__ x, float* __restrict__ y,
     const int stride = gridDim.y;  // planes handled by one grid row
     for (int nc0 = blockIdx.y; nc0 < NC; nc0 += stride * PPT) {
         float bv[PPT];
-        int best[PPT];
+        int best[PPT], boff[PPT];  // the winner: plane index, offset in the window
         if constexpr (KS > 0) {
             // fixed window: every load is independent; out-of-image taps are
             // replaced by the window's first tap (strict '>' keeps the first
@@ -67,6 +68,7 @@ maxpool_forward_kernel(const float* __restrict__ x, float* __restrict__ y,
 #pragma unroll
             for (int t = 0; t < PPT; ++t) {
                 best[t] = first;
+                boff[t] = (h0 - hs) * KS + (w0 - ws);
 #pragma unroll
                 for (int du = 0; du < KS; ++du)
 #pragma unroll
@@ -74,6 +76,7 @@ maxpool_forward_kernel(const float* __restrict__ x, float* __restrict__ y,
                         if (v[t][du][dv] > bv[t]) {
                             bv[t] = v[t][du][dv];
                             best[t] = (hs + du) * W + ws + dv;
+                            boff[t] = du * KS + dv;
                         }
             }
         } else {
@@ -84,12 +87,14 @@ maxpool_forward_kernel(const float* __restrict__ x, float* __restrict__ y,
                 const float* plane = x + nc * (H * W);
                 bv[t] = plane[first];
                 best[t] = first;
+                boff[t] = (h0 - hs) * kw + (w0 - ws);
                 for (int h = h0; h < h1; ++h)
                     for (int w = w0; w < w1; ++w) {
                         const float v = plane[h * W + w];
                         if (v > bv[t]) {
                             bv[t] = v;
                             best[t] = h * W + w;
+                            boff[t] = (h - hs) * kw + (w - ws);
                         }
                     }
             }
@@ -99,8 +104,12 @@ maxpool_forward_kernel(const float* __restrict__ x, float* __restrict__ y,
             const int nc = nc0 + t * stride;
             if (nc < NC) {
                 y[nc * OHW + p] = bv[t];
-                if (mask)  // a ReLU output window with no positive value routes nothing
-                    mask[nc * OHW + p] = (relu_input && !(bv[t] > 0.f)) ? -1 : best[t];
+                // a ReLU output window with no positive value routes nothing
+                const bool none = relu_input && !(bv[t] > 0.f);
+                if (mask && mask_u8)
+                    ((uint8_t*)mask)[nc * OHW + p] = none ? (uint8_t)255 : (uint8_t)boff[t];
+                else if (mask)
+                    mask[nc * OHW + p] = none ? -1 : best[t];
             }
         }
     }
@@ -191,7 +200,7 @@ __global__ void __launch_bounds__(256)
 maxpool_forward_lds_kernel(const float* __restrict__ x, float* __restrict__ y,
                            int32_t* __restrict__ mask, int NC, int H, int W, int OH, int OW,
                            int kh_, int kw_, int sh_, int sw_, int ph, int pw, int PB,
-                           FastDiv div_ohw, FastDiv div_ow, int relu_input)
+                           FastDiv div_ohw, FastDiv div_ow, int relu_input, int mask_u8)
 {
     __shared__ float xs[kPoolLdsFloats];
     const int kh = KS ? KS : kh_, kw = KS ? KS : kw_;
@@ -227,6 +236,7 @@ maxpool_forward_lds_kernel(const float* __restrict__ x, float* __restrict__ y,
         const int first = h0 * W + w0;
         float bv = plane[first];
         int best = first;
+        int boff = (h0 - hs) * kw + (w0 - ws);  // the winner's offset in its window
         if constexpr (KS > 0) {
             // all taps read first; taps outside the image read the window's
             // first tap, which never wins the strict '>' below
@@ -246,6 +256,7 @@ maxpool_forward_lds_kernel(const float* __restrict__ x, float* __restrict__ y,
                     if (v[du][dv] > bv) {
                         bv = v[du][dv];
                         best = (hs + du) * W + ws + dv;
+                        boff = du * KS + dv;
                     }
         } else {
             for (int h = h0; h < h1; ++h)
@@ -254,13 +265,18 @@ maxpool_forward_lds_kernel(const float* __restrict__ x, float* __restrict__ y,
                     if (v > bv) {
                         bv = v;
                         best = h * W + w;
+                        boff = (h - hs) * kw + (w - ws);
                     }
                 }
         }
         const size_t out = (size_t)nc0 * OHW + o;
         y[out] = bv;
-        if (mask)  // a ReLU output window with no positive value routes nothing
-            mask[out] = (relu_input && !(bv > 0.f)) ? -1 : best;
+        // a ReLU output window with no positive value routes nothing
+        const bool none = relu_input && !(bv > 0.f);
+        if (mask && mask_u8)
+            ((uint8_t*)mask)[out] = none ? (uint8_t)255 : (uint8_t)boff;
+        else if (mask)
+            mask[out] = none ? -1 : best;
     }
 }
 
@@ -360,10 +376,12 @@ static dim3 plane_grid(int pixels, int planes)
 
 hipError_t launch_maxpool_forward(const float* x, float* y, int32_t* mask, int NC, int H, int W,
                                   int OH, int OW, int kh, int kw, int sh, int sw, int ph, int pw,
-                                  int relu_input, hipStream_t s)
+                                  int relu_input, hipStream_t s, int mask_u8)
 {
     if ((long)NC * OH * OW == 0)
         return hipSuccess;
+    if (mask_u8 && kh * kw > 255)
+        return hipErrorInvalidValue;
     const FastDiv d = make_fastdiv((uint32_t)OW);
     if (H * W <= kPoolLdsFloats) {
         // planes staged in LDS, as many whole planes per block as fit
@@ -372,25 +390,28 @@ hipError_t launch_maxpool_forward(const float* x, float* y, int32_t* mask, int N
         const FastDiv dohw = make_fastdiv((uint32_t)(OH * OW));
         if (kh == 3 && kw == 3 && sh == 2 && sw == 2)
             hipLaunchKernelGGL((maxpool_forward_lds_kernel<3, 2>), g, dim3(256), 0, s, x, y, mask,
-                               NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, PB, dohw, d, relu_input);
+                               NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, PB, dohw, d, relu_input,
+                               mask_u8);
         else if (kh == 2 && kw == 2 && sh == 2 && sw == 2)
             hipLaunchKernelGGL((maxpool_forward_lds_kernel<2, 2>), g, dim3(256), 0, s, x, y, mask,
-                               NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, PB, dohw, d, relu_input);
+                               NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, PB, dohw, d, relu_input,
+                               mask_u8);
         else
             hipLaunchKernelGGL((maxpool_forward_lds_kernel<0, 0>), g, dim3(256), 0, s, x, y, mask,
-                               NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, PB, dohw, d, relu_input);
+                               NC, H, W, OH, OW, kh, kw, sh, sw, ph, pw, PB, dohw, d, relu_input,
+                               mask_u8);
         return hipGetLastError();
     }
     const dim3 grid = plane_grid(OH * OW, NC);
     if (kh == 3 && kw == 3 && sh == 2 && sw == 2)
         hipLaunchKernelGGL((maxpool_forward_kernel<3, 2>), grid, dim3(256), 0, s, x, y, mask, NC,
-                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d, relu_input);
+                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d, relu_input, mask_u8);
     else if (kh == 2 && kw == 2 && sh == 2 && sw == 2)
         hipLaunchKernelGGL((maxpool_forward_kernel<2, 2>), grid, dim3(256), 0, s, x, y, mask, NC,
-                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d, relu_input);
+                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d, relu_input, mask_u8);
     else
         hipLaunchKernelGGL((maxpool_forward_kernel<0, 0>), grid, dim3(256), 0, s, x, y, mask, NC,
-                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d, relu_input);
+                           H, W, OH, OW, kh, kw, sh, sw, ph, pw, d, relu_input, mask_u8);
     return hipGetLastError();
 }
 
@@ -782,12 +803,15 @@ __device__ __forceinline__ FuseBlock fuse_block(int H, int OH, int kh, int sh, i
 // pooled inputs exactly as the forward kernel forms it (the same fused
 // multiply-adds, the same hardware exp2 / log2), so it has the same bits,
 // and the pass reads a fifth fewer bytes.
+// With mask_u8 the mask holds each winner's offset du * kw + dv in its window
+// (255: none), staged as the plane index it stands for.
 template <int SIZE>
 __device__ __forceinline__ void fuse_stage_pooled_grad(
     const FuseBlock& f, const float* __restrict__ a_in, const float* __restrict__ g_in,
     const int32_t* __restrict__ mask,
     float (&gs)[kFuseCh][kFusePos], int32_t (&ms)[kFuseCh][kFusePos], int N, int C, int OH, int OW,
-    float alpha_over_n, float beta, float k)
+    float alpha_over_n, float beta, float k, int mask_u8, int W, int kw, int sh, int sw, int ph,
+    int pw)
 {
     constexpr int PRE = (SIZE - 1) / 2;
     constexpr int POST = SIZE - 1 - PRE;
@@ -799,11 +823,13 @@ __device__ __forceinline__ void fuse_stage_pooled_grad(
     const int pos = threadIdx.x;
     if (pos >= npos)
         return;
-    const int pix = (f.i_lo + pos / OW) * OW + (pos - (pos / OW) * OW);
+    const int pi = f.i_lo + pos / OW, pj = pos - (pos / OW) * OW;
+    const int pix = pi * OW + pj;
     const uint32_t bytes = (uint32_t)(N * C * OHW) * 4u;
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_in, bytes);
     const __amdgpu_buffer_rsrc_t rg = make_rsrc(g_in, bytes);
-    const __amdgpu_buffer_rsrc_t rm = make_rsrc(mask, bytes);
+    const __amdgpu_buffer_rsrc_t rm = make_rsrc(mask, mask_u8 ? bytes / 4u : bytes);
+    const int wh0 = pi * sh - ph, ww0 = pj * sw - pw;  // the window's first position
     const uint32_t base4 = (uint32_t)(f.n * C * OHW + pix) * 4u;
     const uint32_t hw4 = (uint32_t)OHW * 4u;
     auto off = [&](int ch) {
@@ -839,8 +865,15 @@ __device__ __forceinline__ void fuse_stage_pooled_grad(
         for (int q = 0; q < SIZE; ++q)
             cross += r[t + q];
         gs[t][pos] = g[t + POST] * pc[t] - coef * a[t + POST + PRE] * cross;
-        // (channels past C stage zeros; phase 2 never reads them)
-        ms[t][pos] = (int32_t)__builtin_bit_cast(uint32_t, buf_ld_f32(rm, off(c0 + t)));
+        // (channels past C stage zeros or 0 offsets; phase 2 never reads them)
+        if (mask_u8) {
+            const uint32_t o = off(c0 + t);
+            const int b = buf_ld_u8(rm, ((o & ~kOob) >> 2) | (o & kOob));
+            const int du = b / kw;
+            ms[t][pos] = b == 255 ? -1 : (wh0 + du) * W + ww0 + (b - du * kw);
+        } else {
+            ms[t][pos] = (int32_t)__builtin_bit_cast(uint32_t, buf_ld_f32(rm, off(c0 + t)));
+        }
     }
 }
 
@@ -959,7 +992,8 @@ __global__ void __launch_bounds__(256)
 lrn_pool_backward_kernel(const float* __restrict__ a_in, const float* __restrict__ g_in,
                          const int32_t* __restrict__ mask, float* __restrict__ dx, int N, int C, int H, int W, int OH, int OW,
                          int kh_, int kw_, int sh_, int sw_, int ph, int pw, int yrows,
-                         int nstrips, int nchunks, float alpha_over_n, float beta, float k)
+                         int nstrips, int nchunks, float alpha_over_n, float beta, float k,
+                         int mask_u8)
 {
     __shared__ float gs[kFuseCh][kFusePos];
     __shared__ int32_t ms[kFuseCh][kFusePos];
@@ -967,7 +1001,7 @@ lrn_pool_backward_kernel(const float* __restrict__ a_in, const float* __restrict
     const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
     const FuseBlock f = fuse_block(H, OH, kh, sh, ph, yrows, nstrips, nchunks);
     fuse_stage_pooled_grad<SIZE>(f, a_in, g_in, mask, gs, ms, N, C, OH, OW, alpha_over_n, beta,
-                                 k);
+                                 k, mask_u8, W, kw, sh, sw, ph, pw);
     __syncthreads();
     if constexpr (KS == 3 && SS == 2) {
         // phase 2: thread -> one column pair b and every g-th row pair a
@@ -1037,7 +1071,8 @@ lrn_pool_backward_bf16_kernel(const float* __restrict__ a_in, const float* __res
                               float* __restrict__ sums, int N, int C, int H, int W, int OH, int OW,
                               int kh_, int kw_, int sh_, int sw_, int ph, int pw, int yrows,
                               int nstrips, int nchunks, float alpha_over_n, float beta, float k,
-                              int Kg, int Kgp, int Ktot, int DHp, int DWp, int tb, int lb)
+                              int Kg, int Kgp, int Ktot, int DHp, int DWp, int tb, int lb,
+                              int mask_u8)
 {
     __shared__ float gs[kFuseCh][kFusePos];
     __shared__ int32_t ms[kFuseCh][kFusePos];
@@ -1045,7 +1080,7 @@ lrn_pool_backward_bf16_kernel(const float* __restrict__ a_in, const float* __res
     const int sh = SS ? SS : sh_, sw = SS ? SS : sw_;
     const FuseBlock f = fuse_block(H, OH, kh, sh, ph, yrows, nstrips, nchunks);
     fuse_stage_pooled_grad<SIZE>(f, a_in, g_in, mask, gs, ms, N, C, OH, OW, alpha_over_n, beta,
-                                 k);
+                                 k, mask_u8, W, kw, sh, sw, ph, pw);
     __syncthreads();
     const int groups = 256 / W;
     const int grp = threadIdx.x / W;
@@ -1233,12 +1268,13 @@ bool pool_lrn_fusable(int H, int W, int OH, int OW, int kh, int sh, int ph, int 
 hipError_t launch_lrn_pool_backward(const float* pooled, const float* top, const float* top_diff,
                                     const int32_t* mask, float* dx, int N, int C, int H, int W,
                                     int OH, int OW, int kh, int kw, int sh, int sw, int ph, int pw,
-                                    int size, float alpha, float beta, float k, hipStream_t s)
+                                    int size, float alpha, float beta, float k, hipStream_t s,
+                                    int mask_u8)
 {
     if ((long)N * C * H * W == 0)
         return hipSuccess;
     const int yrows = fused_backward_yrows(H, OH, OW, kh, sh, ph);
-    if (yrows == 0 || (size != 3 && size != 5))
+    if (yrows == 0 || (size != 3 && size != 5) || (mask_u8 && kh * kw > 255))
         return hipErrorInvalidValue;
     const int nstrips = (H + yrows - 1) / yrows;
     const int nchunks = (C + kFuseCh - 1) / kFuseCh;
@@ -1247,7 +1283,7 @@ hipError_t launch_lrn_pool_backward(const float* pooled, const float* top, const
 #define FUSED_BWD(KS_, SS_, SZ_)                                                                  \
     hipLaunchKernelGGL((lrn_pool_backward_kernel<KS_, SS_, SZ_>), g, dim3(256), 0, s, pooled,    \
                        top_diff, mask, dx, N, C, H, W, OH, OW, kh, kw, sh, sw, ph, pw, yrows,   \
-                       nstrips, nchunks, an, beta, k)
+                       nstrips, nchunks, an, beta, k, mask_u8)
     const bool k32 = kh == 3 && kw == 3 && sh == 2 && sw == 2;
     if (size == 5) {
         if (k32)
@@ -1276,13 +1312,13 @@ hipError_t launch_lrn_pool_backward_bf16(const float* pooled, const float* top,
                                          int C, int H, int W, int OH, int OW, int kh, int kw,
                                          int sh, int sw, int ph, int pw, int size, float alpha,
                                          float beta, float k, int Kg, int Kgp, int Ktot, int DHp,
-                                         int DWp, int tb, int lb, hipStream_t s)
+                                         int DWp, int tb, int lb, hipStream_t s, int mask_u8)
 {
     if ((long)N * C * H * W == 0)
         return hipSuccess;
     const int yrows = fused_backward_yrows(H, OH, OW, kh, sh, ph);
     if (yrows == 0 || (size != 3 && size != 5) || Kg % kFuseCh != 0 || Ktot % 8 != 0 ||
-        tb < 0 || lb < 0 || DHp < tb + H || DWp < lb + W)
+        tb < 0 || lb < 0 || DHp < tb + H || DWp < lb + W || (mask_u8 && kh * kw > 255))
         return hipErrorInvalidValue;
     const hipError_t e = launch_dh_zero_border(Dh, N, DHp, DWp, tb, lb, H, W, Ktot, s);
     if (e != hipSuccess)
@@ -1295,7 +1331,7 @@ hipError_t launch_lrn_pool_backward_bf16(const float* pooled, const float* top,
     hipLaunchKernelGGL((lrn_pool_backward_bf16_kernel<KS_, SS_, SZ_>), g, dim3(256), 0, s,       \
                        pooled, top_diff, mask, relu_top, Dh, sums, N, C, H, W, OH, OW, kh, kw,   \
                        sh, sw, ph, pw, yrows, nstrips, nchunks, an, beta, k, Kg, Kgp, Ktot, DHp, \
-                       DWp, tb, lb)
+                       DWp, tb, lb, mask_u8)
     const bool k32 = kh == 3 && kw == 3 && sh == 2 && sw == 2;
     if (size == 5) {
         if (k32)

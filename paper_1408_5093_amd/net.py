@@ -13,11 +13,13 @@ call; this module only owns buffers and the call order.
 """
 import torch
 
-from . import (BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_TOP_DIFF_MASKED,
+from . import (BACKWARD_BOTTOM_STAGED, BACKWARD_MASK_BOTTOM_DIFF, BACKWARD_POOL_MASK_OFFSETS,
+               BACKWARD_TOP_DIFF_MASKED,
                BACKWARD_TOP_STAGED, CAFFE_BF16_F32_BOTTOM, CAFFE_F32, FORWARD_BOTTOM_STAGED,
                caffe_conv_backward_into, conv_stage_below_supported, pool_lrn_stage_supported,
                PASS_BACKWARD, PASS_BACKWARD_POOL_LRN, PASS_BACKWARD_WEIGHTS, PASS_FORWARD,
-               POOL_LRN_STAGE_ONLY, POOL_RELU_INPUT, Workspace, caffe_conv_backward,
+               POOL_LRN_STAGE_ONLY, POOL_MASK_OFFSETS, POOL_RELU_INPUT, Workspace,
+               caffe_conv_backward,
                caffe_conv_backward_pool_lrn,
                caffe_conv_forward, conv_desc, conv_out_shape, lrn_desc,
                conv_workspace_size, lrn_backward, lrn_forward, maxpool_backward, maxpool_forward,
@@ -34,7 +36,7 @@ class ConvStack:
 
     def __init__(self, layers, N, weights, biases, glue=None, bf16=False, device="cuda",
                  fuse_glue=True, split_backward=True, fuse_staging=True, chain_staging=True,
-                 lrn_staging=True, lrn_stage_only=True):
+                 lrn_staging=True, lrn_stage_only=True, mask_offsets=True):
         self.layers = list(layers)
         self.N = N
         self.bf16 = bf16
@@ -192,6 +194,15 @@ class ConvStack:
         # glue's backward is the fused one that forms the output again
         self.lrn_stage_only = [lrn_stage_only and l + 1 < n and self.bottom_staged[l + 1] and
                                self.fuse_staging[l] for l in range(n)]
+        # ... and its max-pool records each winner as a byte (its offset in
+        # the window) where only that fused backward reads the mask
+        self.mask_u8 = [False] * n
+        for l in range(n):
+            if mask_offsets and self.fuse_staging[l]:
+                pst = self.stages[l][0]
+                if pst["prm"]["kernel"] ** 2 <= 255:
+                    self.mask_u8[l] = True
+                    pst["mask"] = torch.empty(pst["mask"].shape, dtype=torch.uint8, device=dev)
         for l in range(n):
             if self.fuse_staging[l]:
                 pst, lst = self.stages[l]
@@ -236,7 +247,8 @@ class ConvStack:
                                  r["alpha"], r["beta"], r["k"], pooled=pst["y"], mask=pst["mask"],
                                  out=lst["y"], stream=s,
                                  flags=self.pool_flags[l] |
-                                 (POOL_LRN_STAGE_ONLY if self.lrn_stage_only[l] else 0),
+                                 (POOL_LRN_STAGE_ONLY if self.lrn_stage_only[l] else 0) |
+                                 (POOL_MASK_OFFSETS if self.mask_u8[l] else 0),
                                  stage_for=((self.descs[l + 1], self.ws_of[l + 1])
                                             if l + 1 < n_l and self.bottom_staged[l + 1]
                                             else None))
@@ -376,6 +388,8 @@ class ConvStack:
         pst, lst = self.stages[l]
         L = self.layers[l]
         flags = BACKWARD_BOTTOM_STAGED
+        if self.mask_u8[l]:
+            flags |= BACKWARD_POOL_MASK_OFFSETS
         if self.top_masked[l]:
             flags |= BACKWARD_TOP_DIFF_MASKED
         if self.mask_bottom[l] and want_dx:

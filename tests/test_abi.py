@@ -293,6 +293,11 @@ def test_glue_validation():
     into = lambda nd: lib.caffe_pool_lrn_forward_into(
         ctypes.byref(pd2), ctypes.byref(ld2), P(0x1000), P(0x2000), None, P(0x3000), 0,
         ctypes.byref(nd), P(0x100000), 1 << 30, None)
+    # byte winner offsets need windows of at most 255 taps
+    big = cc.pool_desc((2, 96, 40, 40), 16, 2)
+    bigl = cc.lrn_desc((2, 96) + cc.pool_out_shape(big), 5)
+    assert lib.caffe_pool_lrn_forward(ctypes.byref(big), ctypes.byref(bigl), P(0x1000), P(0x2000),
+                                      P(0x4000), P(0x3000), cc.POOL_MASK_OFFSETS, None) in (-4,)
     # the stage-only flag belongs to the staging call
     assert lib.caffe_pool_lrn_forward(ctypes.byref(pd2), ctypes.byref(ld2), P(0x1000), P(0x2000),
                                       None, P(0x3000), cc.POOL_LRN_STAGE_ONLY, None) == -1

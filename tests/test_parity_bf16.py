@@ -503,6 +503,32 @@ def test_lrn_forward_into_next_staging(case):
     assert torch.isfinite(outs[1][3]).all()
 
 
+def test_caffenet_bf16_step_byte_masks_match():
+    """The bf16 step at N=512 with the max-pools after conv1 and conv2
+    recording their winners as bytes (the default where the fused backward
+    reads them) against 32-bit plane-index masks: every top and gradient
+    the same bits."""
+    N = 512
+    inp = wl.caffenet_step(N, wl.CAFFENET_STEP_BF16)
+    x = torch.from_numpy(inp["x"]).to(DEV)
+    g = torch.from_numpy(inp["top_diff"]).to(DEV)
+    nets = [ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(), bf16=True,
+                      mask_offsets=f) for f in (True, False)]
+    assert nets[0].mask_u8 == [True, True, False, False, False]
+    assert not any(nets[1].mask_u8)
+    for net in nets:
+        net.forward(x)
+        net.backward(g)
+    torch.cuda.synchronize()
+    a, b = nets
+    for l in range(len(wl.CAFFENET)):
+        assert torch.equal(a.top[l], b.top[l]), f"layer {l} top"
+        if not a.stage_into[l]:
+            assert torch.equal(a.dbottom[l], b.dbottom[l]), f"layer {l} data gradient"
+        assert torch.equal(a.dW[l], b.dW[l]), f"layer {l} weight gradient"
+        assert torch.equal(a.db[l], b.db[l]), f"layer {l} bias gradient"
+
+
 def test_caffenet_bf16_step_lrn_staging_matches():
     """The bf16 step at N=512 with the LRN after conv1 and conv2 staging conv2's
     and conv3's bf16 bottoms as it forms its output (the default) against the

@@ -101,6 +101,49 @@ def test_backward_pool_lrn(case):
     assert_close(_np(db), db_r, TOL_F32, "bias gradient vs the oracle")
 
 
+@pytest.mark.parametrize("case", CASES)
+def test_backward_pool_lrn_byte_mask(case):
+    """The max-pool's winners recorded as bytes (each one's offset in its
+    window, CAFFE_POOL_MASK_OFFSETS) and read so by the fused backward
+    (CAFFE_BACKWARD_POOL_MASK_OFFSETS): the same pooled blob and every
+    gradient bit for bit against the 32-bit plane-index mask."""
+    N, C, H, W, K, k, s, p, g, bf16, relu_input = case
+    print(f"backward_pool_lrn byte mask {case}", flush=True)
+    rng = np.random.default_rng([1408, 5093, 92, sum(case[:9])])
+    f32_bottom = bf16 == "f32"
+    op = torch.bfloat16 if bf16 else torch.float32
+    x = torch.from_numpy(rng.standard_normal((N, C, H, W)).astype(np.float32)).to(DEV)
+    x = x if f32_bottom else x.to(op)
+    w = torch.from_numpy((rng.standard_normal((K, C // g, k, k)) * 0.2).astype(np.float32))
+    w = w.to(DEV).to(op)
+    b = torch.from_numpy(rng.standard_normal(K).astype(np.float32) * 0.1 - 0.2).to(DEV)
+    top = cc.conv_forward(x, w, b, s, p, g, relu=True)
+    dt = cc.CAFFE_BF16_F32_BOTTOM if f32_bottom else cc.CAFFE_BF16 if bf16 else cc.CAFFE_F32
+    d = cc.conv_desc(x.shape, w.shape, s, p, g, True, dt)
+    fl_pool = cc.POOL_RELU_INPUT if relu_input else 0
+    fl = cc.BACKWARD_TOP_DIFF_MASKED if relu_input else 0
+    outs = []
+    for byte in (False, True):
+        pooled, mask, lrn_top = cc.pool_lrn_forward(
+            top, flags=fl_pool | (cc.POOL_MASK_OFFSETS if byte else 0), **POOL, **LRN)
+        assert mask.dtype == (torch.uint8 if byte else torch.int32)
+        gl = torch.from_numpy(np.random.default_rng(7).standard_normal(
+            tuple(lrn_top.shape)).astype(np.float32)).to(DEV)
+        pd = cc.pool_desc(top.shape, POOL["kernel"], POOL["stride"], POOL["pad"])
+        ld = cc.lrn_desc(pooled.shape, **LRN)
+        dx = torch.full(x.shape, float("nan"), device=DEV)
+        dw = torch.full(w.shape, float("nan"), device=DEV)
+        db = torch.full((K,), float("nan"), device=DEV)
+        ws = cc.Workspace().get(cc.conv_workspace_size(d, cc.PASS_BACKWARD_POOL_LRN))
+        cc.caffe_conv_backward_pool_lrn(d, pd, ld, pooled, lrn_top, gl, mask,
+                                        None if relu_input else top, x, w, dx, dw, db, 0,
+                                        fl | (cc.BACKWARD_POOL_MASK_OFFSETS if byte else 0), ws)
+        torch.cuda.synchronize()
+        outs.append((pooled, dx, dw, db))
+    for name, a, c in zip(("pooled", "dx", "dw", "db"), *outs):
+        assert torch.equal(a, c), name
+
+
 def test_backward_pool_lrn_rejects_mismatched_pool():
     """The pool must describe the layer's top: checked on the host, nothing
     launched."""

@@ -140,6 +140,15 @@ int caffe_lrn_pool_backward(const caffe_pool_desc* pool, const caffe_lrn_desc* l
                             const float* pooled, const float* top, const float* top_diff,
                             const int32_t* mask, float* bottom_diff, void* stream);
 
+/* caffe_lrn_pool_backward with flags: CAFFE_BACKWARD_POOL_MASK_OFFSETS
+ * (caffe_conv.h) reads `mask` as the bytes caffe_pool_lrn_forward writes
+ * with CAFFE_POOL_MASK_OFFSETS (CAFFE_ERR_UNSUPPORTED for windows of more
+ * than 255 taps); other flags are CAFFE_ERR_INVALID_ARG. */
+int caffe_lrn_pool_backward_ex(const caffe_pool_desc* pool, const caffe_lrn_desc* lrn,
+                               const float* pooled, const float* top, const float* top_diff,
+                               const int32_t* mask, float* bottom_diff, int32_t flags,
+                               void* stream);
+
 /* The backward pass of a convolution layer whose output feeds max pooling
  * followed by LRN (CaffeNet's conv1 and conv2 with their glue): the layer's
  * top gradient is the glue's backward, caffe_lrn_pool_backward(pool, lrn,

@@ -368,18 +368,22 @@ def pool_lrn_stage_supported(x_shape, kernel, stride, pad, size, alpha, beta, k,
 
 
 def lrn_pool_backward(x_shape, pooled, top, top_diff, mask, kernel, stride, pad=0, size=5,
-                      alpha=1e-4, beta=0.75, k=1.0, out=None, stream=None):
-    """The backward of pool_lrn_forward in one pass; returns bottom_diff."""
+                      alpha=1e-4, beta=0.75, k=1.0, out=None, stream=None, flags=0):
+    """The backward of pool_lrn_forward in one pass; returns bottom_diff.  With
+    flags (BACKWARD_POOL_MASK_OFFSETS: a byte mask) caffe_lrn_pool_backward_ex."""
     pd, ld, _ = _pool_lrn_descs(x_shape, kernel, stride, pad, size, alpha, beta, k)
     for t, n in ((pooled, "pooled"), (top, "top"), (top_diff, "top_diff")):
         _dev(t, n, torch.float32)
-    _dev(mask, "mask", torch.int32)
+    _dev(mask, "mask", torch.uint8 if flags & BACKWARD_POOL_MASK_OFFSETS else torch.int32)
     if out is None:
         out = torch.empty(tuple(x_shape), dtype=torch.float32, device=top_diff.device)
     _dev(out, "bottom_diff", torch.float32)
-    check(load().caffe_lrn_pool_backward(ctypes.byref(pd), ctypes.byref(ld), _ptr(pooled),
-                                         _ptr(top), _ptr(top_diff), _ptr(mask), _ptr(out),
-                                         _stream(stream)))
+    args = (ctypes.byref(pd), ctypes.byref(ld), _ptr(pooled), _ptr(top), _ptr(top_diff),
+            _ptr(mask), _ptr(out))
+    if flags:
+        check(load().caffe_lrn_pool_backward_ex(*args, int(flags), _stream(stream)))
+    else:
+        check(load().caffe_lrn_pool_backward(*args, _stream(stream)))
     return out
 
 

@@ -57,7 +57,7 @@ EXPORTS = (
     "caffe_conv_backward_pool_lrn", "caffe_relu_backward", "caffe_conv_backward_ex",
     "caffe_conv_backward_pool_lrn_ex", "caffe_conv_backward_into",
     "caffe_conv_stage_below_supported", "caffe_conv_forward_ex", "caffe_pool_lrn_forward_into",
-    "caffe_pool_lrn_stage_supported",
+    "caffe_pool_lrn_stage_supported", "caffe_lrn_pool_backward_ex",
 )
 
 
@@ -132,6 +132,7 @@ def load():
         "caffe_pool_lrn_forward": [pdp, ldp, vp, vp, vp, vp, i32, vp],
         "caffe_pool_lrn_forward_into": [pdp, ldp, vp, vp, vp, vp, i32, cdp, vp, sz, vp],
         "caffe_pool_lrn_stage_supported": [pdp, ldp, cdp],
+        "caffe_lrn_pool_backward_ex": [pdp, ldp, vp, vp, vp, vp, vp, i32, vp],
         "caffe_lrn_pool_backward": [pdp, ldp, vp, vp, vp, vp, vp, vp],
         "caffe_conv_backward_pool_lrn": [cdp, pdp, ldp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                          i32, i32, vp, sz, vp],

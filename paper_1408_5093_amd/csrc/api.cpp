@@ -2025,8 +2025,21 @@ int caffe_lrn_pool_backward(const caffe_pool_desc* pd, const caffe_lrn_desc* ld,
                             const float* pooled, const float* top, const float* top_diff,
                             const int32_t* mask, float* bottom_diff, void* stream)
 {
+    return caffe_lrn_pool_backward_ex(pd, ld, pooled, top, top_diff, mask, bottom_diff, 0, stream);
+}
+
+int caffe_lrn_pool_backward_ex(const caffe_pool_desc* pd, const caffe_lrn_desc* ld,
+                               const float* pooled, const float* top, const float* top_diff,
+                               const int32_t* mask, float* bottom_diff, int32_t flags,
+                               void* stream)
+{
+    if (flags & ~CAFFE_BACKWARD_POOL_MASK_OFFSETS)
+        return fail(CAFFE_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
+    const int mask_u8 = flags ? 1 : 0;
     int Ho, Wo;
     CHECK(check_pool_lrn(pd, ld, &Ho, &Wo));
+    if (mask_u8 && pd->kernel_h * pd->kernel_w > 255)
+        return fail(CAFFE_ERR_UNSUPPORTED, "byte winner offsets need windows of at most 255 taps");
     const bool nz = pd->N > 0;
     CHECK(check_ptr(pooled, nz, "pooled"));
     CHECK(check_ptr(top, nz, "top"));
@@ -2036,7 +2049,7 @@ int caffe_lrn_pool_backward(const caffe_pool_desc* pd, const caffe_lrn_desc* ld,
     LAUNCH(launch_lrn_pool_backward(pooled, top, top_diff, mask, bottom_diff, pd->N, pd->C, pd->H,
                                     pd->W, Ho, Wo, pd->kernel_h, pd->kernel_w, pd->stride_h,
                                     pd->stride_w, pd->pad_h, pd->pad_w, ld->local_size, ld->alpha,
-                                    ld->beta, ld->k, (hipStream_t)stream),
+                                    ld->beta, ld->k, (hipStream_t)stream, mask_u8),
            "fused LRN + pool backward launch");
     return CAFFE_OK;
 }

@@ -194,11 +194,11 @@ class ConvStack:
         # glue's backward is the fused one that forms the output again
         self.lrn_stage_only = [lrn_stage_only and l + 1 < n and self.bottom_staged[l + 1] and
                                self.fuse_staging[l] for l in range(n)]
-        # ... and its max-pool records each winner as a byte (its offset in
-        # the window) where only that fused backward reads the mask
+        # A fused max-pool + LRN records each winner as a byte (its offset in
+        # the window): only the fused backward passes read the mask
         self.mask_u8 = [False] * n
         for l in range(n):
-            if mask_offsets and self.fuse_staging[l]:
+            if mask_offsets and self.fused[l]:
                 pst = self.stages[l][0]
                 if pst["prm"]["kernel"] ** 2 <= 255:
                     self.mask_u8[l] = True
@@ -293,7 +293,8 @@ class ConvStack:
                 p, r = pst["prm"], lst["prm"]
                 g = lrn_pool_backward(pst["in_shape"], pst["y"], lst["y"], g, pst["mask"],
                                       p["kernel"], p["stride"], p.get("pad", 0), r["size"],
-                                      r["alpha"], r["beta"], r["k"], out=pst["dx"], stream=s)
+                                      r["alpha"], r["beta"], r["k"], out=pst["dx"], stream=s,
+                                      flags=BACKWARD_POOL_MASK_OFFSETS if self.mask_u8[l] else 0)
             for st in (reversed(self.stages[l]) if not self.fused[l] else ()):
                 p = st["prm"]
                 if st["kind"] == "pool":

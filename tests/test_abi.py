@@ -298,6 +298,9 @@ def test_glue_validation():
     bigl = cc.lrn_desc((2, 96) + cc.pool_out_shape(big), 5)
     assert lib.caffe_pool_lrn_forward(ctypes.byref(big), ctypes.byref(bigl), P(0x1000), P(0x2000),
                                       P(0x4000), P(0x3000), cc.POOL_MASK_OFFSETS, None) in (-4,)
+    assert lib.caffe_lrn_pool_backward_ex(ctypes.byref(pd2), ctypes.byref(ld2), P(0x1000),
+                                          P(0x2000), P(0x3000), P(0x4000), P(0x5000), 1,
+                                          None) == -1       # an unknown flag
     # the stage-only flag belongs to the staging call
     assert lib.caffe_pool_lrn_forward(ctypes.byref(pd2), ctypes.byref(ld2), P(0x1000), P(0x2000),
                                       None, P(0x3000), cc.POOL_LRN_STAGE_ONLY, None) == -1

@@ -180,3 +180,28 @@ def test_caffenet_step_side_stream_matches_one_stream():
             assert torch.equal(a.top[l], b.top[l])
             assert torch.equal(a.dW[l], b.dW[l]) and torch.equal(a.db[l], b.db[l])
             assert torch.equal(a.dbottom[l], b.dbottom[l])
+
+
+def test_caffenet_step_byte_masks_match():
+    """The fp32 step with the fused max-pools recording their winners as
+    bytes (the default: the fused glue backward reads them) against 32-bit
+    plane-index masks: every top and gradient the same bits."""
+    N = 32
+    inp = wl.caffenet_step(N, wl.CAFFENET_STEP)
+    x = torch.from_numpy(inp["x"]).to(DEV)
+    g = torch.from_numpy(inp["top_diff"]).to(DEV)
+    nets = [ConvStack(wl.CAFFENET, N, inp["W"], inp["b"], glue=caffenet_glue(),
+                      mask_offsets=f) for f in (True, False)]
+    assert nets[0].mask_u8 == [True, True, False, False, False]
+    assert nets[0].stages[0][0]["mask"].dtype == torch.uint8
+    assert not any(nets[1].mask_u8)
+    for net in nets:
+        net.forward(x)
+        net.backward(g)
+    torch.cuda.synchronize()
+    a, b = nets
+    for l in range(len(wl.CAFFENET)):
+        assert torch.equal(a.top[l], b.top[l]), f"layer {l} top"
+        assert torch.equal(a.dbottom[l], b.dbottom[l]), f"layer {l} data gradient"
+        assert torch.equal(a.dW[l], b.dW[l]), f"layer {l} weight gradient"
+        assert torch.equal(a.db[l], b.db[l]), f"layer {l} bias gradient"

@@ -274,10 +274,10 @@ def cpu_baseline(inp, wl, n_img):
     except OSError:
         pass
     n_all = inp["x"].shape[0]
-    which = "all" if n_img >= n_all else f"the first {n_img}"
+    which = f"all {n_img}" if n_img >= n_all else f"the first {n_img}"
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
             "kind": "oracle", "images_per_s": n_img / dt, "seconds": dt, "cpu": cpu,
-            "sample": f"CaffeNet conv1-5 fwd + bwd (with pool/LRN glue) on {which} {n_img} of the "
+            "sample": f"CaffeNet conv1-5 fwd + bwd (with pool/LRN glue) on {which} of the "
                       f"step's {n_all} seeded images (full batch: {n_img >= n_all}), plain fp64 "
                       f"loops, OpenMP"}
 

@@ -70,6 +70,7 @@ def test_backward_pool_lrn(case):
     dw = torch.full(w.shape, float("nan"), device=DEV)
     db = torch.full((K,), float("nan"), device=DEV)
     ws = cc.Workspace().get(cc.conv_workspace_size(d, cc.PASS_BACKWARD_POOL_LRN))
+    ws.fill_(0x7E)  # (large finite bf16 values: a staging border left unzeroed shows)
     cc.caffe_conv_backward_pool_lrn(d, pd, ld, pooled, lrn_top, gl, mask,
                                     None if relu_input else top, x, w, dx, dw, db, 0, flags, ws)
 

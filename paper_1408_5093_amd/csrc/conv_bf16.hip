@@ -1672,12 +1672,14 @@ hipError_t launch_stage_s2d_bf16(const void* X, int x_f32, uint16_t* Xp, int N, 
 {
     if (N == 0)
         return hipSuccess;
-    // staged rows per block: about 32 KB of source rows in LDS
+    // staged rows per block: at most 16 KB of source rows in LDS (eight
+    // blocks per compute unit, so that one block's loads overlap another's
+    // stores)
     const size_t row_lds = (size_t)C * S * XWp * S * 2;
     if (row_lds > 64 * 1024 || Csp % 8 != 0 || C * S * S > Csp || Csp > 64 || N > 65535 ||
         (int64_t)C * H * W * 4 >= (int64_t(1) << 31))
         return hipErrorInvalidValue;
-    const int RA = (int)std::max<size_t>(1, std::min<size_t>(8, (32 * 1024) / row_lds));
+    const int RA = (int)std::max<size_t>(1, std::min<size_t>(8, (16 * 1024) / row_lds));
     const dim3 grid((unsigned)((XHp + RA - 1) / RA), (unsigned)N);
     const size_t lds = row_lds * RA;
     const FastDiv dc8 = make_fastdiv((uint32_t)(Csp / 8)), dxw = make_fastdiv((uint32_t)XWp);
